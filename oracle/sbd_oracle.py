@@ -1,0 +1,354 @@
+"""CPU oracle for one Set Block Decoding (SBD) step.  TEST INFRASTRUCTURE ONLY.
+
+Only the test suite, the smoke entry point and the benchmark's CPU-baseline leg may
+import this module.  The product path (the HIP library and its Python binding) never
+calls it, and it shares no code with that path: it takes plain numpy arrays (weights
+as floats or as raw bf16 bit patterns in uint16) and computes everything itself.
+
+What it computes, following the paper (Set Block Decoding, arXiv 2509.04185):
+
+* The SBD network f_theta of eq. (hybrid): a standard decoder in which the tokens left
+  of ';' (the committed prefix) use causal attention and the k block tokens right of
+  ';' use bidirectional attention (Sec. 2.3, Fig. 3).  The inference attention mask is
+  the one of App. A (inference mask): key kv is visible to query q iff kv <= q, or q is
+  at or after the first index of the prediction block.
+* The block logits z_hat_{t+i} predict the token at their own position t+i (Sec. 2.3,
+  eq. (p_theta_masked)); all block rows share the positions of the tokens they stand
+  for (App. A, training code: one position id per token location).
+* Exact KV caching (Sec. 1, advantages list; Alg. 3): the cache only ever receives the
+  keys/values of causal rows.  ``commit`` appends those rows.
+* The EB-Sampler of Sec. 2.2, eq. (eb_sampler): sort masked positions by ascending
+  entropy of their predicted distributions; reveal the first s, s >= 1 the largest
+  integer with sum_{j<s} H_(j) <= gamma.
+
+The decoder body (RMSNorm, rotate-half RoPE, grouped-query attention, SwiGLU MLP,
+optional per-head q/k RMSNorm of Qwen-3) is the standard Llama-3.1 / Qwen-3 block;
+the paper states there are no architectural changes (Sec. 1, advantages list).
+
+Readings where the paper is silent (each is listed with its reason in the design notes):
+* the mask token is excluded from the entropy and the argmax (the output distribution
+  lives on V, Sec. 2 notation; the mask token is an input-only symbol);
+* entropies are in nats of softmax(z) at temperature 1; tokens are argmax (Sec. 3.1
+  uses temperature 0 for tokens);
+* equal entropies are ordered by row index; argmax ties go to the smallest token id;
+* gamma may be 0 (used in Sec. 3.2) or +inf.
+
+Precision: everything runs in the dtype given to ``Model`` (float64 by default);
+EB statistics are always float64.
+"""
+from __future__ import annotations
+
+import math
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+# ----------------------------------------------------------------------------- helpers
+
+
+def decode_weight(a, dtype=np.float64) -> np.ndarray:
+    """Float view of a weight array; uint16 arrays are raw bf16 bit patterns."""
+    a = np.asarray(a)
+    if a.dtype == np.uint16:
+        a = (a.astype(np.uint32) << 16).view(np.float32)
+    return a.astype(dtype, copy=False)
+
+
+def rms_norm(x: np.ndarray, g: np.ndarray, eps: float) -> np.ndarray:
+    """x / sqrt(mean(x^2) + eps) * g over the last axis (Llama/Qwen RMSNorm)."""
+    ms = np.mean(x * x, axis=-1, keepdims=True)
+    return x / np.sqrt(ms + eps) * g
+
+
+def silu(z: np.ndarray) -> np.ndarray:
+    return z / (1.0 + np.exp(-z))
+
+
+def rope_cos_sin(pos: Sequence[int], head_dim: int, theta: float, dtype) -> tuple:
+    """cos/sin of the rotate-half RoPE angles p * theta^(-2i/d_h), i < d_h/2.
+
+    Angles are formed in float64 and then cast to the working dtype.
+    """
+    i = np.arange(head_dim // 2, dtype=np.float64)
+    inv_freq = theta ** (-2.0 * i / head_dim)
+    phi = np.asarray(pos, dtype=np.float64)[:, None] * inv_freq[None, :]
+    return np.cos(phi).astype(dtype), np.sin(phi).astype(dtype)
+
+
+def apply_rope(u: np.ndarray, cos: np.ndarray, sin: np.ndarray) -> np.ndarray:
+    """Rotate the pairs (u_i, u_{i+d/2}) of every head by the row's angles.
+
+    u: [rows, heads, d_h]; cos, sin: [rows, d_h/2].
+    """
+    half = u.shape[-1] // 2
+    a, b = u[..., :half], u[..., half:]
+    c, s = cos[:, None, :], sin[:, None, :]
+    return np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
+
+
+def inference_mask(n_prefix: int, k: int, n_causal: int) -> np.ndarray:
+    """Visibility [k, n_prefix + k] of the block rows over prefix + block keys.
+
+    The App. A inference mask with query index q = n_prefix + j, key index kv and
+    causal point = n_prefix + n_causal (the first index of the prediction block):
+    visible iff kv <= q or causal_point <= q.
+    """
+    q_idx = n_prefix + np.arange(k)[:, None]
+    kv_idx = np.arange(n_prefix + k)[None, :]
+    causal_point = n_prefix + n_causal
+    return (kv_idx <= q_idx) | (causal_point <= q_idx)
+
+
+def attention(q: np.ndarray, K: np.ndarray, V: np.ndarray, visible: np.ndarray) -> np.ndarray:
+    """Grouped-query softmax attention.
+
+    q: [rows, H_q, d_h]; K, V: [keys, H_kv, d_h]; visible: [rows, keys] bool.
+    Query head h reads key/value head floor(h * H_kv / H_q).
+    """
+    rows, n_q, d_h = q.shape
+    n_kv = K.shape[1]
+    out = np.zeros_like(q)
+    scale = 1.0 / math.sqrt(d_h)
+    for h in range(n_q):
+        g = h * n_kv // n_q
+        s = (q[:, h, :] @ K[:, g, :].T) * scale
+        s = np.where(visible, s, -np.inf)
+        s = s - s.max(axis=1, keepdims=True)
+        p = np.exp(s)
+        p = p / p.sum(axis=1, keepdims=True)
+        out[:, h, :] = p @ V[:, g, :]
+    return out
+
+
+# ----------------------------------------------------------------------------- model
+
+
+class SeqCache:
+    """Exact KV cache of one sequence: per layer K, V as [L][H_kv][d_h] arrays."""
+
+    def __init__(self, n_layers: int, n_kv: int, d_h: int, dtype):
+        self.K = [np.zeros((0, n_kv, d_h), dtype) for _ in range(n_layers)]
+        self.V = [np.zeros((0, n_kv, d_h), dtype) for _ in range(n_layers)]
+
+    @property
+    def length(self) -> int:
+        return self.K[0].shape[0]
+
+    def copy(self) -> "SeqCache":
+        c = SeqCache.__new__(SeqCache)
+        c.K = [a.copy() for a in self.K]
+        c.V = [a.copy() for a in self.V]
+        return c
+
+    @classmethod
+    def from_arrays(cls, K, V, dtype) -> "SeqCache":
+        """K, V: [n_layers][L][H_kv][d_h] (float or bf16 bits)."""
+        c = cls.__new__(cls)
+        c.K = [decode_weight(K[i], dtype) for i in range(len(K))]
+        c.V = [decode_weight(V[i], dtype) for i in range(len(V))]
+        return c
+
+
+class BlockResult:
+    """Output of one block forward: logits per row plus the staged K/V of every row."""
+
+    def __init__(self, logits, K_new, V_new, n_causal):
+        self.logits = logits          # [B][k][V]
+        self.K_new = K_new            # per sequence: per layer [k][H_kv][d_h]
+        self.V_new = V_new
+        self.n_causal = n_causal      # per sequence
+
+
+class Model:
+    """The SBD network f_theta on plain arrays.
+
+    ``shape`` needs the attributes n_layers, d_model, n_q_heads, n_kv_heads, head_dim,
+    ffn_dim, vocab, qk_norm, rms_eps, rope_theta.  ``weights`` is a dict with embed,
+    lm_head, final_norm and a list ``layers`` of dicts (attn_norm, wq, wk, wv, wo,
+    q_norm, k_norm, mlp_norm, w_gate, w_up, w_down); matrices are [out][in].
+    """
+
+    def __init__(self, shape, weights: dict, dtype=np.float64, cache_decoded: bool = True):
+        self.s = shape
+        self.w = weights
+        self.dtype = np.dtype(dtype)
+        self._memo = {} if cache_decoded else None
+
+    def W(self, name: str, layer: Optional[int] = None) -> np.ndarray:
+        key = (name, layer)
+        if self._memo is not None and key in self._memo:
+            return self._memo[key]
+        src = self.w[name] if layer is None else self.w["layers"][layer][name]
+        a = decode_weight(src, self.dtype)
+        if self._memo is not None:
+            self._memo[key] = a
+        return a
+
+    def new_cache(self) -> SeqCache:
+        s = self.s
+        return SeqCache(s.n_layers, s.n_kv_heads, s.head_dim, self.dtype)
+
+    # -- the network ---------------------------------------------------------------
+    def _qkv(self, h, li, pos):
+        s = self.s
+        rows = h.shape[0]
+        q = (h @ self.W("wq", li).T).reshape(rows, s.n_q_heads, s.head_dim)
+        k = (h @ self.W("wk", li).T).reshape(rows, s.n_kv_heads, s.head_dim)
+        v = (h @ self.W("wv", li).T).reshape(rows, s.n_kv_heads, s.head_dim)
+        if s.qk_norm:
+            q = rms_norm(q, self.W("q_norm", li), s.rms_eps)
+            k = rms_norm(k, self.W("k_norm", li), s.rms_eps)
+        cos, sin = rope_cos_sin(pos, s.head_dim, s.rope_theta, self.dtype)
+        return apply_rope(q, cos, sin), apply_rope(k, cos, sin), v
+
+    def _mlp(self, x, li):
+        s = self.s
+        h2 = rms_norm(x, self.W("mlp_norm", li), s.rms_eps)
+        a = silu(h2 @ self.W("w_gate", li).T) * (h2 @ self.W("w_up", li).T)
+        return a @ self.W("w_down", li).T
+
+    def block_forward(self, caches: List[SeqCache], tokens, n_causal, pos=None) -> BlockResult:
+        """Eq. (hybrid_block) for a batch of independent sequences.
+
+        tokens: [B][k] ids (mask id allowed); n_causal: [B], rows < n_causal[b] are the
+        committed-but-uncached causal rows, the rest form the prediction block;
+        pos: [B][k] position ids, default cache length + row.
+        Returns logits [B][k][V] and the post-RoPE K and the V of every block row.
+        """
+        s = self.s
+        tokens = np.asarray(tokens)
+        B, k = tokens.shape
+        n_causal = [int(n) for n in np.broadcast_to(np.asarray(n_causal), (B,))]
+        L = [c.length for c in caches]
+        if pos is None:
+            pos = np.array([[L[b] + j for j in range(k)] for b in range(B)])
+        pos = np.asarray(pos)
+        E = self.W("embed")
+        x = E[tokens.reshape(-1)].astype(self.dtype)           # [B*k][d]
+        K_new = [[None] * s.n_layers for _ in range(B)]
+        V_new = [[None] * s.n_layers for _ in range(B)]
+        for li in range(s.n_layers):
+            h = rms_norm(x, self.W("attn_norm", li), s.rms_eps)
+            o = np.zeros((B * k, s.n_q_heads, s.head_dim), self.dtype)
+            for b in range(B):
+                r = slice(b * k, (b + 1) * k)
+                q, kk, vv = self._qkv(h[r], li, pos[b])
+                K_new[b][li], V_new[b][li] = kk, vv
+                Kall = np.concatenate([caches[b].K[li], kk], axis=0)
+                Vall = np.concatenate([caches[b].V[li], vv], axis=0)
+                vis = inference_mask(L[b], k, n_causal[b])
+                o[r] = attention(q, Kall, Vall, vis)
+            x = x + o.reshape(B * k, -1) @ self.W("wo", li).T
+            x = x + self._mlp(x, li)
+        hf = rms_norm(x, self.W("final_norm"), s.rms_eps)
+        logits = hf @ self.W("lm_head").T
+        return BlockResult(logits.reshape(B, k, s.vocab), K_new, V_new, n_causal)
+
+    @staticmethod
+    def commit(caches: List[SeqCache], res: BlockResult, n_commit) -> None:
+        """Append the staged K/V of rows [0, n) of the last forward (exact caching)."""
+        for b, c in enumerate(caches):
+            n = int(n_commit[b])
+            if n > res.n_causal[b]:
+                raise ValueError("only causal rows can be committed")
+            for li in range(len(c.K)):
+                c.K[li] = np.concatenate([c.K[li], res.K_new[b][li][:n]], axis=0)
+                c.V[li] = np.concatenate([c.V[li], res.V_new[b][li][:n]], axis=0)
+
+    def prefill(self, tokens) -> tuple:
+        """NTP forward over a prompt (all rows causal), then commit every row.
+
+        Returns (cache, logits of the last prompt row).
+        """
+        tokens = np.asarray(tokens).reshape(1, -1)
+        c = self.new_cache()
+        res = self.block_forward([c], tokens, [tokens.shape[1]])
+        self.commit([c], res, [tokens.shape[1]])
+        return c, res.logits[0, -1]
+
+    def full_forward(self, tokens, causal_point: int, pos=None) -> np.ndarray:
+        """All rows at once, no cache, with the App. A inference mask over the whole sequence.
+
+        Used to check that cached decoding is exact.  Returns logits [T][V].
+        """
+        s = self.s
+        tokens = np.asarray(tokens).reshape(-1)
+        T = tokens.shape[0]
+        pos = np.arange(T) if pos is None else np.asarray(pos)
+        q_idx = np.arange(T)[:, None]
+        kv_idx = np.arange(T)[None, :]
+        vis = (kv_idx <= q_idx) | (causal_point <= q_idx)
+        x = self.W("embed")[tokens].astype(self.dtype)
+        for li in range(s.n_layers):
+            h = rms_norm(x, self.W("attn_norm", li), s.rms_eps)
+            q, kk, vv = self._qkv(h, li, pos)
+            o = attention(q, kk, vv, vis)
+            x = x + o.reshape(T, -1) @ self.W("wo", li).T
+            x = x + self._mlp(x, li)
+        return rms_norm(x, self.W("final_norm"), s.rms_eps) @ self.W("lm_head").T
+
+
+# ----------------------------------------------------------------------------- EB sampler
+
+
+def row_entropy(logits_row, mask_id: int) -> tuple:
+    """Entropy (nats) and argmax of softmax over the vocabulary without the mask token.
+
+    With m the row maximum and t_v = l_v - m (float64): Z = sum e^t, S = sum e^t * t,
+    H = log Z - S / Z, which equals -sum p log p for p = e^t / Z.
+    The argmax is the smallest token id reaching the maximum.
+    """
+    l = np.asarray(logits_row, dtype=np.float32)
+    keep = np.ones(l.shape[0], dtype=bool)
+    if 0 <= mask_id < l.shape[0]:
+        keep[mask_id] = False
+    ids = np.nonzero(keep)[0]
+    lv = l[ids]
+    m = lv.max()
+    tok = int(ids[np.argmax(lv == m)])
+    t = lv.astype(np.float64) - np.float64(m)
+    e = np.exp(t)
+    Z = e.sum()
+    S = (e * t).sum()
+    return math.log(Z) - S / Z, tok
+
+
+def eb_select_from_entropy(H: Sequence[float], masked_rows: Sequence[int], gamma: float) -> List[int]:
+    """Eq. (eb_sampler): rows to reveal, given per-row entropies.
+
+    Masked rows are ordered by (H, row) ascending as i_1..i_n; c_0 = 0 and
+    c_r = c_{r-1} + H_{i_r}, summed left to right in float64; s is the largest
+    r in [1, n] with c_{r-1} <= gamma (so s >= 1 whenever n >= 1).  Returns the first
+    s rows of the order, sorted by row.
+    """
+    order = sorted(masked_rows, key=lambda j: (float(H[j]), int(j)))
+    s = 0
+    c = 0.0
+    for r, j in enumerate(order, start=1):
+        if c <= gamma:
+            s = r
+        c = c + float(H[j])
+    return sorted(int(j) for j in order[:s])
+
+
+def eb_select(logits, is_mask, gamma: float, mask_id: int) -> tuple:
+    """One EB-Sampler step on a batch of blocks (Sec. 2.2 and Alg. 3).
+
+    logits: [B][k][V] float32; is_mask: [B][k].  Returns (accepted, tokens, H):
+    accepted[b] = rows revealed (ascending), tokens[b] = their argmax ids,
+    H[b][j] = entropy of masked rows (nan for unmasked rows).
+    """
+    logits = np.asarray(logits, dtype=np.float32)
+    is_mask = np.asarray(is_mask).astype(bool)
+    B, k, _ = logits.shape
+    accepted, tokens = [], []
+    H = np.full((B, k), np.nan)
+    for b in range(B):
+        rows = [j for j in range(k) if is_mask[b, j]]
+        toks = {}
+        for j in rows:
+            H[b, j], toks[j] = row_entropy(logits[b, j], mask_id)
+        acc = eb_select_from_entropy(H[b], rows, gamma)
+        accepted.append(acc)
+        tokens.append([toks[j] for j in acc])
+    return accepted, tokens, H
