@@ -1,0 +1,238 @@
+#!/usr/bin/env python3
+"""Benchmark of one Set Block Decoding decode step on one MI355X.
+
+One step = the whole hot path over one batch: the SBD block forward of the decoder
+(all layers + LM head, fp32 logits for every block row) followed by one EB-Sampler
+step on those logits.  Workload: Llama-3.1-8B shape with random-init bf16 weights,
+batch 1, a 2048-token random prompt prefilled into the KV cache, block k = 16 (the last
+committed token + 15 masks), gamma = 1.0.  Inputs are resident in HBM before timing.
+
+Prints one JSON line: value = algorithmic HBM bytes of a step / step time (GB/s),
+plus the block-forward ms, the EB-select microseconds, a roofline entry for the
+dominant kernel (gate/up projection, timed live with HIP events on the library
+stream) and the CPU oracle timed on a bounded sample of the same workload.
+"""
+import argparse
+import dataclasses
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "SBD block-forward ms + HBM GB/s (8B shape, k=16); EB-select µs"
+PEAK_HBM_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gate_up_traffic_llama8b_b1_l2048_k16.json")
+
+
+def step_bytes(shape, lens, k):
+    """Algorithmic HBM bytes of one step: weights once, KV read once, staged K/V written,
+    fp32 logits written, EB reads the masked rows' logits."""
+    s = shape
+    d, F, V = s.d_model, s.ffn_dim, s.vocab
+    qd, kvd = s.n_q_heads * s.head_dim, s.n_kv_heads * s.head_dim
+    per_layer = (qd + 2 * kvd) * d + d * qd + 2 * F * d + d * F
+    weights = 2 * (s.n_layers * per_layer + V * d)
+    B = len(lens)
+    M = B * k
+    kv_read = sum(lens) * s.n_layers * kvd * 2 * 2
+    kv_write = M * s.n_layers * kvd * 2 * 2
+    logits = 4 * M * V
+    eb = 4 * B * (k - 1) * V
+    fwd = weights + kv_read + kv_write + logits
+    return fwd, eb
+
+
+def gate_up_bytes(shape, M):
+    """Algorithmic bytes of one gate/up launch: both weight matrices, the bf16 input rows,
+    the bf16 SwiGLU output rows."""
+    return 2 * 2 * shape.ffn_dim * shape.d_model + 2 * M * shape.d_model + 2 * M * shape.ffn_dim
+
+
+def source_hash():
+    h = hashlib.sha256()
+    with open(os.path.join(ROOT, "paper_2509_04185_amd", "csrc", "gemm.hip"), "rb") as f:
+        h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def cpu_baseline(wl, w_dev, lens, toks, n_layers_sample, gamma):
+    """Time the oracle (fp32, as it stands) on the host for a sample of the workload's layers
+    plus the LM head and the EB step; scale to a full step."""
+    import numpy as np
+    import synth
+    from oracle import sbd_oracle as O
+
+    s = wl.shape
+    ns = min(n_layers_sample, s.n_layers)
+    sub = dataclasses.replace(s, n_layers=ns)
+    host = {"embed": synth.to_host_bits(w_dev["embed"]), "lm_head": synth.to_host_bits(w_dev["lm_head"]),
+            "final_norm": synth.to_host_bits(w_dev["final_norm"]),
+            "layers": [{kk: synth.to_host_bits(vv) for kk, vv in w_dev["layers"][l].items()}
+                       for l in range(ns)]}
+    caches = []
+    for b, L in enumerate(lens):
+        kk, vv = synth.make_kv(sub, wl.seed, b, L, device="cpu")
+        caches.append(O.SeqCache.from_arrays(synth.to_host_bits(kk), synth.to_host_bits(vv), np.float32))
+    model = O.Model(sub, host, dtype=np.float32, cache_decoded=False)
+    t0 = time.perf_counter()
+    res = model.block_forward(caches, toks, [1] * len(lens))
+    t_fwd = time.perf_counter() - t0
+    # the LM head alone, to separate it from the per-layer cost
+    t0 = time.perf_counter()
+    xf = np.zeros((toks.size, s.d_model), np.float32)
+    _ = O.rms_norm(xf, model.W("final_norm"), s.rms_eps) @ model.W("lm_head").T
+    t_head = time.perf_counter() - t0
+    is_mask = (toks == s.mask_id).astype(np.uint8)
+    t0 = time.perf_counter()
+    O.eb_select(res.logits.astype(np.float32), is_mask, gamma, s.mask_id)
+    t_eb = time.perf_counter() - t0
+    per_layer = max(t_fwd - t_head, 1e-9) / ns
+    est = per_layer * s.n_layers + t_head + t_eb
+    return est, {"layers_timed": ns, "per_layer_s": per_layer, "lm_head_s": t_head, "eb_s": t_eb,
+                 "sample_s": t_fwd + t_eb}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama8b_b1_l2048_k16")
+    ap.add_argument("--cpu-layers", type=int, default=8, help="layers of the oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event pass")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(batch sharding across GPUs is a design note only).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2509_04185_amd import Sbd
+
+    wl = synth.WORKLOADS[args.workload]
+    s = wl.shape
+    gamma = wl.gammas[0]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    lens = wl.cache_lens()
+    B, k = wl.batch, wl.k
+    print(f"[bench] {wl.name}: generating weights", file=sys.stderr, flush=True)
+    w = synth.make_weights(s, wl.seed, device=dev)
+    lib = Sbd(s, w, max_batch=B, max_seq_len=max(lens) + k + 64, max_block=k)
+    print(f"[bench] prefilling {B} x {lens[0]}..{lens[-1]} tokens", file=sys.stderr, flush=True)
+    for b, L in enumerate(lens):
+        lib.prefill(b, synth.make_tokens(wl.seed, L, s, stream=100 + b), want_logits=False)
+    torch.cuda.synchronize()
+    toks, is_mask = synth.block_rows(wl.seed, s, B, k, n_causal=1)
+    seq_ids = list(range(B))
+    logits = torch.empty((B, k, s.vocab), dtype=torch.float32, device=dev)
+
+    def step():
+        lib.block_forward(seq_ids, toks, is_mask=is_mask, out=logits)
+        return lib.eb_select(logits, is_mask, gamma, s.mask_id, want_entropy=False)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    e0.record()
+    for _ in range(args.steps):
+        out = step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / args.steps
+    n_acc = int(out[0][0])
+
+    # block forward alone and EB select alone
+    e0.record()
+    for _ in range(args.steps):
+        lib.block_forward(seq_ids, toks, is_mask=is_mask, out=logits)
+    e1.record()
+    torch.cuda.synchronize()
+    ms_fwd = e0.elapsed_time(e1) / args.steps
+    e0.record()
+    for _ in range(args.steps):
+        lib.eb_select(logits, is_mask, gamma, s.mask_id, want_entropy=False)
+    e1.record()
+    torch.cuda.synchronize()
+    us_eb = 1000.0 * e0.elapsed_time(e1) / args.steps
+
+    fwd_bytes, eb_bytes = step_bytes(s, lens, k)
+    value = (fwd_bytes + eb_bytes) / (ms_step * 1e-3) / 1e9
+
+    # per-kernel durations, HIP events around each launch on the library stream
+    kernels = {}
+    roofline = None
+    if not args.no_profile:
+        lib.profile(True)
+        lib.profile_read()
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        prof = lib.profile_read()
+        lib.profile(False)
+        kernels = {n: {"launches": c, "avg_us": 1000.0 * t / c if c else None}
+                   for n, (c, t) in prof.items() if c}
+        c, t = prof["gate_up"]
+        avg_s = t / c * 1e-3
+        bpl = gate_up_bytes(s, B * k)
+        achieved = bpl / avg_s / 1e9
+        traffic = None
+        if os.path.exists(TRAFFIC_FILE):
+            with open(TRAFFIC_FILE) as f:
+                tr = json.load(f)
+            if tr.get("gemm_source") == source_hash():
+                traffic = tr.get("bytes_per_launch")
+        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                    "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
+                    "kernel": "gemm_kernel<1,8,8,EPI_SWIGLU> (gate/up + SwiGLU)",
+                    "bytes_per_launch": bpl, "avg_launch_us": round(avg_s * 1e6, 2),
+                    "launches": c}
+
+    # a plain copy of known size, so counter runs can calibrate FETCH_SIZE / WRITE_SIZE
+    src = torch.empty(256 * 2**20, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        print(f"[bench] oracle on {args.cpu_layers} layers", file=sys.stderr, flush=True)
+        est, info = cpu_baseline(wl, w, lens, toks, args.cpu_layers, gamma)
+        cores = len(os.sched_getaffinity(0))
+        cpu = {"value": round((fwd_bytes + eb_bytes) / est / 1e9, 4), "unit": "GB/s", "cores": cores,
+               "kind": "oracle", "ms_per_step": round(est * 1e3, 1),
+               "sample": (f"fp32 numpy oracle block forward over the first {info['layers_timed']} of "
+                          f"{s.n_layers} layers + LM head + EB select on the same block; per-layer "
+                          f"time x {s.n_layers} + head + EB ({info['sample_s']:.1f} s timed)")}
+
+    line = {
+        "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded random-init weights, uniform random prompt tokens)",
+        "config": {"workload": wl.name, "shape": s.name, "batch": B, "cache_len": lens, "k": k,
+                   "gamma": gamma, "n_causal": 1},
+        "block_forward_ms": round(ms_fwd, 4),
+        "block_forward_gbs": round(fwd_bytes / (ms_fwd * 1e-3) / 1e9, 1),
+        "block_forward_frac_of_peak": round(fwd_bytes / (ms_fwd * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "eb_select_us": round(us_eb, 2),
+        "step_bytes": fwd_bytes + eb_bytes, "eb_accepted": n_acc,
+        "roofline": roofline, "cpu_baseline": cpu, "kernels": kernels,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,224 @@
+/*
+ * sbd.h - C ABI of the MI355X (gfx950) Set Block Decoding decode step.
+ *
+ * One decode step of Set Block Decoding (SBD, arXiv 2509.04185) is one forward pass
+ * of the SBD network f_theta over a block of k rows against an exact KV cache
+ * (Sec. 2.3, eq. (hybrid_block); Alg. 3), followed by one step of the entropy-bounded
+ * (EB) sampler (Sec. 2.2, eq. (eb_sampler)).  This library runs both on one GPU with
+ * hand-written HIP kernels.
+ *
+ * Conventions shared by every entry point
+ *  - Every function returns an sbd_status; no exception crosses the ABI.
+ *  - Arguments and state are validated on the host before anything is enqueued; on
+ *    any error nothing is enqueued and no state changes.  sbd_last_error() then gives
+ *    a one-line reason.
+ *  - "device" pointers are GPU global memory (e.g. torch CUDA tensors); "host"
+ *    pointers are ordinary CPU memory that is read before the call returns.
+ *  - All GPU work is enqueued on the context's stream and is asynchronous: outputs are
+ *    valid once that stream has been synchronised.  An asynchronous device fault is
+ *    reported as SBD_ERR_HIP by a later call.
+ *  - Row-major layouts throughout; bf16 means IEEE bfloat16 (1/8/7 bits).
+ *  - A context is used by one host thread at a time.  The library keeps no global
+ *    state other than the thread-local error text of context-less calls.
+ */
+#ifndef SBD_H_
+#define SBD_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SBD_OK = 0,
+  SBD_ERR_INVALID_ARG = 1,   /* a pointer, size, id or value is out of its documented range */
+  SBD_ERR_STATE = 2,         /* the call is not allowed in the context's current state */
+  SBD_ERR_CAPACITY = 3,      /* a sequence would exceed max_seq_len */
+  SBD_ERR_OUT_OF_MEMORY = 4, /* the workspace is smaller than sbd_workspace_bytes() */
+  SBD_ERR_HIP = 5,           /* a HIP runtime call or an earlier kernel failed */
+  SBD_ERR_UNSUPPORTED = 6    /* the model shape is outside what the kernels implement */
+} sbd_status;
+
+typedef struct sbd_ctx sbd_ctx; /* opaque, created by sbd_create */
+
+/*
+ * Decoder shape (Llama-3.1 / Qwen-3 style; the SBD network has no architectural
+ * changes, Sec. 1) plus capacity limits.
+ *   n_q_heads % n_kv_heads == 0; query head h reads KV head h / (n_q_heads/n_kv_heads).
+ *   head_dim is 64 or 128.  d_model, n_q_heads*head_dim and ffn_dim are multiples of 256;
+ *   vocab is a multiple of 32.  mask_id in [0, vocab) is the input-only mask token 'm'.
+ *   qk_norm != 0 enables the per-head RMSNorm of q and k before RoPE (Qwen-3).
+ *   max_batch: number of sequence slots (ids 0..max_batch-1).
+ *   max_seq_len: tokens per slot, including the k rows staged by a block forward.
+ *   max_block: largest k accepted by sbd_block_forward / sbd_eb_select (<= 64).
+ *   prefill_chunk: rows per forward inside sbd_prefill (0 selects 256).
+ */
+typedef struct {
+  int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, ffn_dim, vocab, mask_id;
+  int32_t qk_norm;
+  float rms_eps, rope_theta;
+  int32_t max_batch, max_seq_len, max_block, prefill_chunk;
+} sbd_model_config;
+
+/*
+ * Weights: device bf16, borrowed (they must outlive the context and not change).
+ * Matrices are logical [out][in] row-major.  Per-layer fields are host arrays of
+ * n_layers device pointers.  q_norm / k_norm may be NULL when qk_norm == 0.
+ *   embed [vocab][d_model], lm_head [vocab][d_model], final_norm [d_model]
+ *   attn_norm [d_model], wq [n_q_heads*head_dim][d_model], wk, wv [n_kv_heads*head_dim][d_model],
+ *   wo [d_model][n_q_heads*head_dim], q_norm, k_norm [head_dim], mlp_norm [d_model],
+ *   w_gate, w_up [ffn_dim][d_model], w_down [d_model][ffn_dim]
+ */
+typedef struct {
+  const void *embed, *lm_head, *final_norm;
+  const void *const *attn_norm, *const *wq, *const *wk, *const *wv, *const *wo;
+  const void *const *q_norm, *const *k_norm, *const *mlp_norm;
+  const void *const *w_gate, *const *w_up, *const *w_down;
+} sbd_weights;
+
+/* Bytes of device workspace sbd_create needs for this config (KV cache, activations,
+ * partial results, RoPE table).  *bytes is set only on SBD_OK. */
+sbd_status sbd_workspace_bytes(const sbd_model_config* cfg, size_t* bytes);
+
+/*
+ * Create a context on the current HIP device.  workspace: device memory of at least
+ * sbd_workspace_bytes() bytes, 256-byte aligned, caller-owned, not touched by anyone
+ * else while the context lives.  stream: a hipStream_t (NULL = the null stream).
+ * Every sequence slot starts empty.  The library allocates no device memory itself;
+ * it allocates a small pinned host staging buffer here.
+ */
+sbd_status sbd_create(const sbd_model_config* cfg, const sbd_weights* w, void* workspace,
+                      size_t workspace_bytes, void* stream, sbd_ctx** out);
+sbd_status sbd_destroy(sbd_ctx* ctx);
+/* Replace the stream later calls enqueue on (e.g. torch's current stream). */
+sbd_status sbd_set_stream(sbd_ctx* ctx, void* stream);
+
+/* Empty one sequence slot (cache length 0, nothing staged). */
+sbd_status sbd_reset(sbd_ctx* ctx, int32_t seq);
+/* Number of committed tokens in a slot. */
+sbd_status sbd_cache_len(const sbd_ctx* ctx, int32_t seq, int32_t* len);
+
+/*
+ * Prefill (Alg. 2, first step): a causal forward f_theta(x;) over n prompt tokens
+ * (host int32 ids in [0, vocab), mask id excluded) appended after the slot's cache,
+ * committing all n rows.  Runs in forwards of at most prefill_chunk rows.
+ * last_logits: device fp32 [vocab] receiving the logits of the last prompt row, or NULL.
+ * Errors: CAPACITY if cache_len + n > max_seq_len.
+ */
+sbd_status sbd_prefill(sbd_ctx* ctx, int32_t seq, const int32_t* tokens, int32_t n,
+                       float* last_logits);
+
+/*
+ * Block forward (eq. (hybrid_block); one iteration of Alg. 3) for `batch` sequences.
+ *   seq_ids  host [batch], distinct slot ids.
+ *   tokens   host [batch][k] ids in [0, vocab); mask rows hold mask_id.
+ *   is_mask  host [batch][k] or NULL; when given it must equal (tokens == mask_id).
+ *   n_causal host [batch] or NULL (= all 1).  Rows j < n_causal[b] are committed but
+ *            not yet cached tokens and attend causally; rows j >= n_causal[b] form the
+ *            prediction block and see every row (App. A inference mask: key kv is
+ *            visible to query q iff kv <= q or q >= the first prediction index).
+ *            Causal rows may not be masks.
+ *   pos_ids  host [batch][k] or NULL (= cache_len + j).  RoPE positions; causal rows
+ *            must keep cache_len + j.  Values in [0, max_seq_len).
+ *   logits   device fp32 [batch][k][vocab], all rows, all vocab columns (row j's
+ *            logits predict the token at its own position, eq. (p_theta_masked)).
+ * The K/V of all k rows are staged in cache slots [cache_len, cache_len + k); the
+ * first n_causal of them become permanent with sbd_commit.
+ * Errors: CAPACITY if cache_len + k > max_seq_len for some sequence.
+ */
+sbd_status sbd_block_forward(sbd_ctx* ctx, int32_t batch, const int32_t* seq_ids, int32_t k,
+                             const int32_t* tokens, const uint8_t* is_mask,
+                             const int32_t* n_causal, const int32_t* pos_ids, float* logits);
+
+/*
+ * Exact KV caching (Sec. 1, advantages; Alg. 3): make the K/V staged by the last block
+ * forward of each listed sequence permanent for its first n_commit[b] rows
+ * (cache_len += n_commit[b]).  n_commit[b] <= that forward's n_causal[b], else STATE.
+ * Host arrays seq_ids, n_commit [batch].  Bookkeeping only: no data moves.
+ */
+sbd_status sbd_commit(sbd_ctx* ctx, int32_t batch, const int32_t* seq_ids,
+                      const int32_t* n_commit);
+
+/*
+ * EB-Sampler step (Sec. 2.2, eq. (eb_sampler)) on fp32 logits.
+ *   logits   device fp32 [batch][k][vocab] (any logits; vocab <= the config's vocab).
+ *   is_mask  host [batch][k]: the masked set M of each block.
+ *   gamma    >= 0, may be +INFINITY; NaN is rejected.
+ *   mask_id  column excluded from the distribution, or -1 for none.
+ * For each masked row: H = entropy (nats, float64) of softmax over the vocabulary
+ * without mask_id, tok = smallest id attaining the maximum logit.  Masked rows are
+ * ordered by (H, row) ascending; with c_r the float64 running sum of the first r
+ * entropies (c_0 = 0), s = largest r in [1, |M|] with c_{r-1} <= gamma.
+ * Outputs (device): n_accepted [batch] = s (0 if M is empty); accepted_pos
+ * [batch][k] = the s rows ascending, then -1; accepted_tok [batch][k] = their tokens,
+ * then -1; entropy [batch][k] (nullable) = H for masked rows, NaN otherwise.
+ */
+sbd_status sbd_eb_select(sbd_ctx* ctx, int32_t batch, int32_t k, int32_t vocab,
+                         const float* logits, const uint8_t* is_mask, double gamma,
+                         int32_t mask_id, int32_t* n_accepted, int32_t* accepted_pos,
+                         int32_t* accepted_tok, double* entropy);
+
+/*
+ * The selection part of sbd_eb_select alone, on given entropies (device float64
+ * [batch][k]); same ordering, rule and outputs (no tokens).
+ */
+sbd_status sbd_eb_select_entropies(sbd_ctx* ctx, int32_t batch, int32_t k,
+                                   const double* entropy, const uint8_t* is_mask, double gamma,
+                                   int32_t* n_accepted, int32_t* accepted_pos);
+
+/*
+ * Write n cached rows of a slot from device bf16 K, V [n_layers][n][n_kv_heads][head_dim]
+ * (K after RoPE), starting at position pos0 <= cache_len; the slot's cache length
+ * becomes pos0 + n and nothing stays staged.  Restores a saved cache, or installs a
+ * cache produced elsewhere.  Errors: CAPACITY if pos0 + n > max_seq_len.
+ */
+sbd_status sbd_kv_import(sbd_ctx* ctx, int32_t seq, int32_t pos0, int32_t n, const void* k,
+                         const void* v);
+/* Read rows [pos0, pos0 + n) of a slot (committed or staged) into the same layout. */
+sbd_status sbd_kv_export(sbd_ctx* ctx, int32_t seq, int32_t pos0, int32_t n, void* k, void* v);
+
+/*
+ * Byte offset and size inside the workspace of a named internal buffer, for
+ * inspection by tests: "x" (fp32 residual [rows][d_model]), "qkv" (fp32 projections),
+ * "q" (bf16 rotated queries), "attn" (bf16 attention output), "act" (bf16 SwiGLU output),
+ * "xn" (bf16 gain-scaled residual).  Values are those of the last layer of the last
+ * forward.  INVALID_ARG for an unknown name.
+ */
+sbd_status sbd_workspace_region(const sbd_model_config* cfg, const char* name, size_t* offset,
+                                size_t* bytes);
+
+/*
+ * Per-kernel timing, for measurement tools.  While enabled, every kernel launch the
+ * context makes is bracketed by a pair of HIP events on its stream (this adds a little
+ * time between kernels).  sbd_profile_read waits for the recorded work, adds up the
+ * elapsed times of all launches of one kernel kind since the previous read of that kind,
+ * and returns the launch count and the total in milliseconds.
+ */
+typedef enum {
+  SBD_KERNEL_EMBED = 0,      /* embedding gather + first RMSNorm inputs */
+  SBD_KERNEL_QKV = 1,        /* QKV projection */
+  SBD_KERNEL_ROPE = 2,       /* q/k norm, RoPE, KV staging */
+  SBD_KERNEL_ATTENTION = 3,  /* split-KV block-hybrid attention */
+  SBD_KERNEL_ATTN_MERGE = 4, /* merge of the attention splits */
+  SBD_KERNEL_O_PROJ = 5,     /* output projection + residual */
+  SBD_KERNEL_GATE_UP = 6,    /* gate/up projection + SwiGLU */
+  SBD_KERNEL_DOWN = 7,       /* down projection + residual */
+  SBD_KERNEL_LM_HEAD = 8,    /* final norm + LM head */
+  SBD_KERNEL_EB_PARTIAL = 9, /* EB per-chunk softmax statistics */
+  SBD_KERNEL_EB_SELECT = 10, /* EB merge, sort and select */
+  SBD_KERNEL_COUNT = 11
+} sbd_kernel;
+sbd_status sbd_profile_enable(sbd_ctx* ctx, int32_t enable);
+sbd_status sbd_profile_read(sbd_ctx* ctx, int32_t kernel, int32_t* launches, double* total_ms);
+
+const char* sbd_status_string(sbd_status s);
+/* Reason for the last failed call on ctx; ctx == NULL gives the calling thread's last
+ * context-less failure (e.g. of sbd_create). */
+const char* sbd_last_error(const sbd_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SBD_H_ */

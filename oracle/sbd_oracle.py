@@ -50,7 +50,9 @@ def decode_weight(a, dtype=np.float64) -> np.ndarray:
     """Float view of a weight array; uint16 arrays are raw bf16 bit patterns."""
     a = np.asarray(a)
     if a.dtype == np.uint16:
-        a = (a.astype(np.uint32) << 16).view(np.float32)
+        bits = np.empty(a.shape, dtype=np.uint32)
+        np.left_shift(a, 16, out=bits, dtype=np.uint32)
+        a = bits.view(np.float32)
     return a.astype(dtype, copy=False)
 
 

@@ -1,0 +1,209 @@
+// EB-Sampler step (Sec. 2.2, eq. (eb_sampler)) on the block's fp32 logits.
+//
+// eb_partial: one workgroup per (vocabulary chunk of 4096, masked row).  It finds the
+// chunk maximum m_c (and the smallest id reaching it, the mask column excluded), then
+// with t = l - m_c in float64 accumulates Z_c = sum e^t and S_c = sum e^t t.  Sums are
+// per-thread in a fixed order followed by a fixed tree, so results are reproducible.
+//
+// eb_select: one wave per sequence, lane j = block row j.  Rows merge their chunks in
+// vocabulary order with M = max m_c, delta_c = m_c - M:
+//   Z = sum_c e^delta_c Z_c,  S = sum_c e^delta_c (S_c + delta_c Z_c),  H = log Z - S / Z
+// (the entropy of softmax over the row; argmax = first chunk reaching M).  Then the
+// masked rows are ranked by (H, row), lane 0 forms the running float64 sums c_r in
+// that order, s = max{r >= 1 : c_{r-1} <= gamma}, and the first s rows are written out
+// in ascending row order.
+
+#include "sbd_device.h"
+
+namespace sbd {
+
+__device__ __forceinline__ double shfl_xor_d(double v, int m) {
+  const int2 iv = *reinterpret_cast<int2*>(&v);
+  int2 o;
+  o.x = __shfl_xor(iv.x, m);
+  o.y = __shfl_xor(iv.y, m);
+  return *reinterpret_cast<double*>(&o);
+}
+
+constexpr int kEbThreads = 256;
+constexpr int kEbPer = kEbChunk / kEbThreads;  // 16 entries per thread
+
+__global__ __launch_bounds__(kEbThreads) void eb_partial_kernel(EbArgs a) {
+  __shared__ float smax[kEbThreads / 64];
+  __shared__ int sarg[kEbThreads / 64];
+  __shared__ double sz[kEbThreads / 64], ss[kEbThreads / 64];
+  const int row = blockIdx.y;
+  if (!a.is_mask[row]) return;
+  const int c = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const float* lr = a.logits + (int64_t)row * a.vocab;
+  const int v0 = c * kEbChunk;
+
+  float val[kEbPer];
+  float mx = -INFINITY;
+  int arg = INT32_MAX;
+#pragma unroll
+  for (int e = 0; e < kEbPer; ++e) {
+    const int v = v0 + tid + e * kEbThreads;
+    const bool ok = v < a.vocab && v != a.mask_id;
+    val[e] = ok ? lr[v] : -INFINITY;
+    if (ok && (val[e] > mx || (val[e] == mx && v < arg))) {
+      mx = val[e];
+      arg = v;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const float om = __shfl_xor(mx, o);
+    const int oa = __shfl_xor(arg, o);
+    if (om > mx || (om == mx && oa < arg)) {
+      mx = om;
+      arg = oa;
+    }
+  }
+  if (lane == 0) {
+    smax[w] = mx;
+    sarg[w] = arg;
+  }
+  __syncthreads();
+  mx = smax[0];
+  arg = sarg[0];
+  for (int i = 1; i < kEbThreads / 64; ++i)
+    if (smax[i] > mx || (smax[i] == mx && sarg[i] < arg)) {
+      mx = smax[i];
+      arg = sarg[i];
+    }
+
+  double z = 0.0, s = 0.0;
+  if (mx != -INFINITY) {
+    const double md = (double)mx;
+#pragma unroll
+    for (int e = 0; e < kEbPer; ++e) {
+      if (val[e] != -INFINITY) {
+        const double t = (double)val[e] - md;
+        const double ex = exp(t);
+        z += ex;
+        s += ex * t;
+      }
+    }
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    z += shfl_xor_d(z, o);
+    s += shfl_xor_d(s, o);
+  }
+  if (lane == 0) {
+    sz[w] = z;
+    ss[w] = s;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    double zt = 0.0, st = 0.0;
+    for (int i = 0; i < kEbThreads / 64; ++i) {
+      zt += sz[i];
+      st += ss[i];
+    }
+    double* p = a.part + ((int64_t)row * a.n_chunks + c) * 3;
+    p[0] = (double)mx;
+    p[1] = zt;
+    p[2] = st;
+    a.part_arg[(int64_t)row * a.n_chunks + c] = (mx == -INFINITY) ? -1 : arg;
+  }
+}
+
+template <bool SELECT_ONLY>
+__global__ __launch_bounds__(64) void eb_select_kernel(EbArgs a) {
+  __shared__ double sh[64];
+  __shared__ int smask[64];
+  __shared__ int order[64];
+  __shared__ int s_count;
+  const int b = blockIdx.x;
+  const int j = threadIdx.x;
+  const int k = a.k;
+  const bool in = j < k;
+  const int64_t row = (int64_t)b * k + j;
+  const bool masked = in && a.is_mask[row] != 0;
+
+  double H = 0.0;
+  int tok = -1;
+  if (masked) {
+    if (SELECT_ONLY) {
+      H = a.entropy_in[row];
+    } else {
+      const double* p = a.part + row * a.n_chunks * 3;
+      double M = -INFINITY;
+      for (int c = 0; c < a.n_chunks; ++c) M = fmax(M, p[c * 3]);
+      double Z = 0.0, S = 0.0;
+      for (int c = 0; c < a.n_chunks; ++c) {
+        const double mc = p[c * 3];
+        if (mc == -INFINITY) continue;
+        const double d = mc - M;
+        const double f = exp(d);
+        Z += f * p[c * 3 + 1];
+        S += f * (p[c * 3 + 2] + d * p[c * 3 + 1]);
+        if (tok < 0 && mc == M) tok = a.part_arg[row * a.n_chunks + c];
+      }
+      H = log(Z) - S / Z;
+    }
+  }
+  sh[j] = H;
+  smask[j] = masked ? 1 : 0;
+  __syncthreads();
+
+  int rank = 0, n = 0;
+  for (int i = 0; i < k; ++i) {
+    if (!smask[i]) continue;
+    ++n;
+    if (sh[i] < H || (sh[i] == H && i < j)) ++rank;
+  }
+  if (masked) order[rank] = j;
+  __syncthreads();
+  if (j == 0) {
+    int s = 0;
+    double c = 0.0;
+    for (int r = 0; r < n; ++r) {
+      if (c <= a.gamma) s = r + 1;
+      c += sh[order[r]];
+    }
+    s_count = s;
+    a.n_accepted[b] = s;
+  }
+  __syncthreads();
+  const int s = s_count;
+  const bool acc = masked && rank < s;
+  int idx = 0;
+  for (int i = 0; i < j; ++i) {
+    if (!smask[i]) continue;
+    int ri = 0;
+    for (int q = 0; q < k; ++q)
+      if (smask[q] && (sh[q] < sh[i] || (sh[q] == sh[i] && q < i))) ++ri;
+    if (ri < s) ++idx;
+  }
+  if (in) {
+    if (j >= s) {
+      a.accepted_pos[row] = -1;
+      if (a.accepted_tok) a.accepted_tok[row] = -1;
+    }
+    if (a.entropy_out) a.entropy_out[row] = masked ? H : __builtin_nan("");
+  }
+  __syncthreads();
+  if (acc) {
+    a.accepted_pos[(int64_t)b * k + idx] = j;
+    if (a.accepted_tok) a.accepted_tok[(int64_t)b * k + idx] = tok;
+  }
+}
+
+hipError_t launch_eb_partial(const EbArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(eb_partial_kernel, dim3(a.n_chunks, a.B * a.k), dim3(kEbThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_eb_select(const EbArgs& a, bool select_only, hipStream_t s) {
+  if (select_only)
+    hipLaunchKernelGGL(eb_select_kernel<true>, dim3(a.B), dim3(64), 0, s, a);
+  else
+    hipLaunchKernelGGL(eb_select_kernel<false>, dim3(a.B), dim3(64), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace sbd

@@ -1,0 +1,153 @@
+// Small per-row kernels of the block forward: embedding gather, RoPE + q/k-norm +
+// KV staging, the RoPE angle table, and KV-cache import/export.
+//
+// KV-cache layout, per (layer, slot, KV head), capacity `cap` positions:
+//   K: [cap][d_h] bf16, post-RoPE keys, one row per position.
+//   V: [cap/32][d_h][32] bf16, each 32-position block stored transposed (dimension-major)
+//      with its positions permuted by vslot() so that one 16-byte load gives the eight
+//      values the attention kernel's P.V MFMA needs for one dimension.
+
+#include "sbd_device.h"
+
+namespace sbd {
+
+// Storage slot inside a 32-position V block of position p (0..31): positions
+// {16t + 4q + i : t in {0,1}, i < 4} (the keys lane group q holds after the score MFMA)
+// become the contiguous slots 8q .. 8q + 7.
+__device__ __forceinline__ int vslot(int p) { return ((p & 15) >> 2) * 8 + (p >> 4) * 4 + (p & 3); }
+
+__device__ __forceinline__ int64_t kv_head_base(int layer, int slot, int g, int n_slots, int n_kv,
+                                                int64_t cap, int d_h) {
+  return (((int64_t)layer * n_slots + slot) * n_kv + g) * cap * d_h;
+}
+
+// x[m] = E[tok[m]] (fp32), xn[m] = bf16(x * g), sumsq[m][c/32] = sum over 32 columns of x^2.
+__global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
+  const int m = blockIdx.y;
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  const int tok = a.rows[m].tok;
+  const float v = bf2f(a.embed[(int64_t)tok * a.d + c]);
+  a.x[(int64_t)m * a.d + c] = v;
+  a.xn[(int64_t)m * a.d + c] = f2bf(v * bf2f(a.g[c]));
+  const float s = half_wave_sum(v * v);
+  if ((threadIdx.x & 31) == 0) a.sumsq[(int64_t)m * (a.d / 32) + c / 32] = s;
+}
+
+hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(embed_kernel, dim3(a.d / 256, a.M), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// One wave per (row, head).  Lane i < d_h/2 owns the RoPE pair (i, i + d_h/2).
+// Query heads: optional per-head RMSNorm, rotation, scaling, bf16 store.
+// Key heads: optional per-head RMSNorm, rotation, store into the cache at position
+// cache_len + j.  Value heads: store into the transposed V block.
+__global__ __launch_bounds__(64) void rope_stage_kernel(RopeStageArgs a) {
+  const int h = blockIdx.x;
+  const int m = blockIdx.y;
+  const int lane = threadIdx.x;
+  const int half = a.d_h / 2;
+  const bool act = lane < half;
+  const int b = m / a.k, j = m % a.k;
+  const SeqParam sp = a.seqs[b];
+  const int p_cache = sp.cache_len + j;
+  const int pos = a.rows[m].pos;
+  const float* src = a.qkv + (int64_t)m * (a.n_q + 2 * a.n_kv) * a.d_h + (int64_t)h * a.d_h;
+  float u0 = act ? src[lane] : 0.f;
+  float u1 = act ? src[lane + half] : 0.f;
+
+  if (h < a.n_q + a.n_kv) {
+    const bool is_q = h < a.n_q;
+    if (a.qk_norm) {
+      const float ss = wave_sum(u0 * u0 + u1 * u1);
+      const float rinv = 1.0f / sqrtf(ss / (float)a.d_h + a.eps);
+      const bf16_t* gn = is_q ? a.q_norm : a.k_norm;
+      if (act) {
+        u0 = u0 * rinv * bf2f(gn[lane]);
+        u1 = u1 * rinv * bf2f(gn[lane + half]);
+      }
+    }
+    if (!act) return;
+    const float c = a.rope[((int64_t)pos * half + lane) * 2 + 0];
+    const float sn = a.rope[((int64_t)pos * half + lane) * 2 + 1];
+    const float r0 = u0 * c - u1 * sn;
+    const float r1 = u1 * c + u0 * sn;
+    if (is_q) {
+      bf16_t* dst = a.q + ((int64_t)m * a.n_q + h) * a.d_h;
+      dst[lane] = f2bf(r0 * a.q_scale);
+      dst[lane + half] = f2bf(r1 * a.q_scale);
+    } else {
+      const int g = h - a.n_q;
+      bf16_t* dst = a.kcache + kv_head_base(a.layer, sp.slot, g, a.n_slots, a.n_kv, a.cap, a.d_h) +
+                    (int64_t)p_cache * a.d_h;
+      dst[lane] = f2bf(r0);
+      dst[lane + half] = f2bf(r1);
+    }
+  } else {
+    if (!act) return;
+    const int g = h - a.n_q - a.n_kv;
+    bf16_t* blk = a.vcache + kv_head_base(a.layer, sp.slot, g, a.n_slots, a.n_kv, a.cap, a.d_h) +
+                  (int64_t)(p_cache / 32) * a.d_h * 32;
+    const int sl = vslot(p_cache & 31);
+    blk[(int64_t)lane * 32 + sl] = f2bf(u0);
+    blk[(int64_t)(lane + half) * 32 + sl] = f2bf(u1);
+  }
+}
+
+hipError_t launch_rope_stage(const RopeStageArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(rope_stage_kernel, dim3(a.n_q + 2 * a.n_kv, a.M), dim3(64), 0, s, a);
+  return hipGetLastError();
+}
+
+// rope[p][i] = (cos, sin)(p * theta^(-2i/d_h)), angles in float64.
+__global__ void rope_table_kernel(float* rope, int64_t cap, int d_h, double theta) {
+  const int half = d_h / 2;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= cap * half) return;
+  const int64_t p = idx / half;
+  const int i = (int)(idx % half);
+  const double inv_freq = pow(theta, -2.0 * (double)i / (double)d_h);
+  const double phi = (double)p * inv_freq;
+  rope[idx * 2 + 0] = (float)cos(phi);
+  rope[idx * 2 + 1] = (float)sin(phi);
+}
+
+hipError_t launch_rope_table(float* rope, int64_t cap, int d_h, double theta, hipStream_t s) {
+  const int64_t n = cap * (d_h / 2);
+  hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, rope,
+                     cap, d_h, theta);
+  return hipGetLastError();
+}
+
+// grid (n, n_kv, n_layers); lanes walk the head dimension.
+template <bool IMPORT>
+__global__ __launch_bounds__(64) void kv_copy_kernel(KvCopyArgs a) {
+  const int t = blockIdx.x, g = blockIdx.y, layer = blockIdx.z;
+  const int p = a.pos0 + t;
+  const int64_t hb = kv_head_base(layer, a.slot, g, a.n_slots, a.n_kv, a.cap, a.d_h);
+  const int64_t io = (((int64_t)layer * a.n + t) * a.n_kv + g) * a.d_h;
+  bf16_t* kc = a.kcache + hb + (int64_t)p * a.d_h;
+  bf16_t* vb = a.vcache + hb + (int64_t)(p / 32) * a.d_h * 32;
+  const int sl = vslot(p & 31);
+  for (int i = threadIdx.x; i < a.d_h; i += 64) {
+    if (IMPORT) {
+      kc[i] = a.k_in[io + i];
+      vb[(int64_t)i * 32 + sl] = a.v_in[io + i];
+    } else {
+      a.k_out[io + i] = kc[i];
+      a.v_out[io + i] = vb[(int64_t)i * 32 + sl];
+    }
+  }
+}
+
+hipError_t launch_kv_import(const KvCopyArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(kv_copy_kernel<true>, dim3(a.n, a.n_kv, a.n_layers), dim3(64), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_export(const KvCopyArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(kv_copy_kernel<false>, dim3(a.n, a.n_kv, a.n_layers), dim3(64), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace sbd

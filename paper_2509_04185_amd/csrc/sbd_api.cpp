@@ -1,0 +1,673 @@
+// C ABI of the SBD decode step: argument/state validation, KV-cache bookkeeping and the
+// launch sequence of the block forward (eq. (hybrid_block) of Set Block Decoding) and of
+// the EB-Sampler step (eq. (eb_sampler)).  Everything here runs on the host; all
+// arithmetic happens in the kernels of gemm.hip, attention.hip, misc.hip and eb.hip.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "sbd_internal.h"
+
+using namespace sbd;
+
+namespace {
+
+thread_local std::string g_err;  // last error of a context-less call
+
+size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+
+int effective_chunk(const sbd_model_config& c) { return c.prefill_chunk > 0 ? c.prefill_chunk : 256; }
+
+const char* check_config(const sbd_model_config& c) {
+  if (c.n_layers < 1) return "n_layers must be >= 1";
+  if (c.d_model < 256 || c.d_model % 256) return "d_model must be a positive multiple of 256";
+  if (c.head_dim != 64 && c.head_dim != 128) return "head_dim must be 64 or 128";
+  if (c.n_q_heads < 1 || c.n_kv_heads < 1 || c.n_q_heads % c.n_kv_heads)
+    return "n_q_heads must be a positive multiple of n_kv_heads";
+  if ((c.n_q_heads * c.head_dim) % 256) return "n_q_heads*head_dim must be a multiple of 256";
+  if (c.ffn_dim < 256 || c.ffn_dim % 256) return "ffn_dim must be a positive multiple of 256";
+  if (c.vocab < 32 || c.vocab % 32) return "vocab must be a positive multiple of 32";
+  if (c.mask_id < 0 || c.mask_id >= c.vocab) return "mask_id must lie in [0, vocab)";
+  if (c.qk_norm != 0 && c.qk_norm != 1) return "qk_norm must be 0 or 1";
+  if (!(c.rms_eps > 0.f) || !std::isfinite(c.rms_eps)) return "rms_eps must be a positive number";
+  if (!(c.rope_theta > 0.f) || !std::isfinite(c.rope_theta)) return "rope_theta must be a positive number";
+  if (c.max_batch < 1 || c.max_batch > 4096) return "max_batch must lie in [1, 4096]";
+  if (c.max_seq_len < 1 || c.max_seq_len > (1 << 24)) return "max_seq_len must lie in [1, 2^24]";
+  if (c.max_block < 1 || c.max_block > kMaxBlock) return "max_block must lie in [1, 64]";
+  if (c.prefill_chunk < 0 || c.prefill_chunk > 4096) return "prefill_chunk must lie in [0, 4096]";
+  return nullptr;
+}
+
+}  // namespace
+
+bool sbd::compute_layout(const sbd_model_config& c, Layout* L) {
+  if (check_config(c)) return false;
+  Layout o{};
+  o.cap = ((int64_t)c.max_seq_len + 63) / 64 * 64;
+  o.m_max = std::max<int64_t>((int64_t)c.max_batch * c.max_block, effective_chunk(c));
+  o.n_qkv = (int64_t)(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+  o.n_part = c.d_model / 32;
+  o.eb_chunks = (c.vocab + kEbChunk - 1) / kEbChunk;
+  const int64_t qd = (int64_t)c.n_q_heads * c.head_dim;
+  const int64_t kv_elems = (int64_t)c.n_layers * c.max_batch * c.n_kv_heads * o.cap * c.head_dim;
+  const int64_t eb_rows = (int64_t)c.max_batch * c.max_block;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align256(off + bytes);
+    return at;
+  };
+  o.kcache = take(kv_elems * 2);
+  o.vcache = take(kv_elems * 2);
+  o.rope = take(o.cap * (c.head_dim / 2) * 2 * sizeof(float));
+  o.x = take(o.m_max * c.d_model * sizeof(float));
+  o.xn = take(o.m_max * c.d_model * 2);
+  o.sumsq = take(o.m_max * o.n_part * sizeof(float));
+  o.qkv = take(o.m_max * o.n_qkv * sizeof(float));
+  o.q = take(o.m_max * qd * 2);
+  o.attn = take(o.m_max * qd * 2);
+  o.act = take(o.m_max * (int64_t)c.ffn_dim * 2);
+  o.attn_ml = take((int64_t)kMaxSplits * o.m_max * c.n_q_heads * 2 * sizeof(float));
+  o.attn_o = take((int64_t)kMaxSplits * o.m_max * qd * sizeof(float));
+  o.rows = take(o.m_max * sizeof(RowParam));
+  o.seqs = take((int64_t)c.max_batch * sizeof(SeqParam));
+  o.eb_mask = take(eb_rows);
+  o.eb_part = take(eb_rows * o.eb_chunks * 3 * sizeof(double));
+  o.eb_arg = take(eb_rows * o.eb_chunks * sizeof(int32_t));
+  o.total = off;
+  *L = o;
+  return true;
+}
+
+struct sbd_ctx {
+  sbd_model_config cfg{};
+  Layout lay{};
+  std::vector<LayerW> layers;
+  const bf16_t *embed = nullptr, *lm_head = nullptr, *final_norm = nullptr;
+  char* ws = nullptr;
+  hipStream_t stream = nullptr;
+  std::vector<int32_t> cache_len, staged;
+  static constexpr int kRing = 4;
+  void* stage[kRing] = {};
+  hipEvent_t ev[kRing] = {};
+  bool ev_used[kRing] = {};
+  int ring = 0;
+  size_t stage_bytes = 0;
+  std::string err;
+  // per-kernel timing (sbd_profile_enable)
+  bool prof = false;
+  struct Rec { int kind; hipEvent_t a, b; };
+  std::vector<Rec> recs;
+  std::vector<hipEvent_t> pool;
+  int32_t prof_count[SBD_KERNEL_COUNT] = {};
+  double prof_ms[SBD_KERNEL_COUNT] = {};
+
+  template <class T>
+  T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
+};
+
+namespace {
+
+sbd_status fail(sbd_ctx* c, sbd_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  if (c) c->err = buf; else g_err = buf;
+  return st;
+}
+
+#define SBD_HIP(ctx, expr)                                                                  \
+  do {                                                                                      \
+    hipError_t e_ = (expr);                                                                 \
+    if (e_ != hipSuccess)                                                                   \
+      return fail(ctx, SBD_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(e_));         \
+  } while (0)
+
+// Asynchronous faults of earlier work surface here.
+sbd_status check_sticky(sbd_ctx* c) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(c, SBD_ERR_HIP, "earlier HIP error: %s", hipGetErrorString(e));
+  return SBD_OK;
+}
+
+// Copy host bytes to a device address on the context stream through a pinned ring slot.
+sbd_status upload(sbd_ctx* c, void* dst, const void* src, size_t bytes) {
+  if (bytes == 0) return SBD_OK;
+  if (bytes > c->stage_bytes) return fail(c, SBD_ERR_INVALID_ARG, "upload of %zu bytes too large", bytes);
+  const int i = c->ring;
+  c->ring = (c->ring + 1) % sbd_ctx::kRing;
+  if (c->ev_used[i]) SBD_HIP(c, hipEventSynchronize(c->ev[i]));
+  std::memcpy(c->stage[i], src, bytes);
+  SBD_HIP(c, hipMemcpyAsync(dst, c->stage[i], bytes, hipMemcpyHostToDevice, c->stream));
+  SBD_HIP(c, hipEventRecord(c->ev[i], c->stream));
+  c->ev_used[i] = true;
+  return SBD_OK;
+}
+
+hipEvent_t take_event(sbd_ctx* c) {
+  if (!c->pool.empty()) {
+    hipEvent_t e = c->pool.back();
+    c->pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Launch `expr` on the context stream; when profiling, bracket it with a pair of events.
+#define SBD_LAUNCH(ctx, kind, expr)                                               \
+  do {                                                                            \
+    hipEvent_t ea_ = nullptr, eb_ = nullptr;                                      \
+    if ((ctx)->prof) {                                                            \
+      ea_ = take_event(ctx);                                                      \
+      eb_ = take_event(ctx);                                                      \
+      if (!ea_ || !eb_) return fail(ctx, SBD_ERR_HIP, "hipEventCreate failed");   \
+      SBD_HIP(ctx, hipEventRecord(ea_, (ctx)->stream));                           \
+    }                                                                             \
+    SBD_HIP(ctx, expr);                                                           \
+    if ((ctx)->prof) {                                                            \
+      SBD_HIP(ctx, hipEventRecord(eb_, (ctx)->stream));                           \
+      (ctx)->recs.push_back(sbd_ctx::Rec{kind, ea_, eb_});                        \
+    }                                                                             \
+  } while (0)
+
+int pick_splits(int64_t work_groups_per_split, int nblocks) {
+  int s = (int)std::max<int64_t>(1, (1024 + work_groups_per_split - 1) / work_groups_per_split);
+  s = std::min(s, kMaxSplits);
+  s = std::min(s, std::max(1, nblocks));
+  return s;
+}
+
+// One forward of B sequences x k rows whose per-row / per-sequence parameters are given.
+// lm_row < 0: logits for all rows into `logits`; otherwise only for row lm_row.
+sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& rows,
+                       const std::vector<SeqParam>& seqs, float* logits, int lm_row) {
+  const sbd_model_config& m = c->cfg;
+  const Layout& L = c->lay;
+  const int M = B * k;
+  const int d = m.d_model, dh = m.head_dim, nq = m.n_q_heads, nkv = m.n_kv_heads;
+  const int qd = nq * dh;
+  sbd_status st = upload(c, c->ws + L.rows, rows.data(), rows.size() * sizeof(RowParam));
+  if (st) return st;
+  st = upload(c, c->ws + L.seqs, seqs.data(), seqs.size() * sizeof(SeqParam));
+  if (st) return st;
+
+  float* x = c->at<float>(L.x);
+  bf16_t* xn = c->at<bf16_t>(L.xn);
+  float* sumsq = c->at<float>(L.sumsq);
+  float* qkv = c->at<float>(L.qkv);
+  bf16_t* q = c->at<bf16_t>(L.q);
+  bf16_t* attn = c->at<bf16_t>(L.attn);
+  bf16_t* act = c->at<bf16_t>(L.act);
+  const RowParam* drows = c->at<RowParam>(L.rows);
+  const SeqParam* dseqs = c->at<SeqParam>(L.seqs);
+
+  EmbedArgs ea{drows, M, d, c->embed, c->layers[0].attn_norm, x, xn, sumsq};
+  SBD_LAUNCH(c, SBD_KERNEL_EMBED, launch_embed(ea, c->stream));
+
+  int max_end = 0;
+  for (const SeqParam& s : seqs) max_end = std::max(max_end, s.cache_len + k);
+  const int G = nq / nkv;
+  const int n_rb = (G * k + 63) / 64;
+  const int nblocks = (max_end + 31) / 32;
+  int n_splits = pick_splits((int64_t)B * nkv * n_rb, nblocks);
+  const int bps = (nblocks + n_splits - 1) / n_splits;
+  n_splits = (nblocks + bps - 1) / bps;
+
+  for (int l = 0; l < m.n_layers; ++l) {
+    const LayerW& w = c->layers[l];
+    GemmArgs g{};
+    g.A = xn; g.lda = d; g.M = M; g.K = d;
+    g.W0 = w.wq; g.W1 = w.wk; g.W2 = w.wv; g.n0 = qd; g.n1 = nkv * dh;
+    g.n_tiles = (int)(L.n_qkv / 32);
+    g.out_f32 = qkv; g.ldo = L.n_qkv;
+    g.sumsq_in = sumsq; g.n_part = (int)L.n_part; g.inv_d = 1.0f / d; g.eps = m.rms_eps;
+    SBD_LAUNCH(c, SBD_KERNEL_QKV, launch_gemm(EPI_SCALED_STORE, g, c->stream));
+
+    RopeStageArgs ra{};
+    ra.rows = drows; ra.seqs = dseqs; ra.M = M; ra.k = k; ra.layer = l;
+    ra.n_q = nq; ra.n_kv = nkv; ra.d_h = dh; ra.qk_norm = m.qk_norm; ra.eps = m.rms_eps;
+    ra.q_scale = (float)(1.4426950408889634 / std::sqrt((double)dh));
+    ra.qkv = qkv; ra.q_norm = w.q_norm; ra.k_norm = w.k_norm; ra.rope = c->at<float>(L.rope);
+    ra.q = q; ra.kcache = c->at<bf16_t>(L.kcache); ra.vcache = c->at<bf16_t>(L.vcache);
+    ra.cap = L.cap; ra.n_slots = m.max_batch;
+    SBD_LAUNCH(c, SBD_KERNEL_ROPE, launch_rope_stage(ra, c->stream));
+
+    AttnArgs aa{};
+    aa.seqs = dseqs; aa.B = B; aa.k = k; aa.layer = l; aa.n_q = nq; aa.n_kv = nkv; aa.d_h = dh;
+    aa.q = q; aa.kcache = ra.kcache; aa.vcache = ra.vcache; aa.cap = L.cap; aa.n_slots = m.max_batch;
+    aa.n_rowblocks = n_rb; aa.n_splits = n_splits; aa.blocks_per_split = bps;
+    aa.part_ml = c->at<float>(L.attn_ml); aa.part_o = c->at<float>(L.attn_o); aa.out = attn;
+    SBD_LAUNCH(c, SBD_KERNEL_ATTENTION, launch_attention_split(aa, c->stream));
+    SBD_LAUNCH(c, SBD_KERNEL_ATTN_MERGE, launch_attention_merge(aa, c->stream));
+
+    GemmArgs go{};
+    go.A = attn; go.lda = qd; go.M = M; go.K = qd;
+    go.W0 = w.wo; go.n0 = d; go.n1 = 0; go.n_tiles = d / 32;
+    go.x = x; go.ldx = d; go.xn = xn; go.g_next = w.mlp_norm; go.sumsq_out = sumsq;
+    go.n_part = (int)L.n_part;
+    SBD_LAUNCH(c, SBD_KERNEL_O_PROJ, launch_gemm(EPI_RESID, go, c->stream));
+
+    GemmArgs gu{};
+    gu.A = xn; gu.lda = d; gu.M = M; gu.K = d;
+    gu.W0 = w.w_gate; gu.W1 = w.w_up; gu.n_tiles = m.ffn_dim / 16;
+    gu.sumsq_in = sumsq; gu.n_part = (int)L.n_part; gu.inv_d = 1.0f / d; gu.eps = m.rms_eps;
+    gu.act = act; gu.ld_act = m.ffn_dim;
+    SBD_LAUNCH(c, SBD_KERNEL_GATE_UP, launch_gemm(EPI_SWIGLU, gu, c->stream));
+
+    GemmArgs gd{};
+    gd.A = act; gd.lda = m.ffn_dim; gd.M = M; gd.K = m.ffn_dim;
+    gd.W0 = w.w_down; gd.n0 = d; gd.n1 = 0; gd.n_tiles = d / 32;
+    gd.x = x; gd.ldx = d; gd.xn = xn;
+    gd.g_next = (l + 1 < m.n_layers) ? c->layers[l + 1].attn_norm : c->final_norm;
+    gd.sumsq_out = sumsq; gd.n_part = (int)L.n_part;
+    SBD_LAUNCH(c, SBD_KERNEL_DOWN, launch_gemm(EPI_RESID, gd, c->stream));
+  }
+
+  if (logits != nullptr) {
+    GemmArgs gl{};
+    const int r0 = lm_row < 0 ? 0 : lm_row;
+    gl.A = xn + (int64_t)r0 * d; gl.lda = d; gl.M = lm_row < 0 ? M : 1; gl.K = d;
+    gl.W0 = c->lm_head; gl.n0 = m.vocab; gl.n1 = 0; gl.n_tiles = m.vocab / 32;
+    gl.out_f32 = logits; gl.ldo = m.vocab;
+    gl.sumsq_in = sumsq + (int64_t)r0 * L.n_part; gl.n_part = (int)L.n_part;
+    gl.inv_d = 1.0f / d; gl.eps = m.rms_eps;
+    SBD_LAUNCH(c, SBD_KERNEL_LM_HEAD, launch_gemm(EPI_SCALED_STORE, gl, c->stream));
+  }
+  return SBD_OK;
+}
+
+bool seq_ok(const sbd_ctx* c, int32_t seq) { return seq >= 0 && seq < c->cfg.max_batch; }
+
+}  // namespace
+
+extern "C" {
+
+sbd_status sbd_workspace_bytes(const sbd_model_config* cfg, size_t* bytes) {
+  if (!cfg || !bytes) return fail(nullptr, SBD_ERR_INVALID_ARG, "null argument");
+  if (const char* why = check_config(*cfg)) return fail(nullptr, SBD_ERR_UNSUPPORTED, "%s", why);
+  Layout L;
+  compute_layout(*cfg, &L);
+  *bytes = L.total;
+  return SBD_OK;
+}
+
+sbd_status sbd_workspace_region(const sbd_model_config* cfg, const char* name, size_t* offset,
+                                size_t* bytes) {
+  if (!cfg || !name || !offset || !bytes) return fail(nullptr, SBD_ERR_INVALID_ARG, "null argument");
+  if (const char* why = check_config(*cfg)) return fail(nullptr, SBD_ERR_UNSUPPORTED, "%s", why);
+  Layout L;
+  compute_layout(*cfg, &L);
+  const int64_t qd = (int64_t)cfg->n_q_heads * cfg->head_dim;
+  struct R { const char* n; size_t off, sz; } regions[] = {
+      {"x", L.x, (size_t)(L.m_max * cfg->d_model * 4)},
+      {"qkv", L.qkv, (size_t)(L.m_max * L.n_qkv * 4)},
+      {"q", L.q, (size_t)(L.m_max * qd * 2)},
+      {"attn", L.attn, (size_t)(L.m_max * qd * 2)},
+      {"act", L.act, (size_t)(L.m_max * cfg->ffn_dim * 2)},
+      {"xn", L.xn, (size_t)(L.m_max * cfg->d_model * 2)},
+  };
+  for (const R& r : regions)
+    if (std::strcmp(r.n, name) == 0) {
+      *offset = r.off;
+      *bytes = r.sz;
+      return SBD_OK;
+    }
+  return fail(nullptr, SBD_ERR_INVALID_ARG, "unknown region '%s'", name);
+}
+
+sbd_status sbd_create(const sbd_model_config* cfg, const sbd_weights* w, void* workspace,
+                      size_t workspace_bytes, void* stream, sbd_ctx** out) {
+  if (!cfg || !w || !out) return fail(nullptr, SBD_ERR_INVALID_ARG, "null argument");
+  *out = nullptr;
+  if (const char* why = check_config(*cfg)) return fail(nullptr, SBD_ERR_UNSUPPORTED, "%s", why);
+  Layout L;
+  compute_layout(*cfg, &L);
+  if (!workspace) return fail(nullptr, SBD_ERR_INVALID_ARG, "workspace is null");
+  if (reinterpret_cast<uintptr_t>(workspace) % 256)
+    return fail(nullptr, SBD_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  if (workspace_bytes < L.total)
+    return fail(nullptr, SBD_ERR_OUT_OF_MEMORY, "workspace has %zu bytes, needs %zu", workspace_bytes, L.total);
+  if (!w->embed || !w->lm_head || !w->final_norm || !w->attn_norm || !w->wq || !w->wk || !w->wv ||
+      !w->wo || !w->mlp_norm || !w->w_gate || !w->w_up || !w->w_down)
+    return fail(nullptr, SBD_ERR_INVALID_ARG, "a weight pointer is null");
+  if (cfg->qk_norm && (!w->q_norm || !w->k_norm))
+    return fail(nullptr, SBD_ERR_INVALID_ARG, "qk_norm needs q_norm and k_norm");
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    if (!w->attn_norm[l] || !w->wq[l] || !w->wk[l] || !w->wv[l] || !w->wo[l] || !w->mlp_norm[l] ||
+        !w->w_gate[l] || !w->w_up[l] || !w->w_down[l] ||
+        (cfg->qk_norm && (!w->q_norm[l] || !w->k_norm[l])))
+      return fail(nullptr, SBD_ERR_INVALID_ARG, "a weight pointer of layer %d is null", l);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(nullptr, SBD_ERR_HIP, "earlier HIP error: %s", hipGetErrorString(e));
+
+  sbd_ctx* c = new sbd_ctx();
+  c->cfg = *cfg;
+  c->lay = L;
+  c->ws = static_cast<char*>(workspace);
+  c->stream = static_cast<hipStream_t>(stream);
+  c->embed = static_cast<const bf16_t*>(w->embed);
+  c->lm_head = static_cast<const bf16_t*>(w->lm_head);
+  c->final_norm = static_cast<const bf16_t*>(w->final_norm);
+  c->layers.resize(cfg->n_layers);
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    LayerW& lw = c->layers[l];
+    lw.attn_norm = static_cast<const bf16_t*>(w->attn_norm[l]);
+    lw.wq = static_cast<const bf16_t*>(w->wq[l]);
+    lw.wk = static_cast<const bf16_t*>(w->wk[l]);
+    lw.wv = static_cast<const bf16_t*>(w->wv[l]);
+    lw.wo = static_cast<const bf16_t*>(w->wo[l]);
+    lw.q_norm = cfg->qk_norm ? static_cast<const bf16_t*>(w->q_norm[l]) : nullptr;
+    lw.k_norm = cfg->qk_norm ? static_cast<const bf16_t*>(w->k_norm[l]) : nullptr;
+    lw.mlp_norm = static_cast<const bf16_t*>(w->mlp_norm[l]);
+    lw.w_gate = static_cast<const bf16_t*>(w->w_gate[l]);
+    lw.w_up = static_cast<const bf16_t*>(w->w_up[l]);
+    lw.w_down = static_cast<const bf16_t*>(w->w_down[l]);
+  }
+  c->cache_len.assign(cfg->max_batch, 0);
+  c->staged.assign(cfg->max_batch, 0);
+  c->stage_bytes = std::max<size_t>(L.m_max * sizeof(RowParam),
+                                    std::max<size_t>((size_t)cfg->max_batch * sizeof(SeqParam),
+                                                     (size_t)cfg->max_batch * cfg->max_block));
+  auto cleanup = [&](sbd_status st) {
+    for (int i = 0; i < sbd_ctx::kRing; ++i) {
+      if (c->stage[i]) (void)hipHostFree(c->stage[i]);
+      if (c->ev[i]) (void)hipEventDestroy(c->ev[i]);
+    }
+    g_err = c->err;
+    delete c;
+    return st;
+  };
+  for (int i = 0; i < sbd_ctx::kRing; ++i) {
+    if (hipHostMalloc(&c->stage[i], c->stage_bytes, hipHostMallocDefault) != hipSuccess) {
+      c->stage[i] = nullptr;
+      c->err = "hipHostMalloc of the staging buffer failed";
+      return cleanup(SBD_ERR_HIP);
+    }
+    if (hipEventCreateWithFlags(&c->ev[i], hipEventDisableTiming) != hipSuccess) {
+      c->ev[i] = nullptr;
+      c->err = "hipEventCreate failed";
+      return cleanup(SBD_ERR_HIP);
+    }
+  }
+  // Zero the KV cache once so never-written slots hold finite values.
+  const size_t kv_bytes = L.rope - L.kcache;
+  if (hipMemsetAsync(c->ws + L.kcache, 0, kv_bytes, c->stream) != hipSuccess ||
+      launch_rope_table(c->at<float>(L.rope), L.cap, cfg->head_dim, (double)cfg->rope_theta,
+                        c->stream) != hipSuccess) {
+    c->err = "initialising the workspace failed";
+    return cleanup(SBD_ERR_HIP);
+  }
+  *out = c;
+  return SBD_OK;
+}
+
+sbd_status sbd_destroy(sbd_ctx* c) {
+  if (!c) return fail(nullptr, SBD_ERR_INVALID_ARG, "null context");
+  (void)hipStreamSynchronize(c->stream);
+  for (auto& r : c->recs) {
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  for (hipEvent_t e : c->pool) (void)hipEventDestroy(e);
+  for (int i = 0; i < sbd_ctx::kRing; ++i) {
+    if (c->stage[i]) (void)hipHostFree(c->stage[i]);
+    if (c->ev[i]) (void)hipEventDestroy(c->ev[i]);
+  }
+  delete c;
+  return SBD_OK;
+}
+
+sbd_status sbd_set_stream(sbd_ctx* c, void* stream) {
+  if (!c) return fail(nullptr, SBD_ERR_INVALID_ARG, "null context");
+  c->stream = static_cast<hipStream_t>(stream);
+  return SBD_OK;
+}
+
+sbd_status sbd_reset(sbd_ctx* c, int32_t seq) {
+  if (!c) return fail(nullptr, SBD_ERR_INVALID_ARG, "null context");
+  if (!seq_ok(c, seq)) return fail(c, SBD_ERR_INVALID_ARG, "seq %d out of range", seq);
+  c->cache_len[seq] = 0;
+  c->staged[seq] = 0;
+  return SBD_OK;
+}
+
+sbd_status sbd_cache_len(const sbd_ctx* c, int32_t seq, int32_t* len) {
+  if (!c || !len) return fail(nullptr, SBD_ERR_INVALID_ARG, "null argument");
+  if (!seq_ok(c, seq)) return fail(const_cast<sbd_ctx*>(c), SBD_ERR_INVALID_ARG, "seq %d out of range", seq);
+  *len = c->cache_len[seq];
+  return SBD_OK;
+}
+
+sbd_status sbd_prefill(sbd_ctx* c, int32_t seq, const int32_t* tokens, int32_t n, float* last_logits) {
+  if (!c) return fail(nullptr, SBD_ERR_INVALID_ARG, "null context");
+  if (!seq_ok(c, seq)) return fail(c, SBD_ERR_INVALID_ARG, "seq %d out of range", seq);
+  if (!tokens || n < 1) return fail(c, SBD_ERR_INVALID_ARG, "need n >= 1 tokens");
+  for (int i = 0; i < n; ++i)
+    if (tokens[i] < 0 || tokens[i] >= c->cfg.vocab || tokens[i] == c->cfg.mask_id)
+      return fail(c, SBD_ERR_INVALID_ARG, "prompt token %d (=%d) out of range or the mask id", i, tokens[i]);
+  if ((int64_t)c->cache_len[seq] + n > c->cfg.max_seq_len)
+    return fail(c, SBD_ERR_CAPACITY, "cache_len %d + %d exceeds max_seq_len %d", c->cache_len[seq], n,
+                c->cfg.max_seq_len);
+  if (sbd_status st = check_sticky(c)) return st;
+  const int chunk = effective_chunk(c->cfg);
+  for (int off = 0; off < n; off += chunk) {
+    const int kk = std::min(chunk, n - off);
+    std::vector<RowParam> rows(kk);
+    for (int j = 0; j < kk; ++j) rows[j] = RowParam{tokens[off + j], c->cache_len[seq] + j};
+    std::vector<SeqParam> seqs{SeqParam{seq, c->cache_len[seq], kk, 0}};
+    const bool last = off + kk == n;
+    sbd_status st = run_forward(c, 1, kk, rows, seqs, last ? last_logits : nullptr, kk - 1);
+    if (st) return st;
+    c->cache_len[seq] += kk;
+  }
+  c->staged[seq] = 0;
+  return SBD_OK;
+}
+
+sbd_status sbd_block_forward(sbd_ctx* c, int32_t batch, const int32_t* seq_ids, int32_t k,
+                             const int32_t* tokens, const uint8_t* is_mask, const int32_t* n_causal,
+                             const int32_t* pos_ids, float* logits) {
+  if (!c) return fail(nullptr, SBD_ERR_INVALID_ARG, "null context");
+  const sbd_model_config& m = c->cfg;
+  if (batch < 1 || batch > m.max_batch) return fail(c, SBD_ERR_INVALID_ARG, "batch %d out of [1, %d]", batch, m.max_batch);
+  if (k < 1 || k > m.max_block) return fail(c, SBD_ERR_INVALID_ARG, "k %d out of [1, %d]", k, m.max_block);
+  if (!seq_ids || !tokens || !logits) return fail(c, SBD_ERR_INVALID_ARG, "null argument");
+  std::vector<char> seen(m.max_batch, 0);
+  for (int b = 0; b < batch; ++b) {
+    const int s = seq_ids[b];
+    if (!seq_ok(c, s)) return fail(c, SBD_ERR_INVALID_ARG, "seq_ids[%d] = %d out of range", b, s);
+    if (seen[s]) return fail(c, SBD_ERR_INVALID_ARG, "seq id %d appears twice", s);
+    seen[s] = 1;
+    const int nc = n_causal ? n_causal[b] : 1;
+    if (nc < 0 || nc > k) return fail(c, SBD_ERR_INVALID_ARG, "n_causal[%d] = %d out of [0, k]", b, nc);
+    const int Lb = c->cache_len[s];
+    if ((int64_t)Lb + k > m.max_seq_len)
+      return fail(c, SBD_ERR_CAPACITY, "seq %d: cache_len %d + k %d exceeds max_seq_len %d", s, Lb, k, m.max_seq_len);
+    for (int j = 0; j < k; ++j) {
+      const int t = tokens[b * k + j];
+      if (t < 0 || t >= m.vocab) return fail(c, SBD_ERR_INVALID_ARG, "token[%d][%d] = %d out of range", b, j, t);
+      if (is_mask && (is_mask[b * k + j] != 0) != (t == m.mask_id))
+        return fail(c, SBD_ERR_INVALID_ARG, "is_mask[%d][%d] disagrees with the token", b, j);
+      if (j < nc && t == m.mask_id) return fail(c, SBD_ERR_INVALID_ARG, "causal row %d of batch %d is a mask", j, b);
+      if (pos_ids) {
+        const int p = pos_ids[b * k + j];
+        if (p < 0 || p >= m.max_seq_len) return fail(c, SBD_ERR_INVALID_ARG, "pos_ids[%d][%d] = %d out of range", b, j, p);
+        if (j < nc && p != Lb + j)
+          return fail(c, SBD_ERR_INVALID_ARG, "causal row %d of batch %d must have position %d", j, b, Lb + j);
+      }
+    }
+  }
+  if (sbd_status st = check_sticky(c)) return st;
+  std::vector<RowParam> rows((size_t)batch * k);
+  std::vector<SeqParam> seqs(batch);
+  for (int b = 0; b < batch; ++b) {
+    const int s = seq_ids[b];
+    seqs[b] = SeqParam{s, c->cache_len[s], n_causal ? n_causal[b] : 1, 0};
+    for (int j = 0; j < k; ++j)
+      rows[b * k + j] = RowParam{tokens[b * k + j], pos_ids ? pos_ids[b * k + j] : c->cache_len[s] + j};
+  }
+  sbd_status st = run_forward(c, batch, k, rows, seqs, logits, -1);
+  if (st) return st;
+  for (int b = 0; b < batch; ++b) c->staged[seq_ids[b]] = seqs[b].n_causal;
+  return SBD_OK;
+}
+
+sbd_status sbd_commit(sbd_ctx* c, int32_t batch, const int32_t* seq_ids, const int32_t* n_commit) {
+  if (!c) return fail(nullptr, SBD_ERR_INVALID_ARG, "null context");
+  if (batch < 1 || batch > c->cfg.max_batch || !seq_ids || !n_commit)
+    return fail(c, SBD_ERR_INVALID_ARG, "bad batch or null argument");
+  std::vector<char> seen(c->cfg.max_batch, 0);
+  for (int b = 0; b < batch; ++b) {
+    const int s = seq_ids[b];
+    if (!seq_ok(c, s)) return fail(c, SBD_ERR_INVALID_ARG, "seq_ids[%d] = %d out of range", b, s);
+    if (seen[s]) return fail(c, SBD_ERR_INVALID_ARG, "seq id %d appears twice", s);
+    seen[s] = 1;
+    if (n_commit[b] < 0) return fail(c, SBD_ERR_INVALID_ARG, "n_commit[%d] < 0", b);
+    if (n_commit[b] > c->staged[s])
+      return fail(c, SBD_ERR_STATE, "seq %d: commit of %d rows but only %d causal rows are staged", s,
+                  n_commit[b], c->staged[s]);
+  }
+  for (int b = 0; b < batch; ++b) {
+    c->cache_len[seq_ids[b]] += n_commit[b];
+    c->staged[seq_ids[b]] = 0;
+  }
+  return SBD_OK;
+}
+
+static sbd_status eb_common(sbd_ctx* c, int32_t batch, int32_t k, const uint8_t* is_mask, double gamma,
+                            int32_t* n_accepted, int32_t* accepted_pos) {
+  if (!c) return fail(nullptr, SBD_ERR_INVALID_ARG, "null context");
+  if (batch < 1 || batch > c->cfg.max_batch) return fail(c, SBD_ERR_INVALID_ARG, "batch %d out of range", batch);
+  if (k < 1 || k > c->cfg.max_block) return fail(c, SBD_ERR_INVALID_ARG, "k %d out of range", k);
+  if (!is_mask || !n_accepted || !accepted_pos) return fail(c, SBD_ERR_INVALID_ARG, "null argument");
+  if (std::isnan(gamma) || gamma < 0.0) return fail(c, SBD_ERR_INVALID_ARG, "gamma must be >= 0 (got %g)", gamma);
+  return SBD_OK;
+}
+
+sbd_status sbd_eb_select(sbd_ctx* c, int32_t batch, int32_t k, int32_t vocab, const float* logits,
+                         const uint8_t* is_mask, double gamma, int32_t mask_id, int32_t* n_accepted,
+                         int32_t* accepted_pos, int32_t* accepted_tok, double* entropy) {
+  if (sbd_status st = eb_common(c, batch, k, is_mask, gamma, n_accepted, accepted_pos)) return st;
+  if (!logits || !accepted_tok) return fail(c, SBD_ERR_INVALID_ARG, "null argument");
+  if (vocab < 1 || vocab > c->cfg.vocab) return fail(c, SBD_ERR_INVALID_ARG, "vocab %d out of [1, %d]", vocab, c->cfg.vocab);
+  if (mask_id < -1 || mask_id >= vocab) return fail(c, SBD_ERR_INVALID_ARG, "mask_id %d out of [-1, vocab)", mask_id);
+  if (sbd_status st = check_sticky(c)) return st;
+  if (sbd_status st = upload(c, c->ws + c->lay.eb_mask, is_mask, (size_t)batch * k)) return st;
+  EbArgs a{};
+  a.B = batch; a.k = k; a.vocab = vocab; a.mask_id = mask_id; a.logits = logits;
+  a.is_mask = c->at<uint8_t>(c->lay.eb_mask); a.gamma = gamma;
+  a.n_chunks = (vocab + kEbChunk - 1) / kEbChunk;
+  a.part = c->at<double>(c->lay.eb_part); a.part_arg = c->at<int32_t>(c->lay.eb_arg);
+  a.n_accepted = n_accepted; a.accepted_pos = accepted_pos; a.accepted_tok = accepted_tok;
+  a.entropy_out = entropy;
+  SBD_LAUNCH(c, SBD_KERNEL_EB_PARTIAL, launch_eb_partial(a, c->stream));
+  SBD_LAUNCH(c, SBD_KERNEL_EB_SELECT, launch_eb_select(a, false, c->stream));
+  return SBD_OK;
+}
+
+sbd_status sbd_eb_select_entropies(sbd_ctx* c, int32_t batch, int32_t k, const double* entropy,
+                                   const uint8_t* is_mask, double gamma, int32_t* n_accepted,
+                                   int32_t* accepted_pos) {
+  if (sbd_status st = eb_common(c, batch, k, is_mask, gamma, n_accepted, accepted_pos)) return st;
+  if (!entropy) return fail(c, SBD_ERR_INVALID_ARG, "null argument");
+  if (sbd_status st = check_sticky(c)) return st;
+  if (sbd_status st = upload(c, c->ws + c->lay.eb_mask, is_mask, (size_t)batch * k)) return st;
+  EbArgs a{};
+  a.B = batch; a.k = k; a.is_mask = c->at<uint8_t>(c->lay.eb_mask); a.entropy_in = entropy;
+  a.gamma = gamma; a.n_accepted = n_accepted; a.accepted_pos = accepted_pos;
+  SBD_LAUNCH(c, SBD_KERNEL_EB_SELECT, launch_eb_select(a, true, c->stream));
+  return SBD_OK;
+}
+
+static sbd_status kv_common(sbd_ctx* c, int32_t seq, int32_t pos0, int32_t n, const void* kp, const void* vp,
+                            bool import) {
+  if (!c) return fail(nullptr, SBD_ERR_INVALID_ARG, "null context");
+  if (!seq_ok(c, seq)) return fail(c, SBD_ERR_INVALID_ARG, "seq %d out of range", seq);
+  if (!kp || !vp || n < 1 || pos0 < 0) return fail(c, SBD_ERR_INVALID_ARG, "bad pointer, n or pos0");
+  if ((int64_t)pos0 + n > c->cfg.max_seq_len)
+    return fail(c, SBD_ERR_CAPACITY, "pos0 %d + n %d exceeds max_seq_len %d", pos0, n, c->cfg.max_seq_len);
+  if (import && pos0 > c->cache_len[seq])
+    return fail(c, SBD_ERR_INVALID_ARG, "pos0 %d beyond cache_len %d", pos0, c->cache_len[seq]);
+  return check_sticky(c);
+}
+
+sbd_status sbd_kv_import(sbd_ctx* c, int32_t seq, int32_t pos0, int32_t n, const void* k, const void* v) {
+  if (sbd_status st = kv_common(c, seq, pos0, n, k, v, true)) return st;
+  KvCopyArgs a{};
+  a.kcache = c->at<bf16_t>(c->lay.kcache); a.vcache = c->at<bf16_t>(c->lay.vcache); a.cap = c->lay.cap;
+  a.n_layers = c->cfg.n_layers; a.n_slots = c->cfg.max_batch; a.n_kv = c->cfg.n_kv_heads;
+  a.d_h = c->cfg.head_dim; a.slot = seq; a.pos0 = pos0; a.n = n;
+  a.k_in = static_cast<const bf16_t*>(k); a.v_in = static_cast<const bf16_t*>(v);
+  SBD_HIP(c, launch_kv_import(a, c->stream));
+  c->cache_len[seq] = pos0 + n;
+  c->staged[seq] = 0;
+  return SBD_OK;
+}
+
+sbd_status sbd_kv_export(sbd_ctx* c, int32_t seq, int32_t pos0, int32_t n, void* k, void* v) {
+  if (sbd_status st = kv_common(c, seq, pos0, n, k, v, false)) return st;
+  KvCopyArgs a{};
+  a.kcache = c->at<bf16_t>(c->lay.kcache); a.vcache = c->at<bf16_t>(c->lay.vcache); a.cap = c->lay.cap;
+  a.n_layers = c->cfg.n_layers; a.n_slots = c->cfg.max_batch; a.n_kv = c->cfg.n_kv_heads;
+  a.d_h = c->cfg.head_dim; a.slot = seq; a.pos0 = pos0; a.n = n;
+  a.k_out = static_cast<bf16_t*>(k); a.v_out = static_cast<bf16_t*>(v);
+  SBD_HIP(c, launch_kv_export(a, c->stream));
+  return SBD_OK;
+}
+
+sbd_status sbd_profile_enable(sbd_ctx* c, int32_t enable) {
+  if (!c) return fail(nullptr, SBD_ERR_INVALID_ARG, "null context");
+  c->prof = enable != 0;
+  return SBD_OK;
+}
+
+sbd_status sbd_profile_read(sbd_ctx* c, int32_t kernel, int32_t* launches, double* total_ms) {
+  if (!c || !launches || !total_ms) return fail(c, SBD_ERR_INVALID_ARG, "null argument");
+  if (kernel < 0 || kernel >= SBD_KERNEL_COUNT) return fail(c, SBD_ERR_INVALID_ARG, "kernel %d out of range", kernel);
+  if (!c->recs.empty()) {
+    SBD_HIP(c, hipEventSynchronize(c->recs.back().b));
+    for (auto& r : c->recs) {
+      float ms = 0.f;
+      SBD_HIP(c, hipEventElapsedTime(&ms, r.a, r.b));
+      c->prof_count[r.kind] += 1;
+      c->prof_ms[r.kind] += ms;
+      c->pool.push_back(r.a);
+      c->pool.push_back(r.b);
+    }
+    c->recs.clear();
+  }
+  *launches = c->prof_count[kernel];
+  *total_ms = c->prof_ms[kernel];
+  c->prof_count[kernel] = 0;
+  c->prof_ms[kernel] = 0.0;
+  return SBD_OK;
+}
+
+const char* sbd_status_string(sbd_status s) {
+  switch (s) {
+    case SBD_OK: return "ok";
+    case SBD_ERR_INVALID_ARG: return "invalid argument";
+    case SBD_ERR_STATE: return "invalid state";
+    case SBD_ERR_CAPACITY: return "capacity exceeded";
+    case SBD_ERR_OUT_OF_MEMORY: return "workspace too small";
+    case SBD_ERR_HIP: return "HIP error";
+    case SBD_ERR_UNSUPPORTED: return "unsupported shape";
+  }
+  return "unknown status";
+}
+
+const char* sbd_last_error(const sbd_ctx* c) { return c ? c->err.c_str() : g_err.c_str(); }
+
+}  // extern "C"

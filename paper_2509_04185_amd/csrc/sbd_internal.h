@@ -1,0 +1,175 @@
+// Internal declarations shared by the host orchestration (sbd_api.cpp) and the
+// gfx950 kernels (*.hip).  Not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "sbd.h"
+
+namespace sbd {
+
+typedef uint16_t bf16_t;            // raw IEEE bfloat16 bits
+
+constexpr int kWave = 64;           // CDNA wavefront width
+constexpr int kColTile = 32;        // GEMM output columns per workgroup (two 16-wide MFMA tiles)
+constexpr int kKeyBlock = 32;       // keys per attention step / per V^T storage block
+constexpr int kMaxSplits = 64;      // split-KV partitions per (sequence, KV head, row block)
+constexpr int kEbChunk = 4096;      // vocabulary entries per EB partial workgroup
+constexpr int kMaxBlock = 64;       // largest block size k
+
+// Per-row parameters of one forward (row m = b * k + j).
+struct RowParam {
+  int32_t tok;   // token id
+  int32_t pos;   // RoPE position
+};
+
+// Per-sequence parameters of one forward.
+struct SeqParam {
+  int32_t slot;       // cache slot
+  int32_t cache_len;  // committed tokens before this forward
+  int32_t n_causal;   // rows [0, n_causal) are causal
+  int32_t pad;
+};
+
+// Where each buffer lives inside the caller's workspace (byte offsets).
+struct Layout {
+  int64_t cap;            // cache capacity per slot (max_seq_len rounded up to 64)
+  int64_t m_max;          // rows per forward (max(max_batch*max_block, prefill_chunk))
+  int64_t n_qkv;          // (n_q_heads + 2 n_kv_heads) * head_dim
+  int64_t n_part;         // d_model / 32 sum-of-squares partials per row
+  int64_t eb_chunks;      // ceil(vocab / kEbChunk)
+  size_t kcache, vcache, rope, x, xn, sumsq, qkv, q, attn, act;
+  size_t attn_ml, attn_o, rows, seqs, eb_mask, eb_part, eb_arg;
+  size_t total;
+};
+
+bool compute_layout(const sbd_model_config& c, Layout* out);
+
+// Weight pointers of one layer (device bf16).
+struct LayerW {
+  const bf16_t *attn_norm, *wq, *wk, *wv, *wo, *q_norm, *k_norm, *mlp_norm;
+  const bf16_t *w_gate, *w_up, *w_down;
+};
+
+// ---------------------------------------------------------------------------- GEMM
+enum GemmEpi { EPI_SCALED_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+
+// y[m][n] = sum_k A[m][k] * W[n][k] over the row-major [out][in] weight segments.
+struct GemmArgs {
+  const bf16_t* A;  // [M][K] bf16, row stride lda
+  int64_t lda;
+  int M, K;
+  const bf16_t* W0;  // segment 0 (or gate)
+  const bf16_t* W1;  // segment 1 (or up)
+  const bf16_t* W2;  // segment 2
+  int n0, n1;                // rows of segments 0 and 1 (segment 2 takes the rest)
+  int n_tiles;               // number of 32-column output tiles
+  // EPI_SCALED_STORE: out[m][n] = rinv[m] * y (rinv = 1 when sumsq_in == nullptr)
+  float* out_f32;
+  int64_t ldo;
+  // row RMS from per-row partial sums of squares [M][n_part] (EPI_SCALED_STORE, EPI_SWIGLU)
+  const float* sumsq_in;
+  int n_part;
+  float inv_d, eps;
+  // EPI_RESID: x[m][n] += y; xn[m][n] = bf16(x * g_next[n]); sumsq_out[m][n/32] = sum x^2
+  float* x;
+  int64_t ldx;
+  bf16_t* xn;
+  const bf16_t* g_next;
+  float* sumsq_out;
+  // EPI_SWIGLU: act[m][j] = bf16(silu(rinv*gate) * rinv*up)
+  bf16_t* act;
+  int64_t ld_act;
+};
+
+hipError_t launch_gemm(GemmEpi epi, const GemmArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------------------- misc kernels
+struct EmbedArgs {
+  const RowParam* rows;
+  int M, d;
+  const bf16_t* embed;
+  const bf16_t* g;  // first attention-norm gain
+  float* x;
+  bf16_t* xn;
+  float* sumsq;  // [M][d/32]
+};
+hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
+
+struct RopeStageArgs {
+  const RowParam* rows;
+  const SeqParam* seqs;
+  int M, k, layer;
+  int n_q, n_kv, d_h;
+  int qk_norm;
+  float eps;
+  float q_scale;  // folded into the stored queries
+  const float* qkv;  // [M][(n_q + 2 n_kv) d_h]
+  const bf16_t* q_norm;
+  const bf16_t* k_norm;
+  const float* rope;  // [cap][d_h/2][2] (cos, sin)
+  bf16_t* q;  // [M][n_q][d_h]
+  bf16_t* kcache;
+  bf16_t* vcache;
+  int64_t cap;
+  int n_slots;
+};
+hipError_t launch_rope_stage(const RopeStageArgs& a, hipStream_t s);
+
+hipError_t launch_rope_table(float* rope, int64_t cap, int d_h, double theta, hipStream_t s);
+
+struct KvCopyArgs {
+  bf16_t* kcache;
+  bf16_t* vcache;
+  int64_t cap;
+  int n_layers, n_slots, n_kv, d_h;
+  int slot, pos0, n;
+  const bf16_t* k_in;  // import source [n_layers][n][n_kv][d_h]
+  const bf16_t* v_in;
+  bf16_t* k_out;       // export destination
+  bf16_t* v_out;
+};
+hipError_t launch_kv_import(const KvCopyArgs& a, hipStream_t s);
+hipError_t launch_kv_export(const KvCopyArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------------------- attention
+struct AttnArgs {
+  const SeqParam* seqs;
+  int B, k, layer;
+  int n_q, n_kv, d_h;
+  const bf16_t* q;  // [B*k][n_q][d_h], pre-scaled by log2(e)/sqrt(d_h)
+  const bf16_t* kcache;
+  const bf16_t* vcache;
+  int64_t cap;
+  int n_slots;
+  int n_rowblocks;  // ceil(group * k / 64)
+  int n_splits;
+  int blocks_per_split;  // 32-key blocks per split
+  float* part_ml;   // [n_splits][B*k*n_q][2]
+  float* part_o;    // [n_splits][B*k*n_q][d_h]
+  bf16_t* out;  // [B*k][n_q*d_h]
+};
+hipError_t launch_attention_split(const AttnArgs& a, hipStream_t s);
+hipError_t launch_attention_merge(const AttnArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------------------- EB sampler
+struct EbArgs {
+  int B, k, vocab, mask_id;
+  const float* logits;      // [B][k][vocab]
+  const uint8_t* is_mask;   // device [B][k]
+  const double* entropy_in; // select-only mode: device [B][k]
+  double gamma;
+  int n_chunks;
+  double* part;             // [B*k][n_chunks][3] (max, Z, S)
+  int32_t* part_arg;        // [B*k][n_chunks]
+  int32_t* n_accepted;      // [B]
+  int32_t* accepted_pos;    // [B][k]
+  int32_t* accepted_tok;    // [B][k] or null
+  double* entropy_out;      // [B][k] or null
+};
+hipError_t launch_eb_partial(const EbArgs& a, hipStream_t s);
+hipError_t launch_eb_select(const EbArgs& a, bool select_only, hipStream_t s);
+
+}  // namespace sbd

@@ -1,0 +1,121 @@
+"""CPU-only checks of the C ABI: the library loads, exports what sbd.h declares, and rejects
+bad arguments on the host before touching a GPU."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import synth
+import paper_2509_04185_amd as P
+from paper_2509_04185_amd import binding as Bd
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "sbd.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(sbd_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return P.load_library()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert len(names) >= 14
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(Bd.SIGNATURES) == names
+
+
+def test_status_strings(lib):
+    for s in range(7):
+        assert lib.sbd_status_string(s)
+    assert P.status_string(3) == "capacity exceeded"
+
+
+def test_config_struct_matches_header():
+    src = open(HEADER).read()
+    m = re.search(r"typedef struct \{(.*?)\} sbd_model_config;", src, re.S)
+    fields = re.findall(r"\b([a-z_]+)\s*[,;]", re.sub(r"(int32_t|float)", "", m.group(1)))
+    assert [f for f, _ in Bd.ModelConfig._fields_] == fields
+
+
+@pytest.mark.parametrize("name", sorted(synth.WORKLOADS))
+def test_workspace_bytes_for_every_workload(name):
+    w = synth.WORKLOADS[name]
+    cfg = P.make_config(w.shape, w.batch, max(w.cache_lens()) + 64, w.k)
+    n = P.workspace_bytes(cfg)
+    s = w.shape
+    cap = (max(w.cache_lens()) + 64 + 63) // 64 * 64
+    kv = 2 * s.n_layers * w.batch * s.n_kv_heads * cap * s.head_dim * 2
+    assert kv < n < kv + 2 * 2**30
+
+
+@pytest.mark.parametrize("field,value", [("head_dim", 96), ("d_model", 200), ("vocab", 1000),
+                                         ("n_kv_heads", 3), ("max_block", 65), ("mask_id", 1024),
+                                         ("max_batch", 0), ("ffn_dim", 100), ("qk_norm", 2)])
+def test_unsupported_configs_are_rejected(field, value):
+    cfg = P.make_config(synth.TINY, 1, 128, 4)
+    setattr(cfg, field, value)
+    with pytest.raises(P.SbdError) as e:
+        P.workspace_bytes(cfg)
+    assert e.value.name == "SBD_ERR_UNSUPPORTED"
+
+
+def test_bad_eps_and_theta_rejected():
+    for field, value in (("rms_eps", 0.0), ("rms_eps", math.nan), ("rope_theta", -1.0)):
+        cfg = P.make_config(synth.TINY, 1, 128, 4)
+        setattr(cfg, field, value)
+        with pytest.raises(P.SbdError):
+            P.workspace_bytes(cfg)
+
+
+def test_create_argument_errors(lib):
+    cfg = P.make_config(synth.TINY, 1, 128, 4)
+    out = ctypes.c_void_p()
+    w = Bd.Weights()
+    st = lib.sbd_create(ctypes.byref(cfg), ctypes.byref(w), None, 0, None, ctypes.byref(out))
+    assert st == 1 and out.value is None
+    assert b"workspace" in lib.sbd_last_error(None)
+    # misaligned workspace
+    st = lib.sbd_create(ctypes.byref(cfg), ctypes.byref(w), ctypes.c_void_p(0x1001), 1 << 40, None,
+                        ctypes.byref(out))
+    assert st == 1 and b"aligned" in lib.sbd_last_error(None)
+    # too small
+    st = lib.sbd_create(ctypes.byref(cfg), ctypes.byref(w), ctypes.c_void_p(0x100000), 16, None,
+                        ctypes.byref(out))
+    assert st == 4
+    # null weights
+    st = lib.sbd_create(ctypes.byref(cfg), ctypes.byref(w), ctypes.c_void_p(0x100000), 1 << 40, None,
+                        ctypes.byref(out))
+    assert st == 1 and b"weight" in lib.sbd_last_error(None)
+
+
+def test_null_context_is_rejected(lib):
+    assert lib.sbd_eb_select(None, 1, 4, 32, None, None, 0.5, -1, None, None, None, None) == 1
+    assert lib.sbd_block_forward(None, 1, None, 4, None, None, None, None, None) == 1
+    assert lib.sbd_commit(None, 1, None, None) == 1
+    assert lib.sbd_prefill(None, 0, None, 1, None) == 1
+    assert lib.sbd_destroy(None) == 1
+    assert lib.sbd_kv_import(None, 0, 0, 1, None, None) == 1
+    n = ctypes.c_int32()
+    assert lib.sbd_cache_len(None, 0, ctypes.byref(n)) == 1
+
+
+def test_workspace_regions():
+    cfg = P.make_config(synth.TINY, 1, 128, 4)
+    total = P.workspace_bytes(cfg)
+    lib = P.load_library()
+    for name in Bd.Sbd.REGION_DTYPES:
+        off, nb = ctypes.c_size_t(), ctypes.c_size_t()
+        assert lib.sbd_workspace_region(ctypes.byref(cfg), name.encode(), ctypes.byref(off),
+                                        ctypes.byref(nb)) == 0
+        assert off.value % 256 == 0 and off.value + nb.value <= total
+    off, nb = ctypes.c_size_t(), ctypes.c_size_t()
+    assert lib.sbd_workspace_region(ctypes.byref(cfg), b"nope", ctypes.byref(off), ctypes.byref(nb)) == 1

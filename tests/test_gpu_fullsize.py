@@ -1,0 +1,135 @@
+"""GPU parity at the full 8B shapes of the four decode workloads.
+
+The GPU runs the whole batch in the launch configuration of each workload; the fp32
+oracle recomputes sampled sequences one by one (sequences are independent) from the same
+bf16 weights and the same synthetic KV cache, installed on the GPU through sbd_kv_import.
+The benchmark's own configuration (Llama-3.1-8B shape, batch 1, 2048-token prompt, k=16)
+is also checked end to end with a real prefill on both sides.
+
+Tolerance: max-abs <= 5e-2 and rel-L2 <= 1e-2 on the logits of the sampled rows; EB
+selections bit-exact on identical fp32 logits.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import sbd_oracle as O
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS, REL_L2 = 5e-2, 1e-2
+
+
+def close(got, ref, max_abs=MAX_ABS, rel_l2=REL_L2):
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    err = np.abs(got - ref).max()
+    rel = np.linalg.norm(got - ref) / np.linalg.norm(ref)
+    print(f"    max-abs {err:.3e}  rel-L2 {rel:.3e}", flush=True)
+    assert err <= max_abs and rel <= rel_l2, f"max-abs {err:.3e} rel-L2 {rel:.3e}"
+
+
+def eb_bit_exact(lib, logits_np, is_mask, gammas, mask_id):
+    for gamma in gammas:
+        acc, rtok, rH = O.eb_select(logits_np, is_mask, gamma, mask_id)
+        n_acc, pos, tok, H = lib.eb_select(torch.from_numpy(logits_np).cuda(), is_mask, gamma, mask_id)
+        for b in range(logits_np.shape[0]):
+            n = int(n_acc[b])
+            assert pos[b, :n].tolist() == acc[b], (b, gamma)
+            assert tok[b, :n].tolist() == rtok[b], (b, gamma)
+        m = is_mask.astype(bool)
+        np.testing.assert_allclose(H.cpu().numpy()[m], rH[m], rtol=1e-12)
+
+
+def make_ctx(wl, import_cache=True):
+    from paper_2509_04185_amd import Sbd
+    torch.cuda.empty_cache()
+    s = wl.shape
+    w = synth.make_weights(s, wl.seed, device="cuda")
+    lens = wl.cache_lens()
+    lib = Sbd(s, w, max_batch=wl.batch, max_seq_len=max(lens) + wl.k + 64, max_block=wl.k)
+    if import_cache:
+        for b, L in enumerate(lens):
+            kk, vv = synth.make_kv(s, wl.seed, b, L, device="cuda")
+            lib.kv_import(b, 0, kk, vv)
+            del kk, vv
+    return w, lib, lens
+
+
+SAMPLES = {"llama8b_b1_l2048_k16": [0], "llama8b_b32_ragged_k8": "minmax",
+           "llama8b_b4_l32768_k16": [3], "qwen8b_b8_l8192_k16": [5]}
+
+
+@pytest.mark.parametrize("name", list(SAMPLES))
+def test_fullsize_block_forward(name):
+    wl = synth.WORKLOADS[name]
+    s = wl.shape
+    print(f"[gpu] {name}: B={wl.batch} k={wl.k}", flush=True)
+    w, lib, lens = make_ctx(wl)
+    sample = SAMPLES[name]
+    if sample == "minmax":
+        sample = [int(np.argmin(lens)), int(np.argmax(lens))]
+    toks, is_mask = synth.block_rows(wl.seed, s, wl.batch, wl.k, n_causal=1)
+    logits = lib.block_forward(list(range(wl.batch)), toks, is_mask=is_mask)
+    n_acc, _, _, _ = lib.eb_select(logits, is_mask, wl.gammas[0], s.mask_id)
+    torch.cuda.synchronize()
+    assert (n_acc >= 1).all()
+    got = logits[sample].cpu().numpy()
+    del logits
+    host = synth.weights_to_host(w)
+    model = O.Model(s, host, dtype=np.float32, cache_decoded=False)
+    caches = []
+    for b in sample:
+        kk, vv = synth.make_kv(s, wl.seed, b, lens[b], device="cuda")
+        caches.append(O.SeqCache.from_arrays(synth.to_host_bits(kk), synth.to_host_bits(vv), np.float32))
+        del kk, vv
+    print(f"    oracle on sequences {sample} (cache {[lens[b] for b in sample]})", flush=True)
+    ref = model.block_forward(caches, toks[sample], [1] * len(sample)).logits
+    close(got, ref)
+    eb_bit_exact(lib, ref.astype(np.float32), is_mask[sample], wl.gammas, s.mask_id)
+
+
+@pytest.mark.parametrize("name", list(SAMPLES))
+def test_fullsize_eb_ladder(name):
+    """EB at each workload's (batch, k, vocab) on logits that spread the entropies."""
+    wl = synth.WORKLOADS[name]
+    s = wl.shape
+    from paper_2509_04185_amd import Sbd
+    import dataclasses
+    one = dataclasses.replace(s, n_layers=1)
+    torch.cuda.empty_cache()
+    w = synth.make_weights(one, wl.seed, device="cuda")
+    lib = Sbd(one, w, max_batch=wl.batch, max_seq_len=64, max_block=wl.k)
+    logits = synth.entropy_ladder_logits(wl.seed, wl.batch, wl.k, s.vocab).numpy()
+    _, is_mask = synth.block_rows(wl.seed, s, wl.batch, wl.k, n_causal=1)
+    eb_bit_exact(lib, logits, is_mask, sorted(set(wl.gammas) | {0.0, 1.0, 4.0, math.inf}), s.mask_id)
+
+
+def test_benched_configuration_with_real_prefill():
+    """Llama-3.1-8B shape, batch 1, 2048-token prompt prefilled on both sides, k = 16."""
+    wl = synth.WORKLOADS["llama8b_b1_l2048_k16"]
+    s = wl.shape
+    print("[gpu] benched configuration: prefill 2048 + block forward", flush=True)
+    w, lib, lens = make_ctx(wl, import_cache=False)
+    prompt = synth.make_tokens(wl.seed, lens[0], s, stream=100)
+    last = lib.prefill(0, prompt)
+    toks, is_mask = synth.block_rows(wl.seed, s, 1, wl.k, n_causal=1)
+    logits = lib.block_forward([0], toks, is_mask=is_mask)
+    k_gpu, v_gpu = lib.kv_export(0, 0, lens[0])
+    torch.cuda.synchronize()
+    got, got_last = logits.cpu().numpy(), last.cpu().numpy()
+    kl = k_gpu[-1].float().cpu().numpy()
+    vl = v_gpu[-1].float().cpu().numpy()
+    del k_gpu, v_gpu, logits
+    model = O.Model(s, synth.weights_to_host(w), dtype=np.float32, cache_decoded=False)
+    print("    oracle prefill of 2048 tokens", flush=True)
+    cache, ref_last = model.prefill(prompt)
+    close(got_last, ref_last)
+    # bf16 cache entries of magnitude up to ~8: allow a few bf16 ulps at the extremes
+    close(kl, cache.K[-1], max_abs=0.15)
+    close(vl, cache.V[-1], max_abs=0.15)
+    ref = model.block_forward([cache], toks, [1]).logits
+    close(got, ref)

@@ -1,0 +1,352 @@
+"""GPU parity of the HIP path against the CPU oracle on the tiny decoder (and its qk-norm
+variant), plus the SBD invariants and the ABI's state machine on the device.
+
+Tolerance for logits (bf16 weights/activations on the GPU vs the float64 oracle on the
+same bf16 weights): max-abs <= 5e-2 and rel-L2 <= 1e-2 over the whole logits tensor.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import sbd_oracle as O
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS, REL_L2 = 5e-2, 1e-2
+
+
+def close(got, ref, max_abs=MAX_ABS, rel_l2=REL_L2):
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    err = np.abs(got - ref).max()
+    rel = np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-30)
+    assert err <= max_abs and rel <= rel_l2, f"max-abs {err:.3e} rel-L2 {rel:.3e}"
+    return err, rel
+
+
+def to_dev(w, dev):
+    return {k: (v.to(dev) if k != "layers" else [{kk: vv.to(dev) for kk, vv in lw.items()}
+                                                 for lw in v]) for k, v in w.items()}
+
+
+class Tiny:
+    def __init__(self, shape, seed, max_batch=4, max_seq_len=256, max_block=16, chunk=0):
+        from paper_2509_04185_amd import Sbd
+        print(f"[gpu] building {shape.name} seed={seed} batch={max_batch}", flush=True)
+        self.shape = shape
+        self.w_cpu = synth.make_weights(shape, seed)
+        self.lib = Sbd(shape, to_dev(self.w_cpu, "cuda"), max_batch=max_batch,
+                       max_seq_len=max_seq_len, max_block=max_block, prefill_chunk=chunk)
+        self.model = O.Model(shape, synth.weights_to_host(self.w_cpu), dtype=np.float64)
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    return Tiny(synth.TINY, 1001)
+
+
+@pytest.fixture(scope="module")
+def tiny_qk():
+    return Tiny(synth.TINY_QK, 2002, chunk=24)
+
+
+def fresh(t, seqs=(0, 1, 2, 3)):
+    for s in seqs:
+        t.lib.reset(s)
+
+
+# ------------------------------------------------------------------ the tiny workload
+
+
+def test_tiny_workload_block_forward(tiny):
+    """Batch 1, 64-token prompt in the cache, k = 4 (1 real + 3 masks)."""
+    wl = synth.WORKLOADS["tiny_b1_l64_k4"]
+    fresh(tiny)
+    prompt = synth.make_tokens(wl.seed, 64, tiny.shape)
+    last = tiny.lib.prefill(0, prompt)
+    toks, is_mask = synth.block_rows(wl.seed, tiny.shape, 1, 4, n_causal=1)
+    logits = tiny.lib.block_forward([0], toks, is_mask=is_mask)
+    torch.cuda.synchronize()
+    cache, ref_last = tiny.model.prefill(prompt)
+    ref = tiny.model.block_forward([cache], toks, [1]).logits
+    close(last.cpu().numpy(), ref_last)
+    close(logits.cpu().numpy(), ref)
+    assert tiny.lib.cache_len(0) == 64
+
+
+@pytest.mark.parametrize("gamma", [0.0, 0.5, math.inf])
+def test_tiny_workload_eb_select_bit_exact(tiny, gamma):
+    """EB on the oracle's own fp32 logits (x4): identical accepted set and tokens."""
+    wl = synth.WORKLOADS["tiny_b1_l64_k4"]
+    prompt = synth.make_tokens(wl.seed, 64, tiny.shape)
+    cache, _ = tiny.model.prefill(prompt)
+    toks, is_mask = synth.block_rows(wl.seed, tiny.shape, 1, 4, n_causal=1)
+    ref_logits = (tiny.model.block_forward([cache], toks, [1]).logits * wl.logit_scale).astype(np.float32)
+    acc, rtok, rH = O.eb_select(ref_logits, is_mask, gamma, tiny.shape.mask_id)
+    n_acc, pos, tok, H = tiny.lib.eb_select(torch.from_numpy(ref_logits).cuda(), is_mask, gamma,
+                                            tiny.shape.mask_id)
+    n = int(n_acc[0])
+    assert n == len(acc[0])
+    assert pos[0, :n].tolist() == acc[0] and tok[0, :n].tolist() == rtok[0]
+    assert (pos[0, n:] == -1).all()
+    Hg = H.cpu().numpy()
+    for j in range(4):
+        if is_mask[0, j]:
+            assert abs(Hg[0, j] - rH[0, j]) <= 1e-12 * max(1.0, abs(rH[0, j]))
+        else:
+            assert math.isnan(Hg[0, j])
+
+
+# ------------------------------------------------------------------ EB on ladder logits
+
+
+@pytest.fixture(scope="module")
+def wide():
+    """A context whose vocabulary and block size cover the EB cases (one layer suffices)."""
+    import dataclasses
+    shape = dataclasses.replace(synth.TINY, name="tiny_v16k", vocab=16384, mask_id=16383, n_layers=1)
+    return Tiny(shape, 3003, max_batch=4, max_seq_len=64, max_block=64)
+
+
+@pytest.mark.parametrize("B,k,V,mask_id", [(1, 16, 1024, 1023), (3, 8, 4096, 0), (2, 5, 5000, -1),
+                                           (4, 16, 12000, 11999), (1, 64, 2048, 7),
+                                           (2, 64, 16384, 16383), (3, 9, 4097, 4096)])
+def test_eb_select_ladder_bit_exact(wide, B, k, V, mask_id):
+    """EB on entropy-ladder logits: identical accepted sets and tokens at every gamma."""
+    logits = synth.entropy_ladder_logits(B * 100 + k, B, k, V)
+    rng = np.random.default_rng(B * 7 + k)
+    is_mask = (rng.random((B, k)) < 0.8).astype(np.uint8)
+    is_mask[:, 0] = 0
+    if k > 1:
+        is_mask[:, 1] = 1
+    for gamma in (0.0, 0.1, 1.0, 4.0, math.inf):
+        acc, rtok, rH = O.eb_select(logits.numpy(), is_mask, gamma, mask_id)
+        n_acc, pos, tok, H = wide.lib.eb_select(logits.cuda(), is_mask, gamma, mask_id)
+        for b in range(B):
+            n = int(n_acc[b])
+            assert pos[b, :n].tolist() == acc[b], (b, gamma)
+            assert tok[b, :n].tolist() == rtok[b], (b, gamma)
+            assert (pos[b, n:] == -1).all()
+        Hg = H.cpu().numpy()
+        m = is_mask.astype(bool)
+        np.testing.assert_allclose(Hg[m], rH[m], rtol=1e-12, atol=1e-13)
+
+
+def test_eb_select_entropies_hand_cases(tiny):
+    H = torch.tensor([[0.0, 0.25, 0.125, 0.375, 0.125]], dtype=torch.float64, device="cuda")
+    is_mask = np.array([[0, 1, 1, 1, 1]], np.uint8)
+    for gamma, want in ((0.0, [2]), (0.125, [2, 4]), (0.25, [1, 2, 4]), (0.4999, [1, 2, 4]),
+                        (0.5, [1, 2, 3, 4]), (math.inf, [1, 2, 3, 4])):
+        n, pos = tiny.lib.eb_select_entropies(H, is_mask, gamma)
+        assert pos[0, :int(n[0])].tolist() == want
+    n, pos = tiny.lib.eb_select_entropies(H, np.zeros((1, 5), np.uint8), 1.0)
+    assert int(n[0]) == 0 and (pos == -1).all()
+
+
+# ------------------------------------------------------------------ SBD invariants on the GPU
+
+
+def test_k1_is_next_token_prediction(tiny):
+    fresh(tiny)
+    prompt = synth.make_tokens(5, 40, tiny.shape)
+    tiny.lib.prefill(0, prompt[:-1], want_logits=False)
+    got = tiny.lib.block_forward([0], prompt[-1:].reshape(1, 1))
+    tiny.lib.prefill(1, prompt)
+    last = tiny.lib.prefill(2, prompt)
+    torch.cuda.synchronize()
+    ntp = tiny.model.full_forward(prompt, causal_point=len(prompt))[-1]
+    close(got[0, 0].cpu().numpy(), ntp)
+    close(last.cpu().numpy(), ntp)
+
+
+def test_row0_independent_of_prediction_rows(tiny):
+    fresh(tiny)
+    tiny.lib.prefill(0, synth.make_tokens(6, 30, tiny.shape), want_logits=False)
+    toks, _ = synth.block_rows(7, tiny.shape, 1, 6, n_causal=1)
+    a = tiny.lib.block_forward([0], toks).clone()
+    toks2 = toks.copy()
+    toks2[0, 3] = 11
+    b = tiny.lib.block_forward([0], toks2)
+    torch.cuda.synchronize()
+    assert torch.equal(a[0, 0], b[0, 0])
+    assert (a[0, 1] - b[0, 1]).abs().max() > 1e-4
+
+
+def test_prediction_rows_permutation_equivariant(tiny_qk):
+    t = tiny_qk
+    fresh(t)
+    t.lib.prefill(0, synth.make_tokens(8, 33, t.shape), want_logits=False)
+    L = t.lib.cache_len(0)
+    toks = np.array([[3, 77, t.shape.mask_id, 500, t.shape.mask_id, 9]], np.int32)
+    pos = np.array([[L + j for j in range(6)]], np.int32)
+    perm = [0, 4, 1, 5, 3, 2]
+    a = t.lib.block_forward([0], toks, pos_ids=pos).clone()
+    b = t.lib.block_forward([0], toks[:, perm], pos_ids=pos[:, perm])
+    torch.cuda.synchronize()
+    close(b[0].cpu().numpy(), a[0, perm].cpu().numpy(), max_abs=1e-2, rel_l2=1e-3)
+
+
+def test_cached_block_equals_full_recompute(tiny_qk):
+    t = tiny_qk
+    fresh(t)
+    prompt = synth.make_tokens(9, 50, t.shape)      # prefill chunk 24: three chunks
+    t.lib.prefill(0, prompt, want_logits=False)
+    toks, _ = synth.block_rows(10, t.shape, 1, 8, n_causal=2)
+    got = t.lib.block_forward([0], toks, n_causal=[2])
+    torch.cuda.synchronize()
+    full = t.model.full_forward(np.concatenate([prompt, toks[0]]), causal_point=len(prompt) + 2)
+    close(got[0].cpu().numpy(), full[len(prompt):])
+
+
+def test_commit_is_exact(tiny_qk):
+    t = tiny_qk
+    fresh(t)
+    prompt = synth.make_tokens(11, 20, t.shape)
+    nxt = synth.make_tokens(12, 3, t.shape)
+    t.lib.prefill(0, np.concatenate([prompt, nxt]), want_logits=False)
+    t.lib.prefill(1, prompt, want_logits=False)
+    toks = np.array([[nxt[0], nxt[1], nxt[2], t.shape.mask_id, t.shape.mask_id]], np.int32)
+    t.lib.block_forward([1], toks, n_causal=[3])
+    t.lib.commit([1], [3])
+    assert t.lib.cache_len(1) == 23
+    k0, v0 = t.lib.kv_export(0, 0, 23)
+    k1, v1 = t.lib.kv_export(1, 0, 23)
+    torch.cuda.synchronize()
+    # Layer 0 depends only on the token and position: bit-identical.  Later layers went
+    # through attention splits of different shapes, so allow bf16 rounding differences.
+    assert torch.equal(k0[0], k1[0]) and torch.equal(v0[0], v1[0])
+    close(k1.float().cpu().numpy(), k0.float().cpu().numpy(), max_abs=5e-2, rel_l2=1e-2)
+    close(v1.float().cpu().numpy(), v0.float().cpu().numpy(), max_abs=5e-2, rel_l2=1e-2)
+    # and the cache matches the oracle's exact cache
+    c, _ = t.model.prefill(np.concatenate([prompt, nxt]))
+    for li in range(t.shape.n_layers):
+        close(k0[li].float().cpu().numpy(), c.K[li], max_abs=5e-2, rel_l2=1e-2)
+        close(v0[li].float().cpu().numpy(), c.V[li], max_abs=5e-2, rel_l2=1e-2)
+
+
+def test_kv_import_roundtrip_and_parity(tiny):
+    fresh(tiny)
+    s = tiny.shape
+    k, v = synth.make_kv(s, 13, 0, 70, device="cuda")
+    tiny.lib.kv_import(0, 0, k, v)
+    assert tiny.lib.cache_len(0) == 70
+    k2, v2 = tiny.lib.kv_export(0, 0, 70)
+    torch.cuda.synchronize()
+    assert torch.equal(k, k2) and torch.equal(v, v2)
+    toks, is_mask = synth.block_rows(14, s, 1, 4, n_causal=1)
+    got = tiny.lib.block_forward([0], toks, is_mask=is_mask)
+    torch.cuda.synchronize()
+    cache = O.SeqCache.from_arrays(synth.to_host_bits(k), synth.to_host_bits(v), np.float64)
+    ref = tiny.model.block_forward([cache], toks, [1]).logits
+    close(got.cpu().numpy(), ref)
+
+
+def test_ragged_batch_matches_single_sequences(tiny):
+    fresh(tiny)
+    s = tiny.shape
+    lens = [5, 37, 64, 100]
+    prompts = [synth.make_tokens(20 + i, n, s) for i, n in enumerate(lens)]
+    for i, p in enumerate(prompts):
+        tiny.lib.prefill(i, p, want_logits=False)
+    toks, _ = synth.block_rows(30, s, 4, 8, n_causal=2)
+    nc = np.array([1, 2, 0, 1], np.int32)
+    toks[[0, 3], 1] = s.mask_id            # one causal row, then masks
+    toks[2, 0] = s.mask_id                 # no causal row; row 1 is an unmasked block row
+    is_mask = (toks == s.mask_id).astype(np.uint8)
+    both = tiny.lib.block_forward([3, 1, 0, 2], toks[[3, 1, 0, 2]], is_mask=is_mask[[3, 1, 0, 2]],
+                                  n_causal=nc[[3, 1, 0, 2]]).cpu().numpy()
+    caches = [tiny.model.prefill(p)[0] for p in prompts]
+    ref = tiny.model.block_forward(caches, toks, nc).logits
+    close(both, ref[[3, 1, 0, 2]])
+
+
+def test_qk_norm_model_block_forward(tiny_qk):
+    t = tiny_qk
+    fresh(t)
+    prompt = synth.make_tokens(40, 77, t.shape)
+    last = t.lib.prefill(0, prompt)
+    toks, is_mask = synth.block_rows(41, t.shape, 1, 16, n_causal=1)
+    got = t.lib.block_forward([0], toks, is_mask=is_mask)
+    torch.cuda.synchronize()
+    cache, ref_last = t.model.prefill(prompt)
+    close(last.cpu().numpy(), ref_last)
+    close(got.cpu().numpy(), t.model.block_forward([cache], toks, [1]).logits)
+
+
+def test_intermediate_buffers_last_layer(tiny):
+    """The rotated queries and attention output of the last layer against the oracle's steps."""
+    fresh(tiny)
+    s = tiny.shape
+    prompt = synth.make_tokens(50, 31, s)
+    tiny.lib.prefill(0, prompt, want_logits=False)
+    toks, _ = synth.block_rows(51, s, 1, 4, n_causal=1)
+    tiny.lib.block_forward([0], toks)
+    torch.cuda.synchronize()
+    m = tiny.model
+    cache, _ = m.prefill(prompt)
+    # replay the oracle's forward up to the last layer's attention
+    x = m.W("embed")[toks[0]]
+    L = cache.length
+    li_last = s.n_layers - 1
+    for li in range(s.n_layers):
+        h = O.rms_norm(x, m.W("attn_norm", li), s.rms_eps)
+        q, kk, vv = m._qkv(h, li, [L + j for j in range(4)])
+        Kall = np.concatenate([cache.K[li], kk])
+        Vall = np.concatenate([cache.V[li], vv])
+        o = O.attention(q, Kall, Vall, O.inference_mask(L, 4, 1))
+        if li == li_last:
+            break
+        x = x + o.reshape(4, -1) @ m.W("wo", li).T
+        x = x + m._mlp(x, li)
+    qd = s.n_q_heads * s.head_dim
+    scale = math.log2(math.e) / math.sqrt(s.head_dim)
+    gq = tiny.lib.region("q")[: 4 * qd].float().cpu().numpy().reshape(4, s.n_q_heads, s.head_dim)
+    close(gq / scale, q, max_abs=3e-2, rel_l2=1e-2)
+    ga = tiny.lib.region("attn")[: 4 * qd].float().cpu().numpy().reshape(4, s.n_q_heads, s.head_dim)
+    close(ga, o, max_abs=3e-2, rel_l2=1e-2)
+
+
+# ------------------------------------------------------------------ state machine and errors
+
+
+def test_state_and_argument_errors(tiny):
+    from paper_2509_04185_amd import SbdError
+    fresh(tiny)
+    s = tiny.shape
+    lib = tiny.lib
+    lib.prefill(0, synth.make_tokens(60, 10, s), want_logits=False)
+    toks, is_mask = synth.block_rows(61, s, 1, 4, n_causal=1)
+
+    def err(fn, name):
+        with pytest.raises(SbdError) as e:
+            fn()
+        assert e.value.name == name, str(e.value)
+
+    err(lambda: lib.commit([0], [1]), "SBD_ERR_STATE")                    # nothing staged
+    lib.block_forward([0], toks)
+    err(lambda: lib.commit([0], [2]), "SBD_ERR_STATE")                    # only 1 causal row
+    lib.commit([0], [1])
+    err(lambda: lib.commit([0], [1]), "SBD_ERR_STATE")                    # already committed
+    assert lib.cache_len(0) == 11
+    bad = is_mask.copy()
+    bad[0, 1] = 0
+    err(lambda: lib.block_forward([0], toks, is_mask=bad), "SBD_ERR_INVALID_ARG")
+    err(lambda: lib.block_forward([0], np.full((1, 4), s.mask_id, np.int32)), "SBD_ERR_INVALID_ARG")
+    err(lambda: lib.block_forward([0, 0], np.vstack([toks, toks])), "SBD_ERR_INVALID_ARG")
+    err(lambda: lib.block_forward([9], toks), "SBD_ERR_INVALID_ARG")
+    err(lambda: lib.block_forward([0], toks, pos_ids=[[0, 12, 13, 14]]), "SBD_ERR_INVALID_ARG")
+    err(lambda: lib.prefill(1, synth.make_tokens(62, 300, s)), "SBD_ERR_CAPACITY")
+    logits = torch.zeros((1, 4, s.vocab), device="cuda")
+    err(lambda: lib.eb_select(logits, is_mask, float("nan"), s.mask_id), "SBD_ERR_INVALID_ARG")
+    err(lambda: lib.eb_select(logits, is_mask, -0.1, s.mask_id), "SBD_ERR_INVALID_ARG")
+    err(lambda: lib.eb_select(torch.zeros((1, 4, 2048), device="cuda"), is_mask, 1.0, -1),
+        "SBD_ERR_INVALID_ARG")
+    # a failed call changes nothing
+    assert lib.cache_len(0) == 11
+    lib.block_forward([0], toks, n_causal=[1])
+    lib.commit([0], [1])
+    assert lib.cache_len(0) == 12
