@@ -182,9 +182,11 @@ sbd_status sbd_kv_export(sbd_ctx* ctx, int32_t seq, int32_t pos0, int32_t n, voi
 /*
  * Byte offset and size inside the workspace of a named internal buffer, for
  * inspection by tests: "x" (fp32 residual [rows][d_model]), "qkv" (fp32 projections),
- * "q" (bf16 rotated queries), "attn" (bf16 attention output), "act" (bf16 SwiGLU output),
- * "xn" (bf16 gain-scaled residual).  Values are those of the last layer of the last
- * forward.  INVALID_ARG for an unknown name.
+ * "q" (rotated, scaled queries), "attn" (attention output), "act" (SwiGLU output), "xn"
+ * (gain-scaled residual).  The last four hold bf16 pairs: [2][rows][width], the value
+ * being hi + lo.  rows is the workspace's row capacity, max(max_batch * max_block,
+ * prefill chunk).  Values are those of the last layer of the last forward.  INVALID_ARG
+ * for an unknown name.
  */
 sbd_status sbd_workspace_region(const sbd_model_config* cfg, const char* name, size_t* offset,
                                 size_t* bytes);

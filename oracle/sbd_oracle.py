@@ -34,7 +34,8 @@ Readings where the paper is silent (each is listed with its reason in the design
 * gamma may be 0 (used in Sec. 3.2) or +inf.
 
 Precision: everything runs in the dtype given to ``Model`` (float64 by default);
-EB statistics are always float64.
+EB statistics are always float64.  With ``kv_bf16`` the keys and values are held in
+bfloat16, the storage format of the KV cache; activations stay in the working dtype.
 """
 from __future__ import annotations
 
@@ -54,6 +55,18 @@ def decode_weight(a, dtype=np.float64) -> np.ndarray:
         np.left_shift(a, 16, out=bits, dtype=np.uint32)
         a = bits.view(np.float32)
     return a.astype(dtype, copy=False)
+
+
+def round_to_bf16(a: np.ndarray) -> np.ndarray:
+    """Round to the nearest bfloat16 value (8 significant bits, ties to even), same dtype out.
+
+    Written with frexp/ldexp: a = m * 2^e with 0.5 <= |m| < 1, so m * 2^8 holds the 8
+    kept bits before the point; rint rounds half to even.  Values are assumed to be in
+    the normal range of bfloat16 (the exponent range of float32).
+    """
+    a = np.asarray(a)
+    m, e = np.frexp(a.astype(np.float64))
+    return np.ldexp(np.rint(np.ldexp(m, 8)), e - 8).astype(a.dtype)
 
 
 def rms_norm(x: np.ndarray, g: np.ndarray, eps: float) -> np.ndarray:
@@ -170,11 +183,16 @@ class Model:
     q_norm, k_norm, mlp_norm, w_gate, w_up, w_down); matrices are [out][in].
     """
 
-    def __init__(self, shape, weights: dict, dtype=np.float64, cache_decoded: bool = True):
+    def __init__(self, shape, weights: dict, dtype=np.float64, cache_decoded: bool = True,
+                 kv_bf16: bool = False):
+        """kv_bf16: keys/values are stored in bfloat16 (the KV-cache storage format of the
+        GPU path): every K/V row is rounded to bf16 when it is produced, before it is used
+        by attention or appended to the cache."""
         self.s = shape
         self.w = weights
         self.dtype = np.dtype(dtype)
         self._memo = {} if cache_decoded else None
+        self.kv_bf16 = kv_bf16
 
     def W(self, name: str, layer: Optional[int] = None) -> np.ndarray:
         key = (name, layer)
@@ -201,7 +219,10 @@ class Model:
             q = rms_norm(q, self.W("q_norm", li), s.rms_eps)
             k = rms_norm(k, self.W("k_norm", li), s.rms_eps)
         cos, sin = rope_cos_sin(pos, s.head_dim, s.rope_theta, self.dtype)
-        return apply_rope(q, cos, sin), apply_rope(k, cos, sin), v
+        q, k = apply_rope(q, cos, sin), apply_rope(k, cos, sin)
+        if self.kv_bf16:
+            k, v = round_to_bf16(k), round_to_bf16(v)
+        return q, k, v
 
     def _mlp(self, x, li):
         s = self.s

@@ -8,10 +8,11 @@
 // Work split: one workgroup per (split, KV head x row block, sequence).  The rows of a
 // KV head are the group*k (query head, block row) pairs that read it; each wave takes 16
 // of them (one MFMA tile) and walks the keys of its split in 32-key steps:
-//   S^T = K Q^T   (v_mfma_f32_16x16x32_bf16: keys on M, query rows on N, d_h in 4 steps)
+//   S^T = K Q^T   (v_mfma_f32_16x16x32_bf16: keys on M, query rows on N, d_h in 4 steps;
+//                  Q as hi + lo bf16, two MFMAs per step)
 //   online softmax per query row in base 2 (queries carry log2(e)/sqrt(d_h))
-//   O^T += V^T P^T (d_h/16 MFMAs; P arrives in the B-operand layout straight from the
-//                   score tile, V^T comes from the transposed, permuted cache blocks)
+//   O^T += V^T P^T (P as hi + lo bf16 in the B-operand layout straight from the score
+//                   tile; V^T comes from the transposed, permuted cache blocks)
 // Each split leaves unnormalised (max, sum, O) per row; a merge kernel combines the
 // splits with log-sum-exp weights in split order.
 
@@ -54,12 +55,14 @@ __global__ __launch_bounds__(256) void attn_split_kernel(AttnArgs a) {
   const int blk0 = split * a.blocks_per_split;
   const int blk1 = min(blk0 + a.blocks_per_split, nblk_w);
 
-  // Query fragments (B operand): row r, dims 32*s + 8*grp .. +8.
-  i32x4 qf[NKS];
-  const bf16_t* qrow = a.q + ((int64_t)(b * k + j) * a.n_q + hq) * DH;
+  // Query fragments (B operand, hi and lo): row r, dims 32*s + 8*grp .. +8.
+  i32x4 qf[NKS], ql[NKS];
+  const int64_t qoff = ((int64_t)(b * k + j) * a.n_q + hq) * DH;
 #pragma unroll
-  for (int s = 0; s < NKS; ++s)
-    qf[s] = row_ok ? ld16(qrow + 32 * s + 8 * grp) : i32x4{0, 0, 0, 0};
+  for (int s = 0; s < NKS; ++s) {
+    qf[s] = row_ok ? ld16(a.q + qoff + 32 * s + 8 * grp) : i32x4{0, 0, 0, 0};
+    ql[s] = row_ok ? ld16(a.q_lo + qoff + 32 * s + 8 * grp) : i32x4{0, 0, 0, 0};
+  }
 
   const int64_t hb = attn_head_base(a.layer, sp.slot, g, a.n_slots, a.n_kv, a.cap, DH);
   const bf16_t* kbase = a.kcache + hb;
@@ -78,7 +81,11 @@ __global__ __launch_bounds__(256) void attn_split_kernel(AttnArgs a) {
       st[t] = f32x4{0.f, 0.f, 0.f, 0.f};
       const bf16_t* kp = kbase + (int64_t)(key0 + 16 * t + r) * DH + 8 * grp;
 #pragma unroll
-      for (int s = 0; s < NKS; ++s) st[t] = mfma16x16x32(ld16(kp + 32 * s), qf[s], st[t]);
+      for (int s = 0; s < NKS; ++s) {
+        const i32x4 kf = ld16(kp + 32 * s);
+        st[t] = mfma16x16x32(kf, qf[s], st[t]);
+        st[t] = mfma16x16x32(kf, ql[s], st[t]);
+      }
     }
     // st[t][i]: score of key key0 + 16t + 4grp + i for query row r.
     float mloc = -INFINITY;
@@ -110,15 +117,23 @@ __global__ __launch_bounds__(256) void attn_split_kernel(AttnArgs a) {
     m_run = m_new;
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) o[dt] *= scale;
-    i32x4 pf;
-    pf[0] = (int)pack_bf2(p[0], p[1]);
-    pf[1] = (int)pack_bf2(p[2], p[3]);
-    pf[2] = (int)pack_bf2(p[4], p[5]);
-    pf[3] = (int)pack_bf2(p[6], p[7]);
+    // P as hi/lo bf16 (B operand): element e holds key 16*(e/4) + 4*grp + e%4.
+    i32x4 pf, pl;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      bf16_t h0, l0, h1, l1;
+      split_bf16(p[2 * e], h0, l0);
+      split_bf16(p[2 * e + 1], h1, l1);
+      pf[e] = (int)((uint32_t)h0 | ((uint32_t)h1 << 16));
+      pl[e] = (int)((uint32_t)l0 | ((uint32_t)l1 << 16));
+    }
     const bf16_t* vb = vbase + (int64_t)kb * DH * 32 + 8 * grp;
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt)
-      o[dt] = mfma16x16x32(ld16(vb + (int64_t)(16 * dt + r) * 32), pf, o[dt]);
+    for (int dt = 0; dt < NDT; ++dt) {
+      const i32x4 vf = ld16(vb + (int64_t)(16 * dt + r) * 32);
+      o[dt] = mfma16x16x32(vf, pf, o[dt]);
+      o[dt] = mfma16x16x32(vf, pl, o[dt]);
+    }
   }
 
   if (!row_ok) return;
@@ -134,35 +149,61 @@ __global__ __launch_bounds__(256) void attn_split_kernel(AttnArgs a) {
   for (int dt = 0; dt < NDT; ++dt) *(f32x4*)(po + 16 * dt + 4 * grp) = o[dt];
 }
 
-// One wave per (row, query head): combine the splits, normalise, store bf16.
+// One wave per (row, query head): combine the splits, normalise, store hi/lo bf16.
+// Lane s reads split s's (max, sum); the split weights 2^(m_s - M) are broadcast from
+// their lanes while every lane accumulates its own dimensions over the splits.
 template <int DH>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   const int64_t n_items = (int64_t)a.B * a.k * a.n_q;
   const int64_t item = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (item >= n_items) return;
   const int lane = threadIdx.x & 63;
-  float mx = -INFINITY;
-  for (int s = 0; s < a.n_splits; ++s) mx = fmaxf(mx, a.part_ml[((int64_t)s * n_items + item) * 2]);
+  const int ns = a.n_splits;  // <= 64
+  float ms = -INFINITY, ls = 0.f;
+  if (lane < ns) {
+    const float2 v = *(const float2*)(a.part_ml + ((int64_t)lane * n_items + item) * 2);
+    ms = v.x;
+    ls = v.y;
+  }
+  const float mx = wave_max(ms);
+  const float wgt = (ms == -INFINITY) ? 0.f : exp2f(ms - mx);
+  const float lsum = wave_sum(wgt * ls);
   constexpr int PER = DH / 64;
   float acc[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) acc[e] = 0.f;
-  float lsum = 0.f;
-  for (int s = 0; s < a.n_splits; ++s) {
-    const float ms = a.part_ml[((int64_t)s * n_items + item) * 2];
-    if (ms == -INFINITY) continue;
-    const float wgt = exp2f(ms - mx);
-    lsum += wgt * a.part_ml[((int64_t)s * n_items + item) * 2 + 1];
-    const float* po = a.part_o + ((int64_t)s * n_items + item) * DH;
+  const float* po = a.part_o + item * DH + lane;
+  const int64_t split_stride = n_items * DH;
+  int s = 0;
+  for (; s + 4 <= ns; s += 4) {
+    float v[4][PER];
 #pragma unroll
-    for (int e = 0; e < PER; ++e) acc[e] += wgt * po[lane + 64 * e];
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int e = 0; e < PER; ++e) v[u][e] = po[(int64_t)(s + u) * split_stride + 64 * e];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float wu = __shfl(wgt, s + u);
+#pragma unroll
+      for (int e = 0; e < PER; ++e) acc[e] += wu * v[u][e];
+    }
+  }
+  for (; s < ns; ++s) {
+    const float wu = __shfl(wgt, s);
+#pragma unroll
+    for (int e = 0; e < PER; ++e) acc[e] += wu * po[(int64_t)s * split_stride + 64 * e];
   }
   const float inv = 1.0f / lsum;
   const int64_t orow = item / a.n_q;
   const int hq = (int)(item % a.n_q);
-  bf16_t* dst = a.out + orow * (int64_t)a.n_q * DH + (int64_t)hq * DH;
+  const int64_t dst = orow * (int64_t)a.n_q * DH + (int64_t)hq * DH;
 #pragma unroll
-  for (int e = 0; e < PER; ++e) dst[lane + 64 * e] = f2bf(acc[e] * inv);
+  for (int e = 0; e < PER; ++e) {
+    bf16_t hi, lo;
+    split_bf16(acc[e] * inv, hi, lo);
+    a.out[dst + lane + 64 * e] = hi;
+    a.out_lo[dst + lane + 64 * e] = lo;
+  }
 }
 
 hipError_t launch_attention_split(const AttnArgs& a, hipStream_t s) {

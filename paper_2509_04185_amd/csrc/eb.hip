@@ -5,8 +5,8 @@
 // with t = l - m_c in float64 accumulates Z_c = sum e^t and S_c = sum e^t t.  Sums are
 // per-thread in a fixed order followed by a fixed tree, so results are reproducible.
 //
-// eb_select: one wave per sequence, lane j = block row j.  Rows merge their chunks in
-// vocabulary order with M = max m_c, delta_c = m_c - M:
+// eb_select: one workgroup per sequence.  Each masked row merges its chunks (one lane
+// per chunk, fixed butterfly sums) with M = max m_c, delta_c = m_c - M:
 //   Z = sum_c e^delta_c Z_c,  S = sum_c e^delta_c (S_c + delta_c Z_c),  H = log Z - S / Z
 // (the entropy of softmax over the row; argmax = first chunk reaching M).  Then the
 // masked rows are ranked by (H, row), lane 0 forms the running float64 sums c_r in
@@ -111,45 +111,76 @@ __global__ __launch_bounds__(kEbThreads) void eb_partial_kernel(EbArgs a) {
   }
 }
 
+__device__ __forceinline__ double wave_sum_d(double v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += shfl_xor_d(v, o);
+  return v;
+}
+
+__device__ __forceinline__ double wave_max_d(double v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmax(v, shfl_xor_d(v, o));
+  return v;
+}
+
+// One workgroup (4 waves) per sequence.  Wave w merges the chunk statistics of rows
+// w, w + 4, ... with one lane per chunk; wave 0 then ranks and selects.
 template <bool SELECT_ONLY>
-__global__ __launch_bounds__(64) void eb_select_kernel(EbArgs a) {
+__global__ __launch_bounds__(256) void eb_select_kernel(EbArgs a) {
   __shared__ double sh[64];
   __shared__ int smask[64];
+  __shared__ int stok[64];
   __shared__ int order[64];
   __shared__ int s_count;
   const int b = blockIdx.x;
-  const int j = threadIdx.x;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int k = a.k;
-  const bool in = j < k;
-  const int64_t row = (int64_t)b * k + j;
-  const bool masked = in && a.is_mask[row] != 0;
 
-  double H = 0.0;
-  int tok = -1;
-  if (masked) {
-    if (SELECT_ONLY) {
-      H = a.entropy_in[row];
-    } else {
-      const double* p = a.part + row * a.n_chunks * 3;
-      double M = -INFINITY;
-      for (int c = 0; c < a.n_chunks; ++c) M = fmax(M, p[c * 3]);
-      double Z = 0.0, S = 0.0;
-      for (int c = 0; c < a.n_chunks; ++c) {
-        const double mc = p[c * 3];
-        if (mc == -INFINITY) continue;
-        const double d = mc - M;
-        const double f = exp(d);
-        Z += f * p[c * 3 + 1];
-        S += f * (p[c * 3 + 2] + d * p[c * 3 + 1]);
-        if (tok < 0 && mc == M) tok = a.part_arg[row * a.n_chunks + c];
+  for (int j = w; j < k; j += 4) {
+    const int64_t row = (int64_t)b * k + j;
+    const bool masked = a.is_mask[row] != 0;
+    double H = 0.0;
+    int tok = -1;
+    if (masked) {
+      if (SELECT_ONLY) {
+        H = a.entropy_in[row];
+      } else {
+        const double* p = a.part + row * a.n_chunks * 3;
+        double mloc = -INFINITY;
+        for (int c = lane; c < a.n_chunks; c += 64) mloc = fmax(mloc, p[c * 3]);
+        const double M = wave_max_d(mloc);
+        double z = 0.0, sacc = 0.0;
+        int cfirst = INT32_MAX;
+        for (int c = lane; c < a.n_chunks; c += 64) {
+          const double mc = p[c * 3];
+          if (mc == -INFINITY) continue;
+          const double d = mc - M;
+          const double f = exp(d);
+          z += f * p[c * 3 + 1];
+          sacc += f * (p[c * 3 + 2] + d * p[c * 3 + 1]);
+          if (mc == M && c < cfirst) cfirst = c;
+        }
+        const double Z = wave_sum_d(z);
+        const double S = wave_sum_d(sacc);
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) cfirst = min(cfirst, __shfl_xor(cfirst, o));
+        tok = a.part_arg[row * a.n_chunks + cfirst];
+        H = log(Z) - S / Z;
       }
-      H = log(Z) - S / Z;
+    }
+    if (lane == 0) {
+      sh[j] = H;
+      smask[j] = masked ? 1 : 0;
+      stok[j] = tok;
     }
   }
-  sh[j] = H;
-  smask[j] = masked ? 1 : 0;
   __syncthreads();
+  if (w != 0) return;
 
+  const int j = lane;
+  const bool in = j < k;
+  const bool masked = in && smask[j] != 0;
+  const double H = in ? sh[j] : 0.0;
   int rank = 0, n = 0;
   for (int i = 0; i < k; ++i) {
     if (!smask[i]) continue;
@@ -171,14 +202,10 @@ __global__ __launch_bounds__(64) void eb_select_kernel(EbArgs a) {
   __syncthreads();
   const int s = s_count;
   const bool acc = masked && rank < s;
-  int idx = 0;
-  for (int i = 0; i < j; ++i) {
-    if (!smask[i]) continue;
-    int ri = 0;
-    for (int q = 0; q < k; ++q)
-      if (smask[q] && (sh[q] < sh[i] || (sh[q] == sh[i] && q < i))) ++ri;
-    if (ri < s) ++idx;
-  }
+  // output slot = number of accepted rows before j
+  const unsigned long long before = __ballot(acc) & ((1ull << j) - 1ull);
+  const int idx = __popcll(before);
+  const int64_t row = (int64_t)b * k + j;
   if (in) {
     if (j >= s) {
       a.accepted_pos[row] = -1;
@@ -189,7 +216,7 @@ __global__ __launch_bounds__(64) void eb_select_kernel(EbArgs a) {
   __syncthreads();
   if (acc) {
     a.accepted_pos[(int64_t)b * k + idx] = j;
-    if (a.accepted_tok) a.accepted_tok[(int64_t)b * k + idx] = tok;
+    if (a.accepted_tok) a.accepted_tok[(int64_t)b * k + idx] = stok[j];
   }
 }
 
@@ -200,9 +227,9 @@ hipError_t launch_eb_partial(const EbArgs& a, hipStream_t s) {
 
 hipError_t launch_eb_select(const EbArgs& a, bool select_only, hipStream_t s) {
   if (select_only)
-    hipLaunchKernelGGL(eb_select_kernel<true>, dim3(a.B), dim3(64), 0, s, a);
+    hipLaunchKernelGGL(eb_select_kernel<true>, dim3(a.B), dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL(eb_select_kernel<false>, dim3(a.B), dim3(64), 0, s, a);
+    hipLaunchKernelGGL(eb_select_kernel<false>, dim3(a.B), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

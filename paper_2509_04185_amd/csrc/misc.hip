@@ -21,16 +21,24 @@ __device__ __forceinline__ int64_t kv_head_base(int layer, int slot, int g, int 
   return (((int64_t)layer * n_slots + slot) * n_kv + g) * cap * d_h;
 }
 
-// x[m] = E[tok[m]] (fp32), xn[m] = bf16(x * g), sumsq[m][c/32] = sum over 32 columns of x^2.
+// x[m] = E[tok[m]] (fp32), xn[m] = x * g as hi/lo bf16, sumsq[m][c/16] = sum over 16
+// columns of x^2.
 __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
   const int m = blockIdx.y;
   const int c = blockIdx.x * 256 + threadIdx.x;
   const int tok = a.rows[m].tok;
   const float v = bf2f(a.embed[(int64_t)tok * a.d + c]);
   a.x[(int64_t)m * a.d + c] = v;
-  a.xn[(int64_t)m * a.d + c] = f2bf(v * bf2f(a.g[c]));
-  const float s = half_wave_sum(v * v);
-  if ((threadIdx.x & 31) == 0) a.sumsq[(int64_t)m * (a.d / 32) + c / 32] = s;
+  bf16_t hi, lo;
+  split_bf16(v * bf2f(a.g[c]), hi, lo);
+  a.xn[(int64_t)m * a.d + c] = hi;
+  a.xn_lo[(int64_t)m * a.d + c] = lo;
+  float s = v * v;
+  s += __shfl_xor(s, 8);
+  s += __shfl_xor(s, 4);
+  s += __shfl_xor(s, 2);
+  s += __shfl_xor(s, 1);
+  if ((threadIdx.x & 15) == 0) a.sumsq[(int64_t)m * (a.d / 16) + c / 16] = s;
 }
 
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
@@ -39,7 +47,7 @@ hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
 }
 
 // One wave per (row, head).  Lane i < d_h/2 owns the RoPE pair (i, i + d_h/2).
-// Query heads: optional per-head RMSNorm, rotation, scaling, bf16 store.
+// Query heads: optional per-head RMSNorm, rotation, scaling, hi/lo bf16 store.
 // Key heads: optional per-head RMSNorm, rotation, store into the cache at position
 // cache_len + j.  Value heads: store into the transposed V block.
 __global__ __launch_bounds__(64) void rope_stage_kernel(RopeStageArgs a) {
@@ -73,9 +81,14 @@ __global__ __launch_bounds__(64) void rope_stage_kernel(RopeStageArgs a) {
     const float r0 = u0 * c - u1 * sn;
     const float r1 = u1 * c + u0 * sn;
     if (is_q) {
-      bf16_t* dst = a.q + ((int64_t)m * a.n_q + h) * a.d_h;
-      dst[lane] = f2bf(r0 * a.q_scale);
-      dst[lane + half] = f2bf(r1 * a.q_scale);
+      const int64_t o = ((int64_t)m * a.n_q + h) * a.d_h;
+      bf16_t hi, lo;
+      split_bf16(r0 * a.q_scale, hi, lo);
+      a.q[o + lane] = hi;
+      a.q_lo[o + lane] = lo;
+      split_bf16(r1 * a.q_scale, hi, lo);
+      a.q[o + lane + half] = hi;
+      a.q_lo[o + lane + half] = lo;
     } else {
       const int g = h - a.n_q;
       bf16_t* dst = a.kcache + kv_head_base(a.layer, sp.slot, g, a.n_slots, a.n_kv, a.cap, a.d_h) +

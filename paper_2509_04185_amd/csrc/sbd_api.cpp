@@ -53,7 +53,7 @@ bool sbd::compute_layout(const sbd_model_config& c, Layout* L) {
   o.cap = ((int64_t)c.max_seq_len + 63) / 64 * 64;
   o.m_max = std::max<int64_t>((int64_t)c.max_batch * c.max_block, effective_chunk(c));
   o.n_qkv = (int64_t)(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
-  o.n_part = c.d_model / 32;
+  o.n_part = c.d_model / 16;
   o.eb_chunks = (c.vocab + kEbChunk - 1) / kEbChunk;
   const int64_t qd = (int64_t)c.n_q_heads * c.head_dim;
   const int64_t kv_elems = (int64_t)c.n_layers * c.max_batch * c.n_kv_heads * o.cap * c.head_dim;
@@ -68,12 +68,12 @@ bool sbd::compute_layout(const sbd_model_config& c, Layout* L) {
   o.vcache = take(kv_elems * 2);
   o.rope = take(o.cap * (c.head_dim / 2) * 2 * sizeof(float));
   o.x = take(o.m_max * c.d_model * sizeof(float));
-  o.xn = take(o.m_max * c.d_model * 2);
+  o.xn = take(2 * o.m_max * c.d_model * 2);             // hi then lo
   o.sumsq = take(o.m_max * o.n_part * sizeof(float));
   o.qkv = take(o.m_max * o.n_qkv * sizeof(float));
-  o.q = take(o.m_max * qd * 2);
-  o.attn = take(o.m_max * qd * 2);
-  o.act = take(o.m_max * (int64_t)c.ffn_dim * 2);
+  o.q = take(2 * o.m_max * qd * 2);
+  o.attn = take(2 * o.m_max * qd * 2);
+  o.act = take(2 * o.m_max * (int64_t)c.ffn_dim * 2);
   o.attn_ml = take((int64_t)kMaxSplits * o.m_max * c.n_q_heads * 2 * sizeof(float));
   o.attn_o = take((int64_t)kMaxSplits * o.m_max * qd * sizeof(float));
   o.rows = take(o.m_max * sizeof(RowParam));
@@ -204,15 +204,19 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
 
   float* x = c->at<float>(L.x);
   bf16_t* xn = c->at<bf16_t>(L.xn);
+  bf16_t* xn_lo = xn + L.m_max * d;
   float* sumsq = c->at<float>(L.sumsq);
   float* qkv = c->at<float>(L.qkv);
   bf16_t* q = c->at<bf16_t>(L.q);
+  bf16_t* q_lo = q + L.m_max * qd;
   bf16_t* attn = c->at<bf16_t>(L.attn);
+  bf16_t* attn_lo = attn + L.m_max * qd;
   bf16_t* act = c->at<bf16_t>(L.act);
+  bf16_t* act_lo = act + L.m_max * (int64_t)m.ffn_dim;
   const RowParam* drows = c->at<RowParam>(L.rows);
   const SeqParam* dseqs = c->at<SeqParam>(L.seqs);
 
-  EmbedArgs ea{drows, M, d, c->embed, c->layers[0].attn_norm, x, xn, sumsq};
+  EmbedArgs ea{drows, M, d, c->embed, c->layers[0].attn_norm, x, xn, xn_lo, sumsq};
   SBD_LAUNCH(c, SBD_KERNEL_EMBED, launch_embed(ea, c->stream));
 
   int max_end = 0;
@@ -227,7 +231,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   for (int l = 0; l < m.n_layers; ++l) {
     const LayerW& w = c->layers[l];
     GemmArgs g{};
-    g.A = xn; g.lda = d; g.M = M; g.K = d;
+    g.A = xn; g.A_lo = xn_lo; g.lda = d; g.M = M; g.K = d;
     g.W0 = w.wq; g.W1 = w.wk; g.W2 = w.wv; g.n0 = qd; g.n1 = nkv * dh;
     g.n_tiles = (int)(L.n_qkv / 32);
     g.out_f32 = qkv; g.ldo = L.n_qkv;
@@ -239,36 +243,37 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     ra.n_q = nq; ra.n_kv = nkv; ra.d_h = dh; ra.qk_norm = m.qk_norm; ra.eps = m.rms_eps;
     ra.q_scale = (float)(1.4426950408889634 / std::sqrt((double)dh));
     ra.qkv = qkv; ra.q_norm = w.q_norm; ra.k_norm = w.k_norm; ra.rope = c->at<float>(L.rope);
-    ra.q = q; ra.kcache = c->at<bf16_t>(L.kcache); ra.vcache = c->at<bf16_t>(L.vcache);
+    ra.q = q; ra.q_lo = q_lo; ra.kcache = c->at<bf16_t>(L.kcache); ra.vcache = c->at<bf16_t>(L.vcache);
     ra.cap = L.cap; ra.n_slots = m.max_batch;
     SBD_LAUNCH(c, SBD_KERNEL_ROPE, launch_rope_stage(ra, c->stream));
 
     AttnArgs aa{};
     aa.seqs = dseqs; aa.B = B; aa.k = k; aa.layer = l; aa.n_q = nq; aa.n_kv = nkv; aa.d_h = dh;
-    aa.q = q; aa.kcache = ra.kcache; aa.vcache = ra.vcache; aa.cap = L.cap; aa.n_slots = m.max_batch;
+    aa.q = q; aa.q_lo = q_lo; aa.kcache = ra.kcache; aa.vcache = ra.vcache; aa.cap = L.cap; aa.n_slots = m.max_batch;
     aa.n_rowblocks = n_rb; aa.n_splits = n_splits; aa.blocks_per_split = bps;
     aa.part_ml = c->at<float>(L.attn_ml); aa.part_o = c->at<float>(L.attn_o); aa.out = attn;
+    aa.out_lo = attn_lo;
     SBD_LAUNCH(c, SBD_KERNEL_ATTENTION, launch_attention_split(aa, c->stream));
     SBD_LAUNCH(c, SBD_KERNEL_ATTN_MERGE, launch_attention_merge(aa, c->stream));
 
     GemmArgs go{};
-    go.A = attn; go.lda = qd; go.M = M; go.K = qd;
+    go.A = attn; go.A_lo = attn_lo; go.lda = qd; go.M = M; go.K = qd;
     go.W0 = w.wo; go.n0 = d; go.n1 = 0; go.n_tiles = d / 32;
-    go.x = x; go.ldx = d; go.xn = xn; go.g_next = w.mlp_norm; go.sumsq_out = sumsq;
+    go.x = x; go.ldx = d; go.xn = xn; go.xn_lo = xn_lo; go.g_next = w.mlp_norm; go.sumsq_out = sumsq;
     go.n_part = (int)L.n_part;
     SBD_LAUNCH(c, SBD_KERNEL_O_PROJ, launch_gemm(EPI_RESID, go, c->stream));
 
     GemmArgs gu{};
-    gu.A = xn; gu.lda = d; gu.M = M; gu.K = d;
+    gu.A = xn; gu.A_lo = xn_lo; gu.lda = d; gu.M = M; gu.K = d;
     gu.W0 = w.w_gate; gu.W1 = w.w_up; gu.n_tiles = m.ffn_dim / 16;
     gu.sumsq_in = sumsq; gu.n_part = (int)L.n_part; gu.inv_d = 1.0f / d; gu.eps = m.rms_eps;
-    gu.act = act; gu.ld_act = m.ffn_dim;
+    gu.act = act; gu.act_lo = act_lo; gu.ld_act = m.ffn_dim;
     SBD_LAUNCH(c, SBD_KERNEL_GATE_UP, launch_gemm(EPI_SWIGLU, gu, c->stream));
 
     GemmArgs gd{};
-    gd.A = act; gd.lda = m.ffn_dim; gd.M = M; gd.K = m.ffn_dim;
+    gd.A = act; gd.A_lo = act_lo; gd.lda = m.ffn_dim; gd.M = M; gd.K = m.ffn_dim;
     gd.W0 = w.w_down; gd.n0 = d; gd.n1 = 0; gd.n_tiles = d / 32;
-    gd.x = x; gd.ldx = d; gd.xn = xn;
+    gd.x = x; gd.ldx = d; gd.xn = xn; gd.xn_lo = xn_lo;
     gd.g_next = (l + 1 < m.n_layers) ? c->layers[l + 1].attn_norm : c->final_norm;
     gd.sumsq_out = sumsq; gd.n_part = (int)L.n_part;
     SBD_LAUNCH(c, SBD_KERNEL_DOWN, launch_gemm(EPI_RESID, gd, c->stream));
@@ -277,7 +282,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   if (logits != nullptr) {
     GemmArgs gl{};
     const int r0 = lm_row < 0 ? 0 : lm_row;
-    gl.A = xn + (int64_t)r0 * d; gl.lda = d; gl.M = lm_row < 0 ? M : 1; gl.K = d;
+    gl.A = xn + (int64_t)r0 * d; gl.A_lo = xn_lo + (int64_t)r0 * d; gl.lda = d; gl.M = lm_row < 0 ? M : 1; gl.K = d;
     gl.W0 = c->lm_head; gl.n0 = m.vocab; gl.n1 = 0; gl.n_tiles = m.vocab / 32;
     gl.out_f32 = logits; gl.ldo = m.vocab;
     gl.sumsq_in = sumsq + (int64_t)r0 * L.n_part; gl.n_part = (int)L.n_part;
@@ -312,10 +317,10 @@ sbd_status sbd_workspace_region(const sbd_model_config* cfg, const char* name, s
   struct R { const char* n; size_t off, sz; } regions[] = {
       {"x", L.x, (size_t)(L.m_max * cfg->d_model * 4)},
       {"qkv", L.qkv, (size_t)(L.m_max * L.n_qkv * 4)},
-      {"q", L.q, (size_t)(L.m_max * qd * 2)},
-      {"attn", L.attn, (size_t)(L.m_max * qd * 2)},
-      {"act", L.act, (size_t)(L.m_max * cfg->ffn_dim * 2)},
-      {"xn", L.xn, (size_t)(L.m_max * cfg->d_model * 2)},
+      {"q", L.q, (size_t)(2 * L.m_max * qd * 2)},
+      {"attn", L.attn, (size_t)(2 * L.m_max * qd * 2)},
+      {"act", L.act, (size_t)(2 * L.m_max * cfg->ffn_dim * 2)},
+      {"xn", L.xn, (size_t)(2 * L.m_max * cfg->d_model * 2)},
   };
   for (const R& r : regions)
     if (std::strcmp(r.n, name) == 0) {

@@ -38,7 +38,7 @@ struct Layout {
   int64_t cap;            // cache capacity per slot (max_seq_len rounded up to 64)
   int64_t m_max;          // rows per forward (max(max_batch*max_block, prefill_chunk))
   int64_t n_qkv;          // (n_q_heads + 2 n_kv_heads) * head_dim
-  int64_t n_part;         // d_model / 32 sum-of-squares partials per row
+  int64_t n_part;         // d_model / 16 sum-of-squares partials per row
   int64_t eb_chunks;      // ceil(vocab / kEbChunk)
   size_t kcache, vcache, rope, x, xn, sumsq, qkv, q, attn, act;
   size_t attn_ml, attn_o, rows, seqs, eb_mask, eb_part, eb_arg;
@@ -56,9 +56,14 @@ struct LayerW {
 // ---------------------------------------------------------------------------- GEMM
 enum GemmEpi { EPI_SCALED_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
 
+// Activations travel as two bf16 arrays, hi = bf16(a) and lo = bf16(a - hi), which
+// together carry about 16 significant bits; products with bf16 weights are exact in the
+// fp32 accumulators, so a GEMM over (hi, lo) loses only the lo truncation.
+//
 // y[m][n] = sum_k A[m][k] * W[n][k] over the row-major [out][in] weight segments.
 struct GemmArgs {
-  const bf16_t* A;  // [M][K] bf16, row stride lda
+  const bf16_t* A;     // hi part [M][K], row stride lda
+  const bf16_t* A_lo;  // lo part, same layout
   int64_t lda;
   int M, K;
   const bf16_t* W0;  // segment 0 (or gate)
@@ -73,14 +78,16 @@ struct GemmArgs {
   const float* sumsq_in;
   int n_part;
   float inv_d, eps;
-  // EPI_RESID: x[m][n] += y; xn[m][n] = bf16(x * g_next[n]); sumsq_out[m][n/32] = sum x^2
+  // EPI_RESID: x[m][n] += y; xn[m][n] = bf16(x * g_next[n]); sumsq_out[m][n/16] = sum x^2
   float* x;
   int64_t ldx;
   bf16_t* xn;
+  bf16_t* xn_lo;
   const bf16_t* g_next;
   float* sumsq_out;
-  // EPI_SWIGLU: act[m][j] = bf16(silu(rinv*gate) * rinv*up)
+  // EPI_SWIGLU: act[m][j] = silu(rinv*gate) * rinv*up as hi/lo
   bf16_t* act;
+  bf16_t* act_lo;
   int64_t ld_act;
 };
 
@@ -94,7 +101,8 @@ struct EmbedArgs {
   const bf16_t* g;  // first attention-norm gain
   float* x;
   bf16_t* xn;
-  float* sumsq;  // [M][d/32]
+  bf16_t* xn_lo;
+  float* sumsq;  // [M][d/16]
 };
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
 
@@ -110,7 +118,8 @@ struct RopeStageArgs {
   const bf16_t* q_norm;
   const bf16_t* k_norm;
   const float* rope;  // [cap][d_h/2][2] (cos, sin)
-  bf16_t* q;  // [M][n_q][d_h]
+  bf16_t* q;     // [M][n_q][d_h] hi
+  bf16_t* q_lo;  // lo
   bf16_t* kcache;
   bf16_t* vcache;
   int64_t cap;
@@ -139,7 +148,8 @@ struct AttnArgs {
   const SeqParam* seqs;
   int B, k, layer;
   int n_q, n_kv, d_h;
-  const bf16_t* q;  // [B*k][n_q][d_h], pre-scaled by log2(e)/sqrt(d_h)
+  const bf16_t* q;     // [B*k][n_q][d_h] hi, pre-scaled by log2(e)/sqrt(d_h)
+  const bf16_t* q_lo;  // lo
   const bf16_t* kcache;
   const bf16_t* vcache;
   int64_t cap;
@@ -149,7 +159,8 @@ struct AttnArgs {
   int blocks_per_split;  // 32-key blocks per split
   float* part_ml;   // [n_splits][B*k*n_q][2]
   float* part_o;    // [n_splits][B*k*n_q][d_h]
-  bf16_t* out;  // [B*k][n_q*d_h]
+  bf16_t* out;     // [B*k][n_q*d_h] hi
+  bf16_t* out_lo;  // lo
 };
 hipError_t launch_attention_split(const AttnArgs& a, hipStream_t s);
 hipError_t launch_attention_merge(const AttnArgs& a, hipStream_t s);

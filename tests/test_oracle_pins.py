@@ -123,6 +123,25 @@ def test_rope_scores_depend_on_relative_position_only():
     assert abs(score(0, 0) - float((q * k).sum())) < 1e-12
 
 
+def test_round_to_bf16_matches_torch():
+    rng = np.random.default_rng(5)
+    a = (rng.normal(size=20000) * np.exp(rng.uniform(-20, 20, 20000))).astype(np.float32)
+    # exact ties: 1 + 2^-8 (-> 1, even) and 1 + 3*2^-8 (-> 1 + 2^-6... rounds up to even)
+    a = np.concatenate([a, np.array([1 + 2**-8, 1 + 3 * 2**-8, -(1 + 2**-8), 3.0], np.float32)])
+    want = torch.from_numpy(a).to(torch.bfloat16).float().numpy()
+    assert np.array_equal(O.round_to_bf16(a), want)
+    assert O.round_to_bf16(np.array([1 + 2**-8], np.float64))[0] == 1.0
+
+
+def test_kv_bf16_model_stores_bf16_values():
+    shape, m = tiny_model()
+    mb = O.Model(shape, m.w, dtype=np.float64, kv_bf16=True)
+    c, _ = mb.prefill(synth.make_tokens(3, 9, shape))
+    for li in range(shape.n_layers):
+        assert np.array_equal(O.round_to_bf16(c.K[li]), c.K[li])
+        assert np.array_equal(O.round_to_bf16(c.V[li]), c.V[li])
+
+
 # ------------------------------------------------------------------ SBD network invariants
 
 @pytest.mark.parametrize("qk_norm", [False, True])
