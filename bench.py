@@ -195,7 +195,7 @@ def main():
                 traffic = tr.get("bytes_per_launch")
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                     "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-                    "kernel": "gemm_kernel<1,8,8,EPI_SWIGLU> (gate/up + SwiGLU)",
+                    "kernel": "gemm_kernel<1,2,4,8,EPI_SWIGLU> (gate/up projection + SwiGLU)",
                     "bytes_per_launch": bpl, "avg_launch_us": round(avg_s * 1e6, 2),
                     "launches": c}
 

@@ -79,15 +79,18 @@ typedef struct {
 } sbd_weights;
 
 /* Bytes of device workspace sbd_create needs for this config (KV cache, activations,
- * partial results, RoPE table).  *bytes is set only on SBD_OK. */
+ * partial results, RoPE table, and a copy of every weight matrix repacked into the
+ * order the GEMM kernels stream).  *bytes is set only on SBD_OK. */
 sbd_status sbd_workspace_bytes(const sbd_model_config* cfg, size_t* bytes);
 
 /*
  * Create a context on the current HIP device.  workspace: device memory of at least
  * sbd_workspace_bytes() bytes, 256-byte aligned, caller-owned, not touched by anyone
  * else while the context lives.  stream: a hipStream_t (NULL = the null stream).
- * Every sequence slot starts empty.  The library allocates no device memory itself;
- * it allocates a small pinned host staging buffer here.
+ * Every sequence slot starts empty.  The weights are read here once, to repack them into
+ * the workspace (the originals must still outlive the context: the embedding and norm
+ * gains are read from them).  The library allocates no device memory itself; it
+ * allocates a small pinned host staging buffer here.
  */
 sbd_status sbd_create(const sbd_model_config* cfg, const sbd_weights* w, void* workspace,
                       size_t workspace_bytes, void* stream, sbd_ctx** out);

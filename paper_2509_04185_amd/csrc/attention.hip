@@ -206,24 +206,24 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   }
 }
 
-hipError_t launch_attention_split(const AttnArgs& a, hipStream_t s) {
+hipError_t launch_attention_split(const AttnArgs& a, const Exec& ex) {
   dim3 grid(a.n_splits, a.n_kv * a.n_rowblocks, a.B);
   if (a.d_h == 128)
-    hipLaunchKernelGGL(attn_split_kernel<128>, grid, dim3(256), 0, s, a);
+    SBD_KLAUNCH(attn_split_kernel<128>, grid, dim3(256), ex, a);
   else if (a.d_h == 64)
-    hipLaunchKernelGGL(attn_split_kernel<64>, grid, dim3(256), 0, s, a);
+    SBD_KLAUNCH(attn_split_kernel<64>, grid, dim3(256), ex, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
-hipError_t launch_attention_merge(const AttnArgs& a, hipStream_t s) {
+hipError_t launch_attention_merge(const AttnArgs& a, const Exec& ex) {
   const int64_t n_items = (int64_t)a.B * a.k * a.n_q;
   dim3 grid((unsigned)((n_items + 3) / 4));
   if (a.d_h == 128)
-    hipLaunchKernelGGL(attn_merge_kernel<128>, grid, dim3(256), 0, s, a);
+    SBD_KLAUNCH(attn_merge_kernel<128>, grid, dim3(256), ex, a);
   else if (a.d_h == 64)
-    hipLaunchKernelGGL(attn_merge_kernel<64>, grid, dim3(256), 0, s, a);
+    SBD_KLAUNCH(attn_merge_kernel<64>, grid, dim3(256), ex, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

@@ -175,10 +175,10 @@ __global__ __launch_bounds__(256) void eb_select_kernel(EbArgs a) {
     }
   }
   __syncthreads();
-  if (w != 0) return;
-
+  // Wave 0 ranks and selects; the other waves only join the barriers below.
+  const bool w0 = w == 0;
   const int j = lane;
-  const bool in = j < k;
+  const bool in = w0 && j < k;
   const bool masked = in && smask[j] != 0;
   const double H = in ? sh[j] : 0.0;
   int rank = 0, n = 0;
@@ -189,7 +189,7 @@ __global__ __launch_bounds__(256) void eb_select_kernel(EbArgs a) {
   }
   if (masked) order[rank] = j;
   __syncthreads();
-  if (j == 0) {
+  if (w0 && j == 0) {
     int s = 0;
     double c = 0.0;
     for (int r = 0; r < n; ++r) {
@@ -220,16 +220,16 @@ __global__ __launch_bounds__(256) void eb_select_kernel(EbArgs a) {
   }
 }
 
-hipError_t launch_eb_partial(const EbArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(eb_partial_kernel, dim3(a.n_chunks, a.B * a.k), dim3(kEbThreads), 0, s, a);
+hipError_t launch_eb_partial(const EbArgs& a, const Exec& ex) {
+  SBD_KLAUNCH(eb_partial_kernel, dim3(a.n_chunks, a.B * a.k), dim3(kEbThreads), ex, a);
   return hipGetLastError();
 }
 
-hipError_t launch_eb_select(const EbArgs& a, bool select_only, hipStream_t s) {
+hipError_t launch_eb_select(const EbArgs& a, bool select_only, const Exec& ex) {
   if (select_only)
-    hipLaunchKernelGGL(eb_select_kernel<true>, dim3(a.B), dim3(256), 0, s, a);
+    SBD_KLAUNCH(eb_select_kernel<true>, dim3(a.B), dim3(256), ex, a);
   else
-    hipLaunchKernelGGL(eb_select_kernel<false>, dim3(a.B), dim3(256), 0, s, a);
+    SBD_KLAUNCH(eb_select_kernel<false>, dim3(a.B), dim3(256), ex, a);
   return hipGetLastError();
 }
 

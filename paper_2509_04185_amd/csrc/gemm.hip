@@ -2,21 +2,29 @@
 //
 // The block forward multiplies M = batch * k activation rows (16 at batch 1, k = 16) by
 // every weight matrix of the decoder, so it is bound by streaming the weights from HBM.
-// Each workgroup owns 16*C output columns (C 16-wide MFMA tiles) and a row block; its
-// NW waves split the reduction dimension K and stream disjoint K ranges of the same
-// weight rows with 16-byte non-temporal loads, double-buffered in registers.  The
-// activations come as hi/lo bf16 pairs (two MFMAs per step, see GemmArgs).  Partial
-// sums meet in LDS and are added in a fixed wave order (deterministic), and the
-// epilogue applies the operation that follows the product in the decoder block:
+//
+// Weights are repacked once (pack_kernel) into MFMA fragment order: a matrix with N rows
+// and K columns becomes [N/16 tiles][K/32 steps][64 lanes][8], the 16-byte piece of lane
+// l in step s of tile t holding W[16t + l%16][32s + 8(l/16) .. +8].  One 16-byte load per
+// lane then reads 1 KB of contiguous memory and lands directly in the B operand of
+// v_mfma_f32_16x16x32_bf16.  The gate and up projections share one packed matrix whose
+// tile t holds gate rows 8t..8t+7 followed by up rows 8t..8t+7, so SwiGLU pairs stay
+// inside one tile.
+//
+// Each workgroup owns C consecutive tiles (16*C output columns) and a row block; its NW
+// waves split the K/32 steps and stream disjoint contiguous ranges with non-temporal
+// loads, double-buffered in registers.  The activations come as hi/lo bf16 pairs (two
+// MFMAs per step, see GemmArgs).  Partial sums meet in LDS and are added in a fixed wave
+// order (deterministic); the epilogue applies what follows the product in the block:
 //   EPI_SCALED_STORE  out = rinv[m] * y           (QKV projection, LM head)
-//   EPI_RESID         x += y; xn = bf16(x * g_next); per-row sums of x^2 over each
-//                     16 columns (O and down projections: residual add, the next
-//                     RMSNorm's inputs)
-//   EPI_SWIGLU        act = bf16(silu(rinv*gate) * rinv*up)  (gate/up projection)
-// RMSNorm is split across two kernels: the producer writes x * g (gain applied, bf16)
-// plus per-16-column partial sums of squares; the consumer adds the partials of a row
-// and scales its fp32 result by 1/sqrt(mean(x^2) + eps), which equals normalising the
-// input first because the scale is constant along a row.
+//   EPI_RESID         x += y; xn = x * g_next as hi/lo; per-row sums of x^2 over each 16
+//                     columns (O and down projections: residual add, the next RMSNorm's
+//                     inputs)
+//   EPI_SWIGLU        act = silu(rinv*gate) * rinv*up as hi/lo (gate/up projection)
+// RMSNorm is split across two kernels: the producer writes x * g (gain applied) plus
+// per-16-column partial sums of squares; the consumer adds the partials of a row and
+// scales its fp32 result by 1/sqrt(mean(x^2) + eps), which equals normalising the input
+// first because the scale is constant along a row.
 //
 // MFMA v_mfma_f32_16x16x32_bf16: lane l holds row (l % 16) of A and column (l % 16) of
 // B^T for the 8 consecutive k of group l / 16; the result holds rows 4*(l/16)+i of
@@ -41,46 +49,26 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(GemmArgs a) {
   const int row0 = blockIdx.x * (MT * 16);
   const int K = a.K;
 
-  // Weight row feeding column 16*ct + r of this workgroup.
-  const bf16_t* wrow[C];
-  if (EPI == EPI_SWIGLU) {
-    // columns [0, 8C) are gate rows j0.., columns [8C, 16C) the matching up rows
-    const int j0 = tile * 8 * C;
-#pragma unroll
-    for (int ct = 0; ct < C; ++ct) {
-      const int c = 16 * ct + r;
-      wrow[ct] = (c < 8 * C) ? a.W0 + (int64_t)(j0 + c) * K : a.W1 + (int64_t)(j0 + c - 8 * C) * K;
-    }
-  } else {
-    const int n = tile * NC;
-    const bf16_t* base;
-    int nloc;
-    if (n < a.n0) {
-      base = a.W0; nloc = n;
-    } else if (n < a.n0 + a.n1) {
-      base = a.W1; nloc = n - a.n0;
-    } else {
-      base = a.W2; nloc = n - a.n0 - a.n1;
-    }
-#pragma unroll
-    for (int ct = 0; ct < C; ++ct) wrow[ct] = base + (int64_t)(nloc + 16 * ct + r) * K;
-  }
-  const bf16_t* arow[MT];
-  const bf16_t* arow_lo[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    int m = row0 + mt * 16 + r;
-    if (m >= a.M) m = a.M - 1;
-    arow[mt] = a.A + (int64_t)m * a.lda;
-    arow_lo[mt] = a.A_lo + (int64_t)m * a.lda;
-  }
-
   // This wave's share of the K/32 steps.
   const int S = K / 32;
   const int base_steps = S / NW, rem = S % NW;
   const int s0 = w * base_steps + (w < rem ? w : rem);
   const int ns = base_steps + (w < rem ? 1 : 0);
   const int kbase = s0 * 32 + g * 8;
+
+  const bf16_t* wbase[C];
+#pragma unroll
+  for (int ct = 0; ct < C; ++ct)
+    wbase[ct] = a.Wp + ((int64_t)(tile * C + ct) * S + s0) * 512 + lane * 8;
+  const bf16_t* arow[MT];
+  const bf16_t* arow_lo[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    int m = row0 + mt * 16 + r;
+    if (m >= a.M) m = a.M - 1;
+    arow[mt] = a.A + (int64_t)m * a.lda + kbase;
+    arow_lo[mt] = a.A_lo + (int64_t)m * a.lda + kbase;
+  }
 
   f32x4 acc[MT][C];
 #pragma unroll
@@ -92,11 +80,12 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(GemmArgs a) {
 
 #define SBD_LOAD(WB, AB, AL, STEP)                                                 \
   _Pragma("unroll") for (int u = 0; u < U; ++u) {                                 \
-    const int kk = kbase + ((STEP) + u) * 32;                                     \
-    _Pragma("unroll") for (int ct = 0; ct < C; ++ct) WB[u][ct] = ld16_stream(wrow[ct] + kk); \
+    const int st_ = (STEP) + u;                                                   \
+    _Pragma("unroll") for (int ct = 0; ct < C; ++ct)                              \
+      WB[u][ct] = ld16_stream(wbase[ct] + (int64_t)st_ * 512);                    \
     _Pragma("unroll") for (int mt = 0; mt < MT; ++mt) {                           \
-      AB[u][mt] = ld16(arow[mt] + kk);                                            \
-      AL[u][mt] = ld16(arow_lo[mt] + kk);                                         \
+      AB[u][mt] = ld16(arow[mt] + st_ * 32);                                      \
+      AL[u][mt] = ld16(arow_lo[mt] + st_ * 32);                                   \
     }                                                                              \
   }
 #define SBD_COMPUTE(WB, AB, AL)                                                    \
@@ -133,14 +122,13 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(GemmArgs a) {
     }
   }
   for (int st = nchunks * U; st < ns; ++st) {
-    const int kk = kbase + st * 32;
     i32x4 wv[C];
 #pragma unroll
-    for (int ct = 0; ct < C; ++ct) wv[ct] = ld16_stream(wrow[ct] + kk);
+    for (int ct = 0; ct < C; ++ct) wv[ct] = ld16_stream(wbase[ct] + (int64_t)st * 512);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      const i32x4 av = ld16(arow[mt] + kk);
-      const i32x4 avl = ld16(arow_lo[mt] + kk);
+      const i32x4 av = ld16(arow[mt] + st * 32);
+      const i32x4 avl = ld16(arow_lo[mt] + st * 32);
 #pragma unroll
       for (int ct = 0; ct < C; ++ct) {
         acc[mt][ct] = mfma16x16x32(av, wv[ct], acc[mt][ct]);
@@ -160,7 +148,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(GemmArgs a) {
   __syncthreads();
 
   // Epilogue: thread idx -> (row idx / NC, column idx % NC); each 16-lane group holds
-  // 16 consecutive columns of one row.
+  // the 16 columns of one tile of one row.
   constexpr int TOTAL = MT * 16 * NC;
   constexpr int STRIDE = NW * 64;
   for (int idx = threadIdx.x; idx < (TOTAL + STRIDE - 1) / STRIDE * STRIDE; idx += STRIDE) {
@@ -193,49 +181,96 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(GemmArgs a) {
       s2 += __shfl_xor(s2, 2);
       s2 += __shfl_xor(s2, 1);
       if ((col & 15) == 0 && ok) a.sumsq_out[(int64_t)m * a.n_part + n / 16] = s2;
-    } else {  // EPI_SWIGLU
-      if (ok && col < 8 * C) {
+    } else {  // EPI_SWIGLU: column c < 8 of a tile is gate j, column c + 8 the matching up
+      const int c = col & 15;
+      if (ok && c < 8) {
         float yu = 0.f;
 #pragma unroll
-        for (int w2 = 0; w2 < NW; ++w2) yu += red[w2][rr][col + 8 * C];
+        for (int w2 = 0; w2 < NW; ++w2) yu += red[w2][rr][col + 8];
         const float gt = y * rinv_s[rr];
         const float up = yu * rinv_s[rr];
         const float sg = gt / (1.0f + expf(-gt));
+        const int j = (tile * C + (col >> 4)) * 8 + c;
         bf16_t hi, lo;
         split_bf16(sg * up, hi, lo);
-        a.act[(int64_t)m * a.ld_act + tile * 8 * C + col] = hi;
-        a.act_lo[(int64_t)m * a.ld_act + tile * 8 * C + col] = lo;
+        a.act[(int64_t)m * a.ld_act + j] = hi;
+        a.act_lo[(int64_t)m * a.ld_act + j] = lo;
       }
     }
   }
 }
 
 template <int MT, int C, int NW, int U, int EPI>
-static void launch_cfg(const GemmArgs& a, hipStream_t s) {
-  // n_tiles counts 32-column tiles; this configuration covers 16*C columns per workgroup.
-  const int tiles = a.n_tiles * 32 / (16 * C);
-  dim3 grid((a.M + 16 * MT - 1) / (16 * MT), tiles);
-  hipLaunchKernelGGL((gemm_kernel<MT, C, NW, U, EPI>), grid, dim3(NW * 64), 0, s, a);
+static void launch_cfg(const GemmArgs& a, const Exec& ex) {
+  dim3 grid((a.M + 16 * MT - 1) / (16 * MT), a.n_tiles / C);
+  SBD_KLAUNCH((gemm_kernel<MT, C, NW, U, EPI>), grid, dim3(NW * 64), ex, a);
 }
 
+// Configurations picked from a sweep over the decode shapes of the 8B models (M = 16):
+// many tiles (LM head, gate/up, QKV) favour two tiles per workgroup and 4 K-waves; the
+// 4096-column projections favour one tile and 8 K-waves (more workgroups in flight).
 template <int EPI>
-static hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
-  if (a.M <= 16)
-    launch_cfg<1, 2, 8, 4, EPI>(a, s);
-  else if (a.M <= 32)
-    launch_cfg<2, 2, 8, 4, EPI>(a, s);
-  else
-    launch_cfg<4, 2, 4, 2, EPI>(a, s);
+static hipError_t launch_epi(const GemmArgs& a, const Exec& ex) {
+  const bool even = a.n_tiles % 2 == 0;
+  if (a.M <= 16) {
+    if (even && a.n_tiles >= 4096)
+      launch_cfg<1, 2, 4, 4, EPI>(a, ex);
+    else if (even && a.n_tiles >= 384)
+      launch_cfg<1, 2, 4, 8, EPI>(a, ex);
+    else if (a.K > 8192)
+      launch_cfg<1, 1, 8, 4, EPI>(a, ex);
+    else
+      launch_cfg<1, 1, 8, 8, EPI>(a, ex);
+  } else if (a.M <= 32) {
+    if (even)
+      launch_cfg<2, 2, 8, 4, EPI>(a, ex);
+    else
+      launch_cfg<2, 1, 8, 4, EPI>(a, ex);
+  } else {
+    if (even)
+      launch_cfg<4, 2, 4, 2, EPI>(a, ex);
+    else
+      launch_cfg<4, 1, 4, 2, EPI>(a, ex);
+  }
   return hipGetLastError();
 }
 
-hipError_t launch_gemm(GemmEpi epi, const GemmArgs& a, hipStream_t s) {
+hipError_t launch_gemm(GemmEpi epi, const GemmArgs& a, const Exec& ex) {
   switch (epi) {
-    case EPI_SCALED_STORE: return launch_epi<EPI_SCALED_STORE>(a, s);
-    case EPI_RESID: return launch_epi<EPI_RESID>(a, s);
-    case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(a, s);
+    case EPI_SCALED_STORE: return launch_epi<EPI_SCALED_STORE>(a, ex);
+    case EPI_RESID: return launch_epi<EPI_RESID>(a, ex);
+    case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(a, ex);
   }
   return hipErrorInvalidValue;
+}
+
+// One thread per 16-byte piece of the packed matrix (see the top of this file).
+// Mode 0: packed row n is src0 row n.  Mode 1 (gate/up): packed tile t holds src0 rows
+// 8t..8t+7 then src1 rows 8t..8t+7.
+__global__ __launch_bounds__(256) void pack_kernel(const bf16_t* src0, const bf16_t* src1,
+                                                   bf16_t* dst, int64_t n_pieces, int K, int mode) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n_pieces) return;
+  const int S = K / 32;
+  const int lane = (int)(i % 64);
+  const int64_t s = (i / 64) % S;
+  const int64_t t = i / (64 * (int64_t)S);
+  const int rr = lane & 15;
+  const int64_t k0 = 32 * s + 8 * (lane >> 4);
+  const bf16_t* row;
+  if (mode == 0)
+    row = src0 + (t * 16 + rr) * (int64_t)K;
+  else
+    row = (rr < 8) ? src0 + (t * 8 + rr) * (int64_t)K : src1 + (t * 8 + rr - 8) * (int64_t)K;
+  *(i32x4*)(dst + i * 8) = *(const i32x4*)(row + k0);
+}
+
+hipError_t launch_pack(const bf16_t* src0, const bf16_t* src1, bf16_t* dst, int64_t rows, int K,
+                       int mode, hipStream_t s) {
+  const int64_t n_pieces = rows * K / 8;
+  hipLaunchKernelGGL(pack_kernel, dim3((unsigned)((n_pieces + 255) / 256)), dim3(256), 0, s, src0,
+                     src1, dst, n_pieces, K, mode);
+  return hipGetLastError();
 }
 
 }  // namespace sbd

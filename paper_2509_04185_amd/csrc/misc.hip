@@ -41,8 +41,8 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
   if ((threadIdx.x & 15) == 0) a.sumsq[(int64_t)m * (a.d / 16) + c / 16] = s;
 }
 
-hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(embed_kernel, dim3(a.d / 256, a.M), dim3(256), 0, s, a);
+hipError_t launch_embed(const EmbedArgs& a, const Exec& ex) {
+  SBD_KLAUNCH(embed_kernel, dim3(a.d / 256, a.M), dim3(256), ex, a);
   return hipGetLastError();
 }
 
@@ -107,8 +107,8 @@ __global__ __launch_bounds__(64) void rope_stage_kernel(RopeStageArgs a) {
   }
 }
 
-hipError_t launch_rope_stage(const RopeStageArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(rope_stage_kernel, dim3(a.n_q + 2 * a.n_kv, a.M), dim3(64), 0, s, a);
+hipError_t launch_rope_stage(const RopeStageArgs& a, const Exec& ex) {
+  SBD_KLAUNCH(rope_stage_kernel, dim3(a.n_q + 2 * a.n_kv, a.M), dim3(64), ex, a);
   return hipGetLastError();
 }
 

@@ -81,6 +81,13 @@ bool sbd::compute_layout(const sbd_model_config& c, Layout* L) {
   o.eb_mask = take(eb_rows);
   o.eb_part = take(eb_rows * o.eb_chunks * 3 * sizeof(double));
   o.eb_arg = take(eb_rows * o.eb_chunks * sizeof(int32_t));
+  // packed weights: per layer qkv [n_qkv][d], o [d][qd], gate/up [2F][d], down [d][F]
+  o.wp_o = o.n_qkv * c.d_model;
+  o.wp_gu = o.wp_o + (int64_t)c.d_model * qd;
+  o.wp_down = o.wp_gu + 2 * (int64_t)c.ffn_dim * c.d_model;
+  o.wp_layer = o.wp_down + (int64_t)c.d_model * c.ffn_dim;
+  o.wp_lm = o.wp_layer * c.n_layers;
+  o.wpack = take((o.wp_lm + (int64_t)c.vocab * c.d_model) * 2);
   o.total = off;
   *L = o;
   return true;
@@ -164,21 +171,18 @@ hipEvent_t take_event(sbd_ctx* c) {
   return e;
 }
 
-// Launch `expr` on the context stream; when profiling, bracket it with a pair of events.
+// Launch one kernel on the context stream: `expr` uses the Exec named `ex`.  When
+// profiling, the runtime records a pair of events at the kernel's start and end.
 #define SBD_LAUNCH(ctx, kind, expr)                                               \
   do {                                                                            \
-    hipEvent_t ea_ = nullptr, eb_ = nullptr;                                      \
+    Exec ex{(ctx)->stream, nullptr, nullptr};                                     \
     if ((ctx)->prof) {                                                            \
-      ea_ = take_event(ctx);                                                      \
-      eb_ = take_event(ctx);                                                      \
-      if (!ea_ || !eb_) return fail(ctx, SBD_ERR_HIP, "hipEventCreate failed");   \
-      SBD_HIP(ctx, hipEventRecord(ea_, (ctx)->stream));                           \
+      ex.start = take_event(ctx);                                                 \
+      ex.stop = take_event(ctx);                                                  \
+      if (!ex.start || !ex.stop) return fail(ctx, SBD_ERR_HIP, "hipEventCreate failed"); \
     }                                                                             \
     SBD_HIP(ctx, expr);                                                           \
-    if ((ctx)->prof) {                                                            \
-      SBD_HIP(ctx, hipEventRecord(eb_, (ctx)->stream));                           \
-      (ctx)->recs.push_back(sbd_ctx::Rec{kind, ea_, eb_});                        \
-    }                                                                             \
+    if ((ctx)->prof) (ctx)->recs.push_back(sbd_ctx::Rec{kind, ex.start, ex.stop}); \
   } while (0)
 
 int pick_splits(int64_t work_groups_per_split, int nblocks) {
@@ -217,7 +221,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   const SeqParam* dseqs = c->at<SeqParam>(L.seqs);
 
   EmbedArgs ea{drows, M, d, c->embed, c->layers[0].attn_norm, x, xn, xn_lo, sumsq};
-  SBD_LAUNCH(c, SBD_KERNEL_EMBED, launch_embed(ea, c->stream));
+  SBD_LAUNCH(c, SBD_KERNEL_EMBED, launch_embed(ea, ex));
 
   int max_end = 0;
   for (const SeqParam& s : seqs) max_end = std::max(max_end, s.cache_len + k);
@@ -230,13 +234,13 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
 
   for (int l = 0; l < m.n_layers; ++l) {
     const LayerW& w = c->layers[l];
+    const bf16_t* wp = c->at<bf16_t>(L.wpack) + (int64_t)l * L.wp_layer;
     GemmArgs g{};
     g.A = xn; g.A_lo = xn_lo; g.lda = d; g.M = M; g.K = d;
-    g.W0 = w.wq; g.W1 = w.wk; g.W2 = w.wv; g.n0 = qd; g.n1 = nkv * dh;
-    g.n_tiles = (int)(L.n_qkv / 32);
+    g.Wp = wp; g.n_tiles = (int)(L.n_qkv / 16);
     g.out_f32 = qkv; g.ldo = L.n_qkv;
     g.sumsq_in = sumsq; g.n_part = (int)L.n_part; g.inv_d = 1.0f / d; g.eps = m.rms_eps;
-    SBD_LAUNCH(c, SBD_KERNEL_QKV, launch_gemm(EPI_SCALED_STORE, g, c->stream));
+    SBD_LAUNCH(c, SBD_KERNEL_QKV, launch_gemm(EPI_SCALED_STORE, g, ex));
 
     RopeStageArgs ra{};
     ra.rows = drows; ra.seqs = dseqs; ra.M = M; ra.k = k; ra.layer = l;
@@ -245,7 +249,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     ra.qkv = qkv; ra.q_norm = w.q_norm; ra.k_norm = w.k_norm; ra.rope = c->at<float>(L.rope);
     ra.q = q; ra.q_lo = q_lo; ra.kcache = c->at<bf16_t>(L.kcache); ra.vcache = c->at<bf16_t>(L.vcache);
     ra.cap = L.cap; ra.n_slots = m.max_batch;
-    SBD_LAUNCH(c, SBD_KERNEL_ROPE, launch_rope_stage(ra, c->stream));
+    SBD_LAUNCH(c, SBD_KERNEL_ROPE, launch_rope_stage(ra, ex));
 
     AttnArgs aa{};
     aa.seqs = dseqs; aa.B = B; aa.k = k; aa.layer = l; aa.n_q = nq; aa.n_kv = nkv; aa.d_h = dh;
@@ -253,41 +257,41 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     aa.n_rowblocks = n_rb; aa.n_splits = n_splits; aa.blocks_per_split = bps;
     aa.part_ml = c->at<float>(L.attn_ml); aa.part_o = c->at<float>(L.attn_o); aa.out = attn;
     aa.out_lo = attn_lo;
-    SBD_LAUNCH(c, SBD_KERNEL_ATTENTION, launch_attention_split(aa, c->stream));
-    SBD_LAUNCH(c, SBD_KERNEL_ATTN_MERGE, launch_attention_merge(aa, c->stream));
+    SBD_LAUNCH(c, SBD_KERNEL_ATTENTION, launch_attention_split(aa, ex));
+    SBD_LAUNCH(c, SBD_KERNEL_ATTN_MERGE, launch_attention_merge(aa, ex));
 
     GemmArgs go{};
     go.A = attn; go.A_lo = attn_lo; go.lda = qd; go.M = M; go.K = qd;
-    go.W0 = w.wo; go.n0 = d; go.n1 = 0; go.n_tiles = d / 32;
+    go.Wp = wp + L.wp_o; go.n_tiles = d / 16;
     go.x = x; go.ldx = d; go.xn = xn; go.xn_lo = xn_lo; go.g_next = w.mlp_norm; go.sumsq_out = sumsq;
     go.n_part = (int)L.n_part;
-    SBD_LAUNCH(c, SBD_KERNEL_O_PROJ, launch_gemm(EPI_RESID, go, c->stream));
+    SBD_LAUNCH(c, SBD_KERNEL_O_PROJ, launch_gemm(EPI_RESID, go, ex));
 
     GemmArgs gu{};
     gu.A = xn; gu.A_lo = xn_lo; gu.lda = d; gu.M = M; gu.K = d;
-    gu.W0 = w.w_gate; gu.W1 = w.w_up; gu.n_tiles = m.ffn_dim / 16;
+    gu.Wp = wp + L.wp_gu; gu.n_tiles = m.ffn_dim / 8;
     gu.sumsq_in = sumsq; gu.n_part = (int)L.n_part; gu.inv_d = 1.0f / d; gu.eps = m.rms_eps;
     gu.act = act; gu.act_lo = act_lo; gu.ld_act = m.ffn_dim;
-    SBD_LAUNCH(c, SBD_KERNEL_GATE_UP, launch_gemm(EPI_SWIGLU, gu, c->stream));
+    SBD_LAUNCH(c, SBD_KERNEL_GATE_UP, launch_gemm(EPI_SWIGLU, gu, ex));
 
     GemmArgs gd{};
     gd.A = act; gd.A_lo = act_lo; gd.lda = m.ffn_dim; gd.M = M; gd.K = m.ffn_dim;
-    gd.W0 = w.w_down; gd.n0 = d; gd.n1 = 0; gd.n_tiles = d / 32;
+    gd.Wp = wp + L.wp_down; gd.n_tiles = d / 16;
     gd.x = x; gd.ldx = d; gd.xn = xn; gd.xn_lo = xn_lo;
     gd.g_next = (l + 1 < m.n_layers) ? c->layers[l + 1].attn_norm : c->final_norm;
     gd.sumsq_out = sumsq; gd.n_part = (int)L.n_part;
-    SBD_LAUNCH(c, SBD_KERNEL_DOWN, launch_gemm(EPI_RESID, gd, c->stream));
+    SBD_LAUNCH(c, SBD_KERNEL_DOWN, launch_gemm(EPI_RESID, gd, ex));
   }
 
   if (logits != nullptr) {
     GemmArgs gl{};
     const int r0 = lm_row < 0 ? 0 : lm_row;
     gl.A = xn + (int64_t)r0 * d; gl.A_lo = xn_lo + (int64_t)r0 * d; gl.lda = d; gl.M = lm_row < 0 ? M : 1; gl.K = d;
-    gl.W0 = c->lm_head; gl.n0 = m.vocab; gl.n1 = 0; gl.n_tiles = m.vocab / 32;
+    gl.Wp = c->at<bf16_t>(L.wpack) + L.wp_lm; gl.n_tiles = m.vocab / 16;
     gl.out_f32 = logits; gl.ldo = m.vocab;
     gl.sumsq_in = sumsq + (int64_t)r0 * L.n_part; gl.n_part = (int)L.n_part;
     gl.inv_d = 1.0f / d; gl.eps = m.rms_eps;
-    SBD_LAUNCH(c, SBD_KERNEL_LM_HEAD, launch_gemm(EPI_SCALED_STORE, gl, c->stream));
+    SBD_LAUNCH(c, SBD_KERNEL_LM_HEAD, launch_gemm(EPI_SCALED_STORE, gl, ex));
   }
   return SBD_OK;
 }
@@ -406,11 +410,27 @@ sbd_status sbd_create(const sbd_model_config* cfg, const sbd_weights* w, void* w
       return cleanup(SBD_ERR_HIP);
     }
   }
-  // Zero the KV cache once so never-written slots hold finite values.
+  // Zero the KV cache once so never-written slots hold finite values; build the RoPE
+  // table; repack every weight matrix into the GEMM's fragment order.
   const size_t kv_bytes = L.rope - L.kcache;
-  if (hipMemsetAsync(c->ws + L.kcache, 0, kv_bytes, c->stream) != hipSuccess ||
-      launch_rope_table(c->at<float>(L.rope), L.cap, cfg->head_dim, (double)cfg->rope_theta,
-                        c->stream) != hipSuccess) {
+  bool ok = hipMemsetAsync(c->ws + L.kcache, 0, kv_bytes, c->stream) == hipSuccess &&
+            launch_rope_table(c->at<float>(L.rope), L.cap, cfg->head_dim, (double)cfg->rope_theta,
+                              c->stream) == hipSuccess;
+  const int d = cfg->d_model, F = cfg->ffn_dim;
+  const int qd = cfg->n_q_heads * cfg->head_dim, kvd = cfg->n_kv_heads * cfg->head_dim;
+  for (int l = 0; ok && l < cfg->n_layers; ++l) {
+    const LayerW& lw = c->layers[l];
+    bf16_t* wp = c->at<bf16_t>(L.wpack) + (int64_t)l * L.wp_layer;
+    ok = launch_pack(lw.wq, nullptr, wp, qd, d, 0, c->stream) == hipSuccess &&
+         launch_pack(lw.wk, nullptr, wp + (int64_t)qd * d, kvd, d, 0, c->stream) == hipSuccess &&
+         launch_pack(lw.wv, nullptr, wp + (int64_t)(qd + kvd) * d, kvd, d, 0, c->stream) == hipSuccess &&
+         launch_pack(lw.wo, nullptr, wp + L.wp_o, d, qd, 0, c->stream) == hipSuccess &&
+         launch_pack(lw.w_gate, lw.w_up, wp + L.wp_gu, 2 * (int64_t)F, d, 1, c->stream) == hipSuccess &&
+         launch_pack(lw.w_down, nullptr, wp + L.wp_down, d, F, 0, c->stream) == hipSuccess;
+  }
+  ok = ok && launch_pack(c->lm_head, nullptr, c->at<bf16_t>(L.wpack) + L.wp_lm, cfg->vocab, d, 0,
+                         c->stream) == hipSuccess;
+  if (!ok) {
     c->err = "initialising the workspace failed";
     return cleanup(SBD_ERR_HIP);
   }
@@ -577,8 +597,8 @@ sbd_status sbd_eb_select(sbd_ctx* c, int32_t batch, int32_t k, int32_t vocab, co
   a.part = c->at<double>(c->lay.eb_part); a.part_arg = c->at<int32_t>(c->lay.eb_arg);
   a.n_accepted = n_accepted; a.accepted_pos = accepted_pos; a.accepted_tok = accepted_tok;
   a.entropy_out = entropy;
-  SBD_LAUNCH(c, SBD_KERNEL_EB_PARTIAL, launch_eb_partial(a, c->stream));
-  SBD_LAUNCH(c, SBD_KERNEL_EB_SELECT, launch_eb_select(a, false, c->stream));
+  SBD_LAUNCH(c, SBD_KERNEL_EB_PARTIAL, launch_eb_partial(a, ex));
+  SBD_LAUNCH(c, SBD_KERNEL_EB_SELECT, launch_eb_select(a, false, ex));
   return SBD_OK;
 }
 
@@ -592,7 +612,7 @@ sbd_status sbd_eb_select_entropies(sbd_ctx* c, int32_t batch, int32_t k, const d
   EbArgs a{};
   a.B = batch; a.k = k; a.is_mask = c->at<uint8_t>(c->lay.eb_mask); a.entropy_in = entropy;
   a.gamma = gamma; a.n_accepted = n_accepted; a.accepted_pos = accepted_pos;
-  SBD_LAUNCH(c, SBD_KERNEL_EB_SELECT, launch_eb_select(a, true, c->stream));
+  SBD_LAUNCH(c, SBD_KERNEL_EB_SELECT, launch_eb_select(a, true, ex));
   return SBD_OK;
 }
 

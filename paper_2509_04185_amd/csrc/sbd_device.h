@@ -2,7 +2,14 @@
 // reductions.  Included only by *.hip files.
 #pragma once
 
+#include <hip/hip_ext.h>
+
 #include "sbd_internal.h"
+
+// Launch on ex.s; the runtime records ex.start / ex.stop (when set) at the kernel's
+// start and end.
+#define SBD_KLAUNCH(kernel, grid, block, ex, ...) \
+  hipExtLaunchKernelGGL(kernel, grid, block, 0, (ex).s, (ex).start, (ex).stop, 0, __VA_ARGS__)
 
 namespace sbd {
 

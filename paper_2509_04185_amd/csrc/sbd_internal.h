@@ -19,6 +19,14 @@ constexpr int kMaxSplits = 64;      // split-KV partitions per (sequence, KV hea
 constexpr int kEbChunk = 4096;      // vocabulary entries per EB partial workgroup
 constexpr int kMaxBlock = 64;       // largest block size k
 
+// Where a kernel is enqueued: the stream, plus optional start/stop events that the
+// runtime records at the kernel's own start and end (per-kernel timing).
+struct Exec {
+  hipStream_t s;
+  hipEvent_t start;
+  hipEvent_t stop;
+};
+
 // Per-row parameters of one forward (row m = b * k + j).
 struct RowParam {
   int32_t tok;   // token id
@@ -41,6 +49,9 @@ struct Layout {
   int64_t n_part;         // d_model / 16 sum-of-squares partials per row
   int64_t eb_chunks;      // ceil(vocab / kEbChunk)
   size_t kcache, vcache, rope, x, xn, sumsq, qkv, q, attn, act;
+  size_t wpack;              // packed weights (see gemm.hip), element offsets below
+  int64_t wp_layer;          // elements per layer: qkv, then o, then gate/up, then down
+  int64_t wp_o, wp_gu, wp_down, wp_lm;
   size_t attn_ml, attn_o, rows, seqs, eb_mask, eb_part, eb_arg;
   size_t total;
 };
@@ -60,17 +71,14 @@ enum GemmEpi { EPI_SCALED_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
 // together carry about 16 significant bits; products with bf16 weights are exact in the
 // fp32 accumulators, so a GEMM over (hi, lo) loses only the lo truncation.
 //
-// y[m][n] = sum_k A[m][k] * W[n][k] over the row-major [out][in] weight segments.
+// y[m][n] = sum_k A[m][k] * W[n][k] with W in the packed fragment order of gemm.hip.
 struct GemmArgs {
   const bf16_t* A;     // hi part [M][K], row stride lda
   const bf16_t* A_lo;  // lo part, same layout
   int64_t lda;
   int M, K;
-  const bf16_t* W0;  // segment 0 (or gate)
-  const bf16_t* W1;  // segment 1 (or up)
-  const bf16_t* W2;  // segment 2
-  int n0, n1;                // rows of segments 0 and 1 (segment 2 takes the rest)
-  int n_tiles;               // number of 32-column output tiles
+  const bf16_t* Wp;    // packed weights
+  int n_tiles;         // 16-row tiles of the packed matrix
   // EPI_SCALED_STORE: out[m][n] = rinv[m] * y (rinv = 1 when sumsq_in == nullptr)
   float* out_f32;
   int64_t ldo;
@@ -91,7 +99,11 @@ struct GemmArgs {
   int64_t ld_act;
 };
 
-hipError_t launch_gemm(GemmEpi epi, const GemmArgs& a, hipStream_t s);
+hipError_t launch_gemm(GemmEpi epi, const GemmArgs& a, const Exec& ex);
+// Repack a row-major [rows][K] matrix (mode 0) or a gate/up pair (mode 1, rows = 2 * F
+// packed rows) into the fragment order read by gemm_kernel.
+hipError_t launch_pack(const bf16_t* src0, const bf16_t* src1, bf16_t* dst, int64_t rows, int K,
+                       int mode, hipStream_t s);
 
 // ---------------------------------------------------------------------------- misc kernels
 struct EmbedArgs {
@@ -104,7 +116,7 @@ struct EmbedArgs {
   bf16_t* xn_lo;
   float* sumsq;  // [M][d/16]
 };
-hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
+hipError_t launch_embed(const EmbedArgs& a, const Exec& ex);
 
 struct RopeStageArgs {
   const RowParam* rows;
@@ -125,7 +137,7 @@ struct RopeStageArgs {
   int64_t cap;
   int n_slots;
 };
-hipError_t launch_rope_stage(const RopeStageArgs& a, hipStream_t s);
+hipError_t launch_rope_stage(const RopeStageArgs& a, const Exec& ex);
 
 hipError_t launch_rope_table(float* rope, int64_t cap, int d_h, double theta, hipStream_t s);
 
@@ -162,8 +174,8 @@ struct AttnArgs {
   bf16_t* out;     // [B*k][n_q*d_h] hi
   bf16_t* out_lo;  // lo
 };
-hipError_t launch_attention_split(const AttnArgs& a, hipStream_t s);
-hipError_t launch_attention_merge(const AttnArgs& a, hipStream_t s);
+hipError_t launch_attention_split(const AttnArgs& a, const Exec& ex);
+hipError_t launch_attention_merge(const AttnArgs& a, const Exec& ex);
 
 // ---------------------------------------------------------------------------- EB sampler
 struct EbArgs {
@@ -180,7 +192,7 @@ struct EbArgs {
   int32_t* accepted_tok;    // [B][k] or null
   double* entropy_out;      // [B][k] or null
 };
-hipError_t launch_eb_partial(const EbArgs& a, hipStream_t s);
-hipError_t launch_eb_select(const EbArgs& a, bool select_only, hipStream_t s);
+hipError_t launch_eb_partial(const EbArgs& a, const Exec& ex);
+hipError_t launch_eb_select(const EbArgs& a, bool select_only, const Exec& ex);
 
 }  // namespace sbd

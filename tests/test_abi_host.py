@@ -54,7 +54,9 @@ def test_workspace_bytes_for_every_workload(name):
     s = w.shape
     cap = (max(w.cache_lens()) + 64 + 63) // 64 * 64
     kv = 2 * s.n_layers * w.batch * s.n_kv_heads * cap * s.head_dim * 2
-    assert kv < n < kv + 2 * 2**30
+    qd, kvd, d, F = s.n_q_heads * s.head_dim, s.n_kv_heads * s.head_dim, s.d_model, s.ffn_dim
+    weights = 2 * (s.n_layers * ((qd + 2 * kvd) * d + d * qd + 3 * F * d) + s.vocab * d)
+    assert kv + weights < n < kv + weights + 2 * 2**30
 
 
 @pytest.mark.parametrize("field,value", [("head_dim", 96), ("d_model", 200), ("vocab", 1000),
