@@ -55,8 +55,9 @@ def gate_up_bytes(shape, M):
 
 def source_hash():
     h = hashlib.sha256()
-    with open(os.path.join(ROOT, "paper_2509_04185_amd", "csrc", "gemm.hip"), "rb") as f:
-        h.update(f.read())
+    for name in ("gemv.hip", "sbd_device.h"):
+        with open(os.path.join(ROOT, "paper_2509_04185_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
     return h.hexdigest()[:16]
 
 
@@ -191,11 +192,11 @@ def main():
         if os.path.exists(TRAFFIC_FILE):
             with open(TRAFFIC_FILE) as f:
                 tr = json.load(f)
-            if tr.get("gemm_source") == source_hash():
+            if tr.get("kernel_source") == source_hash():
                 traffic = tr.get("bytes_per_launch")
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                     "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-                    "kernel": "gemm_kernel<1,2,4,8,EPI_SWIGLU> (gate/up projection + SwiGLU)",
+                    "kernel": "gemv_kernel<8,4,1,EPI_SWIGLU> (gate/up projection + SwiGLU)",
                     "bytes_per_launch": bpl, "avg_launch_us": round(avg_s * 1e6, 2),
                     "launches": c}
 

@@ -48,7 +48,8 @@ typedef struct sbd_ctx sbd_ctx; /* opaque, created by sbd_create */
  * changes, Sec. 1) plus capacity limits.
  *   n_q_heads % n_kv_heads == 0; query head h reads KV head h / (n_q_heads/n_kv_heads).
  *   head_dim is 64 or 128.  d_model, n_q_heads*head_dim and ffn_dim are multiples of 256;
- *   vocab is a multiple of 32.  mask_id in [0, vocab) is the input-only mask token 'm'.
+ *   vocab and (n_q_heads + 2 n_kv_heads) * head_dim are multiples of 128.  mask_id in
+ *   [0, vocab) is the input-only mask token 'm'.
  *   qk_norm != 0 enables the per-head RMSNorm of q and k before RoPE (Qwen-3).
  *   max_batch: number of sequence slots (ids 0..max_batch-1).
  *   max_seq_len: tokens per slot, including the k rows staged by a block forward.

@@ -3,19 +3,23 @@
 // The block forward multiplies M = batch * k activation rows (16 at batch 1, k = 16) by
 // every weight matrix of the decoder, so it is bound by streaming the weights from HBM.
 //
-// Weights are repacked once (pack_kernel) into MFMA fragment order: a matrix with N rows
-// and K columns becomes [N/16 tiles][K/32 steps][64 lanes][8], the 16-byte piece of lane
-// l in step s of tile t holding W[16t + l%16][32s + 8(l/16) .. +8].  One 16-byte load per
-// lane then reads 1 KB of contiguous memory and lands directly in the B operand of
-// v_mfma_f32_16x16x32_bf16.  The gate and up projections share one packed matrix whose
-// tile t holds gate rows 8t..8t+7 followed by up rows 8t..8t+7, so SwiGLU pairs stay
-// inside one tile.
+// Weights are repacked once (pack_kernel) into MFMA fragment order.  A matrix with N rows
+// and K columns is cut into 16-row tiles; the 16-byte piece of lane l in step s of tile t
+// holds W[16t + l%16][32s + 8(l/16) .. +8], so one 16-byte load per lane reads a 1 KB
+// fragment that lands directly in the B operand of v_mfma_f32_16x16x32_bf16.  Tiles are
+// grouped by 8 (128 rows) and a group's 8 fragments of one step are stored together:
+// [N/128 groups][K/32 steps][8 tiles][64 lanes][8] (packed_frag() in sbd_device.h), so a
+// decode-sized GEMM reading several tiles of a group per step reads contiguous memory.
+// The gate and up projections share one packed matrix whose tile t holds gate rows
+// 8t..8t+7 followed by up rows 8t..8t+7, so SwiGLU pairs stay inside one tile.
 //
-// Each workgroup owns C consecutive tiles (16*C output columns) and a row block; its NW
-// waves split the K/32 steps and stream disjoint contiguous ranges with non-temporal
-// loads, double-buffered in registers.  The activations come as hi/lo bf16 pairs (two
-// MFMAs per step, see GemmArgs).  Partial sums meet in LDS and are added in a fixed wave
-// order (deterministic); the epilogue applies what follows the product in the block:
+// This kernel serves M > 16 (prefill chunks, large batches); decode-sized products go
+// through gemv.hip.  Each workgroup owns C consecutive tiles (16*C output columns) and a
+// row block; its NW waves split the K/32 steps and stream disjoint contiguous ranges with
+// non-temporal loads, double-buffered in registers.  The activations come as hi/lo bf16
+// pairs (two MFMAs per step, see GemmArgs).  Partial sums meet in LDS and are added in a
+// fixed wave order (deterministic); the epilogue applies what follows the product in the
+// block:
 //   EPI_SCALED_STORE  out = rinv[m] * y           (QKV projection, LM head)
 //   EPI_RESID         x += y; xn = x * g_next as hi/lo; per-row sums of x^2 over each 16
 //                     columns (O and down projections: residual add, the next RMSNorm's
@@ -50,8 +54,8 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(GemmArgs a) {
   const int K = a.K;
 
   // This wave's share of the K/32 steps.
-  const int S = K / 32;
-  const int base_steps = S / NW, rem = S % NW;
+  const int S_all = K / 32;
+  const int base_steps = S_all / NW, rem = S_all % NW;
   const int s0 = w * base_steps + (w < rem ? w : rem);
   const int ns = base_steps + (w < rem ? 1 : 0);
   const int kbase = s0 * 32 + g * 8;
@@ -59,7 +63,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(GemmArgs a) {
   const bf16_t* wbase[C];
 #pragma unroll
   for (int ct = 0; ct < C; ++ct)
-    wbase[ct] = a.Wp + ((int64_t)(tile * C + ct) * S + s0) * 512 + lane * 8;
+    wbase[ct] = a.Wp + packed_frag(tile * C + ct, s0, S_all) + lane * 8;
   const bf16_t* arow[MT];
   const bf16_t* arow_lo[MT];
 #pragma unroll
@@ -82,7 +86,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(GemmArgs a) {
   _Pragma("unroll") for (int u = 0; u < U; ++u) {                                 \
     const int st_ = (STEP) + u;                                                   \
     _Pragma("unroll") for (int ct = 0; ct < C; ++ct)                              \
-      WB[u][ct] = ld16_stream(wbase[ct] + (int64_t)st_ * 512);                    \
+      WB[u][ct] = ld16_stream(wbase[ct] + (int64_t)st_ * kPackStep);              \
     _Pragma("unroll") for (int mt = 0; mt < MT; ++mt) {                           \
       AB[u][mt] = ld16(arow[mt] + st_ * 32);                                      \
       AL[u][mt] = ld16(arow_lo[mt] + st_ * 32);                                   \
@@ -124,7 +128,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(GemmArgs a) {
   for (int st = nchunks * U; st < ns; ++st) {
     i32x4 wv[C];
 #pragma unroll
-    for (int ct = 0; ct < C; ++ct) wv[ct] = ld16_stream(wbase[ct] + (int64_t)st * 512);
+    for (int ct = 0; ct < C; ++ct) wv[ct] = ld16_stream(wbase[ct] + (int64_t)st * kPackStep);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const i32x4 av = ld16(arow[mt] + st * 32);
@@ -147,20 +151,27 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(GemmArgs a) {
       for (int i = 0; i < 4; ++i) red[w][mt * 16 + 4 * g + i][16 * ct + r] = acc[mt][ct][i];
   __syncthreads();
 
-  // Epilogue: thread idx -> (row idx / NC, column idx % NC); each 16-lane group holds
-  // the 16 columns of one tile of one row.
+  // Sum the waves' partial tiles into red[0] (fixed wave order).
   constexpr int TOTAL = MT * 16 * NC;
   constexpr int STRIDE = NW * 64;
+  for (int idx = threadIdx.x; idx < TOTAL; idx += STRIDE) {
+    const int rr = idx / NC, col = idx % NC;
+    float y = red[0][rr][col];
+#pragma unroll
+    for (int w2 = 1; w2 < NW; ++w2) y += red[w2][rr][col];
+    red[0][rr][col] = y;
+  }
+
+  __syncthreads();
+
+  // Epilogue: thread idx -> (row idx / NC, column idx % NC); each 16-lane group holds
+  // the 16 columns of one tile of one row.
   for (int idx = threadIdx.x; idx < (TOTAL + STRIDE - 1) / STRIDE * STRIDE; idx += STRIDE) {
     const bool in = idx < TOTAL;
     const int rr = in ? idx / NC : 0, col = idx % NC;
     const int m = row0 + rr;
     const bool ok = in && m < a.M;
-    float y = 0.f;
-    if (in) {
-#pragma unroll
-      for (int w2 = 0; w2 < NW; ++w2) y += red[w2][rr][col];
-    }
+    const float y = in ? red[0][rr][col] : 0.f;
     if (EPI == EPI_SCALED_STORE) {
       if (ok) a.out_f32[(int64_t)m * a.ldo + tile * NC + col] = y * rinv_s[rr];
     } else if (EPI == EPI_RESID) {
@@ -184,11 +195,8 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(GemmArgs a) {
     } else {  // EPI_SWIGLU: column c < 8 of a tile is gate j, column c + 8 the matching up
       const int c = col & 15;
       if (ok && c < 8) {
-        float yu = 0.f;
-#pragma unroll
-        for (int w2 = 0; w2 < NW; ++w2) yu += red[w2][rr][col + 8];
         const float gt = y * rinv_s[rr];
-        const float up = yu * rinv_s[rr];
+        const float up = red[0][rr][col + 8] * rinv_s[rr];
         const float sg = gt / (1.0f + expf(-gt));
         const int j = (tile * C + (col >> 4)) * 8 + c;
         bf16_t hi, lo;
@@ -206,45 +214,28 @@ static void launch_cfg(const GemmArgs& a, const Exec& ex) {
   SBD_KLAUNCH((gemm_kernel<MT, C, NW, U, EPI>), grid, dim3(NW * 64), ex, a);
 }
 
-// Configurations picked from a sweep over the decode shapes of the 8B models (M = 16):
-// many tiles (LM head, gate/up, QKV) favour two tiles per workgroup and 4 K-waves; the
-// 4096-column projections favour one tile and 8 K-waves (more workgroups in flight).
 template <int EPI>
 static hipError_t launch_epi(const GemmArgs& a, const Exec& ex) {
-  const bool even = a.n_tiles % 2 == 0;
-  if (a.M <= 16) {
-    if (even && a.n_tiles >= 4096)
-      launch_cfg<1, 2, 4, 4, EPI>(a, ex);
-    else if (even && a.n_tiles >= 384)
-      launch_cfg<1, 2, 4, 8, EPI>(a, ex);
-    else if (a.K > 8192)
-      launch_cfg<1, 1, 8, 4, EPI>(a, ex);
-    else
-      launch_cfg<1, 1, 8, 8, EPI>(a, ex);
-  } else if (a.M <= 32) {
-    if (even)
-      launch_cfg<2, 2, 8, 4, EPI>(a, ex);
-    else
-      launch_cfg<2, 1, 8, 4, EPI>(a, ex);
-  } else {
-    if (even)
-      launch_cfg<4, 2, 4, 2, EPI>(a, ex);
-    else
-      launch_cfg<4, 1, 4, 2, EPI>(a, ex);
-  }
+  if (a.M <= 16)
+    launch_cfg<1, 2, 4, 4, EPI>(a, ex);
+  else if (a.M <= 32)
+    launch_cfg<2, 2, 8, 4, EPI>(a, ex);
+  else
+    launch_cfg<4, 2, 4, 2, EPI>(a, ex);
   return hipGetLastError();
 }
 
 hipError_t launch_gemm(GemmEpi epi, const GemmArgs& a, const Exec& ex) {
+  if (a.M < 1 || a.K < 32 || a.K % 32 || a.n_tiles % 8) return hipErrorInvalidValue;
   switch (epi) {
     case EPI_SCALED_STORE: return launch_epi<EPI_SCALED_STORE>(a, ex);
     case EPI_RESID: return launch_epi<EPI_RESID>(a, ex);
     case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(a, ex);
+    default: return hipErrorInvalidValue;
   }
-  return hipErrorInvalidValue;
 }
 
-// One thread per 16-byte piece of the packed matrix (see the top of this file).
+// One thread per 16-byte piece of the packed matrix (layout at the top of this file).
 // Mode 0: packed row n is src0 row n.  Mode 1 (gate/up): packed tile t holds src0 rows
 // 8t..8t+7 then src1 rows 8t..8t+7.
 __global__ __launch_bounds__(256) void pack_kernel(const bf16_t* src0, const bf16_t* src1,
@@ -253,8 +244,9 @@ __global__ __launch_bounds__(256) void pack_kernel(const bf16_t* src0, const bf1
   if (i >= n_pieces) return;
   const int S = K / 32;
   const int lane = (int)(i % 64);
-  const int64_t s = (i / 64) % S;
-  const int64_t t = i / (64 * (int64_t)S);
+  const int64_t tt = (i / 64) % 8;            // tile inside the group
+  const int64_t s = (i / 512) % S;            // K step
+  const int64_t t = (i / (512 * (int64_t)S)) * 8 + tt;
   const int rr = lane & 15;
   const int64_t k0 = 32 * s + 8 * (lane >> 4);
   const bf16_t* row;
@@ -267,6 +259,7 @@ __global__ __launch_bounds__(256) void pack_kernel(const bf16_t* src0, const bf1
 
 hipError_t launch_pack(const bf16_t* src0, const bf16_t* src1, bf16_t* dst, int64_t rows, int K,
                        int mode, hipStream_t s) {
+  if (rows % 128 || K % 32) return hipErrorInvalidValue;
   const int64_t n_pieces = rows * K / 8;
   hipLaunchKernelGGL(pack_kernel, dim3((unsigned)((n_pieces + 255) / 256)), dim3(256), 0, s, src0,
                      src1, dst, n_pieces, K, mode);

@@ -1,0 +1,369 @@
+// Decode-sized GEMM (M <= 16 rows): y[m][n] = sum_k A[m][k] W[n][k].
+//
+// At M <= 16 every projection of the block forward is a stream of its weights from HBM.
+// The kernel is shaped by three measured costs: bytes in flight per CU, the activation
+// fragments re-read for every weight fragment, and the fixed latency at the start and end
+// of a launch.
+//   - A workgroup owns C tiles (C = 4 or 8) of one packed group (gemm.hip: a group's 8
+//     fragments of one K step are 8 KB of contiguous memory) and a K range; a K step then
+//     reads C KB of weights against 2 KB of activation fragments (hi and lo).
+//   - Its NW waves split the K range.  A wave issues the loads of U steps before the first
+//     MFMA that consumes them: a scheduling barrier keeps the compiler from interleaving
+//     loads and MFMAs, which would leave only a few loads in flight.
+//   - The NW partial tiles are added in LDS in wave order.  When the K range is split over
+//     KS workgroups (grid y), each parks its partial tiles with device-coherent stores and
+//     the last to arrive adds the KS slices in order and runs the epilogue.  Results are
+//     deterministic; no workgroup waits for another.
+//
+// Epilogues (acc in the v_mfma_f32_16x16x32_bf16 D layout: lane l holds column l % 16 of
+// a tile, rows 4*(l/16) + i):
+//   EPI_SCALED_STORE  out = rinv[m] * y                      (LM head)
+//   EPI_RESID         x += y; xn = x * g_next as hi/lo bf16; per-tile sums of x^2; the
+//                     last workgroup to finish turns them into rinv_out[m] =
+//                     1/sqrt(mean(x^2) + eps) for the next RMSNorm (O, down projections)
+//   EPI_SWIGLU        act = silu(rinv*gate) * rinv*up as hi/lo (gate/up: packed tile t
+//                     holds gate rows 8t..8t+7 then up rows 8t..8t+7)
+//   EPI_QKV           C = 8 (128 columns = whole heads): per-head q/k RMSNorm, rotate-half
+//                     RoPE, q as scaled hi/lo, K and V into the cache at cache_len + j
+// Activations are hi/lo bf16 pairs: two MFMAs per step, exact products in fp32.
+
+#include "sbd_device.h"
+
+namespace sbd {
+
+// QKV epilogue of one packed group (8 tiles = 128 columns = 128 / DH whole heads), run by
+// one wave holding all 8 accumulator tiles.
+template <int DH>
+__device__ __forceinline__ void qkv_epilogue(const GemvArgs& a, int grp, const f32x4 (&acc)[8],
+                                             const float (&rinv)[4]) {
+  constexpr int tph = DH / 16, ptiles = tph / 2, half = DH / 2, heads = 8 / tph;
+  const QkvEpi& e = a.qkv;
+  const int lane = threadIdx.x & 63;
+  const int r = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = 4 * g + i;
+    const bool row_ok = m < a.M;
+    const float rv = row_ok ? rinv[i] : 0.f;
+    float u[8];
+#pragma unroll
+    for (int ct = 0; ct < 8; ++ct) u[ct] = acc[ct][i] * rv;
+#pragma unroll
+    for (int hh = 0; hh < heads; ++hh) {
+      const int h = grp * heads + hh;  // q heads, then k heads, then v heads
+      if (e.qk_norm && h < e.n_q + e.n_kv) {
+        float ss = 0.f;
+#pragma unroll
+        for (int t = 0; t < tph; ++t) ss += u[hh * tph + t] * u[hh * tph + t];
+        ss += __shfl_xor(ss, 1);
+        ss += __shfl_xor(ss, 2);
+        ss += __shfl_xor(ss, 4);
+        ss += __shfl_xor(ss, 8);
+        const float rn = 1.0f / sqrtf(ss / (float)DH + e.eps);
+        const bf16_t* gn = h < e.n_q ? e.q_norm : e.k_norm;
+#pragma unroll
+        for (int t = 0; t < tph; ++t) u[hh * tph + t] *= rn * bf2f(gn[16 * t + r]);
+      }
+    }
+    if (!row_ok) continue;
+    const int b = m / e.kblk, j = m % e.kblk;
+    const SeqParam sp = e.seqs[b];
+    const int p_cache = sp.cache_len + j;
+    const int pos = e.rows[m].pos;
+#pragma unroll
+    for (int hh = 0; hh < heads; ++hh) {
+      const int h = grp * heads + hh;
+      if (h >= e.n_q + e.n_kv) {  // V: transposed cache block, slot order of misc.hip vslot()
+        const int gk = h - e.n_q - e.n_kv;
+        bf16_t* blk = e.vcache + (((int64_t)e.layer * e.n_slots + sp.slot) * e.n_kv + gk) * e.cap * DH +
+                      (int64_t)(p_cache / 32) * DH * 32;
+        const int p = p_cache & 31;
+        const int sl = ((p & 15) >> 2) * 8 + (p >> 4) * 4 + (p & 3);
+#pragma unroll
+        for (int t = 0; t < tph; ++t) blk[(16 * t + r) * 32 + sl] = f2bf(u[hh * tph + t]);
+        continue;
+      }
+#pragma unroll
+      for (int pr = 0; pr < ptiles; ++pr) {
+        const int dim = pr * 16 + r;
+        const float cs = e.rope[((int64_t)pos * half + dim) * 2 + 0];
+        const float sn = e.rope[((int64_t)pos * half + dim) * 2 + 1];
+        const float u0 = u[hh * tph + pr], u1 = u[hh * tph + pr + ptiles];
+        const float r0 = u0 * cs - u1 * sn;
+        const float r1 = u1 * cs + u0 * sn;
+        if (h < e.n_q) {
+          const int64_t o = ((int64_t)m * e.n_q + h) * DH;
+          bf16_t hi, lo;
+          split_bf16(r0 * e.q_scale, hi, lo);
+          e.q[o + dim] = hi;
+          e.q_lo[o + dim] = lo;
+          split_bf16(r1 * e.q_scale, hi, lo);
+          e.q[o + dim + half] = hi;
+          e.q_lo[o + dim + half] = lo;
+        } else {
+          const int gk = h - e.n_q;
+          bf16_t* dst = e.kcache + (((int64_t)e.layer * e.n_slots + sp.slot) * e.n_kv + gk) * e.cap * DH +
+                        (int64_t)p_cache * DH;
+          dst[dim] = f2bf(r0);
+          dst[dim + half] = f2bf(r1);
+        }
+      }
+    }
+  }
+}
+
+// Tile ct of a workgroup is summed and finished by wave ct % NW.
+template <int NW>
+__device__ __forceinline__ bool owns_tile(int ct, int wave) { return ct % NW == wave; }
+
+template <int C, int NW, int U, int EPI, int DH>
+__global__ __launch_bounds__(NW * 64) void gemv_kernel(GemvArgs a) {
+  static_assert(C == 4 || C == 8, "a workgroup takes half or all of a packed group");
+  static_assert(EPI != EPI_QKV || C == 8, "the QKV epilogue works on whole groups");
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int r = lane & 15, g = lane >> 4;
+  const int sub = blockIdx.x;  // tiles sub*C .. sub*C + C-1
+  const int t0 = sub * C;
+  const int S = a.K / 32;
+  const int KS = gridDim.y, kc = blockIdx.y;
+  const int z0 = (int)((int64_t)S * kc / KS), z1 = (int)((int64_t)S * (kc + 1) / KS);
+  const int s_b = z0 + (z1 - z0) * wave / NW, s_e = z0 + (z1 - z0) * (wave + 1) / NW;
+  const int ns = s_e - s_b;
+
+  // 1/rms of this lane's accumulator rows 4g + i (loaded early, used by the epilogue)
+  float rinv[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = 4 * g + i;
+    rinv[i] = (EPI != EPI_RESID && a.rinv_in != nullptr && m < a.M) ? a.rinv_in[m] : 1.f;
+  }
+
+  const int arow_m = r < a.M ? r : a.M - 1;
+  const bf16_t* ab = a.A + (int64_t)arow_m * a.lda + g * 8 + s_b * 32;
+  const bf16_t* al = a.A_lo + (int64_t)arow_m * a.lda + g * 8 + s_b * 32;
+  const bf16_t* wb = a.Wp + packed_frag(t0, s_b, S) + lane * 8;  // tile t0 + ct at + ct * 512
+
+  f32x4 acc[C];
+#pragma unroll
+  for (int ct = 0; ct < C; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+  int st = 0;
+  for (; st + U <= ns; st += U) {
+    // Activation fragments first (cache hits), then the weight fragments in the order
+    // the MFMAs consume them, so each MFMA waits only for its own loads.
+    i32x4 wv[U][C], xa[U], xl[U];
+#pragma unroll
+    for (int uu = 0; uu < U; ++uu) {
+      xa[uu] = ld16(ab + (st + uu) * 32);
+      xl[uu] = ld16(al + (st + uu) * 32);
+    }
+#pragma unroll
+    for (int uu = 0; uu < U; ++uu)
+#pragma unroll
+      for (int ct = 0; ct < C; ++ct) wv[uu][ct] = ld16_stream(wb + (int64_t)(st + uu) * kPackStep + ct * 512);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int uu = 0; uu < U; ++uu)
+#pragma unroll
+      for (int ct = 0; ct < C; ++ct) {
+        acc[ct] = mfma16x16x32(xa[uu], wv[uu][ct], acc[ct]);
+        acc[ct] = mfma16x16x32(xl[uu], wv[uu][ct], acc[ct]);
+      }
+  }
+  for (; st < ns; ++st) {
+    const i32x4 xa = ld16(ab + st * 32), xl = ld16(al + st * 32);
+    i32x4 wv[C];
+#pragma unroll
+    for (int ct = 0; ct < C; ++ct) wv[ct] = ld16_stream(wb + (int64_t)st * kPackStep + ct * 512);
+#pragma unroll
+    for (int ct = 0; ct < C; ++ct) {
+      acc[ct] = mfma16x16x32(xa, wv[ct], acc[ct]);
+      acc[ct] = mfma16x16x32(xl, wv[ct], acc[ct]);
+    }
+  }
+
+  // ---- the NW partial tiles, added in LDS in wave order
+  if constexpr (NW > 1) {
+    __shared__ f32x4 red[NW][C][64];
+#pragma unroll
+    for (int ct = 0; ct < C; ++ct) red[wave][ct][lane] = acc[ct];
+    __syncthreads();
+#pragma unroll
+    for (int ct = 0; ct < C; ++ct) {
+      if (!owns_tile<NW>(ct, wave)) continue;
+      f32x4 s = red[0][ct][lane];
+      for (int w = 1; w < NW; ++w) s += red[w][ct][lane];
+      acc[ct] = s;
+    }
+  }
+
+  // ---- K split over workgroups: park the slice, the last to arrive adds all in order
+  if (KS > 1) {
+#pragma unroll
+    for (int ct = 0; ct < C; ++ct) {
+      if (!owns_tile<NW>(ct, wave)) continue;
+      float* p = a.part + ((int64_t)kc * a.n_tiles + t0 + ct) * 256 + lane;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) store_coherent(p + i * 64, acc[ct][i]);
+    }
+    if (!last_arrival(a.counters + sub, KS)) return;
+#pragma unroll
+    for (int ct = 0; ct < C; ++ct) {
+      if (!owns_tile<NW>(ct, wave)) continue;
+      f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int z = 0; z < KS; ++z) {
+        const float* p = a.part + ((int64_t)z * a.n_tiles + t0 + ct) * 256 + lane;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) s[i] += load_coherent(p + i * 64);
+      }
+      acc[ct] = s;
+    }
+  }
+
+  // ---- epilogue
+  if constexpr (EPI == EPI_QKV) {
+    if constexpr (NW > 1) {  // gather the group's 8 tiles in wave 0
+      __shared__ f32x4 fin[C][64];
+#pragma unroll
+      for (int ct = 0; ct < C; ++ct)
+        if (owns_tile<NW>(ct, wave)) fin[ct][lane] = acc[ct];
+      __syncthreads();
+      if (wave != 0) return;
+#pragma unroll
+      for (int ct = 0; ct < C; ++ct) acc[ct] = fin[ct][lane];
+    }
+    qkv_epilogue<DH>(a, sub, acc, rinv);
+    return;
+  } else {
+#pragma unroll
+    for (int ct = 0; ct < C; ++ct) {
+      if (!owns_tile<NW>(ct, wave)) continue;
+      const int tile = t0 + ct;
+      if constexpr (EPI == EPI_SCALED_STORE) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int m = 4 * g + i;
+          if (m < a.M) a.out_f32[(int64_t)m * a.ldo + tile * 16 + r] = acc[ct][i] * rinv[i];
+        }
+      } else if constexpr (EPI == EPI_SWIGLU) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int m = 4 * g + i;
+          const float v = acc[ct][i] * (m < a.M ? rinv[i] : 0.f);
+          const float up = __shfl_xor(v, 8);
+          if (r < 8 && m < a.M) {
+            const int jj = tile * 8 + r;
+            bf16_t hi, lo;
+            split_bf16(v / (1.0f + expf(-v)) * up, hi, lo);
+            a.act[(int64_t)m * a.ld_act + jj] = hi;
+            a.act_lo[(int64_t)m * a.ld_act + jj] = lo;
+          }
+        }
+      } else {  // EPI_RESID
+        const int n = tile * 16 + r;
+        const float gn = bf2f(a.g_next[n]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int m = 4 * g + i;
+          float xv = 0.f;
+          if (m < a.M) {
+            float* xp = a.x + (int64_t)m * a.ldx + n;
+            xv = *xp + acc[ct][i];
+            *xp = xv;
+            bf16_t hi, lo;
+            split_bf16(xv * gn, hi, lo);
+            a.xn[(int64_t)m * a.ldx + n] = hi;
+            a.xn_lo[(int64_t)m * a.ldx + n] = lo;
+          }
+          float s2 = xv * xv;
+          s2 += __shfl_xor(s2, 1);
+          s2 += __shfl_xor(s2, 2);
+          s2 += __shfl_xor(s2, 4);
+          s2 += __shfl_xor(s2, 8);
+          if (r == 0 && m < a.M) store_coherent(a.sumsq + (int64_t)m * a.n_part + tile, s2);
+        }
+      }
+    }
+  }
+
+  if constexpr (EPI == EPI_RESID) {
+    // The last workgroup to finish its epilogue turns the per-tile sums into 1/rms per
+    // row: wave w takes rows w, w + NW, ...
+    if (!last_arrival(a.counters + gridDim.x, (int)gridDim.x)) return;
+    for (int m = wave; m < a.M; m += NW) {
+      float s = 0.f;
+      for (int p = lane; p < a.n_part; p += 64) s += load_coherent(a.sumsq + (int64_t)m * a.n_part + p);
+      s = wave_sum(s);
+      if (lane == 0) a.rinv_out[m] = 1.0f / sqrtf(s * a.inv_d + a.eps);
+    }
+  }
+}
+
+template <int C, int NW, int U, int EPI, int DH = 128>
+static void launch_gemv_cfg(const GemvArgs& a, int KS, const Exec& ex) {
+  SBD_KLAUNCH((gemv_kernel<C, NW, U, EPI, DH>), dim3((unsigned)(a.n_tiles / C), (unsigned)KS), dim3(NW * 64),
+              ex, a);
+}
+
+// Launch shapes from sweeps over the 8B decode shapes (M = 16).  Many tiles (LM head,
+// gate/up): whole groups, few waves per workgroup, no split.  A few hundred tiles (QKV, O,
+// down): the K range is split over workgroups until about one workgroup per CU streams,
+// keeping at least 8 K steps per workgroup.
+GemvShape gemv_pick(GemmEpi epi, int n_tiles, int K) {
+  (void)epi;
+  const int groups = n_tiles / 8, S = K / 32;
+  if (groups >= 512) return GemvShape{8, 1, 1, 1};
+  if (groups >= 192) return GemvShape{8, 4, 1, 1};
+  int KS = 1;
+  while (2 * KS * groups <= 256 && 2 * KS <= kGemvMaxSplit && S / (2 * KS) >= 8) KS *= 2;
+  return GemvShape{8, S / KS >= 16 ? 16 : 8, 1, KS};
+}
+
+template <int EPI, int DH = 128>
+static bool dispatch(const GemvArgs& a, GemvShape sh, const Exec& ex) {
+  const int c = sh.C * 1000 + sh.NW * 10 + sh.U;
+  switch (c) {
+    case 8161: launch_gemv_cfg<8, 16, 1, EPI, DH>(a, sh.KS, ex); return true;
+    case 8081: launch_gemv_cfg<8, 8, 1, EPI, DH>(a, sh.KS, ex); return true;
+    case 8041: launch_gemv_cfg<8, 4, 1, EPI, DH>(a, sh.KS, ex); return true;
+    case 8021: launch_gemv_cfg<8, 2, 1, EPI, DH>(a, sh.KS, ex); return true;
+    case 8011: launch_gemv_cfg<8, 1, 1, EPI, DH>(a, sh.KS, ex); return true;
+    default: break;
+  }
+  if constexpr (EPI != EPI_QKV) {
+    switch (c) {
+      case 4082: launch_gemv_cfg<4, 8, 2, EPI>(a, sh.KS, ex); return true;
+      case 4042: launch_gemv_cfg<4, 4, 2, EPI>(a, sh.KS, ex); return true;
+      case 4022: launch_gemv_cfg<4, 2, 2, EPI>(a, sh.KS, ex); return true;
+      case 4012: launch_gemv_cfg<4, 1, 2, EPI>(a, sh.KS, ex); return true;
+      default: break;
+    }
+  }
+  return false;
+}
+
+hipError_t launch_gemv(GemmEpi epi, const GemvArgs& a, GemvShape sh, const Exec& ex) {
+  if (a.M < 1 || a.M > 16 || a.K < 32 || a.K % 32 || a.n_tiles < 8 || a.n_tiles % 8) return hipErrorInvalidValue;
+  if (sh.C == 0) sh = gemv_pick(epi, a.n_tiles, a.K);
+  if (sh.KS < 1 || sh.KS > kGemvMaxSplit || a.n_tiles / sh.C + 1 > kCounters) return hipErrorInvalidValue;
+  if ((sh.KS > 1 || epi == EPI_RESID) && a.counters == nullptr) return hipErrorInvalidValue;
+  if (sh.KS > 1 && (a.part == nullptr || (int64_t)sh.KS * a.n_tiles * 256 > a.part_cap))
+    return hipErrorInvalidValue;
+  bool ok = false;
+  switch (epi) {
+    case EPI_QKV:
+      if (sh.C != 8) return hipErrorInvalidValue;
+      if (a.qkv.d_h == 128)
+        ok = dispatch<EPI_QKV, 128>(a, sh, ex);
+      else if (a.qkv.d_h == 64)
+        ok = dispatch<EPI_QKV, 64>(a, sh, ex);
+      break;
+    case EPI_RESID: ok = dispatch<EPI_RESID>(a, sh, ex); break;
+    case EPI_SWIGLU: ok = dispatch<EPI_SWIGLU>(a, sh, ex); break;
+    case EPI_SCALED_STORE: ok = dispatch<EPI_SCALED_STORE>(a, sh, ex); break;
+  }
+  if (!ok) return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace sbd

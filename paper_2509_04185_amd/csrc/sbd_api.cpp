@@ -33,7 +33,9 @@ const char* check_config(const sbd_model_config& c) {
     return "n_q_heads must be a positive multiple of n_kv_heads";
   if ((c.n_q_heads * c.head_dim) % 256) return "n_q_heads*head_dim must be a multiple of 256";
   if (c.ffn_dim < 256 || c.ffn_dim % 256) return "ffn_dim must be a positive multiple of 256";
-  if (c.vocab < 32 || c.vocab % 32) return "vocab must be a positive multiple of 32";
+  if (c.vocab < 128 || c.vocab % 128) return "vocab must be a positive multiple of 128";
+  if (((c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim) % 128)
+    return "(n_q_heads + 2 n_kv_heads) * head_dim must be a multiple of 128";
   if (c.mask_id < 0 || c.mask_id >= c.vocab) return "mask_id must lie in [0, vocab)";
   if (c.qk_norm != 0 && c.qk_norm != 1) return "qk_norm must be 0 or 1";
   if (!(c.rms_eps > 0.f) || !std::isfinite(c.rms_eps)) return "rms_eps must be a positive number";
@@ -88,6 +90,12 @@ bool sbd::compute_layout(const sbd_model_config& c, Layout* L) {
   o.wp_layer = o.wp_down + (int64_t)c.d_model * c.ffn_dim;
   o.wp_lm = o.wp_layer * c.n_layers;
   o.wpack = take((o.wp_lm + (int64_t)c.vocab * c.d_model) * 2);
+  const int64_t widest = std::max<int64_t>(std::max<int64_t>(o.n_qkv, 2 * (int64_t)c.ffn_dim), c.d_model);
+  o.gemv_part_floats = (int64_t)kGemvMaxSplit * 16 * widest;
+  o.gemv_part = take(o.gemv_part_floats * sizeof(float));
+  o.counters = take((int64_t)kCounters * sizeof(int32_t));
+  o.rinv_a = take(o.m_max * sizeof(float));
+  o.rinv_m = take(o.m_max * sizeof(float));
   o.total = off;
   *L = o;
   return true;
@@ -185,6 +193,14 @@ hipEvent_t take_event(sbd_ctx* c) {
     if ((ctx)->prof) (ctx)->recs.push_back(sbd_ctx::Rec{kind, ex.start, ex.stop}); \
   } while (0)
 
+GemvArgs gemv_base(const bf16_t* A, const bf16_t* A_lo, int64_t lda, int M, int K, const bf16_t* Wp,
+                   int n_tiles, float* part, int64_t part_cap, int* counters) {
+  GemvArgs v{};
+  v.A = A; v.A_lo = A_lo; v.lda = lda; v.M = M; v.K = K; v.Wp = Wp; v.n_tiles = n_tiles;
+  v.part = part; v.part_cap = part_cap; v.counters = counters;
+  return v;
+}
+
 int pick_splits(int64_t work_groups_per_split, int nblocks) {
   int s = (int)std::max<int64_t>(1, (1024 + work_groups_per_split - 1) / work_groups_per_split);
   s = std::min(s, kMaxSplits);
@@ -220,9 +236,15 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   const RowParam* drows = c->at<RowParam>(L.rows);
   const SeqParam* dseqs = c->at<SeqParam>(L.seqs);
 
-  EmbedArgs ea{drows, M, d, c->embed, c->layers[0].attn_norm, x, xn, xn_lo, sumsq};
+  float* rinv_a = c->at<float>(L.rinv_a);
+  float* rinv_m = c->at<float>(L.rinv_m);
+  EmbedArgs ea{drows, M, d, c->embed, c->layers[0].attn_norm, x, xn, xn_lo, sumsq, rinv_a, m.rms_eps};
   SBD_LAUNCH(c, SBD_KERNEL_EMBED, launch_embed(ea, ex));
 
+  const bool small = M <= 16;  // decode-sized forward: fused QKV epilogue and split-K
+  int* counters = c->at<int>(L.counters);
+  float* vpart = c->at<float>(L.gemv_part);
+  const int64_t vpart_cap = L.gemv_part_floats;
   int max_end = 0;
   for (const SeqParam& s : seqs) max_end = std::max(max_end, s.cache_len + k);
   const int G = nq / nkv;
@@ -235,63 +257,102 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   for (int l = 0; l < m.n_layers; ++l) {
     const LayerW& w = c->layers[l];
     const bf16_t* wp = c->at<bf16_t>(L.wpack) + (int64_t)l * L.wp_layer;
-    GemmArgs g{};
-    g.A = xn; g.A_lo = xn_lo; g.lda = d; g.M = M; g.K = d;
-    g.Wp = wp; g.n_tiles = (int)(L.n_qkv / 16);
-    g.out_f32 = qkv; g.ldo = L.n_qkv;
-    g.sumsq_in = sumsq; g.n_part = (int)L.n_part; g.inv_d = 1.0f / d; g.eps = m.rms_eps;
-    SBD_LAUNCH(c, SBD_KERNEL_QKV, launch_gemm(EPI_SCALED_STORE, g, ex));
-
-    RopeStageArgs ra{};
-    ra.rows = drows; ra.seqs = dseqs; ra.M = M; ra.k = k; ra.layer = l;
-    ra.n_q = nq; ra.n_kv = nkv; ra.d_h = dh; ra.qk_norm = m.qk_norm; ra.eps = m.rms_eps;
-    ra.q_scale = (float)(1.4426950408889634 / std::sqrt((double)dh));
-    ra.qkv = qkv; ra.q_norm = w.q_norm; ra.k_norm = w.k_norm; ra.rope = c->at<float>(L.rope);
-    ra.q = q; ra.q_lo = q_lo; ra.kcache = c->at<bf16_t>(L.kcache); ra.vcache = c->at<bf16_t>(L.vcache);
-    ra.cap = L.cap; ra.n_slots = m.max_batch;
-    SBD_LAUNCH(c, SBD_KERNEL_ROPE, launch_rope_stage(ra, ex));
+    QkvEpi qe{};
+    qe.rows = drows; qe.seqs = dseqs; qe.kblk = k; qe.layer = l;
+    qe.n_q = nq; qe.n_kv = nkv; qe.d_h = dh; qe.qk_norm = m.qk_norm; qe.eps = m.rms_eps;
+    qe.q_scale = (float)(1.4426950408889634 / std::sqrt((double)dh));
+    qe.rope = c->at<float>(L.rope); qe.q_norm = w.q_norm; qe.k_norm = w.k_norm;
+    qe.q = q; qe.q_lo = q_lo; qe.kcache = c->at<bf16_t>(L.kcache); qe.vcache = c->at<bf16_t>(L.vcache);
+    qe.cap = L.cap; qe.n_slots = m.max_batch;
+    if (small) {
+      // QKV + q/k norm + RoPE + KV staging in one kernel
+      GemvArgs v = gemv_base(xn, xn_lo, d, M, d, wp, (int)(L.n_qkv / 16), vpart, vpart_cap, counters);
+      v.rinv_in = rinv_a;
+      v.qkv = qe;
+      SBD_LAUNCH(c, SBD_KERNEL_QKV, launch_gemv(EPI_QKV, v, GemvShape{}, ex));
+    } else {
+      GemmArgs g{};
+      g.A = xn; g.A_lo = xn_lo; g.lda = d; g.M = M; g.K = d;
+      g.Wp = wp; g.n_tiles = (int)(L.n_qkv / 16);
+      g.out_f32 = qkv; g.ldo = L.n_qkv;
+      g.sumsq_in = sumsq; g.n_part = (int)L.n_part; g.inv_d = 1.0f / d; g.eps = m.rms_eps;
+      SBD_LAUNCH(c, SBD_KERNEL_QKV, launch_gemm(EPI_SCALED_STORE, g, ex));
+      RopeStageArgs ra{};
+      ra.rows = drows; ra.seqs = dseqs; ra.M = M; ra.k = k; ra.layer = l;
+      ra.n_q = nq; ra.n_kv = nkv; ra.d_h = dh; ra.qk_norm = m.qk_norm; ra.eps = m.rms_eps;
+      ra.q_scale = qe.q_scale;
+      ra.qkv = qkv; ra.q_norm = w.q_norm; ra.k_norm = w.k_norm; ra.rope = c->at<float>(L.rope);
+      ra.q = q; ra.q_lo = q_lo; ra.kcache = qe.kcache; ra.vcache = qe.vcache;
+      ra.cap = L.cap; ra.n_slots = m.max_batch;
+      SBD_LAUNCH(c, SBD_KERNEL_ROPE, launch_rope_stage(ra, ex));
+    }
 
     AttnArgs aa{};
     aa.seqs = dseqs; aa.B = B; aa.k = k; aa.layer = l; aa.n_q = nq; aa.n_kv = nkv; aa.d_h = dh;
-    aa.q = q; aa.q_lo = q_lo; aa.kcache = ra.kcache; aa.vcache = ra.vcache; aa.cap = L.cap; aa.n_slots = m.max_batch;
+    aa.q = q; aa.q_lo = q_lo; aa.kcache = qe.kcache; aa.vcache = qe.vcache; aa.cap = L.cap; aa.n_slots = m.max_batch;
     aa.n_rowblocks = n_rb; aa.n_splits = n_splits; aa.blocks_per_split = bps;
     aa.part_ml = c->at<float>(L.attn_ml); aa.part_o = c->at<float>(L.attn_o); aa.out = attn;
     aa.out_lo = attn_lo;
     SBD_LAUNCH(c, SBD_KERNEL_ATTENTION, launch_attention_split(aa, ex));
     SBD_LAUNCH(c, SBD_KERNEL_ATTN_MERGE, launch_attention_merge(aa, ex));
 
-    GemmArgs go{};
-    go.A = attn; go.A_lo = attn_lo; go.lda = qd; go.M = M; go.K = qd;
-    go.Wp = wp + L.wp_o; go.n_tiles = d / 16;
-    go.x = x; go.ldx = d; go.xn = xn; go.xn_lo = xn_lo; go.g_next = w.mlp_norm; go.sumsq_out = sumsq;
-    go.n_part = (int)L.n_part;
-    SBD_LAUNCH(c, SBD_KERNEL_O_PROJ, launch_gemm(EPI_RESID, go, ex));
+    if (small) {
+      GemvArgs v = gemv_base(attn, attn_lo, qd, M, qd, wp + L.wp_o, d / 16, vpart, vpart_cap, counters);
+      v.x = x; v.ldx = d; v.xn = xn; v.xn_lo = xn_lo; v.g_next = w.mlp_norm;
+      v.sumsq = sumsq; v.n_part = (int)L.n_part; v.inv_d = 1.0f / d; v.eps = m.rms_eps; v.rinv_out = rinv_m;
+      SBD_LAUNCH(c, SBD_KERNEL_O_PROJ, launch_gemv(EPI_RESID, v, GemvShape{}, ex));
+    } else {
+      GemmArgs go{};
+      go.A = attn; go.A_lo = attn_lo; go.lda = qd; go.M = M; go.K = qd;
+      go.Wp = wp + L.wp_o; go.n_tiles = d / 16;
+      go.x = x; go.ldx = d; go.xn = xn; go.xn_lo = xn_lo; go.g_next = w.mlp_norm; go.sumsq_out = sumsq;
+      go.n_part = (int)L.n_part;
+      SBD_LAUNCH(c, SBD_KERNEL_O_PROJ, launch_gemm(EPI_RESID, go, ex));
+    }
 
-    GemmArgs gu{};
-    gu.A = xn; gu.A_lo = xn_lo; gu.lda = d; gu.M = M; gu.K = d;
-    gu.Wp = wp + L.wp_gu; gu.n_tiles = m.ffn_dim / 8;
-    gu.sumsq_in = sumsq; gu.n_part = (int)L.n_part; gu.inv_d = 1.0f / d; gu.eps = m.rms_eps;
-    gu.act = act; gu.act_lo = act_lo; gu.ld_act = m.ffn_dim;
-    SBD_LAUNCH(c, SBD_KERNEL_GATE_UP, launch_gemm(EPI_SWIGLU, gu, ex));
+    const bf16_t* g_after = (l + 1 < m.n_layers) ? c->layers[l + 1].attn_norm : c->final_norm;
+    if (small) {
+      GemvArgs vu = gemv_base(xn, xn_lo, d, M, d, wp + L.wp_gu, m.ffn_dim / 8, vpart, vpart_cap, counters);
+      vu.rinv_in = rinv_m; vu.act = act; vu.act_lo = act_lo; vu.ld_act = m.ffn_dim;
+      SBD_LAUNCH(c, SBD_KERNEL_GATE_UP, launch_gemv(EPI_SWIGLU, vu, GemvShape{}, ex));
+      GemvArgs vd = gemv_base(act, act_lo, m.ffn_dim, M, m.ffn_dim, wp + L.wp_down, d / 16, vpart, vpart_cap, counters);
+      vd.x = x; vd.ldx = d; vd.xn = xn; vd.xn_lo = xn_lo; vd.g_next = g_after;
+      vd.sumsq = sumsq; vd.n_part = (int)L.n_part; vd.inv_d = 1.0f / d; vd.eps = m.rms_eps; vd.rinv_out = rinv_a;
+      SBD_LAUNCH(c, SBD_KERNEL_DOWN, launch_gemv(EPI_RESID, vd, GemvShape{}, ex));
+    } else {
+      GemmArgs gu{};
+      gu.A = xn; gu.A_lo = xn_lo; gu.lda = d; gu.M = M; gu.K = d;
+      gu.Wp = wp + L.wp_gu; gu.n_tiles = m.ffn_dim / 8;
+      gu.sumsq_in = sumsq; gu.n_part = (int)L.n_part; gu.inv_d = 1.0f / d; gu.eps = m.rms_eps;
+      gu.act = act; gu.act_lo = act_lo; gu.ld_act = m.ffn_dim;
+      SBD_LAUNCH(c, SBD_KERNEL_GATE_UP, launch_gemm(EPI_SWIGLU, gu, ex));
 
-    GemmArgs gd{};
-    gd.A = act; gd.A_lo = act_lo; gd.lda = m.ffn_dim; gd.M = M; gd.K = m.ffn_dim;
-    gd.Wp = wp + L.wp_down; gd.n_tiles = d / 16;
-    gd.x = x; gd.ldx = d; gd.xn = xn; gd.xn_lo = xn_lo;
-    gd.g_next = (l + 1 < m.n_layers) ? c->layers[l + 1].attn_norm : c->final_norm;
-    gd.sumsq_out = sumsq; gd.n_part = (int)L.n_part;
-    SBD_LAUNCH(c, SBD_KERNEL_DOWN, launch_gemm(EPI_RESID, gd, ex));
+      GemmArgs gd{};
+      gd.A = act; gd.A_lo = act_lo; gd.lda = m.ffn_dim; gd.M = M; gd.K = m.ffn_dim;
+      gd.Wp = wp + L.wp_down; gd.n_tiles = d / 16;
+      gd.x = x; gd.ldx = d; gd.xn = xn; gd.xn_lo = xn_lo; gd.g_next = g_after;
+      gd.sumsq_out = sumsq; gd.n_part = (int)L.n_part;
+      SBD_LAUNCH(c, SBD_KERNEL_DOWN, launch_gemm(EPI_RESID, gd, ex));
+    }
   }
 
   if (logits != nullptr) {
-    GemmArgs gl{};
     const int r0 = lm_row < 0 ? 0 : lm_row;
-    gl.A = xn + (int64_t)r0 * d; gl.A_lo = xn_lo + (int64_t)r0 * d; gl.lda = d; gl.M = lm_row < 0 ? M : 1; gl.K = d;
-    gl.Wp = c->at<bf16_t>(L.wpack) + L.wp_lm; gl.n_tiles = m.vocab / 16;
-    gl.out_f32 = logits; gl.ldo = m.vocab;
-    gl.sumsq_in = sumsq + (int64_t)r0 * L.n_part; gl.n_part = (int)L.n_part;
-    gl.inv_d = 1.0f / d; gl.eps = m.rms_eps;
-    SBD_LAUNCH(c, SBD_KERNEL_LM_HEAD, launch_gemm(EPI_SCALED_STORE, gl, ex));
+    const int Ml = lm_row < 0 ? M : 1;
+    if (small) {
+      GemvArgs v = gemv_base(xn + (int64_t)r0 * d, xn_lo + (int64_t)r0 * d, d, Ml, d,
+                             c->at<bf16_t>(L.wpack) + L.wp_lm, m.vocab / 16, vpart, vpart_cap, counters);
+      v.rinv_in = rinv_a + r0; v.out_f32 = logits; v.ldo = m.vocab;
+      SBD_LAUNCH(c, SBD_KERNEL_LM_HEAD, launch_gemv(EPI_SCALED_STORE, v, GemvShape{}, ex));
+    } else {
+      GemmArgs gl{};
+      gl.A = xn + (int64_t)r0 * d; gl.A_lo = xn_lo + (int64_t)r0 * d; gl.lda = d; gl.M = Ml; gl.K = d;
+      gl.Wp = c->at<bf16_t>(L.wpack) + L.wp_lm; gl.n_tiles = m.vocab / 16;
+      gl.out_f32 = logits; gl.ldo = m.vocab;
+      gl.sumsq_in = sumsq + (int64_t)r0 * L.n_part; gl.n_part = (int)L.n_part;
+      gl.inv_d = 1.0f / d; gl.eps = m.rms_eps;
+      SBD_LAUNCH(c, SBD_KERNEL_LM_HEAD, launch_gemm(EPI_SCALED_STORE, gl, ex));
+    }
   }
   return SBD_OK;
 }
@@ -414,6 +475,8 @@ sbd_status sbd_create(const sbd_model_config* cfg, const sbd_weights* w, void* w
   // table; repack every weight matrix into the GEMM's fragment order.
   const size_t kv_bytes = L.rope - L.kcache;
   bool ok = hipMemsetAsync(c->ws + L.kcache, 0, kv_bytes, c->stream) == hipSuccess &&
+            hipMemsetAsync(c->ws + L.counters, 0, (size_t)kCounters * sizeof(int32_t), c->stream) ==
+                hipSuccess &&
             launch_rope_table(c->at<float>(L.rope), L.cap, cfg->head_dim, (double)cfg->rope_theta,
                               c->stream) == hipSuccess;
   const int d = cfg->d_model, F = cfg->ffn_dim;

@@ -44,6 +44,14 @@ __device__ __forceinline__ i32x4 ld16_stream(const void* p) {
   return __builtin_nontemporal_load((const i32x4*)p);
 }
 
+// Packed weights: 16-row tiles in groups of 8, [N/128][K/32 steps][8 tiles][64 lanes][8]
+// bf16 (see gemm.hip).  Element offset of tile t's 1 KB fragment at K step s (S steps);
+// consecutive steps of one tile are kPackStep elements apart.
+constexpr int64_t kPackStep = 8 * 512;
+__device__ __forceinline__ int64_t packed_frag(int64_t t, int64_t s, int64_t S) {
+  return (((t >> 3) * S + s) * 8 + (t & 7)) * 512;
+}
+
 __device__ __forceinline__ f32x4 mfma16x16x32(i32x4 a, i32x4 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
@@ -57,6 +65,72 @@ __device__ __forceinline__ float half_wave_sum(float v) {
   v += __shfl_xor(v, 2);
   v += __shfl_xor(v, 1);
   return v;
+}
+
+// Cross-workgroup reduction handshake.  Every workgroup writes its partial results with
+// store_coherent(), then calls last_arrival(); it returns true in exactly one workgroup —
+// the last of `expected` to arrive at `counter` — which then reads the partials with
+// load_coherent().  The counter is reset to 0 for the next launch.  No workgroup ever
+// waits on another.
+//
+// Each XCD has its own L2, so the partials must be visible across L2s.  Variant selected
+// by SBD_SPLITK_SYNC:
+//   0  device-scope fences around the counter (L2 write-back and invalidate by every wave)
+//   1  one release fence per workgroup before the counter, one acquire fence in the last
+//   2  partials stored/loaded with device-coherent (sc1) accesses; the counter increment
+//      only waits for those stores to complete (no cache-wide write-back or invalidate)
+#ifndef SBD_SPLITK_SYNC
+#define SBD_SPLITK_SYNC 2
+#endif
+
+__device__ __forceinline__ void store_coherent(float* p, float v) {
+#if SBD_SPLITK_SYNC == 2
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#else
+  *p = v;
+#endif
+}
+
+__device__ __forceinline__ float load_coherent(const float* p) {
+#if SBD_SPLITK_SYNC == 2
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#else
+  return *p;
+#endif
+}
+
+__device__ __forceinline__ bool last_arrival(int* counter, int expected) {
+  __shared__ int s_last;
+#if SBD_SPLITK_SYNC == 0
+  __threadfence();
+  __syncthreads();
+#elif SBD_SPLITK_SYNC == 1
+  __syncthreads();
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+#else
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's coherent stores have completed
+  __syncthreads();
+#endif
+  if (threadIdx.x == 0) {
+#if SBD_SPLITK_SYNC == 1
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+#endif
+    const int prev = atomicAdd(counter, 1);
+    s_last = (prev == expected - 1) ? 1 : 0;
+    if (s_last) {
+      atomicExch(counter, 0);
+#if SBD_SPLITK_SYNC == 1
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+#endif
+    }
+  }
+  __syncthreads();
+  const bool last = s_last != 0;
+#if SBD_SPLITK_SYNC == 0
+  if (last) __threadfence();
+#endif
+  return last;
 }
 
 __device__ __forceinline__ float wave_sum(float v) {

@@ -18,6 +18,7 @@ constexpr int kKeyBlock = 32;       // keys per attention step / per V^T storage
 constexpr int kMaxSplits = 64;      // split-KV partitions per (sequence, KV head, row block)
 constexpr int kEbChunk = 4096;      // vocabulary entries per EB partial workgroup
 constexpr int kMaxBlock = 64;       // largest block size k
+constexpr int kCounters = 16384;    // arrival counters in the workspace
 
 // Where a kernel is enqueued: the stream, plus optional start/stop events that the
 // runtime records at the kernel's own start and end (per-kernel timing).
@@ -52,7 +53,9 @@ struct Layout {
   size_t wpack;              // packed weights (see gemm.hip), element offsets below
   int64_t wp_layer;          // elements per layer: qkv, then o, then gate/up, then down
   int64_t wp_o, wp_gu, wp_down, wp_lm;
-  size_t attn_ml, attn_o, rows, seqs, eb_mask, eb_part, eb_arg;
+  size_t attn_ml, attn_o, rows, seqs, eb_mask, eb_part, eb_arg, gemv_part, counters;
+  int64_t gemv_part_floats;  // split-K partial tiles of the decode GEMM
+  size_t rinv_a, rinv_m;  // 1/rms per row (attention/final norm, MLP norm)
   size_t total;
 };
 
@@ -65,7 +68,27 @@ struct LayerW {
 };
 
 // ---------------------------------------------------------------------------- GEMM
-enum GemmEpi { EPI_SCALED_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+enum GemmEpi { EPI_SCALED_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3 };
+
+// EPI_QKV (decode-sized GEMM only): the QKV projection's epilogue does the rest of the
+// attention input — per-head RMSNorm of q and k (Qwen-3), rotate-half RoPE, q stored as
+// scaled hi/lo, K and V written to the cache at position cache_len + j.
+struct QkvEpi {
+  const RowParam* rows;
+  const SeqParam* seqs;
+  int kblk, layer;
+  int n_q, n_kv, d_h, qk_norm;
+  float eps, q_scale;
+  const float* rope;  // [cap][d_h/2][2]
+  const bf16_t* q_norm;
+  const bf16_t* k_norm;
+  bf16_t* q;
+  bf16_t* q_lo;
+  bf16_t* kcache;
+  bf16_t* vcache;
+  int64_t cap;
+  int n_slots;
+};
 
 // Activations travel as two bf16 arrays, hi = bf16(a) and lo = bf16(a - hi), which
 // together carry about 16 significant bits; products with bf16 weights are exact in the
@@ -100,6 +123,44 @@ struct GemmArgs {
 };
 
 hipError_t launch_gemm(GemmEpi epi, const GemmArgs& a, const Exec& ex);
+
+// Decode-sized GEMM (M <= 16), gemv.hip: a workgroup owns C tiles of one packed group and
+// a K range; its waves split the range, partial tiles meet in LDS, and K ranges split
+// across workgroups are added by the last one to finish.
+struct GemvArgs {
+  const bf16_t* A;     // hi [M][K], row stride lda
+  const bf16_t* A_lo;  // lo
+  int64_t lda;
+  int M, K;
+  const bf16_t* Wp;    // packed weights
+  int n_tiles;         // 16-row tiles of the packed matrix (a multiple of 8)
+  const float* rinv_in;  // [M] 1/rms of the input rows (EPI_SCALED_STORE, SWIGLU, QKV)
+  float* out_f32;        // EPI_SCALED_STORE
+  int64_t ldo;
+  float* x;              // EPI_RESID
+  int64_t ldx;
+  bf16_t* xn;
+  bf16_t* xn_lo;
+  const bf16_t* g_next;
+  float* sumsq;          // [M][n_part], one partial per 16-column tile
+  int n_part;
+  float inv_d, eps;
+  float* rinv_out;       // [M]
+  bf16_t* act;           // EPI_SWIGLU
+  bf16_t* act_lo;
+  int64_t ld_act;
+  QkvEpi qkv;            // EPI_QKV
+  float* part;           // split K: partial tiles [splits][n_tiles][4][64]
+  int64_t part_cap;      // floats available at part (bounds the split)
+  int* counters;         // arrival counters (kCounters), zero between launches
+};
+// Launch shape of the decode GEMM; a zero field means "pick for the shape".
+struct GemvShape {
+  int C, NW, U, KS;
+};
+constexpr int kGemvMaxSplit = 16;
+GemvShape gemv_pick(GemmEpi epi, int n_tiles, int K);
+hipError_t launch_gemv(GemmEpi epi, const GemvArgs& a, GemvShape shape, const Exec& ex);
 // Repack a row-major [rows][K] matrix (mode 0) or a gate/up pair (mode 1, rows = 2 * F
 // packed rows) into the fragment order read by gemm_kernel.
 hipError_t launch_pack(const bf16_t* src0, const bf16_t* src1, bf16_t* dst, int64_t rows, int K,
@@ -115,6 +176,8 @@ struct EmbedArgs {
   bf16_t* xn;
   bf16_t* xn_lo;
   float* sumsq;  // [M][d/16]
+  float* rinv;   // [M] 1/sqrt(mean(x^2) + eps)
+  float eps;
 };
 hipError_t launch_embed(const EmbedArgs& a, const Exec& ex);
 
