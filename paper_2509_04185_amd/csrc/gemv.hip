@@ -18,14 +18,17 @@
 // Epilogues (acc in the v_mfma_f32_16x16x32_bf16 D layout: lane l holds column l % 16 of
 // a tile, rows 4*(l/16) + i):
 //   EPI_SCALED_STORE  out = rinv[m] * y                      (LM head)
-//   EPI_RESID         x += y; xn = x * g_next as hi/lo bf16; per-tile sums of x^2; the
-//                     last workgroup to finish turns them into rinv_out[m] =
-//                     1/sqrt(mean(x^2) + eps) for the next RMSNorm (O, down projections)
+//   EPI_RESID         x += y; xn = x * g_next as hi/lo bf16; one partial sum of x^2 per
+//                     row and workgroup for the next RMSNorm (O, down projections)
 //   EPI_SWIGLU        act = silu(rinv*gate) * rinv*up as hi/lo (gate/up: packed tile t
 //                     holds gate rows 8t..8t+7 then up rows 8t..8t+7)
 //   EPI_QKV           C = 8 (128 columns = whole heads): per-head q/k RMSNorm, rotate-half
 //                     RoPE, q as scaled hi/lo, K and V into the cache at cache_len + j
 // Activations are hi/lo bf16 pairs: two MFMAs per step, exact products in fp32.
+// RMSNorm is split between kernels: the producer of x (EPI_RESID, or the embedding) writes
+// x * g and partial sums of x^2; the consumer adds the partials of its rows, loaded before
+// its weight stream starts, and scales its fp32 products by rinv[m] = 1/sqrt(mean(x^2) +
+// eps), which equals normalising the input because the scale is constant along a row.
 
 #include "sbd_device.h"
 
@@ -131,12 +134,32 @@ __global__ __launch_bounds__(NW * 64) void gemv_kernel(GemvArgs a) {
   const int s_b = z0 + (z1 - z0) * wave / NW, s_e = z0 + (z1 - z0) * (wave + 1) / NW;
   const int ns = s_e - s_b;
 
-  // 1/rms of this lane's accumulator rows 4g + i (loaded early, used by the epilogue)
-  float rinv[4];
+  // Consumers: the partial sums of squares of the input rows, loaded before the weight
+  // stream; thread t adds partials q, q + tpr, ... of row t / tpr (tpr threads per row).
+  constexpr int tpr = NW * 4;
+  constexpr int kPre = 8;
+  float sq_pre[kPre];
+  const int sq_m = threadIdx.x / tpr, sq_q = threadIdx.x % tpr;
+  const bool sq_on = EPI != EPI_RESID && a.sumsq_in != nullptr && sq_m < a.M;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int m = 4 * g + i;
-    rinv[i] = (EPI != EPI_RESID && a.rinv_in != nullptr && m < a.M) ? a.rinv_in[m] : 1.f;
+  for (int j = 0; j < kPre; ++j) {
+    const int p = sq_q + j * tpr;
+    sq_pre[j] = (sq_on && p < a.n_part_in) ? a.sumsq_in[(int64_t)sq_m * a.n_part_in + p] : 0.f;
+  }
+  // EPI_RESID: the residual rows and the next norm's gain for the tiles this wave finishes
+  float x_pre[(C + NW - 1) / NW][4], g_pre[(C + NW - 1) / NW];
+  if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+    for (int k2 = 0; k2 < (C + NW - 1) / NW; ++k2) {
+      const int ct = wave + k2 * NW;
+      const int n = (t0 + (ct < C ? ct : 0)) * 16 + r;
+      g_pre[k2] = bf2f(a.g_next[n]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = 4 * g + i;
+        x_pre[k2][i] = (ct < C && m < a.M) ? a.x[(int64_t)m * a.ldx + n] : 0.f;
+      }
+    }
   }
 
   const int arow_m = r < a.M ? r : a.M - 1;
@@ -179,6 +202,26 @@ __global__ __launch_bounds__(NW * 64) void gemv_kernel(GemvArgs a) {
     for (int ct = 0; ct < C; ++ct) {
       acc[ct] = mfma16x16x32(xa, wv[ct], acc[ct]);
       acc[ct] = mfma16x16x32(xl, wv[ct], acc[ct]);
+    }
+  }
+
+  // ---- 1/rms of this lane's accumulator rows 4g + i
+  __shared__ float rinv_s[16];
+  __shared__ float ssq_s[C][16];  // EPI_RESID: per-tile sums of x^2 of each row
+  float rinv[4] = {1.f, 1.f, 1.f, 1.f};
+  if constexpr (EPI != EPI_RESID) {
+    if (a.sumsq_in != nullptr) {
+      float s = 0.f;
+#pragma unroll
+      for (int j = 0; j < kPre; ++j) s += sq_pre[j];
+      for (int p = sq_q + kPre * tpr; sq_on && p < a.n_part_in; p += tpr)
+        s += a.sumsq_in[(int64_t)sq_m * a.n_part_in + p];
+#pragma unroll
+      for (int o = tpr / 2; o >= 1; o /= 2) s += __shfl_xor(s, o);
+      if (sq_q == 0 && sq_m < 16) rinv_s[sq_m] = 1.0f / sqrtf(s * a.inv_d + a.eps);
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < 4; ++i) rinv[i] = rinv_s[4 * g + i];
     }
   }
 
@@ -260,18 +303,17 @@ __global__ __launch_bounds__(NW * 64) void gemv_kernel(GemvArgs a) {
           }
         }
       } else {  // EPI_RESID
+        const int k2 = ct / NW;
         const int n = tile * 16 + r;
-        const float gn = bf2f(a.g_next[n]);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int m = 4 * g + i;
           float xv = 0.f;
           if (m < a.M) {
-            float* xp = a.x + (int64_t)m * a.ldx + n;
-            xv = *xp + acc[ct][i];
-            *xp = xv;
+            xv = x_pre[k2][i] + acc[ct][i];
+            a.x[(int64_t)m * a.ldx + n] = xv;
             bf16_t hi, lo;
-            split_bf16(xv * gn, hi, lo);
+            split_bf16(xv * g_pre[k2], hi, lo);
             a.xn[(int64_t)m * a.ldx + n] = hi;
             a.xn_lo[(int64_t)m * a.ldx + n] = lo;
           }
@@ -280,21 +322,20 @@ __global__ __launch_bounds__(NW * 64) void gemv_kernel(GemvArgs a) {
           s2 += __shfl_xor(s2, 2);
           s2 += __shfl_xor(s2, 4);
           s2 += __shfl_xor(s2, 8);
-          if (r == 0 && m < a.M) store_coherent(a.sumsq + (int64_t)m * a.n_part + tile, s2);
+          if (r == 0) ssq_s[ct][m] = s2;
         }
       }
     }
   }
 
   if constexpr (EPI == EPI_RESID) {
-    // The last workgroup to finish its epilogue turns the per-tile sums into 1/rms per
-    // row: wave w takes rows w, w + NW, ...
-    if (!last_arrival(a.counters + gridDim.x, (int)gridDim.x)) return;
-    for (int m = wave; m < a.M; m += NW) {
+    // one partial sum of x^2 per row for this workgroup's C tiles, added in tile order
+    __syncthreads();
+    if (threadIdx.x < a.M) {
       float s = 0.f;
-      for (int p = lane; p < a.n_part; p += 64) s += load_coherent(a.sumsq + (int64_t)m * a.n_part + p);
-      s = wave_sum(s);
-      if (lane == 0) a.rinv_out[m] = 1.0f / sqrtf(s * a.inv_d + a.eps);
+#pragma unroll
+      for (int ct = 0; ct < C; ++ct) s += ssq_s[ct][threadIdx.x];
+      a.sumsq[(int64_t)threadIdx.x * a.n_part + sub] = s;
     }
   }
 }
@@ -346,7 +387,8 @@ hipError_t launch_gemv(GemmEpi epi, const GemvArgs& a, GemvShape sh, const Exec&
   if (a.M < 1 || a.M > 16 || a.K < 32 || a.K % 32 || a.n_tiles < 8 || a.n_tiles % 8) return hipErrorInvalidValue;
   if (sh.C == 0) sh = gemv_pick(epi, a.n_tiles, a.K);
   if (sh.KS < 1 || sh.KS > kGemvMaxSplit || a.n_tiles / sh.C + 1 > kCounters) return hipErrorInvalidValue;
-  if ((sh.KS > 1 || epi == EPI_RESID) && a.counters == nullptr) return hipErrorInvalidValue;
+  if (sh.KS > 1 && a.counters == nullptr) return hipErrorInvalidValue;
+  if (epi == EPI_RESID && (a.sumsq == nullptr || a.n_part != a.n_tiles / sh.C)) return hipErrorInvalidValue;
   if (sh.KS > 1 && (a.part == nullptr || (int64_t)sh.KS * a.n_tiles * 256 > a.part_cap))
     return hipErrorInvalidValue;
   bool ok = false;

@@ -22,12 +22,10 @@ __device__ __forceinline__ int64_t kv_head_base(int layer, int slot, int g, int 
 }
 
 // One workgroup per row m: x[m] = E[tok[m]] (fp32), xn[m] = x * g as hi/lo bf16,
-// sumsq[m][c/16] = sum over each 16 columns of x^2, rinv[m] = 1/sqrt(mean(x^2) + eps).
+// sumsq[m][c/16] = sum over each 16 columns of x^2 (the consumer forms 1/rms).
 __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
-  __shared__ float part[4];
   const int m = blockIdx.x;
   const int tok = a.rows[m].tok;
-  float tot = 0.f;
   for (int c = threadIdx.x; c < a.d; c += 256) {
     const float v = bf2f(a.embed[(int64_t)tok * a.d + c]);
     a.x[(int64_t)m * a.d + c] = v;
@@ -40,15 +38,8 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
     s += __shfl_xor(s, 4);
     s += __shfl_xor(s, 2);
     s += __shfl_xor(s, 1);
-    if ((threadIdx.x & 15) == 0) {
-      a.sumsq[(int64_t)m * (a.d / 16) + c / 16] = s;
-      tot += s;
-    }
+    if ((threadIdx.x & 15) == 0) a.sumsq[(int64_t)m * (a.d / 16) + c / 16] = s;
   }
-  tot = wave_sum(tot);
-  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = tot;
-  __syncthreads();
-  if (threadIdx.x == 0) a.rinv[m] = 1.0f / sqrtf((part[0] + part[1] + part[2] + part[3]) / (float)a.d + a.eps);
 }
 
 hipError_t launch_embed(const EmbedArgs& a, const Exec& ex) {

@@ -94,8 +94,6 @@ bool sbd::compute_layout(const sbd_model_config& c, Layout* L) {
   o.gemv_part_floats = (int64_t)kGemvMaxSplit * 16 * widest;
   o.gemv_part = take(o.gemv_part_floats * sizeof(float));
   o.counters = take((int64_t)kCounters * sizeof(int32_t));
-  o.rinv_a = take(o.m_max * sizeof(float));
-  o.rinv_m = take(o.m_max * sizeof(float));
   o.total = off;
   *L = o;
   return true;
@@ -236,12 +234,15 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   const RowParam* drows = c->at<RowParam>(L.rows);
   const SeqParam* dseqs = c->at<SeqParam>(L.seqs);
 
-  float* rinv_a = c->at<float>(L.rinv_a);
-  float* rinv_m = c->at<float>(L.rinv_m);
-  EmbedArgs ea{drows, M, d, c->embed, c->layers[0].attn_norm, x, xn, xn_lo, sumsq, rinv_a, m.rms_eps};
+  EmbedArgs ea{drows, M, d, c->embed, c->layers[0].attn_norm, x, xn, xn_lo, sumsq};
   SBD_LAUNCH(c, SBD_KERNEL_EMBED, launch_embed(ea, ex));
 
   const bool small = M <= 16;  // decode-sized forward: fused QKV epilogue and split-K
+  // Partial sums of x^2 per row handed from each RESID producer to the next consumer:
+  // d/16 from the embedding, one per workgroup of the decode O and down projections.
+  const int n_part_o = (d / 16) / gemv_pick(EPI_RESID, d / 16, qd).C;
+  const int n_part_down = (d / 16) / gemv_pick(EPI_RESID, d / 16, m.ffn_dim).C;
+  int n_part_cur = d / 16;
   int* counters = c->at<int>(L.counters);
   float* vpart = c->at<float>(L.gemv_part);
   const int64_t vpart_cap = L.gemv_part_floats;
@@ -267,7 +268,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     if (small) {
       // QKV + q/k norm + RoPE + KV staging in one kernel
       GemvArgs v = gemv_base(xn, xn_lo, d, M, d, wp, (int)(L.n_qkv / 16), vpart, vpart_cap, counters);
-      v.rinv_in = rinv_a;
+      v.sumsq_in = sumsq; v.n_part_in = n_part_cur; v.inv_d = 1.0f / d; v.eps = m.rms_eps;
       v.qkv = qe;
       SBD_LAUNCH(c, SBD_KERNEL_QKV, launch_gemv(EPI_QKV, v, GemvShape{}, ex));
     } else {
@@ -299,7 +300,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     if (small) {
       GemvArgs v = gemv_base(attn, attn_lo, qd, M, qd, wp + L.wp_o, d / 16, vpart, vpart_cap, counters);
       v.x = x; v.ldx = d; v.xn = xn; v.xn_lo = xn_lo; v.g_next = w.mlp_norm;
-      v.sumsq = sumsq; v.n_part = (int)L.n_part; v.inv_d = 1.0f / d; v.eps = m.rms_eps; v.rinv_out = rinv_m;
+      v.sumsq = sumsq; v.n_part = n_part_o;
       SBD_LAUNCH(c, SBD_KERNEL_O_PROJ, launch_gemv(EPI_RESID, v, GemvShape{}, ex));
     } else {
       GemmArgs go{};
@@ -313,11 +314,13 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     const bf16_t* g_after = (l + 1 < m.n_layers) ? c->layers[l + 1].attn_norm : c->final_norm;
     if (small) {
       GemvArgs vu = gemv_base(xn, xn_lo, d, M, d, wp + L.wp_gu, m.ffn_dim / 8, vpart, vpart_cap, counters);
-      vu.rinv_in = rinv_m; vu.act = act; vu.act_lo = act_lo; vu.ld_act = m.ffn_dim;
+      vu.sumsq_in = sumsq; vu.n_part_in = n_part_o; vu.inv_d = 1.0f / d; vu.eps = m.rms_eps;
+      vu.act = act; vu.act_lo = act_lo; vu.ld_act = m.ffn_dim;
       SBD_LAUNCH(c, SBD_KERNEL_GATE_UP, launch_gemv(EPI_SWIGLU, vu, GemvShape{}, ex));
       GemvArgs vd = gemv_base(act, act_lo, m.ffn_dim, M, m.ffn_dim, wp + L.wp_down, d / 16, vpart, vpart_cap, counters);
       vd.x = x; vd.ldx = d; vd.xn = xn; vd.xn_lo = xn_lo; vd.g_next = g_after;
-      vd.sumsq = sumsq; vd.n_part = (int)L.n_part; vd.inv_d = 1.0f / d; vd.eps = m.rms_eps; vd.rinv_out = rinv_a;
+      vd.sumsq = sumsq; vd.n_part = n_part_down;
+      n_part_cur = n_part_down;
       SBD_LAUNCH(c, SBD_KERNEL_DOWN, launch_gemv(EPI_RESID, vd, GemvShape{}, ex));
     } else {
       GemmArgs gu{};
@@ -342,7 +345,9 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     if (small) {
       GemvArgs v = gemv_base(xn + (int64_t)r0 * d, xn_lo + (int64_t)r0 * d, d, Ml, d,
                              c->at<bf16_t>(L.wpack) + L.wp_lm, m.vocab / 16, vpart, vpart_cap, counters);
-      v.rinv_in = rinv_a + r0; v.out_f32 = logits; v.ldo = m.vocab;
+      v.sumsq_in = sumsq + (int64_t)r0 * n_part_cur; v.n_part_in = n_part_cur;
+      v.inv_d = 1.0f / d; v.eps = m.rms_eps;
+      v.out_f32 = logits; v.ldo = m.vocab;
       SBD_LAUNCH(c, SBD_KERNEL_LM_HEAD, launch_gemv(EPI_SCALED_STORE, v, GemvShape{}, ex));
     } else {
       GemmArgs gl{};

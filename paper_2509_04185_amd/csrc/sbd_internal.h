@@ -55,7 +55,6 @@ struct Layout {
   int64_t wp_o, wp_gu, wp_down, wp_lm;
   size_t attn_ml, attn_o, rows, seqs, eb_mask, eb_part, eb_arg, gemv_part, counters;
   int64_t gemv_part_floats;  // split-K partial tiles of the decode GEMM
-  size_t rinv_a, rinv_m;  // 1/rms per row (attention/final norm, MLP norm)
   size_t total;
 };
 
@@ -134,7 +133,10 @@ struct GemvArgs {
   int M, K;
   const bf16_t* Wp;    // packed weights
   int n_tiles;         // 16-row tiles of the packed matrix (a multiple of 8)
-  const float* rinv_in;  // [M] 1/rms of the input rows (EPI_SCALED_STORE, SWIGLU, QKV)
+  // EPI_SCALED_STORE, SWIGLU, QKV: the input rows' RMSNorm scale 1/sqrt(mean(x^2) + eps)
+  // is formed from the producer's partial sums of squares [M][n_part_in] (none: scale 1)
+  const float* sumsq_in;
+  int n_part_in;
   float* out_f32;        // EPI_SCALED_STORE
   int64_t ldo;
   float* x;              // EPI_RESID
@@ -142,10 +144,9 @@ struct GemvArgs {
   bf16_t* xn;
   bf16_t* xn_lo;
   const bf16_t* g_next;
-  float* sumsq;          // [M][n_part], one partial per 16-column tile
+  float* sumsq;          // EPI_RESID: [M][n_part] partial sums of x^2, n_part = n_tiles / C
   int n_part;
   float inv_d, eps;
-  float* rinv_out;       // [M]
   bf16_t* act;           // EPI_SWIGLU
   bf16_t* act_lo;
   int64_t ld_act;
@@ -176,8 +177,6 @@ struct EmbedArgs {
   bf16_t* xn;
   bf16_t* xn_lo;
   float* sumsq;  // [M][d/16]
-  float* rinv;   // [M] 1/sqrt(mean(x^2) + eps)
-  float eps;
 };
 hipError_t launch_embed(const EmbedArgs& a, const Exec& ex);
 
