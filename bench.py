@@ -9,8 +9,8 @@ committed token + 15 masks), gamma = 1.0.  Inputs are resident in HBM before tim
 
 Prints one JSON line: value = algorithmic HBM bytes of a step / step time (GB/s),
 plus the block-forward ms, the EB-select microseconds, a roofline entry for the
-dominant kernel (gate/up projection, timed live with HIP events on the library
-stream) and the CPU oracle timed on a bounded sample of the same workload.
+dominant kernel (the fused decode forward, or the gate/up projection on the per-kernel
+path; timed live with HIP events on the library stream) and the CPU oracle timed on a bounded sample of the same workload.
 """
 import argparse
 import dataclasses
@@ -26,7 +26,6 @@ sys.path.insert(0, ROOT)
 
 METRIC = "SBD block-forward ms + HBM GB/s (8B shape, k=16); EB-select µs"
 PEAK_HBM_GBS = 8000.0
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gate_up_traffic_llama8b_b1_l2048_k16.json")
 
 
 def step_bytes(shape, lens, k):
@@ -53,9 +52,16 @@ def gate_up_bytes(shape, M):
     return 2 * 2 * shape.ffn_dim * shape.d_model + 2 * M * shape.d_model + 2 * M * shape.ffn_dim
 
 
-def source_hash():
+KERNEL_SOURCES = {
+    "fused": ("fused.hip", "attention_body.h", "qkv_epilogue.h", "sbd_device.h"),
+    "gate_up": ("gemv.hip", "qkv_epilogue.h", "sbd_device.h"),
+}
+
+
+def source_hash(kind):
+    """Hash of the sources of the kernel the counter file describes (stale counters are not used)."""
     h = hashlib.sha256()
-    for name in ("gemv.hip", "sbd_device.h"):
+    for name in KERNEL_SOURCES[kind]:
         with open(os.path.join(ROOT, "paper_2509_04185_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -107,6 +113,8 @@ def main():
     ap.add_argument("--cpu-layers", type=int, default=8, help="layers of the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event pass")
+    ap.add_argument("--decode-path", default="auto", choices=["auto", "fused", "kernels"],
+                    help="kernels of decode-sized forwards (sbd_set_decode_path)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -129,6 +137,7 @@ def main():
     print(f"[bench] {wl.name}: generating weights", file=sys.stderr, flush=True)
     w = synth.make_weights(s, wl.seed, device=dev)
     lib = Sbd(s, w, max_batch=B, max_seq_len=max(lens) + k + 64, max_block=k)
+    lib.set_decode_path(args.decode_path)
     print(f"[bench] prefilling {B} x {lens[0]}..{lens[-1]} tokens", file=sys.stderr, flush=True)
     for b, L in enumerate(lens):
         lib.prefill(b, synth.make_tokens(wl.seed, L, s, stream=100 + b), want_logits=False)
@@ -184,20 +193,26 @@ def main():
         lib.profile(False)
         kernels = {n: {"launches": c, "avg_us": 1000.0 * t / c if c else None}
                    for n, (c, t) in prof.items() if c}
-        c, t = prof["gate_up"]
+        if prof.get("fused", (0, 0.0))[0]:
+            # one launch runs every layer and the LM head: its bytes are the block forward's
+            kind, bpl = "fused", fwd_bytes
+            label = "fused_forward_kernel<128> (all layers + LM head, M = 16)"
+        else:
+            kind, bpl = "gate_up", gate_up_bytes(s, B * k)
+            label = "gemv_kernel<8,4,1,EPI_SWIGLU> (gate/up projection + SwiGLU)"
+        c, t = prof[kind]
         avg_s = t / c * 1e-3
-        bpl = gate_up_bytes(s, B * k)
         achieved = bpl / avg_s / 1e9
         traffic = None
-        if os.path.exists(TRAFFIC_FILE):
-            with open(TRAFFIC_FILE) as f:
+        traffic_file = os.path.join(ROOT, "profiles", f"{kind}_traffic_{wl.name}.json")
+        if os.path.exists(traffic_file):
+            with open(traffic_file) as f:
                 tr = json.load(f)
-            if tr.get("kernel_source") == source_hash():
+            if tr.get("kernel_source") == source_hash(kind):
                 traffic = tr.get("bytes_per_launch")
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                     "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-                    "kernel": "gemv_kernel<8,4,1,EPI_SWIGLU> (gate/up projection + SwiGLU)",
-                    "bytes_per_launch": bpl, "avg_launch_us": round(avg_s * 1e6, 2),
+                    "kernel": label, "bytes_per_launch": bpl, "avg_launch_us": round(avg_s * 1e6, 2),
                     "launches": c}
 
     # a plain copy of known size, so counter runs can calibrate FETCH_SIZE / WRITE_SIZE
@@ -224,7 +239,7 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded random-init weights, uniform random prompt tokens)",
         "config": {"workload": wl.name, "shape": s.name, "batch": B, "cache_len": lens, "k": k,
-                   "gamma": gamma, "n_causal": 1},
+                   "gamma": gamma, "n_causal": 1, "decode_path": args.decode_path},
         "block_forward_ms": round(ms_fwd, 4),
         "block_forward_gbs": round(fwd_bytes / (ms_fwd * 1e-3) / 1e9, 1),
         "block_forward_frac_of_peak": round(fwd_bytes / (ms_fwd * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),

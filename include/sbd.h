@@ -196,6 +196,23 @@ sbd_status sbd_workspace_region(const sbd_model_config* cfg, const char* name, s
                                 size_t* bytes);
 
 /*
+ * Which kernels run a decode-sized forward (at most 16 rows: sbd_block_forward with
+ * batch * k <= 16, and prefill chunks that small).
+ *   SBD_DECODE_AUTO     the fused forward (every layer and the LM head in one launch of one
+ *                       persistent workgroup per CU) when the model and device fit it, else
+ *                       one kernel per step.
+ *   SBD_DECODE_FUSED    the fused forward; a forward it cannot take fails with
+ *                       SBD_ERR_UNSUPPORTED.  It needs d_model a multiple of 128, head_dim 64
+ *                       or 128, and at most as many 128-column weight groups per projection
+ *                       as the device has CUs (capped at 256).
+ *   SBD_DECODE_KERNELS  one kernel per step (the default: the faster of the two at present).
+ * Both give the same results up to float summation order.  Larger forwards always run one
+ * kernel per step.  INVALID_ARG for another value.
+ */
+typedef enum { SBD_DECODE_AUTO = 0, SBD_DECODE_FUSED = 1, SBD_DECODE_KERNELS = 2 } sbd_decode_path;
+sbd_status sbd_set_decode_path(sbd_ctx* ctx, int32_t path);
+
+/*
  * Per-kernel timing, for measurement tools.  While enabled, every kernel launch the
  * context makes is bracketed by a pair of HIP events on its stream (this adds a little
  * time between kernels).  sbd_profile_read waits for the recorded work, adds up the
@@ -214,7 +231,8 @@ typedef enum {
   SBD_KERNEL_LM_HEAD = 8,    /* final norm + LM head */
   SBD_KERNEL_EB_PARTIAL = 9, /* EB per-chunk softmax statistics */
   SBD_KERNEL_EB_SELECT = 10, /* EB merge, sort and select */
-  SBD_KERNEL_COUNT = 11
+  SBD_KERNEL_FUSED = 11,     /* fused decode forward: all layers + LM head in one launch */
+  SBD_KERNEL_COUNT = 12
 } sbd_kernel;
 sbd_status sbd_profile_enable(sbd_ctx* ctx, int32_t enable);
 sbd_status sbd_profile_read(sbd_ctx* ctx, int32_t kernel, int32_t* launches, double* total_ms);

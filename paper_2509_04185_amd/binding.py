@@ -25,7 +25,8 @@ LAYER_FIELDS = ("attn_norm", "wq", "wk", "wv", "wo", "q_norm", "k_norm", "mlp_no
 
 # sbd_kernel values, in order.
 KERNEL_NAMES = ("embed", "qkv", "rope", "attention", "attn_merge", "o_proj", "gate_up", "down",
-                "lm_head", "eb_partial", "eb_select")
+                "lm_head", "eb_partial", "eb_select", "fused")
+DECODE_PATHS = {"auto": 0, "fused": 1, "kernels": 2}  # sbd_decode_path
 
 # Every entry point of sbd.h with its argument types.
 SIGNATURES = {
@@ -46,6 +47,7 @@ SIGNATURES = {
                                 c_void_p, c_void_p],
     "sbd_kv_import": [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p],
     "sbd_kv_export": [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p],
+    "sbd_set_decode_path": [c_void_p, c_int32],
     "sbd_profile_enable": [c_void_p, c_int32],
     "sbd_profile_read": [c_void_p, c_int32, POINTER(c_int32), POINTER(c_double)],
     "sbd_status_string": [c_int32],
@@ -249,6 +251,11 @@ class Sbd:
         v = torch.empty(shp, dtype=torch.bfloat16, device=self.device)
         self._call("sbd_kv_export", int(seq), int(pos0), int(n), _dev(k), _dev(v))
         return k, v
+
+    def set_decode_path(self, path: str):
+        """Kernels of decode-sized forwards: "auto", "fused" or "kernels" (sbd_set_decode_path)."""
+        code = DECODE_PATHS[path]
+        _check(self.lib, self.lib.sbd_set_decode_path(self.ctx, code), "sbd_set_decode_path", self.ctx)
 
     def profile(self, enable: bool):
         _check(self.lib, self.lib.sbd_profile_enable(self.ctx, int(bool(enable))),

@@ -30,90 +30,9 @@
 // its weight stream starts, and scales its fp32 products by rinv[m] = 1/sqrt(mean(x^2) +
 // eps), which equals normalising the input because the scale is constant along a row.
 
-#include "sbd_device.h"
+#include "qkv_epilogue.h"
 
 namespace sbd {
-
-// QKV epilogue of one packed group (8 tiles = 128 columns = 128 / DH whole heads), run by
-// one wave holding all 8 accumulator tiles.
-template <int DH>
-__device__ __forceinline__ void qkv_epilogue(const GemvArgs& a, int grp, const f32x4 (&acc)[8],
-                                             const float (&rinv)[4]) {
-  constexpr int tph = DH / 16, ptiles = tph / 2, half = DH / 2, heads = 8 / tph;
-  const QkvEpi& e = a.qkv;
-  const int lane = threadIdx.x & 63;
-  const int r = lane & 15, g = lane >> 4;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int m = 4 * g + i;
-    const bool row_ok = m < a.M;
-    const float rv = row_ok ? rinv[i] : 0.f;
-    float u[8];
-#pragma unroll
-    for (int ct = 0; ct < 8; ++ct) u[ct] = acc[ct][i] * rv;
-#pragma unroll
-    for (int hh = 0; hh < heads; ++hh) {
-      const int h = grp * heads + hh;  // q heads, then k heads, then v heads
-      if (e.qk_norm && h < e.n_q + e.n_kv) {
-        float ss = 0.f;
-#pragma unroll
-        for (int t = 0; t < tph; ++t) ss += u[hh * tph + t] * u[hh * tph + t];
-        ss += __shfl_xor(ss, 1);
-        ss += __shfl_xor(ss, 2);
-        ss += __shfl_xor(ss, 4);
-        ss += __shfl_xor(ss, 8);
-        const float rn = 1.0f / sqrtf(ss / (float)DH + e.eps);
-        const bf16_t* gn = h < e.n_q ? e.q_norm : e.k_norm;
-#pragma unroll
-        for (int t = 0; t < tph; ++t) u[hh * tph + t] *= rn * bf2f(gn[16 * t + r]);
-      }
-    }
-    if (!row_ok) continue;
-    const int b = m / e.kblk, j = m % e.kblk;
-    const SeqParam sp = e.seqs[b];
-    const int p_cache = sp.cache_len + j;
-    const int pos = e.rows[m].pos;
-#pragma unroll
-    for (int hh = 0; hh < heads; ++hh) {
-      const int h = grp * heads + hh;
-      if (h >= e.n_q + e.n_kv) {  // V: transposed cache block, slot order of misc.hip vslot()
-        const int gk = h - e.n_q - e.n_kv;
-        bf16_t* blk = e.vcache + (((int64_t)e.layer * e.n_slots + sp.slot) * e.n_kv + gk) * e.cap * DH +
-                      (int64_t)(p_cache / 32) * DH * 32;
-        const int p = p_cache & 31;
-        const int sl = ((p & 15) >> 2) * 8 + (p >> 4) * 4 + (p & 3);
-#pragma unroll
-        for (int t = 0; t < tph; ++t) blk[(16 * t + r) * 32 + sl] = f2bf(u[hh * tph + t]);
-        continue;
-      }
-#pragma unroll
-      for (int pr = 0; pr < ptiles; ++pr) {
-        const int dim = pr * 16 + r;
-        const float cs = e.rope[((int64_t)pos * half + dim) * 2 + 0];
-        const float sn = e.rope[((int64_t)pos * half + dim) * 2 + 1];
-        const float u0 = u[hh * tph + pr], u1 = u[hh * tph + pr + ptiles];
-        const float r0 = u0 * cs - u1 * sn;
-        const float r1 = u1 * cs + u0 * sn;
-        if (h < e.n_q) {
-          const int64_t o = ((int64_t)m * e.n_q + h) * DH;
-          bf16_t hi, lo;
-          split_bf16(r0 * e.q_scale, hi, lo);
-          e.q[o + dim] = hi;
-          e.q_lo[o + dim] = lo;
-          split_bf16(r1 * e.q_scale, hi, lo);
-          e.q[o + dim + half] = hi;
-          e.q_lo[o + dim + half] = lo;
-        } else {
-          const int gk = h - e.n_q;
-          bf16_t* dst = e.kcache + (((int64_t)e.layer * e.n_slots + sp.slot) * e.n_kv + gk) * e.cap * DH +
-                        (int64_t)p_cache * DH;
-          dst[dim] = f2bf(r0);
-          dst[dim + half] = f2bf(r1);
-        }
-      }
-    }
-  }
-}
 
 // Tile ct of a workgroup is summed and finished by wave ct % NW.
 template <int NW>
@@ -275,7 +194,7 @@ __global__ __launch_bounds__(NW * 64) void gemv_kernel(GemvArgs a) {
 #pragma unroll
       for (int ct = 0; ct < C; ++ct) acc[ct] = fin[ct][lane];
     }
-    qkv_epilogue<DH>(a, sub, acc, rinv);
+    qkv_epilogue<DH, false>(a.qkv, a.M, sub, acc, rinv);
     return;
   } else {
 #pragma unroll

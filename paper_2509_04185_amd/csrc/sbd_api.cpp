@@ -91,8 +91,15 @@ bool sbd::compute_layout(const sbd_model_config& c, Layout* L) {
   o.wp_lm = o.wp_layer * c.n_layers;
   o.wpack = take((o.wp_lm + (int64_t)c.vocab * c.d_model) * 2);
   const int64_t widest = std::max<int64_t>(std::max<int64_t>(o.n_qkv, 2 * (int64_t)c.ffn_dim), c.d_model);
-  o.gemv_part_floats = (int64_t)kGemvMaxSplit * 16 * widest;
+  // split-K partials of the per-kernel path, or the parked partial tiles of the fused forward
+  o.gemv_part_floats = std::max<int64_t>((int64_t)kGemvMaxSplit * 16 * widest, (int64_t)kFwdMaxWorkgroups * kFwdPartFloats);
   o.gemv_part = take(o.gemv_part_floats * sizeof(float));
+  o.xn2 = take(2 * o.m_max * c.d_model * 2);
+  o.sumsq2 = take(o.m_max * o.n_part * sizeof(float));
+  o.fwd_gains = take((int64_t)c.n_layers * sizeof(FwdGains));
+  o.fwd_ctl_ints = (int64_t)c.n_layers * fused_counters_per_layer(c.n_kv_heads, o.n_qkv, c.d_model, c.ffn_dim);
+  o.fwd_ctl = take(o.fwd_ctl_ints * sizeof(int32_t));
+  o.fwd_err = take(2 * sizeof(int32_t));
   o.counters = take((int64_t)kCounters * sizeof(int32_t));
   o.total = off;
   *L = o;
@@ -121,6 +128,10 @@ struct sbd_ctx {
   std::vector<hipEvent_t> pool;
   int32_t prof_count[SBD_KERNEL_COUNT] = {};
   double prof_ms[SBD_KERNEL_COUNT] = {};
+  // decode path for M <= 16 (sbd_set_decode_path)
+  int decode_path = SBD_DECODE_KERNELS;
+  int n_cu = 0;                 // workgroups of the fused forward: one per CU, at most kFwdMaxWorkgroups
+  int32_t* err_host = nullptr;  // pinned copy of the fused forward's sticky error word
 
   template <class T>
   T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
@@ -149,6 +160,10 @@ sbd_status fail(sbd_ctx* c, sbd_status st, const char* fmt, ...) {
 sbd_status check_sticky(sbd_ctx* c) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(c, SBD_ERR_HIP, "earlier HIP error: %s", hipGetErrorString(e));
+  // written by copies queued after each fused forward; it never goes back to zero
+  if (c->err_host != nullptr && __atomic_load_n(c->err_host, __ATOMIC_ACQUIRE) != 0)
+    return fail(c, SBD_ERR_HIP, "a fused decode forward gave up waiting (task code %d)",
+                __atomic_load_n(c->err_host + 1, __ATOMIC_ACQUIRE));
   return SBD_OK;
 }
 
@@ -254,6 +269,40 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   int n_splits = pick_splits((int64_t)B * nkv * n_rb, nblocks);
   const int bps = (nblocks + n_splits - 1) / n_splits;
   n_splits = (nblocks + bps - 1) / bps;
+
+  if (small && c->decode_path != SBD_DECODE_KERNELS) {
+    // the whole decode forward as one launch (fused.hip)
+    FwdArgs f{};
+    f.M = M; f.B = B; f.k = k; f.n_layers = m.n_layers;
+    f.d = d; f.n_q = nq; f.n_kv = nkv; f.d_h = dh; f.ffn = m.ffn_dim; f.vocab = m.vocab; f.qk_norm = m.qk_norm;
+    f.eps = m.rms_eps;
+    f.q_scale = (float)(1.4426950408889634 / std::sqrt((double)dh));
+    f.wpack = c->at<bf16_t>(L.wpack);
+    f.wp_layer = L.wp_layer; f.wp_o = L.wp_o; f.wp_gu = L.wp_gu; f.wp_down = L.wp_down; f.wp_lm = L.wp_lm;
+    f.gains = c->at<FwdGains>(L.fwd_gains); f.final_norm = c->final_norm;
+    f.rows = drows; f.seqs = dseqs;
+    f.x = x; f.xn_d = xn; f.xn_d_lo = xn_lo;
+    f.xn_o = c->at<bf16_t>(L.xn2); f.xn_o_lo = f.xn_o + L.m_max * d;
+    f.ssq_d = sumsq; f.ssq_o = c->at<float>(L.sumsq2); f.n_part_embed = d / 16;
+    f.q = q; f.q_lo = q_lo; f.attn = attn; f.attn_lo = attn_lo; f.act = act; f.act_lo = act_lo;
+    f.kcache = c->at<bf16_t>(L.kcache); f.vcache = c->at<bf16_t>(L.vcache); f.cap = L.cap;
+    f.n_slots = m.max_batch; f.rope = c->at<float>(L.rope);
+    f.n_rowblocks = n_rb; f.n_splits = n_splits; f.blocks_per_split = bps;
+    f.part_ml = c->at<float>(L.attn_ml); f.part_o = c->at<float>(L.attn_o);
+    f.part = vpart;
+    f.logits = logits; f.lm_row0 = lm_row < 0 ? 0 : lm_row; f.lm_rows = lm_row < 0 ? M : 1;
+    f.ctl = c->at<int>(L.fwd_ctl); f.err = c->at<int>(L.fwd_err);
+    const bool fits = c->n_cu > 0 && fused_plan(f, c->n_cu, vpart_cap) && f.plan.n_ctl <= L.fwd_ctl_ints;
+    if (!fits && c->decode_path == SBD_DECODE_FUSED)
+      return fail(c, SBD_ERR_UNSUPPORTED, "the fused decode forward does not fit this model or device (%d CUs)",
+                  c->n_cu);
+    if (fits) {
+      SBD_HIP(c, hipMemsetAsync(f.ctl, 0, (size_t)f.plan.n_ctl * sizeof(int32_t), c->stream));
+      SBD_LAUNCH(c, SBD_KERNEL_FUSED, launch_fused_forward(f, c->n_cu, ex));
+      SBD_HIP(c, hipMemcpyAsync(c->err_host, f.err, 2 * sizeof(int32_t), hipMemcpyDeviceToHost, c->stream));
+      return SBD_OK;
+    }
+  }
 
   for (int l = 0; l < m.n_layers; ++l) {
     const LayerW& w = c->layers[l];
@@ -498,6 +547,23 @@ sbd_status sbd_create(const sbd_model_config* cfg, const sbd_weights* w, void* w
   }
   ok = ok && launch_pack(c->lm_head, nullptr, c->at<bf16_t>(L.wpack) + L.wp_lm, cfg->vocab, d, 0,
                          c->stream) == hipSuccess;
+  // fused decode forward: per-layer gains, error word (sticky) and its pinned host copy
+  if (ok) {
+    std::vector<FwdGains> gains(cfg->n_layers);
+    for (int l = 0; l < cfg->n_layers; ++l)
+      gains[l] = FwdGains{c->layers[l].attn_norm, c->layers[l].mlp_norm, c->layers[l].q_norm, c->layers[l].k_norm};
+    ok = hipMemcpy(c->ws + L.fwd_gains, gains.data(), gains.size() * sizeof(FwdGains), hipMemcpyHostToDevice) ==
+             hipSuccess &&
+         hipMemsetAsync(c->ws + L.fwd_err, 0, 2 * sizeof(int32_t), c->stream) == hipSuccess &&
+         hipHostMalloc((void**)&c->err_host, 2 * sizeof(int32_t), hipHostMallocDefault) == hipSuccess;
+    if (ok) c->err_host[0] = c->err_host[1] = 0;
+    else c->err_host = nullptr;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      c->n_cu = 0;
+    c->n_cu = std::min(c->n_cu, kFwdMaxWorkgroups);
+  }
   if (!ok) {
     c->err = "initialising the workspace failed";
     return cleanup(SBD_ERR_HIP);
@@ -518,6 +584,7 @@ sbd_status sbd_destroy(sbd_ctx* c) {
     if (c->stage[i]) (void)hipHostFree(c->stage[i]);
     if (c->ev[i]) (void)hipEventDestroy(c->ev[i]);
   }
+  if (c->err_host) (void)hipHostFree(c->err_host);
   delete c;
   return SBD_OK;
 }
@@ -717,6 +784,14 @@ sbd_status sbd_kv_export(sbd_ctx* c, int32_t seq, int32_t pos0, int32_t n, void*
   a.d_h = c->cfg.head_dim; a.slot = seq; a.pos0 = pos0; a.n = n;
   a.k_out = static_cast<bf16_t*>(k); a.v_out = static_cast<bf16_t*>(v);
   SBD_HIP(c, launch_kv_export(a, c->stream));
+  return SBD_OK;
+}
+
+sbd_status sbd_set_decode_path(sbd_ctx* c, int32_t path) {
+  if (!c) return fail(nullptr, SBD_ERR_INVALID_ARG, "null context");
+  if (path != SBD_DECODE_AUTO && path != SBD_DECODE_FUSED && path != SBD_DECODE_KERNELS)
+    return fail(c, SBD_ERR_INVALID_ARG, "unknown decode path %d", path);
+  c->decode_path = path;
   return SBD_OK;
 }
 

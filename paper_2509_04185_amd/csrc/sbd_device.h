@@ -97,6 +97,36 @@ __device__ __forceinline__ float load_coherent(const float* p) {
 #endif
 }
 
+// Device-scope (sc1) accesses for data that one workgroup writes and a workgroup on another
+// XCD reads later in the same launch: the stores write through to the coherence point and
+// the loads bypass possibly stale L2 lines.  Buffer forms take a wave-uniform base (a
+// buffer resource) and a per-lane byte offset.
+constexpr int kPolicyDevice = 16;  // cache-policy bits of a device-scope access (sc1)
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, 0x7fffffff, 0x00020000);
+}
+__device__ __forceinline__ i32x4 ld16_dev(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, kPolicyDevice);
+}
+__device__ __forceinline__ float ld32_dev(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, byte_off, 0, kPolicyDevice));
+}
+__device__ __forceinline__ void st16_dev(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, i32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, byte_off, 0, kPolicyDevice);
+}
+__device__ __forceinline__ void st_bf16_dev(bf16_t* p, bf16_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_f32_dev(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_f32_dev(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int ld_i32_dev(const int* p) {
+  return __hip_atomic_load(const_cast<int*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 __device__ __forceinline__ bool last_arrival(int* counter, int expected) {
   __shared__ int s_last;
 #if SBD_SPLITK_SYNC == 0

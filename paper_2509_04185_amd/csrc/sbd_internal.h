@@ -55,6 +55,9 @@ struct Layout {
   int64_t wp_o, wp_gu, wp_down, wp_lm;
   size_t attn_ml, attn_o, rows, seqs, eb_mask, eb_part, eb_arg, gemv_part, counters;
   int64_t gemv_part_floats;  // split-K partial tiles of the decode GEMM
+  size_t xn2, sumsq2;        // fused decode forward: second copy of xn (hi, lo) and its partials
+  size_t fwd_gains, fwd_ctl, fwd_err;
+  int64_t fwd_ctl_ints;
   size_t total;
 };
 
@@ -238,6 +241,59 @@ struct AttnArgs {
 };
 hipError_t launch_attention_split(const AttnArgs& a, const Exec& ex);
 hipError_t launch_attention_merge(const AttnArgs& a, const Exec& ex);
+
+// ---------------------------------------------------------------------------- fused decode forward
+// The whole decode-sized forward (M <= 16 rows: every layer, then the LM head) as one launch
+// of one persistent workgroup per CU (fused.hip); phases are separated by counters.
+enum FwdPhase { PH_QKV = 0, PH_ATTN, PH_MERGE, PH_O, PH_GU, PH_DOWN, PH_N };
+constexpr int kFwdMaxWorkgroups = 256;       // persistent workgroups (one per CU) at most
+constexpr int kFwdPartFloats = 2 * 8 * 256;  // parked partial tiles per workgroup: 2 groups x 8 tiles
+// Counters of one layer: the phase counters, one per KV head, one per group of each GEMM phase.
+inline int64_t fused_counters_per_layer(int n_kv, int64_t n_qkv, int d, int ffn) {
+  return 5 + n_kv + n_qkv / 128 + 2 * (d / 128) + 2 * (int64_t)ffn / 128;
+}
+struct FwdGains {
+  const bf16_t *attn_norm, *mlp_norm, *q_norm, *k_norm;
+};
+struct FwdPlan {
+  int groups[PH_N];    // 128-column groups of the GEMM phases
+  // counters (int32) of layer l start at ctl[ctr0 + l * ctr_stride]
+  int ctr0, ctr_stride;
+  int c_down_done, c_attn_ready, c_attn_done, c_merge_done, c_o_done, c_gu_done;
+  int c_arr_q, c_arr_o, c_arr_gu, c_arr_d;  // per-group arrival counters of the GEMM phases
+  int n_ctl;           // int32 words to zero before a launch
+};
+struct FwdArgs {
+  int M, B, k, n_layers;
+  int d, n_q, n_kv, d_h, ffn, vocab, qk_norm;
+  float eps, q_scale;
+  const bf16_t* wpack;
+  int64_t wp_layer, wp_o, wp_gu, wp_down, wp_lm;
+  const FwdGains* gains;  // [n_layers], device
+  const bf16_t* final_norm;
+  const RowParam* rows;
+  const SeqParam* seqs;
+  float* x;               // residual stream [M][d]
+  bf16_t *xn_d, *xn_d_lo; // x * g after the embedding or a down projection (QKV, LM head input)
+  bf16_t *xn_o, *xn_o_lo; // x * g after an O projection (gate/up input)
+  float *ssq_d, *ssq_o;   // their partial sums of x^2
+  int n_part_embed;       // partials per row written by the embedding (later: one per group)
+  bf16_t *q, *q_lo, *attn, *attn_lo, *act, *act_lo;
+  bf16_t *kcache, *vcache;
+  int64_t cap;
+  int n_slots;
+  const float* rope;
+  int n_rowblocks, n_splits, blocks_per_split;
+  float *part_ml, *part_o;
+  float* part;            // split-K partial tiles
+  float* logits;          // LM head output [lm_rows][vocab]
+  int lm_row0, lm_rows;
+  FwdPlan plan;
+  int* ctl;               // dependency and arrival counters, zeroed before every launch
+  int* err;               // [0] sticky error flag, [1] the task that gave up waiting
+};
+bool fused_plan(FwdArgs& f, int nwg, int64_t part_cap_floats);
+hipError_t launch_fused_forward(const FwdArgs& f, int nwg, const Exec& ex);
 
 // ---------------------------------------------------------------------------- EB sampler
 struct EbArgs {

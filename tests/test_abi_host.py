@@ -105,6 +105,7 @@ def test_null_context_is_rejected(lib):
     assert lib.sbd_commit(None, 1, None, None) == 1
     assert lib.sbd_prefill(None, 0, None, 1, None) == 1
     assert lib.sbd_destroy(None) == 1
+    assert lib.sbd_set_decode_path(None, 0) == 1
     assert lib.sbd_kv_import(None, 0, 0, 1, None, None) == 1
     n = ctypes.c_int32()
     assert lib.sbd_cache_len(None, 0, ctypes.byref(n)) == 1

@@ -73,12 +73,17 @@ def test_fullsize_block_forward(name):
     if sample == "minmax":
         sample = [int(np.argmin(lens)), int(np.argmax(lens))]
     toks, is_mask = synth.block_rows(wl.seed, s, wl.batch, wl.k, n_causal=1)
-    logits = lib.block_forward(list(range(wl.batch)), toks, is_mask=is_mask)
-    n_acc, _, _, _ = lib.eb_select(logits, is_mask, wl.gammas[0], s.mask_id)
-    torch.cuda.synchronize()
-    assert (n_acc >= 1).all()
-    got = logits[sample].cpu().numpy()
-    del logits
+    # a decode-sized forward (<= 16 rows) is checked on both of its paths
+    paths = ["fused", "kernels"] if wl.batch * wl.k <= 16 else ["auto"]
+    got = {}
+    for path in paths:
+        lib.set_decode_path(path)
+        logits = lib.block_forward(list(range(wl.batch)), toks, is_mask=is_mask)
+        n_acc, _, _, _ = lib.eb_select(logits, is_mask, wl.gammas[0], s.mask_id)
+        torch.cuda.synchronize()
+        assert (n_acc >= 1).all()
+        got[path] = logits[sample].cpu().numpy()
+        del logits
     host = synth.weights_to_host(w)
     model = O.Model(s, host, dtype=np.float32, cache_decoded=False, kv_bf16=True)
     caches = []
@@ -88,7 +93,9 @@ def test_fullsize_block_forward(name):
         del kk, vv
     print(f"    oracle on sequences {sample} (cache {[lens[b] for b in sample]})", flush=True)
     ref = model.block_forward(caches, toks[sample], [1] * len(sample)).logits
-    close(got, ref)
+    for path in paths:
+        print(f"    decode path {path}", flush=True)
+        close(got[path], ref)
     eb_bit_exact(lib, ref.astype(np.float32), is_mask[sample], wl.gammas, s.mask_id)
 
 
@@ -114,6 +121,7 @@ def test_benched_configuration_with_real_prefill():
     s = wl.shape
     print("[gpu] benched configuration: prefill 2048 + block forward", flush=True)
     w, lib, lens = make_ctx(wl, import_cache=False)
+    lib.set_decode_path("fused")
     prompt = synth.make_tokens(wl.seed, lens[0], s, stream=100)
     last = lib.prefill(0, prompt)
     toks, is_mask = synth.block_rows(wl.seed, s, 1, wl.k, n_causal=1)

@@ -35,25 +35,33 @@ def to_dev(w, dev):
 
 
 class Tiny:
-    def __init__(self, shape, seed, max_batch=4, max_seq_len=256, max_block=16, chunk=0):
+    def __init__(self, shape, seed, max_batch=4, max_seq_len=256, max_block=16, chunk=0, path="auto"):
         from paper_2509_04185_amd import Sbd
-        print(f"[gpu] building {shape.name} seed={seed} batch={max_batch}", flush=True)
+        print(f"[gpu] building {shape.name} seed={seed} batch={max_batch} decode path {path}", flush=True)
         self.shape = shape
+        self.path = path
         self.w_cpu = synth.make_weights(shape, seed)
         self.lib = Sbd(shape, to_dev(self.w_cpu, "cuda"), max_batch=max_batch,
                        max_seq_len=max_seq_len, max_block=max_block, prefill_chunk=chunk)
+        self.lib.set_decode_path(path)
         # The KV cache stores bf16: the oracle rounds K/V the same way (activations stay fp64).
         self.model = O.Model(shape, synth.weights_to_host(self.w_cpu), dtype=np.float64, kv_bf16=True)
 
 
-@pytest.fixture(scope="module")
-def tiny():
-    return Tiny(synth.TINY, 1001)
+# Decode-sized forwards (<= 16 rows) run either as the fused single launch or as one kernel
+# per step; every forward test runs on both.  "fused" makes a forward the fused launch cannot
+# take an error, so these tests cannot pass on the other path by accident.
+PATHS = ["fused", "kernels"]
 
 
-@pytest.fixture(scope="module")
-def tiny_qk():
-    return Tiny(synth.TINY_QK, 2002, chunk=24)
+@pytest.fixture(scope="module", params=PATHS)
+def tiny(request):
+    return Tiny(synth.TINY, 1001, path=request.param)
+
+
+@pytest.fixture(scope="module", params=PATHS)
+def tiny_qk(request):
+    return Tiny(synth.TINY_QK, 2002, chunk=24, path=request.param)
 
 
 def fresh(t, seqs=(0, 1, 2, 3)):
@@ -315,6 +323,27 @@ def test_intermediate_buffers_last_layer(tiny):
     close(pair("attn"), o, max_abs=1e-3, rel_l2=1e-4)
 
 
+def test_decode_path_kernels_launched(tiny):
+    """The selected decode path is the one that runs: one fused launch, or none."""
+    fresh(tiny)
+    s = tiny.shape
+    tiny.lib.prefill(0, synth.make_tokens(70, 20, s), want_logits=False)
+    toks, is_mask = synth.block_rows(71, s, 1, 16, n_causal=1)
+    tiny.lib.profile(True)
+    try:
+        tiny.lib.profile_read()
+        tiny.lib.block_forward([0], toks, is_mask=is_mask)
+        stats = tiny.lib.profile_read()
+    finally:
+        tiny.lib.profile(False)
+    launches = {k: n for k, (n, _) in stats.items() if n}
+    print(f"    launches {launches}", flush=True)
+    if tiny.path == "fused":
+        assert launches.get("fused") == 1 and "qkv" not in launches and "lm_head" not in launches
+    else:
+        assert "fused" not in launches and launches.get("qkv") == s.n_layers
+
+
 # ------------------------------------------------------------------ state machine and errors
 
 
@@ -350,6 +379,7 @@ def test_state_and_argument_errors(tiny):
     err(lambda: lib.eb_select(logits, is_mask, -0.1, s.mask_id), "SBD_ERR_INVALID_ARG")
     err(lambda: lib.eb_select(torch.zeros((1, 4, 2048), device="cuda"), is_mask, 1.0, -1),
         "SBD_ERR_INVALID_ARG")
+    assert lib.lib.sbd_set_decode_path(lib.ctx, 3) == 1                     # unknown path
     # a failed call changes nothing
     assert lib.cache_len(0) == 11
     lib.block_forward([0], toks, n_causal=[1])
