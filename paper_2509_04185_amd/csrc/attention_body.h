@@ -277,6 +277,21 @@ __device__ __forceinline__ void attn_merge_body(const AttnArgs& a, int64_t item)
   const int lane = threadIdx.x & 63;
   const __amdgpu_buffer_rsrc_t rml = buf_rsrc(a.part_ml), ro = buf_rsrc(a.part_o);
   const int ns = a.n_splits;  // <= 64
+  constexpr int PER = DH / 64;
+  const int64_t po = item * DH + lane;
+  const int64_t split_stride = n_items * DH;
+  auto ld_part = [&](int64_t e) -> float {
+    if constexpr (DEV) return ld32_dev(ro, (uint32_t)(e * 4));
+    else return a.part_o[e];
+  };
+  // Every load is requested before any is used: the (max, sum) pairs and the partial
+  // outputs of the first kBatch splits, then the partial outputs kBatch splits at a time.
+  constexpr int kBatch = 32;
+  float v[kBatch][PER];
+#pragma unroll
+  for (int u = 0; u < kBatch; ++u)
+#pragma unroll
+    for (int e = 0; e < PER; ++e) v[u][e] = (u < ns) ? ld_part(po + (int64_t)u * split_stride + 64 * e) : 0.f;
   float ms = -INFINITY, ls = 0.f;
   if (lane < ns) {
     const int64_t e = ((int64_t)lane * n_items + item) * 2;
@@ -284,41 +299,31 @@ __device__ __forceinline__ void attn_merge_body(const AttnArgs& a, int64_t item)
       ms = ld32_dev(rml, (uint32_t)(e * 4));
       ls = ld32_dev(rml, (uint32_t)(e * 4 + 4));
     } else {
-      const float2 v = *(const float2*)(a.part_ml + e);
-      ms = v.x;
-      ls = v.y;
+      const float2 mv = *(const float2*)(a.part_ml + e);
+      ms = mv.x;
+      ls = mv.y;
     }
   }
   const float mx = wave_max(ms);
   const float wgt = (ms == -INFINITY) ? 0.f : exp2f(ms - mx);
   const float lsum = wave_sum(wgt * ls);
-  constexpr int PER = DH / 64;
   float acc[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) acc[e] = 0.f;
-  const int64_t po = item * DH + lane;
-  const int64_t split_stride = n_items * DH;
-  auto ld_part = [&](int64_t e) -> float {
-    if constexpr (DEV) return ld32_dev(ro, (uint32_t)(e * 4));
-    else return a.part_o[e];
-  };
-  // the first kFirst splits' partial outputs are all requested before any is used
-  constexpr int kFirst = 16;
-  float v[kFirst][PER];
+  for (int s0 = 0; s0 < ns; s0 += kBatch) {  // wave-uniform
+    if (s0 > 0) {
 #pragma unroll
-  for (int u = 0; u < kFirst; ++u)
+      for (int u = 0; u < kBatch; ++u)
 #pragma unroll
-    for (int e = 0; e < PER; ++e) v[u][e] = (u < ns) ? ld_part(po + (int64_t)u * split_stride + 64 * e) : 0.f;
+        for (int e = 0; e < PER; ++e)
+          v[u][e] = (s0 + u < ns) ? ld_part(po + (int64_t)(s0 + u) * split_stride + 64 * e) : 0.f;
+    }
 #pragma unroll
-  for (int u = 0; u < kFirst; ++u) {
-    const float wu = __shfl(wgt, u);
+    for (int u = 0; u < kBatch; ++u) {
+      const float wu = __shfl(wgt, s0 + u);
 #pragma unroll
-    for (int e = 0; e < PER; ++e) acc[e] += wu * v[u][e];
-  }
-  for (int s = kFirst; s < ns; ++s) {
-    const float wu = __shfl(wgt, s);
-#pragma unroll
-    for (int e = 0; e < PER; ++e) acc[e] += wu * ld_part(po + (int64_t)s * split_stride + 64 * e);
+      for (int e = 0; e < PER; ++e) acc[e] += wu * v[u][e];
+    }
   }
   const float inv = 1.0f / lsum;
   const int64_t orow = item / a.n_q;

@@ -97,7 +97,10 @@ bool sbd::compute_layout(const sbd_model_config& c, Layout* L) {
   o.xn2 = take(2 * o.m_max * c.d_model * 2);
   o.sumsq2 = take(o.m_max * o.n_part * sizeof(float));
   o.fwd_gains = take((int64_t)c.n_layers * sizeof(FwdGains));
-  o.fwd_ctl_ints = (int64_t)c.n_layers * fused_counters_per_layer(c.n_kv_heads, o.n_qkv, c.d_model, c.ffn_dim);
+  const int64_t n_rb_max = ((int64_t)(c.n_q_heads / c.n_kv_heads) * c.max_block + 63) / 64;
+  o.fwd_ctl_ints = (int64_t)c.n_layers *
+                   fused_counters_per_layer(c.n_kv_heads, o.n_qkv, c.d_model, c.ffn_dim,
+                                            (int64_t)c.max_batch * c.n_kv_heads * n_rb_max);
   o.fwd_ctl = take(o.fwd_ctl_ints * sizeof(int32_t));
   o.fwd_err = take(2 * sizeof(int32_t));
   o.counters = take((int64_t)kCounters * sizeof(int32_t));
@@ -287,7 +290,13 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     f.q = q; f.q_lo = q_lo; f.attn = attn; f.attn_lo = attn_lo; f.act = act; f.act_lo = act_lo;
     f.kcache = c->at<bf16_t>(L.kcache); f.vcache = c->at<bf16_t>(L.vcache); f.cap = L.cap;
     f.n_slots = m.max_batch; f.rope = c->at<float>(L.rope);
-    f.n_rowblocks = n_rb; f.n_splits = n_splits; f.blocks_per_split = bps;
+    // key splits: as many as fit one attention task per workgroup
+    {
+      const int per = B * nkv * n_rb;
+      const int fit = std::max(1, std::min(kMaxSplits, std::max(1, c->n_cu) / per));
+      const int fbps = (nblocks + std::min(fit, nblocks) - 1) / std::min(fit, nblocks);
+      f.n_rowblocks = n_rb; f.blocks_per_split = fbps; f.n_splits = (nblocks + fbps - 1) / fbps;
+    }
     f.part_ml = c->at<float>(L.attn_ml); f.part_o = c->at<float>(L.attn_o);
     f.part = vpart;
     f.logits = logits; f.lm_row0 = lm_row < 0 ? 0 : lm_row; f.lm_rows = lm_row < 0 ? M : 1;

@@ -36,6 +36,14 @@ __device__ __forceinline__ uint32_t pack_bf2(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2{a, b}), bf16x2));
 }
 
+// Four floats as hi = bf16(v) and lo = bf16(v - hi), each packed into two 32-bit words.
+__device__ __forceinline__ void split_bf16x4(f32x4 v, i32x2& hi, i32x2& lo) {
+  const uint32_t h0 = pack_bf2(v[0], v[1]), h1 = pack_bf2(v[2], v[3]);
+  hi = i32x2{(int)h0, (int)h1};
+  lo = i32x2{(int)pack_bf2(v[0] - __uint_as_float(h0 << 16), v[1] - __uint_as_float(h0 & 0xffff0000u)),
+             (int)pack_bf2(v[2] - __uint_as_float(h1 << 16), v[3] - __uint_as_float(h1 & 0xffff0000u))};
+}
+
 // 16-byte loads; the streaming variant marks the line non-temporal (read once).
 __device__ __forceinline__ i32x4 ld16(const void* p) { return *(const i32x4*)p; }
 __device__ __forceinline__ i32x4 ld16_stream(const void* p) {
@@ -113,6 +121,9 @@ __device__ __forceinline__ float ld32_dev(__amdgpu_buffer_rsrc_t r, uint32_t byt
 }
 __device__ __forceinline__ void st16_dev(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, i32x4 v) {
   __builtin_amdgcn_raw_buffer_store_b128(v, r, byte_off, 0, kPolicyDevice);
+}
+__device__ __forceinline__ void st8_dev(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, i32x2 v) {
+  __builtin_amdgcn_raw_buffer_store_b64(v, r, byte_off, 0, kPolicyDevice);
 }
 __device__ __forceinline__ void st_bf16_dev(bf16_t* p, bf16_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

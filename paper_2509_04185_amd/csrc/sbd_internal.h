@@ -247,19 +247,27 @@ hipError_t launch_attention_merge(const AttnArgs& a, const Exec& ex);
 // of one persistent workgroup per CU (fused.hip); phases are separated by counters.
 enum FwdPhase { PH_QKV = 0, PH_ATTN, PH_MERGE, PH_O, PH_GU, PH_DOWN, PH_N };
 constexpr int kFwdMaxWorkgroups = 256;       // persistent workgroups (one per CU) at most
-constexpr int kFwdPartFloats = 2 * 8 * 256;  // parked partial tiles per workgroup: 2 groups x 8 tiles
-// Counters of one layer: the phase counters, one per KV head, one per group of each GEMM phase.
-inline int64_t fused_counters_per_layer(int n_kv, int64_t n_qkv, int d, int ffn) {
-  return 5 + n_kv + n_qkv / 128 + 2 * (d / 128) + 2 * (int64_t)ffn / 128;
+constexpr int kFwdMaxKw = 16;                // workgroups sharing one 128-column group at most
+constexpr int kFwdPartFloats = 2048;         // parked partial of one workgroup: 16 rows x 128 columns
+// Counters of one layer: phase counters, two per KV head, one per (sequence, KV head, row
+// block) of the attention, one per group of each GEMM phase.
+inline int64_t fused_counters_per_layer(int n_kv, int64_t n_qkv, int d, int ffn, int64_t n_attn_groups) {
+  return 3 + 2 * n_kv + n_attn_groups + n_qkv / 128 + 2 * (d / 128) + 2 * (int64_t)ffn / 128;
 }
 struct FwdGains {
   const bf16_t *attn_norm, *mlp_norm, *q_norm, *k_norm;
 };
 struct FwdPlan {
   int groups[PH_N];    // 128-column groups of the GEMM phases
+  int kw[PH_N];        // workgroups per group (each a 1/kw slice of K)
+  int units[PH_N];     // groups x kw: completion count of a phase
+  int attn_ready_target, merge_target;
   // counters (int32) of layer l start at ctl[ctr0 + l * ctr_stride]
   int ctr0, ctr_stride;
-  int c_down_done, c_attn_ready, c_attn_done, c_merge_done, c_o_done, c_gu_done;
+  int c_down_done, c_o_done, c_gu_done;
+  int c_attn_ready;    // [n_kv] QKV units done per KV head
+  int c_merge_done;    // [n_kv] merge tasks done per KV head
+  int c_arr_attn;      // [B][n_kv][row blocks] split tasks done
   int c_arr_q, c_arr_o, c_arr_gu, c_arr_d;  // per-group arrival counters of the GEMM phases
   int n_ctl;           // int32 words to zero before a launch
 };
