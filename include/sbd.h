@@ -198,14 +198,13 @@ sbd_status sbd_workspace_region(const sbd_model_config* cfg, const char* name, s
 /*
  * Which kernels run a decode-sized forward (at most 16 rows: sbd_block_forward with
  * batch * k <= 16, and prefill chunks that small).
- *   SBD_DECODE_AUTO     the fused forward (every layer and the LM head in one launch of one
- *                       persistent workgroup per CU) when the model and device fit it, else
- *                       one kernel per step.
- *   SBD_DECODE_FUSED    the fused forward; a forward it cannot take fails with
- *                       SBD_ERR_UNSUPPORTED.  It needs d_model a multiple of 128, head_dim 64
- *                       or 128, and at most as many 128-column weight groups per projection
- *                       as the device has CUs (capped at 256).
- *   SBD_DECODE_KERNELS  one kernel per step (the default: the faster of the two at present).
+ *   SBD_DECODE_AUTO     the library's choice (the default); at present one kernel per step,
+ *                       the faster of the two on MI355X.
+ *   SBD_DECODE_FUSED    the fused forward: every layer and the LM head in one launch of one
+ *                       persistent workgroup per CU.  A forward it cannot take fails with
+ *                       SBD_ERR_UNSUPPORTED: it needs d_model a multiple of 128 and head_dim
+ *                       64 or 128.
+ *   SBD_DECODE_KERNELS  one kernel per step.
  * Both give the same results up to float summation order.  Larger forwards always run one
  * kernel per step.  INVALID_ARG for another value.
  */

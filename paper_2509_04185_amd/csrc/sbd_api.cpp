@@ -132,7 +132,7 @@ struct sbd_ctx {
   int32_t prof_count[SBD_KERNEL_COUNT] = {};
   double prof_ms[SBD_KERNEL_COUNT] = {};
   // decode path for M <= 16 (sbd_set_decode_path)
-  int decode_path = SBD_DECODE_KERNELS;
+  int decode_path = SBD_DECODE_AUTO;
   int n_cu = 0;                 // workgroups of the fused forward: one per CU, at most kFwdMaxWorkgroups
   int32_t* err_host = nullptr;  // pinned copy of the fused forward's sticky error word
 
@@ -233,11 +233,6 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   const int M = B * k;
   const int d = m.d_model, dh = m.head_dim, nq = m.n_q_heads, nkv = m.n_kv_heads;
   const int qd = nq * dh;
-  sbd_status st = upload(c, c->ws + L.rows, rows.data(), rows.size() * sizeof(RowParam));
-  if (st) return st;
-  st = upload(c, c->ws + L.seqs, seqs.data(), seqs.size() * sizeof(SeqParam));
-  if (st) return st;
-
   float* x = c->at<float>(L.x);
   bf16_t* xn = c->at<bf16_t>(L.xn);
   bf16_t* xn_lo = xn + L.m_max * d;
@@ -251,17 +246,6 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   bf16_t* act_lo = act + L.m_max * (int64_t)m.ffn_dim;
   const RowParam* drows = c->at<RowParam>(L.rows);
   const SeqParam* dseqs = c->at<SeqParam>(L.seqs);
-
-  EmbedArgs ea{drows, M, d, c->embed, c->layers[0].attn_norm, x, xn, xn_lo, sumsq};
-  SBD_LAUNCH(c, SBD_KERNEL_EMBED, launch_embed(ea, ex));
-
-  const bool small = M <= 16;  // decode-sized forward: fused QKV epilogue and split-K
-  // Partial sums of x^2 per row handed from each RESID producer to the next consumer:
-  // d/16 from the embedding, one per workgroup of the decode O and down projections.
-  const int n_part_o = (d / 16) / gemv_pick(EPI_RESID, d / 16, qd).C;
-  const int n_part_down = (d / 16) / gemv_pick(EPI_RESID, d / 16, m.ffn_dim).C;
-  int n_part_cur = d / 16;
-  int* counters = c->at<int>(L.counters);
   float* vpart = c->at<float>(L.gemv_part);
   const int64_t vpart_cap = L.gemv_part_floats;
   int max_end = 0;
@@ -269,13 +253,12 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   const int G = nq / nkv;
   const int n_rb = (G * k + 63) / 64;
   const int nblocks = (max_end + 31) / 32;
-  int n_splits = pick_splits((int64_t)B * nkv * n_rb, nblocks);
-  const int bps = (nblocks + n_splits - 1) / n_splits;
-  n_splits = (nblocks + bps - 1) / bps;
+  const bool small = M <= 16;  // decode-sized forward
 
-  if (small && c->decode_path != SBD_DECODE_KERNELS) {
-    // the whole decode forward as one launch (fused.hip)
-    FwdArgs f{};
+  // The fused decode forward: checked before anything is enqueued.
+  const bool fused = small && c->decode_path == SBD_DECODE_FUSED;
+  FwdArgs f{};
+  if (fused) {
     f.M = M; f.B = B; f.k = k; f.n_layers = m.n_layers;
     f.d = d; f.n_q = nq; f.n_kv = nkv; f.d_h = dh; f.ffn = m.ffn_dim; f.vocab = m.vocab; f.qk_norm = m.qk_norm;
     f.eps = m.rms_eps;
@@ -291,27 +274,42 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     f.kcache = c->at<bf16_t>(L.kcache); f.vcache = c->at<bf16_t>(L.vcache); f.cap = L.cap;
     f.n_slots = m.max_batch; f.rope = c->at<float>(L.rope);
     // key splits: as many as fit one attention task per workgroup
-    {
-      const int per = B * nkv * n_rb;
-      const int fit = std::max(1, std::min(kMaxSplits, std::max(1, c->n_cu) / per));
-      const int fbps = (nblocks + std::min(fit, nblocks) - 1) / std::min(fit, nblocks);
-      f.n_rowblocks = n_rb; f.blocks_per_split = fbps; f.n_splits = (nblocks + fbps - 1) / fbps;
-    }
+    const int per = B * nkv * n_rb;
+    const int fit = std::min(nblocks, std::max(1, std::min(kMaxSplits, std::max(1, c->n_cu) / per)));
+    const int fbps = (nblocks + fit - 1) / fit;
+    f.n_rowblocks = n_rb; f.blocks_per_split = fbps; f.n_splits = (nblocks + fbps - 1) / fbps;
     f.part_ml = c->at<float>(L.attn_ml); f.part_o = c->at<float>(L.attn_o);
     f.part = vpart;
     f.logits = logits; f.lm_row0 = lm_row < 0 ? 0 : lm_row; f.lm_rows = lm_row < 0 ? M : 1;
     f.ctl = c->at<int>(L.fwd_ctl); f.err = c->at<int>(L.fwd_err);
-    const bool fits = c->n_cu > 0 && fused_plan(f, c->n_cu, vpart_cap) && f.plan.n_ctl <= L.fwd_ctl_ints;
-    if (!fits && c->decode_path == SBD_DECODE_FUSED)
+    if (c->n_cu < 1 || !fused_plan(f, c->n_cu, vpart_cap) || f.plan.n_ctl > L.fwd_ctl_ints)
       return fail(c, SBD_ERR_UNSUPPORTED, "the fused decode forward does not fit this model or device (%d CUs)",
                   c->n_cu);
-    if (fits) {
-      SBD_HIP(c, hipMemsetAsync(f.ctl, 0, (size_t)f.plan.n_ctl * sizeof(int32_t), c->stream));
-      SBD_LAUNCH(c, SBD_KERNEL_FUSED, launch_fused_forward(f, c->n_cu, ex));
-      SBD_HIP(c, hipMemcpyAsync(c->err_host, f.err, 2 * sizeof(int32_t), hipMemcpyDeviceToHost, c->stream));
-      return SBD_OK;
-    }
   }
+
+  sbd_status st = upload(c, c->ws + L.rows, rows.data(), rows.size() * sizeof(RowParam));
+  if (st) return st;
+  st = upload(c, c->ws + L.seqs, seqs.data(), seqs.size() * sizeof(SeqParam));
+  if (st) return st;
+  EmbedArgs ea{drows, M, d, c->embed, c->layers[0].attn_norm, x, xn, xn_lo, sumsq};
+  SBD_LAUNCH(c, SBD_KERNEL_EMBED, launch_embed(ea, ex));
+  if (fused) {
+    SBD_HIP(c, hipMemsetAsync(f.ctl, 0, (size_t)f.plan.n_ctl * sizeof(int32_t), c->stream));
+    SBD_LAUNCH(c, SBD_KERNEL_FUSED, launch_fused_forward(f, c->n_cu, ex));
+    SBD_HIP(c, hipMemcpyAsync(c->err_host, f.err, 2 * sizeof(int32_t), hipMemcpyDeviceToHost, c->stream));
+    return SBD_OK;
+  }
+
+  // Per-kernel path; for decode-sized forwards the QKV epilogue is fused and K is split.
+  // Partial sums of x^2 per row handed from each RESID producer to the next consumer:
+  // d/16 from the embedding, one per workgroup of the decode O and down projections.
+  const int n_part_o = (d / 16) / gemv_pick(EPI_RESID, d / 16, qd).C;
+  const int n_part_down = (d / 16) / gemv_pick(EPI_RESID, d / 16, m.ffn_dim).C;
+  int n_part_cur = d / 16;
+  int* counters = c->at<int>(L.counters);
+  int n_splits = pick_splits((int64_t)B * nkv * n_rb, nblocks);
+  const int bps = (nblocks + n_splits - 1) / n_splits;
+  n_splits = (nblocks + bps - 1) / bps;
 
   for (int l = 0; l < m.n_layers; ++l) {
     const LayerW& w = c->layers[l];
