@@ -4,16 +4,20 @@
 // The kernel is shaped by three measured costs: bytes in flight per CU, the activation
 // fragments re-read for every weight fragment, and the fixed latency at the start and end
 // of a launch.
-//   - A workgroup owns C tiles (C = 4 or 8) of one packed group (gemm.hip: a group's 8
-//     fragments of one K step are 8 KB of contiguous memory) and a K range; a K step then
-//     reads C KB of weights against 2 KB of activation fragments (hi and lo).
-//   - Its NW waves split the K range.  A wave issues the loads of U steps before the first
-//     MFMA that consumes them: a scheduling barrier keeps the compiler from interleaving
-//     loads and MFMAs, which would leave only a few loads in flight.
+//   - A workgroup owns C consecutive tiles (C = 1..8; they may straddle packed groups) and
+//     a K range; a K step then reads C KB of weights against 2 KB of activation fragments
+//     (hi and lo).  C need not divide 8, so a projection can be cut into exactly as many
+//     workgroups as the chip has CUs (gate/up at the 8B shape: 1792 tiles = 256 x 7).
+//   - Its NW waves split the K range.  A wave works in batches of U steps, double-buffered:
+//     the loads of the next batch are issued before the MFMAs of the current one wait for
+//     theirs (scheduling barriers keep the compiler from interleaving them), so 2U steps
+//     are in flight per wave.  A short kernel is a few memory round trips long; what it
+//     needs from memory besides the weights (norm partials, residual rows, rotary rows,
+//     positions) is requested before the weight stream starts.
 //   - The NW partial tiles are added in LDS in wave order.  When the K range is split over
-//     KS workgroups (grid y), each parks its partial tiles with device-coherent stores and
-//     the last to arrive adds the KS slices in order and runs the epilogue.  Results are
-//     deterministic; no workgroup waits for another.
+//     KS workgroups, all of them run on one XCD: each parks its partial tiles in that XCD's
+//     L2 and the last to arrive adds the KS slices in order and runs the epilogue.  Results
+//     are deterministic; no workgroup waits for another.
 //
 // Epilogues (acc in the v_mfma_f32_16x16x32_bf16 D layout: lane l holds column l % 16 of
 // a tile, rows 4*(l/16) + i):
@@ -30,6 +34,8 @@
 // its weight stream starts, and scales its fp32 products by rinv[m] = 1/sqrt(mean(x^2) +
 // eps), which equals normalising the input because the scale is constant along a row.
 
+#include <algorithm>
+
 #include "qkv_epilogue.h"
 
 namespace sbd {
@@ -40,15 +46,20 @@ __device__ __forceinline__ bool owns_tile(int ct, int wave) { return ct % NW == 
 
 template <int C, int NW, int U, int EPI, int DH>
 __global__ __launch_bounds__(NW * 64) void gemv_kernel(GemvArgs a) {
-  static_assert(C == 4 || C == 8, "a workgroup takes half or all of a packed group");
+  static_assert(C >= 1 && C <= 8, "a workgroup takes one to eight tiles");
   static_assert(EPI != EPI_QKV || C == 8, "the QKV epilogue works on whole groups");
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int r = lane & 15, g = lane >> 4;
-  const int sub = blockIdx.x;  // tiles sub*C .. sub*C + C-1
+  // Workgroup x runs on XCD x % 8; the KS slices of unit `sub` (tiles sub*C .. sub*C + C-1)
+  // all sit on XCD sub % 8, so their hand-off stays in that XCD's L2.  The unit count is
+  // padded to a multiple of 8; padding workgroups leave at once.
+  const int KS = a.splits;
+  const int sub = (int)((blockIdx.x >> 3) / KS) * 8 + (int)(blockIdx.x & 7);
+  const int kc = (int)((blockIdx.x >> 3) % KS);
+  if (sub * C >= a.n_tiles) return;
   const int t0 = sub * C;
   const int S = a.K / 32;
-  const int KS = gridDim.y, kc = blockIdx.y;
   const int z0 = (int)((int64_t)S * kc / KS), z1 = (int)((int64_t)S * (kc + 1) / KS);
   const int s_b = z0 + (z1 - z0) * wave / NW, s_e = z0 + (z1 - z0) * (wave + 1) / NW;
   const int ns = s_e - s_b;
@@ -81,47 +92,63 @@ __global__ __launch_bounds__(NW * 64) void gemv_kernel(GemvArgs a) {
     }
   }
 
+  QkvPre<DH> qpre;
+  if constexpr (EPI == EPI_QKV) qkv_epi_prefetch<DH>(a.qkv, a.M, qpre);
+
   const int arow_m = r < a.M ? r : a.M - 1;
   const bf16_t* ab = a.A + (int64_t)arow_m * a.lda + g * 8 + s_b * 32;
   const bf16_t* al = a.A_lo + (int64_t)arow_m * a.lda + g * 8 + s_b * 32;
-  const bf16_t* wb = a.Wp + packed_frag(t0, s_b, S) + lane * 8;  // tile t0 + ct at + ct * 512
+  // tile t0 + ct at step s_b; consecutive steps of a tile are kPackStep apart
+  const bf16_t* wt[C];
+#pragma unroll
+  for (int ct = 0; ct < C; ++ct) wt[ct] = a.Wp + packed_frag(t0 + ct, s_b, S) + lane * 8;
 
   f32x4 acc[C];
 #pragma unroll
   for (int ct = 0; ct < C; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-  int st = 0;
-  for (; st + U <= ns; st += U) {
-    // Activation fragments first (cache hits), then the weight fragments in the order
-    // the MFMAs consume them, so each MFMA waits only for its own loads.
-    i32x4 wv[U][C], xa[U], xl[U];
-#pragma unroll
-    for (int uu = 0; uu < U; ++uu) {
-      xa[uu] = ld16(ab + (st + uu) * 32);
-      xl[uu] = ld16(al + (st + uu) * 32);
+  // Batches of U steps, double-buffered: the loads of batch b + 1 are issued before the
+  // MFMAs of batch b wait for theirs, so 2U steps of weights are in flight per wave.  The
+  // last batch clamps its step index (a repeated fragment, no extra HBM traffic) and zeroes
+  // the activation fragments of the steps past the end, which then add nothing.
+  if (ns > 0) {
+    const int nb = (ns + U - 1) / U;
+    i32x4 wv0[U][C], xa0[U], xl0[U], wv1[U][C], xa1[U], xl1[U];
+#define GEMV_LOAD(WV, XA, XL, B0)                                                       \
+    _Pragma("unroll") for (int uu = 0; uu < U; ++uu) {                                 \
+      const int st_ = min((B0) + uu, ns - 1);                                          \
+      XA[uu] = ld16(ab + st_ * 32);                                                    \
+      XL[uu] = ld16(al + st_ * 32);                                                    \
+    }                                                                                  \
+    _Pragma("unroll") for (int uu = 0; uu < U; ++uu) {                                 \
+      const int st_ = min((B0) + uu, ns - 1);                                          \
+      _Pragma("unroll") for (int ct = 0; ct < C; ++ct)                                 \
+        WV[uu][ct] = ld16_stream(wt[ct] + (int64_t)st_ * kPackStep);                   \
     }
-#pragma unroll
-    for (int uu = 0; uu < U; ++uu)
-#pragma unroll
-      for (int ct = 0; ct < C; ++ct) wv[uu][ct] = ld16_stream(wb + (int64_t)(st + uu) * kPackStep + ct * 512);
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int uu = 0; uu < U; ++uu)
-#pragma unroll
-      for (int ct = 0; ct < C; ++ct) {
-        acc[ct] = mfma16x16x32(xa[uu], wv[uu][ct], acc[ct]);
-        acc[ct] = mfma16x16x32(xl[uu], wv[uu][ct], acc[ct]);
+#define GEMV_COMPUTE(WV, XA, XL, B0)                                                    \
+    _Pragma("unroll") for (int uu = 0; uu < U; ++uu) {                                 \
+      const bool ok_ = (B0) + uu < ns;                                                 \
+      const i32x4 xa_ = ok_ ? XA[uu] : i32x4{0, 0, 0, 0};                              \
+      const i32x4 xl_ = ok_ ? XL[uu] : i32x4{0, 0, 0, 0};                              \
+      _Pragma("unroll") for (int ct = 0; ct < C; ++ct) {                               \
+        acc[ct] = mfma16x16x32(xa_, WV[uu][ct], acc[ct]);                              \
+        acc[ct] = mfma16x16x32(xl_, WV[uu][ct], acc[ct]);                              \
+      }                                                                                \
+    }
+    GEMV_LOAD(wv0, xa0, xl0, 0)
+    for (int b = 0; b < nb; b += 2) {
+      if (b + 1 < nb) { GEMV_LOAD(wv1, xa1, xl1, (b + 1) * U) }
+      __builtin_amdgcn_sched_barrier(0);
+      GEMV_COMPUTE(wv0, xa0, xl0, b * U)
+      __builtin_amdgcn_sched_barrier(0);
+      if (b + 1 < nb) {
+        if (b + 2 < nb) { GEMV_LOAD(wv0, xa0, xl0, (b + 2) * U) }
+        __builtin_amdgcn_sched_barrier(0);
+        GEMV_COMPUTE(wv1, xa1, xl1, (b + 1) * U)
+        __builtin_amdgcn_sched_barrier(0);
       }
-  }
-  for (; st < ns; ++st) {
-    const i32x4 xa = ld16(ab + st * 32), xl = ld16(al + st * 32);
-    i32x4 wv[C];
-#pragma unroll
-    for (int ct = 0; ct < C; ++ct) wv[ct] = ld16_stream(wb + (int64_t)st * kPackStep + ct * 512);
-#pragma unroll
-    for (int ct = 0; ct < C; ++ct) {
-      acc[ct] = mfma16x16x32(xa, wv[ct], acc[ct]);
-      acc[ct] = mfma16x16x32(xl, wv[ct], acc[ct]);
     }
+#undef GEMV_LOAD
+#undef GEMV_COMPUTE
   }
 
   // ---- 1/rms of this lane's accumulator rows 4g + i
@@ -161,22 +188,25 @@ __global__ __launch_bounds__(NW * 64) void gemv_kernel(GemvArgs a) {
 
   // ---- K split over workgroups: park the slice, the last to arrive adds all in order
   if (KS > 1) {
+    const __amdgpu_buffer_rsrc_t rp = buf_rsrc(a.part);
 #pragma unroll
     for (int ct = 0; ct < C; ++ct) {
       if (!owns_tile<NW>(ct, wave)) continue;
-      float* p = a.part + ((int64_t)kc * a.n_tiles + t0 + ct) * 256 + lane;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) store_coherent(p + i * 64, acc[ct][i]);
+      *(f32x4*)(a.part + (((int64_t)kc * a.n_tiles + t0 + ct) * 64 + lane) * 4) = acc[ct];
     }
-    if (!last_arrival(a.counters + sub, KS)) return;
+    if (!last_arrival_xcd(a.counters + (int64_t)sub * kCtrStride, KS)) return;
 #pragma unroll
     for (int ct = 0; ct < C; ++ct) {
       if (!owns_tile<NW>(ct, wave)) continue;
       f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
-      for (int z = 0; z < KS; ++z) {
-        const float* p = a.part + ((int64_t)z * a.n_tiles + t0 + ct) * 256 + lane;
+      for (int z0 = 0; z0 < KS; z0 += 4) {  // four slices in flight, added in slice order
+        i32x4 v[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) s[i] += load_coherent(p + i * 64);
+        for (int u = 0; u < 4; ++u)
+          v[u] = z0 + u < KS ? ld16_l2(rp, (uint32_t)((((int64_t)(z0 + u) * a.n_tiles + t0 + ct) * 64 + lane) * 16))
+                             : i32x4{0, 0, 0, 0};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) s += __builtin_bit_cast(f32x4, v[u]);
       }
       acc[ct] = s;
     }
@@ -194,7 +224,7 @@ __global__ __launch_bounds__(NW * 64) void gemv_kernel(GemvArgs a) {
 #pragma unroll
       for (int ct = 0; ct < C; ++ct) acc[ct] = fin[ct][lane];
     }
-    qkv_epilogue<DH, false>(a.qkv, a.M, sub, acc, rinv);
+    qkv_epilogue<DH>(a.qkv, a.M, sub, acc, rinv, qpre);
     return;
   } else {
 #pragma unroll
@@ -261,41 +291,44 @@ __global__ __launch_bounds__(NW * 64) void gemv_kernel(GemvArgs a) {
 
 template <int C, int NW, int U, int EPI, int DH = 128>
 static void launch_gemv_cfg(const GemvArgs& a, int KS, const Exec& ex) {
-  SBD_KLAUNCH((gemv_kernel<C, NW, U, EPI, DH>), dim3((unsigned)(a.n_tiles / C), (unsigned)KS), dim3(NW * 64),
-              ex, a);
+  const int units = (a.n_tiles / C + 7) / 8 * 8;
+  GemvArgs b = a;
+  b.splits = KS;
+  SBD_KLAUNCH((gemv_kernel<C, NW, U, EPI, DH>), dim3((unsigned)(units * KS)), dim3(NW * 64), ex, b);
 }
 
-// Launch shapes from sweeps over the 8B decode shapes (M = 16).  Many tiles (LM head,
-// gate/up): whole groups, few waves per workgroup, no split.  A few hundred tiles (QKV, O,
-// down): the K range is split over workgroups until about one workgroup per CU streams,
-// keeping at least 8 K steps per workgroup.
+// Launch shapes from sweeps over the 8B decode shapes (M = 16), timed as chains of launches
+// over rotating weight copies.  Many tiles (LM head, gate/up): whole groups, few waves, no
+// split.  Few tiles (QKV, O, down): the K range is split over workgroups until about one
+// workgroup per CU streams (QKV 48 groups x 5, O and down 64 half groups x 4), keeping at
+// least 8 K steps per workgroup.
 GemvShape gemv_pick(GemmEpi epi, int n_tiles, int K) {
-  (void)epi;
   const int groups = n_tiles / 8, S = K / 32;
-  if (groups >= 512) return GemvShape{8, 1, 1, 1};
+  if (groups >= 512) return GemvShape{8, 1, 2, 1};
   if (groups >= 192) return GemvShape{8, 4, 1, 1};
-  int KS = 1;
-  while (2 * KS * groups <= 256 && 2 * KS <= kGemvMaxSplit && S / (2 * KS) >= 8) KS *= 2;
-  return GemvShape{8, S / KS >= 16 ? 16 : 8, 1, KS};
+  if (epi == EPI_QKV) {
+    int KS = std::max(1, std::min(256 / groups, kGemvMaxSplit));
+    while (KS > 1 && S / KS < 8) --KS;
+    return GemvShape{8, 4, 1, KS};
+  }
+  const int units = n_tiles / 4;
+  int KS = std::max(1, std::min(256 / std::max(units, 1), kGemvMaxSplit));
+  while (KS > 1 && S / KS < 8) --KS;
+  return GemvShape{4, 8, (S / KS) / 8 >= 8 ? 2 : 4, KS};
 }
 
 template <int EPI, int DH = 128>
 static bool dispatch(const GemvArgs& a, GemvShape sh, const Exec& ex) {
   const int c = sh.C * 1000 + sh.NW * 10 + sh.U;
   switch (c) {
-    case 8161: launch_gemv_cfg<8, 16, 1, EPI, DH>(a, sh.KS, ex); return true;
-    case 8081: launch_gemv_cfg<8, 8, 1, EPI, DH>(a, sh.KS, ex); return true;
     case 8041: launch_gemv_cfg<8, 4, 1, EPI, DH>(a, sh.KS, ex); return true;
-    case 8021: launch_gemv_cfg<8, 2, 1, EPI, DH>(a, sh.KS, ex); return true;
-    case 8011: launch_gemv_cfg<8, 1, 1, EPI, DH>(a, sh.KS, ex); return true;
+    case 8012: launch_gemv_cfg<8, 1, 2, EPI, DH>(a, sh.KS, ex); return true;
     default: break;
   }
   if constexpr (EPI != EPI_QKV) {
     switch (c) {
+      case 4084: launch_gemv_cfg<4, 8, 4, EPI>(a, sh.KS, ex); return true;
       case 4082: launch_gemv_cfg<4, 8, 2, EPI>(a, sh.KS, ex); return true;
-      case 4042: launch_gemv_cfg<4, 4, 2, EPI>(a, sh.KS, ex); return true;
-      case 4022: launch_gemv_cfg<4, 2, 2, EPI>(a, sh.KS, ex); return true;
-      case 4012: launch_gemv_cfg<4, 1, 2, EPI>(a, sh.KS, ex); return true;
       default: break;
     }
   }
@@ -305,7 +338,8 @@ static bool dispatch(const GemvArgs& a, GemvShape sh, const Exec& ex) {
 hipError_t launch_gemv(GemmEpi epi, const GemvArgs& a, GemvShape sh, const Exec& ex) {
   if (a.M < 1 || a.M > 16 || a.K < 32 || a.K % 32 || a.n_tiles < 8 || a.n_tiles % 8) return hipErrorInvalidValue;
   if (sh.C == 0) sh = gemv_pick(epi, a.n_tiles, a.K);
-  if (sh.KS < 1 || sh.KS > kGemvMaxSplit || a.n_tiles / sh.C + 1 > kCounters) return hipErrorInvalidValue;
+  if (sh.KS < 1 || sh.KS > kGemvMaxSplit || a.n_tiles % sh.C) return hipErrorInvalidValue;
+  if (sh.KS > 1 && (int64_t)(a.n_tiles / sh.C + 7) / 8 * 8 * kCtrStride > kAttnCtr0) return hipErrorInvalidValue;
   if (sh.KS > 1 && a.counters == nullptr) return hipErrorInvalidValue;
   if (epi == EPI_RESID && (a.sumsq == nullptr || a.n_part != a.n_tiles / sh.C)) return hipErrorInvalidValue;
   if (sh.KS > 1 && (a.part == nullptr || (int64_t)sh.KS * a.n_tiles * 256 > a.part_cap))

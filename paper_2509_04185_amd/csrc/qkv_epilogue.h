@@ -1,24 +1,57 @@
-// QKV epilogue of the decode GEMM (gemv.hip and the fused forward): per-head q/k RMSNorm,
-// rotate-half RoPE, q as scaled hi/lo bf16, K and V into the cache at cache_len + j.
+// QKV epilogue of the decode GEMM (gemv.hip): per-head q/k RMSNorm, rotate-half RoPE, q as
+// scaled hi/lo bf16, K and V into the cache at cache_len + j.
 #pragma once
 
 #include "sbd_device.h"
 
 namespace sbd {
 
+// What the epilogue reads besides the accumulators, loaded before the weight stream so
+// that none of it is on the kernel's tail: for the lane's rows 4g + i, the cache position
+// and slot, and the rotary (cos, sin) of the dims 16 pr + r it rotates; the q/k norm gains
+// of the dims it holds.
+template <int DH>
+struct QkvPre {
+  static constexpr int tph = DH / 16, ptiles = tph / 2;
+  int p_cache[4], slot[4];
+  float cs[4][ptiles], sn[4][ptiles];
+  float gq[tph], gk[tph];
+};
+
+template <int DH>
+__device__ __forceinline__ void qkv_epi_prefetch(const QkvEpi& e, int M, QkvPre<DH>& pre) {
+  constexpr int tph = DH / 16, ptiles = tph / 2, half = DH / 2;
+  const int lane = threadIdx.x & 63;
+  const int r = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = min(4 * g + i, M - 1);
+    const SeqParam sp = e.seqs[m / e.kblk];
+    const int pos = e.rows[m].pos;
+    pre.p_cache[i] = sp.cache_len + m % e.kblk;
+    pre.slot[i] = sp.slot;
+#pragma unroll
+    for (int pr = 0; pr < ptiles; ++pr) {
+      const float2 v = *(const float2*)(e.rope + ((int64_t)pos * half + pr * 16 + r) * 2);
+      pre.cs[i][pr] = v.x;
+      pre.sn[i][pr] = v.y;
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < tph; ++t) {
+    pre.gq[t] = e.qk_norm ? bf2f(e.q_norm[16 * t + r]) : 1.f;
+    pre.gk[t] = e.qk_norm ? bf2f(e.k_norm[16 * t + r]) : 1.f;
+  }
+}
+
 // QKV epilogue of one packed group (8 tiles = 128 columns = 128 / DH whole heads), run by
-// one wave holding all 8 accumulator tiles.  DEV: the stores are device-scope (read by other
-// workgroups of the same launch).
-template <int DH, bool DEV>
+// one wave holding all 8 accumulator tiles.
+template <int DH>
 __device__ __forceinline__ void qkv_epilogue(const QkvEpi& e, int M, int grp, const f32x4 (&acc)[8],
-                                             const float (&rinv)[4]) {
+                                             const float (&rinv)[4], const QkvPre<DH>& pre) {
   constexpr int tph = DH / 16, ptiles = tph / 2, half = DH / 2, heads = 8 / tph;
   const int lane = threadIdx.x & 63;
   const int r = lane & 15, g = lane >> 4;
-  auto put = [](bf16_t* p, bf16_t v) {
-    if constexpr (DEV) st_bf16_dev(p, v);
-    else *p = v;
-  };
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int m = 4 * g + i;
@@ -39,34 +72,29 @@ __device__ __forceinline__ void qkv_epilogue(const QkvEpi& e, int M, int grp, co
         ss += __shfl_xor(ss, 4);
         ss += __shfl_xor(ss, 8);
         const float rn = 1.0f / sqrtf(ss / (float)DH + e.eps);
-        const bf16_t* gn = h < e.n_q ? e.q_norm : e.k_norm;
 #pragma unroll
-        for (int t = 0; t < tph; ++t) u[hh * tph + t] *= rn * bf2f(gn[16 * t + r]);
+        for (int t = 0; t < tph; ++t) u[hh * tph + t] *= rn * (h < e.n_q ? pre.gq[t] : pre.gk[t]);
       }
     }
     if (!row_ok) continue;
-    const int b = m / e.kblk, j = m % e.kblk;
-    const SeqParam sp = e.seqs[b];
-    const int p_cache = sp.cache_len + j;
-    const int pos = e.rows[m].pos;
+    const int p_cache = pre.p_cache[i];
 #pragma unroll
     for (int hh = 0; hh < heads; ++hh) {
       const int h = grp * heads + hh;
       if (h >= e.n_q + e.n_kv) {  // V: transposed cache block, slot order of misc.hip vslot()
         const int gk = h - e.n_q - e.n_kv;
-        bf16_t* blk = e.vcache + (((int64_t)e.layer * e.n_slots + sp.slot) * e.n_kv + gk) * e.cap * DH +
+        bf16_t* blk = e.vcache + (((int64_t)e.layer * e.n_slots + pre.slot[i]) * e.n_kv + gk) * e.cap * DH +
                       (int64_t)(p_cache / 32) * DH * 32;
         const int p = p_cache & 31;
         const int sl = ((p & 15) >> 2) * 8 + (p >> 4) * 4 + (p & 3);
 #pragma unroll
-        for (int t = 0; t < tph; ++t) put(blk + (16 * t + r) * 32 + sl, f2bf(u[hh * tph + t]));
+        for (int t = 0; t < tph; ++t) blk[(16 * t + r) * 32 + sl] = f2bf(u[hh * tph + t]);
         continue;
       }
 #pragma unroll
       for (int pr = 0; pr < ptiles; ++pr) {
         const int dim = pr * 16 + r;
-        const float cs = e.rope[((int64_t)pos * half + dim) * 2 + 0];
-        const float sn = e.rope[((int64_t)pos * half + dim) * 2 + 1];
+        const float cs = pre.cs[i][pr], sn = pre.sn[i][pr];
         const float u0 = u[hh * tph + pr], u1 = u[hh * tph + pr + ptiles];
         const float r0 = u0 * cs - u1 * sn;
         const float r1 = u1 * cs + u0 * sn;
@@ -74,17 +102,17 @@ __device__ __forceinline__ void qkv_epilogue(const QkvEpi& e, int M, int grp, co
           const int64_t o = ((int64_t)m * e.n_q + h) * DH;
           bf16_t hi, lo;
           split_bf16(r0 * e.q_scale, hi, lo);
-          put(e.q + o + dim, hi);
-          put(e.q_lo + o + dim, lo);
+          e.q[o + dim] = hi;
+          e.q_lo[o + dim] = lo;
           split_bf16(r1 * e.q_scale, hi, lo);
-          put(e.q + o + dim + half, hi);
-          put(e.q_lo + o + dim + half, lo);
+          e.q[o + dim + half] = hi;
+          e.q_lo[o + dim + half] = lo;
         } else {
           const int gk = h - e.n_q;
-          bf16_t* dst = e.kcache + (((int64_t)e.layer * e.n_slots + sp.slot) * e.n_kv + gk) * e.cap * DH +
+          bf16_t* dst = e.kcache + (((int64_t)e.layer * e.n_slots + pre.slot[i]) * e.n_kv + gk) * e.cap * DH +
                         (int64_t)p_cache * DH;
-          put(dst + dim, f2bf(r0));
-          put(dst + dim + half, f2bf(r1));
+          dst[dim] = f2bf(r0);
+          dst[dim + half] = f2bf(r1);
         }
       }
     }

@@ -172,6 +172,37 @@ __device__ __forceinline__ bool last_arrival(int* counter, int expected) {
   return last;
 }
 
+// XCD-local hand-off.  A launch places workgroup i on XCD i % 8 (the round-robin dispatch
+// of the 8 XCDs), and the 32 CUs of an XCD share one L2.  Workgroups that exchange data only
+// with workgroups of their own XCD therefore need no device-scope traffic: partials are
+// written with plain stores (they reach the shared L2 before the writer's vmcnt drops),
+// read with L1-bypassing loads, and the arrival counter is an atomic performed in that L2.
+// Every counter used this way sits on a 128-byte line of its own.
+constexpr int kCtrStride = 32;  // int32 words between XCD-local counters
+constexpr int kPolicyL2 = 1;    // cache-policy bits of an L1-bypassing access (sc0)
+__device__ __forceinline__ i32x4 ld16_l2(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, kPolicyL2);
+}
+__device__ __forceinline__ i32x2 ld8_l2(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_amdgcn_raw_buffer_load_b64(r, byte_off, 0, kPolicyL2);
+}
+
+// last_arrival() for workgroups that all run on one XCD: true in exactly one of the
+// `expected` workgroups arriving at `counter` (the last), which then reads the others'
+// partials with ld16_l2 / ld8_l2.  The counter is reset to 0 for the next launch.
+__device__ __forceinline__ bool last_arrival_xcd(int* counter, int expected) {
+  __shared__ int s_last;
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's stores have reached the L2
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int prev = __hip_atomic_fetch_add(counter, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    s_last = (prev == expected - 1) ? 1 : 0;
+    if (s_last) __hip_atomic_store(counter, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
+  __syncthreads();
+  return s_last != 0;
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
   v += __shfl_xor(v, 32);
   return half_wave_sum(v);

@@ -18,7 +18,8 @@ constexpr int kKeyBlock = 32;       // keys per attention step / per V^T storage
 constexpr int kMaxSplits = 64;      // split-KV partitions per (sequence, KV head, row block)
 constexpr int kEbChunk = 4096;      // vocabulary entries per EB partial workgroup
 constexpr int kMaxBlock = 64;       // largest block size k
-constexpr int kCounters = 16384;    // arrival counters in the workspace
+constexpr int kCounters = 65536;    // int32 words of arrival counters in the workspace
+constexpr int kAttnCtr0 = 16384;    // first counter word of the attention splits (GEMMs below)
 
 // Where a kernel is enqueued: the stream, plus optional start/stop events that the
 // runtime records at the kernel's own start and end (per-kernel timing).
@@ -154,9 +155,10 @@ struct GemvArgs {
   bf16_t* act_lo;
   int64_t ld_act;
   QkvEpi qkv;            // EPI_QKV
-  float* part;           // split K: partial tiles [splits][n_tiles][4][64]
+  float* part;           // split K: partial tiles [splits][n_tiles][64 lanes][4]
   int64_t part_cap;      // floats available at part (bounds the split)
-  int* counters;         // arrival counters (kCounters), zero between launches
+  int* counters;         // arrival counters (kCounters words), zero between launches
+  int splits;            // K slices per unit (set by the launcher)
 };
 // Launch shape of the decode GEMM; a zero field means "pick for the shape".
 struct GemvShape {
