@@ -9,8 +9,8 @@ committed token + 15 masks), gamma = 1.0.  Inputs are resident in HBM before tim
 
 Prints one JSON line: value = algorithmic HBM bytes of a step / step time (GB/s),
 plus the block-forward ms, the EB-select microseconds, a roofline entry for the
-dominant kernel (the fused decode forward, or the gate/up projection on the per-kernel
-path; timed live with HIP events on the library stream) and the CPU oracle timed on a bounded sample of the same workload.
+dominant kernel (the per-XCD MLP layer kernel, the fused decode forward, or the gate/up
+projection on the per-kernel path; timed live with HIP events on the library stream) and the CPU oracle timed on a bounded sample of the same workload.
 """
 import argparse
 import dataclasses
@@ -52,9 +52,18 @@ def gate_up_bytes(shape, M):
     return 2 * 2 * shape.ffn_dim * shape.d_model + 2 * M * shape.d_model + 2 * M * shape.ffn_dim
 
 
+def layer_mlp_bytes(shape, M):
+    """Algorithmic bytes of one layer_mlp launch (gate/up + SwiGLU + down + residual): the three
+    MLP weight matrices, the bf16 input rows, the fp32 residual rows read and written, the
+    bf16 rows of the next norm's input written."""
+    d, F = shape.d_model, shape.ffn_dim
+    return 2 * 3 * F * d + 2 * M * d + 2 * 4 * M * d + 2 * M * d
+
+
 KERNEL_SOURCES = {
     "fused": ("fused.hip", "attention_body.h", "qkv_epilogue.h", "sbd_device.h"),
-    "gate_up": ("gemv.hip", "qkv_epilogue.h", "sbd_device.h"),
+    "gate_up": ("gemv.hip", "gemv_body.h", "qkv_epilogue.h", "sbd_device.h"),
+    "layer_mlp": ("layer_xcd.hip", "gemv_body.h", "attention_body.h", "qkv_epilogue.h", "sbd_device.h"),
 }
 
 
@@ -116,7 +125,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum time of the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event pass")
-    ap.add_argument("--decode-path", default="auto", choices=["auto", "fused", "kernels"],
+    ap.add_argument("--decode-path", default="auto", choices=["auto", "fused", "kernels", "layers"],
                     help="kernels of decode-sized forwards (sbd_set_decode_path)")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -200,6 +209,9 @@ def main():
             # one launch runs every layer and the LM head: its bytes are the block forward's
             kind, bpl = "fused", fwd_bytes
             label = "fused_forward_kernel<128> (all layers + LM head, M = 16)"
+        elif prof.get("layer_mlp", (0, 0.0))[0]:
+            kind, bpl = "layer_mlp", layer_mlp_bytes(s, B * k)
+            label = "layer_mlp_kernel (gate/up + SwiGLU + down + residual, per-XCD)"
         else:
             kind, bpl = "gate_up", gate_up_bytes(s, B * k)
             label = "gemv_kernel<8,4,1,EPI_SWIGLU> (gate/up projection + SwiGLU)"

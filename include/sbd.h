@@ -198,18 +198,35 @@ sbd_status sbd_workspace_region(const sbd_model_config* cfg, const char* name, s
 /*
  * Which kernels run a decode-sized forward (at most 16 rows: sbd_block_forward with
  * batch * k <= 16, and prefill chunks that small).
- *   SBD_DECODE_AUTO     the library's choice (the default); at present one kernel per step,
- *                       the faster of the two on MI355X.
+ *   SBD_DECODE_AUTO     the library's choice (the default): SBD_DECODE_LAYERS where it
+ *                       applies, otherwise one kernel per step.
  *   SBD_DECODE_FUSED    the fused forward: every layer and the LM head in one launch of one
  *                       persistent workgroup per CU.  A forward it cannot take fails with
  *                       SBD_ERR_UNSUPPORTED: it needs d_model a multiple of 128 and head_dim
  *                       64 or 128.
  *   SBD_DECODE_KERNELS  one kernel per step.
- * Both give the same results up to float summation order.  Larger forwards always run one
+ *   SBD_DECODE_LAYERS   two launches per layer (QKV + attention + O projection; gate/up +
+ *                       down), each XCD of the chip owning one KV head's share.  Needs a
+ *                       device of 256 CUs in 8 XCDs, n_kv_heads 8, head_dim 128, d_model
+ *                       4096, ffn_dim 12288, 14336 or 16384, batch * k <= 16 and
+ *                       (n_q_heads / n_kv_heads) * k <= 64; a forward it cannot take fails
+ *                       with SBD_ERR_UNSUPPORTED.
+ * All give the same results up to float summation order.  Larger forwards always run one
  * kernel per step.  INVALID_ARG for another value.
  */
-typedef enum { SBD_DECODE_AUTO = 0, SBD_DECODE_FUSED = 1, SBD_DECODE_KERNELS = 2 } sbd_decode_path;
+typedef enum {
+  SBD_DECODE_AUTO = 0,
+  SBD_DECODE_FUSED = 1,
+  SBD_DECODE_KERNELS = 2,
+  SBD_DECODE_LAYERS = 3
+} sbd_decode_path;
 sbd_status sbd_set_decode_path(sbd_ctx* ctx, int32_t path);
+/*
+ * *fits = 1 when `path` can run a decode-sized forward of `batch` sequences of `k` rows on
+ * this context's model and device, else 0 (SBD_DECODE_AUTO and SBD_DECODE_KERNELS always
+ * can).  INVALID_ARG for a null pointer or an unknown path.
+ */
+sbd_status sbd_decode_path_fits(const sbd_ctx* ctx, int32_t path, int32_t batch, int32_t k, int32_t* fits);
 
 /*
  * Per-kernel timing, for measurement tools.  While enabled, every kernel launch the
@@ -231,7 +248,9 @@ typedef enum {
   SBD_KERNEL_EB_PARTIAL = 9, /* EB per-chunk softmax statistics */
   SBD_KERNEL_EB_SELECT = 10, /* EB merge, sort and select */
   SBD_KERNEL_FUSED = 11,     /* fused decode forward: all layers + LM head in one launch */
-  SBD_KERNEL_COUNT = 12
+  SBD_KERNEL_LAYER_ATTN = 12,/* per-XCD layer kernel: QKV + attention + O projection */
+  SBD_KERNEL_LAYER_MLP = 13, /* per-XCD layer kernel: gate/up + down projection */
+  SBD_KERNEL_COUNT = 14
 } sbd_kernel;
 sbd_status sbd_profile_enable(sbd_ctx* ctx, int32_t enable);
 sbd_status sbd_profile_read(sbd_ctx* ctx, int32_t kernel, int32_t* launches, double* total_ms);

@@ -25,8 +25,8 @@ LAYER_FIELDS = ("attn_norm", "wq", "wk", "wv", "wo", "q_norm", "k_norm", "mlp_no
 
 # sbd_kernel values, in order.
 KERNEL_NAMES = ("embed", "qkv", "rope", "attention", "attn_merge", "o_proj", "gate_up", "down",
-                "lm_head", "eb_partial", "eb_select", "fused")
-DECODE_PATHS = {"auto": 0, "fused": 1, "kernels": 2}  # sbd_decode_path
+                "lm_head", "eb_partial", "eb_select", "fused", "layer_attn", "layer_mlp")
+DECODE_PATHS = {"auto": 0, "fused": 1, "kernels": 2, "layers": 3}  # sbd_decode_path
 
 # Every entry point of sbd.h with its argument types.
 SIGNATURES = {
@@ -48,6 +48,7 @@ SIGNATURES = {
     "sbd_kv_import": [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p],
     "sbd_kv_export": [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p],
     "sbd_set_decode_path": [c_void_p, c_int32],
+    "sbd_decode_path_fits": [c_void_p, c_int32, c_int32, c_int32, POINTER(c_int32)],
     "sbd_profile_enable": [c_void_p, c_int32],
     "sbd_profile_read": [c_void_p, c_int32, POINTER(c_int32), POINTER(c_double)],
     "sbd_status_string": [c_int32],
@@ -253,9 +254,16 @@ class Sbd:
         return k, v
 
     def set_decode_path(self, path: str):
-        """Kernels of decode-sized forwards: "auto", "fused" or "kernels" (sbd_set_decode_path)."""
+        """Kernels of decode-sized forwards: "auto", "fused", "kernels" or "layers" (sbd_set_decode_path)."""
         code = DECODE_PATHS[path]
         _check(self.lib, self.lib.sbd_set_decode_path(self.ctx, code), "sbd_set_decode_path", self.ctx)
+
+    def decode_path_fits(self, path: str, batch: int, k: int) -> bool:
+        """Whether `path` can run a forward of `batch` x `k` rows here (sbd_decode_path_fits)."""
+        fits = c_int32(0)
+        _check(self.lib, self.lib.sbd_decode_path_fits(self.ctx, DECODE_PATHS[path], batch, k, ctypes.byref(fits)),
+               "sbd_decode_path_fits", self.ctx)
+        return bool(fits.value)
 
     def profile(self, enable: bool):
         _check(self.lib, self.lib.sbd_profile_enable(self.ctx, int(bool(enable))),

@@ -13,16 +13,25 @@ __device__ __forceinline__ int64_t attn_head_base(int layer, int slot, int g, in
   return (((int64_t)layer * n_slots + slot) * n_kv + g) * cap * d_h;
 }
 
-// One workgroup (4 waves) of the attention splits: split `split`, KV head x row block gy,
-// sequence b.  smem: kAttnSmem bytes of LDS.  DEV: the queries, keys and values were
-// written earlier in the same launch (device-scope loads), and the partial results are
-// read by another workgroup of the same launch (device-scope stores).
-template <int DH, bool DEV>
-__device__ __forceinline__ void attn_split_body(const AttnArgs& a, int split, int gy, int b, char* smem) {
+// What one wave holds after its key range: unnormalised O^T tiles of its 16 query rows
+// (lane: row r = lane % 16, dims 16 dt + 4 (lane / 16) + i), the running max and sum.
+template <int DH>
+struct AttnPart {
+  f32x4 o[DH / 16];
+  float m, l;
+  bool row_ok;  // this lane's row exists
+  int rho;      // its row within the KV head's rows (query head within the group, block row)
+};
+
+// One workgroup (4 waves) of the attention over key blocks [blk0, blk_lim) of KV head g,
+// row block rb, sequence b.  smem: kAttnSmem bytes of LDS.  POL: cache policy of the loads
+// of the queries and of the keys and values (they may have been written earlier in the same
+// launch: kPolicyL2 when by the same XCD, kPolicyDevice when by any).
+template <int DH, int POL>
+__device__ __forceinline__ void attn_core(const AttnArgs& a, int g, int rb, int b, int blk0, int blk_lim,
+                                          char* smem, AttnPart<DH>& out) {
   constexpr int NDT = DH / 16;  // 16-wide dimension tiles
   constexpr int NKS = DH / 32;  // 32-wide reduction steps for the scores
-  const int g = gy / a.n_rowblocks;
-  const int rb = gy % a.n_rowblocks;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int r = lane & 15, grp = lane >> 4;
   const SeqParam sp = a.seqs[b];
@@ -42,8 +51,7 @@ __device__ __forceinline__ void attn_split_body(const AttnArgs& a, int split, in
 #pragma unroll
   for (int o = 1; o < 16; o <<= 1) kend_w = max(kend_w, __shfl_xor(kend_w, o));
   const int nblk_w = (kend_w + 31) / 32;
-  const int blk0 = split * a.blocks_per_split;
-  const int blk1 = min(blk0 + a.blocks_per_split, nblk_w);
+  const int blk1 = min(blk_lim, nblk_w);
 
   // Query fragments (B operand, hi and lo): row r, dims 32*s + 8*grp .. +8.
   i32x4 qf[NKS], ql[NKS];
@@ -51,14 +59,9 @@ __device__ __forceinline__ void attn_split_body(const AttnArgs& a, int split, in
   const __amdgpu_buffer_rsrc_t rq = buf_rsrc(a.q), rql = buf_rsrc(a.q_lo);
 #pragma unroll
   for (int s = 0; s < NKS; ++s) {
-    const int64_t e = qoff + 32 * s + 8 * grp;
-    if constexpr (DEV) {
-      qf[s] = row_ok ? ld16_dev(rq, (uint32_t)(e * 2)) : i32x4{0, 0, 0, 0};
-      ql[s] = row_ok ? ld16_dev(rql, (uint32_t)(e * 2)) : i32x4{0, 0, 0, 0};
-    } else {
-      qf[s] = row_ok ? ld16(a.q + e) : i32x4{0, 0, 0, 0};
-      ql[s] = row_ok ? ld16(a.q_lo + e) : i32x4{0, 0, 0, 0};
-    }
+    const uint32_t e = (uint32_t)((qoff + 32 * s + 8 * grp) * 2);
+    qf[s] = row_ok ? __builtin_amdgcn_raw_buffer_load_b128(rq, e, 0, POL) : i32x4{0, 0, 0, 0};
+    ql[s] = row_ok ? __builtin_amdgcn_raw_buffer_load_b128(rql, e, 0, POL) : i32x4{0, 0, 0, 0};
   }
 
   const int64_t hb = attn_head_base(a.layer, sp.slot, g, a.n_slots, a.n_kv, a.cap, DH);
@@ -92,7 +95,7 @@ __device__ __forceinline__ void attn_split_body(const AttnArgs& a, int split, in
   if (lane == 0) s_kend[w] = kend_wg;
   __syncthreads();
   kend_wg = max(max(s_kend[0], s_kend[1]), max(s_kend[2], s_kend[3]));
-  const int blk1_wg = min(blk0 + a.blocks_per_split, (kend_wg + 31) / 32);
+  const int blk1_wg = min(blk_lim, (kend_wg + 31) / 32);
   const int n_chunks = blk1_wg > blk0 ? (blk1_wg - blk0 + CH - 1) / CH : 0;
 
   // Wave-load u of wave w in chunk c: index i = w + 4u -> block i / (2 LPB), part
@@ -114,7 +117,7 @@ __device__ __forceinline__ void attn_split_body(const AttnArgs& a, int split, in
       }
       __builtin_amdgcn_global_load_lds((const void*)src,
                                        (__attribute__((address_space(3))) void*)&buf[bi][part][sub * 1024],
-                                       16, 0, DEV ? kPolicyDevice : 0);
+                                       16, 0, POL);
     }
   };
   // s_waitcnt immediates: vmcnt(n) with the other counters left free
@@ -243,17 +246,39 @@ __device__ __forceinline__ void attn_split_body(const AttnArgs& a, int split, in
     }
   }
 
-  if (!row_ok) return;
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt) out.o[dt] = o[dt];
+  out.m = m_run;
+  out.l = l_run;
+  out.row_ok = row_ok;
+  out.rho = rho;
+}
+
+// One workgroup of the split-KV attention: split `split` of the key blocks, KV head x row
+// block gy, sequence b.  Leaves the split's unnormalised (max, sum, O) per row for the merge.
+// DEV: the queries, keys and values were written earlier in the same launch (device-scope
+// loads), and the partial results are read by another workgroup of it (device-scope stores).
+template <int DH, bool DEV>
+__device__ __forceinline__ void attn_split_body(const AttnArgs& a, int split, int gy, int b, char* smem) {
+  constexpr int NDT = DH / 16;
+  const int g = gy / a.n_rowblocks, rb = gy % a.n_rowblocks;
+  const int blk0 = split * a.blocks_per_split;
+  AttnPart<DH> pt;
+  attn_core<DH, DEV ? kPolicyDevice : 0>(a, g, rb, b, blk0, blk0 + a.blocks_per_split, smem, pt);
+  if (!pt.row_ok) return;
+  const int lane = threadIdx.x & 63, grp = lane >> 4;
+  const int k = a.k, G = a.n_q / a.n_kv;
+  const int hh = pt.rho / k, j = pt.rho % k, hq = g * G + hh;
   const int64_t item = (int64_t)(b * k + j) * a.n_q + hq;
   const int64_t n_items = (int64_t)a.B * k * a.n_q;
   if (grp == 0) {
     float* ml = a.part_ml + ((int64_t)split * n_items + item) * 2;
     if constexpr (DEV) {
-      st_f32_dev(ml, m_run);
-      st_f32_dev(ml + 1, l_run);
+      st_f32_dev(ml, pt.m);
+      st_f32_dev(ml + 1, pt.l);
     } else {
-      ml[0] = m_run;
-      ml[1] = l_run;
+      ml[0] = pt.m;
+      ml[1] = pt.l;
     }
   }
   const int64_t po = ((int64_t)split * n_items + item) * DH;
@@ -261,9 +286,9 @@ __device__ __forceinline__ void attn_split_body(const AttnArgs& a, int split, in
 #pragma unroll
   for (int dt = 0; dt < NDT; ++dt) {
     if constexpr (DEV)
-      st16_dev(ro, (uint32_t)((po + 16 * dt + 4 * grp) * 4), __builtin_bit_cast(i32x4, o[dt]));
+      st16_dev(ro, (uint32_t)((po + 16 * dt + 4 * grp) * 4), __builtin_bit_cast(i32x4, pt.o[dt]));
     else
-      *(f32x4*)(a.part_o + po + 16 * dt + 4 * grp) = o[dt];
+      *(f32x4*)(a.part_o + po + 16 * dt + 4 * grp) = pt.o[dt];
   }
 }
 

@@ -8,12 +8,10 @@
 //     a K range; a K step then reads C KB of weights against 2 KB of activation fragments
 //     (hi and lo).  C need not divide 8, so a projection can be cut into exactly as many
 //     workgroups as the chip has CUs (gate/up at the 8B shape: 1792 tiles = 256 x 7).
-//   - Its NW waves split the K range.  A wave works in batches of U steps, double-buffered:
-//     the loads of the next batch are issued before the MFMAs of the current one wait for
-//     theirs (scheduling barriers keep the compiler from interleaving them), so 2U steps
-//     are in flight per wave.  A short kernel is a few memory round trips long; what it
-//     needs from memory besides the weights (norm partials, residual rows, rotary rows,
-//     positions) is requested before the weight stream starts.
+//   - Its NW waves split the K range and stream it (gemv_body.h: batches of U steps,
+//     double-buffered, 2U steps in flight per wave).  A short kernel is a few memory round
+//     trips long; what it needs from memory besides the weights (norm partials, residual
+//     rows, rotary rows, positions) is requested before the weight stream starts.
 //   - The NW partial tiles are added in LDS in wave order.  When the K range is split over
 //     KS workgroups, all of them run on one XCD: each parks its partial tiles in that XCD's
 //     L2 and the last to arrive adds the KS slices in order and runs the epilogue.  Results
@@ -36,6 +34,7 @@
 
 #include <algorithm>
 
+#include "gemv_body.h"
 #include "qkv_epilogue.h"
 
 namespace sbd {
@@ -96,8 +95,7 @@ __global__ __launch_bounds__(NW * 64) void gemv_kernel(GemvArgs a) {
   if constexpr (EPI == EPI_QKV) qkv_epi_prefetch<DH>(a.qkv, a.M, qpre);
 
   const int arow_m = r < a.M ? r : a.M - 1;
-  const bf16_t* ab = a.A + (int64_t)arow_m * a.lda + g * 8 + s_b * 32;
-  const bf16_t* al = a.A_lo + (int64_t)arow_m * a.lda + g * 8 + s_b * 32;
+  const uint32_t a_off = (uint32_t)(((int64_t)arow_m * a.lda + g * 8 + s_b * 32) * 2);
   // tile t0 + ct at step s_b; consecutive steps of a tile are kPackStep apart
   const bf16_t* wt[C];
 #pragma unroll
@@ -106,49 +104,9 @@ __global__ __launch_bounds__(NW * 64) void gemv_kernel(GemvArgs a) {
   f32x4 acc[C];
 #pragma unroll
   for (int ct = 0; ct < C; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // Batches of U steps, double-buffered: the loads of batch b + 1 are issued before the
-  // MFMAs of batch b wait for theirs, so 2U steps of weights are in flight per wave.  The
-  // last batch clamps its step index (a repeated fragment, no extra HBM traffic) and zeroes
-  // the activation fragments of the steps past the end, which then add nothing.
-  if (ns > 0) {
-    const int nb = (ns + U - 1) / U;
-    i32x4 wv0[U][C], xa0[U], xl0[U], wv1[U][C], xa1[U], xl1[U];
-#define GEMV_LOAD(WV, XA, XL, B0)                                                       \
-    _Pragma("unroll") for (int uu = 0; uu < U; ++uu) {                                 \
-      const int st_ = min((B0) + uu, ns - 1);                                          \
-      XA[uu] = ld16(ab + st_ * 32);                                                    \
-      XL[uu] = ld16(al + st_ * 32);                                                    \
-    }                                                                                  \
-    _Pragma("unroll") for (int uu = 0; uu < U; ++uu) {                                 \
-      const int st_ = min((B0) + uu, ns - 1);                                          \
-      _Pragma("unroll") for (int ct = 0; ct < C; ++ct)                                 \
-        WV[uu][ct] = ld16_stream(wt[ct] + (int64_t)st_ * kPackStep);                   \
-    }
-#define GEMV_COMPUTE(WV, XA, XL, B0)                                                    \
-    _Pragma("unroll") for (int uu = 0; uu < U; ++uu) {                                 \
-      const bool ok_ = (B0) + uu < ns;                                                 \
-      const i32x4 xa_ = ok_ ? XA[uu] : i32x4{0, 0, 0, 0};                              \
-      const i32x4 xl_ = ok_ ? XL[uu] : i32x4{0, 0, 0, 0};                              \
-      _Pragma("unroll") for (int ct = 0; ct < C; ++ct) {                               \
-        acc[ct] = mfma16x16x32(xa_, WV[uu][ct], acc[ct]);                              \
-        acc[ct] = mfma16x16x32(xl_, WV[uu][ct], acc[ct]);                              \
-      }                                                                                \
-    }
-    GEMV_LOAD(wv0, xa0, xl0, 0)
-    for (int b = 0; b < nb; b += 2) {
-      if (b + 1 < nb) { GEMV_LOAD(wv1, xa1, xl1, (b + 1) * U) }
-      __builtin_amdgcn_sched_barrier(0);
-      GEMV_COMPUTE(wv0, xa0, xl0, b * U)
-      __builtin_amdgcn_sched_barrier(0);
-      if (b + 1 < nb) {
-        if (b + 2 < nb) { GEMV_LOAD(wv0, xa0, xl0, (b + 2) * U) }
-        __builtin_amdgcn_sched_barrier(0);
-        GEMV_COMPUTE(wv1, xa1, xl1, (b + 1) * U)
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    }
-#undef GEMV_LOAD
-#undef GEMV_COMPUTE
+  {
+    i32x4 w0[U][C];
+    gemv_stream<C, U, 0, false>(buf_rsrc(a.A), buf_rsrc(a.A_lo), a_off, wt, ns, w0, acc);
   }
 
   // ---- 1/rms of this lane's accumulator rows 4g + i
@@ -339,7 +297,7 @@ hipError_t launch_gemv(GemmEpi epi, const GemvArgs& a, GemvShape sh, const Exec&
   if (a.M < 1 || a.M > 16 || a.K < 32 || a.K % 32 || a.n_tiles < 8 || a.n_tiles % 8) return hipErrorInvalidValue;
   if (sh.C == 0) sh = gemv_pick(epi, a.n_tiles, a.K);
   if (sh.KS < 1 || sh.KS > kGemvMaxSplit || a.n_tiles % sh.C) return hipErrorInvalidValue;
-  if (sh.KS > 1 && (int64_t)(a.n_tiles / sh.C + 7) / 8 * 8 * kCtrStride > kAttnCtr0) return hipErrorInvalidValue;
+  if (sh.KS > 1 && (int64_t)(a.n_tiles / sh.C + 7) / 8 * 8 * kCtrStride > kLayerCtr0) return hipErrorInvalidValue;
   if (sh.KS > 1 && a.counters == nullptr) return hipErrorInvalidValue;
   if (epi == EPI_RESID && (a.sumsq == nullptr || a.n_part != a.n_tiles / sh.C)) return hipErrorInvalidValue;
   if (sh.KS > 1 && (a.part == nullptr || (int64_t)sh.KS * a.n_tiles * 256 > a.part_cap))

@@ -1,0 +1,525 @@
+// Per-XCD layer kernels: a decode-sized layer (M <= 16 block rows) of the SBD block forward
+// as two launches, each of one workgroup per CU, with the work of every phase divided
+// between the 8 XCDs so that almost every hand-off stays inside one XCD's L2.
+//
+// One kernel per projection (gemv.hip) pays, at every kernel boundary, the launch gap, the
+// first-load latency of the next kernel and the tail of the previous one (wave reduction,
+// split-K hand-off, epilogue).  At the 8B decode shapes that is 3-6 us per kernel against
+// 6-35 us of weight streaming.  Here a layer is two launches:
+//
+//   layer_attn_kernel  XCD x owns KV head x.  Its 32 workgroups
+//     1. project Q for the x-th group of G query heads, K and V of head x (G + 2 packed
+//        groups, K split KS = 32 / (G + 2) ways; the last of a group's slices adds them and
+//        runs the q/k-norm + RoPE epilogue, writing q and the new K/V cache rows);
+//     2. run the attention of KV head x, one task per key range (32 / B per sequence);
+//     3. merge the tasks, one wave per query row, into the attention output;
+//     4. multiply that output - the K slice x of the O projection - by W_o, one packed group
+//        (128 output columns) per workgroup; the 8 XCDs' partials of a group are added by
+//        the last to arrive (in XCD order), which runs the residual epilogue.
+//   layer_mlp_kernel   XCD x owns columns [x F/8, (x+1) F/8) of the MLP.  Its 32 workgroups
+//     1. project gate/up for those columns (F/2048 tiles each) with the SwiGLU epilogue;
+//     2. multiply them - the K slice x of the down projection - by W_down, one packed group
+//        per workgroup; partials of the 8 XCDs are added as in step 4 above.
+//
+// Phases 1-4 of a kernel depend on each other only within an XCD: a producer writes with
+// plain stores (they reach the XCD's L2 before its vmcnt drops), raises an XCD counter with
+// an L2 atomic, and consumers poll it with L2 atomics and then read the data (lines their
+// CU has not read before in the launch, so they come from the L2).  Only the O and down partials cross XCDs (device-scope stores and loads, as in the
+// split-K hand-off of gemv.hip).  The weights of a phase never depend on activations, so
+// each workgroup requests its first O / down weights before it waits for its inputs.
+//
+// Every wait is bounded: a wait that gives up raises a sticky error (device word and pinned
+// host copy) that the next API call reports, and the launch runs to its end.  All 32
+// workgroups of an XCD are resident at once (one per CU: the LDS request is more than half a
+// CU's), so every wait is for work that is already running.
+
+#include "attention_body.h"
+#include "gemv_body.h"
+#include "qkv_epilogue.h"
+
+namespace sbd {
+
+namespace {
+
+constexpr int kLxSmem = 98304;       // LDS per workgroup: more than half a CU's, so one per CU
+constexpr int kLxSpin = 1 << 21;     // polls before a wait gives up
+constexpr int kDH = 128;
+// counter lines of XCD x: [x * 64, x * 64 + 64); device-wide lines after all XCDs'
+constexpr int kCtrQkv = 0;           // + group: last-arrival counters of the QKV slices
+constexpr int kCtrQkvDone = 40;      // QKV groups finished (epilogue stored)
+constexpr int kCtrAttnDone = 41;     // attention tasks finished
+constexpr int kCtrMergeDone = 42;    // workgroups past the merge
+constexpr int kCtrOStart = 43;       // workgroups past the O projection's wait
+constexpr int kCtrGuDone = 44;       // workgroups past gate/up
+constexpr int kCtrDownStart = 45;    // workgroups past the down projection's wait
+constexpr int kCtrDevO = kXcds * 64;              // + group: O partial arrivals (device-wide)
+constexpr int kCtrDevDown = kXcds * 64 + kXcdWgs;  // + group: down partial arrivals
+
+__device__ __forceinline__ int* xcd_ctr(const LayerXArgs& a, int x, int line) {
+  return a.ctr + (int64_t)(x * 64 + line) * kCtrStride;
+}
+
+// Add 1 to an XCD counter once every store of this workgroup has reached the L2.
+__device__ __forceinline__ void xcd_signal(int* ctr) {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// Value of an XCD counter as the L2 holds it.  A load would do only once: a workgroup-scope
+// load may be served by this CU's L1, which keeps the first value it fetched.  An atomic is
+// always performed in the L2; adding a zero the compiler cannot see keeps it from turning
+// the idempotent update back into a load.
+__device__ __forceinline__ int xcd_peek(int* ctr) {
+  int zero;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(zero));
+  return __hip_atomic_fetch_add(ctr, zero, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// Wait until *ctr >= target (thread 0 polls, then the workgroup proceeds).
+__device__ __forceinline__ void xcd_wait(const LayerXArgs& a, int* ctr, int target, int what) {
+  if (threadIdx.x == 0) {
+    int it = 0;
+    while (xcd_peek(ctr) < target) {
+      __builtin_amdgcn_s_sleep(1);
+      if (++it > kLxSpin) {
+        atomicOr(a.err, 1);
+        atomicExch(a.err + 1, what);
+        if (a.err_host != nullptr) {
+          __hip_atomic_store(a.err_host + 1, what, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+          __hip_atomic_store(a.err_host, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        }
+        break;
+      }
+    }
+  }
+  __syncthreads();
+}
+
+// Counts workgroups past their last wait on this XCD's phase counters; the last of the 32
+// resets those counters (and itself) for the next launch.
+__device__ __forceinline__ void xcd_passed(const LayerXArgs& a, int x, int line, const int* resets, int n) {
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int* c = xcd_ctr(a, x, line);
+    if (__hip_atomic_fetch_add(c, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) == kXcdWgs - 1) {
+      for (int i = 0; i < n; ++i)
+        __hip_atomic_store(xcd_ctr(a, x, resets[i]), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      __hip_atomic_store(c, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+  }
+}
+
+// 1/rms of rows 0..15 from partial sums of squares [M][n_part]: 16 threads per row.
+__device__ __forceinline__ float ssq_share(const float* ssq, int n_part, int M) {
+  const int m = threadIdx.x >> 4, q = threadIdx.x & 15;
+  float s = 0.f;
+  if (m < M)
+    for (int p = q; p < n_part; p += 16) s += ssq[(int64_t)m * n_part + p];
+  return s;
+}
+__device__ __forceinline__ void rinv_finish(float s, float inv_d, float eps, float* rinv_s) {
+#pragma unroll
+  for (int o = 8; o >= 1; o >>= 1) s += __shfl_xor(s, o);
+  if ((threadIdx.x & 15) == 0) rinv_s[threadIdx.x >> 4] = 1.0f / sqrtf(s * inv_d + eps);
+}
+
+// The 4 waves' partial tiles of a C-tile unit added in wave order; wave w ends with the sums
+// of the tiles ct = w, w + 4, ... (the tiles it owns).  red: 4 * C KB of LDS.
+template <int C>
+__device__ __forceinline__ void reduce_waves(f32x4 (&acc)[C], char* red_mem) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  f32x4* red = reinterpret_cast<f32x4*>(red_mem);  // [4][C][64]
+#pragma unroll
+  for (int ct = 0; ct < C; ++ct) red[(wave * C + ct) * 64 + lane] = acc[ct];
+  __syncthreads();
+#pragma unroll
+  for (int ct = 0; ct < C; ++ct) {
+    if (ct % 4 != wave) continue;
+    f32x4 s = red[(0 * C + ct) * 64 + lane];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) s += red[(w * C + ct) * 64 + lane];
+    acc[ct] = s;
+  }
+  __syncthreads();  // red is free again
+}
+
+// Residual epilogue of packed group grp from its 8 summed tiles (wave w owns tiles w, w + 4):
+// x += y; xn = x * g as hi/lo; one partial sum of x^2 per row for this group.
+__device__ __forceinline__ void resid_epilogue(const LayerXArgs& a, int grp, const f32x4 (&acc)[8],
+                                               const f32x4 (&x_pre)[2], const float (&g_pre)[2], const bf16_t* g,
+                                               bf16_t* xn, bf16_t* xn_lo, float* ssq, char* smem) {
+  (void)g;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = lane & 15, g4 = lane >> 4;
+  float* ssq_s = reinterpret_cast<float*>(smem);  // [8 tiles][16 rows]
+#pragma unroll
+  for (int k2 = 0; k2 < 2; ++k2) {
+    const int ct = wave + 4 * k2;
+    const int n = (grp * 8 + ct) * 16 + r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = 4 * g4 + i;
+      float xv = 0.f;
+      if (m < a.M) {
+        xv = x_pre[k2][i] + acc[ct][i];
+        a.x[(int64_t)m * a.d + n] = xv;
+        bf16_t hi, lo;
+        split_bf16(xv * g_pre[k2], hi, lo);
+        xn[(int64_t)m * a.d + n] = hi;
+        xn_lo[(int64_t)m * a.d + n] = lo;
+      }
+      float s2 = xv * xv;
+      s2 += __shfl_xor(s2, 1);
+      s2 += __shfl_xor(s2, 2);
+      s2 += __shfl_xor(s2, 4);
+      s2 += __shfl_xor(s2, 8);
+      if (r == 0) ssq_s[ct * 16 + m] = s2;
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x < a.M) {
+    float s = 0.f;
+#pragma unroll
+    for (int ct = 0; ct < 8; ++ct) s += ssq_s[ct * 16 + threadIdx.x];
+    ssq[(int64_t)threadIdx.x * kXcdWgs + grp] = s;
+  }
+}
+
+// The residual rows and the next norm's gain of the two tiles wave w finishes (w, w + 4).
+__device__ __forceinline__ void resid_prefetch(const LayerXArgs& a, int grp, const bf16_t* g, f32x4 (&x_pre)[2],
+                                               float (&g_pre)[2]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = lane & 15, g4 = lane >> 4;
+#pragma unroll
+  for (int k2 = 0; k2 < 2; ++k2) {
+    const int n = (grp * 8 + wave + 4 * k2) * 16 + r;
+    g_pre[k2] = bf2f(g[n]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = 4 * g4 + i;
+      x_pre[k2][i] = m < a.M ? a.x[(int64_t)m * a.d + n] : 0.f;
+    }
+  }
+}
+
+// Cross-XCD split of a packed group's 8 tiles: park this XCD's sums (device-scope), and in
+// the last of the 8 to arrive add all of them in XCD order.  True in that workgroup.
+__device__ __forceinline__ bool cross_xcd_sum(const LayerXArgs& a, int grp, int x, int ctr_line, f32x4 (&acc)[8]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const __amdgpu_buffer_rsrc_t rp = buf_rsrc(a.dpart);
+#pragma unroll
+  for (int k2 = 0; k2 < 2; ++k2) {
+    const int ct = wave + 4 * k2;
+    st16_dev(rp, (uint32_t)(((((int64_t)grp * kXcds + x) * 8 + ct) * 64 + lane) * 16), __builtin_bit_cast(i32x4, acc[ct]));
+  }
+  if (!last_arrival(a.ctr + (int64_t)(ctr_line + grp) * kCtrStride, kXcds)) return false;
+#pragma unroll
+  for (int k2 = 0; k2 < 2; ++k2) {
+    const int ct = wave + 4 * k2;
+    i32x4 v[kXcds];
+#pragma unroll
+    for (int z = 0; z < kXcds; ++z)
+      v[z] = ld16_dev(rp, (uint32_t)(((((int64_t)grp * kXcds + z) * 8 + ct) * 64 + lane) * 16));
+    f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int z = 0; z < kXcds; ++z) s += __builtin_bit_cast(f32x4, v[z]);
+    acc[ct] = s;
+  }
+  return true;
+}
+
+}  // namespace
+
+__global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
+  __shared__ __attribute__((aligned(16))) char smem[kLxSmem];
+  const int x = blockIdx.x & 7, lw = blockIdx.x >> 3;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = lane & 15, g4 = lane >> 4;
+  const int G = a.n_q / a.n_kv;
+  const int ngrp = G + 2, KS = kXcdWgs / ngrp;
+  float* xpart = a.xpart + (int64_t)x * kLxXcdFloats;
+  float* rinv_s = reinterpret_cast<float*>(smem + 65536 + 1024);  // [16]
+
+  // ---- 1. QKV projection, unit (group gi of this XCD, K slice kc)
+  if (lw < ngrp * KS) {
+    const int gi = lw / KS, kc = lw % KS;
+    const int grp = gi < G ? x * G + gi : (gi == G ? a.n_q + x : a.n_q + a.n_kv + x);
+    const int S = a.d / 32;
+    const int z0 = S * kc / KS, z1 = S * (kc + 1) / KS;
+    const int s_b = z0 + (z1 - z0) * wave / 4, ns = z0 + (z1 - z0) * (wave + 1) / 4 - s_b;
+    QkvEpi e{};
+    e.rows = a.rows; e.seqs = a.seqs; e.kblk = a.k; e.layer = a.layer;
+    e.n_q = a.n_q; e.n_kv = a.n_kv; e.d_h = kDH; e.qk_norm = a.qk_norm; e.eps = a.eps; e.q_scale = a.q_scale;
+    e.rope = a.rope; e.q_norm = a.q_norm; e.k_norm = a.k_norm; e.q = a.q; e.q_lo = a.q_lo;
+    e.kcache = a.kcache; e.vcache = a.vcache; e.cap = a.cap; e.n_slots = a.n_slots;
+    const float sq = ssq_share(a.ssq, a.n_part, a.M);
+    QkvPre<kDH> qpre;
+    qkv_epi_prefetch<kDH>(e, a.M, qpre);
+    const int arow = r < a.M ? r : a.M - 1;
+    const bf16_t* wt[8];
+#pragma unroll
+    for (int ct = 0; ct < 8; ++ct) wt[ct] = a.wqkv + packed_frag(grp * 8 + ct, s_b, S) + lane * 8;
+    f32x4 acc[8];
+#pragma unroll
+    for (int ct = 0; ct < 8; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+    {
+      i32x4 w0[1][8];
+      gemv_stream<8, 1, 0, false>(buf_rsrc(a.xn), buf_rsrc(a.xn_lo),
+                                  (uint32_t)(((int64_t)arow * a.d + g4 * 8 + s_b * 32) * 2), wt, ns, w0, acc);
+    }
+    rinv_finish(sq, 1.0f / a.d, a.eps, rinv_s);
+    reduce_waves<8>(acc, smem);
+    // park this slice in the XCD's L2; the last of the group's KS slices finishes the group
+    float* qp = xpart + (int64_t)gi * KS * 2048;
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) {
+      const int ct = wave + 4 * k2;
+      *(f32x4*)(qp + (((int64_t)kc * 8 + ct) * 64 + lane) * 4) = acc[ct];
+    }
+    if (last_arrival_xcd(xcd_ctr(a, x, kCtrQkv + gi), KS)) {
+      const __amdgpu_buffer_rsrc_t rq = buf_rsrc(qp);
+      f32x4* fin = reinterpret_cast<f32x4*>(smem);  // [8][64]
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2) {
+        const int ct = wave + 4 * k2;
+        f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int z0_ = 0; z0_ < KS; z0_ += 4) {
+          i32x4 v[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            v[u] = z0_ + u < KS ? ld16_l2(rq, (uint32_t)((((int64_t)(z0_ + u) * 8 + ct) * 64 + lane) * 16))
+                                : i32x4{0, 0, 0, 0};
+#pragma unroll
+          for (int u = 0; u < 4; ++u) s += __builtin_bit_cast(f32x4, v[u]);
+        }
+        fin[ct * 64 + lane] = s;
+      }
+      __syncthreads();
+#pragma unroll
+      for (int ct = 0; ct < 8; ++ct) acc[ct] = fin[ct * 64 + lane];
+      float rinv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) rinv[i] = rinv_s[4 * g4 + i];
+      qkv_epilogue<kDH>(e, a.M, grp, acc, rinv, qpre, wave);  // wave w: rows 4g + w
+      xcd_signal(xcd_ctr(a, x, kCtrQkvDone));
+    }
+  }
+  __syncthreads();
+
+  // ---- 2. attention of KV head x: task t = (sequence, key range)
+  const int n_tasks = a.B * a.n_tasks;
+  float* att_ml = xpart + kLxQkvFloats;                         // [task][64 rows][2]
+  float* att_o = att_ml + (int64_t)kLxAttnTasks * kLxRows * 2;  // [task][64 rows][128]
+  if (lw < n_tasks) {
+    const int b = lw / a.n_tasks, s = lw % a.n_tasks;
+    xcd_wait(a, xcd_ctr(a, x, kCtrQkvDone), ngrp, a.layer * 16 + 1);
+    const int L = a.seqs[b].cache_len;
+    const int nblk = (L + a.k + 31) / 32;
+    AttnArgs aa{};
+    aa.seqs = a.seqs; aa.B = a.B; aa.k = a.k; aa.layer = a.layer; aa.n_q = a.n_q; aa.n_kv = a.n_kv; aa.d_h = kDH;
+    aa.q = a.q; aa.q_lo = a.q_lo; aa.kcache = a.kcache; aa.vcache = a.vcache; aa.cap = a.cap; aa.n_slots = a.n_slots;
+    aa.n_rowblocks = 1;
+    AttnPart<kDH> pt;
+    attn_core<kDH, kPolicyL2>(aa, x, 0, b, nblk * s / a.n_tasks, nblk * (s + 1) / a.n_tasks, smem, pt);
+    if (pt.row_ok) {
+      if (g4 == 0) *(float2*)(att_ml + ((int64_t)lw * kLxRows + pt.rho) * 2) = float2{pt.m, pt.l};
+#pragma unroll
+      for (int dt = 0; dt < kDH / 16; ++dt)
+        *(f32x4*)(att_o + ((int64_t)lw * kLxRows + pt.rho) * kDH + 16 * dt + 4 * g4) = pt.o[dt];
+    }
+    xcd_signal(xcd_ctr(a, x, kCtrAttnDone));
+  }
+
+  // ---- 3. merge: one wave per query row (sequence b, row rho = head-in-group * k + j)
+  {
+    const int R = G * a.k, n_rows = a.B * R;
+    const int row = lw * 4 + wave;
+    if (lw * 4 < n_rows) {
+      xcd_wait(a, xcd_ctr(a, x, kCtrAttnDone), n_tasks, a.layer * 16 + 2);
+      if (row < n_rows) {
+        const int b = row / R, rho = row % R;
+        const int nt = a.n_tasks;
+        const __amdgpu_buffer_rsrc_t rml = buf_rsrc(att_ml), ro = buf_rsrc(att_o);
+        float2 ml = float2{-INFINITY, 0.f};
+        if (lane < nt) {
+          const i32x2 v = ld8_l2(rml, (uint32_t)((((int64_t)(b * nt + lane)) * kLxRows + rho) * 8));
+          ml = float2{__int_as_float(v[0]), __int_as_float(v[1])};
+        }
+        const float mx = wave_max(ml.x);
+        const float wgt = ml.x == -INFINITY ? 0.f : exp2f(ml.x - mx);
+        const float lsum = wave_sum(wgt * ml.y);
+        float acc0 = 0.f, acc1 = 0.f;
+        for (int t0 = 0; t0 < nt; t0 += 8) {  // wave-uniform; eight tasks in flight
+          float v0[8], v1[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            const int t = min(t0 + u, nt - 1);
+            const uint32_t base = (uint32_t)((((int64_t)(b * nt + t)) * kLxRows + rho) * kDH * 4);
+            v0[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ro, base + lane * 4, 0, kPolicyL2));
+            v1[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ro, base + (lane + 64) * 4, 0, kPolicyL2));
+          }
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            const float wu = t0 + u < nt ? __shfl(wgt, t0 + u) : 0.f;
+            acc0 += wu * v0[u];
+            acc1 += wu * v1[u];
+          }
+        }
+        const float inv = 1.0f / lsum;
+        const int hh = rho / a.k, j = rho % a.k;
+        const int64_t dst = ((int64_t)(b * a.k + j) * a.n_q + x * G + hh) * kDH;
+        bf16_t hi, lo;
+        split_bf16(acc0 * inv, hi, lo);
+        a.attn[dst + lane] = hi;
+        a.attn_lo[dst + lane] = lo;
+        split_bf16(acc1 * inv, hi, lo);
+        a.attn[dst + lane + 64] = hi;
+        a.attn_lo[dst + lane + 64] = lo;
+      }
+    }
+    xcd_signal(xcd_ctr(a, x, kCtrMergeDone));
+  }
+
+  // ---- 4. O projection: group lw, K slice x (the query heads of KV head x)
+  {
+    const int grp = lw;
+    const int qd = a.n_q * kDH, S = qd / 32;
+    const int z0 = x * G * kDH / 32, zn = G * kDH / 32;
+    const int s_b = z0 + zn * wave / 4, ns = z0 + zn * (wave + 1) / 4 - s_b;
+    const bf16_t* wt[8];
+#pragma unroll
+    for (int ct = 0; ct < 8; ++ct) wt[ct] = a.wo + packed_frag(grp * 8 + ct, s_b, S) + lane * 8;
+    constexpr int U = 4;
+    i32x4 w0[U][8];
+    if (ns > 0) gemv_issue_w<8, U>(wt, 0, ns, w0);  // weights first: they wait for nothing
+    f32x4 x_pre[2];
+    float g_pre[2];
+    resid_prefetch(a, grp, a.g_mid, x_pre, g_pre);
+    xcd_wait(a, xcd_ctr(a, x, kCtrMergeDone), kXcdWgs, a.layer * 16 + 3);
+    {
+      const int resets[3] = {kCtrQkvDone, kCtrAttnDone, kCtrMergeDone};
+      xcd_passed(a, x, kCtrOStart, resets, 3);
+    }
+    f32x4 acc[8];
+#pragma unroll
+    for (int ct = 0; ct < 8; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int arow = r < a.M ? r : a.M - 1;
+    gemv_stream<8, U, kPolicyL2, true>(buf_rsrc(a.attn), buf_rsrc(a.attn_lo),
+                                       (uint32_t)(((int64_t)arow * qd + g4 * 8 + s_b * 32) * 2), wt, ns, w0, acc);
+    reduce_waves<8>(acc, smem);
+    if (cross_xcd_sum(a, grp, x, kCtrDevO, acc))
+      resid_epilogue(a, grp, acc, x_pre, g_pre, a.g_mid, a.xn_mid, a.xn_mid_lo, a.ssq_mid, smem);
+  }
+}
+
+template <int CG>
+__global__ __launch_bounds__(256) void layer_mlp_kernel(LayerXArgs a) {
+  __shared__ __attribute__((aligned(16))) char smem[kLxSmem];
+  const int x = blockIdx.x & 7, lw = blockIdx.x >> 3;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = lane & 15, g4 = lane >> 4;
+  float* rinv_s = reinterpret_cast<float*>(smem + 65536 + 1024);
+
+  // ---- 1. gate/up + SwiGLU: tiles t0 .. t0 + CG - 1 (activation columns 8 t .. 8 t + 7)
+  {
+    const int t0 = (x * kXcdWgs + lw) * CG;
+    const int S = a.d / 32;
+    const int s_b = S * wave / 4, ns = S * (wave + 1) / 4 - s_b;
+    const float sq = ssq_share(a.ssq_mid, kXcdWgs, a.M);
+    const int arow = r < a.M ? r : a.M - 1;
+    const bf16_t* wt[CG];
+#pragma unroll
+    for (int ct = 0; ct < CG; ++ct) wt[ct] = a.wgu + packed_frag(t0 + ct, s_b, S) + lane * 8;
+    f32x4 acc[CG];
+#pragma unroll
+    for (int ct = 0; ct < CG; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+    {
+      i32x4 w0[1][CG];
+      gemv_stream<CG, 1, 0, false>(buf_rsrc(a.xn_mid), buf_rsrc(a.xn_mid_lo),
+                                   (uint32_t)(((int64_t)arow * a.d + g4 * 8 + s_b * 32) * 2), wt, ns, w0, acc);
+    }
+    rinv_finish(sq, 1.0f / a.d, a.eps, rinv_s);
+    reduce_waves<CG>(acc, smem);
+#pragma unroll
+    for (int ct = 0; ct < CG; ++ct) {
+      if (ct % 4 != wave) continue;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = 4 * g4 + i;
+        const float v = acc[ct][i] * (m < a.M ? rinv_s[m] : 0.f);
+        const float up = __shfl_xor(v, 8);
+        if (r < 8 && m < a.M) {
+          const int jj = (t0 + ct) * 8 + r;
+          bf16_t hi, lo;
+          split_bf16(v / (1.0f + expf(-v)) * up, hi, lo);
+          a.act[(int64_t)m * a.ffn + jj] = hi;
+          a.act_lo[(int64_t)m * a.ffn + jj] = lo;
+        }
+      }
+    }
+    xcd_signal(xcd_ctr(a, x, kCtrGuDone));
+  }
+
+  // ---- 2. down projection: group lw, K slice x (activation columns [x F/8, (x+1) F/8))
+  {
+    const int grp = lw;
+    const int S = a.ffn / 32, zn = a.ffn / 8 / 32, z0 = x * zn;
+    const int s_b = z0 + zn * wave / 4, ns = z0 + zn * (wave + 1) / 4 - s_b;
+    const bf16_t* wt[8];
+#pragma unroll
+    for (int ct = 0; ct < 8; ++ct) wt[ct] = a.wdown + packed_frag(grp * 8 + ct, s_b, S) + lane * 8;
+    constexpr int U = 2;
+    i32x4 w0[U][8];
+    if (ns > 0) gemv_issue_w<8, U>(wt, 0, ns, w0);  // weights first: they wait for nothing
+    f32x4 x_pre[2];
+    float g_pre[2];
+    resid_prefetch(a, grp, a.g_out, x_pre, g_pre);
+    xcd_wait(a, xcd_ctr(a, x, kCtrGuDone), kXcdWgs, a.layer * 16 + 5);
+    {
+      const int resets[1] = {kCtrGuDone};
+      xcd_passed(a, x, kCtrDownStart, resets, 1);
+    }
+    f32x4 acc[8];
+#pragma unroll
+    for (int ct = 0; ct < 8; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int arow = r < a.M ? r : a.M - 1;
+    gemv_stream<8, U, kPolicyL2, true>(buf_rsrc(a.act), buf_rsrc(a.act_lo),
+                                       (uint32_t)(((int64_t)arow * a.ffn + g4 * 8 + s_b * 32) * 2), wt, ns, w0, acc);
+    reduce_waves<8>(acc, smem);
+    if (cross_xcd_sum(a, grp, x, kCtrDevDown, acc))
+      resid_epilogue(a, grp, acc, x_pre, g_pre, a.g_out, a.xn_out, a.xn_out_lo, a.ssq_out, smem);
+  }
+}
+
+bool layer_xcd_fits(const sbd_model_config& c, int n_cu, int B, int k) {
+  if (n_cu != kXcds * kXcdWgs) return false;
+  if (c.n_kv_heads != kXcds || c.head_dim != kDH || c.d_model != kXcdWgs * 128) return false;
+  if (c.n_q_heads % c.n_kv_heads) return false;
+  const int G = c.n_q_heads / c.n_kv_heads;
+  if (G + 2 > kXcdWgs || (c.d_model / 32) / (kXcdWgs / (G + 2)) < 4) return false;
+  if (c.ffn_dim % (kXcds * kXcdWgs * 8) != 0) return false;
+  const int cg = c.ffn_dim / (kXcds * kXcdWgs * 8);
+  if (cg < 6 || cg > 8) return false;
+  if (B < 1 || k < 1 || B * k > 16 || G * k > kLxRows || B > kLxAttnTasks) return false;
+  if ((B * G * k + 3) / 4 > kXcdWgs) return false;  // one wave per merged row
+  return true;
+}
+
+hipError_t launch_layer_attn(const LayerXArgs& a, const Exec& ex) {
+  SBD_KLAUNCH(layer_attn_kernel, dim3(kXcds * kXcdWgs), dim3(256), ex, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_layer_mlp(const LayerXArgs& a, const Exec& ex) {
+  const int cg = a.ffn / (kXcds * kXcdWgs * 8);
+  switch (cg) {
+    case 6: SBD_KLAUNCH(layer_mlp_kernel<6>, dim3(kXcds * kXcdWgs), dim3(256), ex, a); break;
+    case 7: SBD_KLAUNCH(layer_mlp_kernel<7>, dim3(kXcds * kXcdWgs), dim3(256), ex, a); break;
+    case 8: SBD_KLAUNCH(layer_mlp_kernel<8>, dim3(kXcds * kXcdWgs), dim3(256), ex, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace sbd

@@ -44,16 +44,18 @@ __device__ __forceinline__ void qkv_epi_prefetch(const QkvEpi& e, int M, QkvPre<
   }
 }
 
-// QKV epilogue of one packed group (8 tiles = 128 columns = 128 / DH whole heads), run by
-// one wave holding all 8 accumulator tiles.
+// QKV epilogue of one packed group (8 tiles = 128 columns = 128 / DH whole heads), run by a
+// wave holding all 8 accumulator tiles: of the lane's rows 4g + i, those with i == i_sel
+// (every i when i_sel < 0), so that four waves can share the rows.
 template <int DH>
 __device__ __forceinline__ void qkv_epilogue(const QkvEpi& e, int M, int grp, const f32x4 (&acc)[8],
-                                             const float (&rinv)[4], const QkvPre<DH>& pre) {
+                                             const float (&rinv)[4], const QkvPre<DH>& pre, int i_sel = -1) {
   constexpr int tph = DH / 16, ptiles = tph / 2, half = DH / 2, heads = 8 / tph;
   const int lane = threadIdx.x & 63;
   const int r = lane & 15, g = lane >> 4;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
+    if (i_sel >= 0 && i != i_sel) continue;
     const int m = 4 * g + i;
     const bool row_ok = m < M;
     const float rv = row_ok ? rinv[i] : 0.f;

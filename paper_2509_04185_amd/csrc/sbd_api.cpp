@@ -103,6 +103,8 @@ bool sbd::compute_layout(const sbd_model_config& c, Layout* L) {
                                             (int64_t)c.max_batch * c.n_kv_heads * n_rb_max);
   o.fwd_ctl = take(o.fwd_ctl_ints * sizeof(int32_t));
   o.fwd_err = take(2 * sizeof(int32_t));
+  o.lx_part = take(kLxPartFloats * sizeof(float));
+  o.lx_dev = take(kLxDevFloats * sizeof(float));
   o.counters = take((int64_t)kCounters * sizeof(int32_t));
   o.total = off;
   *L = o;
@@ -134,6 +136,7 @@ struct sbd_ctx {
   // decode path for M <= 16 (sbd_set_decode_path)
   int decode_path = SBD_DECODE_AUTO;
   int n_cu = 0;                 // workgroups of the fused forward: one per CU, at most kFwdMaxWorkgroups
+  int n_cu_dev = 0;             // CUs of the device
   int32_t* err_host = nullptr;  // pinned copy of the fused forward's sticky error word
 
   template <class T>
@@ -163,9 +166,10 @@ sbd_status fail(sbd_ctx* c, sbd_status st, const char* fmt, ...) {
 sbd_status check_sticky(sbd_ctx* c) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(c, SBD_ERR_HIP, "earlier HIP error: %s", hipGetErrorString(e));
-  // written by copies queued after each fused forward; it never goes back to zero
+  // written by copies queued after each fused forward, or by a layer kernel whose wait gave
+  // up; it never goes back to zero
   if (c->err_host != nullptr && __atomic_load_n(c->err_host, __ATOMIC_ACQUIRE) != 0)
-    return fail(c, SBD_ERR_HIP, "a fused decode forward gave up waiting (task code %d)",
+    return fail(c, SBD_ERR_HIP, "a decode forward gave up waiting for its inputs (task code %d)",
                 __atomic_load_n(c->err_host + 1, __ATOMIC_ACQUIRE));
   return SBD_OK;
 }
@@ -287,6 +291,14 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
                   c->n_cu);
   }
 
+  // The per-XCD layer kernels: chosen by AUTO where they apply; checked before anything is
+  // enqueued when asked for explicitly.
+  const bool layers_fit = small && !fused && c->decode_path != SBD_DECODE_KERNELS &&
+                          layer_xcd_fits(m, c->n_cu_dev, B, k);
+  if (small && c->decode_path == SBD_DECODE_LAYERS && !layers_fit)
+    return fail(c, SBD_ERR_UNSUPPORTED, "the per-XCD layer kernels do not fit this forward or device (%d CUs)",
+                c->n_cu_dev);
+
   sbd_status st = upload(c, c->ws + L.rows, rows.data(), rows.size() * sizeof(RowParam));
   if (st) return st;
   st = upload(c, c->ws + L.seqs, seqs.data(), seqs.size() * sizeof(SeqParam));
@@ -311,7 +323,34 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   const int bps = (nblocks + n_splits - 1) / n_splits;
   n_splits = (nblocks + bps - 1) / bps;
 
-  for (int l = 0; l < m.n_layers; ++l) {
+  if (layers_fit) {
+    LayerXArgs lx{};
+    lx.M = M; lx.B = B; lx.k = k; lx.d = d; lx.n_q = nq; lx.n_kv = nkv; lx.ffn = m.ffn_dim;
+    lx.qk_norm = m.qk_norm; lx.eps = m.rms_eps;
+    lx.q_scale = (float)(1.4426950408889634 / std::sqrt((double)dh));
+    lx.n_tasks = kXcdWgs / B;
+    lx.x = x; lx.xn = xn; lx.xn_lo = xn_lo; lx.ssq = sumsq;
+    lx.xn_mid = c->at<bf16_t>(L.xn2); lx.xn_mid_lo = lx.xn_mid + L.m_max * d; lx.ssq_mid = c->at<float>(L.sumsq2);
+    lx.xn_out = xn; lx.xn_out_lo = xn_lo; lx.ssq_out = sumsq;
+    lx.q = q; lx.q_lo = q_lo; lx.attn = attn; lx.attn_lo = attn_lo; lx.act = act; lx.act_lo = act_lo;
+    lx.kcache = c->at<bf16_t>(L.kcache); lx.vcache = c->at<bf16_t>(L.vcache); lx.cap = L.cap;
+    lx.n_slots = m.max_batch; lx.rope = c->at<float>(L.rope); lx.rows = drows; lx.seqs = dseqs;
+    lx.xpart = c->at<float>(L.lx_part); lx.dpart = c->at<float>(L.lx_dev);
+    lx.ctr = c->at<int>(L.counters) + kLayerCtr0; lx.err = c->at<int>(L.fwd_err); lx.err_host = c->err_host;
+    for (int l = 0; l < m.n_layers; ++l) {
+      const LayerW& w = c->layers[l];
+      const bf16_t* wp = c->at<bf16_t>(L.wpack) + (int64_t)l * L.wp_layer;
+      lx.layer = l;
+      lx.wqkv = wp; lx.wo = wp + L.wp_o; lx.wgu = wp + L.wp_gu; lx.wdown = wp + L.wp_down;
+      lx.q_norm = w.q_norm; lx.k_norm = w.k_norm; lx.g_mid = w.mlp_norm;
+      lx.g_out = (l + 1 < m.n_layers) ? c->layers[l + 1].attn_norm : c->final_norm;
+      lx.n_part = l == 0 ? d / 16 : kXcdWgs;
+      SBD_LAUNCH(c, SBD_KERNEL_LAYER_ATTN, launch_layer_attn(lx, ex));
+      SBD_LAUNCH(c, SBD_KERNEL_LAYER_MLP, launch_layer_mlp(lx, ex));
+    }
+    n_part_cur = kXcdWgs;
+  }
+  for (int l = 0; l < m.n_layers && !layers_fit; ++l) {
     const LayerW& w = c->layers[l];
     const bf16_t* wp = c->at<bf16_t>(L.wpack) + (int64_t)l * L.wp_layer;
     QkvEpi qe{};
@@ -569,6 +608,7 @@ sbd_status sbd_create(const sbd_model_config* cfg, const sbd_weights* w, void* w
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
       c->n_cu = 0;
+    c->n_cu_dev = c->n_cu;
     c->n_cu = std::min(c->n_cu, kFwdMaxWorkgroups);
   }
   if (!ok) {
@@ -796,10 +836,26 @@ sbd_status sbd_kv_export(sbd_ctx* c, int32_t seq, int32_t pos0, int32_t n, void*
 
 sbd_status sbd_set_decode_path(sbd_ctx* c, int32_t path) {
   if (!c) return fail(nullptr, SBD_ERR_INVALID_ARG, "null context");
-  if (path != SBD_DECODE_AUTO && path != SBD_DECODE_FUSED && path != SBD_DECODE_KERNELS)
+  if (path != SBD_DECODE_AUTO && path != SBD_DECODE_FUSED && path != SBD_DECODE_KERNELS &&
+      path != SBD_DECODE_LAYERS)
     return fail(c, SBD_ERR_INVALID_ARG, "unknown decode path %d", path);
   c->decode_path = path;
   return SBD_OK;
+}
+
+sbd_status sbd_decode_path_fits(const sbd_ctx* c, int32_t path, int32_t batch, int32_t k, int32_t* fits) {
+  if (!c || !fits) return fail(nullptr, SBD_ERR_INVALID_ARG, "null argument");
+  switch (path) {
+    case SBD_DECODE_AUTO:
+    case SBD_DECODE_KERNELS: *fits = 1; return SBD_OK;
+    case SBD_DECODE_FUSED: {
+      const sbd_model_config& m = c->cfg;
+      *fits = c->n_cu >= 1 && m.d_model % 128 == 0 && (m.head_dim == 64 || m.head_dim == 128) ? 1 : 0;
+      return SBD_OK;
+    }
+    case SBD_DECODE_LAYERS: *fits = layer_xcd_fits(c->cfg, c->n_cu_dev, batch, k) ? 1 : 0; return SBD_OK;
+    default: return fail(nullptr, SBD_ERR_INVALID_ARG, "unknown decode path %d", path);
+  }
 }
 
 sbd_status sbd_profile_enable(sbd_ctx* c, int32_t enable) {

@@ -178,7 +178,6 @@ __device__ __forceinline__ bool last_arrival(int* counter, int expected) {
 // written with plain stores (they reach the shared L2 before the writer's vmcnt drops),
 // read with L1-bypassing loads, and the arrival counter is an atomic performed in that L2.
 // Every counter used this way sits on a 128-byte line of its own.
-constexpr int kCtrStride = 32;  // int32 words between XCD-local counters
 constexpr int kPolicyL2 = 1;    // cache-policy bits of an L1-bypassing access (sc0)
 __device__ __forceinline__ i32x4 ld16_l2(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, kPolicyL2);

@@ -19,7 +19,8 @@ constexpr int kMaxSplits = 64;      // split-KV partitions per (sequence, KV hea
 constexpr int kEbChunk = 4096;      // vocabulary entries per EB partial workgroup
 constexpr int kMaxBlock = 64;       // largest block size k
 constexpr int kCounters = 65536;    // int32 words of arrival counters in the workspace
-constexpr int kAttnCtr0 = 16384;    // first counter word of the attention splits (GEMMs below)
+constexpr int kLayerCtr0 = 16384;    // first counter word of the per-XCD layer kernels (decode GEMMs below)
+constexpr int kCtrStride = 32;      // int32 words between counters that live in one XCD's L2 (a 128-byte line each)
 
 // Where a kernel is enqueued: the stream, plus optional start/stop events that the
 // runtime records at the kernel's own start and end (per-kernel timing).
@@ -58,6 +59,7 @@ struct Layout {
   int64_t gemv_part_floats;  // split-K partial tiles of the decode GEMM
   size_t xn2, sumsq2;        // fused decode forward: second copy of xn (hi, lo) and its partials
   size_t fwd_gains, fwd_ctl, fwd_err;
+  size_t lx_part, lx_dev;     // per-XCD layer kernels: XCD-local and cross-XCD partials
   int64_t fwd_ctl_ints;
   size_t total;
 };
@@ -304,6 +306,57 @@ struct FwdArgs {
 };
 bool fused_plan(FwdArgs& f, int nwg, int64_t part_cap_floats);
 hipError_t launch_fused_forward(const FwdArgs& f, int nwg, const Exec& ex);
+
+// ---------------------------------------------------------------------------- per-XCD layer kernels
+// A decode-sized layer (M <= 16 rows) as two launches of one workgroup per CU, each XCD
+// owning one KV head's share of the work (layer_xcd.hip):
+//   layer_attn_kernel: QKV projection (+ q/k norm, RoPE, K/V into the cache), attention,
+//                      merge and O projection (+ residual, next norm's inputs)
+//   layer_mlp_kernel:  gate/up (+ SwiGLU) and down projection (+ residual, next norm's inputs)
+constexpr int kXcds = 8;        // XCDs of the chip; workgroup i runs on XCD i % 8
+constexpr int kXcdWgs = 32;     // persistent workgroups (CUs) per XCD
+constexpr int kLxQkvFloats = kXcdWgs * 2048;             // per XCD: parked QKV partial tiles
+constexpr int kLxAttnTasks = kXcdWgs;                     // attention tasks per XCD at most
+constexpr int kLxRows = 64;                               // query rows per KV head at most
+constexpr int64_t kLxXcdFloats = kLxQkvFloats + (int64_t)kLxAttnTasks * kLxRows * (128 + 2);
+constexpr int64_t kLxPartFloats = (int64_t)kXcds * kLxXcdFloats;  // XCD-local partials
+constexpr int64_t kLxDevFloats = (int64_t)kXcdWgs * kXcds * 2048; // cross-XCD partials (O, down)
+constexpr int kLxCtrLines = kXcds * 64 + 2 * kXcdWgs;     // counter lines (kCtrStride words each)
+
+struct LayerXArgs {
+  int M, B, k, layer;
+  int d, n_q, n_kv, ffn, qk_norm;
+  float eps, q_scale;
+  int n_tasks;                       // attention key splits per sequence
+  const bf16_t *wqkv, *wo, *wgu, *wdown;   // packed weights of the layer
+  const bf16_t *q_norm, *k_norm;           // Qwen-3 per-head gains (qk_norm)
+  const bf16_t* g_mid;               // MLP norm gain (applied after the O projection)
+  const bf16_t* g_out;               // next attention norm's gain, or the final norm's
+  float* x;                          // residual stream [M][d]
+  const bf16_t *xn, *xn_lo;          // attention input x * g (hi, lo) [M][d]
+  const float* ssq;                  // its partial sums of squares [M][n_part]
+  int n_part;
+  bf16_t *xn_mid, *xn_mid_lo;        // MLP input x * g_mid (hi, lo), written by the O projection
+  float* ssq_mid;                    // its partial sums [M][32]
+  bf16_t *xn_out, *xn_out_lo;        // next layer's input, written by the down projection
+  float* ssq_out;                    // [M][32]
+  bf16_t *q, *q_lo, *attn, *attn_lo, *act, *act_lo;
+  bf16_t *kcache, *vcache;
+  int64_t cap;
+  int n_slots;
+  const float* rope;
+  const RowParam* rows;
+  const SeqParam* seqs;
+  float* xpart;                      // kLxPartFloats
+  float* dpart;                      // kLxDevFloats
+  int* ctr;                          // kLxCtrLines * kCtrStride words, zero at creation
+  int* err;                          // sticky error word and the task code of a failed wait
+  int* err_host;                     // pinned host copy of the same two words
+};
+// True when the per-XCD layer kernels implement this decode-sized forward on this device.
+bool layer_xcd_fits(const sbd_model_config& c, int n_cu, int B, int k);
+hipError_t launch_layer_attn(const LayerXArgs& a, const Exec& ex);
+hipError_t launch_layer_mlp(const LayerXArgs& a, const Exec& ex);
 
 // ---------------------------------------------------------------------------- EB sampler
 struct EbArgs {

@@ -62,19 +62,40 @@ def make_ctx(wl, import_cache=True):
 SAMPLES = {"llama8b_b1_l2048_k16": [0], "llama8b_b32_ragged_k8": "minmax",
            "llama8b_b4_l32768_k16": [3], "qwen8b_b8_l8192_k16": [5]}
 
+# Extra decode-sized cases for the per-XCD layer kernels (at most 16 rows): the Qwen-3-8B
+# shape (q/k norm, ffn 12288) at batch 1, and two sequences of different lengths in one
+# block forward.  Parity cases only, not benchmark workloads.
+EXTRA = {
+    "qwen8b_b1_l2048_k16": (synth.Workload("qwen8b_b1_l2048_k16", synth.QWEN8B, 1006, 1, 16, (1.0,),
+                                           prompt_lens=(2048,)), [0]),
+    "llama8b_b2_ragged_k8": (synth.Workload("llama8b_b2_ragged_k8", synth.LLAMA8B, 1007, 2, 8, (0.5,),
+                                            prompt_lens=(1500, 700)), [0, 1]),
+}
 
-@pytest.mark.parametrize("name", list(SAMPLES))
+
+def workload(name):
+    return EXTRA[name][0] if name in EXTRA else synth.WORKLOADS[name]
+
+
+def decode_paths(lib, batch, k):
+    """The decode paths a forward of batch x k rows runs on: every one that takes it."""
+    if batch * k > 16:
+        return ["auto"]
+    return [p for p in ("layers", "fused", "kernels") if lib.decode_path_fits(p, batch, k)]
+
+
+@pytest.mark.parametrize("name", list(SAMPLES) + list(EXTRA))
 def test_fullsize_block_forward(name):
-    wl = synth.WORKLOADS[name]
+    wl = workload(name)
     s = wl.shape
     print(f"[gpu] {name}: B={wl.batch} k={wl.k}", flush=True)
     w, lib, lens = make_ctx(wl)
-    sample = SAMPLES[name]
+    sample = EXTRA[name][1] if name in EXTRA else SAMPLES[name]
     if sample == "minmax":
         sample = [int(np.argmin(lens)), int(np.argmax(lens))]
     toks, is_mask = synth.block_rows(wl.seed, s, wl.batch, wl.k, n_causal=1)
-    # a decode-sized forward (<= 16 rows) is checked on both of its paths
-    paths = ["fused", "kernels"] if wl.batch * wl.k <= 16 else ["auto"]
+    # a decode-sized forward (<= 16 rows) is checked on every path that takes it
+    paths = decode_paths(lib, wl.batch, wl.k)
     got = {}
     for path in paths:
         lib.set_decode_path(path)
@@ -121,10 +142,13 @@ def test_benched_configuration_with_real_prefill():
     s = wl.shape
     print("[gpu] benched configuration: prefill 2048 + block forward", flush=True)
     w, lib, lens = make_ctx(wl, import_cache=False)
-    lib.set_decode_path("fused")
     prompt = synth.make_tokens(wl.seed, lens[0], s, stream=100)
     last = lib.prefill(0, prompt)
     toks, is_mask = synth.block_rows(wl.seed, s, 1, wl.k, n_causal=1)
+    got_paths = {}
+    for path in decode_paths(lib, 1, wl.k):
+        lib.set_decode_path(path)
+        got_paths[path] = lib.block_forward([0], toks, is_mask=is_mask).cpu().numpy()
     logits = lib.block_forward([0], toks, is_mask=is_mask)
     k_gpu, v_gpu = lib.kv_export(0, 0, lens[0])
     torch.cuda.synchronize()
@@ -141,3 +165,6 @@ def test_benched_configuration_with_real_prefill():
     close(vl, cache.V[-1], max_abs=0.07)
     ref = model.block_forward([cache], toks, [1]).logits
     close(got, ref)
+    for path, g in got_paths.items():
+        print(f"    decode path {path}", flush=True)
+        close(g, ref)
