@@ -52,6 +52,7 @@ constexpr int kCtrMergeDone = 42;    // workgroups past the merge
 constexpr int kCtrOStart = 43;       // workgroups past the O projection's wait
 constexpr int kCtrGuDone = 44;       // workgroups past gate/up
 constexpr int kCtrDownStart = 45;    // workgroups past the down projection's wait
+constexpr int kCtrScratch = 63;      // a line nothing reads (target of l2_touch_keep)
 constexpr int kCtrDevO = kXcds * 64;              // + group: O partial arrivals (device-wide)
 constexpr int kCtrDevDown = kXcds * 64 + kXcdWgs;  // + group: down partial arrivals
 
@@ -74,6 +75,23 @@ __device__ __forceinline__ int xcd_peek(int* ctr) {
   int zero;
   asm volatile("v_mov_b32 %0, 0" : "=v"(zero));
   return __hip_atomic_fetch_add(ctr, zero, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// Pull [p, p + bytes) into the L2 of this XCD: one 4-byte load per 128-byte line, spread
+// over the workgroup.  Ordinary loads, so the compiler tracks their completion; their sum
+// is returned for a use the compiler cannot remove (l2_touch_keep) and never matters.
+__device__ __forceinline__ int l2_touch(const void* p, int64_t bytes) {
+  const char* c = static_cast<const char*>(p);
+  int sum = 0;
+  for (int64_t o = (int64_t)threadIdx.x * 128; o < bytes; o += (int64_t)blockDim.x * 128)
+    sum += *reinterpret_cast<const int*>(c + o);
+  return sum;
+}
+// Consumes the sum of l2_touch: `never` is a value the sum cannot be told from at compile
+// time; the store, into this workgroup's own scratch, is not reached in practice either
+// way and changes nothing another phase reads.
+__device__ __forceinline__ void l2_touch_keep(int sum, int never, int* scratch) {
+  if (sum == never) scratch[threadIdx.x % kCtrStride] = sum;
 }
 
 // Wait until *ctr >= target (thread 0 polls, then the workgroup proceeds).
@@ -313,9 +331,19 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
   float* att_o = att_ml + (int64_t)kLxAttnTasks * kLxRows * 2;  // [task][64 rows][128]
   if (lw < n_tasks) {
     const int b = lw / a.n_tasks, s = lw % a.n_tasks;
-    xcd_wait(a, xcd_ctr(a, x, kCtrQkvDone), ngrp, a.layer * 16 + 1);
-    const int L = a.seqs[b].cache_len;
+    const SeqParam sp = a.seqs[b];
+    const int L = sp.cache_len;
     const int nblk = (L + a.k + 31) / 32;
+    int touched = 0;
+    {  // key blocks holding only positions cached before this forward: into the L2 now
+      const int kb0 = nblk * s / a.n_tasks, kb1 = min(nblk * (s + 1) / a.n_tasks, L / 32);
+      if (kb1 > kb0) {
+        const int64_t hb = attn_head_base(a.layer, sp.slot, x, a.n_slots, a.n_kv, a.cap, kDH);
+        touched += l2_touch(a.kcache + hb + (int64_t)kb0 * 32 * kDH, (int64_t)(kb1 - kb0) * 32 * kDH * 2);
+        touched += l2_touch(a.vcache + hb + (int64_t)kb0 * 32 * kDH, (int64_t)(kb1 - kb0) * 32 * kDH * 2);
+      }
+    }
+    xcd_wait(a, xcd_ctr(a, x, kCtrQkvDone), ngrp, a.layer * 16 + 1);
     AttnArgs aa{};
     aa.seqs = a.seqs; aa.B = a.B; aa.k = a.k; aa.layer = a.layer; aa.n_q = a.n_q; aa.n_kv = a.n_kv; aa.d_h = kDH;
     aa.q = a.q; aa.q_lo = a.q_lo; aa.kcache = a.kcache; aa.vcache = a.vcache; aa.cap = a.cap; aa.n_slots = a.n_slots;
@@ -329,6 +357,7 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
         *(f32x4*)(att_o + ((int64_t)lw * kLxRows + pt.rho) * kDH + 16 * dt + 4 * g4) = pt.o[dt];
     }
     xcd_signal(xcd_ctr(a, x, kCtrAttnDone));
+    l2_touch_keep(touched, a.layer - (1 << 30), xcd_ctr(a, x, kCtrScratch));
   }
 
   // ---- 3. merge: one wave per query row (sequence b, row rho = head-in-group * k + j)

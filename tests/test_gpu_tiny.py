@@ -379,7 +379,13 @@ def test_state_and_argument_errors(tiny):
     err(lambda: lib.eb_select(logits, is_mask, -0.1, s.mask_id), "SBD_ERR_INVALID_ARG")
     err(lambda: lib.eb_select(torch.zeros((1, 4, 2048), device="cuda"), is_mask, 1.0, -1),
         "SBD_ERR_INVALID_ARG")
-    assert lib.lib.sbd_set_decode_path(lib.ctx, 3) == 1                     # unknown path
+    assert lib.lib.sbd_set_decode_path(lib.ctx, 4) == 1                     # unknown path
+    # the per-XCD layer kernels need the 8B layer shape: the tiny decoder is refused before
+    # anything is enqueued
+    assert not lib.decode_path_fits("layers", 1, 4)
+    lib.set_decode_path("layers")
+    err(lambda: lib.block_forward([0], toks), "SBD_ERR_UNSUPPORTED")
+    lib.set_decode_path(tiny.path)
     # a failed call changes nothing
     assert lib.cache_len(0) == 11
     lib.block_forward([0], toks, n_causal=[1])
