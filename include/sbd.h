@@ -250,7 +250,8 @@ typedef enum {
   SBD_KERNEL_FUSED = 11,     /* fused decode forward: all layers + LM head in one launch */
   SBD_KERNEL_LAYER_ATTN = 12,/* per-XCD layer kernel: QKV + attention + O projection */
   SBD_KERNEL_LAYER_MLP = 13, /* per-XCD layer kernel: gate/up + down projection */
-  SBD_KERNEL_COUNT = 14
+  SBD_KERNEL_LAYER_FINAL = 14, /* per-XCD layer kernels: final norm inputs from the residual */
+  SBD_KERNEL_COUNT = 15
 } sbd_kernel;
 sbd_status sbd_profile_enable(sbd_ctx* ctx, int32_t enable);
 sbd_status sbd_profile_read(sbd_ctx* ctx, int32_t kernel, int32_t* launches, double* total_ms);

@@ -25,7 +25,7 @@ LAYER_FIELDS = ("attn_norm", "wq", "wk", "wv", "wo", "q_norm", "k_norm", "mlp_no
 
 # sbd_kernel values, in order.
 KERNEL_NAMES = ("embed", "qkv", "rope", "attention", "attn_merge", "o_proj", "gate_up", "down",
-                "lm_head", "eb_partial", "eb_select", "fused", "layer_attn", "layer_mlp")
+                "lm_head", "eb_partial", "eb_select", "fused", "layer_attn", "layer_mlp", "layer_final")
 DECODE_PATHS = {"auto": 0, "fused": 1, "kernels": 2, "layers": 3}  # sbd_decode_path
 
 # Every entry point of sbd.h with its argument types.

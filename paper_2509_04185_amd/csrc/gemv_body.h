@@ -87,3 +87,110 @@ __device__ __forceinline__ void gemv_stream(__amdgpu_buffer_rsrc_t ra, __amdgpu_
 }
 
 }  // namespace sbd
+
+namespace sbd {
+
+// ---- the same stream with the activations taken from the fixed-point residual
+//
+// The per-XCD layer kernels keep the residual stream x as int64 fixed point (value * 2^32):
+// partial sums from several XCDs are then added with integer atomics, exactly and in any
+// order.  A consumer forms its operand itself: x = hi32 + lo32 * 2^-32 in fp32, times the
+// norm gain g[k], split into hi/lo bf16; it also accumulates x^2 of the elements it reads,
+// the input of its RMSNorm scale.  A lane reads 8 consecutive k of its row per step: 64
+// bytes of x plus 16 bytes of g.
+
+constexpr float kFixScale = 4294967296.0f;  // 2^32
+__device__ __forceinline__ float fix_to_f32(int lo, int hi) {
+  return (float)hi + (float)(uint32_t)lo * (1.0f / kFixScale);
+}
+
+template <int U>
+__device__ __forceinline__ void gemv_issue_x64(__amdgpu_buffer_rsrc_t rx, __amdgpu_buffer_rsrc_t rg, uint32_t x_off,
+                                               uint32_t g_off, int b0, int ns, i32x4 (&xv)[U][4], i32x4 (&gv)[U]) {
+#pragma unroll
+  for (int uu = 0; uu < U; ++uu) {
+    const uint32_t st = (uint32_t)min(b0 + uu, ns - 1);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) xv[uu][q] = __builtin_amdgcn_raw_buffer_load_b128(rx, x_off + st * 256u + q * 16u, 0, 0);
+    gv[uu] = __builtin_amdgcn_raw_buffer_load_b128(rg, g_off + st * 64u, 0, 0);
+  }
+}
+
+// hi/lo bf16 operands of 8 elements; ss += their x^2 (steps past the end add nothing).
+__device__ __forceinline__ void x64_operand(const i32x4 (&xv)[4], i32x4 gv, bool ok, i32x4& a_hi, i32x4& a_lo, float& ss) {
+  float v[8];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    v[2 * q] = fix_to_f32(xv[q][0], xv[q][1]);
+    v[2 * q + 1] = fix_to_f32(xv[q][2], xv[q][3]);
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ss += ok ? v[e] * v[e] : 0.f;
+  float xg[8];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const uint32_t gw = (uint32_t)gv[e];
+    xg[2 * e] = v[2 * e] * __uint_as_float(gw << 16);
+    xg[2 * e + 1] = v[2 * e + 1] * __uint_as_float(gw & 0xffff0000u);
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const uint32_t h = pack_bf2(xg[2 * e], xg[2 * e + 1]);
+    a_hi[e] = ok ? (int)h : 0;
+    a_lo[e] = ok ? (int)pack_bf2(xg[2 * e] - __uint_as_float(h << 16), xg[2 * e + 1] - __uint_as_float(h & 0xffff0000u)) : 0;
+  }
+}
+
+template <int C, int U>
+__device__ __forceinline__ void gemv_mfma_x64(const i32x4 (&wv)[U][C], const i32x4 (&xv)[U][4], const i32x4 (&gv)[U],
+                                              int b0, int ns, f32x4 (&acc)[C], float& ss) {
+#pragma unroll
+  for (int uu = 0; uu < U; ++uu) {
+    i32x4 a_hi, a_lo;
+    x64_operand(xv[uu], gv[uu], b0 + uu < ns, a_hi, a_lo, ss);
+#pragma unroll
+    for (int ct = 0; ct < C; ++ct) {
+      acc[ct] = mfma16x16x32(a_hi, wv[uu][ct], acc[ct]);
+      acc[ct] = mfma16x16x32(a_lo, wv[uu][ct], acc[ct]);
+    }
+  }
+}
+
+// gemv_stream with the operand formed from the fixed-point residual: x_off is this lane's
+// byte offset into x at step 0 (8 bytes per element), g_off its byte offset into the gain.
+template <int C, int U>
+__device__ __forceinline__ void gemv_stream_x64(__amdgpu_buffer_rsrc_t rx, __amdgpu_buffer_rsrc_t rg, uint32_t x_off,
+                                                uint32_t g_off, const bf16_t* const (&wt)[C], int ns,
+                                                f32x4 (&acc)[C], float& ss) {
+  if (ns <= 0) return;
+  const int nb = (ns + U - 1) / U;
+  i32x4 w0[U][C], w1[U][C], x0[U][4], x1[U][4], g0[U], g1[U];
+  gemv_issue_x64<U>(rx, rg, x_off, g_off, 0, ns, x0, g0);
+  gemv_issue_w<C, U>(wt, 0, ns, w0);
+  for (int b = 0; b < nb; b += 2) {
+    if (b + 1 < nb) {
+      gemv_issue_x64<U>(rx, rg, x_off, g_off, (b + 1) * U, ns, x1, g1);
+      gemv_issue_w<C, U>(wt, (b + 1) * U, ns, w1);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    gemv_mfma_x64<C, U>(w0, x0, g0, b * U, ns, acc, ss);
+    __builtin_amdgcn_sched_barrier(0);
+    if (b + 1 < nb) {
+      if (b + 2 < nb) {
+        gemv_issue_x64<U>(rx, rg, x_off, g_off, (b + 2) * U, ns, x0, g0);
+        gemv_issue_w<C, U>(wt, (b + 2) * U, ns, w0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      gemv_mfma_x64<C, U>(w1, x1, g1, (b + 1) * U, ns, acc, ss);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+}
+
+// Add a value to the fixed-point residual (exact; any order gives the same sum).
+__device__ __forceinline__ void fix_add(int64_t* p, float v) {
+  const long long q = __double2ll_rn((double)v * 4294967296.0);
+  atomicAdd(reinterpret_cast<unsigned long long*>(p), (unsigned long long)q);
+}
+
+}  // namespace sbd

@@ -1,6 +1,6 @@
 // Per-XCD layer kernels: a decode-sized layer (M <= 16 block rows) of the SBD block forward
 // as two launches, each of one workgroup per CU, with the work of every phase divided
-// between the 8 XCDs so that almost every hand-off stays inside one XCD's L2.
+// between the 8 XCDs so that every hand-off but the residual update stays inside one XCD.
 //
 // One kernel per projection (gemv.hip) pays, at every kernel boundary, the launch gap, the
 // first-load latency of the next kernel and the tail of the previous one (wave reduction,
@@ -14,19 +14,24 @@
 //     2. run the attention of KV head x, one task per key range (32 / B per sequence);
 //     3. merge the tasks, one wave per query row, into the attention output;
 //     4. multiply that output - the K slice x of the O projection - by W_o, one packed group
-//        (128 output columns) per workgroup; the 8 XCDs' partials of a group are added by
-//        the last to arrive (in XCD order), which runs the residual epilogue.
+//        (128 output columns) per workgroup, and add the product into the residual.
 //   layer_mlp_kernel   XCD x owns columns [x F/8, (x+1) F/8) of the MLP.  Its 32 workgroups
 //     1. project gate/up for those columns (F/2048 tiles each) with the SwiGLU epilogue;
 //     2. multiply them - the K slice x of the down projection - by W_down, one packed group
-//        per workgroup; partials of the 8 XCDs are added as in step 4 above.
+//        per workgroup, and add the product into the residual.
+//
+// The residual is int64 fixed point (x * 2^32): the 8 XCDs' partial products of an output
+// column are added with integer atomics, exact in any order, so no XCD waits for another
+// and the result does not depend on timing.  The next consumer (QKV of the next layer,
+// gate/up) forms x * g as hi/lo bf16 from it while it streams and adds up x^2 for its
+// RMSNorm scale: the scale is constant along a row, so it is applied to the products.
 //
 // Phases 1-4 of a kernel depend on each other only within an XCD: a producer writes with
 // plain stores (they reach the XCD's L2 before its vmcnt drops), raises an XCD counter with
-// an L2 atomic, and consumers poll it with L2 atomics and then read the data (lines their
-// CU has not read before in the launch, so they come from the L2).  Only the O and down partials cross XCDs (device-scope stores and loads, as in the
-// split-K hand-off of gemv.hip).  The weights of a phase never depend on activations, so
-// each workgroup requests its first O / down weights before it waits for its inputs.
+// an atomic, and consumers poll it with atomics (a load could be served by the CU's own L1)
+// and then read the data (lines their CU has not read before in the launch).  The weights
+// of a phase never depend on activations, so each workgroup requests its first O / down
+// weights before it waits for its inputs.
 //
 // Every wait is bounded: a wait that gives up raises a sticky error (device word and pinned
 // host copy) that the next API call reports, and the launch runs to its end.  All 32
@@ -53,8 +58,9 @@ constexpr int kCtrOStart = 43;       // workgroups past the O projection's wait
 constexpr int kCtrGuDone = 44;       // workgroups past gate/up
 constexpr int kCtrDownStart = 45;    // workgroups past the down projection's wait
 constexpr int kCtrScratch = 63;      // a line nothing reads (target of l2_touch_keep)
-constexpr int kCtrDevO = kXcds * 64;              // + group: O partial arrivals (device-wide)
-constexpr int kCtrDevDown = kXcds * 64 + kXcdWgs;  // + group: down partial arrivals
+// device-wide lines, after the 8 XCDs' blocks
+constexpr int kCtrDevRead = kXcds * 64;      // workgroups done reading the residual
+constexpr int kCtrDevPassed = kXcds * 64 + 1;  // workgroups past the wait on it
 
 __device__ __forceinline__ int* xcd_ctr(const LayerXArgs& a, int x, int line) {
   return a.ctr + (int64_t)(x * 64 + line) * kCtrStride;
@@ -71,10 +77,11 @@ __device__ __forceinline__ void xcd_signal(int* ctr) {
 // load may be served by this CU's L1, which keeps the first value it fetched.  An atomic is
 // always performed in the L2; adding a zero the compiler cannot see keeps it from turning
 // the idempotent update back into a load.
+template <int SCOPE = __HIP_MEMORY_SCOPE_WORKGROUP>
 __device__ __forceinline__ int xcd_peek(int* ctr) {
   int zero;
   asm volatile("v_mov_b32 %0, 0" : "=v"(zero));
-  return __hip_atomic_fetch_add(ctr, zero, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  return __hip_atomic_fetch_add(ctr, zero, __ATOMIC_RELAXED, SCOPE);
 }
 
 // Pull [p, p + bytes) into the L2 of this XCD: one 4-byte load per 128-byte line, spread
@@ -94,11 +101,13 @@ __device__ __forceinline__ void l2_touch_keep(int sum, int never, int* scratch) 
   if (sum == never) scratch[threadIdx.x % kCtrStride] = sum;
 }
 
-// Wait until *ctr >= target (thread 0 polls, then the workgroup proceeds).
+// Wait until *ctr >= target (thread 0 polls, then the workgroup proceeds).  SCOPE: that of
+// the counter's writers (device scope for a device-wide counter).
+template <int SCOPE = __HIP_MEMORY_SCOPE_WORKGROUP>
 __device__ __forceinline__ void xcd_wait(const LayerXArgs& a, int* ctr, int target, int what) {
   if (threadIdx.x == 0) {
     int it = 0;
-    while (xcd_peek(ctr) < target) {
+    while (xcd_peek<SCOPE>(ctr) < target) {
       __builtin_amdgcn_s_sleep(1);
       if (++it > kLxSpin) {
         atomicOr(a.err, 1);
@@ -128,20 +137,6 @@ __device__ __forceinline__ void xcd_passed(const LayerXArgs& a, int x, int line,
   }
 }
 
-// 1/rms of rows 0..15 from partial sums of squares [M][n_part]: 16 threads per row.
-__device__ __forceinline__ float ssq_share(const float* ssq, int n_part, int M) {
-  const int m = threadIdx.x >> 4, q = threadIdx.x & 15;
-  float s = 0.f;
-  if (m < M)
-    for (int p = q; p < n_part; p += 16) s += ssq[(int64_t)m * n_part + p];
-  return s;
-}
-__device__ __forceinline__ void rinv_finish(float s, float inv_d, float eps, float* rinv_s) {
-#pragma unroll
-  for (int o = 8; o >= 1; o >>= 1) s += __shfl_xor(s, o);
-  if ((threadIdx.x & 15) == 0) rinv_s[threadIdx.x >> 4] = 1.0f / sqrtf(s * inv_d + eps);
-}
-
 // The 4 waves' partial tiles of a C-tile unit added in wave order; wave w ends with the sums
 // of the tiles ct = w, w + 4, ... (the tiles it owns).  red: 4 * C KB of LDS.
 template <int C>
@@ -162,15 +157,46 @@ __device__ __forceinline__ void reduce_waves(f32x4 (&acc)[C], char* red_mem) {
   __syncthreads();  // red is free again
 }
 
-// Residual epilogue of packed group grp from its 8 summed tiles (wave w owns tiles w, w + 4):
-// x += y; xn = x * g as hi/lo; one partial sum of x^2 per row for this group.
-__device__ __forceinline__ void resid_epilogue(const LayerXArgs& a, int grp, const f32x4 (&acc)[8],
-                                               const f32x4 (&x_pre)[2], const float (&g_pre)[2], const bf16_t* g,
-                                               bf16_t* xn, bf16_t* xn_lo, float* ssq, char* smem) {
-  (void)g;
+// Sum of x^2 of rows 0..15 over the lanes and waves of a workgroup: lane (r, g) of every
+// wave holds a share of row r; the 4 waves' row sums are added in wave order.  Result in
+// row_s[0..15] (LDS) after the call.
+__device__ __forceinline__ void row_ss_reduce(float ss, float* tmp_s, float* row_s) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  ss += __shfl_xor(ss, 16);
+  ss += __shfl_xor(ss, 32);
+  if (lane < 16) tmp_s[wave * 16 + lane] = ss;
+  __syncthreads();
+  if (threadIdx.x < 16)
+    row_s[threadIdx.x] = tmp_s[threadIdx.x] + tmp_s[16 + threadIdx.x] + tmp_s[32 + threadIdx.x] + tmp_s[48 + threadIdx.x];
+  __syncthreads();
+}
+
+// The residual is read (phase 1) and updated (last phase) in the same launch, by workgroups
+// of all XCDs: an update may start only once every workgroup has finished reading.  Each
+// workgroup reports when it has (dev_read_done); the first update of a workgroup waits for
+// all 256 reports (dev_read_wait), which in practice have long arrived; the last workgroup
+// past the wait resets both counters for the next launch.
+__device__ __forceinline__ void dev_read_done(const LayerXArgs& a) {
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_fetch_add(a.ctr + (int64_t)kCtrDevRead * kCtrStride, 1, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void dev_read_wait(const LayerXArgs& a, int what) {
+  int* rd = a.ctr + (int64_t)kCtrDevRead * kCtrStride;
+  int* ps = a.ctr + (int64_t)kCtrDevPassed * kCtrStride;
+  xcd_wait<__HIP_MEMORY_SCOPE_AGENT>(a, rd, kXcds * kXcdWgs, what);
+  if (threadIdx.x == 0 &&
+      __hip_atomic_fetch_add(ps, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == kXcds * kXcdWgs - 1) {
+    __hip_atomic_store(rd, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(ps, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// Add the summed tiles of packed group grp (wave w owns tiles w and w + 4) into the
+// fixed-point residual.
+__device__ __forceinline__ void residual_add(const LayerXArgs& a, int grp, const f32x4 (&acc)[8]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = lane & 15, g4 = lane >> 4;
-  float* ssq_s = reinterpret_cast<float*>(smem);  // [8 tiles][16 rows]
 #pragma unroll
   for (int k2 = 0; k2 < 2; ++k2) {
     const int ct = wave + 4 * k2;
@@ -178,73 +204,9 @@ __device__ __forceinline__ void resid_epilogue(const LayerXArgs& a, int grp, con
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int m = 4 * g4 + i;
-      float xv = 0.f;
-      if (m < a.M) {
-        xv = x_pre[k2][i] + acc[ct][i];
-        a.x[(int64_t)m * a.d + n] = xv;
-        bf16_t hi, lo;
-        split_bf16(xv * g_pre[k2], hi, lo);
-        xn[(int64_t)m * a.d + n] = hi;
-        xn_lo[(int64_t)m * a.d + n] = lo;
-      }
-      float s2 = xv * xv;
-      s2 += __shfl_xor(s2, 1);
-      s2 += __shfl_xor(s2, 2);
-      s2 += __shfl_xor(s2, 4);
-      s2 += __shfl_xor(s2, 8);
-      if (r == 0) ssq_s[ct * 16 + m] = s2;
+      if (m < a.M) fix_add(a.x64 + (int64_t)m * a.d + n, acc[ct][i]);
     }
   }
-  __syncthreads();
-  if (threadIdx.x < a.M) {
-    float s = 0.f;
-#pragma unroll
-    for (int ct = 0; ct < 8; ++ct) s += ssq_s[ct * 16 + threadIdx.x];
-    ssq[(int64_t)threadIdx.x * kXcdWgs + grp] = s;
-  }
-}
-
-// The residual rows and the next norm's gain of the two tiles wave w finishes (w, w + 4).
-__device__ __forceinline__ void resid_prefetch(const LayerXArgs& a, int grp, const bf16_t* g, f32x4 (&x_pre)[2],
-                                               float (&g_pre)[2]) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int r = lane & 15, g4 = lane >> 4;
-#pragma unroll
-  for (int k2 = 0; k2 < 2; ++k2) {
-    const int n = (grp * 8 + wave + 4 * k2) * 16 + r;
-    g_pre[k2] = bf2f(g[n]);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int m = 4 * g4 + i;
-      x_pre[k2][i] = m < a.M ? a.x[(int64_t)m * a.d + n] : 0.f;
-    }
-  }
-}
-
-// Cross-XCD split of a packed group's 8 tiles: park this XCD's sums (device-scope), and in
-// the last of the 8 to arrive add all of them in XCD order.  True in that workgroup.
-__device__ __forceinline__ bool cross_xcd_sum(const LayerXArgs& a, int grp, int x, int ctr_line, f32x4 (&acc)[8]) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const __amdgpu_buffer_rsrc_t rp = buf_rsrc(a.dpart);
-#pragma unroll
-  for (int k2 = 0; k2 < 2; ++k2) {
-    const int ct = wave + 4 * k2;
-    st16_dev(rp, (uint32_t)(((((int64_t)grp * kXcds + x) * 8 + ct) * 64 + lane) * 16), __builtin_bit_cast(i32x4, acc[ct]));
-  }
-  if (!last_arrival(a.ctr + (int64_t)(ctr_line + grp) * kCtrStride, kXcds)) return false;
-#pragma unroll
-  for (int k2 = 0; k2 < 2; ++k2) {
-    const int ct = wave + 4 * k2;
-    i32x4 v[kXcds];
-#pragma unroll
-    for (int z = 0; z < kXcds; ++z)
-      v[z] = ld16_dev(rp, (uint32_t)(((((int64_t)grp * kXcds + z) * 8 + ct) * 64 + lane) * 16));
-    f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int z = 0; z < kXcds; ++z) s += __builtin_bit_cast(f32x4, v[z]);
-    acc[ct] = s;
-  }
-  return true;
 }
 
 }  // namespace
@@ -257,7 +219,6 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
   const int G = a.n_q / a.n_kv;
   const int ngrp = G + 2, KS = kXcdWgs / ngrp;
   float* xpart = a.xpart + (int64_t)x * kLxXcdFloats;
-  float* rinv_s = reinterpret_cast<float*>(smem + 65536 + 1024);  // [16]
 
   // ---- 1. QKV projection, unit (group gi of this XCD, K slice kc)
   if (lw < ngrp * KS) {
@@ -271,7 +232,6 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
     e.n_q = a.n_q; e.n_kv = a.n_kv; e.d_h = kDH; e.qk_norm = a.qk_norm; e.eps = a.eps; e.q_scale = a.q_scale;
     e.rope = a.rope; e.q_norm = a.q_norm; e.k_norm = a.k_norm; e.q = a.q; e.q_lo = a.q_lo;
     e.kcache = a.kcache; e.vcache = a.vcache; e.cap = a.cap; e.n_slots = a.n_slots;
-    const float sq = ssq_share(a.ssq, a.n_part, a.M);
     QkvPre<kDH> qpre;
     qkv_epi_prefetch<kDH>(e, a.M, qpre);
     const int arow = r < a.M ? r : a.M - 1;
@@ -281,37 +241,46 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
     f32x4 acc[8];
 #pragma unroll
     for (int ct = 0; ct < 8; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-    {
-      i32x4 w0[1][8];
-      gemv_stream<8, 1, 0, false>(buf_rsrc(a.xn), buf_rsrc(a.xn_lo),
-                                  (uint32_t)(((int64_t)arow * a.d + g4 * 8 + s_b * 32) * 2), wt, ns, w0, acc);
-    }
-    rinv_finish(sq, 1.0f / a.d, a.eps, rinv_s);
+    float ss = 0.f;  // x^2 of this lane's elements of row r: the slice's share of the RMSNorm sums
+    gemv_stream_x64<8, 1>(buf_rsrc(a.x64), buf_rsrc(a.g_attn), (uint32_t)(((int64_t)arow * a.d + g4 * 8 + s_b * 32) * 8),
+                          (uint32_t)((g4 * 8 + s_b * 32) * 2), wt, ns, acc, ss);
+    float* ss_s = reinterpret_cast<float*>(smem + 65536 + 1024);  // [64] wave shares, then [16] rows
+    row_ss_reduce(r < a.M ? ss : 0.f, ss_s, ss_s + 64);
     reduce_waves<8>(acc, smem);
-    // park this slice in the XCD's L2; the last of the group's KS slices finishes the group
-    float* qp = xpart + (int64_t)gi * KS * 2048;
+    // park this slice (tiles, then its 16 row sums of x^2) in the XCD's L2; the last of the
+    // group's KS slices finishes the group
+    float* qp = xpart + (int64_t)gi * KS * kLxQkvSlice;
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) {
       const int ct = wave + 4 * k2;
-      *(f32x4*)(qp + (((int64_t)kc * 8 + ct) * 64 + lane) * 4) = acc[ct];
+      *(f32x4*)(qp + (int64_t)kc * kLxQkvSlice + (ct * 64 + lane) * 4) = acc[ct];
     }
+    if (threadIdx.x < 16) qp[(int64_t)kc * kLxQkvSlice + 2048 + threadIdx.x] = ss_s[64 + threadIdx.x];
     if (last_arrival_xcd(xcd_ctr(a, x, kCtrQkv + gi), KS)) {
       const __amdgpu_buffer_rsrc_t rq = buf_rsrc(qp);
       f32x4* fin = reinterpret_cast<f32x4*>(smem);  // [8][64]
 #pragma unroll
       for (int k2 = 0; k2 < 2; ++k2) {
         const int ct = wave + 4 * k2;
-        f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+        f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
         for (int z0_ = 0; z0_ < KS; z0_ += 4) {
           i32x4 v[4];
 #pragma unroll
           for (int u = 0; u < 4; ++u)
-            v[u] = z0_ + u < KS ? ld16_l2(rq, (uint32_t)((((int64_t)(z0_ + u) * 8 + ct) * 64 + lane) * 16))
+            v[u] = z0_ + u < KS ? ld16_l2(rq, (uint32_t)(((int64_t)(z0_ + u) * kLxQkvSlice + (ct * 64 + lane) * 4) * 4))
                                 : i32x4{0, 0, 0, 0};
 #pragma unroll
-          for (int u = 0; u < 4; ++u) s += __builtin_bit_cast(f32x4, v[u]);
+          for (int u = 0; u < 4; ++u) sum += __builtin_bit_cast(f32x4, v[u]);
         }
-        fin[ct * 64 + lane] = s;
+        fin[ct * 64 + lane] = sum;
+      }
+      float* rinv_s = reinterpret_cast<float*>(smem + 65536 + 2048);  // [16]
+      if (threadIdx.x < 16) {  // the KS slices' sums of x^2 of row threadIdx.x, in slice order
+        float t = 0.f;
+        for (int z = 0; z < KS; ++z)
+          t += __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                             rq, (uint32_t)(((int64_t)z * kLxQkvSlice + 2048 + threadIdx.x) * 4), 0, kPolicyL2));
+        rinv_s[threadIdx.x] = 1.0f / sqrtf(t / (float)a.d + a.eps);
       }
       __syncthreads();
 #pragma unroll
@@ -323,7 +292,7 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
       xcd_signal(xcd_ctr(a, x, kCtrQkvDone));
     }
   }
-  __syncthreads();
+  dev_read_done(a);  // this workgroup reads the residual no more
 
   // ---- 2. attention of KV head x: task t = (sequence, key range)
   const int n_tasks = a.B * a.n_tasks;
@@ -422,9 +391,6 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
     constexpr int U = 4;
     i32x4 w0[U][8];
     if (ns > 0) gemv_issue_w<8, U>(wt, 0, ns, w0);  // weights first: they wait for nothing
-    f32x4 x_pre[2];
-    float g_pre[2];
-    resid_prefetch(a, grp, a.g_mid, x_pre, g_pre);
     xcd_wait(a, xcd_ctr(a, x, kCtrMergeDone), kXcdWgs, a.layer * 16 + 3);
     {
       const int resets[3] = {kCtrQkvDone, kCtrAttnDone, kCtrMergeDone};
@@ -437,8 +403,8 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
     gemv_stream<8, U, kPolicyL2, true>(buf_rsrc(a.attn), buf_rsrc(a.attn_lo),
                                        (uint32_t)(((int64_t)arow * qd + g4 * 8 + s_b * 32) * 2), wt, ns, w0, acc);
     reduce_waves<8>(acc, smem);
-    if (cross_xcd_sum(a, grp, x, kCtrDevO, acc))
-      resid_epilogue(a, grp, acc, x_pre, g_pre, a.g_mid, a.xn_mid, a.xn_mid_lo, a.ssq_mid, smem);
+    dev_read_wait(a, a.layer * 16 + 4);
+    residual_add(a, grp, acc);
   }
 }
 
@@ -448,14 +414,13 @@ __global__ __launch_bounds__(256) void layer_mlp_kernel(LayerXArgs a) {
   const int x = blockIdx.x & 7, lw = blockIdx.x >> 3;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = lane & 15, g4 = lane >> 4;
-  float* rinv_s = reinterpret_cast<float*>(smem + 65536 + 1024);
+  float* ss_s = reinterpret_cast<float*>(smem + 65536 + 1024);  // [64] wave shares, then [16] rows
 
   // ---- 1. gate/up + SwiGLU: tiles t0 .. t0 + CG - 1 (activation columns 8 t .. 8 t + 7)
   {
     const int t0 = (x * kXcdWgs + lw) * CG;
     const int S = a.d / 32;
     const int s_b = S * wave / 4, ns = S * (wave + 1) / 4 - s_b;
-    const float sq = ssq_share(a.ssq_mid, kXcdWgs, a.M);
     const int arow = r < a.M ? r : a.M - 1;
     const bf16_t* wt[CG];
 #pragma unroll
@@ -463,12 +428,13 @@ __global__ __launch_bounds__(256) void layer_mlp_kernel(LayerXArgs a) {
     f32x4 acc[CG];
 #pragma unroll
     for (int ct = 0; ct < CG; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-    {
-      i32x4 w0[1][CG];
-      gemv_stream<CG, 1, 0, false>(buf_rsrc(a.xn_mid), buf_rsrc(a.xn_mid_lo),
-                                   (uint32_t)(((int64_t)arow * a.d + g4 * 8 + s_b * 32) * 2), wt, ns, w0, acc);
-    }
-    rinv_finish(sq, 1.0f / a.d, a.eps, rinv_s);
+    float ss = 0.f;  // the whole row passes through the 4 waves: its sum of x^2 for the RMSNorm
+    gemv_stream_x64<CG, 1>(buf_rsrc(a.x64), buf_rsrc(a.g_mlp), (uint32_t)(((int64_t)arow * a.d + g4 * 8 + s_b * 32) * 8),
+                           (uint32_t)((g4 * 8 + s_b * 32) * 2), wt, ns, acc, ss);
+    dev_read_done(a);
+    row_ss_reduce(r < a.M ? ss : 0.f, ss_s, ss_s + 64);
+    float* rinv_s = ss_s + 64;
+    if (threadIdx.x < 16) rinv_s[threadIdx.x] = 1.0f / sqrtf(rinv_s[threadIdx.x] / (float)a.d + a.eps);
     reduce_waves<CG>(acc, smem);
 #pragma unroll
     for (int ct = 0; ct < CG; ++ct) {
@@ -501,9 +467,6 @@ __global__ __launch_bounds__(256) void layer_mlp_kernel(LayerXArgs a) {
     constexpr int U = 2;
     i32x4 w0[U][8];
     if (ns > 0) gemv_issue_w<8, U>(wt, 0, ns, w0);  // weights first: they wait for nothing
-    f32x4 x_pre[2];
-    float g_pre[2];
-    resid_prefetch(a, grp, a.g_out, x_pre, g_pre);
     xcd_wait(a, xcd_ctr(a, x, kCtrGuDone), kXcdWgs, a.layer * 16 + 5);
     {
       const int resets[1] = {kCtrGuDone};
@@ -516,8 +479,29 @@ __global__ __launch_bounds__(256) void layer_mlp_kernel(LayerXArgs a) {
     gemv_stream<8, U, kPolicyL2, true>(buf_rsrc(a.act), buf_rsrc(a.act_lo),
                                        (uint32_t)(((int64_t)arow * a.ffn + g4 * 8 + s_b * 32) * 2), wt, ns, w0, acc);
     reduce_waves<8>(acc, smem);
-    if (cross_xcd_sum(a, grp, x, kCtrDevDown, acc))
-      resid_epilogue(a, grp, acc, x_pre, g_pre, a.g_out, a.xn_out, a.xn_out_lo, a.ssq_out, smem);
+    dev_read_wait(a, a.layer * 16 + 6);
+    residual_add(a, grp, acc);
+  }
+}
+
+// After the last layer: the LM head's inputs from the fixed-point residual.  Workgroup m
+// takes row m; thread t its 16 columns 16 t .. 16 t + 15.
+__global__ __launch_bounds__(256) void layer_finalize_kernel(FinalizeArgs a) {
+  const int m = blockIdx.x;
+  for (int c0 = threadIdx.x * 16; c0 < a.d; c0 += 256 * 16) {
+    float s = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int64_t v = a.x64[(int64_t)m * a.d + c0 + e];
+      const float xv = fix_to_f32((int)(uint32_t)(uint64_t)v, (int)(v >> 32));
+      a.x[(int64_t)m * a.d + c0 + e] = xv;
+      bf16_t hi, lo;
+      split_bf16(xv * bf2f(a.g[c0 + e]), hi, lo);
+      a.xn[(int64_t)m * a.d + c0 + e] = hi;
+      a.xn_lo[(int64_t)m * a.d + c0 + e] = lo;
+      s += xv * xv;
+    }
+    a.sumsq[(int64_t)m * (a.d / 16) + c0 / 16] = s;
   }
 }
 
@@ -537,6 +521,12 @@ bool layer_xcd_fits(const sbd_model_config& c, int n_cu, int B, int k) {
 
 hipError_t launch_layer_attn(const LayerXArgs& a, const Exec& ex) {
   SBD_KLAUNCH(layer_attn_kernel, dim3(kXcds * kXcdWgs), dim3(256), ex, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_layer_finalize(const FinalizeArgs& a, const Exec& ex) {
+  if (a.d % (16 * 256) != 0) return hipErrorInvalidValue;
+  SBD_KLAUNCH(layer_finalize_kernel, dim3(a.M), dim3(256), ex, a);
   return hipGetLastError();
 }
 

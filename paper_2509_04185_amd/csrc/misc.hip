@@ -29,6 +29,7 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
   for (int c = threadIdx.x; c < a.d; c += 256) {
     const float v = bf2f(a.embed[(int64_t)tok * a.d + c]);
     a.x[(int64_t)m * a.d + c] = v;
+    if (a.x64 != nullptr) a.x64[(int64_t)m * a.d + c] = __double2ll_rn((double)v * 4294967296.0);
     bf16_t hi, lo;
     split_bf16(v * bf2f(a.g[c]), hi, lo);
     a.xn[(int64_t)m * a.d + c] = hi;

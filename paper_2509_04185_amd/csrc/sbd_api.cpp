@@ -104,7 +104,7 @@ bool sbd::compute_layout(const sbd_model_config& c, Layout* L) {
   o.fwd_ctl = take(o.fwd_ctl_ints * sizeof(int32_t));
   o.fwd_err = take(2 * sizeof(int32_t));
   o.lx_part = take(kLxPartFloats * sizeof(float));
-  o.lx_dev = take(kLxDevFloats * sizeof(float));
+  o.x64 = take(o.m_max * c.d_model * sizeof(int64_t));
   o.counters = take((int64_t)kCounters * sizeof(int32_t));
   o.total = off;
   *L = o;
@@ -303,7 +303,8 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   if (st) return st;
   st = upload(c, c->ws + L.seqs, seqs.data(), seqs.size() * sizeof(SeqParam));
   if (st) return st;
-  EmbedArgs ea{drows, M, d, c->embed, c->layers[0].attn_norm, x, xn, xn_lo, sumsq};
+  EmbedArgs ea{drows, M, d, c->embed, c->layers[0].attn_norm, x, xn, xn_lo, sumsq,
+               layers_fit ? c->at<int64_t>(L.x64) : nullptr};
   SBD_LAUNCH(c, SBD_KERNEL_EMBED, launch_embed(ea, ex));
   if (fused) {
     SBD_HIP(c, hipMemsetAsync(f.ctl, 0, (size_t)f.plan.n_ctl * sizeof(int32_t), c->stream));
@@ -329,26 +330,25 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     lx.qk_norm = m.qk_norm; lx.eps = m.rms_eps;
     lx.q_scale = (float)(1.4426950408889634 / std::sqrt((double)dh));
     lx.n_tasks = kXcdWgs / B;
-    lx.x = x; lx.xn = xn; lx.xn_lo = xn_lo; lx.ssq = sumsq;
-    lx.xn_mid = c->at<bf16_t>(L.xn2); lx.xn_mid_lo = lx.xn_mid + L.m_max * d; lx.ssq_mid = c->at<float>(L.sumsq2);
-    lx.xn_out = xn; lx.xn_out_lo = xn_lo; lx.ssq_out = sumsq;
+    lx.x64 = c->at<int64_t>(L.x64);
     lx.q = q; lx.q_lo = q_lo; lx.attn = attn; lx.attn_lo = attn_lo; lx.act = act; lx.act_lo = act_lo;
     lx.kcache = c->at<bf16_t>(L.kcache); lx.vcache = c->at<bf16_t>(L.vcache); lx.cap = L.cap;
     lx.n_slots = m.max_batch; lx.rope = c->at<float>(L.rope); lx.rows = drows; lx.seqs = dseqs;
-    lx.xpart = c->at<float>(L.lx_part); lx.dpart = c->at<float>(L.lx_dev);
+    lx.xpart = c->at<float>(L.lx_part);
     lx.ctr = c->at<int>(L.counters) + kLayerCtr0; lx.err = c->at<int>(L.fwd_err); lx.err_host = c->err_host;
     for (int l = 0; l < m.n_layers; ++l) {
       const LayerW& w = c->layers[l];
       const bf16_t* wp = c->at<bf16_t>(L.wpack) + (int64_t)l * L.wp_layer;
       lx.layer = l;
       lx.wqkv = wp; lx.wo = wp + L.wp_o; lx.wgu = wp + L.wp_gu; lx.wdown = wp + L.wp_down;
-      lx.q_norm = w.q_norm; lx.k_norm = w.k_norm; lx.g_mid = w.mlp_norm;
-      lx.g_out = (l + 1 < m.n_layers) ? c->layers[l + 1].attn_norm : c->final_norm;
-      lx.n_part = l == 0 ? d / 16 : kXcdWgs;
+      lx.q_norm = w.q_norm; lx.k_norm = w.k_norm; lx.g_attn = w.attn_norm; lx.g_mlp = w.mlp_norm;
       SBD_LAUNCH(c, SBD_KERNEL_LAYER_ATTN, launch_layer_attn(lx, ex));
       SBD_LAUNCH(c, SBD_KERNEL_LAYER_MLP, launch_layer_mlp(lx, ex));
     }
-    n_part_cur = kXcdWgs;
+    // the LM head's inputs (and the fp32 residual) from the fixed-point residual
+    FinalizeArgs fa{M, d, lx.x64, c->final_norm, x, xn, xn_lo, sumsq};
+    SBD_LAUNCH(c, SBD_KERNEL_LAYER_FINAL, launch_layer_finalize(fa, ex));
+    n_part_cur = d / 16;
   }
   for (int l = 0; l < m.n_layers && !layers_fit; ++l) {
     const LayerW& w = c->layers[l];

@@ -59,7 +59,7 @@ struct Layout {
   int64_t gemv_part_floats;  // split-K partial tiles of the decode GEMM
   size_t xn2, sumsq2;        // fused decode forward: second copy of xn (hi, lo) and its partials
   size_t fwd_gains, fwd_ctl, fwd_err;
-  size_t lx_part, lx_dev;     // per-XCD layer kernels: XCD-local and cross-XCD partials
+  size_t lx_part, x64;        // per-XCD layer kernels: XCD-local partials, fixed-point residual
   int64_t fwd_ctl_ints;
   size_t total;
 };
@@ -184,6 +184,7 @@ struct EmbedArgs {
   bf16_t* xn;
   bf16_t* xn_lo;
   float* sumsq;  // [M][d/16]
+  int64_t* x64;  // the same rows as fixed point (x * 2^32) for the per-XCD layer kernels, or null
 };
 hipError_t launch_embed(const EmbedArgs& a, const Exec& ex);
 
@@ -315,14 +316,18 @@ hipError_t launch_fused_forward(const FwdArgs& f, int nwg, const Exec& ex);
 //   layer_mlp_kernel:  gate/up (+ SwiGLU) and down projection (+ residual, next norm's inputs)
 constexpr int kXcds = 8;        // XCDs of the chip; workgroup i runs on XCD i % 8
 constexpr int kXcdWgs = 32;     // persistent workgroups (CUs) per XCD
-constexpr int kLxQkvFloats = kXcdWgs * 2048;             // per XCD: parked QKV partial tiles
+constexpr int kLxQkvSlice = 2048 + 16;                    // parked QKV slice: 8 tiles + 16 row sums of x^2
+constexpr int kLxQkvFloats = kXcdWgs * kLxQkvSlice;       // per XCD: parked QKV slices
 constexpr int kLxAttnTasks = kXcdWgs;                     // attention tasks per XCD at most
 constexpr int kLxRows = 64;                               // query rows per KV head at most
 constexpr int64_t kLxXcdFloats = kLxQkvFloats + (int64_t)kLxAttnTasks * kLxRows * (128 + 2);
 constexpr int64_t kLxPartFloats = (int64_t)kXcds * kLxXcdFloats;  // XCD-local partials
-constexpr int64_t kLxDevFloats = (int64_t)kXcdWgs * kXcds * 2048; // cross-XCD partials (O, down)
-constexpr int kLxCtrLines = kXcds * 64 + 2 * kXcdWgs;     // counter lines (kCtrStride words each)
+constexpr int kLxCtrLines = kXcds * 64 + 2;               // counter lines (kCtrStride words each)
 
+// The residual stream of these kernels is int64 fixed point, x * 2^32 (x64): the O and down
+// projections add their partial products into it with integer atomics (exact, in any order,
+// so results do not depend on which XCD finishes first), and each consumer forms its
+// normalised operand from it as it streams.
 struct LayerXArgs {
   int M, B, k, layer;
   int d, n_q, n_kv, ffn, qk_norm;
@@ -330,16 +335,9 @@ struct LayerXArgs {
   int n_tasks;                       // attention key splits per sequence
   const bf16_t *wqkv, *wo, *wgu, *wdown;   // packed weights of the layer
   const bf16_t *q_norm, *k_norm;           // Qwen-3 per-head gains (qk_norm)
-  const bf16_t* g_mid;               // MLP norm gain (applied after the O projection)
-  const bf16_t* g_out;               // next attention norm's gain, or the final norm's
-  float* x;                          // residual stream [M][d]
-  const bf16_t *xn, *xn_lo;          // attention input x * g (hi, lo) [M][d]
-  const float* ssq;                  // its partial sums of squares [M][n_part]
-  int n_part;
-  bf16_t *xn_mid, *xn_mid_lo;        // MLP input x * g_mid (hi, lo), written by the O projection
-  float* ssq_mid;                    // its partial sums [M][32]
-  bf16_t *xn_out, *xn_out_lo;        // next layer's input, written by the down projection
-  float* ssq_out;                    // [M][32]
+  const bf16_t* g_attn;              // attention norm gain of the layer
+  const bf16_t* g_mlp;               // MLP norm gain of the layer
+  int64_t* x64;                      // residual stream [M][d], fixed point
   bf16_t *q, *q_lo, *attn, *attn_lo, *act, *act_lo;
   bf16_t *kcache, *vcache;
   int64_t cap;
@@ -348,15 +346,25 @@ struct LayerXArgs {
   const RowParam* rows;
   const SeqParam* seqs;
   float* xpart;                      // kLxPartFloats
-  float* dpart;                      // kLxDevFloats
   int* ctr;                          // kLxCtrLines * kCtrStride words, zero at creation
   int* err;                          // sticky error word and the task code of a failed wait
   int* err_host;                     // pinned host copy of the same two words
+};
+// After the last layer: x (fp32), x * g (hi, lo) and per-16-column sums of squares of the
+// fixed-point residual, the inputs of the LM head.
+struct FinalizeArgs {
+  int M, d;
+  const int64_t* x64;
+  const bf16_t* g;
+  float* x;
+  bf16_t *xn, *xn_lo;
+  float* sumsq;  // [M][d/16]
 };
 // True when the per-XCD layer kernels implement this decode-sized forward on this device.
 bool layer_xcd_fits(const sbd_model_config& c, int n_cu, int B, int k);
 hipError_t launch_layer_attn(const LayerXArgs& a, const Exec& ex);
 hipError_t launch_layer_mlp(const LayerXArgs& a, const Exec& ex);
+hipError_t launch_layer_finalize(const FinalizeArgs& a, const Exec& ex);
 
 // ---------------------------------------------------------------------------- EB sampler
 struct EbArgs {
