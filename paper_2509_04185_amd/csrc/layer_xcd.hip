@@ -49,6 +49,7 @@ namespace {
 constexpr int kLxSmem = 98304;       // LDS per workgroup: more than half a CU's, so one per CU
 constexpr int kLxSpin = 1 << 21;     // polls before a wait gives up
 constexpr int kDH = 128;
+constexpr int kLxMaxKs = 8;          // K slices of a QKV group at most (32 / (G + 2), G >= 2)
 // counter lines of XCD x: [x * 64, x * 64 + 64); device-wide lines after all XCDs'
 constexpr int kCtrQkv = 0;           // + group: last-arrival counters of the QKV slices
 constexpr int kCtrQkvDone = 40;      // QKV groups finished (epilogue stored)
@@ -262,25 +263,28 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
 #pragma unroll
       for (int k2 = 0; k2 < 2; ++k2) {
         const int ct = wave + 4 * k2;
+        i32x4 v[kLxMaxKs];  // every slice requested at once, added in slice order
+#pragma unroll
+        for (int z = 0; z < kLxMaxKs; ++z)
+          v[z] = z < KS ? ld16_l2(rq, (uint32_t)(((int64_t)z * kLxQkvSlice + (ct * 64 + lane) * 4) * 4))
+                        : i32x4{0, 0, 0, 0};
         f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
-        for (int z0_ = 0; z0_ < KS; z0_ += 4) {
-          i32x4 v[4];
 #pragma unroll
-          for (int u = 0; u < 4; ++u)
-            v[u] = z0_ + u < KS ? ld16_l2(rq, (uint32_t)(((int64_t)(z0_ + u) * kLxQkvSlice + (ct * 64 + lane) * 4) * 4))
-                                : i32x4{0, 0, 0, 0};
-#pragma unroll
-          for (int u = 0; u < 4; ++u) sum += __builtin_bit_cast(f32x4, v[u]);
-        }
+        for (int z = 0; z < kLxMaxKs; ++z) sum += __builtin_bit_cast(f32x4, v[z]);
         fin[ct * 64 + lane] = sum;
       }
       float* rinv_s = reinterpret_cast<float*>(smem + 65536 + 2048);  // [16]
       if (threadIdx.x < 16) {  // the KS slices' sums of x^2 of row threadIdx.x, in slice order
-        float t = 0.f;
-        for (int z = 0; z < KS; ++z)
-          t += __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                                             rq, (uint32_t)(((int64_t)z * kLxQkvSlice + 2048 + threadIdx.x) * 4), 0, kPolicyL2));
-        rinv_s[threadIdx.x] = 1.0f / sqrtf(t / (float)a.d + a.eps);
+        float t[kLxMaxKs];
+#pragma unroll
+        for (int z = 0; z < kLxMaxKs; ++z)
+          t[z] = z < KS ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                              rq, (uint32_t)(((int64_t)z * kLxQkvSlice + 2048 + threadIdx.x) * 4), 0, kPolicyL2))
+                        : 0.f;
+        float tt = 0.f;
+#pragma unroll
+        for (int z = 0; z < kLxMaxKs; ++z) tt += t[z];
+        rinv_s[threadIdx.x] = 1.0f / sqrtf(tt / (float)a.d + a.eps);
       }
       __syncthreads();
 #pragma unroll
@@ -510,7 +514,7 @@ bool layer_xcd_fits(const sbd_model_config& c, int n_cu, int B, int k) {
   if (c.n_kv_heads != kXcds || c.head_dim != kDH || c.d_model != kXcdWgs * 128) return false;
   if (c.n_q_heads % c.n_kv_heads) return false;
   const int G = c.n_q_heads / c.n_kv_heads;
-  if (G + 2 > kXcdWgs || (c.d_model / 32) / (kXcdWgs / (G + 2)) < 4) return false;
+  if (G < 2 || G + 2 > kXcdWgs || (c.d_model / 32) / (kXcdWgs / (G + 2)) < 4) return false;
   if (c.ffn_dim % (kXcds * kXcdWgs * 8) != 0) return false;
   const int cg = c.ffn_dim / (kXcds * kXcdWgs * 8);
   if (cg < 6 || cg > 8) return false;

@@ -101,10 +101,14 @@ def test_fullsize_block_forward(name):
         lib.set_decode_path(path)
         logits = lib.block_forward(list(range(wl.batch)), toks, is_mask=is_mask)
         n_acc, _, _, _ = lib.eb_select(logits, is_mask, wl.gammas[0], s.mask_id)
+        # every path adds its partial sums in a fixed order (or exactly, in integers): the
+        # same forward again gives the same bits
+        again = lib.block_forward(list(range(wl.batch)), toks, is_mask=is_mask)
         torch.cuda.synchronize()
         assert (n_acc >= 1).all()
+        assert torch.equal(logits, again), f"decode path {path} is not reproducible"
         got[path] = logits[sample].cpu().numpy()
-        del logits
+        del logits, again
     host = synth.weights_to_host(w)
     model = O.Model(s, host, dtype=np.float32, cache_decoded=False, kv_bf16=True)
     caches = []
