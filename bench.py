@@ -54,10 +54,9 @@ def gate_up_bytes(shape, M):
 
 def layer_mlp_bytes(shape, M):
     """Algorithmic bytes of one layer_mlp launch (gate/up + SwiGLU + down + residual): the three
-    MLP weight matrices, the bf16 input rows, the fp32 residual rows read and written, the
-    bf16 rows of the next norm's input written."""
+    MLP weight matrices, plus the residual rows (int64 fixed point) read once and updated once."""
     d, F = shape.d_model, shape.ffn_dim
-    return 2 * 3 * F * d + 2 * M * d + 2 * 4 * M * d + 2 * M * d
+    return 2 * 3 * F * d + 8 * M * d + 8 * M * d
 
 
 KERNEL_SOURCES = {
