@@ -222,6 +222,15 @@ typedef enum {
 } sbd_decode_path;
 sbd_status sbd_set_decode_path(sbd_ctx* ctx, int32_t path);
 /*
+ * Testing aid: the number of polls after which a dependency wait inside a decode launch of
+ * the per-XCD layer kernels gives up (a negative value restores the default of about two
+ * million, which no correct launch comes near).  A wait that gives up raises the sticky
+ * error that every later call on the context reports as SBD_ERR_HIP; the launch still runs
+ * to its end (on wrong data), it never hangs.  With a small limit a test can take that
+ * path on purpose.  INVALID_ARG for a null context.
+ */
+sbd_status sbd_set_wait_limit(sbd_ctx* ctx, int32_t polls);
+/*
  * *fits = 1 when `path` can run a decode-sized forward of `batch` sequences of `k` rows on
  * this context's model and device, else 0 (SBD_DECODE_AUTO and SBD_DECODE_KERNELS always
  * can).  INVALID_ARG for a null pointer or an unknown path.

@@ -49,6 +49,7 @@ SIGNATURES = {
     "sbd_kv_export": [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p],
     "sbd_set_decode_path": [c_void_p, c_int32],
     "sbd_decode_path_fits": [c_void_p, c_int32, c_int32, c_int32, POINTER(c_int32)],
+    "sbd_set_wait_limit": [c_void_p, c_int32],
     "sbd_profile_enable": [c_void_p, c_int32],
     "sbd_profile_read": [c_void_p, c_int32, POINTER(c_int32), POINTER(c_double)],
     "sbd_status_string": [c_int32],
@@ -257,6 +258,10 @@ class Sbd:
         """Kernels of decode-sized forwards: "auto", "fused", "kernels" or "layers" (sbd_set_decode_path)."""
         code = DECODE_PATHS[path]
         _check(self.lib, self.lib.sbd_set_decode_path(self.ctx, code), "sbd_set_decode_path", self.ctx)
+
+    def set_wait_limit(self, polls: int):
+        """Polls before a wait inside a layer-kernel launch gives up; negative: the default."""
+        _check(self.lib, self.lib.sbd_set_wait_limit(self.ctx, polls), "sbd_set_wait_limit", self.ctx)
 
     def decode_path_fits(self, path: str, batch: int, k: int) -> bool:
         """Whether `path` can run a forward of `batch` x `k` rows here (sbd_decode_path_fits)."""

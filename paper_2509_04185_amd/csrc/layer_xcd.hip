@@ -47,7 +47,6 @@ namespace sbd {
 namespace {
 
 constexpr int kLxSmem = 98304;       // LDS per workgroup: more than half a CU's, so one per CU
-constexpr int kLxSpin = 1 << 21;     // polls before a wait gives up
 constexpr int kDH = 128;
 constexpr int kLxMaxKs = 8;          // K slices of a QKV group at most (32 / (G + 2), G >= 2)
 // counter lines of XCD x: [x * 64, x * 64 + 64); device-wide lines after all XCDs'
@@ -110,7 +109,7 @@ __device__ __forceinline__ void xcd_wait(const LayerXArgs& a, int* ctr, int targ
     int it = 0;
     while (xcd_peek<SCOPE>(ctr) < target) {
       __builtin_amdgcn_s_sleep(1);
-      if (++it > kLxSpin) {
+      if (++it > a.spin_limit) {
         atomicOr(a.err, 1);
         atomicExch(a.err + 1, what);
         if (a.err_host != nullptr) {

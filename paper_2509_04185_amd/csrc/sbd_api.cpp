@@ -135,6 +135,7 @@ struct sbd_ctx {
   double prof_ms[SBD_KERNEL_COUNT] = {};
   // decode path for M <= 16 (sbd_set_decode_path)
   int decode_path = SBD_DECODE_AUTO;
+  int wait_limit = kLxSpinDefault;  // sbd_set_wait_limit
   int n_cu = 0;                 // workgroups of the fused forward: one per CU, at most kFwdMaxWorkgroups
   int n_cu_dev = 0;             // CUs of the device
   int32_t* err_host = nullptr;  // pinned copy of the fused forward's sticky error word
@@ -336,6 +337,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     lx.n_slots = m.max_batch; lx.rope = c->at<float>(L.rope); lx.rows = drows; lx.seqs = dseqs;
     lx.xpart = c->at<float>(L.lx_part);
     lx.ctr = c->at<int>(L.counters) + kLayerCtr0; lx.err = c->at<int>(L.fwd_err); lx.err_host = c->err_host;
+    lx.spin_limit = c->wait_limit;
     for (int l = 0; l < m.n_layers; ++l) {
       const LayerW& w = c->layers[l];
       const bf16_t* wp = c->at<bf16_t>(L.wpack) + (int64_t)l * L.wp_layer;
@@ -840,6 +842,12 @@ sbd_status sbd_set_decode_path(sbd_ctx* c, int32_t path) {
       path != SBD_DECODE_LAYERS)
     return fail(c, SBD_ERR_INVALID_ARG, "unknown decode path %d", path);
   c->decode_path = path;
+  return SBD_OK;
+}
+
+sbd_status sbd_set_wait_limit(sbd_ctx* c, int32_t polls) {
+  if (!c) return fail(nullptr, SBD_ERR_INVALID_ARG, "null context");
+  c->wait_limit = polls < 0 ? kLxSpinDefault : polls;
   return SBD_OK;
 }
 

@@ -349,7 +349,9 @@ struct LayerXArgs {
   int* ctr;                          // kLxCtrLines * kCtrStride words, zero at creation
   int* err;                          // sticky error word and the task code of a failed wait
   int* err_host;                     // pinned host copy of the same two words
+  int spin_limit;                    // polls before a wait gives up
 };
+constexpr int kLxSpinDefault = 1 << 21;
 // After the last layer: x (fp32), x * g (hi, lo) and per-16-column sums of squares of the
 // fixed-point residual, the inputs of the LM head.
 struct FinalizeArgs {

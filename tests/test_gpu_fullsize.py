@@ -172,3 +172,43 @@ def test_benched_configuration_with_real_prefill():
     for path, g in got_paths.items():
         print(f"    decode path {path}", flush=True)
         close(g, ref)
+
+
+def test_layer_kernel_wait_that_gives_up_is_reported():
+    """A dependency wait inside the per-XCD layer kernels that gives up - forced from the host
+    with a poll limit of 0, so the launch itself stays in bounds and ends - is reported by the
+    next call on the context as SBD_ERR_HIP; a fresh context then gives the same logits as
+    before.  One layer of the Llama-3.1-8B shape, 128 cached positions, k = 16."""
+    import dataclasses
+    from paper_2509_04185_amd import Sbd
+    from paper_2509_04185_amd.binding import SbdError
+    s = dataclasses.replace(synth.LLAMA8B, n_layers=1)
+    torch.cuda.empty_cache()
+    w = synth.make_weights(s, 1008, device="cuda")
+
+    def fresh_ctx():
+        lib = Sbd(s, w, max_batch=1, max_seq_len=256, max_block=16)
+        kk, vv = synth.make_kv(s, 1008, 0, 128, device="cuda")
+        lib.kv_import(0, 0, kk, vv)
+        return lib
+
+    lib = fresh_ctx()
+    if not lib.decode_path_fits("layers", 1, 16):
+        pytest.skip("the per-XCD layer kernels need a device of 256 CUs in 8 XCDs")
+    print("[gpu] layer kernels: forced wait failure", flush=True)
+    lib.set_decode_path("layers")
+    toks, is_mask = synth.block_rows(1008, s, 1, 16, n_causal=1)
+    ref = lib.block_forward([0], toks, is_mask=is_mask)
+    torch.cuda.synchronize()
+    lib.set_wait_limit(0)
+    lib.block_forward([0], toks, is_mask=is_mask)  # its waits give up; the launch still ends
+    torch.cuda.synchronize()
+    with pytest.raises(SbdError) as err:
+        lib.block_forward([0], toks, is_mask=is_mask)
+    assert "SBD_ERR_HIP" in str(err.value) and "gave up waiting" in str(err.value), str(err.value)
+    del lib
+    lib2 = fresh_ctx()
+    lib2.set_decode_path("layers")
+    got = lib2.block_forward([0], toks, is_mask=is_mask)
+    torch.cuda.synchronize()
+    assert torch.equal(got, ref)
