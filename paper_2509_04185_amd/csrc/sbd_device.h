@@ -73,38 +73,6 @@ __device__ __forceinline__ float half_wave_sum(float v) {
   return v;
 }
 
-// Cross-workgroup reduction handshake.  Every workgroup writes its partial results with
-// store_coherent(), then calls last_arrival(); it returns true in exactly one workgroup —
-// the last of `expected` to arrive at `counter` — which then reads the partials with
-// load_coherent().  The counter is reset to 0 for the next launch.  No workgroup ever
-// waits on another.
-//
-// Each XCD has its own L2, so the partials must be visible across L2s.  Variant selected
-// by SBD_SPLITK_SYNC:
-//   0  device-scope fences around the counter (L2 write-back and invalidate by every wave)
-//   1  one release fence per workgroup before the counter, one acquire fence in the last
-//   2  partials stored/loaded with device-coherent (sc1) accesses; the counter increment
-//      only waits for those stores to complete (no cache-wide write-back or invalidate)
-#ifndef SBD_SPLITK_SYNC
-#define SBD_SPLITK_SYNC 2
-#endif
-
-__device__ __forceinline__ void store_coherent(float* p, float v) {
-#if SBD_SPLITK_SYNC == 2
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-#else
-  *p = v;
-#endif
-}
-
-__device__ __forceinline__ float load_coherent(const float* p) {
-#if SBD_SPLITK_SYNC == 2
-  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-#else
-  return *p;
-#endif
-}
-
 // Device-scope (sc1) accesses for data that one workgroup writes and a workgroup on another
 // XCD reads later in the same launch: the stores write through to the coherence point and
 // the loads bypass possibly stale L2 lines.  Buffer forms take a wave-uniform base (a
@@ -138,47 +106,17 @@ __device__ __forceinline__ int ld_i32_dev(const int* p) {
   return __hip_atomic_load(const_cast<int*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__device__ __forceinline__ bool last_arrival(int* counter, int expected) {
-  __shared__ int s_last;
-#if SBD_SPLITK_SYNC == 0
-  __threadfence();
-  __syncthreads();
-#elif SBD_SPLITK_SYNC == 1
-  __syncthreads();
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-#else
-  __builtin_amdgcn_s_waitcnt(0);  // this wave's coherent stores have completed
-  __syncthreads();
-#endif
-  if (threadIdx.x == 0) {
-#if SBD_SPLITK_SYNC == 1
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-#endif
-    const int prev = atomicAdd(counter, 1);
-    s_last = (prev == expected - 1) ? 1 : 0;
-    if (s_last) {
-      atomicExch(counter, 0);
-#if SBD_SPLITK_SYNC == 1
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-#endif
-    }
-  }
-  __syncthreads();
-  const bool last = s_last != 0;
-#if SBD_SPLITK_SYNC == 0
-  if (last) __threadfence();
-#endif
-  return last;
-}
-
 // XCD-local hand-off.  A launch places workgroup i on XCD i % 8 (the round-robin dispatch
 // of the 8 XCDs), and the 32 CUs of an XCD share one L2.  Workgroups that exchange data only
 // with workgroups of their own XCD therefore need no device-scope traffic: partials are
-// written with plain stores (they reach the shared L2 before the writer's vmcnt drops),
-// read with L1-bypassing loads, and the arrival counter is an atomic performed in that L2.
-// Every counter used this way sits on a 128-byte line of its own.
-constexpr int kPolicyL2 = 1;    // cache-policy bits of an L1-bypassing access (sc0)
+// written with plain stores (the L1 is write-through: they are in the shared L2 once the
+// writer's vmcnt drops), and the arrival counter is a workgroup-scope atomic, performed in
+// that L2 (measured: such atomics are not seen across XCDs, and are not meant to be).  The
+// reader's loads are workgroup-scope (sc0): they may be served by its own L1, so a line is
+// read this way only if the reading CU has not read it earlier in the launch (the L1 is
+// invalidated at every launch); a value that changes while being watched is polled with an
+// atomic instead.  Every counter used this way sits on a 128-byte line of its own.
+constexpr int kPolicyL2 = 1;    // cache-policy bits of a workgroup-scope access (sc0)
 __device__ __forceinline__ i32x4 ld16_l2(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, kPolicyL2);
 }
@@ -186,9 +124,11 @@ __device__ __forceinline__ i32x2 ld8_l2(__amdgpu_buffer_rsrc_t r, uint32_t byte_
   return __builtin_amdgcn_raw_buffer_load_b64(r, byte_off, 0, kPolicyL2);
 }
 
-// last_arrival() for workgroups that all run on one XCD: true in exactly one of the
-// `expected` workgroups arriving at `counter` (the last), which then reads the others'
-// partials with ld16_l2 / ld8_l2.  The counter is reset to 0 for the next launch.
+// Cross-workgroup reduction handshake for workgroups that all run on one XCD: every
+// workgroup stores its partial results, then calls last_arrival_xcd(); it returns true in
+// exactly one of the `expected` workgroups arriving at `counter` (the last), which then
+// reads the others' partials with ld16_l2 / ld8_l2.  The counter is reset to 0 for the next
+// launch.  No workgroup ever waits for another.
 __device__ __forceinline__ bool last_arrival_xcd(int* counter, int expected) {
   __shared__ int s_last;
   __builtin_amdgcn_s_waitcnt(0);  // this wave's stores have reached the L2

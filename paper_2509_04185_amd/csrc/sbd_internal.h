@@ -13,8 +13,6 @@ namespace sbd {
 typedef uint16_t bf16_t;            // raw IEEE bfloat16 bits
 
 constexpr int kWave = 64;           // CDNA wavefront width
-constexpr int kColTile = 32;        // GEMM output columns per workgroup (two 16-wide MFMA tiles)
-constexpr int kKeyBlock = 32;       // keys per attention step / per V^T storage block
 constexpr int kMaxSplits = 64;      // split-KV partitions per (sequence, KV head, row block)
 constexpr int kEbChunk = 4096;      // vocabulary entries per EB partial workgroup
 constexpr int kMaxBlock = 64;       // largest block size k
