@@ -1,238 +1,411 @@
-// Skinny weight-streaming GEMM for the block forward: y[m][n] = sum_k A[m][k] W[n][k].
-//
-// The block forward multiplies M = batch * k activation rows (16 at batch 1, k = 16) by
-// every weight matrix of the decoder, so it is bound by streaming the weights from HBM.
+// Weight-streaming GEMM for M > 16 rows: y[m][n] = sum_k A[m][k] W[n][k].
 //
 // Weights are repacked once (pack_kernel) into MFMA fragment order.  A matrix with N rows
 // and K columns is cut into 16-row tiles; the 16-byte piece of lane l in step s of tile t
 // holds W[16t + l%16][32s + 8(l/16) .. +8], so one 16-byte load per lane reads a 1 KB
-// fragment that lands directly in the B operand of v_mfma_f32_16x16x32_bf16.  Tiles are
-// grouped by 8 (128 rows) and a group's 8 fragments of one step are stored together:
-// [N/128 groups][K/32 steps][8 tiles][64 lanes][8] (packed_frag() in sbd_device.h), so a
-// decode-sized GEMM reading several tiles of a group per step reads contiguous memory.
-// The gate and up projections share one packed matrix whose tile t holds gate rows
-// 8t..8t+7 followed by up rows 8t..8t+7, so SwiGLU pairs stay inside one tile.
+// fragment in the B-operand order of v_mfma_f32_16x16x32_bf16.  Tiles are grouped by 8
+// (128 rows) and a group's 8 fragments of one step are stored together:
+// [N/128 groups][K/32 steps][8 tiles][64 lanes][8] (packed_frag() in sbd_device.h).  The
+// gate and up projections share one packed matrix whose tile t holds gate rows 8t..8t+7
+// followed by up rows 8t..8t+7, so SwiGLU pairs stay inside one tile.
 //
-// This kernel serves M > 16 (prefill chunks, large batches); decode-sized products go
-// through gemv.hip.  Each workgroup owns C consecutive tiles (16*C output columns) and a
-// row block; its NW waves split the K/32 steps and stream disjoint contiguous ranges with
-// non-temporal loads, double-buffered in registers.  The activations come as hi/lo bf16
-// pairs (two MFMAs per step, see GemmArgs).  Partial sums meet in LDS and are added in a
-// fixed wave order (deterministic); the epilogue applies what follows the product in the
-// block:
+// This kernel serves the block forwards of several sequences (M = batch * k up to a few
+// hundred rows) and the prefill chunks; decode-sized products (M <= 16) go through
+// gemv.hip.  At these M every projection still reads far more weight bytes than it does
+// MFMA work per byte (M flop per weight byte, against a ridge of ~300), so the design
+// streams every weight byte from HBM once:
+//   - A workgroup owns a column block of NT tiles (128 or 256 columns) and a row block of
+//     MT tiles (up to 128 rows; larger M is cut into row blocks that run on the same XCD
+//     and meet the same weights in its L2), and a range of K steps.
+//   - Weights and activations reach LDS by direct loads (global_load_lds, no registers)
+//     in stages of one K step, a ring of NS stages, so NS - 1 steps are in flight while
+//     the waves multiply the current one.  The four waves split the block into column
+//     quarters (or halves x row halves); a wave reads its weight fragments and the A
+//     fragments (hi and lo) of its rows from LDS and runs two MFMAs per pair.
+//   - When there are too few column blocks to fill the chip, K is split over workgroups
+//     of one XCD: each parks its partial tiles in that XCD's L2, and the last to arrive
+//     adds the slices in slice order (deterministic) and runs the epilogue.
+// Epilogues (acc in the MFMA D layout: lane l holds column l % 16 of a tile, rows
+// 4*(l/16) + i):
 //   EPI_SCALED_STORE  out = rinv[m] * y           (QKV projection, LM head)
-//   EPI_RESID         x += y; xn = x * g_next as hi/lo; per-row sums of x^2 over each 16
-//                     columns (O and down projections: residual add, the next RMSNorm's
-//                     inputs)
+//   EPI_RESID         x += y; xn = x * g_next as hi/lo; the sum of x^2 over the block's
+//                     columns per row (O and down projections: residual add, the next
+//                     RMSNorm's inputs)
 //   EPI_SWIGLU        act = silu(rinv*gate) * rinv*up as hi/lo (gate/up projection)
 // RMSNorm is split across two kernels: the producer writes x * g (gain applied) plus
-// per-16-column partial sums of squares; the consumer adds the partials of a row and
-// scales its fp32 result by 1/sqrt(mean(x^2) + eps), which equals normalising the input
-// first because the scale is constant along a row.
-//
-// MFMA v_mfma_f32_16x16x32_bf16: lane l holds row (l % 16) of A and column (l % 16) of
-// B^T for the 8 consecutive k of group l / 16; the result holds rows 4*(l/16)+i of
-// column l % 16.
+// partial sums of squares; the consumer adds the partials of a row and scales its fp32
+// result by 1/sqrt(mean(x^2) + eps), which equals normalising the input first because the
+// scale is constant along a row.
+
+#include <algorithm>
+#include <utility>
 
 #include "sbd_device.h"
 
 namespace sbd {
 
-template <int MT, int C, int NW, int U, int EPI>
-__global__ __launch_bounds__(NW * 64) void gemm_kernel(GemmArgs a) {
-  constexpr int NC = 16 * C;  // output columns of the workgroup
-  __shared__ float red[NW][MT * 16][NC + 1];
+template <int MT, int NT>
+struct MidCfg {
+  static constexpr int WC = NT == 16 ? 4 : 2;  // waves across the column block
+  static constexpr int WM = 4 / WC;            // waves across the row block
+  static constexpr int CW = NT / WC;           // tiles per wave
+  static constexpr int MTW = MT / WM;          // row tiles per wave
+  static constexpr int STAGE = (NT + 2 * MT) * 1024;  // one K step: NT weight + 2 MT A fragments
+  static constexpr int NS = (144 * 1024) / STAGE > 8 ? 8 : (144 * 1024) / STAGE;  // ring stages
+  static constexpr int FPW = (NT + 2 * MT) / 4;       // fragments each wave loads per stage
+  static_assert(MTW >= 1 && (NT + 2 * MT) % 4 == 0, "unsupported tile shape");
+  static_assert((NS - 2) * FPW <= 63, "vmcnt range");
+};
+
+// f(std::integral_constant<int, 0>{}), ..., f(std::integral_constant<int, N - 1>{})
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// ds_read_b128 at LDS byte address addr + OFF, invisible to the compiler's wait insertion:
+// the caller waits (lgkmcnt) before using the result.
+template <int OFF>
+__device__ __forceinline__ i32x4 ds_read16(uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
+  i32x4 v;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF));
+  return v;
+}
+
+// s_waitcnt vmcnt(N), other counters left free
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  __builtin_amdgcn_s_waitcnt(((N & 15) | ((N >> 4) << 14)) | (7 << 4) | (15 << 8));
+}
+// Wait until at most n stages of FPW loads each are still in flight (n in [0, NMAX]).
+template <int FPW, int NMAX>
+__device__ __forceinline__ void vm_wait_stages(int n) {
+  if constexpr (NMAX > 0) {
+    if (n >= NMAX) {
+      vm_wait<NMAX * FPW>();
+      return;
+    }
+    vm_wait_stages<FPW, NMAX - 1>(n);
+  } else {
+    vm_wait<0>();
+  }
+}
+// Barrier between stages: LDS reads of this wave complete, then s_barrier.  The empty asm
+// statements keep the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void stage_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// STREAM: every weight byte is read by one workgroup (one row block): non-temporal loads.
+template <int MT, int NT, int EPI, bool STREAM>
+__global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
+  using Cfg = MidCfg<MT, NT>;
+  constexpr int WC = Cfg::WC, CW = Cfg::CW, MTW = Cfg::MTW, NS = Cfg::NS, FPW = Cfg::FPW;
+  constexpr int STAGE = Cfg::STAGE;
+  constexpr int WB = NT * 1024;  // weight bytes of a stage; A fragments follow
+  constexpr int NWU = NT / 4;    // of a wave's FPW loads, the first NWU are weights
+  __shared__ __attribute__((aligned(16))) char smem[NS * STAGE];
   __shared__ float rinv_s[MT * 16];
+  __shared__ float ssq_s[WC][MT * 16];
 
-  const int lane = threadIdx.x & 63;
-  const int w = threadIdx.x >> 6;
-  const int r = lane & 15;
-  const int g = lane >> 4;
-  // Row blocks vary fastest so the blocks re-reading one weight tile run together.
-  const int tile = blockIdx.y;
-  const int row0 = blockIdx.x * (MT * 16);
-  const int K = a.K;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int r = lane & 15, g = lane >> 4;
+  const int wc = w % WC, wm = w / WC;
 
-  // This wave's share of the K/32 steps.
-  const int S_all = K / 32;
-  const int base_steps = S_all / NW, rem = S_all % NW;
-  const int s0 = w * base_steps + (w < rem ? w : rem);
-  const int ns = base_steps + (w < rem ? 1 : 0);
-  const int kbase = s0 * 32 + g * 8;
+  // Workgroup i runs on XCD i % 8; the m_blocks x splits units of column block cb all sit
+  // on XCD cb % 8.  The count is padded to a multiple of 8; padding workgroups leave.
+  const int KS = a.splits, MB = a.m_blocks, P = KS * MB;
+  const int jx = (int)(blockIdx.x >> 3);
+  const int cb = (jx / P) * 8 + (int)(blockIdx.x & 7);
+  const int n_cb = a.n_tiles / NT;
+  if (cb >= n_cb) return;
+  const int mb = (jx % P) / KS, kc = (jx % P) % KS;
+  const int uid = cb * MB + mb;
+  const int row0 = mb * MT * 16;
+  const int S_all = a.K / 32;
+  const int s_b = (int)((int64_t)S_all * kc / KS), s_e = (int)((int64_t)S_all * (kc + 1) / KS);
+  const int nst = s_e - s_b;
+  const int t0 = cb * NT;
 
-  const bf16_t* wbase[C];
+  // Sources of this wave's loads: load u of a stage fills fragment f = w + 4u of it;
+  // f < NT is weight tile t0 + f, else A fragment f - NT = 2 * (row tile) + (0: hi, 1: lo).
+  const char* src[FPW];
+  int64_t stride[FPW];
 #pragma unroll
-  for (int ct = 0; ct < C; ++ct)
-    wbase[ct] = a.Wp + packed_frag(tile * C + ct, s0, S_all) + lane * 8;
-  const bf16_t* arow[MT];
-  const bf16_t* arow_lo[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    int m = row0 + mt * 16 + r;
-    if (m >= a.M) m = a.M - 1;
-    arow[mt] = a.A + (int64_t)m * a.lda + kbase;
-    arow_lo[mt] = a.A_lo + (int64_t)m * a.lda + kbase;
-  }
-
-  f32x4 acc[MT][C];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int ct = 0; ct < C; ++ct) acc[mt][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  i32x4 wb0[U][C], ab0[U][MT], al0[U][MT], wb1[U][C], ab1[U][MT], al1[U][MT];
-
-#define SBD_LOAD(WB, AB, AL, STEP)                                                 \
-  _Pragma("unroll") for (int u = 0; u < U; ++u) {                                 \
-    const int st_ = (STEP) + u;                                                   \
-    _Pragma("unroll") for (int ct = 0; ct < C; ++ct)                              \
-      WB[u][ct] = ld16_stream(wbase[ct] + (int64_t)st_ * kPackStep);              \
-    _Pragma("unroll") for (int mt = 0; mt < MT; ++mt) {                           \
-      AB[u][mt] = ld16(arow[mt] + st_ * 32);                                      \
-      AL[u][mt] = ld16(arow_lo[mt] + st_ * 32);                                   \
-    }                                                                              \
-  }
-#define SBD_COMPUTE(WB, AB, AL)                                                    \
-  _Pragma("unroll") for (int u = 0; u < U; ++u) {                                 \
-    _Pragma("unroll") for (int mt = 0; mt < MT; ++mt)                             \
-      _Pragma("unroll") for (int ct = 0; ct < C; ++ct) {                          \
-        acc[mt][ct] = mfma16x16x32(AB[u][mt], WB[u][ct], acc[mt][ct]);            \
-        acc[mt][ct] = mfma16x16x32(AL[u][mt], WB[u][ct], acc[mt][ct]);            \
-      }                                                                            \
-  }
-
-  const int nchunks = ns / U;
-  if (nchunks > 0) { SBD_LOAD(wb0, ab0, al0, 0); }
-
-  // Per-row 1/rms from the producer's partial sums of squares (overlaps the first loads).
-  if (EPI != EPI_RESID) {
-    const int half = threadIdx.x >> 5, hl = threadIdx.x & 31;
-    for (int rr = half; rr < MT * 16; rr += NW * 2) {
-      const int m = row0 + rr;
-      float sq = 0.f;
-      if (a.sumsq_in != nullptr && m < a.M)
-        for (int p = hl; p < a.n_part; p += 32) sq += a.sumsq_in[(int64_t)m * a.n_part + p];
-      sq = half_wave_sum(sq);
-      if (hl == 0) rinv_s[rr] = (a.sumsq_in != nullptr) ? 1.0f / sqrtf(sq * a.inv_d + a.eps) : 1.0f;
+  for (int u = 0; u < FPW; ++u) {
+    const int f = w + 4 * u;
+    if (u < NWU) {
+      src[u] = (const char*)(a.Wp + packed_frag(t0 + f, s_b, S_all) + lane * 8);
+      stride[u] = kPackStep * 2;
+    } else {
+      const int ai = f - NT;
+      int row = row0 + (ai >> 1) * 16 + r;
+      if (row >= a.M) row = a.M - 1;  // rows past the end: valid data, results discarded
+      const bf16_t* base = (ai & 1) ? a.A_lo : a.A;
+      src[u] = (const char*)(base + (int64_t)row * a.lda + (int64_t)s_b * 32 + g * 8);
+      stride[u] = 64;
     }
   }
+  // stage st into ring slot B (= st % NS)
+  auto issue = [&](auto B, int st) {
+    char* dst = smem + decltype(B)::value * STAGE + w * 1024;
+    constexpr int kPolW = STREAM ? 2 : 0;  // nt: read once
+#pragma unroll
+    for (int u = 0; u < NWU; ++u)
+      __builtin_amdgcn_global_load_lds((const void*)(src[u] + st * stride[u]),
+                                       (__attribute__((address_space(3))) void*)(dst + u * 4096), 16, 0, kPolW);
+#pragma unroll
+    for (int u = NWU; u < FPW; ++u)
+      __builtin_amdgcn_global_load_lds((const void*)(src[u] + st * stride[u]),
+                                       (__attribute__((address_space(3))) void*)(dst + u * 4096), 16, 0, 0);
+  };
 
-  for (int c = 0; c < nchunks; c += 2) {
-    if (c + 1 < nchunks) { SBD_LOAD(wb1, ab1, al1, (c + 1) * U); }
-    SBD_COMPUTE(wb0, ab0, al0);
-    if (c + 1 < nchunks) {
-      if (c + 2 < nchunks) { SBD_LOAD(wb0, ab0, al0, (c + 2) * U); }
-      SBD_COMPUTE(wb1, ab1, al1);
-    }
-  }
-  for (int st = nchunks * U; st < ns; ++st) {
-    i32x4 wv[C];
+  f32x4 acc[MTW][CW];
 #pragma unroll
-    for (int ct = 0; ct < C; ++ct) wv[ct] = ld16_stream(wbase[ct] + (int64_t)st * kPackStep);
+  for (int mw = 0; mw < MTW; ++mw)
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const i32x4 av = ld16(arow[mt] + st * 32);
-      const i32x4 avl = ld16(arow_lo[mt] + st * 32);
+    for (int cw = 0; cw < CW; ++cw) acc[mw][cw] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // LDS reads of a stage as inline assembly: the compiler would otherwise guard every read
+  // of LDS with a wait for all direct loads in flight (it cannot tell the ring slots
+  // apart), draining the ring at each step.  Ordering is explicit instead: the stage
+  // barrier before the reads, one lgkmcnt(0) after them, and the results pinned behind it.
+  const uint32_t lds_w = (uint32_t)(uintptr_t)smem + (uint32_t)(wc * CW * 1024 + lane * 16);
+  const uint32_t lds_a = (uint32_t)(uintptr_t)smem + (uint32_t)(WB + wm * MTW * 2048 + lane * 16);
+  auto compute = [&](auto B) {
+    constexpr uint32_t SB = decltype(B)::value * STAGE;
+    const uint32_t aw = lds_w + SB, aa = lds_a + SB;
+    i32x4 wv[CW], av[MTW][2];
+    static_for<CW>([&](auto I) { wv[decltype(I)::value] = ds_read16<decltype(I)::value * 1024>(aw); });
+    static_for<MTW * 2>([&](auto I) {
+      constexpr int i = decltype(I)::value;
+      av[i / 2][i % 2] = ds_read16<i * 1024>(aa);
+    });
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
-      for (int ct = 0; ct < C; ++ct) {
-        acc[mt][ct] = mfma16x16x32(av, wv[ct], acc[mt][ct]);
-        acc[mt][ct] = mfma16x16x32(avl, wv[ct], acc[mt][ct]);
+    for (int cw = 0; cw < CW; ++cw) asm volatile("" : "+v"(wv[cw]));
+#pragma unroll
+    for (int mw = 0; mw < MTW; ++mw)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) asm volatile("" : "+v"(av[mw][h]));
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int mw = 0; mw < MTW; ++mw)
+#pragma unroll
+        for (int cw = 0; cw < CW; ++cw) acc[mw][cw] = mfma16x16x32(av[mw][h], wv[cw], acc[mw][cw]);
+  };
+
+  static_for<NS - 1>([&](auto B) {
+    if (decltype(B)::value < nst) issue(B, decltype(B)::value);
+  });
+  // the loop is unrolled by NS so that every ring slot is named statically
+  for (int c0 = 0; c0 < nst; c0 += NS) {
+    static_for<NS>([&](auto B) {
+      constexpr int b = decltype(B)::value;
+      const int c = c0 + b;
+      if (c < nst) {
+        vm_wait_stages<FPW, NS - 2>(min(NS - 2, nst - 1 - c));  // stage c has landed (this wave's part)
+        stage_barrier();                                         // ... and every wave's; stage c - 1 is free
+        if (c + NS - 1 < nst) issue(std::integral_constant<int, (b + NS - 1) % NS>{}, c + NS - 1);
+        compute(B);
       }
-    }
-  }
-#undef SBD_LOAD
-#undef SBD_COMPUTE
-
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int ct = 0; ct < C; ++ct)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) red[w][mt * 16 + 4 * g + i][16 * ct + r] = acc[mt][ct][i];
-  __syncthreads();
-
-  // Sum the waves' partial tiles into red[0] (fixed wave order).
-  constexpr int TOTAL = MT * 16 * NC;
-  constexpr int STRIDE = NW * 64;
-  for (int idx = threadIdx.x; idx < TOTAL; idx += STRIDE) {
-    const int rr = idx / NC, col = idx % NC;
-    float y = red[0][rr][col];
-#pragma unroll
-    for (int w2 = 1; w2 < NW; ++w2) y += red[w2][rr][col];
-    red[0][rr][col] = y;
+    });
   }
 
-  __syncthreads();
+  // ---- K split over workgroups: park the slice, the last to arrive adds all in order
+  if (KS > 1) {
+    const int n_units = n_cb * MB;
+    const int64_t slot = ((int64_t)uid * 4 + w) * (MTW * CW);  // in 1 KB (64 x f32x4) pieces
+#pragma unroll
+    for (int mw = 0; mw < MTW; ++mw)
+#pragma unroll
+      for (int cw = 0; cw < CW; ++cw)
+        *(f32x4*)(a.part + (((int64_t)kc * n_units * 4 * MTW * CW + slot + mw * CW + cw) * 64 + lane) * 4) =
+            acc[mw][cw];
+    if (!last_arrival_xcd(a.counters + (int64_t)uid * kCtrStride, KS)) return;
+    const __amdgpu_buffer_rsrc_t rp = buf_rsrc(a.part);
+#pragma unroll
+    for (int mw = 0; mw < MTW; ++mw)
+#pragma unroll
+      for (int cw = 0; cw < CW; ++cw) {
+        f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int z0 = 0; z0 < KS; z0 += 4) {  // four slices in flight, added in slice order
+          i32x4 v[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            v[u] = z0 + u < KS
+                       ? ld16_l2(rp, (uint32_t)((((int64_t)(z0 + u) * n_units * 4 * MTW * CW + slot + mw * CW + cw) *
+                                                     64 + lane) * 16))
+                       : i32x4{0, 0, 0, 0};
+#pragma unroll
+          for (int u = 0; u < 4; ++u) s += __builtin_bit_cast(f32x4, v[u]);
+        }
+        acc[mw][cw] = s;
+      }
+  }
 
-  // Epilogue: thread idx -> (row idx / NC, column idx % NC); each 16-lane group holds
-  // the 16 columns of one tile of one row.
-  for (int idx = threadIdx.x; idx < (TOTAL + STRIDE - 1) / STRIDE * STRIDE; idx += STRIDE) {
-    const bool in = idx < TOTAL;
-    const int rr = in ? idx / NC : 0, col = idx % NC;
+  // ---- 1/rms of the row block's rows from the producer's partial sums of squares
+  if constexpr (EPI != EPI_RESID) {
+    constexpr int TPR = 256 / (MT * 16);  // threads per row
+    const int rr = threadIdx.x / TPR, q = threadIdx.x % TPR;
     const int m = row0 + rr;
-    const bool ok = in && m < a.M;
-    const float y = in ? red[0][rr][col] : 0.f;
-    if (EPI == EPI_SCALED_STORE) {
-      if (ok) a.out_f32[(int64_t)m * a.ldo + tile * NC + col] = y * rinv_s[rr];
-    } else if (EPI == EPI_RESID) {
-      const int n = tile * NC + col;
-      float xv = 0.f;
-      if (ok) {
-        float* xp = a.x + (int64_t)m * a.ldx + n;
-        xv = *xp + y;
-        *xp = xv;
-        bf16_t hi, lo;
-        split_bf16(xv * bf2f(a.g_next[n]), hi, lo);
-        a.xn[(int64_t)m * a.ldx + n] = hi;
-        a.xn_lo[(int64_t)m * a.ldx + n] = lo;
+    float sq = 0.f;
+    if (a.sumsq_in != nullptr && m < a.M)
+      for (int p = q; p < a.n_part; p += TPR) sq += a.sumsq_in[(int64_t)m * a.n_part + p];
+#pragma unroll
+    for (int o = TPR / 2; o >= 1; o /= 2) sq += __shfl_xor(sq, o);
+    if (q == 0) rinv_s[rr] = (a.sumsq_in != nullptr) ? 1.0f / sqrtf(sq * a.inv_d + a.eps) : 1.0f;
+    __syncthreads();
+  }
+
+  // ---- epilogue
+#pragma unroll
+  for (int mw = 0; mw < MTW; ++mw) {
+    const int rl0 = (wm * MTW + mw) * 16 + 4 * g;  // local row of element 0
+    float ss[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int cw = 0; cw < CW; ++cw) {
+      const int tile = t0 + wc * CW + cw;
+      const int n = tile * 16 + r;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = row0 + rl0 + i;
+        const bool ok = m < a.M;
+        const float y = acc[mw][cw][i];
+        if constexpr (EPI == EPI_SCALED_STORE) {
+          if (ok) a.out_f32[(int64_t)m * a.ldo + n] = y * rinv_s[rl0 + i];
+        } else if constexpr (EPI == EPI_SWIGLU) {
+          const float up = __shfl_xor(y, 8);  // column c + 8 of the tile: the matching up row
+          if (ok && r < 8) {
+            const float rv = rinv_s[rl0 + i];
+            const float gt = y * rv;
+            bf16_t hi, lo;
+            split_bf16(gt / (1.0f + expf(-gt)) * (up * rv), hi, lo);
+            const int64_t o = (int64_t)m * a.ld_act + tile * 8 + r;
+            a.act[o] = hi;
+            a.act_lo[o] = lo;
+          }
+        } else {  // EPI_RESID
+          if (ok) {
+            float* xp = a.x + (int64_t)m * a.ldx + n;
+            const float xv = *xp + y;
+            *xp = xv;
+            bf16_t hi, lo;
+            split_bf16(xv * bf2f(a.g_next[n]), hi, lo);
+            a.xn[(int64_t)m * a.ldx + n] = hi;
+            a.xn_lo[(int64_t)m * a.ldx + n] = lo;
+            ss[i] += xv * xv;
+          }
+        }
       }
-      float s2 = xv * xv;
-      s2 += __shfl_xor(s2, 8);
-      s2 += __shfl_xor(s2, 4);
-      s2 += __shfl_xor(s2, 2);
-      s2 += __shfl_xor(s2, 1);
-      if ((col & 15) == 0 && ok) a.sumsq_out[(int64_t)m * a.n_part + n / 16] = s2;
-    } else {  // EPI_SWIGLU: column c < 8 of a tile is gate j, column c + 8 the matching up
-      const int c = col & 15;
-      if (ok && c < 8) {
-        const float gt = y * rinv_s[rr];
-        const float up = red[0][rr][col + 8] * rinv_s[rr];
-        const float sg = gt / (1.0f + expf(-gt));
-        const int j = (tile * C + (col >> 4)) * 8 + c;
-        bf16_t hi, lo;
-        split_bf16(sg * up, hi, lo);
-        a.act[(int64_t)m * a.ld_act + j] = hi;
-        a.act_lo[(int64_t)m * a.ld_act + j] = lo;
+    }
+    if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float s = ss[i];
+        s += __shfl_xor(s, 8);
+        s += __shfl_xor(s, 4);
+        s += __shfl_xor(s, 2);
+        s += __shfl_xor(s, 1);
+        if (r == 0) ssq_s[wc][rl0 + i] = s;
       }
+    }
+  }
+  if constexpr (EPI == EPI_RESID) {
+    __syncthreads();
+    if (threadIdx.x < MT * 16) {
+      const int m = row0 + threadIdx.x;
+      float s = ssq_s[0][threadIdx.x];
+#pragma unroll
+      for (int q = 1; q < WC; ++q) s += ssq_s[q][threadIdx.x];
+      if (m < a.M) a.sumsq_out[(int64_t)m * a.n_part_out + cb] = s;
     }
   }
 }
 
-template <int MT, int C, int NW, int U, int EPI>
+// ---- host side: plan and launch
+
+GemmPlan gemm_plan(int M, int n_tiles, int K, int64_t part_cap) {
+  GemmPlan best{};
+  const int mt = M <= 32 ? 2 : (M <= 64 ? 4 : 8);
+  const int mb = (M + mt * 16 - 1) / (mt * 16);
+  const int S_all = K / 32;
+  double best_cost = 1e300;
+  for (int nt : {16, 8}) {
+    if (n_tiles % nt) continue;
+    const int n_cb = n_tiles / nt;
+    for (int ks = 1; ks <= 8; ++ks) {
+      if (ks > 1 && S_all / ks < 4) break;
+      if (ks > 1 && (int64_t)ks * n_cb * nt * 16 * mb * mt * 16 > part_cap) break;
+      if (ks > 1 && (int64_t)n_cb * mb * kCtrStride > kLayerCtr0) break;  // one counter line per unit
+      // one workgroup per CU, 32 CUs per XCD; units of a column block share its XCD
+      const int per_xcd = ((n_cb + 7) / 8) * mb * ks;
+      const int rounds = (per_xcd + 31) / 32;
+      const double steps = (double)S_all / ks;
+      const double w_time = steps * nt * 1024.0 / (8e12 / 256);                   // weights at a CU's share of HBM
+      const double m_time = steps * nt * mt * 2.0 * 16.0 / 4.0 / 2.4e9;           // MFMA issue, 4 SIMDs
+      const double part_bytes = ks > 1 ? 2.0 * ks * n_tiles * 16.0 * mb * mt * 16 * 4 : 0.0;
+      const double a_bytes = (double)n_cb * mb * mt * 16 * K * 4;
+      const double cost = rounds * std::max(w_time, m_time) + 0.5 * part_bytes / 8e12 + a_bytes / 32e12 +
+                          (ks > 1 ? 1e-6 : 0.0);
+      if (cost < best_cost) {
+        best_cost = cost;
+        best = GemmPlan{mt, nt, ks, mb, n_cb};
+      }
+    }
+  }
+  return best;
+}
+
+template <int MT, int NT, int EPI>
 static void launch_cfg(const GemmArgs& a, const Exec& ex) {
-  dim3 grid((a.M + 16 * MT - 1) / (16 * MT), a.n_tiles / C);
-  SBD_KLAUNCH((gemm_kernel<MT, C, NW, U, EPI>), grid, dim3(NW * 64), ex, a);
+  const int n_cb = a.n_tiles / NT;
+  const unsigned grid = (unsigned)(((n_cb + 7) / 8) * 8 * a.splits * a.m_blocks);
+  if (a.m_blocks == 1)
+    SBD_KLAUNCH((gemm_kernel<MT, NT, EPI, true>), dim3(grid), dim3(256), ex, a);
+  else
+    SBD_KLAUNCH((gemm_kernel<MT, NT, EPI, false>), dim3(grid), dim3(256), ex, a);
 }
 
 template <int EPI>
-static hipError_t launch_epi(const GemmArgs& a, const Exec& ex) {
-  if (a.M <= 16)
-    launch_cfg<1, 2, 4, 4, EPI>(a, ex);
-  else if (a.M <= 32)
-    launch_cfg<2, 2, 8, 4, EPI>(a, ex);
-  else
-    launch_cfg<4, 2, 4, 2, EPI>(a, ex);
-  return hipGetLastError();
+static void launch_epi(const GemmArgs& a, int mt, int nt, const Exec& ex) {
+  if (nt == 16) {
+    if (mt == 2) launch_cfg<2, 16, EPI>(a, ex);
+    else if (mt == 4) launch_cfg<4, 16, EPI>(a, ex);
+    else launch_cfg<8, 16, EPI>(a, ex);
+  } else {
+    if (mt == 2) launch_cfg<2, 8, EPI>(a, ex);
+    else if (mt == 4) launch_cfg<4, 8, EPI>(a, ex);
+    else launch_cfg<8, 8, EPI>(a, ex);
+  }
 }
 
-hipError_t launch_gemm(GemmEpi epi, const GemmArgs& a, const Exec& ex) {
-  if (a.M < 1 || a.K < 32 || a.K % 32 || a.n_tiles % 8) return hipErrorInvalidValue;
+hipError_t launch_gemm(GemmEpi epi, const GemmArgs& a0, const Exec& ex) {
+  if (a0.M < 1 || a0.K < 32 || a0.K % 32 || a0.n_tiles < 8 || a0.n_tiles % 8) return hipErrorInvalidValue;
+  const GemmPlan p = gemm_plan(a0.M, a0.n_tiles, a0.K, a0.part ? a0.part_cap : 0);
+  if (p.nt == 0) return hipErrorInvalidValue;
+  if (p.splits > 1 && (a0.counters == nullptr || (int64_t)p.n_cb * p.m_blocks * kCtrStride > kLayerCtr0))
+    return hipErrorInvalidValue;
+  if (epi == EPI_RESID && a0.n_part_out != p.n_cb) return hipErrorInvalidValue;
+  GemmArgs a = a0;
+  a.splits = p.splits;
+  a.m_blocks = p.m_blocks;
   switch (epi) {
-    case EPI_SCALED_STORE: return launch_epi<EPI_SCALED_STORE>(a, ex);
-    case EPI_RESID: return launch_epi<EPI_RESID>(a, ex);
-    case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(a, ex);
+    case EPI_SCALED_STORE: launch_epi<EPI_SCALED_STORE>(a, p.mt, p.nt, ex); break;
+    case EPI_RESID: launch_epi<EPI_RESID>(a, p.mt, p.nt, ex); break;
+    case EPI_SWIGLU: launch_epi<EPI_SWIGLU>(a, p.mt, p.nt, ex); break;
     default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
 }
 
 // One thread per 16-byte piece of the packed matrix (layout at the top of this file).

@@ -93,6 +93,9 @@ bool sbd::compute_layout(const sbd_model_config& c, Layout* L) {
   const int64_t widest = std::max<int64_t>(std::max<int64_t>(o.n_qkv, 2 * (int64_t)c.ffn_dim), c.d_model);
   // split-K partials of the per-kernel path, or the parked partial tiles of the fused forward
   o.gemv_part_floats = std::max<int64_t>((int64_t)kGemvMaxSplit * 16 * widest, (int64_t)kFwdMaxWorkgroups * kFwdPartFloats);
+  // M > 16: up to 8 K slices of every output of the QKV, O and down projections at 256 rows
+  o.gemv_part_floats = std::max<int64_t>(o.gemv_part_floats, 8 * std::min<int64_t>(o.m_max, 256) *
+                                                                 std::max<int64_t>(o.n_qkv, c.d_model));
   o.gemv_part = take(o.gemv_part_floats * sizeof(float));
   o.xn2 = take(2 * o.m_max * c.d_model * 2);
   o.sumsq2 = take(o.m_max * o.n_part * sizeof(float));
@@ -213,6 +216,14 @@ hipEvent_t take_event(sbd_ctx* c) {
     SBD_HIP(ctx, expr);                                                           \
     if ((ctx)->prof) (ctx)->recs.push_back(sbd_ctx::Rec{kind, ex.start, ex.stop}); \
   } while (0)
+
+GemmArgs gemm_base(const bf16_t* A, const bf16_t* A_lo, int64_t lda, int M, int K, const bf16_t* Wp,
+                   int n_tiles, float* part, int64_t part_cap, int* counters) {
+  GemmArgs g{};
+  g.A = A; g.A_lo = A_lo; g.lda = lda; g.M = M; g.K = K; g.Wp = Wp; g.n_tiles = n_tiles;
+  g.part = part; g.part_cap = part_cap; g.counters = counters;
+  return g;
+}
 
 GemvArgs gemv_base(const bf16_t* A, const bf16_t* A_lo, int64_t lda, int M, int K, const bf16_t* Wp,
                    int n_tiles, float* part, int64_t part_cap, int* counters) {
@@ -369,11 +380,9 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
       v.qkv = qe;
       SBD_LAUNCH(c, SBD_KERNEL_QKV, launch_gemv(EPI_QKV, v, GemvShape{}, ex));
     } else {
-      GemmArgs g{};
-      g.A = xn; g.A_lo = xn_lo; g.lda = d; g.M = M; g.K = d;
-      g.Wp = wp; g.n_tiles = (int)(L.n_qkv / 16);
+      GemmArgs g = gemm_base(xn, xn_lo, d, M, d, wp, (int)(L.n_qkv / 16), vpart, vpart_cap, counters);
       g.out_f32 = qkv; g.ldo = L.n_qkv;
-      g.sumsq_in = sumsq; g.n_part = (int)L.n_part; g.inv_d = 1.0f / d; g.eps = m.rms_eps;
+      g.sumsq_in = sumsq; g.n_part = n_part_cur; g.inv_d = 1.0f / d; g.eps = m.rms_eps;
       SBD_LAUNCH(c, SBD_KERNEL_QKV, launch_gemm(EPI_SCALED_STORE, g, ex));
       RopeStageArgs ra{};
       ra.rows = drows; ra.seqs = dseqs; ra.M = M; ra.k = k; ra.layer = l;
@@ -400,11 +409,10 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
       v.sumsq = sumsq; v.n_part = n_part_o;
       SBD_LAUNCH(c, SBD_KERNEL_O_PROJ, launch_gemv(EPI_RESID, v, GemvShape{}, ex));
     } else {
-      GemmArgs go{};
-      go.A = attn; go.A_lo = attn_lo; go.lda = qd; go.M = M; go.K = qd;
-      go.Wp = wp + L.wp_o; go.n_tiles = d / 16;
+      GemmArgs go = gemm_base(attn, attn_lo, qd, M, qd, wp + L.wp_o, d / 16, vpart, vpart_cap, counters);
       go.x = x; go.ldx = d; go.xn = xn; go.xn_lo = xn_lo; go.g_next = w.mlp_norm; go.sumsq_out = sumsq;
-      go.n_part = (int)L.n_part;
+      go.n_part_out = gemm_plan(M, d / 16, qd, vpart_cap).n_cb;
+      n_part_cur = go.n_part_out;
       SBD_LAUNCH(c, SBD_KERNEL_O_PROJ, launch_gemm(EPI_RESID, go, ex));
     }
 
@@ -420,18 +428,17 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
       n_part_cur = n_part_down;
       SBD_LAUNCH(c, SBD_KERNEL_DOWN, launch_gemv(EPI_RESID, vd, GemvShape{}, ex));
     } else {
-      GemmArgs gu{};
-      gu.A = xn; gu.A_lo = xn_lo; gu.lda = d; gu.M = M; gu.K = d;
-      gu.Wp = wp + L.wp_gu; gu.n_tiles = m.ffn_dim / 8;
-      gu.sumsq_in = sumsq; gu.n_part = (int)L.n_part; gu.inv_d = 1.0f / d; gu.eps = m.rms_eps;
+      GemmArgs gu = gemm_base(xn, xn_lo, d, M, d, wp + L.wp_gu, m.ffn_dim / 8, vpart, vpart_cap, counters);
+      gu.sumsq_in = sumsq; gu.n_part = n_part_cur; gu.inv_d = 1.0f / d; gu.eps = m.rms_eps;
       gu.act = act; gu.act_lo = act_lo; gu.ld_act = m.ffn_dim;
       SBD_LAUNCH(c, SBD_KERNEL_GATE_UP, launch_gemm(EPI_SWIGLU, gu, ex));
 
-      GemmArgs gd{};
-      gd.A = act; gd.A_lo = act_lo; gd.lda = m.ffn_dim; gd.M = M; gd.K = m.ffn_dim;
-      gd.Wp = wp + L.wp_down; gd.n_tiles = d / 16;
+      GemmArgs gd = gemm_base(act, act_lo, m.ffn_dim, M, m.ffn_dim, wp + L.wp_down, d / 16, vpart, vpart_cap,
+                              counters);
       gd.x = x; gd.ldx = d; gd.xn = xn; gd.xn_lo = xn_lo; gd.g_next = g_after;
-      gd.sumsq_out = sumsq; gd.n_part = (int)L.n_part;
+      gd.sumsq_out = sumsq;
+      gd.n_part_out = gemm_plan(M, d / 16, m.ffn_dim, vpart_cap).n_cb;
+      n_part_cur = gd.n_part_out;
       SBD_LAUNCH(c, SBD_KERNEL_DOWN, launch_gemm(EPI_RESID, gd, ex));
     }
   }
@@ -439,7 +446,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   if (logits != nullptr) {
     const int r0 = lm_row < 0 ? 0 : lm_row;
     const int Ml = lm_row < 0 ? M : 1;
-    if (small) {
+    if (Ml <= 16) {
       GemvArgs v = gemv_base(xn + (int64_t)r0 * d, xn_lo + (int64_t)r0 * d, d, Ml, d,
                              c->at<bf16_t>(L.wpack) + L.wp_lm, m.vocab / 16, vpart, vpart_cap, counters);
       v.sumsq_in = sumsq + (int64_t)r0 * n_part_cur; v.n_part_in = n_part_cur;
@@ -447,11 +454,10 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
       v.out_f32 = logits; v.ldo = m.vocab;
       SBD_LAUNCH(c, SBD_KERNEL_LM_HEAD, launch_gemv(EPI_SCALED_STORE, v, GemvShape{}, ex));
     } else {
-      GemmArgs gl{};
-      gl.A = xn + (int64_t)r0 * d; gl.A_lo = xn_lo + (int64_t)r0 * d; gl.lda = d; gl.M = Ml; gl.K = d;
-      gl.Wp = c->at<bf16_t>(L.wpack) + L.wp_lm; gl.n_tiles = m.vocab / 16;
+      GemmArgs gl = gemm_base(xn + (int64_t)r0 * d, xn_lo + (int64_t)r0 * d, d, Ml, d,
+                              c->at<bf16_t>(L.wpack) + L.wp_lm, m.vocab / 16, vpart, vpart_cap, counters);
       gl.out_f32 = logits; gl.ldo = m.vocab;
-      gl.sumsq_in = sumsq + (int64_t)r0 * L.n_part; gl.n_part = (int)L.n_part;
+      gl.sumsq_in = sumsq + (int64_t)r0 * n_part_cur; gl.n_part = n_part_cur;
       gl.inv_d = 1.0f / d; gl.eps = m.rms_eps;
       SBD_LAUNCH(c, SBD_KERNEL_LM_HEAD, launch_gemm(EPI_SCALED_STORE, gl, ex));
     }

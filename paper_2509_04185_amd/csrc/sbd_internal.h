@@ -104,26 +104,43 @@ struct GemmArgs {
   int64_t lda;
   int M, K;
   const bf16_t* Wp;    // packed weights
-  int n_tiles;         // 16-row tiles of the packed matrix
+  int n_tiles;         // 16-row tiles of the packed matrix (a multiple of 8)
   // EPI_SCALED_STORE: out[m][n] = rinv[m] * y (rinv = 1 when sumsq_in == nullptr)
   float* out_f32;
   int64_t ldo;
-  // row RMS from per-row partial sums of squares [M][n_part] (EPI_SCALED_STORE, EPI_SWIGLU)
+  // row RMS from the producer's partial sums of squares [M][n_part] (EPI_SCALED_STORE,
+  // EPI_SWIGLU)
   const float* sumsq_in;
   int n_part;
   float inv_d, eps;
-  // EPI_RESID: x[m][n] += y; xn[m][n] = bf16(x * g_next[n]); sumsq_out[m][n/16] = sum x^2
+  // EPI_RESID: x[m][n] += y; xn[m][n] = x * g_next[n] as hi/lo; sumsq_out[m][p] = sum of
+  // x^2 over the columns of column block p (n_part_out = gemm_plan(...).n_cb partials)
   float* x;
   int64_t ldx;
   bf16_t* xn;
   bf16_t* xn_lo;
   const bf16_t* g_next;
   float* sumsq_out;
+  int n_part_out;
   // EPI_SWIGLU: act[m][j] = silu(rinv*gate) * rinv*up as hi/lo
   bf16_t* act;
   bf16_t* act_lo;
   int64_t ld_act;
+  // K split over workgroups: parked partial tiles (part_cap floats) and arrival counters
+  // (zero between launches)
+  float* part;
+  int64_t part_cap;
+  int* counters;
+  // set by launch_gemm from the plan
+  int splits, m_blocks;
 };
+
+// How launch_gemm cuts a product: mt 16-row tiles per row block (m_blocks row blocks),
+// nt 16-column tiles per column block (n_cb blocks), K split `splits` ways.
+struct GemmPlan {
+  int mt, nt, splits, m_blocks, n_cb;
+};
+GemmPlan gemm_plan(int M, int n_tiles, int K, int64_t part_cap);
 
 hipError_t launch_gemm(GemmEpi epi, const GemmArgs& a, const Exec& ex);
 
