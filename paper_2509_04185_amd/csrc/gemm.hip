@@ -67,16 +67,6 @@ __device__ __forceinline__ void static_for(F&& f) {
   static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
-// ds_read_b128 at LDS byte address addr + OFF, invisible to the compiler's wait insertion:
-// the caller waits (lgkmcnt) before using the result.
-template <int OFF>
-__device__ __forceinline__ i32x4 ds_read16(uint32_t addr) {
-  static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
-  i32x4 v;
-  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF));
-  return v;
-}
-
 // s_waitcnt vmcnt(N), other counters left free
 template <int N>
 __device__ __forceinline__ void vm_wait() {
@@ -204,6 +194,23 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
         for (int cw = 0; cw < CW; ++cw) acc[mw][cw] = mfma16x16x32(av[mw][h], wv[cw], acc[mw][cw]);
   };
 
+  // Consumers of a norm: the producer's partial sums of squares of this block's rows,
+  // requested before the stream (thread t adds partials of row t / TPR, float4 at a time).
+  constexpr int TPR = 256 / (MT * 16);
+  constexpr int NPRE = 4;
+  const int rr_t = threadIdx.x / TPR, q_t = threadIdx.x % TPR;
+  const int m_t = row0 + rr_t;
+  const bool norm_in = EPI != EPI_RESID && a.sumsq_in != nullptr;
+  const bool vec4 = (a.n_part & 3) == 0;
+  const int n4 = a.n_part >> 2;
+  const f32x4* prow = reinterpret_cast<const f32x4*>(a.sumsq_in + (int64_t)min(m_t, a.M - 1) * a.n_part);
+  f32x4 pre[NPRE];
+#pragma unroll
+  for (int j = 0; j < NPRE; ++j) {
+    const int p4 = q_t + j * TPR;
+    pre[j] = (norm_in && vec4 && m_t < a.M && p4 < n4) ? prow[p4] : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
   static_for<NS - 1>([&](auto B) {
     if (decltype(B)::value < nst) issue(B, decltype(B)::value);
   });
@@ -225,98 +232,131 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
   if (KS > 1) {
     const int n_units = n_cb * MB;
     const int64_t slot = ((int64_t)uid * 4 + w) * (MTW * CW);  // in 1 KB (64 x f32x4) pieces
+    const int64_t zstride = (int64_t)n_units * 4 * MTW * CW;     // pieces per slice
 #pragma unroll
     for (int mw = 0; mw < MTW; ++mw)
 #pragma unroll
       for (int cw = 0; cw < CW; ++cw)
-        *(f32x4*)(a.part + (((int64_t)kc * n_units * 4 * MTW * CW + slot + mw * CW + cw) * 64 + lane) * 4) =
-            acc[mw][cw];
+        *(f32x4*)(a.part + ((kc * zstride + slot + mw * CW + cw) * 64 + lane) * 4) = acc[mw][cw];
     if (!last_arrival_xcd(a.counters + (int64_t)uid * kCtrStride, KS)) return;
+    // ZB slices at a time, every piece of a slice in flight together; added in slice order
+    constexpr int ZB = MTW * CW >= 32 ? 1 : (MTW * CW >= 16 ? 2 : 4);
     const __amdgpu_buffer_rsrc_t rp = buf_rsrc(a.part);
 #pragma unroll
     for (int mw = 0; mw < MTW; ++mw)
 #pragma unroll
-      for (int cw = 0; cw < CW; ++cw) {
-        f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
-        for (int z0 = 0; z0 < KS; z0 += 4) {  // four slices in flight, added in slice order
-          i32x4 v[4];
+      for (int cw = 0; cw < CW; ++cw) acc[mw][cw] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int z0 = 0; z0 < KS; z0 += ZB) {
+      i32x4 v[ZB][MTW][CW];
 #pragma unroll
-          for (int u = 0; u < 4; ++u)
-            v[u] = z0 + u < KS
-                       ? ld16_l2(rp, (uint32_t)((((int64_t)(z0 + u) * n_units * 4 * MTW * CW + slot + mw * CW + cw) *
-                                                     64 + lane) * 16))
-                       : i32x4{0, 0, 0, 0};
+      for (int zz = 0; zz < ZB; ++zz)
 #pragma unroll
-          for (int u = 0; u < 4; ++u) s += __builtin_bit_cast(f32x4, v[u]);
-        }
-        acc[mw][cw] = s;
-      }
+        for (int mw = 0; mw < MTW; ++mw)
+#pragma unroll
+          for (int cw = 0; cw < CW; ++cw)
+            v[zz][mw][cw] = z0 + zz < KS ? ld16_l2(rp, (uint32_t)((((z0 + zz) * zstride + slot + mw * CW + cw) * 64 + lane) * 16))
+                                         : i32x4{0, 0, 0, 0};
+#pragma unroll
+      for (int zz = 0; zz < ZB; ++zz)
+#pragma unroll
+        for (int mw = 0; mw < MTW; ++mw)
+#pragma unroll
+          for (int cw = 0; cw < CW; ++cw) acc[mw][cw] += __builtin_bit_cast(f32x4, v[zz][mw][cw]);
+    }
   }
 
-  // ---- 1/rms of the row block's rows from the producer's partial sums of squares
+  // ---- 1/rms of the block's rows (partials beyond the prefetched ones read here)
   if constexpr (EPI != EPI_RESID) {
-    constexpr int TPR = 256 / (MT * 16);  // threads per row
-    const int rr = threadIdx.x / TPR, q = threadIdx.x % TPR;
-    const int m = row0 + rr;
     float sq = 0.f;
-    if (a.sumsq_in != nullptr && m < a.M)
-      for (int p = q; p < a.n_part; p += TPR) sq += a.sumsq_in[(int64_t)m * a.n_part + p];
+    if (norm_in && m_t < a.M) {
+      if (vec4) {
 #pragma unroll
-    for (int o = TPR / 2; o >= 1; o /= 2) sq += __shfl_xor(sq, o);
-    if (q == 0) rinv_s[rr] = (a.sumsq_in != nullptr) ? 1.0f / sqrtf(sq * a.inv_d + a.eps) : 1.0f;
-    __syncthreads();
-  }
-
-  // ---- epilogue
-#pragma unroll
-  for (int mw = 0; mw < MTW; ++mw) {
-    const int rl0 = (wm * MTW + mw) * 16 + 4 * g;  // local row of element 0
-    float ss[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int cw = 0; cw < CW; ++cw) {
-      const int tile = t0 + wc * CW + cw;
-      const int n = tile * 16 + r;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int m = row0 + rl0 + i;
-        const bool ok = m < a.M;
-        const float y = acc[mw][cw][i];
-        if constexpr (EPI == EPI_SCALED_STORE) {
-          if (ok) a.out_f32[(int64_t)m * a.ldo + n] = y * rinv_s[rl0 + i];
-        } else if constexpr (EPI == EPI_SWIGLU) {
-          const float up = __shfl_xor(y, 8);  // column c + 8 of the tile: the matching up row
-          if (ok && r < 8) {
-            const float rv = rinv_s[rl0 + i];
-            const float gt = y * rv;
-            bf16_t hi, lo;
-            split_bf16(gt / (1.0f + expf(-gt)) * (up * rv), hi, lo);
-            const int64_t o = (int64_t)m * a.ld_act + tile * 8 + r;
-            a.act[o] = hi;
-            a.act_lo[o] = lo;
-          }
-        } else {  // EPI_RESID
-          if (ok) {
-            float* xp = a.x + (int64_t)m * a.ldx + n;
-            const float xv = *xp + y;
-            *xp = xv;
-            bf16_t hi, lo;
-            split_bf16(xv * bf2f(a.g_next[n]), hi, lo);
-            a.xn[(int64_t)m * a.ldx + n] = hi;
-            a.xn_lo[(int64_t)m * a.ldx + n] = lo;
-            ss[i] += xv * xv;
-          }
+        for (int j = 0; j < NPRE; ++j) sq += (pre[j][0] + pre[j][1]) + (pre[j][2] + pre[j][3]);
+        for (int p4 = q_t + NPRE * TPR; p4 < n4; p4 += TPR) {
+          const f32x4 v = prow[p4];
+          sq += (v[0] + v[1]) + (v[2] + v[3]);
         }
+      } else {
+        for (int p = q_t; p < a.n_part; p += TPR) sq += a.sumsq_in[(int64_t)m_t * a.n_part + p];
       }
     }
-    if constexpr (EPI == EPI_RESID) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float s = ss[i];
-        s += __shfl_xor(s, 8);
-        s += __shfl_xor(s, 4);
-        s += __shfl_xor(s, 2);
-        s += __shfl_xor(s, 1);
-        if (r == 0) ssq_s[wc][rl0 + i] = s;
+    for (int o = TPR / 2; o >= 1; o /= 2) sq += __shfl_xor(sq, o);
+    if (q_t == 0) rinv_s[rr_t] = norm_in ? 1.0f / sqrtf(sq * a.inv_d + a.eps) : 1.0f;
+  }
+  __syncthreads();  // rinv_s written; every wave is past the ring, which now stages results
+
+  // ---- epilogue.  Each wave passes its tiles through LDS one row tile at a time (16 rows x
+  // 16 CW columns, rows padded by 4 floats), then lanes own 4 consecutive columns of a row:
+  // a row's 16 CW columns are written by consecutive lanes as whole 16-byte pieces.
+  constexpr int LDR = CW * 16 + 4;  // staged row length (floats)
+  constexpr int CPR = CW * 4;       // float4 pieces per staged row
+  float* stg = reinterpret_cast<float*>(smem) + w * 16 * LDR;
+  const int n_w0 = (t0 + wc * CW) * 16;  // first output column of this wave
+#pragma unroll
+  for (int mw = 0; mw < MTW; ++mw) {
+    const int rl0 = (wm * MTW + mw) * 16;  // first local row of this row tile
+#pragma unroll
+    for (int cw = 0; cw < CW; ++cw)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) stg[(4 * g + i) * LDR + cw * 16 + r] = acc[mw][cw][i];
+    if constexpr (EPI == EPI_SWIGLU) {
+      // task: (row, tile tt, half h) -> act columns 8 (tile) + 4 h .. + 3
+      constexpr int NT2 = 16 * CW * 2;
+#pragma unroll
+      for (int j = 0; j < (NT2 + 63) / 64; ++j) {
+        const int idx = j * 64 + lane;
+        const int row = idx / (CW * 2), tt = (idx % (CW * 2)) >> 1, h = idx & 1;
+        const int m = row0 + rl0 + row;
+        if (idx < NT2 && m < a.M) {
+          const f32x4 gt = *(const f32x4*)(stg + row * LDR + tt * 16 + h * 4);
+          const f32x4 up = *(const f32x4*)(stg + row * LDR + tt * 16 + 8 + h * 4);
+          const float rv = rinv_s[rl0 + row];
+          f32x4 y;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float gv = gt[e] * rv;
+            y[e] = gv / (1.0f + expf(-gv)) * (up[e] * rv);
+          }
+          i32x2 hi, lo;
+          split_bf16x4(y, hi, lo);
+          const int64_t o = (int64_t)m * a.ld_act + (t0 + wc * CW + tt) * 8 + h * 4;
+          *(i32x2*)(a.act + o) = hi;
+          *(i32x2*)(a.act_lo + o) = lo;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 16 * CPR / 64; ++j) {
+        const int idx = j * 64 + lane;
+        const int row = idx / CPR, pc = idx % CPR;
+        const int m = row0 + rl0 + row;
+        const int n = n_w0 + pc * 4;
+        const f32x4 y = *(const f32x4*)(stg + row * LDR + pc * 4);
+        if constexpr (EPI == EPI_SCALED_STORE) {
+          if (m < a.M) *(f32x4*)(a.out_f32 + (int64_t)m * a.ldo + n) = y * rinv_s[rl0 + row];
+        } else {  // EPI_RESID
+          float s2 = 0.f;
+          if (m < a.M) {
+            f32x4* xp = (f32x4*)(a.x + (int64_t)m * a.ldx + n);
+            const f32x4 xv = *xp + y;
+            *xp = xv;
+            const i32x2 gw = *(const i32x2*)(a.g_next + n);
+            f32x4 xg;
+            xg[0] = xv[0] * __uint_as_float((uint32_t)gw[0] << 16);
+            xg[1] = xv[1] * __uint_as_float((uint32_t)gw[0] & 0xffff0000u);
+            xg[2] = xv[2] * __uint_as_float((uint32_t)gw[1] << 16);
+            xg[3] = xv[3] * __uint_as_float((uint32_t)gw[1] & 0xffff0000u);
+            i32x2 hi, lo;
+            split_bf16x4(xg, hi, lo);
+            *(i32x2*)(a.xn + (int64_t)m * a.ldx + n) = hi;
+            *(i32x2*)(a.xn_lo + (int64_t)m * a.ldx + n) = lo;
+            s2 = (xv[0] * xv[0] + xv[1] * xv[1]) + (xv[2] * xv[2] + xv[3] * xv[3]);
+          }
+#pragma unroll
+          for (int o = 1; o < CPR; o <<= 1) s2 += __shfl_xor(s2, o);  // the row's CPR lanes
+          if (pc == 0) ssq_s[wc][rl0 + row] = s2;
+        }
       }
     }
   }
@@ -396,6 +436,10 @@ hipError_t launch_gemm(GemmEpi epi, const GemmArgs& a0, const Exec& ex) {
   if (p.splits > 1 && (a0.counters == nullptr || (int64_t)p.n_cb * p.m_blocks * kCtrStride > kLayerCtr0))
     return hipErrorInvalidValue;
   if (epi == EPI_RESID && a0.n_part_out != p.n_cb) return hipErrorInvalidValue;
+  // the epilogue writes 16-byte (fp32) and 8-byte (bf16) pieces of 4 columns
+  if ((epi == EPI_SCALED_STORE && a0.ldo % 4) || (epi == EPI_RESID && a0.ldx % 4) ||
+      (epi == EPI_SWIGLU && a0.ld_act % 4))
+    return hipErrorInvalidValue;
   GemmArgs a = a0;
   a.splits = p.splits;
   a.m_blocks = p.m_blocks;

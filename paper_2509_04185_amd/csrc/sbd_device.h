@@ -142,6 +142,24 @@ __device__ __forceinline__ bool last_arrival_xcd(int* counter, int expected) {
   return s_last != 0;
 }
 
+// LDS reads that the compiler does not see as such.  A kernel that fills LDS by direct
+// loads (global_load_lds) while reading another part of it would otherwise get a wait for
+// every direct load in flight before each LDS read (the compiler cannot tell the regions
+// apart), which drains its prefetch.  The caller orders these reads itself: a barrier after
+// the data has landed before them, lds_wait() after them, and lds_pin() on each result
+// before its first use.
+template <int OFF = 0>
+__device__ __forceinline__ i32x4 ds_read16(uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
+  i32x4 v;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF));
+  return v;
+}
+__device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+__device__ __forceinline__ void lds_pin(i32x4& v) { asm volatile("" : "+v"(v)); }
+// LDS byte address of a __shared__ object
+__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
+
 __device__ __forceinline__ float wave_sum(float v) {
   v += __shfl_xor(v, 32);
   return half_wave_sum(v);
