@@ -67,11 +67,6 @@ __device__ __forceinline__ void static_for(F&& f) {
   static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
-// s_waitcnt vmcnt(N), other counters left free
-template <int N>
-__device__ __forceinline__ void vm_wait() {
-  __builtin_amdgcn_s_waitcnt(((N & 15) | ((N >> 4) << 14)) | (7 << 4) | (15 << 8));
-}
 // Wait until at most n stages of FPW loads each are still in flight (n in [0, NMAX]).
 template <int FPW, int NMAX>
 __device__ __forceinline__ void vm_wait_stages(int n) {

@@ -233,8 +233,11 @@ GemvArgs gemv_base(const bf16_t* A, const bf16_t* A_lo, int64_t lda, int M, int 
   return v;
 }
 
-int pick_splits(int64_t work_groups_per_split, int nblocks) {
-  int s = (int)std::max<int64_t>(1, (1024 + work_groups_per_split - 1) / work_groups_per_split);
+// Key splits of the attention: enough workgroups for one round of two per CU (a workgroup
+// takes 64 KB of LDS), as long as every split keeps a block.
+int pick_splits(int64_t work_groups_per_split, int nblocks, int n_cu) {
+  const int64_t target = 2 * (int64_t)std::max(1, n_cu);
+  int s = (int)std::max<int64_t>(1, (target + work_groups_per_split - 1) / work_groups_per_split);
   s = std::min(s, kMaxSplits);
   s = std::min(s, std::max(1, nblocks));
   return s;
@@ -332,7 +335,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   const int n_part_down = (d / 16) / gemv_pick(EPI_RESID, d / 16, m.ffn_dim).C;
   int n_part_cur = d / 16;
   int* counters = c->at<int>(L.counters);
-  int n_splits = pick_splits((int64_t)B * nkv * n_rb, nblocks);
+  int n_splits = pick_splits((int64_t)B * nkv * n_rb, nblocks, c->n_cu_dev);
   const int bps = (nblocks + n_splits - 1) / n_splits;
   n_splits = (nblocks + bps - 1) / bps;
 

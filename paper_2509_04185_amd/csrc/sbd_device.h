@@ -142,6 +142,13 @@ __device__ __forceinline__ bool last_arrival_xcd(int* counter, int expected) {
   return s_last != 0;
 }
 
+// s_waitcnt vmcnt(N) (other counters left free)
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N <= 63, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt(((N & 15) | ((N >> 4) << 14)) | (7 << 4) | (15 << 8));
+}
+
 // LDS reads that the compiler does not see as such.  A kernel that fills LDS by direct
 // loads (global_load_lds) while reading another part of it would otherwise get a wait for
 // every direct load in flight before each LDS read (the compiler cannot tell the regions
