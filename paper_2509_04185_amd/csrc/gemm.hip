@@ -139,9 +139,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
       stride[u] = 64;
     }
   }
-  // stage st into ring slot B (= st % NS)
-  auto issue = [&](auto B, int st) {
-    char* dst = smem + decltype(B)::value * STAGE + w * 1024;
+  // stage st into ring slot st % NS
+  auto issue = [&](int st) {
+    char* dst = smem + (st % NS) * STAGE + w * 1024;
     constexpr int kPolW = STREAM ? 2 : 0;  // nt: read once
 #pragma unroll
     for (int u = 0; u < NWU; ++u)
@@ -159,28 +159,28 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
 #pragma unroll
     for (int cw = 0; cw < CW; ++cw) acc[mw][cw] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // LDS reads of a stage as inline assembly: the compiler would otherwise guard every read
-  // of LDS with a wait for all direct loads in flight (it cannot tell the ring slots
-  // apart), draining the ring at each step.  Ordering is explicit instead: the stage
-  // barrier before the reads, one lgkmcnt(0) after them, and the results pinned behind it.
+  // LDS reads of a stage with ds_read16 (sbd_device.h): the compiler would otherwise guard
+  // every read of LDS with a wait for all direct loads in flight (it cannot tell the ring
+  // slots apart), draining the ring at each step.  Ordering is explicit instead: the stage
+  // barrier before the reads, lds_wait() after them, and the results pinned behind it.
   const uint32_t lds_w = (uint32_t)(uintptr_t)smem + (uint32_t)(wc * CW * 1024 + lane * 16);
   const uint32_t lds_a = (uint32_t)(uintptr_t)smem + (uint32_t)(WB + wm * MTW * 2048 + lane * 16);
-  auto compute = [&](auto B) {
-    constexpr uint32_t SB = decltype(B)::value * STAGE;
-    const uint32_t aw = lds_w + SB, aa = lds_a + SB;
+  auto compute = [&](int st) {
+    const uint32_t sb = (uint32_t)((st % NS) * STAGE);
+    const uint32_t aw = lds_w + sb, aa = lds_a + sb;
     i32x4 wv[CW], av[MTW][2];
     static_for<CW>([&](auto I) { wv[decltype(I)::value] = ds_read16<decltype(I)::value * 1024>(aw); });
     static_for<MTW * 2>([&](auto I) {
       constexpr int i = decltype(I)::value;
       av[i / 2][i % 2] = ds_read16<i * 1024>(aa);
     });
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    lds_wait();
 #pragma unroll
-    for (int cw = 0; cw < CW; ++cw) asm volatile("" : "+v"(wv[cw]));
+    for (int cw = 0; cw < CW; ++cw) lds_pin(wv[cw]);
 #pragma unroll
     for (int mw = 0; mw < MTW; ++mw)
 #pragma unroll
-      for (int h = 0; h < 2; ++h) asm volatile("" : "+v"(av[mw][h]));
+      for (int h = 0; h < 2; ++h) lds_pin(av[mw][h]);
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
@@ -206,21 +206,16 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
     pre[j] = (norm_in && vec4 && m_t < a.M && p4 < n4) ? prow[p4] : f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  static_for<NS - 1>([&](auto B) {
-    if (decltype(B)::value < nst) issue(B, decltype(B)::value);
-  });
-  // the loop is unrolled by NS so that every ring slot is named statically
-  for (int c0 = 0; c0 < nst; c0 += NS) {
-    static_for<NS>([&](auto B) {
-      constexpr int b = decltype(B)::value;
-      const int c = c0 + b;
-      if (c < nst) {
-        vm_wait_stages<FPW, NS - 2>(min(NS - 2, nst - 1 - c));  // stage c has landed (this wave's part)
-        stage_barrier();                                         // ... and every wave's; stage c - 1 is free
-        if (c + NS - 1 < nst) issue(std::integral_constant<int, (b + NS - 1) % NS>{}, c + NS - 1);
-        compute(B);
-      }
-    });
+  // A kernel's code runs cold from the instruction cache in every workgroup: the ring is
+  // driven by compact loops (slot = stage % NS at run time) rather than unrolled code.
+#pragma unroll 1
+  for (int st = 0; st < NS - 1 && st < nst; ++st) issue(st);
+#pragma unroll 1
+  for (int c = 0; c < nst; ++c) {
+    vm_wait_stages<FPW, NS - 2>(min(NS - 2, nst - 1 - c));  // stage c has landed (this wave's part)
+    stage_barrier();                                         // ... and every wave's; stage c - 1 is free
+    if (c + NS - 1 < nst) issue(c + NS - 1);
+    compute(c);
   }
 
   // ---- K split over workgroups: park the slice, the last to arrive adds all in order
@@ -288,9 +283,30 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
   constexpr int CPR = CW * 4;       // float4 pieces per staged row
   float* stg = reinterpret_cast<float*>(smem) + w * 16 * LDR;
   const int n_w0 = (t0 + wc * CW) * 16;  // first output column of this wave
+  // EPI_RESID: a lane's residual pieces of row tile mw + 1 are requested before the stores
+  // of row tile mw (which the compiler may not move them past); the gain is the same for
+  // every row of the lane.
+  constexpr int NPASS = 16 * CPR / 64;  // read-back passes per row tile
+  const int n_l = n_w0 + (lane % CPR) * 4;
+  f32x4 xcur[NPASS], xnxt[NPASS];
+  i32x2 gw{0, 0};
+  auto load_x = [&](int mw, f32x4(&xv)[NPASS]) {
+#pragma unroll
+    for (int j = 0; j < NPASS; ++j) {
+      const int m = row0 + (wm * MTW + mw) * 16 + (j * 64 + lane) / CPR;
+      xv[j] = m < a.M ? *(const f32x4*)(a.x + (int64_t)m * a.ldx + n_l) : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  };
+  if constexpr (EPI == EPI_RESID) {
+    gw = *(const i32x2*)(a.g_next + n_l);
+    load_x(0, xcur);
+  }
 #pragma unroll
   for (int mw = 0; mw < MTW; ++mw) {
     const int rl0 = (wm * MTW + mw) * 16;  // first local row of this row tile
+    if constexpr (EPI == EPI_RESID) {
+      if (mw + 1 < MTW) load_x(mw + 1, xnxt);
+    }
 #pragma unroll
     for (int cw = 0; cw < CW; ++cw)
 #pragma unroll
@@ -333,10 +349,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
         } else {  // EPI_RESID
           float s2 = 0.f;
           if (m < a.M) {
-            f32x4* xp = (f32x4*)(a.x + (int64_t)m * a.ldx + n);
-            const f32x4 xv = *xp + y;
-            *xp = xv;
-            const i32x2 gw = *(const i32x2*)(a.g_next + n);
+            const f32x4 xv = xcur[j] + y;
+            *(f32x4*)(a.x + (int64_t)m * a.ldx + n) = xv;
             f32x4 xg;
             xg[0] = xv[0] * __uint_as_float((uint32_t)gw[0] << 16);
             xg[1] = xv[1] * __uint_as_float((uint32_t)gw[0] & 0xffff0000u);
@@ -353,6 +367,10 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
           if (pc == 0) ssq_s[wc][rl0 + row] = s2;
         }
       }
+    }
+    if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+      for (int j = 0; j < NPASS; ++j) xcur[j] = xnxt[j];
     }
   }
   if constexpr (EPI == EPI_RESID) {
