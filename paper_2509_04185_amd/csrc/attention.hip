@@ -15,16 +15,241 @@
 //                   tile; V^T comes from the transposed, permuted cache blocks)
 // Each split leaves unnormalised (max, sum, O) per row; a merge kernel combines the
 // splits with log-sum-exp weights in split order.  K and V blocks are staged in LDS by the
-// whole workgroup (see the kernel).
+// whole workgroup (see the kernels: attention_body.h for the launches that share a
+// workgroup with other phases, attn_split_kernel below for the standalone split kernel).
 
 #include "attention_body.h"
 
 namespace sbd {
 
+// The split kernel of the per-kernel path streams long key ranges, so it is shaped for
+// bytes in flight: 8 waves; the 64 key positions of a ring stage (two 32-key blocks of K
+// and V, copied straight into LDS) are split between two waves holding the same 16 query
+// rows, so each SIMD has two waves to overlap MFMA, softmax and LDS reads with the stream;
+// a ring of NBUF stages (128 KB) keeps NBUF - 1 stages in flight.  At the end the two key
+// halves of each row set are combined through LDS (log-sum-exp weights) into the split's
+// partial.  LDS reads are ds_read16, ordered by hand (see sbd_device.h).
 template <int DH>
-__global__ __launch_bounds__(256) void attn_split_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) char smem[kAttnSmem];
-  attn_split_body<DH, false>(a, blockIdx.x, blockIdx.y, blockIdx.z, smem);
+__global__ __launch_bounds__(512) void attn_split_kernel(AttnArgs a) {
+  constexpr int NDT = DH / 16;  // 16-wide dimension tiles
+  constexpr int NKS = DH / 32;  // 32-wide reduction steps for the scores
+  constexpr int BLK = 32 * DH * 2;            // bytes of K (or of V) per 32-key block
+  constexpr int STAGE = 2 * 2 * BLK;          // two blocks, K and V
+  constexpr int NBUF = (128 * 1024) / STAGE > 8 ? 8 : (128 * 1024) / STAGE;
+  constexpr int KPR = DH / 8;                 // 16-byte pieces per K row
+  constexpr int LPB = BLK / 1024;             // 1 KB wave-loads per part per block
+  constexpr int PER_WAVE = STAGE / 1024 / 8;  // wave-loads of one wave per stage
+  static_assert(NBUF >= 3 && (NBUF - 2) * PER_WAVE <= 63, "ring shape");
+  __shared__ __attribute__((aligned(16))) char smem[NBUF * STAGE];
+  __shared__ int s_kend[8];
+
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int rs = w & 3, kh = w >> 2;  // row set (16 rows), key half of each stage
+  const int r = lane & 15, grp = lane >> 4;
+  const int split = blockIdx.x, g = blockIdx.y / a.n_rowblocks, rb = blockIdx.y % a.n_rowblocks, b = blockIdx.z;
+  const SeqParam sp = a.seqs[b];
+  const int L = sp.cache_len, nc = sp.n_causal, k = a.k;
+  const int G = a.n_q / a.n_kv;
+  const int R = G * k;
+  const int rho = rb * 64 + rs * 16 + r;
+  const bool row_ok = rho < R;
+  const int hh = row_ok ? rho / k : 0;
+  const int j = row_ok ? rho % k : 0;
+  const int hq = g * G + hh;
+  const int kend = row_ok ? ((j >= nc) ? L + k : L + j + 1) : 0;
+  const int blk0 = split * a.blocks_per_split, blk_lim = blk0 + a.blocks_per_split;
+  int kend_w = kend;
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) kend_w = max(kend_w, __shfl_xor(kend_w, o));
+  const int blk1 = min(blk_lim, (kend_w + 31) / 32);  // this wave's blocks end here
+  int kend_wg = kend_w;
+  kend_wg = max(kend_wg, __shfl_xor(kend_wg, 16));
+  kend_wg = max(kend_wg, __shfl_xor(kend_wg, 32));
+  if (lane == 0) s_kend[w] = kend_wg;
+
+  // queries (B operand, hi and lo): row r, dims 32 s + 8 grp .. + 8; complete before the ring
+  i32x4 qf[NKS], ql[NKS];
+  const int64_t qoff = ((int64_t)(b * k + j) * a.n_q + hq) * DH;
+#pragma unroll
+  for (int s2 = 0; s2 < NKS; ++s2) {
+    qf[s2] = row_ok ? *(const i32x4*)(a.q + qoff + 32 * s2 + 8 * grp) : i32x4{0, 0, 0, 0};
+    ql[s2] = row_ok ? *(const i32x4*)(a.q_lo + qoff + 32 * s2 + 8 * grp) : i32x4{0, 0, 0, 0};
+  }
+  vm_wait<0>();
+  __syncthreads();
+  for (int i = 0; i < 8; ++i) kend_wg = max(kend_wg, s_kend[i]);
+  const int blk1_wg = min(blk_lim, (kend_wg + 31) / 32);
+  const int n_st = blk1_wg > blk0 ? (blk1_wg - blk0 + 1) / 2 : 0;
+
+  const int64_t hb = attn_head_base(a.layer, sp.slot, g, a.n_slots, a.n_kv, a.cap, DH);
+  const bf16_t* kbase = a.kcache + hb;
+  const bf16_t* vbase = a.vcache + hb;
+  // Wave-load u of wave w in stage st: i = w + 8u -> block i / (2 LPB) of the stage, part
+  // (i / LPB) % 2 (K, V), 1 KB slice i % LPB; pieces XOR-swizzled as in attn_core.
+  auto issue = [&](int st) {
+    char* buf = smem + (st % NBUF) * STAGE;
+#pragma unroll
+    for (int u = 0; u < PER_WAVE; ++u) {
+      const int idx = w + 8 * u;
+      const int bi = idx / (2 * LPB), part = (idx / LPB) % 2, sub = idx % LPB;
+      int kb = blk0 + 2 * st + bi;
+      if (kb >= blk1_wg) kb = blk1_wg - 1;  // past the end: a valid block, never used
+      const bf16_t* src;
+      if (part == 0) {
+        const int row = sub * (1024 / (DH * 2)) + lane / KPR, pc = lane % KPR;
+        src = kbase + (int64_t)(kb * 32 + row) * DH + ((pc ^ (row % KPR)) * 8);
+      } else {
+        const int row = sub * 16 + lane / 4, pc = lane % 4;
+        src = vbase + (int64_t)kb * DH * 32 + row * 32 + ((pc ^ ((row >> 2) & 3)) * 8);
+      }
+      __builtin_amdgcn_global_load_lds((const void*)src,
+                                       (__attribute__((address_space(3))) void*)(buf + (bi * 2 + part) * BLK + sub * 1024),
+                                       16, 0, 0);
+    }
+  };
+
+  f32x4 o[NDT];
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+
+  // this wave's block of stage st: scores, online softmax, O^T += V^T P^T
+  auto compute = [&](int st) {
+    const int kb = blk0 + 2 * st + kh;
+    if (kb >= blk1) return;  // wave-uniform: nothing of this block is visible to its rows
+    const char* kblk = smem + (st % NBUF) * STAGE + (kh * 2) * BLK;
+    const char* vblk = kblk + BLK;
+    i32x4 kf[2][NKS];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int s2 = 0; s2 < NKS; ++s2) {
+        const int row = 16 * t + r;
+        kf[t][s2] = ds_read16(lds_addr(kblk + row * DH * 2 + (((4 * s2 + grp) ^ (row % KPR)) * 16)));
+      }
+    lds_wait();
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int s2 = 0; s2 < NKS; ++s2) lds_pin(kf[t][s2]);
+    f32x4 sc[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      sc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s2 = 0; s2 < NKS; ++s2) {
+        sc[t] = mfma16x16x32(kf[t][s2], qf[s2], sc[t]);
+        sc[t] = mfma16x16x32(kf[t][s2], ql[s2], sc[t]);
+      }
+    }
+    i32x4 vf[NDT];  // requested now: the softmax below hides their latency
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) {
+      const int row = 16 * dt + r;
+      vf[dt] = ds_read16(lds_addr(vblk + row * 64 + ((grp ^ ((row >> 2) & 3)) * 16)));
+    }
+    // sc[t][i]: score of key 32 kb + 16 t + 4 grp + i for query row r
+    float mloc = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (32 * kb + 16 * t + 4 * grp + i >= kend) sc[t][i] = -INFINITY;
+        mloc = fmaxf(mloc, sc[t][i]);
+      }
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+    const float m_new = fmaxf(m_run, mloc);
+    // exponents are <= 0 here: the hardware exp2 suffices (results below 2^-126 flush to 0)
+    const float scale = (m_run == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
+    float p[8];
+    float lsum = 0.f;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float sv = sc[t][i];
+        const float v = (sv == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(sv - m_new);
+        p[4 * t + i] = v;
+        lsum += v;
+      }
+    lsum += __shfl_xor(lsum, 16);
+    lsum += __shfl_xor(lsum, 32);
+    l_run = l_run * scale + lsum;
+    m_run = m_new;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) o[dt] *= scale;
+    // P as hi/lo bf16 (B operand): element e holds key 16*(e/4) + 4*grp + e%4.
+    i32x4 pf, pl;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float p0 = p[2 * e], p1 = p[2 * e + 1];
+      const uint32_t hw = pack_bf2(p0, p1);
+      pf[e] = (int)hw;
+      pl[e] = (int)pack_bf2(p0 - __uint_as_float(hw << 16), p1 - __uint_as_float(hw & 0xffff0000u));
+    }
+    lds_wait();
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) lds_pin(vf[dt]);
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) {
+      o[dt] = mfma16x16x32(vf[dt], pf, o[dt]);
+      o[dt] = mfma16x16x32(vf[dt], pl, o[dt]);
+    }
+  };
+
+  // bare s_barrier between stages: the copies are complete once this wave's vmcnt dropped
+  auto bar = [] {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+  for (int st = 0; st < NBUF - 1 && st < n_st; ++st) issue(st);
+  for (int c = 0; c < n_st; ++c) {
+    const int ahead = min(NBUF - 2, n_st - 1 - c);  // later stages still in flight
+    if (ahead >= 6) vm_wait<6 * PER_WAVE>();
+    else if (ahead == 5) vm_wait<5 * PER_WAVE>();
+    else if (ahead == 4) vm_wait<4 * PER_WAVE>();
+    else if (ahead == 3) vm_wait<3 * PER_WAVE>();
+    else if (ahead == 2) vm_wait<2 * PER_WAVE>();
+    else if (ahead == 1) vm_wait<PER_WAVE>();
+    else vm_wait<0>();
+    bar();  // every wave's part of stage c is in; every wave is done with stage c - 1
+    if (c + NBUF - 1 < n_st) issue(c + NBUF - 1);
+    compute(c);
+  }
+  __syncthreads();  // the ring is free: it holds the second key half's states next
+
+  // combine the two key halves of each row set: waves 4..7 park (m, l, O), waves 0..3 add
+  constexpr int SLOT = NDT * 16 + 16;  // bytes per lane (16-byte aligned pieces)
+  char* park = smem + (rs * 64 + lane) * SLOT;
+  if (kh == 1) {
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) *(f32x4*)(park + dt * 16) = o[dt];
+    *(float*)(park + NDT * 16) = m_run;
+    *(float*)(park + NDT * 16 + 4) = l_run;
+  }
+  __syncthreads();
+  if (kh == 1 || !row_ok) return;
+  const float m1 = *(const float*)(park + NDT * 16), l1 = *(const float*)(park + NDT * 16 + 4);
+  const float mm = fmaxf(m_run, m1);
+  const float s0 = (m_run == -INFINITY) ? 0.f : exp2f(m_run - mm);
+  const float s1 = (m1 == -INFINITY) ? 0.f : exp2f(m1 - mm);
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt) o[dt] = o[dt] * s0 + *(const f32x4*)(park + dt * 16) * s1;
+  const float ll = l_run * s0 + l1 * s1;
+
+  // the split's unnormalised (max, sum, O) per row, as attn_split_body leaves them
+  const int64_t item = (int64_t)(b * k + j) * a.n_q + hq;
+  const int64_t n_items = (int64_t)a.B * k * a.n_q;
+  if (grp == 0) {
+    float* ml = a.part_ml + ((int64_t)split * n_items + item) * 2;
+    ml[0] = mm;
+    ml[1] = ll;
+  }
+  const int64_t po = ((int64_t)split * n_items + item) * DH;
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt) *(f32x4*)(a.part_o + po + 16 * dt + 4 * grp) = o[dt];
 }
 
 template <int DH>
@@ -38,9 +263,9 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 hipError_t launch_attention_split(const AttnArgs& a, const Exec& ex) {
   dim3 grid(a.n_splits, a.n_kv * a.n_rowblocks, a.B);
   if (a.d_h == 128)
-    SBD_KLAUNCH(attn_split_kernel<128>, grid, dim3(256), ex, a);
+    SBD_KLAUNCH(attn_split_kernel<128>, grid, dim3(512), ex, a);
   else if (a.d_h == 64)
-    SBD_KLAUNCH(attn_split_kernel<64>, grid, dim3(256), ex, a);
+    SBD_KLAUNCH(attn_split_kernel<64>, grid, dim3(512), ex, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

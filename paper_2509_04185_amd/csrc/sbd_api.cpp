@@ -233,10 +233,10 @@ GemvArgs gemv_base(const bf16_t* A, const bf16_t* A_lo, int64_t lda, int M, int 
   return v;
 }
 
-// Key splits of the attention: enough workgroups for one round of two per CU (a workgroup
-// takes 64 KB of LDS), as long as every split keeps a block.
+// Key splits of the attention: enough workgroups for one round of one per CU (a workgroup
+// takes 128 KB of LDS), as long as every split keeps a block.
 int pick_splits(int64_t work_groups_per_split, int nblocks, int n_cu) {
-  const int64_t target = 2 * (int64_t)std::max(1, n_cu);
+  const int64_t target = std::max(1, n_cu);
   int s = (int)std::max<int64_t>(1, (target + work_groups_per_split - 1) / work_groups_per_split);
   s = std::min(s, kMaxSplits);
   s = std::min(s, std::max(1, nblocks));
