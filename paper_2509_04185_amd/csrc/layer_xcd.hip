@@ -49,6 +49,7 @@ namespace {
 constexpr int kLxSmem = 98304;       // LDS per workgroup: more than half a CU's, so one per CU
 constexpr int kDH = 128;
 constexpr int kLxMaxKs = 8;          // K slices of a QKV group at most (32 / (G + 2), G >= 2)
+constexpr int kLxMergeBatch = kXcdWgs;  // attention tasks of one sequence at most
 // counter lines of XCD x: [x * 64, x * 64 + 64); device-wide lines after all XCDs'
 constexpr int kCtrQkv = 0;           // + group: last-arrival counters of the QKV slices
 constexpr int kCtrQkvDone = 40;      // QKV groups finished (epilogue stored)
@@ -351,17 +352,19 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
         const float wgt = ml.x == -INFINITY ? 0.f : exp2f(ml.x - mx);
         const float lsum = wave_sum(wgt * ml.y);
         float acc0 = 0.f, acc1 = 0.f;
-        for (int t0 = 0; t0 < nt; t0 += 8) {  // wave-uniform; eight tasks in flight
-          float v0[8], v1[8];
+        // every task's partial requested at once (nt <= kLxMergeBatch: one round trip on the
+        // layer's dependency chain), added in task order
+        for (int t0 = 0; t0 < nt; t0 += kLxMergeBatch) {  // wave-uniform
+          float v0[kLxMergeBatch], v1[kLxMergeBatch];
 #pragma unroll
-          for (int u = 0; u < 8; ++u) {
+          for (int u = 0; u < kLxMergeBatch; ++u) {
             const int t = min(t0 + u, nt - 1);
             const uint32_t base = (uint32_t)((((int64_t)(b * nt + t)) * kLxRows + rho) * kDH * 4);
             v0[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ro, base + lane * 4, 0, kPolicyL2));
             v1[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ro, base + (lane + 64) * 4, 0, kPolicyL2));
           }
 #pragma unroll
-          for (int u = 0; u < 8; ++u) {
+          for (int u = 0; u < kLxMergeBatch; ++u) {
             const float wu = t0 + u < nt ? __shfl(wgt, t0 + u) : 0.f;
             acc0 += wu * v0[u];
             acc1 += wu * v1[u];
