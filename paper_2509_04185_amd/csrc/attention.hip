@@ -104,7 +104,7 @@ __global__ __launch_bounds__(512) void attn_split_kernel(AttnArgs a) {
       }
       __builtin_amdgcn_global_load_lds((const void*)src,
                                        (__attribute__((address_space(3))) void*)(buf + (bi * 2 + part) * BLK + sub * 1024),
-                                       16, 0, 0);
+                                       16, 0, 2);  // nt: each cache byte is read once
     }
   };
 
