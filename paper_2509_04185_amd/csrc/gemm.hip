@@ -408,8 +408,12 @@ GemmPlan gemm_plan(int M, int n_tiles, int K, int64_t part_cap) {
       const double m_time = steps * nt * mt * 2.0 * 16.0 / 4.0 / 2.4e9;           // MFMA issue, 4 SIMDs
       const double part_bytes = ks > 1 ? 2.0 * ks * n_tiles * 16.0 * mb * mt * 16 * 4 : 0.0;
       const double a_bytes = (double)n_cb * mb * mt * 16 * K * 4;
-      const double cost = rounds * std::max(w_time, m_time) + 0.5 * part_bytes / 8e12 + a_bytes / 32e12 +
-                          (ks > 1 ? 1e-6 : 0.0);
+      // the last arriver reads the slices in batches of ZB (fewer when a wave holds more
+      // accumulators), one dependent round trip each
+      const int nacc = (nt == 16 ? mt : mt / 2) * 4;
+      const int zb = nacc >= 32 ? 1 : (nacc >= 16 ? 2 : 4);
+      const double reduce = ks > 1 ? 1e-6 + 0.6e-6 * ((ks + zb - 1) / zb) : 0.0;
+      const double cost = rounds * std::max(w_time, m_time) + 0.5 * part_bytes / 8e12 + a_bytes / 32e12 + reduce;
       if (cost < best_cost) {
         best_cost = cost;
         best = GemmPlan{mt, nt, ks, mb, n_cb};
