@@ -1,4 +1,5 @@
 """Build libsbd.so (the HIP kernels and the C ABI) for gfx950 with hipcc, in-tree."""
+import concurrent.futures
 import os
 import shutil
 import subprocess
@@ -29,15 +30,20 @@ def build(verbose: bool = False) -> str:
     """Compile every source and link libsbd.so next to this file; returns its path."""
     objdir = os.path.join(PKG, "_build")
     os.makedirs(objdir, exist_ok=True)
-    objs = []
+    objs, cmds = [], []
     cc = hipcc()
     for src in SOURCES:
         obj = os.path.join(objdir, os.path.splitext(src)[0] + ".o")
         cmd = [cc] + FLAGS + ["-c", os.path.join(CSRC, src), "-o", obj]
         if src.endswith(".cpp"):
             cmd = [cc] + FLAGS + ["-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
-        _run(cmd, verbose)
+        cmds.append(cmd)
         objs.append(obj)
+    # one hipcc per source, a few at a time (each is single-threaded)
+    jobs = max(1, min(len(cmds), len(os.sched_getaffinity(0)), 8))
+    with concurrent.futures.ThreadPoolExecutor(jobs) as pool:
+        for f in [pool.submit(_run, cmd, verbose) for cmd in cmds]:
+            f.result()
     tmp = LIB + ".tmp"
     _run([cc, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp] + objs, verbose)
     os.replace(tmp, LIB)

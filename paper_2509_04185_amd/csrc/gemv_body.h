@@ -187,9 +187,10 @@ __device__ __forceinline__ void gemv_stream_x64(__amdgpu_buffer_rsrc_t rx, __amd
   }
 }
 
-// Add a value to the fixed-point residual (exact; any order gives the same sum).
-__device__ __forceinline__ void fix_add(int64_t* p, float v) {
-  const long long q = __double2ll_rn((double)v * 4294967296.0);
+// A value as fixed point (v * 2^32, rounded to nearest), and the atomic add of such values to
+// the residual (exact; any order gives the same sum).
+__device__ __forceinline__ long long fix_q(float v) { return __double2ll_rn((double)v * 4294967296.0); }
+__device__ __forceinline__ void fix_add_q(int64_t* p, long long q) {
   atomicAdd(reinterpret_cast<unsigned long long*>(p), (unsigned long long)q);
 }
 

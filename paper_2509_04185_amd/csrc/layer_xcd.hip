@@ -59,9 +59,6 @@ constexpr int kCtrOStart = 43;       // workgroups past the O projection's wait
 constexpr int kCtrGuDone = 44;       // workgroups past gate/up
 constexpr int kCtrDownStart = 45;    // workgroups past the down projection's wait
 constexpr int kCtrScratch = 63;      // a line nothing reads (target of l2_touch_keep)
-// device-wide lines, after the 8 XCDs' blocks
-constexpr int kCtrDevRead = kXcds * 64;      // workgroups done reading the residual
-constexpr int kCtrDevPassed = kXcds * 64 + 1;  // workgroups past the wait on it
 
 __device__ __forceinline__ int* xcd_ctr(const LayerXArgs& a, int x, int line) {
   return a.ctr + (int64_t)(x * 64 + line) * kCtrStride;
@@ -172,30 +169,41 @@ __device__ __forceinline__ void row_ss_reduce(float ss, float* tmp_s, float* row
   __syncthreads();
 }
 
-// The residual is read (phase 1) and updated (last phase) in the same launch, by workgroups
-// of all XCDs: an update may start only once every workgroup has finished reading.  Each
-// workgroup reports when it has (dev_read_done); the first update of a workgroup waits for
-// all 256 reports (dev_read_wait), which in practice have long arrived; the last workgroup
-// past the wait resets both counters for the next launch.
-__device__ __forceinline__ void dev_read_done(const LayerXArgs& a) {
-  __syncthreads();
-  if (threadIdx.x == 0) __hip_atomic_fetch_add(a.ctr + (int64_t)kCtrDevRead * kCtrStride, 1, __ATOMIC_RELAXED,
-                                               __HIP_MEMORY_SCOPE_AGENT);
+// The residual lives in three buffers used in turn: launch i reads x_src = R[i % 3], adds
+// its products into x_dst = R[(i + 1) % 3] (zeroed by launch i - 1) and zeroes
+// x_zero = R[(i + 2) % 3] (read by launch i - 1, so nobody uses it any more).  Nothing is
+// read and updated in one launch, so no workgroup waits for the others' reads.  The old
+// value of each output column is added exactly once: XCD x adds it for tile x of each
+// packed group, together with its own partial product.
+
+// Share `part` of `parts` of x_zero (rows [0, M)), 16 bytes per store.
+__device__ __forceinline__ void residual_zero(const LayerXArgs& a, int part, int parts) {
+  const int64_t n = (int64_t)a.M * a.d / 2;  // d is even
+  longlong2* z = reinterpret_cast<longlong2*>(a.x_zero);
+  for (int64_t e = (int64_t)part * 256 + threadIdx.x; e < n; e += (int64_t)parts * 256) z[e] = longlong2{0, 0};
 }
-__device__ __forceinline__ void dev_read_wait(const LayerXArgs& a, int what) {
-  int* rd = a.ctr + (int64_t)kCtrDevRead * kCtrStride;
-  int* ps = a.ctr + (int64_t)kCtrDevPassed * kCtrStride;
-  xcd_wait<__HIP_MEMORY_SCOPE_AGENT>(a, rd, kXcds * kXcdWgs, what);
-  if (threadIdx.x == 0 &&
-      __hip_atomic_fetch_add(ps, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == kXcds * kXcdWgs - 1) {
-    __hip_atomic_store(rd, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(ps, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
+// Old residual of the elements of tile x of group grp that this lane adds (rows 4 g4 + i,
+// column r; wave x % 4 owns the tile); zero elsewhere.
+__device__ __forceinline__ void residual_old(const LayerXArgs& a, int grp, int x, long long (&old)[4]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = lane & 15, g4 = lane >> 4;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) old[i] = 0;
+  if (wave == (x & 3)) {
+    const int n = (grp * 8 + x) * 16 + r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = 4 * g4 + i;
+      if (m < a.M) old[i] = a.x_src[(int64_t)m * a.d + n];
+    }
   }
 }
 
-// Add the summed tiles of packed group grp (wave w owns tiles w and w + 4) into the
-// fixed-point residual.
-__device__ __forceinline__ void residual_add(const LayerXArgs& a, int grp, const f32x4 (&acc)[8]) {
+// Add the summed tiles of packed group grp (wave w owns tiles w and w + 4) into x_dst, with
+// the old values of tile x.
+__device__ __forceinline__ void residual_add(const LayerXArgs& a, int grp, int x, const f32x4 (&acc)[8],
+                                             const long long (&old)[4]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = lane & 15, g4 = lane >> 4;
 #pragma unroll
@@ -205,7 +213,7 @@ __device__ __forceinline__ void residual_add(const LayerXArgs& a, int grp, const
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int m = 4 * g4 + i;
-      if (m < a.M) fix_add(a.x64 + (int64_t)m * a.d + n, acc[ct][i]);
+      if (m < a.M) fix_add_q(a.x_dst + (int64_t)m * a.d + n, fix_q(acc[ct][i]) + (ct == x ? old[i] : 0));
     }
   }
 }
@@ -220,7 +228,11 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
   const int G = a.n_q / a.n_kv;
   const int ngrp = G + 2, KS = kXcdWgs / ngrp;
   float* xpart = a.xpart + (int64_t)x * kLxXcdFloats;
+  // the workgroups without a QKV slice zero the next launch's residual buffer meanwhile
+  const int n_idle = kXcdWgs - ngrp * KS;
+  if (lw >= ngrp * KS) residual_zero(a, x * n_idle + (lw - ngrp * KS), kXcds * n_idle);
 
+  bool finisher = false;  // this workgroup ran a QKV group's epilogue
   // ---- 1. QKV projection, unit (group gi of this XCD, K slice kc)
   if (lw < ngrp * KS) {
     const int gi = lw / KS, kc = lw % KS;
@@ -243,7 +255,7 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
 #pragma unroll
     for (int ct = 0; ct < 8; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
     float ss = 0.f;  // x^2 of this lane's elements of row r: the slice's share of the RMSNorm sums
-    gemv_stream_x64<8, 1>(buf_rsrc(a.x64), buf_rsrc(a.g_attn), (uint32_t)(((int64_t)arow * a.d + g4 * 8 + s_b * 32) * 8),
+    gemv_stream_x64<8, 1>(buf_rsrc(a.x_src), buf_rsrc(a.g_attn), (uint32_t)(((int64_t)arow * a.d + g4 * 8 + s_b * 32) * 8),
                           (uint32_t)((g4 * 8 + s_b * 32) * 2), wt, ns, acc, ss);
     float* ss_s = reinterpret_cast<float*>(smem + 65536 + 1024);  // [64] wave shares, then [16] rows
     row_ss_reduce(r < a.M ? ss : 0.f, ss_s, ss_s + 64);
@@ -294,9 +306,21 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
       for (int i = 0; i < 4; ++i) rinv[i] = rinv_s[4 * g4 + i];
       qkv_epilogue<kDH>(e, a.M, grp, acc, rinv, qpre, wave);  // wave w: rows 4g + w
       xcd_signal(xcd_ctr(a, x, kCtrQkvDone));
+      finisher = true;
     }
   }
-  dev_read_done(a);  // this workgroup reads the residual no more
+
+  // The first two steps of this wave's O weights (phase 4): requested now by the workgroups
+  // that finished no QKV group (the memory system is idle until phase 4), by the others
+  // before their wait in phase 4, so that nothing on the way to the attention waits for them.
+  const int o_S = a.n_q * kDH / 32;
+  const int o_z0 = x * G * kDH / 32, o_zn = G * kDH / 32;
+  const int o_sb = o_z0 + o_zn * wave / 4, o_ns = o_z0 + o_zn * (wave + 1) / 4 - o_sb;
+  const bf16_t* o_wt[8];
+#pragma unroll
+  for (int ct = 0; ct < 8; ++ct) o_wt[ct] = a.wo + packed_frag(lw * 8 + ct, o_sb, o_S) + lane * 8;
+  i32x4 o_w01[2][8];
+  if (!finisher && o_ns > 0) gemv_issue_w<8, 2>(o_wt, 0, o_ns, o_w01);
 
   // ---- 2. attention of KV head x: task t = (sequence, key range)
   const int n_tasks = a.B * a.n_tasks;
@@ -388,15 +412,18 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
   // ---- 4. O projection: group lw, K slice x (the query heads of KV head x)
   {
     const int grp = lw;
-    const int qd = a.n_q * kDH, S = qd / 32;
-    const int z0 = x * G * kDH / 32, zn = G * kDH / 32;
-    const int s_b = z0 + zn * wave / 4, ns = z0 + zn * (wave + 1) / 4 - s_b;
-    const bf16_t* wt[8];
+    const int qd = a.n_q * kDH;
+    const int ns = o_ns;
+    // weights first: they wait for nothing.  Steps 0, 1 in o_w01, the rest in batches of 2.
+    if (finisher && ns > 0) gemv_issue_w<8, 2>(o_wt, 0, ns, o_w01);
+    const bf16_t* wt2[8];
 #pragma unroll
-    for (int ct = 0; ct < 8; ++ct) wt[ct] = a.wo + packed_frag(grp * 8 + ct, s_b, S) + lane * 8;
-    constexpr int U = 4;
+    for (int ct = 0; ct < 8; ++ct) wt2[ct] = o_wt[ct] + 2 * kPackStep;
+    constexpr int U = 2;
     i32x4 w0[U][8];
-    if (ns > 0) gemv_issue_w<8, U>(wt, 0, ns, w0);  // weights first: they wait for nothing
+    if (ns > 2) gemv_issue_w<8, U>(wt2, 0, ns - 2, w0);
+    long long old[4];
+    residual_old(a, grp, x, old);
     xcd_wait(a, xcd_ctr(a, x, kCtrMergeDone), kXcdWgs, a.layer * 16 + 3);
     {
       const int resets[3] = {kCtrQkvDone, kCtrAttnDone, kCtrMergeDone};
@@ -406,12 +433,18 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
 #pragma unroll
     for (int ct = 0; ct < 8; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int arow = r < a.M ? r : a.M - 1;
-    gemv_stream<8, U, kPolicyL2, true>(buf_rsrc(a.attn), buf_rsrc(a.attn_lo),
-                                       (uint32_t)(((int64_t)arow * qd + g4 * 8 + s_b * 32) * 2), wt, ns, w0, acc);
+    const __amdgpu_buffer_rsrc_t ra = buf_rsrc(a.attn), ral = buf_rsrc(a.attn_lo);
+    const uint32_t a_off = (uint32_t)(((int64_t)arow * qd + g4 * 8 + o_sb * 32) * 2);
+    if (ns > 0) {
+      i32x4 xa[2], xl[2];
+      gemv_issue_a<2, kPolicyL2>(ra, ral, a_off, 0, ns, xa, xl);
+      gemv_mfma<8, 2>(o_w01, xa, xl, 0, ns, acc);
+    }
+    if (ns > 2) gemv_stream<8, U, kPolicyL2, true>(ra, ral, a_off + 2 * 64, wt2, ns - 2, w0, acc);
     reduce_waves<8>(acc, smem);
-    dev_read_wait(a, a.layer * 16 + 4);
-    residual_add(a, grp, acc);
+    residual_add(a, grp, x, acc, old);
   }
+  if (n_idle == 0) residual_zero(a, blockIdx.x, gridDim.x);
 }
 
 template <int CG>
@@ -435,9 +468,8 @@ __global__ __launch_bounds__(256) void layer_mlp_kernel(LayerXArgs a) {
 #pragma unroll
     for (int ct = 0; ct < CG; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
     float ss = 0.f;  // the whole row passes through the 4 waves: its sum of x^2 for the RMSNorm
-    gemv_stream_x64<CG, 1>(buf_rsrc(a.x64), buf_rsrc(a.g_mlp), (uint32_t)(((int64_t)arow * a.d + g4 * 8 + s_b * 32) * 8),
+    gemv_stream_x64<CG, 1>(buf_rsrc(a.x_src), buf_rsrc(a.g_mlp), (uint32_t)(((int64_t)arow * a.d + g4 * 8 + s_b * 32) * 8),
                            (uint32_t)((g4 * 8 + s_b * 32) * 2), wt, ns, acc, ss);
-    dev_read_done(a);
     row_ss_reduce(r < a.M ? ss : 0.f, ss_s, ss_s + 64);
     float* rinv_s = ss_s + 64;
     if (threadIdx.x < 16) rinv_s[threadIdx.x] = 1.0f / sqrtf(rinv_s[threadIdx.x] / (float)a.d + a.eps);
@@ -473,6 +505,8 @@ __global__ __launch_bounds__(256) void layer_mlp_kernel(LayerXArgs a) {
     constexpr int U = 2;
     i32x4 w0[U][8];
     if (ns > 0) gemv_issue_w<8, U>(wt, 0, ns, w0);  // weights first: they wait for nothing
+    long long old[4];
+    residual_old(a, grp, x, old);
     xcd_wait(a, xcd_ctr(a, x, kCtrGuDone), kXcdWgs, a.layer * 16 + 5);
     {
       const int resets[1] = {kCtrGuDone};
@@ -485,30 +519,37 @@ __global__ __launch_bounds__(256) void layer_mlp_kernel(LayerXArgs a) {
     gemv_stream<8, U, kPolicyL2, true>(buf_rsrc(a.act), buf_rsrc(a.act_lo),
                                        (uint32_t)(((int64_t)arow * a.ffn + g4 * 8 + s_b * 32) * 2), wt, ns, w0, acc);
     reduce_waves<8>(acc, smem);
-    dev_read_wait(a, a.layer * 16 + 6);
-    residual_add(a, grp, acc);
+    residual_add(a, grp, x, acc, old);
   }
+  // the next launch's residual buffer, zeroed last: nothing here waits for these stores
+  residual_zero(a, blockIdx.x, gridDim.x);
 }
 
-// After the last layer: the LM head's inputs from the fixed-point residual.  Workgroup m
-// takes row m; thread t its 16 columns 16 t .. 16 t + 15.
+// After the last layer: the LM head's inputs from the fixed-point residual.  Row m =
+// blockIdx.x, columns 1024 blockIdx.y + 4 t .. + 3 for thread t.
 __global__ __launch_bounds__(256) void layer_finalize_kernel(FinalizeArgs a) {
   const int m = blockIdx.x;
-  for (int c0 = threadIdx.x * 16; c0 < a.d; c0 += 256 * 16) {
-    float s = 0.f;
+  const int c = (blockIdx.y * 256 + threadIdx.x) * 4;
+  if (c >= a.d) return;  // d % 16 == 0: a 16-column group lies inside or outside as a whole
+  const int64_t o = (int64_t)m * a.d + c;
+  const longlong2 q0 = *reinterpret_cast<const longlong2*>(a.x64 + o);
+  const longlong2 q1 = *reinterpret_cast<const longlong2*>(a.x64 + o + 2);
+  const uint2 gv = *reinterpret_cast<const uint2*>(a.g + c);
+  const long long q[4] = {q0.x, q0.y, q1.x, q1.y};
+  float v[4];
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int64_t v = a.x64[(int64_t)m * a.d + c0 + e];
-      const float xv = fix_to_f32((int)(uint32_t)(uint64_t)v, (int)(v >> 32));
-      a.x[(int64_t)m * a.d + c0 + e] = xv;
-      bf16_t hi, lo;
-      split_bf16(xv * bf2f(a.g[c0 + e]), hi, lo);
-      a.xn[(int64_t)m * a.d + c0 + e] = hi;
-      a.xn_lo[(int64_t)m * a.d + c0 + e] = lo;
-      s += xv * xv;
-    }
-    a.sumsq[(int64_t)m * (a.d / 16) + c0 / 16] = s;
-  }
+  for (int e = 0; e < 4; ++e) v[e] = fix_to_f32((int)(uint32_t)(uint64_t)q[e], (int)(q[e] >> 32));
+  *reinterpret_cast<float4*>(a.x + o) = float4{v[0], v[1], v[2], v[3]};
+  const f32x4 xg = f32x4{v[0] * __uint_as_float(gv.x << 16), v[1] * __uint_as_float(gv.x & 0xffff0000u),
+                         v[2] * __uint_as_float(gv.y << 16), v[3] * __uint_as_float(gv.y & 0xffff0000u)};
+  i32x2 hi, lo;
+  split_bf16x4(xg, hi, lo);
+  *reinterpret_cast<i32x2*>(a.xn + o) = hi;
+  *reinterpret_cast<i32x2*>(a.xn_lo + o) = lo;
+  float s = v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+  s += __shfl_xor(s, 1);
+  s += __shfl_xor(s, 2);
+  if ((threadIdx.x & 3) == 0) a.sumsq[(int64_t)m * (a.d / 16) + c / 16] = s;
 }
 
 bool layer_xcd_fits(const sbd_model_config& c, int n_cu, int B, int k) {
@@ -520,7 +561,7 @@ bool layer_xcd_fits(const sbd_model_config& c, int n_cu, int B, int k) {
   if (c.ffn_dim % (kXcds * kXcdWgs * 8) != 0) return false;
   const int cg = c.ffn_dim / (kXcds * kXcdWgs * 8);
   if (cg < 6 || cg > 8) return false;
-  if (B < 1 || k < 1 || B * k > 16 || G * k > kLxRows || B > kLxAttnTasks) return false;
+  if (B < 1 || k < 1 || B * k > kLxMaxRows || G * k > kLxRows || B > kLxAttnTasks) return false;
   if ((B * G * k + 3) / 4 > kXcdWgs) return false;  // one wave per merged row
   return true;
 }
@@ -531,8 +572,8 @@ hipError_t launch_layer_attn(const LayerXArgs& a, const Exec& ex) {
 }
 
 hipError_t launch_layer_finalize(const FinalizeArgs& a, const Exec& ex) {
-  if (a.d % (16 * 256) != 0) return hipErrorInvalidValue;
-  SBD_KLAUNCH(layer_finalize_kernel, dim3(a.M), dim3(256), ex, a);
+  if (a.d % 16 != 0) return hipErrorInvalidValue;
+  SBD_KLAUNCH(layer_finalize_kernel, dim3(a.M, (a.d + 1023) / 1024), dim3(256), ex, a);
   return hipGetLastError();
 }
 

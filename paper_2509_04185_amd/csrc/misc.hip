@@ -21,30 +21,45 @@ __device__ __forceinline__ int64_t kv_head_base(int layer, int slot, int g, int 
   return (((int64_t)layer * n_slots + slot) * n_kv + g) * cap * d_h;
 }
 
-// One workgroup per row m: x[m] = E[tok[m]] (fp32), xn[m] = x * g as hi/lo bf16,
+// Row m = blockIdx.x, columns 1024 blockIdx.y + 4 t .. + 3 for thread t (every load of a
+// thread is issued at once): x[m] = E[tok[m]] (fp32), xn[m] = x * g as hi/lo bf16,
 // sumsq[m][c/16] = sum over each 16 columns of x^2 (the consumer forms 1/rms).
 __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
   const int m = blockIdx.x;
+  const int c = (blockIdx.y * 256 + threadIdx.x) * 4;
+  if (c >= a.d) return;  // d % 16 == 0: a 16-column group lies inside or outside as a whole
   const int tok = a.rows[m].tok;
-  for (int c = threadIdx.x; c < a.d; c += 256) {
-    const float v = bf2f(a.embed[(int64_t)tok * a.d + c]);
-    a.x[(int64_t)m * a.d + c] = v;
-    if (a.x64 != nullptr) a.x64[(int64_t)m * a.d + c] = __double2ll_rn((double)v * 4294967296.0);
-    bf16_t hi, lo;
-    split_bf16(v * bf2f(a.g[c]), hi, lo);
-    a.xn[(int64_t)m * a.d + c] = hi;
-    a.xn_lo[(int64_t)m * a.d + c] = lo;
-    float s = v * v;
-    s += __shfl_xor(s, 8);
-    s += __shfl_xor(s, 4);
-    s += __shfl_xor(s, 2);
-    s += __shfl_xor(s, 1);
-    if ((threadIdx.x & 15) == 0) a.sumsq[(int64_t)m * (a.d / 16) + c / 16] = s;
+  const uint2 ev = *reinterpret_cast<const uint2*>(a.embed + (int64_t)tok * a.d + c);
+  const uint2 gv = *reinterpret_cast<const uint2*>(a.g + c);
+  const float v[4] = {__uint_as_float(ev.x << 16), __uint_as_float(ev.x & 0xffff0000u),
+                      __uint_as_float(ev.y << 16), __uint_as_float(ev.y & 0xffff0000u)};
+  const float g[4] = {__uint_as_float(gv.x << 16), __uint_as_float(gv.x & 0xffff0000u),
+                      __uint_as_float(gv.y << 16), __uint_as_float(gv.y & 0xffff0000u)};
+  const int64_t o = (int64_t)m * a.d + c;
+  *reinterpret_cast<float4*>(a.x + o) = float4{v[0], v[1], v[2], v[3]};
+  if (a.x64 != nullptr) {
+    long long q[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) q[e] = __double2ll_rn((double)v[e] * 4294967296.0);
+    *reinterpret_cast<longlong2*>(a.x64 + o) = longlong2{q[0], q[1]};
+    *reinterpret_cast<longlong2*>(a.x64 + o + 2) = longlong2{q[2], q[3]};
+    *reinterpret_cast<longlong2*>(a.x64_zero + o) = longlong2{0, 0};
+    *reinterpret_cast<longlong2*>(a.x64_zero + o + 2) = longlong2{0, 0};
   }
+  const f32x4 xg = f32x4{v[0] * g[0], v[1] * g[1], v[2] * g[2], v[3] * g[3]};
+  i32x2 hi, lo;
+  split_bf16x4(xg, hi, lo);
+  *reinterpret_cast<i32x2*>(a.xn + o) = hi;
+  *reinterpret_cast<i32x2*>(a.xn_lo + o) = lo;
+  float s = v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+  s += __shfl_xor(s, 1);
+  s += __shfl_xor(s, 2);
+  if ((threadIdx.x & 3) == 0) a.sumsq[(int64_t)m * (a.d / 16) + c / 16] = s;
 }
 
 hipError_t launch_embed(const EmbedArgs& a, const Exec& ex) {
-  SBD_KLAUNCH(embed_kernel, dim3(a.M), dim3(256), ex, a);
+  if (a.d % 16 != 0) return hipErrorInvalidValue;
+  SBD_KLAUNCH(embed_kernel, dim3(a.M, (a.d + 1023) / 1024), dim3(256), ex, a);
   return hipGetLastError();
 }
 

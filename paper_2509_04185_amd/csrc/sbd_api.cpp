@@ -107,7 +107,7 @@ bool sbd::compute_layout(const sbd_model_config& c, Layout* L) {
   o.fwd_ctl = take(o.fwd_ctl_ints * sizeof(int32_t));
   o.fwd_err = take(2 * sizeof(int32_t));
   o.lx_part = take(kLxPartFloats * sizeof(float));
-  o.x64 = take(o.m_max * c.d_model * sizeof(int64_t));
+  o.x64 = take(3 * kLxMaxRows * (int64_t)c.d_model * sizeof(int64_t));  // three residual buffers
   o.counters = take((int64_t)kCounters * sizeof(int32_t));
   o.total = off;
   *L = o;
@@ -318,8 +318,11 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   if (st) return st;
   st = upload(c, c->ws + L.seqs, seqs.data(), seqs.size() * sizeof(SeqParam));
   if (st) return st;
+  // the per-XCD layer kernels' residual buffers R0, R1, R2 (kLxMaxRows rows each)
+  int64_t* xr[3];
+  for (int i = 0; i < 3; ++i) xr[i] = c->at<int64_t>(L.x64) + (int64_t)i * kLxMaxRows * d;
   EmbedArgs ea{drows, M, d, c->embed, c->layers[0].attn_norm, x, xn, xn_lo, sumsq,
-               layers_fit ? c->at<int64_t>(L.x64) : nullptr};
+               layers_fit ? xr[0] : nullptr, layers_fit ? xr[1] : nullptr};
   SBD_LAUNCH(c, SBD_KERNEL_EMBED, launch_embed(ea, ex));
   if (fused) {
     SBD_HIP(c, hipMemsetAsync(f.ctl, 0, (size_t)f.plan.n_ctl * sizeof(int32_t), c->stream));
@@ -345,7 +348,6 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     lx.qk_norm = m.qk_norm; lx.eps = m.rms_eps;
     lx.q_scale = (float)(1.4426950408889634 / std::sqrt((double)dh));
     lx.n_tasks = kXcdWgs / B;
-    lx.x64 = c->at<int64_t>(L.x64);
     lx.q = q; lx.q_lo = q_lo; lx.attn = attn; lx.attn_lo = attn_lo; lx.act = act; lx.act_lo = act_lo;
     lx.kcache = c->at<bf16_t>(L.kcache); lx.vcache = c->at<bf16_t>(L.vcache); lx.cap = L.cap;
     lx.n_slots = m.max_batch; lx.rope = c->at<float>(L.rope); lx.rows = drows; lx.seqs = dseqs;
@@ -358,11 +360,14 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
       lx.layer = l;
       lx.wqkv = wp; lx.wo = wp + L.wp_o; lx.wgu = wp + L.wp_gu; lx.wdown = wp + L.wp_down;
       lx.q_norm = w.q_norm; lx.k_norm = w.k_norm; lx.g_attn = w.attn_norm; lx.g_mlp = w.mlp_norm;
+      // launch i = 2 l + h reads R[i % 3], adds into R[(i + 1) % 3], zeroes R[(i + 2) % 3]
+      lx.x_src = xr[(2 * l) % 3]; lx.x_dst = xr[(2 * l + 1) % 3]; lx.x_zero = xr[(2 * l + 2) % 3];
       SBD_LAUNCH(c, SBD_KERNEL_LAYER_ATTN, launch_layer_attn(lx, ex));
+      lx.x_src = xr[(2 * l + 1) % 3]; lx.x_dst = xr[(2 * l + 2) % 3]; lx.x_zero = xr[(2 * l + 3) % 3];
       SBD_LAUNCH(c, SBD_KERNEL_LAYER_MLP, launch_layer_mlp(lx, ex));
     }
     // the LM head's inputs (and the fp32 residual) from the fixed-point residual
-    FinalizeArgs fa{M, d, lx.x64, c->final_norm, x, xn, xn_lo, sumsq};
+    FinalizeArgs fa{M, d, xr[(2 * m.n_layers) % 3], c->final_norm, x, xn, xn_lo, sumsq};
     SBD_LAUNCH(c, SBD_KERNEL_LAYER_FINAL, launch_layer_finalize(fa, ex));
     n_part_cur = d / 16;
   }

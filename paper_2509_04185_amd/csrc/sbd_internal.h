@@ -199,7 +199,8 @@ struct EmbedArgs {
   bf16_t* xn;
   bf16_t* xn_lo;
   float* sumsq;  // [M][d/16]
-  int64_t* x64;  // the same rows as fixed point (x * 2^32) for the per-XCD layer kernels, or null
+  int64_t* x64;       // the same rows as fixed point (x * 2^32) for the per-XCD layer kernels, or null
+  int64_t* x64_zero;  // with x64: the buffer the first layer kernel adds into, zeroed here
 };
 hipError_t launch_embed(const EmbedArgs& a, const Exec& ex);
 
@@ -335,6 +336,7 @@ constexpr int kLxQkvSlice = 2048 + 16;                    // parked QKV slice: 8
 constexpr int kLxQkvFloats = kXcdWgs * kLxQkvSlice;       // per XCD: parked QKV slices
 constexpr int kLxAttnTasks = kXcdWgs;                     // attention tasks per XCD at most
 constexpr int kLxRows = 64;                               // query rows per KV head at most
+constexpr int kLxMaxRows = 16;                            // block rows (batch x k) of a forward at most
 constexpr int64_t kLxXcdFloats = kLxQkvFloats + (int64_t)kLxAttnTasks * kLxRows * (128 + 2);
 constexpr int64_t kLxPartFloats = (int64_t)kXcds * kLxXcdFloats;  // XCD-local partials
 constexpr int kLxCtrLines = kXcds * 64 + 2;               // counter lines (kCtrStride words each)
@@ -352,7 +354,9 @@ struct LayerXArgs {
   const bf16_t *q_norm, *k_norm;           // Qwen-3 per-head gains (qk_norm)
   const bf16_t* g_attn;              // attention norm gain of the layer
   const bf16_t* g_mlp;               // MLP norm gain of the layer
-  int64_t* x64;                      // residual stream [M][d], fixed point
+  const int64_t* x_src;              // residual stream [M][d], fixed point: read by this launch
+  int64_t* x_dst;                    // the residual after this launch: zero on entry, atomics add into it
+  int64_t* x_zero;                   // the third buffer: zeroed for the next launch
   bf16_t *q, *q_lo, *attn, *attn_lo, *act, *act_lo;
   bf16_t *kcache, *vcache;
   int64_t cap;
