@@ -54,7 +54,7 @@ struct MidCfg {
   static constexpr int NS = (144 * 1024) / STAGE > 8 ? 8 : (144 * 1024) / STAGE;  // ring stages
   static constexpr int FPW = (NT + 2 * MT) / 4;       // fragments each wave loads per stage
   static_assert(MTW >= 1 && (NT + 2 * MT) % 4 == 0, "unsupported tile shape");
-  static_assert((NS - 2) * FPW <= 63, "vmcnt range");
+  static_assert((NS - 1) * FPW <= 63, "vmcnt range");
 };
 
 // f(std::integral_constant<int, 0>{}), ..., f(std::integral_constant<int, N - 1>{})
@@ -163,24 +163,28 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
   // every read of LDS with a wait for all direct loads in flight (it cannot tell the ring
   // slots apart), draining the ring at each step.  Ordering is explicit instead: the stage
   // barrier before the reads, lds_wait() after them, and the results pinned behind it.
+  // The reads of stage c + 1 are issued before the MFMAs of stage c (two register sets), so
+  // the LDS traffic of one step overlaps the matrix work of the previous one.
   const uint32_t lds_w = (uint32_t)(uintptr_t)smem + (uint32_t)(wc * CW * 1024 + lane * 16);
   const uint32_t lds_a = (uint32_t)(uintptr_t)smem + (uint32_t)(WB + wm * MTW * 2048 + lane * 16);
-  auto compute = [&](int st) {
+  auto read_frags = [&](int st, i32x4 (&wv)[CW], i32x4 (&av)[MTW][2]) {
     const uint32_t sb = (uint32_t)((st % NS) * STAGE);
     const uint32_t aw = lds_w + sb, aa = lds_a + sb;
-    i32x4 wv[CW], av[MTW][2];
     static_for<CW>([&](auto I) { wv[decltype(I)::value] = ds_read16<decltype(I)::value * 1024>(aw); });
     static_for<MTW * 2>([&](auto I) {
       constexpr int i = decltype(I)::value;
       av[i / 2][i % 2] = ds_read16<i * 1024>(aa);
     });
-    lds_wait();
+  };
+  auto pin_frags = [&](i32x4 (&wv)[CW], i32x4 (&av)[MTW][2]) {
 #pragma unroll
     for (int cw = 0; cw < CW; ++cw) lds_pin(wv[cw]);
 #pragma unroll
     for (int mw = 0; mw < MTW; ++mw)
 #pragma unroll
       for (int h = 0; h < 2; ++h) lds_pin(av[mw][h]);
+  };
+  auto mfma_frags = [&](const i32x4 (&wv)[CW], const i32x4 (&av)[MTW][2]) {
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
@@ -208,14 +212,35 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
 
   // A kernel's code runs cold from the instruction cache in every workgroup: the ring is
   // driven by compact loops (slot = stage % NS at run time) rather than unrolled code.
+  // NS stages in flight: stage c's slot is refilled once every wave holds its fragments.
 #pragma unroll 1
-  for (int st = 0; st < NS - 1 && st < nst; ++st) issue(st);
+  for (int st = 0; st < NS && st < nst; ++st) issue(st);
+  i32x4 wv0[CW], av0[MTW][2], wv1[CW], av1[MTW][2];
+  vm_wait_stages<FPW, NS - 1>(min(NS - 1, nst - 1));  // stage 0 has landed (this wave's part)
+  stage_barrier();                                    // ... and every wave's
+  read_frags(0, wv0, av0);
+  lds_wait();
+  pin_frags(wv0, av0);
+  // step c: the fragments of stage c are in registers; stage c + 1 is read meanwhile
+  auto step = [&](int c, i32x4 (&wc_)[CW], i32x4 (&ac_)[MTW][2], i32x4 (&wn)[CW], i32x4 (&an)[MTW][2]) {
+    if (c + 1 < nst) {
+      vm_wait_stages<FPW, NS - 2>(min(NS - 2, nst - 2 - c));  // stage c + 1 has landed (this wave's part)
+      stage_barrier();  // ... and every wave's; every wave holds stage c's fragments: its slot is free
+      if (c + NS < nst) issue(c + NS);
+      read_frags(c + 1, wn, an);
+    }
+    // the MFMAs stay between the reads and their wait (they do not touch memory, so the
+    // compiler would otherwise move them past the wait)
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_frags(wc_, ac_);
+    __builtin_amdgcn_sched_barrier(0);
+    lds_wait();
+    pin_frags(wn, an);
+  };
 #pragma unroll 1
-  for (int c = 0; c < nst; ++c) {
-    vm_wait_stages<FPW, NS - 2>(min(NS - 2, nst - 1 - c));  // stage c has landed (this wave's part)
-    stage_barrier();                                         // ... and every wave's; stage c - 1 is free
-    if (c + NS - 1 < nst) issue(c + NS - 1);
-    compute(c);
+  for (int c = 0; c < nst; c += 2) {
+    step(c, wv0, av0, wv1, av1);
+    if (c + 1 < nst) step(c + 1, wv1, av1, wv0, av0);
   }
 
   // ---- K split over workgroups: park the slice, the last to arrive adds all in order
