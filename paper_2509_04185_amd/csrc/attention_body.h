@@ -353,17 +353,17 @@ __device__ __forceinline__ void attn_merge_body(const AttnArgs& a, int64_t item)
   const float inv = 1.0f / lsum;
   const int64_t orow = item / a.n_q;
   const int hq = (int)(item % a.n_q);
-  const int64_t dst = orow * (int64_t)a.n_q * DH + (int64_t)hq * DH;
 #pragma unroll
   for (int e = 0; e < PER; ++e) {
     bf16_t hi, lo;
     split_bf16(acc[e] * inv, hi, lo);
+    const int64_t dst = aoff(orow, (int64_t)hq * DH + lane + 64 * e, (int64_t)a.n_q * DH, a.out_mtiles);
     if constexpr (DEV) {
-      st_bf16_dev(a.out + dst + lane + 64 * e, hi);
-      st_bf16_dev(a.out_lo + dst + lane + 64 * e, lo);
+      st_bf16_dev(a.out + dst, hi);
+      st_bf16_dev(a.out_lo + dst, lo);
     } else {
-      a.out[dst + lane + 64 * e] = hi;
-      a.out_lo[dst + lane + 64 * e] = lo;
+      a.out[dst] = hi;
+      a.out_lo[dst] = lo;
     }
   }
 }

@@ -135,8 +135,13 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
       int row = row0 + (ai >> 1) * 16 + r;
       if (row >= a.M) row = a.M - 1;  // rows past the end: valid data, results discarded
       const bf16_t* base = (ai & 1) ? a.A_lo : a.A;
-      src[u] = (const char*)(base + (int64_t)row * a.lda + (int64_t)s_b * 32 + g * 8);
-      stride[u] = 64;
+      if (a.a_mtiles) {  // fragment order: one contiguous 1 KB per fragment
+        src[u] = (const char*)(base + apack(a.a_row0 + row, (int64_t)s_b * 32 + g * 8, a.a_mtiles));
+        stride[u] = (int64_t)a.a_mtiles * 1024;
+      } else {
+        src[u] = (const char*)(base + (int64_t)row * a.lda + (int64_t)s_b * 32 + g * 8);
+        stride[u] = 64;
+      }
     }
   }
   // stage st into ring slot st % NS
@@ -356,7 +361,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
           }
           i32x2 hi, lo;
           split_bf16x4(y, hi, lo);
-          const int64_t o = (int64_t)m * a.ld_act + (t0 + wc * CW + tt) * 8 + h * 4;
+          const int64_t o = aoff(m, (int64_t)(t0 + wc * CW + tt) * 8 + h * 4, a.ld_act, a.o_mtiles);
           *(i32x2*)(a.act + o) = hi;
           *(i32x2*)(a.act_lo + o) = lo;
         }
@@ -383,8 +388,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
             xg[3] = xv[3] * __uint_as_float((uint32_t)gw[1] & 0xffff0000u);
             i32x2 hi, lo;
             split_bf16x4(xg, hi, lo);
-            *(i32x2*)(a.xn + (int64_t)m * a.ldx + n) = hi;
-            *(i32x2*)(a.xn_lo + (int64_t)m * a.ldx + n) = lo;
+            const int64_t on = aoff(m, n, a.ldx, a.o_mtiles);
+            *(i32x2*)(a.xn + on) = hi;
+            *(i32x2*)(a.xn_lo + on) = lo;
             s2 = (xv[0] * xv[0] + xv[1] * xv[1]) + (xv[2] * xv[2] + xv[3] * xv[3]);
           }
 #pragma unroll

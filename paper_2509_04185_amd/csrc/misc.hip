@@ -49,8 +49,9 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
   const f32x4 xg = f32x4{v[0] * g[0], v[1] * g[1], v[2] * g[2], v[3] * g[3]};
   i32x2 hi, lo;
   split_bf16x4(xg, hi, lo);
-  *reinterpret_cast<i32x2*>(a.xn + o) = hi;
-  *reinterpret_cast<i32x2*>(a.xn_lo + o) = lo;
+  const int64_t on = aoff(m, c, a.d, a.mtiles);  // 4 consecutive columns stay contiguous
+  *reinterpret_cast<i32x2*>(a.xn + on) = hi;
+  *reinterpret_cast<i32x2*>(a.xn_lo + on) = lo;
   float s = v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
   s += __shfl_xor(s, 1);
   s += __shfl_xor(s, 2);

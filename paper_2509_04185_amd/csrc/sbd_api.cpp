@@ -54,6 +54,7 @@ bool sbd::compute_layout(const sbd_model_config& c, Layout* L) {
   Layout o{};
   o.cap = ((int64_t)c.max_seq_len + 63) / 64 * 64;
   o.m_max = std::max<int64_t>((int64_t)c.max_batch * c.max_block, effective_chunk(c));
+  o.m_max = (o.m_max + 15) / 16 * 16;  // whole row tiles: fragment-order activations
   o.n_qkv = (int64_t)(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
   o.n_part = c.d_model / 16;
   o.eb_chunks = (c.vocab + kEbChunk - 1) / kEbChunk;
@@ -273,6 +274,8 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   const int n_rb = (G * k + 63) / 64;
   const int nblocks = (max_end + 31) / 32;
   const bool small = M <= 16;  // decode-sized forward
+  // forwards of more than 16 rows keep the GEMMs' activation operands in fragment order
+  const int mt = small ? 0 : (M + 15) / 16;
 
   // The fused decode forward: checked before anything is enqueued.
   const bool fused = small && c->decode_path == SBD_DECODE_FUSED;
@@ -321,7 +324,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   // the per-XCD layer kernels' residual buffers R0, R1, R2 (kLxMaxRows rows each)
   int64_t* xr[3];
   for (int i = 0; i < 3; ++i) xr[i] = c->at<int64_t>(L.x64) + (int64_t)i * kLxMaxRows * d;
-  EmbedArgs ea{drows, M, d, c->embed, c->layers[0].attn_norm, x, xn, xn_lo, sumsq,
+  EmbedArgs ea{drows, M, d, c->embed, c->layers[0].attn_norm, x, xn, xn_lo, sumsq, mt,
                layers_fit ? xr[0] : nullptr, layers_fit ? xr[1] : nullptr};
   SBD_LAUNCH(c, SBD_KERNEL_EMBED, launch_embed(ea, ex));
   if (fused) {
@@ -389,6 +392,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
       SBD_LAUNCH(c, SBD_KERNEL_QKV, launch_gemv(EPI_QKV, v, GemvShape{}, ex));
     } else {
       GemmArgs g = gemm_base(xn, xn_lo, d, M, d, wp, (int)(L.n_qkv / 16), vpart, vpart_cap, counters);
+      g.a_mtiles = mt;
       g.out_f32 = qkv; g.ldo = L.n_qkv;
       g.sumsq_in = sumsq; g.n_part = n_part_cur; g.inv_d = 1.0f / d; g.eps = m.rms_eps;
       SBD_LAUNCH(c, SBD_KERNEL_QKV, launch_gemm(EPI_SCALED_STORE, g, ex));
@@ -408,6 +412,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     aa.n_rowblocks = n_rb; aa.n_splits = n_splits; aa.blocks_per_split = bps;
     aa.part_ml = c->at<float>(L.attn_ml); aa.part_o = c->at<float>(L.attn_o); aa.out = attn;
     aa.out_lo = attn_lo;
+    aa.out_mtiles = mt;
     SBD_LAUNCH(c, SBD_KERNEL_ATTENTION, launch_attention_split(aa, ex));
     SBD_LAUNCH(c, SBD_KERNEL_ATTN_MERGE, launch_attention_merge(aa, ex));
 
@@ -418,6 +423,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
       SBD_LAUNCH(c, SBD_KERNEL_O_PROJ, launch_gemv(EPI_RESID, v, GemvShape{}, ex));
     } else {
       GemmArgs go = gemm_base(attn, attn_lo, qd, M, qd, wp + L.wp_o, d / 16, vpart, vpart_cap, counters);
+      go.a_mtiles = mt; go.o_mtiles = mt;
       go.x = x; go.ldx = d; go.xn = xn; go.xn_lo = xn_lo; go.g_next = w.mlp_norm; go.sumsq_out = sumsq;
       go.n_part_out = gemm_plan(M, d / 16, qd, vpart_cap).n_cb;
       n_part_cur = go.n_part_out;
@@ -437,12 +443,14 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
       SBD_LAUNCH(c, SBD_KERNEL_DOWN, launch_gemv(EPI_RESID, vd, GemvShape{}, ex));
     } else {
       GemmArgs gu = gemm_base(xn, xn_lo, d, M, d, wp + L.wp_gu, m.ffn_dim / 8, vpart, vpart_cap, counters);
+      gu.a_mtiles = mt; gu.o_mtiles = mt;
       gu.sumsq_in = sumsq; gu.n_part = n_part_cur; gu.inv_d = 1.0f / d; gu.eps = m.rms_eps;
       gu.act = act; gu.act_lo = act_lo; gu.ld_act = m.ffn_dim;
       SBD_LAUNCH(c, SBD_KERNEL_GATE_UP, launch_gemm(EPI_SWIGLU, gu, ex));
 
       GemmArgs gd = gemm_base(act, act_lo, m.ffn_dim, M, m.ffn_dim, wp + L.wp_down, d / 16, vpart, vpart_cap,
                               counters);
+      gd.a_mtiles = mt; gd.o_mtiles = mt;
       gd.x = x; gd.ldx = d; gd.xn = xn; gd.xn_lo = xn_lo; gd.g_next = g_after;
       gd.sumsq_out = sumsq;
       gd.n_part_out = gemm_plan(M, d / 16, m.ffn_dim, vpart_cap).n_cb;
@@ -454,7 +462,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   if (logits != nullptr) {
     const int r0 = lm_row < 0 ? 0 : lm_row;
     const int Ml = lm_row < 0 ? M : 1;
-    if (Ml <= 16) {
+    if (mt == 0) {  // M <= 16: row-major inputs
       GemvArgs v = gemv_base(xn + (int64_t)r0 * d, xn_lo + (int64_t)r0 * d, d, Ml, d,
                              c->at<bf16_t>(L.wpack) + L.wp_lm, m.vocab / 16, vpart, vpart_cap, counters);
       v.sumsq_in = sumsq + (int64_t)r0 * n_part_cur; v.n_part_in = n_part_cur;
@@ -462,8 +470,10 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
       v.out_f32 = logits; v.ldo = m.vocab;
       SBD_LAUNCH(c, SBD_KERNEL_LM_HEAD, launch_gemv(EPI_SCALED_STORE, v, GemvShape{}, ex));
     } else {
-      GemmArgs gl = gemm_base(xn + (int64_t)r0 * d, xn_lo + (int64_t)r0 * d, d, Ml, d,
-                              c->at<bf16_t>(L.wpack) + L.wp_lm, m.vocab / 16, vpart, vpart_cap, counters);
+      // inputs in fragment order (also for one row of a prefill chunk: rows from a_row0)
+      GemmArgs gl = gemm_base(xn, xn_lo, d, Ml, d, c->at<bf16_t>(L.wpack) + L.wp_lm, m.vocab / 16, vpart,
+                              vpart_cap, counters);
+      gl.a_mtiles = mt; gl.a_row0 = r0;
       gl.out_f32 = logits; gl.ldo = m.vocab;
       gl.sumsq_in = sumsq + (int64_t)r0 * n_part_cur; gl.n_part = n_part_cur;
       gl.inv_d = 1.0f / d; gl.eps = m.rms_eps;

@@ -149,6 +149,20 @@ __device__ __forceinline__ void vm_wait() {
   __builtin_amdgcn_s_waitcnt(((N & 15) | ((N >> 4) << 14)) | (7 << 4) | (15 << 8));
 }
 
+// Activation matrices of forwards of more than 16 rows (the GEMM's A operands: normalised
+// residual, attention output, SwiGLU output) are stored in MFMA fragment order: the 1 KB
+// fragment of 16-row tile t and 32-column step s sits at (s * mtiles + t) KB and holds, for
+// lane (r, g) = (l % 16, l / 16), the 8 values of row 16 t + r, columns 32 s + 8 g .. + 8.
+// The GEMM then reads a fragment with one contiguous 1 KB load instead of 16 pieces of 64
+// bytes from 16 rows.  Element offset of (m, c) in such a matrix of `mtiles` row tiles:
+__device__ __forceinline__ int64_t apack(int64_t m, int64_t c, int mtiles) {
+  return ((((c >> 5) * mtiles + (m >> 4)) * 64 + ((c >> 3) & 3) * 16 + (m & 15)) << 3) + (c & 7);
+}
+// (m, c) in a row-major matrix of row stride ld (mtiles == 0) or in fragment order
+__device__ __forceinline__ int64_t aoff(int64_t m, int64_t c, int64_t ld, int mtiles) {
+  return mtiles ? apack(m, c, mtiles) : m * ld + c;
+}
+
 // LDS reads that the compiler does not see as such.  A kernel that fills LDS by direct
 // loads (global_load_lds) while reading another part of it would otherwise get a wait for
 // every direct load in flight before each LDS read (the compiler cannot tell the regions

@@ -99,10 +99,13 @@ struct QkvEpi {
 //
 // y[m][n] = sum_k A[m][k] * W[n][k] with W in the packed fragment order of gemm.hip.
 struct GemmArgs {
-  const bf16_t* A;     // hi part [M][K], row stride lda
+  const bf16_t* A;     // hi part [M][K], row stride lda (a_mtiles == 0) or fragment order
   const bf16_t* A_lo;  // lo part, same layout
   int64_t lda;
   int M, K;
+  int a_mtiles;        // A in fragment order with this many row tiles (0: row-major)
+  int a_row0;          // first row of A used (fragment order only)
+  int o_mtiles;        // xn (EPI_RESID) and act (EPI_SWIGLU) written in fragment order (0: row-major)
   const bf16_t* Wp;    // packed weights
   int n_tiles;         // 16-row tiles of the packed matrix (a multiple of 8)
   // EPI_SCALED_STORE: out[m][n] = rinv[m] * y (rinv = 1 when sumsq_in == nullptr)
@@ -199,6 +202,7 @@ struct EmbedArgs {
   bf16_t* xn;
   bf16_t* xn_lo;
   float* sumsq;  // [M][d/16]
+  int mtiles;    // xn, xn_lo in fragment order with this many row tiles (0: row-major)
   int64_t* x64;       // the same rows as fixed point (x * 2^32) for the per-XCD layer kernels, or null
   int64_t* x64_zero;  // with x64: the buffer the first layer kernel adds into, zeroed here
 };
@@ -257,8 +261,9 @@ struct AttnArgs {
   int blocks_per_split;  // 32-key blocks per split
   float* part_ml;   // [n_splits][B*k*n_q][2]
   float* part_o;    // [n_splits][B*k*n_q][d_h]
-  bf16_t* out;     // [B*k][n_q*d_h] hi
+  bf16_t* out;     // [B*k][n_q*d_h] hi (row-major, or fragment order when out_mtiles > 0)
   bf16_t* out_lo;  // lo
+  int out_mtiles;  // row tiles of the fragment-order output (0: row-major)
 };
 hipError_t launch_attention_split(const AttnArgs& a, const Exec& ex);
 hipError_t launch_attention_merge(const AttnArgs& a, const Exec& ex);
