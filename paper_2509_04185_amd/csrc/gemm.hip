@@ -46,7 +46,9 @@ namespace sbd {
 
 template <int MT, int NT>
 struct MidCfg {
-  static constexpr int WC = NT == 16 ? 4 : 2;  // waves across the column block
+  // waves across the column block: 2 x 2 waves (each reads half the activation and half the
+  // weight fragments of a stage from LDS: 16 KB per 16-tile stage, against 20 KB in a 4 x 1 split)
+  static constexpr int WC = 2;
   static constexpr int WM = 4 / WC;            // waves across the row block
   static constexpr int CW = NT / WC;           // tiles per wave
   static constexpr int MTW = MT / WM;          // row tiles per wave
@@ -441,7 +443,7 @@ GemmPlan gemm_plan(int M, int n_tiles, int K, int64_t part_cap) {
       const double a_bytes = (double)n_cb * mb * mt * 16 * K * 4;
       // the last arriver reads the slices in batches of ZB (fewer when a wave holds more
       // accumulators), one dependent round trip each
-      const int nacc = (nt == 16 ? mt : mt / 2) * 4;
+      const int nacc = (mt / 2) * (nt / 2);  // accumulator tiles per wave (2 x 2 waves)
       const int zb = nacc >= 32 ? 1 : (nacc >= 16 ? 2 : 4);
       const double reduce = ks > 1 ? 1e-6 + 0.6e-6 * ((ks + zb - 1) / zb) : 0.0;
       const double cost = rounds * std::max(w_time, m_time) + 0.5 * part_bytes / 8e12 + a_bytes / 32e12 + reduce;
