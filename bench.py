@@ -115,6 +115,80 @@ def cpu_baseline(wl, w_dev, lens, toks, gamma, min_seconds):
     return total / reps, {"reps": reps, "sample_s": total}
 
 
+def speedup_table(args):
+    """time(1), time(k), time(2k) of block forwards at the Llama-3.1-8B shape, and the wall-clock
+    speedup model of the paper's Sec. 4.2, speedup(l, k) = k time(1) / (time(2k) + (l - 1) time(k))
+    for a block of k tokens sampled in l forwards (NFE speedup k / l).
+
+    time(1): one causal row per sequence (next-token prediction); time(k): k prediction rows;
+    time(2k): the first forward of a block, the previous block's k tokens re-fed as causal rows
+    plus k new mask rows.  Caches hold synthetic K/V installed with sbd_kv_import (the timing
+    does not depend on their values).  Prints a markdown table on stderr and one JSON line.
+    """
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2509_04185_amd import Sbd
+
+    s = synth.LLAMA8B
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    k = 16
+    batches = (1, 4, 8)
+    lens = (2048, 16384)
+    print("[bench] speedup table: generating weights", file=sys.stderr, flush=True)
+    w = synth.make_weights(s, 1002, device=dev)
+    lib = Sbd(s, w, max_batch=max(batches), max_seq_len=max(lens) + 2 * k + 64, max_block=2 * k)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def fwd_ms(B, kk, nc):
+        toks, msk = synth.block_rows(1002, s, B, kk, n_causal=nc)
+        out = torch.empty((B, kk, s.vocab), dtype=torch.float32, device=dev)
+        ids = list(range(B))
+        ncs = [nc] * B
+        for _ in range(3):
+            lib.block_forward(ids, toks, is_mask=msk, n_causal=ncs, out=out)
+        torch.cuda.synchronize()
+        reps = []
+        for _ in range(args.steps):
+            e0.record()
+            lib.block_forward(ids, toks, is_mask=msk, n_causal=ncs, out=out)
+            e1.record()
+            torch.cuda.synchronize()
+            reps.append(e0.elapsed_time(e1))
+        return float(np.median(reps))
+
+    rows = []
+    for L in lens:
+        print(f"[bench] installing {max(batches)} caches of {L} tokens", file=sys.stderr, flush=True)
+        for b in range(max(batches)):
+            lib.reset(b)
+            kk_, vv_ = synth.make_kv(s, 1002, b, L, device=dev)
+            lib.kv_import(b, 0, kk_, vv_)
+            del kk_, vv_
+        for B in batches:
+            t1, tk, t2k = fwd_ms(B, 1, 1), fwd_ms(B, k, 0), fwd_ms(B, 2 * k, k)
+            sp = {nfe: k * t1 / (t2k + (k // nfe - 1) * tk) for nfe in (2, 4, 8)}
+            rows.append({"cache_len": L, "batch": B, "time_1_ms": round(t1, 4), "time_k_ms": round(tk, 4),
+                         "time_2k_ms": round(t2k, 4), "slowdown_k": round(tk / t1, 3),
+                         "slowdown_2k": round(t2k / t1, 3),
+                         "speedup": {f"nfe_{n}": round(v, 3) for n, v in sp.items()}})
+            print(f"[bench] L {L} B {B}: time(1) {t1:.3f} time({k}) {tk:.3f} time({2 * k}) {t2k:.3f} ms",
+                  file=sys.stderr, flush=True)
+    print(f"\n| cache | batch | time(1) ms | time({k}) ms | time({2 * k}) ms | time({k})/time(1) | "
+          f"time({2 * k})/time(1) | speedup, NFE 2 | NFE 4 | NFE 8 |", file=sys.stderr)
+    print("|---|---|---|---|---|---|---|---|---|---|", file=sys.stderr)
+    for r in rows:
+        sp = r["speedup"]
+        print(f"| {r['cache_len']} | {r['batch']} | {r['time_1_ms']} | {r['time_k_ms']} | {r['time_2k_ms']} | "
+              f"{r['slowdown_k']} | {r['slowdown_2k']} | {sp['nfe_2']} | {sp['nfe_4']} | {sp['nfe_8']} |",
+              file=sys.stderr)
+    print(json.dumps({"metric": "SBD block-forward time(1), time(k), time(2k) and speedup(l, k)", "k": k,
+                      "shape": s.name, "data": "synthetic (random-init weights, synthetic KV caches)",
+                      "rows": rows}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -126,11 +200,15 @@ def main():
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event pass")
     ap.add_argument("--decode-path", default="auto", choices=["auto", "fused", "kernels", "layers"],
                     help="kernels of decode-sized forwards (sbd_set_decode_path)")
+    ap.add_argument("--speedup-table", action="store_true",
+                    help="measure time(1), time(k), time(2k) and the paper's speedup(l, k) instead")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
               "(batch sharding across GPUs is a design note only).", file=sys.stderr)
         sys.exit(2)
+    if args.speedup_table:
+        return speedup_table(args)
 
     import numpy as np
     import torch
