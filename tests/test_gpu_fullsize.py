@@ -70,6 +70,12 @@ EXTRA = {
                                            prompt_lens=(2048,)), [0]),
     "llama8b_b2_ragged_k8": (synth.Workload("llama8b_b2_ragged_k8", synth.LLAMA8B, 1007, 2, 8, (0.5,),
                                             prompt_lens=(1500, 700)), [0, 1]),
+    # forwards of 32 and 48 rows: the GEMM for more than 16 rows with blocks of 2 and 4 row
+    # tiles (48 rows: the last block's fourth tile repeats row 47), activations in fragment order
+    "llama8b_b2_l1024_k16": (synth.Workload("llama8b_b2_l1024_k16", synth.LLAMA8B, 1009, 2, 16, (1.0,),
+                                            prompt_lens=(1024, 1024)), [1]),
+    "llama8b_b3_ragged_k16": (synth.Workload("llama8b_b3_ragged_k16", synth.LLAMA8B, 1010, 3, 16, (1.0,),
+                                             prompt_lens=(900, 1600, 300)), [2]),
 }
 
 
