@@ -336,6 +336,81 @@ def row_entropy(logits_row, mask_id: int) -> tuple:
     return math.log(Z) - S / Z, tok
 
 
+def row_confidence(logits_row, mask_id: int) -> float:
+    """Confidence of a masked row (App. B): the largest probability of softmax over the
+    vocabulary without the mask token, c = max_v p_v = e^0 / Z = 1 / Z with Z as in
+    row_entropy (float64)."""
+    l = np.asarray(logits_row, dtype=np.float32)
+    keep = np.ones(l.shape[0], dtype=bool)
+    if 0 <= mask_id < l.shape[0]:
+        keep[mask_id] = False
+    lv = l[keep]
+    t = lv.astype(np.float64) - np.float64(lv.max())
+    return 1.0 / np.exp(t).sum()
+
+
+# Selection rules of one sampling step (Sec. 2.2 and App. B).
+RULE_EB_ENTROPY, RULE_EB_CONFIDENCE, RULE_FACTOR = 0, 1, 2
+
+
+def select_from_stats(H: Sequence[float], conf: Sequence[float], masked_rows: Sequence[int], rule: int,
+                      threshold: float) -> List[int]:
+    """Rows to reveal under one of the three rules, given per-row entropies and confidences.
+
+    RULE_EB_ENTROPY: eq. (eb_sampler), threshold = gamma (eb_select_from_entropy).
+    RULE_EB_CONFIDENCE: App. B, EB-Sampler with the confidence error proxy: the masked rows
+      ordered by (confidence descending, row) as i_1..i_n; s is the largest r in [1, n] with
+      sum_{j<=r} H_{i_j} - max_{j<=r} H_{i_j} <= gamma (sum left to right in float64).
+    RULE_FACTOR: App. B, Factor parallel decoding: the same order; n is the largest r with
+      (r + 1) * (1 - c_{i_r}) < f, at least 1 (the printed condition lacks the 1 - c; see
+      the design notes).
+    Returns the revealed rows sorted by row.
+    """
+    if rule == RULE_EB_ENTROPY:
+        return eb_select_from_entropy(H, masked_rows, threshold)
+    order = sorted(masked_rows, key=lambda j: (-float(conf[j]), int(j)))
+    if not order:
+        return []
+    s = 1
+    if rule == RULE_EB_CONFIDENCE:
+        c = 0.0
+        top = -math.inf
+        for r, j in enumerate(order, start=1):
+            c = c + float(H[j])
+            top = max(top, float(H[j]))
+            if c - top <= threshold:
+                s = r
+    elif rule == RULE_FACTOR:
+        for r, j in enumerate(order, start=1):
+            if (r + 1) * (1.0 - float(conf[j])) < threshold:
+                s = r
+    else:
+        raise ValueError(f"unknown rule {rule}")
+    return sorted(int(j) for j in order[:s])
+
+
+def select(logits, is_mask, rule: int, threshold: float, mask_id: int) -> tuple:
+    """One sampling step under `rule` on a batch of blocks.  Returns (accepted, tokens, H,
+    conf): revealed rows (ascending), their argmax ids, and the entropies and confidences of
+    the masked rows (nan elsewhere)."""
+    logits = np.asarray(logits, dtype=np.float32)
+    is_mask = np.asarray(is_mask).astype(bool)
+    B, k, _ = logits.shape
+    accepted, tokens = [], []
+    H = np.full((B, k), np.nan)
+    C = np.full((B, k), np.nan)
+    for b in range(B):
+        rows = [j for j in range(k) if is_mask[b, j]]
+        toks = {}
+        for j in rows:
+            H[b, j], toks[j] = row_entropy(logits[b, j], mask_id)
+            C[b, j] = row_confidence(logits[b, j], mask_id)
+        acc = select_from_stats(H[b], C[b], rows, rule, threshold)
+        accepted.append(acc)
+        tokens.append([toks[j] for j in acc])
+    return accepted, tokens, H, C
+
+
 def eb_select_from_entropy(H: Sequence[float], masked_rows: Sequence[int], gamma: float) -> List[int]:
     """Eq. (eb_sampler): rows to reveal, given per-row entropies.
 

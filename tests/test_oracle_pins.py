@@ -344,6 +344,114 @@ def test_eb_select_on_logits():
             assert t == int(np.argmax(logits[b, j, : V - 1]))
 
 
+# ------------------------------------------------------------------ App. B selection rules
+
+
+def brute_confidence(row, mask_id):
+    """max_v p_v over the vocabulary without the mask token, by math.fsum over exp(l - max)."""
+    vals = [float(x) for i, x in enumerate(row) if i != mask_id]
+    m = max(vals)
+    return 1.0 / math.fsum(math.exp(v - m) for v in vals)
+
+
+def test_confidence_closed_forms_and_brute_force():
+    V = 1024
+    assert abs(O.row_confidence(np.zeros(V, np.float32), V - 1) - 1.0 / (V - 1)) < 1e-15
+    one = np.zeros(V, np.float32)
+    one[17] = 900.0
+    assert O.row_confidence(one, V - 1) == 1.0
+    two = np.full(V, -1000.0, np.float32)
+    two[5] = two[9] = 3.0
+    assert abs(O.row_confidence(two, V - 1) - 0.5) < 1e-15
+    m = np.zeros(8, np.float32)
+    m[7] = 50.0                                      # the mask column never counts
+    assert abs(O.row_confidence(m, 7) - 1.0 / 7) < 1e-15
+    rng = np.random.default_rng(33)
+    for _ in range(50):
+        row = (rng.normal(size=16) * rng.uniform(0.1, 10)).astype(np.float32)
+        assert abs(O.row_confidence(row, 15) - brute_confidence(row, 15)) < 1e-13
+
+
+def factor_brute(conf, rows, f):
+    """App. B, Factor decoding: order by confidence (ties: lower row first); the largest n
+    whose n-th confidence satisfies (n + 1)(1 - c) < f, at least one."""
+    order = sorted(rows, key=lambda j: (-conf[j], j))
+    n = 1
+    for cand in range(1, len(order) + 1):
+        if (cand + 1) * (1.0 - conf[order[cand - 1]]) < f:
+            n = cand
+    return sorted(order[:n]) if order else []
+
+
+def eb_conf_brute(H, conf, rows, gamma):
+    """App. B, eq. (eb_sampler_general) with the confidence order: the largest s with
+    sum_{j<=s} H - max_{j<=s} H <= gamma (math.fsum)."""
+    order = sorted(rows, key=lambda j: (-conf[j], j))
+    s = 1
+    for cand in range(1, len(order) + 1):
+        hs = [H[j] for j in order[:cand]]
+        if math.fsum(hs) - max(hs) <= gamma:
+            s = cand
+    return sorted(order[:s]) if order else []
+
+
+def test_factor_hand_examples():
+    # confidences by row; order (2, 0, 1, 3): (n + 1)(1 - c) = 0.02, 0.3, 1.6, 3.5
+    conf = [0.9, 0.6, 0.99, 0.3]
+    H = [0.5, 1.0, 0.05, 2.0]
+    rows = [0, 1, 2, 3]
+    assert O.select_from_stats(H, conf, rows, O.RULE_FACTOR, 0.01) == [2]    # none passes: one
+    assert O.select_from_stats(H, conf, rows, O.RULE_FACTOR, 0.5) == [0, 2]
+    assert O.select_from_stats(H, conf, rows, O.RULE_FACTOR, 2.0) == [0, 1, 2]
+    assert O.select_from_stats(H, conf, rows, O.RULE_FACTOR, 10.0) == [0, 1, 2, 3]
+    assert O.select_from_stats(H, [0.5, 0.5], [1, 0], O.RULE_FACTOR, 0.0) == [0]  # tie: lower row
+    assert O.select_from_stats(H, conf, [], O.RULE_FACTOR, 1.0) == []
+
+
+def test_eb_confidence_hand_examples():
+    # order by confidence: 0, 1, 2; sum - max of the prefixes: 0, 0.125, 0.5 (H dyadic)
+    conf = [0.9, 0.8, 0.7]
+    H = [0.5, 0.125, 0.375]
+    rows = [0, 1, 2]
+    assert O.select_from_stats(H, conf, rows, O.RULE_EB_CONFIDENCE, 0.0) == [0]
+    assert O.select_from_stats(H, conf, rows, O.RULE_EB_CONFIDENCE, 0.125) == [0, 1]
+    assert O.select_from_stats(H, conf, rows, O.RULE_EB_CONFIDENCE, 0.4999) == [0, 1]
+    assert O.select_from_stats(H, conf, rows, O.RULE_EB_CONFIDENCE, 0.5) == [0, 1, 2]
+    assert O.select_from_stats(H, conf, rows, O.RULE_EB_CONFIDENCE, math.inf) == [0, 1, 2]
+
+
+def test_selection_rules_match_brute_force():
+    rng = np.random.default_rng(34)
+    for _ in range(400):
+        k = int(rng.integers(1, 33))
+        H = list(rng.exponential(0.7, k))
+        conf = list(rng.uniform(0.0, 1.0, k))
+        if rng.random() < 0.3:                        # ties in confidence
+            conf = [round(c, 1) for c in conf]
+        rows = sorted(set(int(j) for j in rng.integers(0, k, int(rng.integers(1, k + 1)))))
+        f = float(rng.choice([0.0, 0.05, 0.3, 1.0, 3.0, 100.0]))
+        gamma = float(rng.choice([0.0, 0.1, 0.5, 2.0, math.inf]))
+        assert O.select_from_stats(H, conf, rows, O.RULE_FACTOR, f) == factor_brute(conf, rows, f)
+        assert O.select_from_stats(H, conf, rows, O.RULE_EB_CONFIDENCE, gamma) == eb_conf_brute(H, conf, rows, gamma)
+
+
+def test_confidence_rule_reduces_to_entropy_rule_when_the_orders_agree():
+    # rows sigma_j * z with one z: a larger scale gives a lower entropy and a higher
+    # confidence, so both rules see the same order and App. B's form equals eq. (eb_sampler)
+    rng = np.random.default_rng(35)
+    V = 64
+    for _ in range(40):
+        z = rng.normal(size=V)
+        sig = rng.permutation(np.geomspace(0.1, 8.0, 8))
+        logits = (sig[None, :, None] * z[None, None, :]).astype(np.float32)
+        is_mask = (rng.random((1, 8)) < 0.8).astype(np.uint8)
+        is_mask[0, 0] = 1
+        for gamma in (0.0, 0.3, 1.0, 3.0, math.inf):
+            a_ent, t_ent, _ = O.eb_select(logits, is_mask, gamma, V - 1)
+            a_conf, t_conf, _, _ = O.select(logits, is_mask, O.RULE_EB_CONFIDENCE, gamma, V - 1)
+            assert a_conf == a_ent and t_conf == t_ent
+
+
 # ------------------------------------------------------------------ planted mistakes
 # Each plants a plausible bug in the oracle and checks that one of the pins above fails.
 
@@ -407,6 +515,29 @@ def test_planted_entropy_with_mask_token_is_caught(monkeypatch):
     monkeypatch.setattr(O, "row_entropy", bad)
     with pytest.raises(AssertionError):
         test_entropy_closed_forms()
+
+
+def test_planted_factor_without_one_minus_is_caught(monkeypatch):
+    # the condition as printed in App. B, (n + 1) c < f, instead of (n + 1)(1 - c) < f
+    real = O.select_from_stats
+
+    def bad(H, conf, rows, rule, threshold):
+        if rule == O.RULE_FACTOR:
+            return real(H, [1.0 - c for c in conf], rows, rule, threshold)
+        return real(H, conf, rows, rule, threshold)
+    monkeypatch.setattr(O, "select_from_stats", bad)
+    with pytest.raises(AssertionError):
+        test_factor_hand_examples()
+
+
+def test_planted_confidence_order_ascending_is_caught(monkeypatch):
+    real = O.select_from_stats
+
+    def bad(H, conf, rows, rule, threshold):
+        return real(H, [-c for c in conf], rows, rule, threshold)
+    monkeypatch.setattr(O, "select_from_stats", bad)
+    with pytest.raises(AssertionError):
+        test_eb_confidence_hand_examples()
 
 
 def test_planted_commit_of_bidirectional_rows_is_caught():
