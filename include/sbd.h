@@ -165,6 +165,29 @@ sbd_status sbd_eb_select(sbd_ctx* ctx, int32_t batch, int32_t k, int32_t vocab,
                          int32_t* accepted_tok, double* entropy);
 
 /*
+ * One sampling step under a selection rule (Sec. 2.2 and App. B), on fp32 logits.
+ * Arguments and outputs as sbd_eb_select, plus:
+ *   rule       SBD_SELECT_EB_ENTROPY: exactly sbd_eb_select (threshold = gamma).
+ *              SBD_SELECT_EB_CONFIDENCE: App. B, EB-Sampler with the confidence error
+ *              proxy: masked rows ordered by (confidence descending, row); s = largest r
+ *              in [1, |M|] with sum_{j<=r} H - max_{j<=r} H <= threshold (float64,
+ *              summed in that order).
+ *              SBD_SELECT_FACTOR: App. B, Factor parallel decoding: the same order; s =
+ *              largest r with (r + 1) * (1 - c_r) < threshold, at least 1 (c_r the r-th
+ *              confidence; App. B prints the condition without the 1 -, which would
+ *              reveal fewer rows the more confident they are).
+ *   threshold  gamma (EB rules) or f (Factor): >= 0, may be +INFINITY; NaN is rejected.
+ *   confidence device float64 [batch][k] (nullable) = max_v p_v = 1 / Z of each masked
+ *              row (the softmax without mask_id), NaN otherwise.
+ * Errors: INVALID_ARG for an unknown rule, otherwise as sbd_eb_select.
+ */
+enum { SBD_SELECT_EB_ENTROPY = 0, SBD_SELECT_EB_CONFIDENCE = 1, SBD_SELECT_FACTOR = 2 };
+sbd_status sbd_select(sbd_ctx* ctx, int32_t rule, int32_t batch, int32_t k, int32_t vocab,
+                      const float* logits, const uint8_t* is_mask, double threshold, int32_t mask_id,
+                      int32_t* n_accepted, int32_t* accepted_pos, int32_t* accepted_tok, double* entropy,
+                      double* confidence);
+
+/*
  * The selection part of sbd_eb_select alone, on given entropies (device float64
  * [batch][k]); same ordering, rule and outputs (no tokens).
  */

@@ -27,6 +27,7 @@ LAYER_FIELDS = ("attn_norm", "wq", "wk", "wv", "wo", "q_norm", "k_norm", "mlp_no
 KERNEL_NAMES = ("embed", "qkv", "rope", "attention", "attn_merge", "o_proj", "gate_up", "down",
                 "lm_head", "eb_partial", "eb_select", "fused", "layer_attn", "layer_mlp", "layer_final")
 DECODE_PATHS = {"auto": 0, "fused": 1, "kernels": 2, "layers": 3}  # sbd_decode_path
+SELECT_RULES = {"eb_entropy": 0, "eb_confidence": 1, "factor": 2}  # SBD_SELECT_*
 
 # Every entry point of sbd.h with its argument types.
 SIGNATURES = {
@@ -43,6 +44,8 @@ SIGNATURES = {
     "sbd_commit": [c_void_p, c_int32, c_void_p, c_void_p],
     "sbd_eb_select": [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p, c_double, c_int32,
                       c_void_p, c_void_p, c_void_p, c_void_p],
+    "sbd_select": [c_void_p, c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p, c_double, c_int32,
+                   c_void_p, c_void_p, c_void_p, c_void_p, c_void_p],
     "sbd_eb_select_entropies": [c_void_p, c_int32, c_int32, c_void_p, c_void_p, c_double,
                                 c_void_p, c_void_p],
     "sbd_kv_import": [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p],
@@ -232,6 +235,21 @@ class Sbd:
         self._call("sbd_eb_select", B, k, V, _dev(logits), _ptr(msk), float(gamma), int(mask_id),
                    _dev(n_acc), _dev(pos), _dev(tok), _dev(H))
         return n_acc, pos, tok, H
+
+    def select(self, logits: torch.Tensor, is_mask, rule: str, threshold: float, mask_id: int):
+        """One sampling step under a selection rule (sbd_select): "eb_entropy", "eb_confidence" or
+        "factor".  Returns (n_accepted, accepted_pos, accepted_tok, entropy, confidence)."""
+        B, k, V = logits.shape
+        msk = _host(is_mask, np.uint8)
+        dev = logits.device
+        n_acc = torch.empty(B, dtype=torch.int32, device=dev)
+        pos = torch.empty((B, k), dtype=torch.int32, device=dev)
+        tok = torch.empty((B, k), dtype=torch.int32, device=dev)
+        H = torch.empty((B, k), dtype=torch.float64, device=dev)
+        C = torch.empty((B, k), dtype=torch.float64, device=dev)
+        self._call("sbd_select", SELECT_RULES[rule], B, k, V, _dev(logits), _ptr(msk), float(threshold),
+                   int(mask_id), _dev(n_acc), _dev(pos), _dev(tok), _dev(H), _dev(C))
+        return n_acc, pos, tok, H, C
 
     def eb_select_entropies(self, entropy: torch.Tensor, is_mask, gamma: float):
         B, k = entropy.shape

@@ -128,6 +128,7 @@ __device__ __forceinline__ double wave_max_d(double v) {
 template <bool SELECT_ONLY>
 __global__ __launch_bounds__(256) void eb_select_kernel(EbArgs a) {
   __shared__ double sh[64];
+  __shared__ double sconf[64];
   __shared__ int smask[64];
   __shared__ int stok[64];
   __shared__ int order[64];
@@ -139,7 +140,7 @@ __global__ __launch_bounds__(256) void eb_select_kernel(EbArgs a) {
   for (int j = w; j < k; j += 4) {
     const int64_t row = (int64_t)b * k + j;
     const bool masked = a.is_mask[row] != 0;
-    double H = 0.0;
+    double H = 0.0, conf = 0.0;
     int tok = -1;
     if (masked) {
       if (SELECT_ONLY) {
@@ -166,10 +167,12 @@ __global__ __launch_bounds__(256) void eb_select_kernel(EbArgs a) {
         for (int o = 32; o >= 1; o >>= 1) cfirst = min(cfirst, __shfl_xor(cfirst, o));
         tok = a.part_arg[row * a.n_chunks + cfirst];
         H = log(Z) - S / Z;
+        conf = 1.0 / Z;  // the largest probability: e^0 / Z
       }
     }
     if (lane == 0) {
       sh[j] = H;
+      sconf[j] = conf;
       smask[j] = masked ? 1 : 0;
       stok[j] = tok;
     }
@@ -181,20 +184,36 @@ __global__ __launch_bounds__(256) void eb_select_kernel(EbArgs a) {
   const bool in = w0 && j < k;
   const bool masked = in && smask[j] != 0;
   const double H = in ? sh[j] : 0.0;
+  const double C = in ? sconf[j] : 0.0;
+  const bool by_conf = a.rule != SBD_SELECT_EB_ENTROPY;  // wave-uniform
   int rank = 0, n = 0;
   for (int i = 0; i < k; ++i) {
     if (!smask[i]) continue;
     ++n;
-    if (sh[i] < H || (sh[i] == H && i < j)) ++rank;
+    if (by_conf ? (sconf[i] > C || (sconf[i] == C && i < j)) : (sh[i] < H || (sh[i] == H && i < j))) ++rank;
   }
   if (masked) order[rank] = j;
   __syncthreads();
   if (w0 && j == 0) {
     int s = 0;
-    double c = 0.0;
-    for (int r = 0; r < n; ++r) {
-      if (c <= a.gamma) s = r + 1;
-      c += sh[order[r]];
+    if (a.rule == SBD_SELECT_EB_ENTROPY) {  // eq. (eb_sampler): c_{r-1} <= gamma
+      double c = 0.0;
+      for (int r = 0; r < n; ++r) {
+        if (c <= a.gamma) s = r + 1;
+        c += sh[order[r]];
+      }
+    } else if (a.rule == SBD_SELECT_EB_CONFIDENCE) {  // App. B: sum - max of the prefix <= gamma
+      double c = 0.0, top = -INFINITY;
+      s = n > 0 ? 1 : 0;
+      for (int r = 0; r < n; ++r) {
+        c += sh[order[r]];
+        top = fmax(top, sh[order[r]]);
+        if (c - top <= a.gamma) s = r + 1;
+      }
+    } else {  // Factor: (r + 1)(1 - c_r) < f
+      s = n > 0 ? 1 : 0;
+      for (int r = 0; r < n; ++r)
+        if ((double)(r + 2) * (1.0 - sconf[order[r]]) < a.gamma) s = r + 1;
     }
     s_count = s;
     a.n_accepted[b] = s;
@@ -212,6 +231,7 @@ __global__ __launch_bounds__(256) void eb_select_kernel(EbArgs a) {
       if (a.accepted_tok) a.accepted_tok[row] = -1;
     }
     if (a.entropy_out) a.entropy_out[row] = masked ? H : __builtin_nan("");
+    if (a.conf_out) a.conf_out[row] = masked ? C : __builtin_nan("");
   }
   __syncthreads();
   if (acc) {

@@ -792,7 +792,16 @@ static sbd_status eb_common(sbd_ctx* c, int32_t batch, int32_t k, const uint8_t*
 sbd_status sbd_eb_select(sbd_ctx* c, int32_t batch, int32_t k, int32_t vocab, const float* logits,
                          const uint8_t* is_mask, double gamma, int32_t mask_id, int32_t* n_accepted,
                          int32_t* accepted_pos, int32_t* accepted_tok, double* entropy) {
+  return sbd_select(c, SBD_SELECT_EB_ENTROPY, batch, k, vocab, logits, is_mask, gamma, mask_id, n_accepted,
+                    accepted_pos, accepted_tok, entropy, nullptr);
+}
+
+sbd_status sbd_select(sbd_ctx* c, int32_t rule, int32_t batch, int32_t k, int32_t vocab, const float* logits,
+                      const uint8_t* is_mask, double gamma, int32_t mask_id, int32_t* n_accepted,
+                      int32_t* accepted_pos, int32_t* accepted_tok, double* entropy, double* confidence) {
   if (sbd_status st = eb_common(c, batch, k, is_mask, gamma, n_accepted, accepted_pos)) return st;
+  if (rule != SBD_SELECT_EB_ENTROPY && rule != SBD_SELECT_EB_CONFIDENCE && rule != SBD_SELECT_FACTOR)
+    return fail(c, SBD_ERR_INVALID_ARG, "unknown selection rule %d", rule);
   if (!logits || !accepted_tok) return fail(c, SBD_ERR_INVALID_ARG, "null argument");
   if (vocab < 1 || vocab > c->cfg.vocab) return fail(c, SBD_ERR_INVALID_ARG, "vocab %d out of [1, %d]", vocab, c->cfg.vocab);
   if (mask_id < -1 || mask_id >= vocab) return fail(c, SBD_ERR_INVALID_ARG, "mask_id %d out of [-1, vocab)", mask_id);
@@ -804,7 +813,7 @@ sbd_status sbd_eb_select(sbd_ctx* c, int32_t batch, int32_t k, int32_t vocab, co
   a.n_chunks = (vocab + kEbChunk - 1) / kEbChunk;
   a.part = c->at<double>(c->lay.eb_part); a.part_arg = c->at<int32_t>(c->lay.eb_arg);
   a.n_accepted = n_accepted; a.accepted_pos = accepted_pos; a.accepted_tok = accepted_tok;
-  a.entropy_out = entropy;
+  a.entropy_out = entropy; a.rule = rule; a.conf_out = confidence;
   SBD_LAUNCH(c, SBD_KERNEL_EB_PARTIAL, launch_eb_partial(a, ex));
   SBD_LAUNCH(c, SBD_KERNEL_EB_SELECT, launch_eb_select(a, false, ex));
   return SBD_OK;

@@ -406,6 +406,8 @@ struct EbArgs {
   int32_t* accepted_pos;    // [B][k]
   int32_t* accepted_tok;    // [B][k] or null
   double* entropy_out;      // [B][k] or null
+  int rule;                 // SBD_SELECT_*: the order and the stopping rule (gamma = its threshold)
+  double* conf_out;         // [B][k] or null: max_v p_v of masked rows
 };
 hipError_t launch_eb_partial(const EbArgs& a, const Exec& ex);
 hipError_t launch_eb_select(const EbArgs& a, bool select_only, const Exec& ex);

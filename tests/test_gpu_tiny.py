@@ -146,6 +146,38 @@ def test_eb_select_ladder_bit_exact(wide, B, k, V, mask_id):
         np.testing.assert_allclose(Hg[m], rH[m], rtol=1e-12, atol=1e-13)
 
 
+@pytest.mark.parametrize("B,k,V,mask_id", [(1, 16, 1024, 1023), (3, 8, 4096, 0), (2, 64, 16384, 16383),
+                                           (3, 9, 4097, 4096)])
+def test_select_rules_ladder_bit_exact(wide, B, k, V, mask_id):
+    """The App. B rules (EB with the confidence proxy, Factor) on ladder logits: identical
+    accepted sets and tokens; confidences to float64 rounding; the entropy rule through
+    sbd_select equals sbd_eb_select."""
+    logits = synth.entropy_ladder_logits(B * 100 + k + 1, B, k, V)
+    rng = np.random.default_rng(B * 11 + k)
+    is_mask = (rng.random((B, k)) < 0.8).astype(np.uint8)
+    is_mask[:, 0] = 0
+    if k > 1:
+        is_mask[:, 1] = 1
+    m = is_mask.astype(bool)
+    cases = [("eb_confidence", O.RULE_EB_CONFIDENCE, g) for g in (0.0, 0.1, 1.0, 4.0, math.inf)]
+    cases += [("factor", O.RULE_FACTOR, f) for f in (0.0, 0.05, 0.5, 2.0, 8.0, math.inf)]
+    cases += [("eb_entropy", O.RULE_EB_ENTROPY, 1.0)]
+    for name, rule, thr in cases:
+        acc, rtok, rH, rC = O.select(logits.numpy(), is_mask, rule, thr, mask_id)
+        n_acc, pos, tok, H, C = wide.lib.select(logits.cuda(), is_mask, name, thr, mask_id)
+        for b in range(B):
+            n = int(n_acc[b])
+            assert pos[b, :n].tolist() == acc[b], (name, thr, b)
+            assert tok[b, :n].tolist() == rtok[b], (name, thr, b)
+            assert (pos[b, n:] == -1).all()
+        np.testing.assert_allclose(H.cpu().numpy()[m], rH[m], rtol=1e-12, atol=1e-13)
+        np.testing.assert_allclose(C.cpu().numpy()[m], rC[m], rtol=1e-12, atol=1e-15)
+        assert np.isnan(C.cpu().numpy()[~m]).all()
+    n1, p1, t1, _ = wide.lib.eb_select(logits.cuda(), is_mask, 1.0, mask_id)
+    n2, p2, t2, _, _ = wide.lib.select(logits.cuda(), is_mask, "eb_entropy", 1.0, mask_id)
+    assert torch.equal(n1, n2) and torch.equal(p1, p2) and torch.equal(t1, t2)
+
+
 def test_eb_select_entropies_hand_cases(tiny):
     H = torch.tensor([[0.0, 0.25, 0.125, 0.375, 0.125]], dtype=torch.float64, device="cuda")
     is_mask = np.array([[0, 1, 1, 1, 1]], np.uint8)
@@ -377,6 +409,11 @@ def test_state_and_argument_errors(tiny):
     logits = torch.zeros((1, 4, s.vocab), device="cuda")
     err(lambda: lib.eb_select(logits, is_mask, float("nan"), s.mask_id), "SBD_ERR_INVALID_ARG")
     err(lambda: lib.eb_select(logits, is_mask, -0.1, s.mask_id), "SBD_ERR_INVALID_ARG")
+    err(lambda: lib.select(logits, is_mask, "factor", float("nan"), s.mask_id), "SBD_ERR_INVALID_ARG")
+    dummy = torch.empty((1, 4), dtype=torch.int32, device="cuda")
+    err(lambda: lib._call("sbd_select", 7, 1, 4, logits.shape[2], logits.data_ptr(),
+                          is_mask.astype(np.uint8).ctypes.data, 1.0, s.mask_id, dummy.data_ptr(),
+                          dummy.data_ptr(), dummy.data_ptr(), None, None), "SBD_ERR_INVALID_ARG")
     err(lambda: lib.eb_select(torch.zeros((1, 4, 2048), device="cuda"), is_mask, 1.0, -1),
         "SBD_ERR_INVALID_ARG")
     assert lib.lib.sbd_set_decode_path(lib.ctx, 4) == 1                     # unknown path
