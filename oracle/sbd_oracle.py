@@ -450,3 +450,44 @@ def eb_select(logits, is_mask, gamma: float, mask_id: int) -> tuple:
         accepted.append(acc)
         tokens.append([toks[j] for j in acc])
     return accepted, tokens, H
+
+
+def sample_blocks(model: "Model", caches: List[SeqCache], n_blocks: int, k: int, rule: int, threshold: float,
+                  mask_id: int) -> tuple:
+    """Alg. 2 after its prefill: n_blocks calls of Alg. 3 (Sample block) for every sequence.
+
+    A block starts as k mask tokens.  While it holds masks: one forward of the network; in
+    the first iteration of every block but the first, the previous block's k tokens enter
+    as causal rows ahead of the block (the f(x_<t-k, x_t-k:t-1; x_hat) form of Alg. 3) and
+    are committed to the cache afterwards; later iterations feed the block alone.  The
+    block's rows are then unmasked by the selection rule (eq. (eb_sampler), or App. B), with
+    argmax tokens (temperature 0, Sec. 3.1).  Sequences run in lockstep.
+    Returns (tokens [B][n_blocks*k], trace): trace lists, per forward, the fed tokens,
+    n_causal and the (accepted rows, tokens) of every sequence.
+    """
+    B = len(caches)
+    out = [[] for _ in range(B)]
+    trace = []
+    prev = None
+    for _ in range(n_blocks):
+        xh = np.full((B, k), mask_id, dtype=np.int64)
+        first = True
+        while (xh == mask_id).any():
+            if first and prev is not None:
+                toks, nc, off = np.concatenate([prev, xh], axis=1), k, k
+            else:
+                toks, nc, off = xh.copy(), 0, 0
+            res = model.block_forward(caches, toks, [nc] * B)
+            if nc:
+                Model.commit(caches, res, [k] * B)
+            is_mask = (xh == mask_id).astype(np.uint8)
+            acc, tk, _, _ = select(res.logits[:, off:off + k], is_mask, rule, threshold, mask_id)
+            trace.append((toks.copy(), nc, acc, tk))
+            for b in range(B):
+                for j, t in zip(acc[b], tk[b]):
+                    xh[b, j] = t
+            first = False
+        prev = xh.copy()
+        for b in range(B):
+            out[b].extend(int(t) for t in xh[b])
+    return out, trace

@@ -4,6 +4,7 @@
 """
 from .binding import (LIB_PATH, SIGNATURES, ModelConfig, Sbd, SbdError, load_library,
                       make_config, status_string, workspace_bytes)
+from .sampler import sample_blocks
 
 __all__ = ["LIB_PATH", "SIGNATURES", "ModelConfig", "Sbd", "SbdError", "load_library",
-           "make_config", "status_string", "workspace_bytes"]
+           "make_config", "sample_blocks", "status_string", "workspace_bytes"]

@@ -452,6 +452,58 @@ def test_confidence_rule_reduces_to_entropy_rule_when_the_orders_agree():
             assert a_conf == a_ent and t_conf == t_ent
 
 
+# ------------------------------------------------------------------ the sampling loop, Alg. 2/3
+
+
+def loop_weights(seed=40):
+    """Tiny-model weights whose LM head is scaled by 16 (exact in bf16): entropies near 2
+    instead of near ln V, so the selection rules take several steps per block."""
+    shape = synth.TINY
+    w = synth.make_weights(shape, seed)
+    w["lm_head"] = (w["lm_head"].float() * 16.0).to(torch.bfloat16)
+    return shape, w
+
+
+def loop_model(seed=40):
+    shape, w = loop_weights(seed)
+    return shape, O.Model(shape, synth.weights_to_host(w), dtype=np.float64)
+
+
+@pytest.mark.parametrize("rule,thr,per_block", [(O.RULE_EB_ENTROPY, math.inf, 1), (O.RULE_FACTOR, math.inf, 1),
+                                                (O.RULE_EB_ENTROPY, 0.0, 4), (O.RULE_EB_CONFIDENCE, 0.0, 4)])
+def test_sampling_loop_forwards_and_structure(rule, thr, per_block):
+    shape, m = loop_model()
+    k, n_blocks = 4, 3
+    caches = []
+    for b in range(2):
+        c, _ = m.prefill(synth.make_tokens(41 + b, 10 + 3 * b, shape))
+        caches.append(c)
+    L0 = [c.length for c in caches]
+    out, trace = O.sample_blocks(m, caches, n_blocks, k, rule, thr, shape.mask_id)
+    assert len(trace) == n_blocks * per_block            # gamma = inf: one forward a block; 0: k
+    assert all(len(o) == n_blocks * k and shape.mask_id not in o for o in out)
+    starts = [i * per_block for i in range(n_blocks)]
+    for i, (toks, nc, acc, tk) in enumerate(trace):
+        blk = starts.index(i) if i in starts else None
+        if blk is not None and blk > 0:                   # first forward of a later block
+            assert nc == k and toks.shape[1] == 2 * k
+            for b in range(2):
+                assert toks[b, :k].tolist() == out[b][(blk - 1) * k:blk * k]
+                assert (toks[b, k:] == shape.mask_id).all()
+        else:
+            assert nc == 0 and toks.shape[1] == k
+        for b in range(2):
+            assert len(acc[b]) >= 1                       # every forward reveals a row
+    # the previous blocks were committed exactly: same cache as a prefill of what was emitted
+    for b in range(2):
+        assert caches[b].length == L0[b] + (n_blocks - 1) * k
+        prompt = synth.make_tokens(41 + b, 10 + 3 * b, shape)
+        ref, _ = m.prefill(np.concatenate([prompt, np.asarray(out[b][:(n_blocks - 1) * k])]))
+        for li in range(shape.n_layers):
+            np.testing.assert_allclose(caches[b].K[li], ref.K[li], rtol=1e-10, atol=1e-12)
+            np.testing.assert_allclose(caches[b].V[li], ref.V[li], rtol=1e-10, atol=1e-12)
+
+
 # ------------------------------------------------------------------ planted mistakes
 # Each plants a plausible bug in the oracle and checks that one of the pins above fails.
 
