@@ -5,13 +5,15 @@
 // with t = l - m_c in float64 accumulates Z_c = sum e^t and S_c = sum e^t t.  Sums are
 // per-thread in a fixed order followed by a fixed tree, so results are reproducible.
 //
-// eb_select: one workgroup per sequence.  Each masked row merges its chunks (one lane
-// per chunk, fixed butterfly sums) with M = max m_c, delta_c = m_c - M:
+// eb_select: one workgroup of 16 waves per sequence, one wave per row (rows w, w + 16, ...).
+// Each masked row merges its chunks (one lane per chunk, fixed butterfly sums) with
+// M = max m_c, delta_c = m_c - M:
 //   Z = sum_c e^delta_c Z_c,  S = sum_c e^delta_c (S_c + delta_c Z_c),  H = log Z - S / Z
 // (the entropy of softmax over the row; argmax = first chunk reaching M).  Then the
 // masked rows are ranked by (H, row), lane 0 forms the running float64 sums c_r in
 // that order, s = max{r >= 1 : c_{r-1} <= gamma}, and the first s rows are written out
-// in ascending row order.
+// in ascending row order.  A row without a finite logit (outside the mask column) has
+// entropy and confidence NaN and token -1, and ranks after every other row.
 
 #include "sbd_device.h"
 
@@ -33,25 +35,30 @@ __global__ __launch_bounds__(kEbThreads) void eb_partial_kernel(EbArgs a) {
   __shared__ int sarg[kEbThreads / 64];
   __shared__ double sz[kEbThreads / 64], ss[kEbThreads / 64];
   const int row = blockIdx.y;
-  if (!a.is_mask[row]) return;
   const int c = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const float* lr = a.logits + (int64_t)row * a.vocab;
   const int v0 = c * kEbChunk;
 
+  // every load is unconditional (the index clamped into the row), so that all of them are
+  // in flight at once; entries past the row end and the mask column are dropped afterwards
   float val[kEbPer];
+#pragma unroll
+  for (int e = 0; e < kEbPer; ++e) val[e] = lr[min(v0 + tid + e * kEbThreads, a.vocab - 1)];
   float mx = -INFINITY;
   int arg = INT32_MAX;
 #pragma unroll
   for (int e = 0; e < kEbPer; ++e) {
     const int v = v0 + tid + e * kEbThreads;
     const bool ok = v < a.vocab && v != a.mask_id;
-    val[e] = ok ? lr[v] : -INFINITY;
+    if (!ok) val[e] = -INFINITY;
     if (ok && (val[e] > mx || (val[e] == mx && v < arg))) {
       mx = val[e];
       arg = v;
     }
   }
+  // read after the chunk's loads are issued: the workgroup of an unmasked row stores nothing
+  const bool masked = eb_row_masked(a, row);
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) {
     const float om = __shfl_xor(mx, o);
@@ -97,7 +104,7 @@ __global__ __launch_bounds__(kEbThreads) void eb_partial_kernel(EbArgs a) {
     ss[w] = s;
   }
   __syncthreads();
-  if (tid == 0) {
+  if (tid == 0 && masked) {
     double zt = 0.0, st = 0.0;
     for (int i = 0; i < kEbThreads / 64; ++i) {
       zt += sz[i];
@@ -123,12 +130,15 @@ __device__ __forceinline__ double wave_max_d(double v) {
   return v;
 }
 
-// One workgroup (4 waves) per sequence.  Wave w merges the chunk statistics of rows
-// w, w + 4, ... with one lane per chunk; wave 0 then ranks and selects.
+constexpr int kEbSelWaves = 16;
+
+// One workgroup (16 waves) per sequence.  Wave w merges the chunk statistics of rows
+// w, w + 16, ... with one lane per chunk; wave 0 then ranks and selects.
 template <bool SELECT_ONLY>
-__global__ __launch_bounds__(256) void eb_select_kernel(EbArgs a) {
+__global__ __launch_bounds__(64 * kEbSelWaves) void eb_select_kernel(EbArgs a) {
   __shared__ double sh[64];
   __shared__ double sconf[64];
+  __shared__ double skey[64];  // ranking key, ascending: H or -confidence, NaN -> +inf
   __shared__ int smask[64];
   __shared__ int stok[64];
   __shared__ int order[64];
@@ -136,10 +146,11 @@ __global__ __launch_bounds__(256) void eb_select_kernel(EbArgs a) {
   const int b = blockIdx.x;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int k = a.k;
+  const bool by_conf = a.rule != SBD_SELECT_EB_ENTROPY;
 
-  for (int j = w; j < k; j += 4) {
+  for (int j = w; j < k; j += kEbSelWaves) {
     const int64_t row = (int64_t)b * k + j;
-    const bool masked = a.is_mask[row] != 0;
+    const bool masked = eb_row_masked(a, row);
     double H = 0.0, conf = 0.0;
     int tok = -1;
     if (masked) {
@@ -147,32 +158,67 @@ __global__ __launch_bounds__(256) void eb_select_kernel(EbArgs a) {
         H = a.entropy_in[row];
       } else {
         const double* p = a.part + row * a.n_chunks * 3;
-        double mloc = -INFINITY;
-        for (int c = lane; c < a.n_chunks; c += 64) mloc = fmax(mloc, p[c * 3]);
+        const int* pa = a.part_arg + row * a.n_chunks;
+        // the lane's first chunk is read once, with its argmax; chunks past the 64th
+        // (vocabularies above 256K entries) are read again in the second pass
+        double m0 = -INFINITY, z0 = 0.0, s0 = 0.0;
+        int g0 = -1;
+        if (lane < a.n_chunks) {
+          m0 = p[lane * 3];
+          z0 = p[lane * 3 + 1];
+          s0 = p[lane * 3 + 2];
+          g0 = pa[lane];
+        }
+        double mloc = m0;
+        for (int c = lane + 64; c < a.n_chunks; c += 64) mloc = fmax(mloc, p[c * 3]);
         const double M = wave_max_d(mloc);
         double z = 0.0, sacc = 0.0;
-        int cfirst = INT32_MAX;
-        for (int c = lane; c < a.n_chunks; c += 64) {
+        int cfirst = INT32_MAX, carg = -1;  // the lane's first chunk reaching M, and its argmax
+        if (m0 != -INFINITY) {
+          const double d = m0 - M;
+          const double f = exp(d);
+          z += f * z0;
+          sacc += f * (s0 + d * z0);
+          if (m0 == M) {
+            cfirst = lane;
+            carg = g0;
+          }
+        }
+        for (int c = lane + 64; c < a.n_chunks; c += 64) {
           const double mc = p[c * 3];
           if (mc == -INFINITY) continue;
           const double d = mc - M;
           const double f = exp(d);
           z += f * p[c * 3 + 1];
           sacc += f * (p[c * 3 + 2] + d * p[c * 3 + 1]);
-          if (mc == M && c < cfirst) cfirst = c;
+          if (mc == M && c < cfirst) {
+            cfirst = c;
+            carg = pa[c];
+          }
         }
         const double Z = wave_sum_d(z);
         const double S = wave_sum_d(sacc);
+        int cmin = cfirst;
 #pragma unroll
-        for (int o = 32; o >= 1; o >>= 1) cfirst = min(cfirst, __shfl_xor(cfirst, o));
-        tok = a.part_arg[row * a.n_chunks + cfirst];
-        H = log(Z) - S / Z;
-        conf = 1.0 / Z;  // the largest probability: e^0 / Z
+        for (int o = 32; o >= 1; o >>= 1) cmin = min(cmin, __shfl_xor(cmin, o));
+        const int from = cmin == INT32_MAX ? 0 : (cmin & 63);  // the lane holding chunk cmin
+        const int t = __shfl(carg, from);
+        if (cmin == INT32_MAX) {  // no finite logit in the row
+          tok = -1;
+          H = __builtin_nan("");
+          conf = __builtin_nan("");
+        } else {
+          tok = t;
+          H = log(Z) - S / Z;
+          conf = 1.0 / Z;  // the largest probability: e^0 / Z
+        }
       }
     }
     if (lane == 0) {
       sh[j] = H;
       sconf[j] = conf;
+      const double key = by_conf ? -conf : H;
+      skey[j] = key != key ? INFINITY : key;
       smask[j] = masked ? 1 : 0;
       stok[j] = tok;
     }
@@ -185,12 +231,12 @@ __global__ __launch_bounds__(256) void eb_select_kernel(EbArgs a) {
   const bool masked = in && smask[j] != 0;
   const double H = in ? sh[j] : 0.0;
   const double C = in ? sconf[j] : 0.0;
-  const bool by_conf = a.rule != SBD_SELECT_EB_ENTROPY;  // wave-uniform
-  int rank = 0, n = 0;
+  const double key = in ? skey[j] : 0.0;
+  int rank = 0, n = 0;  // rank by (key, row) ascending: a permutation of the masked rows
   for (int i = 0; i < k; ++i) {
     if (!smask[i]) continue;
     ++n;
-    if (by_conf ? (sconf[i] > C || (sconf[i] == C && i < j)) : (sh[i] < H || (sh[i] == H && i < j))) ++rank;
+    if (skey[i] < key || (skey[i] == key && i < j)) ++rank;
   }
   if (masked) order[rank] = j;
   __syncthreads();
@@ -247,9 +293,9 @@ hipError_t launch_eb_partial(const EbArgs& a, const Exec& ex) {
 
 hipError_t launch_eb_select(const EbArgs& a, bool select_only, const Exec& ex) {
   if (select_only)
-    SBD_KLAUNCH(eb_select_kernel<true>, dim3(a.B), dim3(256), ex, a);
+    SBD_KLAUNCH(eb_select_kernel<true>, dim3(a.B), dim3(64 * kEbSelWaves), ex, a);
   else
-    SBD_KLAUNCH(eb_select_kernel<false>, dim3(a.B), dim3(256), ex, a);
+    SBD_KLAUNCH(eb_select_kernel<false>, dim3(a.B), dim3(64 * kEbSelWaves), ex, a);
   return hipGetLastError();
 }
 

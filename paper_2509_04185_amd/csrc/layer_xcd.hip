@@ -272,30 +272,34 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
     if (last_arrival_xcd(xcd_ctr(a, x, kCtrQkv + gi), KS)) {
       const __amdgpu_buffer_rsrc_t rq = buf_rsrc(qp);
       f32x4* fin = reinterpret_cast<f32x4*>(smem);  // [8][64]
+      // Every reload of the group's slices (this wave's two tiles, and the row sums of x^2)
+      // is requested before any is used: one round trip to the L2.  Slots past KS re-read
+      // slice 0, which keeps the loads unconditional (a load behind a runtime condition
+      // becomes a branch that waits for it), and are dropped from the sums.
+      i32x4 v[2][kLxMaxKs];
+      float t[kLxMaxKs];
+      const int rs = threadIdx.x & 15;
 #pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2) {
-        const int ct = wave + 4 * k2;
-        i32x4 v[kLxMaxKs];  // every slice requested at once, added in slice order
+      for (int z = 0; z < kLxMaxKs; ++z) {
+        const int zz = z < KS ? z : 0;
 #pragma unroll
-        for (int z = 0; z < kLxMaxKs; ++z)
-          v[z] = z < KS ? ld16_l2(rq, (uint32_t)(((int64_t)z * kLxQkvSlice + (ct * 64 + lane) * 4) * 4))
-                        : i32x4{0, 0, 0, 0};
+        for (int k2 = 0; k2 < 2; ++k2)
+          v[k2][z] = ld16_l2(rq, (uint32_t)(((int64_t)zz * kLxQkvSlice + ((wave + 4 * k2) * 64 + lane) * 4) * 4));
+        t[z] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                             rq, (uint32_t)(((int64_t)zz * kLxQkvSlice + 2048 + rs) * 4), 0, kPolicyL2));
+      }
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2) {  // added in slice order
         f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int z = 0; z < kLxMaxKs; ++z) sum += __builtin_bit_cast(f32x4, v[z]);
-        fin[ct * 64 + lane] = sum;
+        for (int z = 0; z < kLxMaxKs; ++z) sum += z < KS ? __builtin_bit_cast(f32x4, v[k2][z]) : f32x4{0.f, 0.f, 0.f, 0.f};
+        fin[(wave + 4 * k2) * 64 + lane] = sum;
       }
       float* rinv_s = reinterpret_cast<float*>(smem + 65536 + 2048);  // [16]
       if (threadIdx.x < 16) {  // the KS slices' sums of x^2 of row threadIdx.x, in slice order
-        float t[kLxMaxKs];
-#pragma unroll
-        for (int z = 0; z < kLxMaxKs; ++z)
-          t[z] = z < KS ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                              rq, (uint32_t)(((int64_t)z * kLxQkvSlice + 2048 + threadIdx.x) * 4), 0, kPolicyL2))
-                        : 0.f;
         float tt = 0.f;
 #pragma unroll
-        for (int z = 0; z < kLxMaxKs; ++z) tt += t[z];
+        for (int z = 0; z < kLxMaxKs; ++z) tt += z < KS ? t[z] : 0.f;
         rinv_s[threadIdx.x] = 1.0f / sqrtf(tt / (float)a.d + a.eps);
       }
       __syncthreads();

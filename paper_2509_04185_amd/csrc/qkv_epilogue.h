@@ -37,10 +37,16 @@ __device__ __forceinline__ void qkv_epi_prefetch(const QkvEpi& e, int M, QkvPre<
       pre.sn[i][pr] = v.y;
     }
   }
+  // one branch around all the gain loads, so that they are in flight together
+  if (e.qk_norm) {
 #pragma unroll
-  for (int t = 0; t < tph; ++t) {
-    pre.gq[t] = e.qk_norm ? bf2f(e.q_norm[16 * t + r]) : 1.f;
-    pre.gk[t] = e.qk_norm ? bf2f(e.k_norm[16 * t + r]) : 1.f;
+    for (int t = 0; t < tph; ++t) {
+      pre.gq[t] = bf2f(e.q_norm[16 * t + r]);
+      pre.gk[t] = bf2f(e.k_norm[16 * t + r]);
+    }
+  } else {
+#pragma unroll
+    for (int t = 0; t < tph; ++t) pre.gq[t] = pre.gk[t] = 1.f;
   }
 }
 

@@ -806,10 +806,17 @@ sbd_status sbd_select(sbd_ctx* c, int32_t rule, int32_t batch, int32_t k, int32_
   if (vocab < 1 || vocab > c->cfg.vocab) return fail(c, SBD_ERR_INVALID_ARG, "vocab %d out of [1, %d]", vocab, c->cfg.vocab);
   if (mask_id < -1 || mask_id >= vocab) return fail(c, SBD_ERR_INVALID_ARG, "mask_id %d out of [-1, vocab)", mask_id);
   if (sbd_status st = check_sticky(c)) return st;
-  if (sbd_status st = upload(c, c->ws + c->lay.eb_mask, is_mask, (size_t)batch * k)) return st;
   EbArgs a{};
+  const int64_t rows = (int64_t)batch * k;
+  if (rows <= kEbInlineRows) {  // by value: no copy on the stream ahead of the kernels
+    for (int64_t i = 0; i < rows; ++i)
+      if (is_mask[i]) a.mask_bits[i >> 6] |= 1ull << (i & 63);
+  } else {
+    if (sbd_status st = upload(c, c->ws + c->lay.eb_mask, is_mask, (size_t)rows)) return st;
+    a.is_mask = c->at<uint8_t>(c->lay.eb_mask);
+  }
   a.B = batch; a.k = k; a.vocab = vocab; a.mask_id = mask_id; a.logits = logits;
-  a.is_mask = c->at<uint8_t>(c->lay.eb_mask); a.gamma = gamma;
+  a.gamma = gamma;
   a.n_chunks = (vocab + kEbChunk - 1) / kEbChunk;
   a.part = c->at<double>(c->lay.eb_part); a.part_arg = c->at<int32_t>(c->lay.eb_arg);
   a.n_accepted = n_accepted; a.accepted_pos = accepted_pos; a.accepted_tok = accepted_tok;

@@ -15,6 +15,7 @@ typedef uint16_t bf16_t;            // raw IEEE bfloat16 bits
 constexpr int kWave = 64;           // CDNA wavefront width
 constexpr int kMaxSplits = 64;      // split-KV partitions per (sequence, KV head, row block)
 constexpr int kEbChunk = 4096;      // vocabulary entries per EB partial workgroup
+constexpr int kEbInlineRows = 2048;  // masks of at most this many rows are passed by value
 constexpr int kMaxBlock = 64;       // largest block size k
 constexpr int kCounters = 65536;    // int32 words of arrival counters in the workspace
 constexpr int kLayerCtr0 = 16384;    // first counter word of the per-XCD layer kernels (decode GEMMs below)
@@ -408,7 +409,13 @@ struct EbArgs {
   double* entropy_out;      // [B][k] or null
   int rule;                 // SBD_SELECT_*: the order and the stopping rule (gamma = its threshold)
   double* conf_out;         // [B][k] or null: max_v p_v of masked rows
+  // Masks of up to kEbInlineRows rows travel in the kernel arguments (bit r of mask_bits is
+  // row r) instead of an upload on the stream; is_mask is then null.
+  uint64_t mask_bits[kEbInlineRows / 64];
 };
+__device__ __forceinline__ bool eb_row_masked(const EbArgs& a, int64_t row) {
+  return a.is_mask ? a.is_mask[row] != 0 : ((a.mask_bits[row >> 6] >> (row & 63)) & 1ull) != 0;
+}
 hipError_t launch_eb_partial(const EbArgs& a, const Exec& ex);
 hipError_t launch_eb_select(const EbArgs& a, bool select_only, const Exec& ex);
 

@@ -178,6 +178,64 @@ def test_select_rules_ladder_bit_exact(wide, B, k, V, mask_id):
     assert torch.equal(n1, n2) and torch.equal(p1, p2) and torch.equal(t1, t2)
 
 
+@pytest.mark.parametrize("name,rule,thr", [("eb_entropy", O.RULE_EB_ENTROPY, 0.5),
+                                           ("eb_entropy", O.RULE_EB_ENTROPY, math.inf),
+                                           ("eb_confidence", O.RULE_EB_CONFIDENCE, 1.0),
+                                           ("factor", O.RULE_FACTOR, 2.0)])
+def test_select_row_without_finite_logit(wide, name, rule, thr):
+    """A masked row whose logits are all -inf outside the mask column (vocabularies of two
+    chunks and more): entropy and confidence NaN, token -1, ranked after every other row;
+    the other rows are selected as the oracle selects them with that row ranked last."""
+    B, k, V, mask_id = 2, 8, 9000, 8999
+    logits = synth.entropy_ladder_logits(77, B, k, V)
+    logits[0, 3, :] = -math.inf
+    logits[0, 3, mask_id] = 5.0  # the excluded column is finite, and must stay excluded
+    is_mask = np.ones((B, k), np.uint8)
+    is_mask[:, 0] = 0
+    m = is_mask.astype(bool)
+    n_acc, pos, tok, H, C = wide.lib.select(logits.cuda(), is_mask, name, thr, mask_id)
+    H, C = H.cpu().numpy(), C.cpu().numpy()
+    assert np.isnan(H[0, 3]) and np.isnan(C[0, 3])
+    rows_ok = m.copy()
+    rows_ok[0, 3] = False
+    _, _, rH, rC = O.select(logits.numpy(), rows_ok, rule, thr, mask_id)
+    np.testing.assert_allclose(H[rows_ok], rH[rows_ok], rtol=1e-12, atol=1e-13)
+    # the oracle's rules with the degenerate row ranked last: +inf entropy, zero confidence
+    rH[0, 3], rC[0, 3] = math.inf, 0.0
+    for b in range(B):
+        rows = [j for j in range(k) if m[b, j]]
+        want = O.select_from_stats(rH[b], rC[b], rows, rule, thr)
+        n = int(n_acc[b])
+        assert pos[b, :n].tolist() == want, (b, name, thr)
+        got_tok = dict(zip(pos[b, :n].tolist(), tok[b, :n].tolist()))
+        if 3 in got_tok and b == 0:
+            assert got_tok[3] == -1
+        assert (pos[b, n:] == -1).all()
+
+
+def test_eb_select_many_rows_mask_upload():
+    """More rows than the masks passed by value (2048): the mask goes through the stream
+    upload instead; same accepted sets and tokens as the oracle."""
+    import dataclasses
+    shape = dataclasses.replace(synth.TINY, name="tiny_b40", n_layers=1)
+    t = Tiny(shape, 4004, max_batch=40, max_seq_len=64, max_block=64)
+    B, k, V, mask_id = 40, 64, shape.vocab, shape.mask_id
+    logits = synth.entropy_ladder_logits(4040, B, k, V)
+    rng = np.random.default_rng(4041)
+    is_mask = (rng.random((B, k)) < 0.7).astype(np.uint8)
+    is_mask[:, 0] = 0
+    is_mask[:, 1] = 1
+    for gamma in (0.5, math.inf):
+        acc, rtok, rH = O.eb_select(logits.numpy(), is_mask, gamma, mask_id)
+        n_acc, pos, tok, H = t.lib.eb_select(logits.cuda(), is_mask, gamma, mask_id)
+        for b in range(B):
+            n = int(n_acc[b])
+            assert pos[b, :n].tolist() == acc[b], (b, gamma)
+            assert tok[b, :n].tolist() == rtok[b], (b, gamma)
+        m = is_mask.astype(bool)
+        np.testing.assert_allclose(H.cpu().numpy()[m], rH[m], rtol=1e-12, atol=1e-13)
+
+
 def test_eb_select_entropies_hand_cases(tiny):
     H = torch.tensor([[0.0, 0.25, 0.125, 0.375, 0.125]], dtype=torch.float64, device="cuda")
     is_mask = np.array([[0, 1, 1, 1, 1]], np.uint8)
