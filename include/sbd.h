@@ -158,6 +158,8 @@ sbd_status sbd_commit(sbd_ctx* ctx, int32_t batch, const int32_t* seq_ids,
  * Outputs (device): n_accepted [batch] = s (0 if M is empty); accepted_pos
  * [batch][k] = the s rows ascending, then -1; accepted_tok [batch][k] = their tokens,
  * then -1; entropy [batch][k] (nullable) = H for masked rows, NaN otherwise.
+ * A masked row with no finite logit outside mask_id (all -inf or NaN) has H = NaN and
+ * tok = -1 and is ordered after every other row; its NaN stops the running sums.
  */
 sbd_status sbd_eb_select(sbd_ctx* ctx, int32_t batch, int32_t k, int32_t vocab,
                          const float* logits, const uint8_t* is_mask, double gamma,
