@@ -158,8 +158,10 @@ sbd_status sbd_commit(sbd_ctx* ctx, int32_t batch, const int32_t* seq_ids,
  * Outputs (device): n_accepted [batch] = s (0 if M is empty); accepted_pos
  * [batch][k] = the s rows ascending, then -1; accepted_tok [batch][k] = their tokens,
  * then -1; entropy [batch][k] (nullable) = H for masked rows, NaN otherwise.
- * A masked row with no finite logit outside mask_id (all -inf or NaN) has H = NaN and
- * tok = -1 and is ordered after every other row; its NaN stops the running sums.
+ * A masked row whose softmax is undefined (no finite logit outside mask_id, or a NaN or
+ * infinite logit) has H = NaN (tok = -1 when no logit is finite), is ordered after every
+ * other row and is never accepted: s runs over the other masked rows only, and is 0 when
+ * there are none.
  */
 sbd_status sbd_eb_select(sbd_ctx* ctx, int32_t batch, int32_t k, int32_t vocab,
                          const float* logits, const uint8_t* is_mask, double gamma,
@@ -181,6 +183,7 @@ sbd_status sbd_eb_select(sbd_ctx* ctx, int32_t batch, int32_t k, int32_t vocab,
  *   threshold  gamma (EB rules) or f (Factor): >= 0, may be +INFINITY; NaN is rejected.
  *   confidence device float64 [batch][k] (nullable) = max_v p_v = 1 / Z of each masked
  *              row (the softmax without mask_id), NaN otherwise.
+ * As for sbd_eb_select, a row with NaN statistics is never accepted.
  * Errors: INVALID_ARG for an unknown rule, otherwise as sbd_eb_select.
  */
 enum { SBD_SELECT_EB_ENTROPY = 0, SBD_SELECT_EB_CONFIDENCE = 1, SBD_SELECT_FACTOR = 2 };
@@ -191,7 +194,7 @@ sbd_status sbd_select(sbd_ctx* ctx, int32_t rule, int32_t batch, int32_t k, int3
 
 /*
  * The selection part of sbd_eb_select alone, on given entropies (device float64
- * [batch][k]); same ordering, rule and outputs (no tokens).
+ * [batch][k]); same ordering, rule and outputs (no tokens); a NaN entropy is never accepted.
  */
 sbd_status sbd_eb_select_entropies(sbd_ctx* ctx, int32_t batch, int32_t k,
                                    const double* entropy, const uint8_t* is_mask, double gamma,

@@ -364,11 +364,14 @@ def select_from_stats(H: Sequence[float], conf: Sequence[float], masked_rows: Se
     RULE_FACTOR: App. B, Factor parallel decoding: the same order; n is the largest r with
       (r + 1) * (1 - c_{i_r}) < f, at least 1 (the printed condition lacks the 1 - c; see
       the design notes).
-    Returns the revealed rows sorted by row.
+    A row whose entropy or confidence is NaN (its softmax is undefined: no finite logit, a
+    NaN or an infinite one) is never revealed and is left out of the order; with no other
+    masked row nothing is revealed.  Returns the revealed rows sorted by row.
     """
     if rule == RULE_EB_ENTROPY:
         return eb_select_from_entropy(H, masked_rows, threshold)
-    order = sorted(masked_rows, key=lambda j: (-float(conf[j]), int(j)))
+    usable = [j for j in masked_rows if not (math.isnan(float(H[j])) or math.isnan(float(conf[j])))]
+    order = sorted(usable, key=lambda j: (-float(conf[j]), int(j)))
     if not order:
         return []
     s = 1
@@ -417,9 +420,11 @@ def eb_select_from_entropy(H: Sequence[float], masked_rows: Sequence[int], gamma
     Masked rows are ordered by (H, row) ascending as i_1..i_n; c_0 = 0 and
     c_r = c_{r-1} + H_{i_r}, summed left to right in float64; s is the largest
     r in [1, n] with c_{r-1} <= gamma (so s >= 1 whenever n >= 1).  Returns the first
-    s rows of the order, sorted by row.
+    s rows of the order, sorted by row.  A row with a NaN entropy (undefined softmax) is
+    left out of the order and never revealed.
     """
-    order = sorted(masked_rows, key=lambda j: (float(H[j]), int(j)))
+    usable = [j for j in masked_rows if not math.isnan(float(H[j]))]
+    order = sorted(usable, key=lambda j: (float(H[j]), int(j)))
     s = 0
     c = 0.0
     for r, j in enumerate(order, start=1):
@@ -482,6 +487,8 @@ def sample_blocks(model: "Model", caches: List[SeqCache], n_blocks: int, k: int,
                 Model.commit(caches, res, [k] * B)
             is_mask = (xh == mask_id).astype(np.uint8)
             acc, tk, _, _ = select(res.logits[:, off:off + k], is_mask, rule, threshold, mask_id)
+            if not all(acc):
+                raise RuntimeError("a block with masks left revealed nothing (no usable softmax in any masked row)")
             trace.append((toks.copy(), nc, acc, tk))
             for b in range(B):
                 for j, t in zip(acc[b], tk[b]):

@@ -13,7 +13,9 @@
 // masked rows are ranked by (H, row), lane 0 forms the running float64 sums c_r in
 // that order, s = max{r >= 1 : c_{r-1} <= gamma}, and the first s rows are written out
 // in ascending row order.  A row without a finite logit (outside the mask column) has
-// entropy and confidence NaN and token -1, and ranks after every other row.
+// entropy and confidence NaN and token -1; a NaN or infinite logit makes them NaN too.
+// Such rows rank after every other row and are never accepted (with no other masked row,
+// s = 0).
 
 #include "sbd_device.h"
 
@@ -37,6 +39,9 @@ __global__ __launch_bounds__(kEbThreads) void eb_partial_kernel(EbArgs a) {
   const int row = blockIdx.y;
   const int c = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  // masks passed by value: an unmasked row's workgroups leave at once (a kernel-argument
+  // read, so nothing waits on memory); an uploaded mask is read after the loads are issued
+  if (a.is_mask == nullptr && !eb_row_masked(a, row)) return;
   const float* lr = a.logits + (int64_t)row * a.vocab;
   const int v0 = c * kEbChunk;
 
@@ -58,7 +63,7 @@ __global__ __launch_bounds__(kEbThreads) void eb_partial_kernel(EbArgs a) {
     }
   }
   // read after the chunk's loads are issued: the workgroup of an unmasked row stores nothing
-  const bool masked = eb_row_masked(a, row);
+  const bool masked = a.is_mask == nullptr || eb_row_masked(a, row);
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) {
     const float om = __shfl_xor(mx, o);
@@ -138,8 +143,9 @@ template <bool SELECT_ONLY>
 __global__ __launch_bounds__(64 * kEbSelWaves) void eb_select_kernel(EbArgs a) {
   __shared__ double sh[64];
   __shared__ double sconf[64];
-  __shared__ double skey[64];  // ranking key, ascending: H or -confidence, NaN -> +inf
+  __shared__ double skey[64];  // ranking key, ascending: H or -confidence
   __shared__ int smask[64];
+  __shared__ int sbad[64];     // 1: the row's statistics are NaN (undefined softmax)
   __shared__ int stok[64];
   __shared__ int order[64];
   __shared__ int s_count;
@@ -217,8 +223,9 @@ __global__ __launch_bounds__(64 * kEbSelWaves) void eb_select_kernel(EbArgs a) {
     if (lane == 0) {
       sh[j] = H;
       sconf[j] = conf;
-      const double key = by_conf ? -conf : H;
-      skey[j] = key != key ? INFINITY : key;
+      const bool nan_stats = H != H || conf != conf;
+      skey[j] = nan_stats ? 0.0 : (by_conf ? -conf : H);  // rows with NaN statistics: by row
+      sbad[j] = nan_stats ? 1 : 0;
       smask[j] = masked ? 1 : 0;
       stok[j] = tok;
     }
@@ -232,11 +239,14 @@ __global__ __launch_bounds__(64 * kEbSelWaves) void eb_select_kernel(EbArgs a) {
   const double H = in ? sh[j] : 0.0;
   const double C = in ? sconf[j] : 0.0;
   const double key = in ? skey[j] : 0.0;
-  int rank = 0, n = 0;  // rank by (key, row) ascending: a permutation of the masked rows
+  const int bad = in ? sbad[j] : 0;
+  // rank by (NaN statistics, key, row) ascending: a permutation of the masked rows whose
+  // first n places hold the rows with usable statistics; only those can be accepted
+  int rank = 0, n = 0;
   for (int i = 0; i < k; ++i) {
     if (!smask[i]) continue;
-    ++n;
-    if (skey[i] < key || (skey[i] == key && i < j)) ++rank;
+    n += sbad[i] ? 0 : 1;
+    if (sbad[i] < bad || (sbad[i] == bad && (skey[i] < key || (skey[i] == key && i < j)))) ++rank;
   }
   if (masked) order[rank] = j;
   __syncthreads();

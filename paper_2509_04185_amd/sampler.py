@@ -45,7 +45,12 @@ def sample_blocks(lib, seq_ids: Sequence[int], n_blocks: int, k: int, rule: str 
             if on_forward is not None:
                 on_forward(toks.copy(), nc, n_acc.copy(), pos.copy(), tok.copy())
             for b in range(B):
+                if int(n_acc[b]) < 1 and (xh[b] == mask).any():
+                    raise RuntimeError(f"sequence {ids[b]}: no masked row of the block has a usable softmax "
+                                       "(every logit non-finite); nothing can be revealed")
                 for i in range(int(n_acc[b])):
+                    if int(tok[b, i]) < 0:
+                        raise RuntimeError(f"sequence {ids[b]}: accepted row {int(pos[b, i])} has no token")
                     xh[b, int(pos[b, i]) - nc] = tok[b, i]
             first = False
         prev = xh.copy()

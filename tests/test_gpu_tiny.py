@@ -181,36 +181,44 @@ def test_select_rules_ladder_bit_exact(wide, B, k, V, mask_id):
 @pytest.mark.parametrize("name,rule,thr", [("eb_entropy", O.RULE_EB_ENTROPY, 0.5),
                                            ("eb_entropy", O.RULE_EB_ENTROPY, math.inf),
                                            ("eb_confidence", O.RULE_EB_CONFIDENCE, 1.0),
-                                           ("factor", O.RULE_FACTOR, 2.0)])
-def test_select_row_without_finite_logit(wide, name, rule, thr):
-    """A masked row whose logits are all -inf outside the mask column (vocabularies of two
-    chunks and more): entropy and confidence NaN, token -1, ranked after every other row;
-    the other rows are selected as the oracle selects them with that row ranked last."""
-    B, k, V, mask_id = 2, 8, 9000, 8999
+                                           ("eb_confidence", O.RULE_EB_CONFIDENCE, math.inf),
+                                           ("factor", O.RULE_FACTOR, 2.0),
+                                           ("factor", O.RULE_FACTOR, math.inf)])
+def test_select_rows_with_undefined_softmax(wide, name, rule, thr):
+    """Masked rows whose softmax is undefined: all -inf outside the mask column (vocabulary
+    of three chunks), a NaN logit, an infinite logit.  Their entropy and confidence are NaN,
+    they are never accepted (not even at an infinite threshold), and the other rows are
+    selected as the oracle selects them; a sequence whose only masked rows are such rows
+    accepts nothing."""
+    B, k, V, mask_id = 3, 8, 9000, 8999
     logits = synth.entropy_ladder_logits(77, B, k, V)
     logits[0, 3, :] = -math.inf
     logits[0, 3, mask_id] = 5.0  # the excluded column is finite, and must stay excluded
+    logits[0, 5, 4321] = math.nan
+    logits[1, 2, 8000] = math.inf
+    logits[2, 1, :] = -math.inf
     is_mask = np.ones((B, k), np.uint8)
     is_mask[:, 0] = 0
+    is_mask[2, 2:] = 0             # sequence 2: its only masked row has no finite logit
     m = is_mask.astype(bool)
+    bad = np.zeros((B, k), bool)
+    bad[0, 3] = bad[0, 5] = bad[1, 2] = bad[2, 1] = True
     n_acc, pos, tok, H, C = wide.lib.select(logits.cuda(), is_mask, name, thr, mask_id)
     H, C = H.cpu().numpy(), C.cpu().numpy()
-    assert np.isnan(H[0, 3]) and np.isnan(C[0, 3])
-    rows_ok = m.copy()
-    rows_ok[0, 3] = False
-    _, _, rH, rC = O.select(logits.numpy(), rows_ok, rule, thr, mask_id)
-    np.testing.assert_allclose(H[rows_ok], rH[rows_ok], rtol=1e-12, atol=1e-13)
-    # the oracle's rules with the degenerate row ranked last: +inf entropy, zero confidence
-    rH[0, 3], rC[0, 3] = math.inf, 0.0
+    assert np.isnan(H[bad]).all() and np.isnan(C[bad]).all()
+    with np.errstate(invalid="ignore"):
+        acc, rtok, rH, rC = O.select(logits.numpy(), is_mask, rule, thr, mask_id)
+    ok = m & ~bad
+    np.testing.assert_allclose(H[ok], rH[ok], rtol=1e-12, atol=1e-13)
     for b in range(B):
-        rows = [j for j in range(k) if m[b, j]]
-        want = O.select_from_stats(rH[b], rC[b], rows, rule, thr)
         n = int(n_acc[b])
-        assert pos[b, :n].tolist() == want, (b, name, thr)
-        got_tok = dict(zip(pos[b, :n].tolist(), tok[b, :n].tolist()))
-        if 3 in got_tok and b == 0:
-            assert got_tok[3] == -1
+        assert pos[b, :n].tolist() == acc[b], (b, name, thr)
+        assert tok[b, :n].tolist() == rtok[b], (b, name, thr)
+        assert not any(bad[b, j] for j in acc[b])
         assert (pos[b, n:] == -1).all()
+    assert int(n_acc[2]) == 0
+    if thr == math.inf:
+        assert sorted(acc[0]) == [j for j in range(k) if ok[0, j]]
 
 
 def test_eb_select_many_rows_mask_upload():

@@ -307,6 +307,34 @@ def test_eb_hand_examples():
     assert O.eb_select_from_entropy([1.0, 1.0, 1.0], [2, 0, 1], 0.0) == [0]
 
 
+def test_rows_with_nan_statistics_are_never_revealed():
+    """A masked row whose softmax is undefined (NaN entropy / confidence) takes no part in
+    any rule: the others are selected as if it were not masked, and alone it reveals
+    nothing (reading R21 of the design notes)."""
+    nan = math.nan
+    H = [0.0, 0.5, nan, 0.25, nan]
+    C = [0.0, 0.4, nan, 0.7, nan]
+    rows = [1, 2, 3, 4]
+    for gamma in (0.0, 0.3, 1.0, math.inf):
+        assert O.eb_select_from_entropy(H, rows, gamma) == O.eb_select_from_entropy(H, [1, 3], gamma)
+    assert O.eb_select_from_entropy(H, rows, math.inf) == [1, 3]
+    assert O.eb_select_from_entropy(H, [2, 4], math.inf) == []
+    for rule in (O.RULE_EB_CONFIDENCE, O.RULE_FACTOR):
+        for thr in (0.0, 1.0, math.inf):
+            assert O.select_from_stats(H, C, rows, rule, thr) == O.select_from_stats(H, C, [1, 3], rule, thr)
+        assert O.select_from_stats(H, C, [2, 4], rule, math.inf) == []
+    # from logits: all -inf outside the mask column, a NaN logit, an infinite logit
+    logits = np.zeros((1, 4, 6), np.float32)
+    logits[0, 0] = [0.1, 0.2, 0.3, 0.4, 0.5, 0.6]
+    logits[0, 1, :5] = -np.inf
+    logits[0, 2, 3] = np.nan
+    logits[0, 3, 1] = np.inf
+    with np.errstate(invalid="ignore"):
+        acc, tok, H2 = O.eb_select(logits, np.ones((1, 4), np.uint8), math.inf, 5)
+    assert acc == [[0]] and tok == [[4]]
+    assert np.isnan(H2[0, 1:]).all() and np.isfinite(H2[0, 0])
+
+
 def test_eb_gamma_zero_and_infinity():
     rng = np.random.default_rng(30)
     for _ in range(200):
