@@ -487,7 +487,7 @@ def sample_blocks(model: "Model", caches: List[SeqCache], n_blocks: int, k: int,
                 Model.commit(caches, res, [k] * B)
             is_mask = (xh == mask_id).astype(np.uint8)
             acc, tk, _, _ = select(res.logits[:, off:off + k], is_mask, rule, threshold, mask_id)
-            if not all(acc):
+            if any(is_mask[b].any() and not acc[b] for b in range(B)):
                 raise RuntimeError("a block with masks left revealed nothing (no usable softmax in any masked row)")
             trace.append((toks.copy(), nc, acc, tk))
             for b in range(B):

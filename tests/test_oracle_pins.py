@@ -532,6 +532,23 @@ def test_sampling_loop_forwards_and_structure(rule, thr, per_block):
             np.testing.assert_allclose(caches[b].V[li], ref.V[li], rtol=1e-10, atol=1e-12)
 
 
+def test_sampling_loop_sequences_finishing_at_different_forwards():
+    """In lockstep, a sequence whose block is complete sits out the remaining forwards of the
+    others (it has no masked row, so it reveals nothing) without stopping the loop."""
+    shape = synth.TINY
+    w = synth.make_weights(shape, 5005)
+    w["lm_head"] = (w["lm_head"].float() * 16.0).to(torch.bfloat16)
+    m = O.Model(shape, synth.weights_to_host(w), dtype=np.float64, kv_bf16=True)
+    caches = [m.prefill(synth.make_tokens(51, 12, shape))[0], m.prefill(synth.make_tokens(52, 17, shape))[0]]
+    out, trace = O.sample_blocks(m, caches, 3, 4, O.RULE_EB_CONFIDENCE, 1.0, shape.mask_id)
+    idle = [(i, b) for i, (_, _, acc, _) in enumerate(trace) for b in range(2) if not acc[b]]
+    assert idle, "the case needs a forward in which one sequence has nothing left to reveal"
+    for i, b in idle:
+        toks, nc = trace[i][0], trace[i][1]
+        assert (toks[b, nc:] != shape.mask_id).all()
+    assert all(len(o) == 12 and shape.mask_id not in o for o in out)
+
+
 # ------------------------------------------------------------------ planted mistakes
 # Each plants a plausible bug in the oracle and checks that one of the pins above fails.
 
