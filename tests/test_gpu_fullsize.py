@@ -6,8 +6,12 @@ bf16 weights and the same synthetic KV cache, installed on the GPU through sbd_k
 The benchmark's own configuration (Llama-3.1-8B shape, batch 1, 2048-token prompt, k=16)
 is also checked end to end with a real prefill on both sides.
 
-Tolerance: max-abs <= 5e-2 and rel-L2 <= 1e-2 on the logits of the sampled rows; EB
-selections bit-exact on identical fp32 logits.
+Tolerance: max-abs <= 5e-2 and rel-L2 <= 1e-2 on the logits of the compared rows (the
+contract), plus a regression bound at about ten times the measured error (synthetic caches:
+max-abs 5e-3, rel-L2 6e-4; measured up to 4.9e-4 / 6.2e-5); EB selections bit-exact on
+identical fp32 logits, with the decision margins printed (a flip at a margin below 1e-9
+would be reported as degenerate).  Sequences compared: every sequence of the batch-4 and
+batch-8 workloads, the shortest, the two middle and the longest of the ragged batch-32 one.
 """
 import math
 
@@ -15,31 +19,25 @@ import numpy as np
 import pytest
 import torch
 
+import parity
 import synth
 from oracle import sbd_oracle as O
 
 pytestmark = pytest.mark.gpu
 
 MAX_ABS, REL_L2 = 5e-2, 1e-2
+REGRESS = (5e-3, 6e-4)          # about ten times the error measured on synthetic caches
 
 
-def close(got, ref, max_abs=MAX_ABS, rel_l2=REL_L2):
-    got = np.asarray(got, dtype=np.float64)
-    ref = np.asarray(ref, dtype=np.float64)
-    err = np.abs(got - ref).max()
-    rel = np.linalg.norm(got - ref) / np.linalg.norm(ref)
-    print(f"    max-abs {err:.3e}  rel-L2 {rel:.3e}", flush=True)
-    assert err <= max_abs and rel <= rel_l2, f"max-abs {err:.3e} rel-L2 {rel:.3e}"
+def close(got, ref, max_abs=MAX_ABS, rel_l2=REL_L2, regress=REGRESS):
+    return parity.close(got, ref, regress=regress, max_abs=max_abs, rel_l2=rel_l2)
 
 
 def eb_bit_exact(lib, logits_np, is_mask, gammas, mask_id):
     for gamma in gammas:
         acc, rtok, rH = O.eb_select(logits_np, is_mask, gamma, mask_id)
         n_acc, pos, tok, H = lib.eb_select(torch.from_numpy(logits_np).cuda(), is_mask, gamma, mask_id)
-        for b in range(logits_np.shape[0]):
-            n = int(n_acc[b])
-            assert pos[b, :n].tolist() == acc[b], (b, gamma)
-            assert tok[b, :n].tolist() == rtok[b], (b, gamma)
+        parity.eb_compare(n_acc, pos, tok, acc, rtok, rH, is_mask, gamma)
         m = is_mask.astype(bool)
         np.testing.assert_allclose(H.cpu().numpy()[m], rH[m], rtol=1e-12, atol=1e-14)
 
@@ -59,8 +57,8 @@ def make_ctx(wl, import_cache=True):
     return w, lib, lens
 
 
-SAMPLES = {"llama8b_b1_l2048_k16": [0], "llama8b_b32_ragged_k8": "minmax",
-           "llama8b_b4_l32768_k16": [3], "qwen8b_b8_l8192_k16": [5]}
+SAMPLES = {"llama8b_b1_l2048_k16": [0], "llama8b_b32_ragged_k8": "spread",
+           "llama8b_b4_l32768_k16": [0, 1, 2, 3], "qwen8b_b8_l8192_k16": list(range(8))}
 
 # Extra decode-sized cases for the per-XCD layer kernels (at most 16 rows): the Qwen-3-8B
 # shape (q/k norm, ffn 12288) at batch 1, and two sequences of different lengths in one
@@ -97,8 +95,9 @@ def test_fullsize_block_forward(name):
     print(f"[gpu] {name}: B={wl.batch} k={wl.k}", flush=True)
     w, lib, lens = make_ctx(wl)
     sample = EXTRA[name][1] if name in EXTRA else SAMPLES[name]
-    if sample == "minmax":
-        sample = [int(np.argmin(lens)), int(np.argmax(lens))]
+    if sample == "spread":  # shortest, the two middle and the longest cache
+        order = [int(i) for i in np.argsort(lens, kind="stable")]
+        sample = sorted({order[0], order[len(order) // 2 - 1], order[len(order) // 2], order[-1]})
     toks, is_mask = synth.block_rows(wl.seed, s, wl.batch, wl.k, n_causal=1)
     # a decode-sized forward (<= 16 rows) is checked on every path that takes it
     paths = decode_paths(lib, wl.batch, wl.k)
@@ -169,15 +168,19 @@ def test_benched_configuration_with_real_prefill():
     model = O.Model(s, synth.weights_to_host(w), dtype=np.float32, cache_decoded=False, kv_bf16=True)
     print("    oracle prefill of 2048 tokens", flush=True)
     cache, ref_last = model.prefill(prompt)
-    close(got_last, ref_last)
+    # a real prefill on both sides: cache errors add up over 2048 positions (measured rel-L2
+    # ~7e-4 on the block logits), so the regression bound is looser here
+    real = (5e-2, 7e-3)
+    close(got_last, ref_last, regress=real)
     # both caches hold bf16 values; allow a bf16 ulp at magnitude ~8 where roundings differ
-    close(kl, cache.K[-1], max_abs=0.07)
-    close(vl, cache.V[-1], max_abs=0.07)
+    # (last layer after 2048 real positions: measured max-abs 3.1e-2, rel-L2 2.0e-3)
+    close(kl, cache.K[-1], max_abs=0.07, regress=(0.07, 6e-3))
+    close(vl, cache.V[-1], max_abs=0.07, regress=(0.07, 6e-3))
     ref = model.block_forward([cache], toks, [1]).logits
-    close(got, ref)
+    close(got, ref, regress=real)
     for path, g in got_paths.items():
         print(f"    decode path {path}", flush=True)
-        close(g, ref)
+        close(g, ref, regress=real)
 
 
 def test_layer_kernel_wait_that_gives_up_is_reported():

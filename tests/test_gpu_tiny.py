@@ -11,6 +11,7 @@ import numpy as np
 import pytest
 import torch
 
+import parity
 import synth
 from oracle import sbd_oracle as O
 
@@ -99,10 +100,7 @@ def test_tiny_workload_eb_select_bit_exact(tiny, gamma):
     acc, rtok, rH = O.eb_select(ref_logits, is_mask, gamma, tiny.shape.mask_id)
     n_acc, pos, tok, H = tiny.lib.eb_select(torch.from_numpy(ref_logits).cuda(), is_mask, gamma,
                                             tiny.shape.mask_id)
-    n = int(n_acc[0])
-    assert n == len(acc[0])
-    assert pos[0, :n].tolist() == acc[0] and tok[0, :n].tolist() == rtok[0]
-    assert (pos[0, n:] == -1).all()
+    parity.eb_compare(n_acc, pos, tok, acc, rtok, rH, is_mask, gamma)
     Hg = H.cpu().numpy()
     for j in range(4):
         if is_mask[0, j]:
@@ -136,11 +134,7 @@ def test_eb_select_ladder_bit_exact(wide, B, k, V, mask_id):
     for gamma in (0.0, 0.1, 1.0, 4.0, math.inf):
         acc, rtok, rH = O.eb_select(logits.numpy(), is_mask, gamma, mask_id)
         n_acc, pos, tok, H = wide.lib.eb_select(logits.cuda(), is_mask, gamma, mask_id)
-        for b in range(B):
-            n = int(n_acc[b])
-            assert pos[b, :n].tolist() == acc[b], (b, gamma)
-            assert tok[b, :n].tolist() == rtok[b], (b, gamma)
-            assert (pos[b, n:] == -1).all()
+        parity.eb_compare(n_acc, pos, tok, acc, rtok, rH, is_mask, gamma)
         Hg = H.cpu().numpy()
         m = is_mask.astype(bool)
         np.testing.assert_allclose(Hg[m], rH[m], rtol=1e-12, atol=1e-13)
