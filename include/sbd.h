@@ -193,6 +193,26 @@ sbd_status sbd_select(sbd_ctx* ctx, int32_t rule, int32_t batch, int32_t k, int3
                       double* confidence);
 
 /*
+ * sbd_eb_select for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, hosts that forbid hipMalloc): no context and no workspace.
+ * The chunk statistics live in a fixed scratch array of the library (1.75 MiB per device,
+ * held until the process ends; its device address is looked up on the first call on each
+ * device).  No hipMalloc, hipFree or other allocating call is made.
+ *   stream   hipStream_t to enqueue on (NULL = the null stream); the current device's
+ *            scratch is used.
+ *   Other arguments, outputs and the selection rule exactly as sbd_eb_select, with
+ *   is_mask a host array [batch][k].
+ * Limits: batch * k <= 1024, k <= 64, vocab <= 262144; beyond them INVALID_ARG (and
+ * nothing is enqueued).  Errors are reported through sbd_last_error(NULL).
+ * All calls on one device share its scratch: two calls that overlap in time on one device
+ * (different streams, or different host threads) race and give wrong results.
+ */
+sbd_status sbd_eb_select_noalloc(void* stream, int32_t batch, int32_t k, int32_t vocab,
+                                 const float* logits, const uint8_t* is_mask, double gamma,
+                                 int32_t mask_id, int32_t* n_accepted, int32_t* accepted_pos,
+                                 int32_t* accepted_tok, double* entropy);
+
+/*
  * The selection part of sbd_eb_select alone, on given entropies (device float64
  * [batch][k]); same ordering, rule and outputs (no tokens); a NaN entropy is never accepted.
  */

@@ -48,6 +48,8 @@ SIGNATURES = {
                    c_void_p, c_void_p, c_void_p, c_void_p, c_void_p],
     "sbd_eb_select_entropies": [c_void_p, c_int32, c_int32, c_void_p, c_void_p, c_double,
                                 c_void_p, c_void_p],
+    "sbd_eb_select_noalloc": [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p, c_double, c_int32,
+                              c_void_p, c_void_p, c_void_p, c_void_p],
     "sbd_kv_import": [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p],
     "sbd_kv_export": [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p],
     "sbd_set_decode_path": [c_void_p, c_int32],
@@ -309,6 +311,23 @@ class Sbd:
                                                        ctypes.byref(off), ctypes.byref(nb)),
                "sbd_workspace_region")
         return self.workspace[off.value: off.value + nb.value].view(self.REGION_DTYPES[name])
+
+
+def eb_select_noalloc(logits: torch.Tensor, is_mask, gamma: float, mask_id: int, out=None):
+    """sbd_eb_select_noalloc on torch's current stream: the EB step without a context or a
+    workspace.  out: optional preallocated (n_accepted, accepted_pos, accepted_tok, entropy)."""
+    lib = load_library()
+    B, k, V = logits.shape
+    msk = _host(is_mask, np.uint8)
+    dev = logits.device
+    if out is None:
+        out = (torch.empty(B, dtype=torch.int32, device=dev), torch.empty((B, k), dtype=torch.int32, device=dev),
+               torch.empty((B, k), dtype=torch.int32, device=dev), torch.empty((B, k), dtype=torch.float64, device=dev))
+    n_acc, pos, tok, H = out
+    stream = c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+    _check(lib, lib.sbd_eb_select_noalloc(stream, B, k, V, _dev(logits), _ptr(msk), float(gamma), int(mask_id),
+                                          _dev(n_acc), _dev(pos), _dev(tok), _dev(H)), "sbd_eb_select_noalloc")
+    return n_acc, pos, tok, H
 
 
 def status_string(status: int) -> str:

@@ -17,6 +17,8 @@
 // Such rows rank after every other row and are never accepted (with no other masked row,
 // s = 0).
 
+#include <mutex>
+
 #include "sbd_device.h"
 
 namespace sbd {
@@ -294,6 +296,35 @@ __global__ __launch_bounds__(64 * kEbSelWaves) void eb_select_kernel(EbArgs a) {
     a.accepted_pos[(int64_t)b * k + idx] = j;
     if (a.accepted_tok) a.accepted_tok[(int64_t)b * k + idx] = stok[j];
   }
+}
+
+// Scratch of sbd_eb_select_noalloc, the entry point for callers that cannot allocate: the
+// chunk statistics (max, Z, S) and the chunk argmaxes of up to kNoAllocRows rows of up to
+// kNoAllocChunks vocabulary chunks each, 1.75 MiB per device for the life of the process.
+// Every statistic a select reads is written by the partial kernel of the same call first, so
+// nothing needs clearing between calls.
+__device__ __align__(256) double scratch[(int64_t)kNoAllocRows * kNoAllocChunks * 3 +
+                                         (int64_t)kNoAllocRows * kNoAllocChunks / 2];
+
+hipError_t eb_noalloc_scratch(double** part, int32_t** part_arg) {
+  static std::mutex mu;
+  static void* addr[kNoAllocMaxDevices] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kNoAllocMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (addr[dev] == nullptr) {
+    // the array's name is a host-side stand-in: its device address comes from the runtime,
+    // once per device, with that device current
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *part = static_cast<double*>(addr[dev]);
+  *part_arg = reinterpret_cast<int32_t*>(*part + (int64_t)kNoAllocRows * kNoAllocChunks * 3);
+  return hipSuccess;
 }
 
 hipError_t launch_eb_partial(const EbArgs& a, const Exec& ex) {

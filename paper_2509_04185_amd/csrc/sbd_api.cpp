@@ -826,6 +826,38 @@ sbd_status sbd_select(sbd_ctx* c, int32_t rule, int32_t batch, int32_t k, int32_
   return SBD_OK;
 }
 
+sbd_status sbd_eb_select_noalloc(void* stream, int32_t batch, int32_t k, int32_t vocab, const float* logits,
+                                 const uint8_t* is_mask, double gamma, int32_t mask_id, int32_t* n_accepted,
+                                 int32_t* accepted_pos, int32_t* accepted_tok, double* entropy) {
+  if (batch < 1 || k < 1 || k > kMaxBlock)
+    return fail(nullptr, SBD_ERR_INVALID_ARG, "batch %d or k %d out of range (k <= %d)", batch, k, kMaxBlock);
+  if ((int64_t)batch * k > kNoAllocRows)
+    return fail(nullptr, SBD_ERR_INVALID_ARG, "batch * k = %lld exceeds the %d rows of the static scratch",
+                (long long)batch * k, kNoAllocRows);
+  if (vocab < 1 || vocab > kNoAllocChunks * kEbChunk)
+    return fail(nullptr, SBD_ERR_INVALID_ARG, "vocab %d out of [1, %d] (the static scratch's limit)", vocab,
+                kNoAllocChunks * kEbChunk);
+  if (!logits || !is_mask || !n_accepted || !accepted_pos || !accepted_tok)
+    return fail(nullptr, SBD_ERR_INVALID_ARG, "null argument");
+  if (mask_id < -1 || mask_id >= vocab) return fail(nullptr, SBD_ERR_INVALID_ARG, "mask_id %d out of [-1, vocab)", mask_id);
+  if (std::isnan(gamma) || gamma < 0.0) return fail(nullptr, SBD_ERR_INVALID_ARG, "gamma must be >= 0 (got %g)", gamma);
+  EbArgs a{};
+  hipError_t e = eb_noalloc_scratch(&a.part, &a.part_arg);
+  if (e != hipSuccess)
+    return fail(nullptr, SBD_ERR_HIP, "device address of the static scratch: %s", hipGetErrorString(e));
+  const int64_t rows = (int64_t)batch * k;  // <= kNoAllocRows <= kEbInlineRows: masks by value
+  for (int64_t i = 0; i < rows; ++i)
+    if (is_mask[i]) a.mask_bits[i >> 6] |= 1ull << (i & 63);
+  a.B = batch; a.k = k; a.vocab = vocab; a.mask_id = mask_id; a.logits = logits; a.gamma = gamma;
+  a.n_chunks = (vocab + kEbChunk - 1) / kEbChunk;
+  a.n_accepted = n_accepted; a.accepted_pos = accepted_pos; a.accepted_tok = accepted_tok;
+  a.entropy_out = entropy; a.rule = SBD_SELECT_EB_ENTROPY;
+  const Exec ex{static_cast<hipStream_t>(stream), nullptr, nullptr};
+  if ((e = launch_eb_partial(a, ex)) != hipSuccess || (e = launch_eb_select(a, false, ex)) != hipSuccess)
+    return fail(nullptr, SBD_ERR_HIP, "EB launch failed: %s", hipGetErrorString(e));
+  return SBD_OK;
+}
+
 sbd_status sbd_eb_select_entropies(sbd_ctx* c, int32_t batch, int32_t k, const double* entropy,
                                    const uint8_t* is_mask, double gamma, int32_t* n_accepted,
                                    int32_t* accepted_pos) {

@@ -417,6 +417,12 @@ __device__ __forceinline__ bool eb_row_masked(const EbArgs& a, int64_t row) {
   return a.is_mask ? a.is_mask[row] != 0 : ((a.mask_bits[row >> 6] >> (row & 63)) & 1ull) != 0;
 }
 hipError_t launch_eb_partial(const EbArgs& a, const Exec& ex);
+// Limits of sbd_eb_select_noalloc and the device address of its file-scope scratch on the
+// current device (looked up once per device).
+constexpr int kNoAllocRows = 1024;       // batch * k
+constexpr int kNoAllocChunks = 64;       // vocab <= 64 * kEbChunk = 262144
+constexpr int kNoAllocMaxDevices = 64;
+hipError_t eb_noalloc_scratch(double** part, int32_t** part_arg);
 hipError_t launch_eb_select(const EbArgs& a, bool select_only, const Exec& ex);
 
 }  // namespace sbd

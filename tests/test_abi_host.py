@@ -112,6 +112,20 @@ def test_null_context_is_rejected(lib):
     assert lib.sbd_cache_len(None, 0, ctypes.byref(n)) == 1
 
 
+def test_noalloc_eb_select_validates_before_any_device_call(lib):
+    """Sizes beyond the static scratch and bad arguments are refused on the host (no GPU here)."""
+    d = ctypes.c_void_p(16)   # never dereferenced: every case fails validation first
+    m = (ctypes.c_uint8 * 2048)()
+    f = lib.sbd_eb_select_noalloc
+    assert f(None, 17, 64, 128, d, m, 1.0, -1, d, d, d, None) == 1          # 1088 rows
+    assert f(None, 1, 65, 128, d, m, 1.0, -1, d, d, d, None) == 1           # k > 64
+    assert f(None, 1, 4, 262145, d, m, 1.0, -1, d, d, d, None) == 1         # vocab > 64 chunks
+    assert f(None, 1, 4, 128, None, m, 1.0, -1, d, d, d, None) == 1         # null logits
+    assert f(None, 1, 4, 128, d, m, float("nan"), -1, d, d, d, None) == 1   # NaN gamma
+    assert f(None, 1, 4, 128, d, m, 1.0, 128, d, d, d, None) == 1           # mask id out of range
+    assert b"static scratch" in lib.sbd_last_error(None) or b"mask_id" in lib.sbd_last_error(None)
+
+
 def test_workspace_regions():
     cfg = P.make_config(synth.TINY, 1, 128, 4)
     total = P.workspace_bytes(cfg)
