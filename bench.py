@@ -8,8 +8,9 @@ batch 1, a 2048-token random prompt prefilled into the KV cache, block k = 16 (t
 committed token + 15 masks), gamma = 1.0.  Inputs are resident in HBM before timing.
 
 Prints one JSON line: value = algorithmic HBM bytes of a step / step time (GB/s),
-plus the block-forward ms, the EB-select microseconds, a roofline entry for the
-dominant kernel (the per-XCD MLP layer kernel, the fused decode forward, or the gate/up
+plus the block-forward ms, the EB-select microseconds, the spread of step times, the same
+step with the EB statistics taken from the LM head (sbd_block_step), the measured
+streaming ceiling of the device, a roofline entry for the dominant kernel (the per-XCD MLP layer kernel, the fused decode forward, or the gate/up
 projection on the per-kernel path; timed live with HIP events on the library stream) and the CPU oracle timed on a bounded sample of the same workload.
 """
 import argparse
@@ -113,6 +114,43 @@ def cpu_baseline(wl, w_dev, lens, toks, gamma, min_seconds):
         total += time.perf_counter() - t0
         reps += 1
     return total / reps, {"reps": reps, "sample_s": total}
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def copy_ceiling(torch, dev):
+    """Measured streaming ceiling of the device (GB/s): the library's read probe
+    (sbd_stream_probe: non-temporal 16-byte loads, 8 in flight per thread, 8 workgroups per
+    CU) over 4 GiB, best of 5 runs.  Before it, a 256 MiB device copy: the calibration that
+    counter runs scale FETCH_SIZE / WRITE_SIZE by."""
+    from paper_2509_04185_amd.binding import stream_probe
+    src = torch.empty(256 * 2**20, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    buf = torch.ones(2**30, dtype=torch.float32, device=dev)
+    sink = torch.zeros(64, dtype=torch.int32, device=dev)
+    best = 0.0
+    for _ in range(5):
+        e0.record()
+        stream_probe(buf, sink)
+        e1.record()
+        torch.cuda.synchronize()
+        best = max(best, buf.numel() * 4 / (e0.elapsed_time(e1) * 1e-3) / 1e9)
+    del buf
+    torch.cuda.empty_cache()
+    return best
 
 
 def speedup_table(args):
@@ -243,13 +281,18 @@ def main():
         step()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # per-step events inside the timed region give the spread of step times
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
     e0.record()
-    for _ in range(args.steps):
+    marks[0].record()
+    for i in range(args.steps):
         out = step()
+        marks[i + 1].record()
     e1.record()
     torch.cuda.synchronize()
     ms_step = e0.elapsed_time(e1) / args.steps
+    per_step = np.array([marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)])
     n_acc = int(out[0][0])
 
     # block forward alone and EB select alone
@@ -270,11 +313,28 @@ def main():
     torch.cuda.synchronize()
     us_eb = 1000.0 * sum(ea.elapsed_time(eb) for ea, eb in evs) / args.steps
 
+    # the same step through sbd_block_step: the EB statistics come from the LM head's
+    # epilogue and the logits are neither stored nor read back
+    if B * k <= 512 and args.decode_path != "fused":
+        for _ in range(3):
+            lib.block_step(seq_ids, toks, "eb_entropy", gamma, is_mask=is_mask)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(args.steps):
+            lib.block_step(seq_ids, toks, "eb_entropy", gamma, is_mask=is_mask)
+        e1.record()
+        torch.cuda.synchronize()
+        ms_fused_step = e0.elapsed_time(e1) / args.steps
+    else:
+        ms_fused_step = None
+
     fwd_bytes, eb_bytes = step_bytes(s, lens, k)
     value = (fwd_bytes + eb_bytes) / (ms_step * 1e-3) / 1e9
+    ceiling = copy_ceiling(torch, dev)
 
     # per-kernel durations, HIP events around each launch on the library stream
     kernels = {}
+    fused_kernels = None
     roofline = None
     if not args.no_profile:
         lib.profile(True)
@@ -286,6 +346,15 @@ def main():
         lib.profile(False)
         kernels = {n: {"launches": c, "avg_us": 1000.0 * t / c if c else None}
                    for n, (c, t) in prof.items() if c}
+        if ms_fused_step is not None:
+            lib.profile(True)
+            for _ in range(args.steps):
+                lib.block_step(seq_ids, toks, "eb_entropy", gamma, is_mask=is_mask)
+            torch.cuda.synchronize()
+            fprof = lib.profile_read()
+            lib.profile(False)
+            fused_kernels = {n: {"launches": c, "avg_us": 1000.0 * t / c}
+                             for n, (c, t) in fprof.items() if c and n in ("lm_head", "eb_partial", "eb_select")}
         if prof.get("fused", (0, 0.0))[0]:
             # one launch runs every layer and the LM head: its bytes are the block forward's
             kind, bpl = "fused", fwd_bytes
@@ -311,12 +380,6 @@ def main():
                     "kernel": label, "bytes_per_launch": bpl, "avg_launch_us": round(avg_s * 1e6, 2),
                     "launches": c}
 
-    # a plain copy of known size, so counter runs can calibrate FETCH_SIZE / WRITE_SIZE
-    src = torch.empty(256 * 2**20, dtype=torch.uint8, device=dev)
-    dst = torch.empty_like(src)
-    dst.copy_(src)
-    torch.cuda.synchronize()
-    del src, dst
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -324,7 +387,7 @@ def main():
         est, info = cpu_baseline(wl, w, lens, toks, gamma, args.cpu_seconds)
         cores = blas_threads()
         cpu = {"value": round((fwd_bytes + eb_bytes) / est / 1e9, 4), "unit": "GB/s", "cores": cores,
-               "kind": "oracle", "ms_per_step": round(est * 1e3, 1),
+               "kind": "oracle", "ms_per_step": round(est * 1e3, 1), "cpu_model": cpu_model(),
                "sample": (f"fp32 numpy oracle: the whole block forward ({s.n_layers} layers + LM head) and the EB "
                           f"select on the same block, {info['reps']} runs, {info['sample_s']:.1f} s timed")}
 
@@ -339,6 +402,11 @@ def main():
         "block_forward_gbs": round(fwd_bytes / (ms_fwd * 1e-3) / 1e9, 1),
         "block_forward_frac_of_peak": round(fwd_bytes / (ms_fwd * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
         "eb_select_us": round(us_eb, 2),
+        "step_ms_p10_p50_p90": [round(float(np.percentile(per_step, q)), 4) for q in (10, 50, 90)],
+        "fused_step_ms": None if ms_fused_step is None else round(ms_fused_step, 4),
+        "fused_step_kernels": fused_kernels,
+        "copy_ceiling_gbs": round(ceiling, 1),
+        "block_forward_frac_of_ceiling": round(fwd_bytes / (ms_fwd * 1e-3) / 1e9 / ceiling, 4),
         "step_bytes": fwd_bytes + eb_bytes, "eb_accepted": n_acc,
         "roofline": roofline, "cpu_baseline": cpu, "kernels": kernels,
     }

@@ -43,6 +43,9 @@ typedef enum {
 
 typedef struct sbd_ctx sbd_ctx; /* opaque, created by sbd_create */
 
+/* Selection rules of one sampling step (sbd_select, sbd_block_step). */
+enum { SBD_SELECT_EB_ENTROPY = 0, SBD_SELECT_EB_CONFIDENCE = 1, SBD_SELECT_FACTOR = 2 };
+
 /*
  * Decoder shape (Llama-3.1 / Qwen-3 style; the SBD network has no architectural
  * changes, Sec. 1) plus capacity limits.
@@ -137,6 +140,33 @@ sbd_status sbd_block_forward(sbd_ctx* ctx, int32_t batch, const int32_t* seq_ids
                              const int32_t* n_causal, const int32_t* pos_ids, float* logits);
 
 /*
+ * One decode step in one call: sbd_block_forward followed by the selection rule `rule`
+ * (SBD_SELECT_*, threshold as for sbd_select) over the masked rows, with the selection's
+ * softmax statistics taken from the LM head itself (Sec. 2.2, eq. (eb_sampler): only each
+ * row's entropy, confidence and argmax are needed, not its logits).  The LM head's epilogue
+ * reduces every 64-column chunk of every row to (max, argmax, Z, S) in float64; a merge
+ * forms each row's entropy, confidence and token; the logits are written only when
+ * `logits` is not NULL, and never read back.
+ *   Arguments as sbd_block_forward and sbd_select; is_mask may be NULL (then the masked
+ *   set is tokens == mask_id); the column mask_id of the config is excluded.
+ *   logits    device fp32 [batch][k][vocab] or NULL.
+ *   outputs   n_accepted [batch], accepted_pos [batch][k] (row indices of the block,
+ *             ascending, then -1), accepted_tok [batch][k], entropy and confidence
+ *             [batch][k] (nullable): as sbd_select.
+ * The entropies equal sbd_select's on the same logits up to float64 summation order (the
+ * chunks differ; ~1e-12 relative); the accepted rows and tokens are the same except where
+ * a decision is that close.  Limits: batch * k <= 512 (INVALID_ARG beyond).  On the fused
+ * decode path (SBD_DECODE_FUSED) the statistics come from the stored logits, which must
+ * then be given (UNSUPPORTED otherwise).  The staged K/V and sbd_commit are as for
+ * sbd_block_forward.
+ */
+sbd_status sbd_block_step(sbd_ctx* ctx, int32_t rule, int32_t batch, const int32_t* seq_ids, int32_t k,
+                          const int32_t* tokens, const uint8_t* is_mask, const int32_t* n_causal,
+                          const int32_t* pos_ids, double threshold, float* logits, int32_t* n_accepted,
+                          int32_t* accepted_pos, int32_t* accepted_tok, double* entropy,
+                          double* confidence);
+
+/*
  * Exact KV caching (Sec. 1, advantages; Alg. 3): make the K/V staged by the last block
  * forward of each listed sequence permanent for its first n_commit[b] rows
  * (cache_len += n_commit[b]).  n_commit[b] <= that forward's n_causal[b], else STATE.
@@ -186,7 +216,6 @@ sbd_status sbd_eb_select(sbd_ctx* ctx, int32_t batch, int32_t k, int32_t vocab,
  * As for sbd_eb_select, a row with NaN statistics is never accepted.
  * Errors: INVALID_ARG for an unknown rule, otherwise as sbd_eb_select.
  */
-enum { SBD_SELECT_EB_ENTROPY = 0, SBD_SELECT_EB_CONFIDENCE = 1, SBD_SELECT_FACTOR = 2 };
 sbd_status sbd_select(sbd_ctx* ctx, int32_t rule, int32_t batch, int32_t k, int32_t vocab,
                       const float* logits, const uint8_t* is_mask, double threshold, int32_t mask_id,
                       int32_t* n_accepted, int32_t* accepted_pos, int32_t* accepted_tok, double* entropy,
@@ -311,6 +340,14 @@ typedef enum {
   SBD_KERNEL_COUNT = 15
 } sbd_kernel;
 sbd_status sbd_profile_enable(sbd_ctx* ctx, int32_t enable);
+/*
+ * Measurement aid: one read of `bytes` of device memory at `buf` (a positive multiple of
+ * 16) by a plain streaming kernel on `stream` (NULL = the null stream), the device's
+ * achievable read rate to compare the block forward's weight streams with.  sink: device
+ * uint32 [64], written practically never (it keeps the loads from being dropped).  No
+ * context needed; errors through sbd_last_error(NULL).
+ */
+sbd_status sbd_stream_probe(void* stream, const void* buf, size_t bytes, uint32_t* sink);
 sbd_status sbd_profile_read(sbd_ctx* ctx, int32_t kernel, int32_t* launches, double* total_ms);
 
 const char* sbd_status_string(sbd_status s);

@@ -42,6 +42,8 @@ SIGNATURES = {
     "sbd_block_forward": [c_void_p, c_int32, c_void_p, c_int32, c_void_p, c_void_p, c_void_p,
                           c_void_p, c_void_p],
     "sbd_commit": [c_void_p, c_int32, c_void_p, c_void_p],
+    "sbd_block_step": [c_void_p, c_int32, c_int32, c_void_p, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
+                       c_double, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p],
     "sbd_eb_select": [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p, c_double, c_int32,
                       c_void_p, c_void_p, c_void_p, c_void_p],
     "sbd_select": [c_void_p, c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p, c_double, c_int32,
@@ -56,6 +58,7 @@ SIGNATURES = {
     "sbd_decode_path_fits": [c_void_p, c_int32, c_int32, c_int32, POINTER(c_int32)],
     "sbd_set_wait_limit": [c_void_p, c_int32],
     "sbd_profile_enable": [c_void_p, c_int32],
+    "sbd_stream_probe": [c_void_p, c_void_p, c_size_t, c_void_p],
     "sbd_profile_read": [c_void_p, c_int32, POINTER(c_int32), POINTER(c_double)],
     "sbd_status_string": [c_int32],
     "sbd_last_error": [c_void_p],
@@ -221,6 +224,27 @@ class Sbd:
                    _ptr(pos), _dev(out))
         return out
 
+    def block_step(self, seq_ids, tokens, rule: str = "eb_entropy", threshold: float = 1.0, is_mask=None,
+                   n_causal=None, pos_ids=None, want_logits: bool = False):
+        """sbd_block_step: block forward + selection with the statistics from the LM head.
+        Returns (n_accepted, accepted_pos, accepted_tok, entropy, confidence, logits or None)."""
+        seq = _host(seq_ids, np.int32).reshape(-1)
+        toks = _host(tokens, np.int32)
+        B, k = toks.shape
+        msk = None if is_mask is None else _host(is_mask, np.uint8)
+        nc = None if n_causal is None else _host(n_causal, np.int32)
+        pos = None if pos_ids is None else _host(pos_ids, np.int32)
+        dev = self.device
+        logits = torch.empty((B, k, self.shape.vocab), dtype=torch.float32, device=dev) if want_logits else None
+        n_acc = torch.empty(B, dtype=torch.int32, device=dev)
+        acc_pos = torch.empty((B, k), dtype=torch.int32, device=dev)
+        acc_tok = torch.empty((B, k), dtype=torch.int32, device=dev)
+        H = torch.empty((B, k), dtype=torch.float64, device=dev)
+        C = torch.empty((B, k), dtype=torch.float64, device=dev)
+        self._call("sbd_block_step", SELECT_RULES[rule], B, _ptr(seq), k, _ptr(toks), _ptr(msk), _ptr(nc), _ptr(pos),
+                   float(threshold), _dev(logits), _dev(n_acc), _dev(acc_pos), _dev(acc_tok), _dev(H), _dev(C))
+        return n_acc, acc_pos, acc_tok, H, C, logits
+
     def commit(self, seq_ids, n_commit):
         seq = _host(seq_ids, np.int32).reshape(-1)
         n = _host(n_commit, np.int32).reshape(-1)
@@ -328,6 +352,14 @@ def eb_select_noalloc(logits: torch.Tensor, is_mask, gamma: float, mask_id: int,
     _check(lib, lib.sbd_eb_select_noalloc(stream, B, k, V, _dev(logits), _ptr(msk), float(gamma), int(mask_id),
                                           _dev(n_acc), _dev(pos), _dev(tok), _dev(H)), "sbd_eb_select_noalloc")
     return n_acc, pos, tok, H
+
+
+def stream_probe(buf: torch.Tensor, sink: torch.Tensor):
+    """sbd_stream_probe on torch's current stream: one streaming read of the whole tensor."""
+    lib = load_library()
+    stream = c_void_p(torch.cuda.current_stream(buf.device).cuda_stream)
+    _check(lib, lib.sbd_stream_probe(stream, _dev(buf), buf.numel() * buf.element_size(), _dev(sink)),
+           "sbd_stream_probe")
 
 
 def status_string(status: int) -> str:

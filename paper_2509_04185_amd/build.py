@@ -10,7 +10,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libsbd.so")
 SOURCES = ["sbd_api.cpp", "gemm.hip", "gemv.hip", "fused.hip", "layer_xcd.hip", "attention.hip", "misc.hip",
-           "eb.hip"]
+           "eb.hip", "probe.hip"]
 ARCH = "gfx950"
 
 # -packed-fp32-ops: keep the compiler from forming packed fp32 instructions.

@@ -19,17 +19,9 @@
 
 #include <mutex>
 
-#include "sbd_device.h"
+#include "eb_stats.h"
 
 namespace sbd {
-
-__device__ __forceinline__ double shfl_xor_d(double v, int m) {
-  const int2 iv = *reinterpret_cast<int2*>(&v);
-  int2 o;
-  o.x = __shfl_xor(iv.x, m);
-  o.y = __shfl_xor(iv.y, m);
-  return *reinterpret_cast<double*>(&o);
-}
 
 constexpr int kEbThreads = 256;
 constexpr int kEbPer = kEbChunk / kEbThreads;  // 16 entries per thread
@@ -141,7 +133,12 @@ constexpr int kEbSelWaves = 16;
 
 // One workgroup (16 waves) per sequence.  Wave w merges the chunk statistics of rows
 // w, w + 16, ... with one lane per chunk; wave 0 then ranks and selects.
-template <bool SELECT_ONLY>
+// MODE: kFromChunks (the partial kernel's chunk statistics, merged here), kFromEntropies
+// (given entropies, no tokens), kFromRows (per-row entropy, confidence and token from
+// eb_merge_kernel).
+enum { kFromChunks = 0, kFromEntropies = 1, kFromRows = 2 };
+
+template <int MODE>
 __global__ __launch_bounds__(64 * kEbSelWaves) void eb_select_kernel(EbArgs a) {
   __shared__ double sh[64];
   __shared__ double sconf[64];
@@ -162,8 +159,12 @@ __global__ __launch_bounds__(64 * kEbSelWaves) void eb_select_kernel(EbArgs a) {
     double H = 0.0, conf = 0.0;
     int tok = -1;
     if (masked) {
-      if (SELECT_ONLY) {
+      if (MODE == kFromEntropies) {
         H = a.entropy_in[row];
+      } else if (MODE == kFromRows) {
+        H = a.row_stats[row * 2];
+        conf = a.row_stats[row * 2 + 1];
+        tok = a.row_tok[row];
       } else {
         const double* p = a.part + row * a.n_chunks * 3;
         const int* pa = a.part_arg + row * a.n_chunks;
@@ -334,9 +335,114 @@ hipError_t launch_eb_partial(const EbArgs& a, const Exec& ex) {
 
 hipError_t launch_eb_select(const EbArgs& a, bool select_only, const Exec& ex) {
   if (select_only)
-    SBD_KLAUNCH(eb_select_kernel<true>, dim3(a.B), dim3(64 * kEbSelWaves), ex, a);
+    SBD_KLAUNCH(eb_select_kernel<kFromEntropies>, dim3(a.B), dim3(64 * kEbSelWaves), ex, a);
+  else if (a.row_stats != nullptr)
+    SBD_KLAUNCH(eb_select_kernel<kFromRows>, dim3(a.B), dim3(64 * kEbSelWaves), ex, a);
   else
-    SBD_KLAUNCH(eb_select_kernel<false>, dim3(a.B), dim3(64 * kEbSelWaves), ex, a);
+    SBD_KLAUNCH(eb_select_kernel<kFromChunks>, dim3(a.B), dim3(64 * kEbSelWaves), ex, a);
+  return hipGetLastError();
+}
+
+// ---- rows of many chunks: the statistics of the LM head's 64-column chunks
+//
+// One workgroup of 512 threads per masked row.  Thread t takes chunks t, t + 512, ... (at
+// most kMergePer: vocabularies up to 512 * 8 * 64 = 262144 entries), all loaded up front.
+// M = max m_c (fixed reduction), the first chunk reaching M gives the token; then with
+// delta_c = m_c - M, Z = sum_c e^delta_c Z_c and S = sum_c e^delta_c (S_c + delta_c Z_c),
+// summed per thread in chunk order and then over lanes and waves in a fixed order; H =
+// log Z - S / Z and the confidence 1 / Z, as the chunk merge of eb_select_kernel.
+constexpr int kMergeThreads = 512;
+constexpr int kMergePer = 8;
+
+__global__ __launch_bounds__(kMergeThreads) void eb_merge_kernel(EbArgs a) {
+  const int64_t row = blockIdx.x;
+  if (a.is_mask == nullptr && !eb_row_masked(a, row)) return;
+  __shared__ double red_d[2][kMergeThreads / 64];
+  __shared__ int red_i[kMergeThreads / 64];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const double* p = a.part + row * a.n_chunks * 3;
+  const int32_t* pa = a.part_arg + row * a.n_chunks;
+  double mc[kMergePer], zc[kMergePer], sc[kMergePer];
+  int ac[kMergePer];
+#pragma unroll
+  for (int i = 0; i < kMergePer; ++i) {  // clamped indices: every load is in flight at once
+    const int c = min(tid + i * kMergeThreads, a.n_chunks - 1);
+    mc[i] = p[c * 3];
+    zc[i] = p[c * 3 + 1];
+    sc[i] = p[c * 3 + 2];
+    ac[i] = pa[c];
+  }
+  const bool masked = a.is_mask == nullptr || eb_row_masked(a, row);
+#pragma unroll
+  for (int i = 0; i < kMergePer; ++i)
+    if (tid + i * kMergeThreads >= a.n_chunks) mc[i] = -INFINITY;
+  double mloc = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < kMergePer; ++i) mloc = fmax(mloc, mc[i]);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) mloc = fmax(mloc, shfl_xor_d(mloc, o));
+  if (lane == 0) red_d[0][w] = mloc;
+  __syncthreads();
+  double M = red_d[0][0];
+#pragma unroll
+  for (int i = 1; i < kMergeThreads / 64; ++i) M = fmax(M, red_d[0][i]);
+  // the first chunk reaching M (none when every chunk is -inf)
+  int cfirst = INT32_MAX;
+#pragma unroll
+  for (int i = kMergePer - 1; i >= 0; --i)
+    if (mc[i] != -INFINITY && mc[i] == M) cfirst = tid + i * kMergeThreads;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) cfirst = min(cfirst, __shfl_xor(cfirst, o));
+  double z = 0.0, s = 0.0;
+#pragma unroll
+  for (int i = 0; i < kMergePer; ++i) {
+    if (mc[i] != -INFINITY) {
+      const double d = mc[i] - M;
+      const double f = exp(d);
+      z += f * zc[i];
+      s += f * (sc[i] + d * zc[i]);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    z += shfl_xor_d(z, o);
+    s += shfl_xor_d(s, o);
+  }
+  __syncthreads();  // every thread has read red_d[0]
+  if (lane == 0) {
+    red_d[0][w] = z;
+    red_d[1][w] = s;
+    red_i[w] = cfirst;
+  }
+  __syncthreads();
+  if (tid == 0 && masked) {
+    double Z = 0.0, S = 0.0;
+    int cmin = INT32_MAX;
+    for (int i = 0; i < kMergeThreads / 64; ++i) {
+      Z += red_d[0][i];
+      S += red_d[1][i];
+      cmin = min(cmin, red_i[i]);
+    }
+    double H, conf;
+    int tok;
+    if (cmin == INT32_MAX) {  // no finite logit in the row
+      H = conf = __builtin_nan("");
+      tok = -1;
+    } else {
+      H = log(Z) - S / Z;
+      conf = 1.0 / Z;
+      tok = pa[cmin];
+    }
+    a.row_stats[row * 2] = H;
+    a.row_stats[row * 2 + 1] = conf;
+    a.row_tok[row] = tok;
+  }
+}
+
+hipError_t launch_eb_merge(const EbArgs& a, const Exec& ex) {
+  if (a.n_chunks < 1 || a.n_chunks > kMergeThreads * kMergePer || a.row_stats == nullptr || a.row_tok == nullptr)
+    return hipErrorInvalidValue;
+  SBD_KLAUNCH(eb_merge_kernel, dim3(a.B * a.k), dim3(kMergeThreads), ex, a);
   return hipGetLastError();
 }
 

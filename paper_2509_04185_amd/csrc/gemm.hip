@@ -28,6 +28,8 @@
 // Epilogues (acc in the MFMA D layout: lane l holds column l % 16 of a tile, rows
 // 4*(l/16) + i):
 //   EPI_SCALED_STORE  out = rinv[m] * y           (QKV projection, LM head)
+//   EPI_LOGITS_EB     the same (stores optional) plus the EB softmax statistics of every
+//                     row's 64-column chunks (LM head; eb_stats.h)
 //   EPI_RESID         x += y; xn = x * g_next as hi/lo; the sum of x^2 over the block's
 //                     columns per row (O and down projections: residual add, the next
 //                     RMSNorm's inputs)
@@ -40,7 +42,7 @@
 #include <algorithm>
 #include <utility>
 
-#include "sbd_device.h"
+#include "eb_stats.h"
 
 namespace sbd {
 
@@ -378,6 +380,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
         const f32x4 y = *(const f32x4*)(stg + row * LDR + pc * 4);
         if constexpr (EPI == EPI_SCALED_STORE) {
           if (m < a.M) *(f32x4*)(a.out_f32 + (int64_t)m * a.ldo + n) = y * rinv_s[rl0 + row];
+        } else if constexpr (EPI == EPI_LOGITS_EB) {
+          if (m < a.M && a.out_f32 != nullptr) *(f32x4*)(a.out_f32 + (int64_t)m * a.ldo + n) = y * rinv_s[rl0 + row];
         } else {  // EPI_RESID
           float s2 = 0.f;
           if (m < a.M) {
@@ -400,6 +404,20 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
           if (pc == 0) ssq_s[wc][rl0 + row] = s2;
         }
       }
+    }
+    if constexpr (EPI == EPI_LOGITS_EB) {
+      // the staged row tile again: lane L reduces VPL = 4 CW consecutive columns of row L / 4,
+      // 16 / CW lanes per 64-column chunk
+      constexpr int VPL = 4 * CW, LPC = 16 / CW;
+      static_assert(VPL * LPC == kEbFChunk, "a chunk is 64 columns");
+      const int row = lane >> 2, seg = lane & 3;
+      const int m = row0 + rl0 + row;
+      const int col0 = n_w0 + seg * VPL;
+      float mx;
+      int arg;
+      double z, sz;
+      eb_seg_stats<VPL, LPC>(stg + row * LDR + seg * VPL, rinv_s[rl0 + row], col0, a.eb_mask_id, mx, arg, z, sz);
+      if (seg % LPC == 0 && m < a.M) eb_chunk_store(a.eb_part, a.eb_arg, a.eb_chunks, m, col0 / kEbFChunk, mx, arg, z, sz);
     }
     if constexpr (EPI == EPI_RESID) {
 #pragma unroll
@@ -488,7 +506,9 @@ hipError_t launch_gemm(GemmEpi epi, const GemmArgs& a0, const Exec& ex) {
   if (epi == EPI_RESID && a0.n_part_out != p.n_cb) return hipErrorInvalidValue;
   // the epilogue writes 16-byte (fp32) and 8-byte (bf16) pieces of 4 columns
   if ((epi == EPI_SCALED_STORE && a0.ldo % 4) || (epi == EPI_RESID && a0.ldx % 4) ||
-      (epi == EPI_SWIGLU && a0.ld_act % 4))
+      (epi == EPI_SWIGLU && a0.ld_act % 4) || (epi == EPI_LOGITS_EB && a0.out_f32 && a0.ldo % 4))
+    return hipErrorInvalidValue;
+  if (epi == EPI_LOGITS_EB && (a0.eb_part == nullptr || a0.eb_arg == nullptr || a0.eb_chunks * kEbFChunk != a0.n_tiles * 16))
     return hipErrorInvalidValue;
   GemmArgs a = a0;
   a.splits = p.splits;
@@ -497,6 +517,7 @@ hipError_t launch_gemm(GemmEpi epi, const GemmArgs& a0, const Exec& ex) {
     case EPI_SCALED_STORE: launch_epi<EPI_SCALED_STORE>(a, p.mt, p.nt, ex); break;
     case EPI_RESID: launch_epi<EPI_RESID>(a, p.mt, p.nt, ex); break;
     case EPI_SWIGLU: launch_epi<EPI_SWIGLU>(a, p.mt, p.nt, ex); break;
+    case EPI_LOGITS_EB: launch_epi<EPI_LOGITS_EB>(a, p.mt, p.nt, ex); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -20,6 +20,8 @@
 // Epilogues (acc in the v_mfma_f32_16x16x32_bf16 D layout: lane l holds column l % 16 of
 // a tile, rows 4*(l/16) + i):
 //   EPI_SCALED_STORE  out = rinv[m] * y                      (LM head)
+//   EPI_LOGITS_EB     the same (stores optional) plus, per row and 64-column chunk (4 of
+//                     the C = 8 tiles), the EB softmax statistics (eb_stats.h)
 //   EPI_RESID         x += y; xn = x * g_next as hi/lo bf16; one partial sum of x^2 per
 //                     row and workgroup for the next RMSNorm (O, down projections)
 //   EPI_SWIGLU        act = silu(rinv*gate) * rinv*up as hi/lo (gate/up: packed tile t
@@ -34,6 +36,7 @@
 
 #include <algorithm>
 
+#include "eb_stats.h"
 #include "gemv_body.h"
 #include "qkv_epilogue.h"
 
@@ -184,6 +187,28 @@ __global__ __launch_bounds__(NW * 64) void gemv_kernel(GemvArgs a) {
     }
     qkv_epilogue<DH>(a.qkv, a.M, sub, acc, rinv, qpre);
     return;
+  } else if constexpr (EPI == EPI_LOGITS_EB) {
+    static_assert(C == 8 && NW == 1, "the logits statistics take whole groups in one wave");
+    // the logits as EPI_SCALED_STORE; the fp32 products staged in LDS as [16 rows][128
+    // columns]; then lane L reduces 32 columns of row L / 4 (quarter L % 4), two lanes per
+    // 64-column chunk
+    __shared__ __attribute__((aligned(16))) float st[16][8 * 16 + 4];
+#pragma unroll
+    for (int ct = 0; ct < C; ++ct)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = 4 * g + i;
+        if (a.out_f32 != nullptr && m < a.M) a.out_f32[(int64_t)m * a.ldo + (t0 + ct) * 16 + r] = acc[ct][i] * rinv[i];
+        st[m][ct * 16 + r] = acc[ct][i];
+      }
+    __builtin_amdgcn_wave_barrier();
+    const int row = lane >> 2, seg = lane & 3;
+    float mx;
+    int arg;
+    double z, sz;
+    eb_seg_stats<32, 2>(&st[row][seg * 32], a.sumsq_in != nullptr ? rinv_s[row] : 1.f, t0 * 16 + seg * 32, a.eb_mask_id, mx, arg, z, sz);
+    if ((seg & 1) == 0 && row < a.M) eb_chunk_store(a.eb_part, a.eb_arg, a.eb_chunks, row, t0 / 4 + seg / 2, mx, arg, z, sz);
+    return;
   } else {
 #pragma unroll
     for (int ct = 0; ct < C; ++ct) {
@@ -278,24 +303,32 @@ GemvShape gemv_pick(GemmEpi epi, int n_tiles, int K) {
 template <int EPI, int DH = 128>
 static bool dispatch(const GemvArgs& a, GemvShape sh, const Exec& ex) {
   const int c = sh.C * 1000 + sh.NW * 10 + sh.U;
-  switch (c) {
-    case 8041: launch_gemv_cfg<8, 4, 1, EPI, DH>(a, sh.KS, ex); return true;
-    case 8012: launch_gemv_cfg<8, 1, 2, EPI, DH>(a, sh.KS, ex); return true;
-    default: break;
-  }
-  if constexpr (EPI != EPI_QKV) {
+  if constexpr (EPI == EPI_LOGITS_EB) {  // one shape: whole groups, one wave, no split
+    if (c != 8012 || sh.KS != 1) return false;
+    launch_gemv_cfg<8, 1, 2, EPI>(a, 1, ex);
+    return true;
+  } else {
     switch (c) {
-      case 4084: launch_gemv_cfg<4, 8, 4, EPI>(a, sh.KS, ex); return true;
-      case 4082: launch_gemv_cfg<4, 8, 2, EPI>(a, sh.KS, ex); return true;
+      case 8041: launch_gemv_cfg<8, 4, 1, EPI, DH>(a, sh.KS, ex); return true;
+      case 8012: launch_gemv_cfg<8, 1, 2, EPI, DH>(a, sh.KS, ex); return true;
       default: break;
     }
+    if constexpr (EPI != EPI_QKV) {
+      switch (c) {
+        case 4084: launch_gemv_cfg<4, 8, 4, EPI>(a, sh.KS, ex); return true;
+        case 4082: launch_gemv_cfg<4, 8, 2, EPI>(a, sh.KS, ex); return true;
+        default: break;
+      }
+    }
+    return false;
   }
-  return false;
 }
 
 hipError_t launch_gemv(GemmEpi epi, const GemvArgs& a, GemvShape sh, const Exec& ex) {
   if (a.M < 1 || a.M > 16 || a.K < 32 || a.K % 32 || a.n_tiles < 8 || a.n_tiles % 8) return hipErrorInvalidValue;
-  if (sh.C == 0) sh = gemv_pick(epi, a.n_tiles, a.K);
+  if (sh.C == 0) sh = epi == EPI_LOGITS_EB ? GemvShape{8, 1, 2, 1} : gemv_pick(epi, a.n_tiles, a.K);
+  if (epi == EPI_LOGITS_EB && (a.eb_part == nullptr || a.eb_arg == nullptr || a.eb_chunks * kEbFChunk != a.n_tiles * 16))
+    return hipErrorInvalidValue;
   if (sh.KS < 1 || sh.KS > kGemvMaxSplit || a.n_tiles % sh.C) return hipErrorInvalidValue;
   if (sh.KS > 1 && (int64_t)(a.n_tiles / sh.C + 7) / 8 * 8 * kCtrStride > kLayerCtr0) return hipErrorInvalidValue;
   if (sh.KS > 1 && a.counters == nullptr) return hipErrorInvalidValue;
@@ -314,6 +347,7 @@ hipError_t launch_gemv(GemmEpi epi, const GemvArgs& a, GemvShape sh, const Exec&
     case EPI_RESID: ok = dispatch<EPI_RESID>(a, sh, ex); break;
     case EPI_SWIGLU: ok = dispatch<EPI_SWIGLU>(a, sh, ex); break;
     case EPI_SCALED_STORE: ok = dispatch<EPI_SCALED_STORE>(a, sh, ex); break;
+    case EPI_LOGITS_EB: ok = dispatch<EPI_LOGITS_EB>(a, sh, ex); break;
   }
   if (!ok) return hipErrorInvalidValue;
   return hipGetLastError();

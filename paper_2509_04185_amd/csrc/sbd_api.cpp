@@ -84,6 +84,12 @@ bool sbd::compute_layout(const sbd_model_config& c, Layout* L) {
   o.eb_mask = take(eb_rows);
   o.eb_part = take(eb_rows * o.eb_chunks * 3 * sizeof(double));
   o.eb_arg = take(eb_rows * o.eb_chunks * sizeof(int32_t));
+  o.eb_frows = std::min<int64_t>(eb_rows, kStepMaxRows);
+  o.eb_fchunks = c.vocab / kEbFChunk;
+  o.eb_fpart = take(o.eb_frows * o.eb_fchunks * 3 * sizeof(double));
+  o.eb_farg = take(o.eb_frows * o.eb_fchunks * sizeof(int32_t));
+  o.eb_rowstat = take(o.eb_frows * 2 * sizeof(double));
+  o.eb_rowtok = take(o.eb_frows * sizeof(int32_t));
   // packed weights: per layer qkv [n_qkv][d], o [d][qd], gate/up [2F][d], down [d][F]
   o.wp_o = o.n_qkv * c.d_model;
   o.wp_gu = o.wp_o + (int64_t)c.d_model * qd;
@@ -244,10 +250,18 @@ int pick_splits(int64_t work_groups_per_split, int nblocks, int n_cu) {
   return s;
 }
 
+// The LM head's EB statistics (sbd_block_step): 64-column chunk statistics of every row.
+struct LmEb {
+  double* part;
+  int32_t* arg;
+  int chunks, mask_id;
+};
+
 // One forward of B sequences x k rows whose per-row / per-sequence parameters are given.
-// lm_row < 0: logits for all rows into `logits`; otherwise only for row lm_row.
+// lm_row < 0: logits for all rows into `logits`; otherwise only for row lm_row.  eb: the LM
+// head also writes the EB chunk statistics of all rows (logits may then be null).
 sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& rows,
-                       const std::vector<SeqParam>& seqs, float* logits, int lm_row) {
+                       const std::vector<SeqParam>& seqs, float* logits, int lm_row, const LmEb* eb = nullptr) {
   const sbd_model_config& m = c->cfg;
   const Layout& L = c->lay;
   const int M = B * k;
@@ -459,16 +473,18 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     }
   }
 
-  if (logits != nullptr) {
+  if (logits != nullptr || eb != nullptr) {
     const int r0 = lm_row < 0 ? 0 : lm_row;
     const int Ml = lm_row < 0 ? M : 1;
+    const GemmEpi lm_epi = eb ? EPI_LOGITS_EB : EPI_SCALED_STORE;
     if (mt == 0) {  // M <= 16: row-major inputs
       GemvArgs v = gemv_base(xn + (int64_t)r0 * d, xn_lo + (int64_t)r0 * d, d, Ml, d,
                              c->at<bf16_t>(L.wpack) + L.wp_lm, m.vocab / 16, vpart, vpart_cap, counters);
       v.sumsq_in = sumsq + (int64_t)r0 * n_part_cur; v.n_part_in = n_part_cur;
       v.inv_d = 1.0f / d; v.eps = m.rms_eps;
       v.out_f32 = logits; v.ldo = m.vocab;
-      SBD_LAUNCH(c, SBD_KERNEL_LM_HEAD, launch_gemv(EPI_SCALED_STORE, v, GemvShape{}, ex));
+      if (eb) { v.eb_part = eb->part; v.eb_arg = eb->arg; v.eb_chunks = eb->chunks; v.eb_mask_id = eb->mask_id; }
+      SBD_LAUNCH(c, SBD_KERNEL_LM_HEAD, launch_gemv(lm_epi, v, GemvShape{}, ex));
     } else {
       // inputs in fragment order (also for one row of a prefill chunk: rows from a_row0)
       GemmArgs gl = gemm_base(xn, xn_lo, d, Ml, d, c->at<bf16_t>(L.wpack) + L.wp_lm, m.vocab / 16, vpart,
@@ -477,7 +493,8 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
       gl.out_f32 = logits; gl.ldo = m.vocab;
       gl.sumsq_in = sumsq + (int64_t)r0 * n_part_cur; gl.n_part = n_part_cur;
       gl.inv_d = 1.0f / d; gl.eps = m.rms_eps;
-      SBD_LAUNCH(c, SBD_KERNEL_LM_HEAD, launch_gemm(EPI_SCALED_STORE, gl, ex));
+      if (eb) { gl.eb_part = eb->part; gl.eb_arg = eb->arg; gl.eb_chunks = eb->chunks; gl.eb_mask_id = eb->mask_id; }
+      SBD_LAUNCH(c, SBD_KERNEL_LM_HEAD, launch_gemm(lm_epi, gl, ex));
     }
   }
   return SBD_OK;
@@ -709,14 +726,19 @@ sbd_status sbd_prefill(sbd_ctx* c, int32_t seq, const int32_t* tokens, int32_t n
   return SBD_OK;
 }
 
-sbd_status sbd_block_forward(sbd_ctx* c, int32_t batch, const int32_t* seq_ids, int32_t k,
-                             const int32_t* tokens, const uint8_t* is_mask, const int32_t* n_causal,
-                             const int32_t* pos_ids, float* logits) {
-  if (!c) return fail(nullptr, SBD_ERR_INVALID_ARG, "null context");
+}  // extern "C"
+
+namespace {
+
+// Validation of a block forward's arguments and state (nothing is changed or enqueued), and
+// its per-row and per-sequence parameters.
+sbd_status prepare_block(sbd_ctx* c, int32_t batch, const int32_t* seq_ids, int32_t k, const int32_t* tokens,
+                         const uint8_t* is_mask, const int32_t* n_causal, const int32_t* pos_ids,
+                         std::vector<RowParam>* rows, std::vector<SeqParam>* seqs) {
   const sbd_model_config& m = c->cfg;
   if (batch < 1 || batch > m.max_batch) return fail(c, SBD_ERR_INVALID_ARG, "batch %d out of [1, %d]", batch, m.max_batch);
   if (k < 1 || k > m.max_block) return fail(c, SBD_ERR_INVALID_ARG, "k %d out of [1, %d]", k, m.max_block);
-  if (!seq_ids || !tokens || !logits) return fail(c, SBD_ERR_INVALID_ARG, "null argument");
+  if (!seq_ids || !tokens) return fail(c, SBD_ERR_INVALID_ARG, "null argument");
   std::vector<char> seen(m.max_batch, 0);
   for (int b = 0; b < batch; ++b) {
     const int s = seq_ids[b];
@@ -742,18 +764,96 @@ sbd_status sbd_block_forward(sbd_ctx* c, int32_t batch, const int32_t* seq_ids, 
       }
     }
   }
-  if (sbd_status st = check_sticky(c)) return st;
-  std::vector<RowParam> rows((size_t)batch * k);
-  std::vector<SeqParam> seqs(batch);
+  rows->resize((size_t)batch * k);
+  seqs->resize(batch);
   for (int b = 0; b < batch; ++b) {
     const int s = seq_ids[b];
-    seqs[b] = SeqParam{s, c->cache_len[s], n_causal ? n_causal[b] : 1, 0};
+    (*seqs)[b] = SeqParam{s, c->cache_len[s], n_causal ? n_causal[b] : 1, 0};
     for (int j = 0; j < k; ++j)
-      rows[b * k + j] = RowParam{tokens[b * k + j], pos_ids ? pos_ids[b * k + j] : c->cache_len[s] + j};
+      (*rows)[b * k + j] = RowParam{tokens[b * k + j], pos_ids ? pos_ids[b * k + j] : c->cache_len[s] + j};
   }
+  return SBD_OK;
+}
+
+// The masks of an EB selection into the kernel arguments (by value up to kEbInlineRows rows,
+// else uploaded into the workspace).
+sbd_status eb_masks(sbd_ctx* c, EbArgs* a, const uint8_t* is_mask, int64_t rows) {
+  if (rows <= kEbInlineRows) {
+    for (int64_t i = 0; i < rows; ++i)
+      if (is_mask[i]) a->mask_bits[i >> 6] |= 1ull << (i & 63);
+    return SBD_OK;
+  }
+  if (sbd_status st = upload(c, c->ws + c->lay.eb_mask, is_mask, (size_t)rows)) return st;
+  a->is_mask = c->at<uint8_t>(c->lay.eb_mask);
+  return SBD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+sbd_status sbd_block_forward(sbd_ctx* c, int32_t batch, const int32_t* seq_ids, int32_t k,
+                             const int32_t* tokens, const uint8_t* is_mask, const int32_t* n_causal,
+                             const int32_t* pos_ids, float* logits) {
+  if (!c) return fail(nullptr, SBD_ERR_INVALID_ARG, "null context");
+  std::vector<RowParam> rows;
+  std::vector<SeqParam> seqs;
+  if (sbd_status st = prepare_block(c, batch, seq_ids, k, tokens, is_mask, n_causal, pos_ids, &rows, &seqs)) return st;
+  if (!logits) return fail(c, SBD_ERR_INVALID_ARG, "null argument");
+  if (sbd_status st = check_sticky(c)) return st;
   sbd_status st = run_forward(c, batch, k, rows, seqs, logits, -1);
   if (st) return st;
   for (int b = 0; b < batch; ++b) c->staged[seq_ids[b]] = seqs[b].n_causal;
+  return SBD_OK;
+}
+
+sbd_status sbd_block_step(sbd_ctx* c, int32_t rule, int32_t batch, const int32_t* seq_ids, int32_t k,
+                          const int32_t* tokens, const uint8_t* is_mask, const int32_t* n_causal,
+                          const int32_t* pos_ids, double threshold, float* logits, int32_t* n_accepted,
+                          int32_t* accepted_pos, int32_t* accepted_tok, double* entropy, double* confidence) {
+  if (!c) return fail(nullptr, SBD_ERR_INVALID_ARG, "null context");
+  std::vector<RowParam> rows;
+  std::vector<SeqParam> seqs;
+  if (sbd_status st = prepare_block(c, batch, seq_ids, k, tokens, is_mask, n_causal, pos_ids, &rows, &seqs)) return st;
+  if (rule != SBD_SELECT_EB_ENTROPY && rule != SBD_SELECT_EB_CONFIDENCE && rule != SBD_SELECT_FACTOR)
+    return fail(c, SBD_ERR_INVALID_ARG, "unknown selection rule %d", rule);
+  if (std::isnan(threshold) || threshold < 0.0)
+    return fail(c, SBD_ERR_INVALID_ARG, "threshold must be >= 0 (got %g)", threshold);
+  if (!n_accepted || !accepted_pos || !accepted_tok) return fail(c, SBD_ERR_INVALID_ARG, "null argument");
+  const sbd_model_config& m = c->cfg;
+  const int64_t M = (int64_t)batch * k;
+  if (M > c->lay.eb_frows)
+    return fail(c, SBD_ERR_INVALID_ARG, "batch * k = %lld exceeds the %lld rows of one block step", (long long)M,
+                (long long)c->lay.eb_frows);
+  if (c->lay.eb_fchunks > 4096)
+    return fail(c, SBD_ERR_UNSUPPORTED, "the block step merges at most 4096 chunks of 64 columns (vocab <= 262144)");
+  // the fused decode forward has its own LM head: its statistics come from stored logits
+  const bool stored = M <= 16 && c->decode_path == SBD_DECODE_FUSED;
+  if (stored && !logits)
+    return fail(c, SBD_ERR_UNSUPPORTED, "the fused decode path takes its statistics from stored logits: pass logits");
+  if (sbd_status st = check_sticky(c)) return st;
+  std::vector<uint8_t> msk((size_t)M);
+  for (int64_t i = 0; i < M; ++i) msk[i] = is_mask ? (is_mask[i] != 0) : (tokens[i] == m.mask_id);
+  LmEb eb{c->at<double>(c->lay.eb_fpart), c->at<int32_t>(c->lay.eb_farg), (int)c->lay.eb_fchunks, m.mask_id};
+  sbd_status st = run_forward(c, batch, k, rows, seqs, logits, -1, stored ? nullptr : &eb);
+  if (st) return st;
+  for (int b = 0; b < batch; ++b) c->staged[seq_ids[b]] = seqs[b].n_causal;
+  EbArgs a{};
+  if ((st = eb_masks(c, &a, msk.data(), M))) return st;
+  a.B = batch; a.k = k; a.vocab = m.vocab; a.mask_id = m.mask_id; a.logits = logits; a.gamma = threshold;
+  a.n_accepted = n_accepted; a.accepted_pos = accepted_pos; a.accepted_tok = accepted_tok;
+  a.entropy_out = entropy; a.rule = rule; a.conf_out = confidence;
+  if (stored) {
+    a.n_chunks = (m.vocab + kEbChunk - 1) / kEbChunk;
+    a.part = c->at<double>(c->lay.eb_part); a.part_arg = c->at<int32_t>(c->lay.eb_arg);
+    SBD_LAUNCH(c, SBD_KERNEL_EB_PARTIAL, launch_eb_partial(a, ex));
+  } else {
+    a.n_chunks = (int)c->lay.eb_fchunks;
+    a.part = eb.part; a.part_arg = eb.arg;
+    a.row_stats = c->at<double>(c->lay.eb_rowstat); a.row_tok = c->at<int32_t>(c->lay.eb_rowtok);
+    SBD_LAUNCH(c, SBD_KERNEL_EB_PARTIAL, launch_eb_merge(a, ex));
+  }
+  SBD_LAUNCH(c, SBD_KERNEL_EB_SELECT, launch_eb_select(a, false, ex));
   return SBD_OK;
 }
 
@@ -807,14 +907,8 @@ sbd_status sbd_select(sbd_ctx* c, int32_t rule, int32_t batch, int32_t k, int32_
   if (mask_id < -1 || mask_id >= vocab) return fail(c, SBD_ERR_INVALID_ARG, "mask_id %d out of [-1, vocab)", mask_id);
   if (sbd_status st = check_sticky(c)) return st;
   EbArgs a{};
-  const int64_t rows = (int64_t)batch * k;
-  if (rows <= kEbInlineRows) {  // by value: no copy on the stream ahead of the kernels
-    for (int64_t i = 0; i < rows; ++i)
-      if (is_mask[i]) a.mask_bits[i >> 6] |= 1ull << (i & 63);
-  } else {
-    if (sbd_status st = upload(c, c->ws + c->lay.eb_mask, is_mask, (size_t)rows)) return st;
-    a.is_mask = c->at<uint8_t>(c->lay.eb_mask);
-  }
+  // masks by value where they fit: no copy on the stream ahead of the kernels
+  if (sbd_status st = eb_masks(c, &a, is_mask, (int64_t)batch * k)) return st;
   a.B = batch; a.k = k; a.vocab = vocab; a.mask_id = mask_id; a.logits = logits;
   a.gamma = gamma;
   a.n_chunks = (vocab + kEbChunk - 1) / kEbChunk;
@@ -855,6 +949,17 @@ sbd_status sbd_eb_select_noalloc(void* stream, int32_t batch, int32_t k, int32_t
   const Exec ex{static_cast<hipStream_t>(stream), nullptr, nullptr};
   if ((e = launch_eb_partial(a, ex)) != hipSuccess || (e = launch_eb_select(a, false, ex)) != hipSuccess)
     return fail(nullptr, SBD_ERR_HIP, "EB launch failed: %s", hipGetErrorString(e));
+  return SBD_OK;
+}
+
+sbd_status sbd_stream_probe(void* stream, const void* buf, size_t bytes, uint32_t* sink) {
+  if (!buf || !sink || bytes < 16 || bytes % 16)
+    return fail(nullptr, SBD_ERR_INVALID_ARG, "need a buffer of a positive multiple of 16 bytes and a sink");
+  int dev = 0, n_cu = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e == hipSuccess) e = launch_stream_probe(buf, (int64_t)bytes, sink, n_cu, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(nullptr, SBD_ERR_HIP, "stream probe: %s", hipGetErrorString(e));
   return SBD_OK;
 }
 

@@ -55,6 +55,9 @@ struct Layout {
   int64_t wp_layer;          // elements per layer: qkv, then o, then gate/up, then down
   int64_t wp_o, wp_gu, wp_down, wp_lm;
   size_t attn_ml, attn_o, rows, seqs, eb_mask, eb_part, eb_arg, gemv_part, counters;
+  // sbd_block_step: the LM head's 64-column chunk statistics and the merged row values
+  size_t eb_fpart, eb_farg, eb_rowstat, eb_rowtok;
+  int64_t eb_frows, eb_fchunks;  // rows (min(max_batch * max_block, kStepMaxRows)), vocab / 64
   int64_t gemv_part_floats;  // split-K partial tiles of the decode GEMM
   size_t xn2, sumsq2;        // fused decode forward: second copy of xn (hi, lo) and its partials
   size_t fwd_gains, fwd_ctl, fwd_err;
@@ -72,7 +75,11 @@ struct LayerW {
 };
 
 // ---------------------------------------------------------------------------- GEMM
-enum GemmEpi { EPI_SCALED_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3 };
+enum GemmEpi { EPI_SCALED_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3, EPI_LOGITS_EB = 4 };
+// EPI_LOGITS_EB (LM head): EPI_SCALED_STORE (out_f32 may be null: nothing stored) plus the
+// EB softmax statistics of every row's 64-column chunks (eb_stats.h) into eb_part / eb_arg.
+constexpr int kEbFChunk = 64;
+constexpr int kStepMaxRows = 512;  // batch * k of one sbd_block_step
 
 // EPI_QKV (decode-sized GEMM only): the QKV projection's epilogue does the rest of the
 // attention input — per-head RMSNorm of q and k (Qwen-3), rotate-half RoPE, q stored as
@@ -112,6 +119,10 @@ struct GemmArgs {
   // EPI_SCALED_STORE: out[m][n] = rinv[m] * y (rinv = 1 when sumsq_in == nullptr)
   float* out_f32;
   int64_t ldo;
+  // EPI_LOGITS_EB: as EPI_SCALED_STORE (out_f32 nullable) plus the chunk statistics
+  double* eb_part;
+  int32_t* eb_arg;
+  int eb_chunks, eb_mask_id;
   // row RMS from the producer's partial sums of squares [M][n_part] (EPI_SCALED_STORE,
   // EPI_SWIGLU)
   const float* sumsq_in;
@@ -162,8 +173,11 @@ struct GemvArgs {
   // is formed from the producer's partial sums of squares [M][n_part_in] (none: scale 1)
   const float* sumsq_in;
   int n_part_in;
-  float* out_f32;        // EPI_SCALED_STORE
+  float* out_f32;        // EPI_SCALED_STORE, EPI_LOGITS_EB (nullable there)
   int64_t ldo;
+  double* eb_part;       // EPI_LOGITS_EB: [M][eb_chunks][3] (max, Z, S) of 64-column chunks
+  int32_t* eb_arg;       // [M][eb_chunks] argmax column or -1
+  int eb_chunks, eb_mask_id;
   float* x;              // EPI_RESID
   int64_t ldx;
   bf16_t* xn;
@@ -409,6 +423,11 @@ struct EbArgs {
   double* entropy_out;      // [B][k] or null
   int rule;                 // SBD_SELECT_*: the order and the stopping rule (gamma = its threshold)
   double* conf_out;         // [B][k] or null: max_v p_v of masked rows
+  // Statistics from the LM head (sbd_block_step): eb_merge_kernel reduces the 64-column
+  // chunks in part / part_arg (n_chunks per row) to these per-row values, which the select
+  // kernel then takes (row_stats != null selects that mode).
+  double* row_stats;        // [B*k][2]: entropy, confidence
+  int32_t* row_tok;         // [B*k]
   // Masks of up to kEbInlineRows rows travel in the kernel arguments (bit r of mask_bits is
   // row r) instead of an upload on the stream; is_mask is then null.
   uint64_t mask_bits[kEbInlineRows / 64];
@@ -424,5 +443,7 @@ constexpr int kNoAllocChunks = 64;       // vocab <= 64 * kEbChunk = 262144
 constexpr int kNoAllocMaxDevices = 64;
 hipError_t eb_noalloc_scratch(double** part, int32_t** part_arg);
 hipError_t launch_eb_select(const EbArgs& a, bool select_only, const Exec& ex);
+hipError_t launch_eb_merge(const EbArgs& a, const Exec& ex);
+hipError_t launch_stream_probe(const void* buf, int64_t bytes, uint32_t* sink, int n_cu, hipStream_t s);
 
 }  // namespace sbd

@@ -104,6 +104,8 @@ def test_null_context_is_rejected(lib):
     assert lib.sbd_select(None, 1, 1, 4, 32, None, None, 0.5, -1, None, None, None, None, None) == 1
     assert lib.sbd_block_forward(None, 1, None, 4, None, None, None, None, None) == 1
     assert lib.sbd_commit(None, 1, None, None) == 1
+    assert lib.sbd_block_step(None, 0, 1, None, 4, None, None, None, None, 1.0, None, None, None, None, None,
+                              None) == 1
     assert lib.sbd_prefill(None, 0, None, 1, None) == 1
     assert lib.sbd_destroy(None) == 1
     assert lib.sbd_set_decode_path(None, 0) == 1
