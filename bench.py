@@ -29,14 +29,15 @@ METRIC = "SBD block-forward ms + HBM GB/s (8B shape, k=16); EB-select µs"
 PEAK_HBM_GBS = 8000.0
 
 
-def step_bytes(shape, lens, k):
-    """Algorithmic HBM bytes of one step: weights once, KV read once, staged K/V written,
-    fp32 logits written, EB reads the masked rows' logits."""
+def step_bytes(shape, lens, k, wbytes=2):
+    """Algorithmic HBM bytes of one step: weights once (wbytes per element: 2 for bf16, 1 for
+    e4m3), KV read once, staged K/V written, fp32 logits written, EB reads the masked rows'
+    logits."""
     s = shape
     d, F, V = s.d_model, s.ffn_dim, s.vocab
     qd, kvd = s.n_q_heads * s.head_dim, s.n_kv_heads * s.head_dim
     per_layer = (qd + 2 * kvd) * d + d * qd + 2 * F * d + d * F
-    weights = 2 * (s.n_layers * per_layer + V * d)
+    weights = wbytes * (s.n_layers * per_layer + V * d)
     B = len(lens)
     M = B * k
     kv_read = sum(lens) * s.n_layers * kvd * 2 * 2
@@ -53,11 +54,11 @@ def gate_up_bytes(shape, M):
     return 2 * 2 * shape.ffn_dim * shape.d_model + 2 * M * shape.d_model + 2 * M * shape.ffn_dim
 
 
-def layer_mlp_bytes(shape, M):
+def layer_mlp_bytes(shape, M, wbytes=2):
     """Algorithmic bytes of one layer_mlp launch (gate/up + SwiGLU + down + residual): the three
     MLP weight matrices, plus the residual rows (int64 fixed point) read once and updated once."""
     d, F = shape.d_model, shape.ffn_dim
-    return 2 * 3 * F * d + 8 * M * d + 8 * M * d
+    return wbytes * 3 * F * d + 8 * M * d + 8 * M * d
 
 
 KERNEL_SOURCES = {
@@ -97,9 +98,7 @@ def cpu_baseline(wl, w_dev, lens, toks, gamma, min_seconds):
     from oracle import sbd_oracle as O
 
     s = wl.shape
-    host = {"embed": synth.to_host_bits(w_dev["embed"]), "lm_head": synth.to_host_bits(w_dev["lm_head"]),
-            "final_norm": synth.to_host_bits(w_dev["final_norm"]),
-            "layers": [{kk: synth.to_host_bits(vv) for kk, vv in lw.items()} for lw in w_dev["layers"]]}
+    host = synth.weights_to_host(w_dev)
     caches = []
     for b, L in enumerate(lens):
         kk, vv = synth.make_kv(s, wl.seed, b, L, device="cpu")
@@ -238,6 +237,8 @@ def main():
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event pass")
     ap.add_argument("--decode-path", default="auto", choices=["auto", "fused", "kernels", "layers"],
                     help="kernels of decode-sized forwards (sbd_set_decode_path)")
+    ap.add_argument("--weights", default="bf16", choices=["bf16", "fp8"],
+                    help="weight format: bf16, or e4m3 with a power-of-two scale per matrix (Sec. 4.1's FP8 weights)")
     ap.add_argument("--speedup-table", action="store_true",
                     help="measure time(1), time(k), time(2k) and the paper's speedup(l, k) instead")
     args = ap.parse_args()
@@ -262,7 +263,9 @@ def main():
     lens = wl.cache_lens()
     B, k = wl.batch, wl.k
     print(f"[bench] {wl.name}: generating weights", file=sys.stderr, flush=True)
-    w = synth.make_weights(s, wl.seed, device=dev)
+    fp8 = args.weights == "fp8"
+    wbytes = 1 if fp8 else 2
+    w = (synth.make_weights_fp8 if fp8 else synth.make_weights)(s, wl.seed, device=dev)
     lib = Sbd(s, w, max_batch=B, max_seq_len=max(lens) + k + 64, max_block=k)
     lib.set_decode_path(args.decode_path)
     print(f"[bench] prefilling {B} x {lens[0]}..{lens[-1]} tokens", file=sys.stderr, flush=True)
@@ -328,7 +331,7 @@ def main():
     else:
         ms_fused_step = None
 
-    fwd_bytes, eb_bytes = step_bytes(s, lens, k)
+    fwd_bytes, eb_bytes = step_bytes(s, lens, k, wbytes)
     value = (fwd_bytes + eb_bytes) / (ms_step * 1e-3) / 1e9
     ceiling = copy_ceiling(torch, dev)
 
@@ -360,7 +363,7 @@ def main():
             kind, bpl = "fused", fwd_bytes
             label = "fused_forward_kernel<128> (all layers + LM head, M = 16)"
         elif prof.get("layer_mlp", (0, 0.0))[0]:
-            kind, bpl = "layer_mlp", layer_mlp_bytes(s, B * k)
+            kind, bpl = "layer_mlp", layer_mlp_bytes(s, B * k, wbytes)
             label = "layer_mlp_kernel (gate/up + SwiGLU + down + residual, per-XCD)"
         else:
             kind, bpl = "gate_up", gate_up_bytes(s, B * k)
@@ -369,7 +372,7 @@ def main():
         avg_s = t / c * 1e-3
         achieved = bpl / avg_s / 1e9
         traffic = None
-        traffic_file = os.path.join(ROOT, "profiles", f"{kind}_traffic_{wl.name}.json")
+        traffic_file = os.path.join(ROOT, "profiles", f"{kind}_traffic_{wl.name}{'_fp8' if fp8 else ''}.json")
         if os.path.exists(traffic_file):
             with open(traffic_file) as f:
                 tr = json.load(f)
@@ -394,10 +397,11 @@ def main():
     line = {
         "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "fp8-e4m3 weights, bf16 activations and KV" if fp8 else "bf16",
         "data": "synthetic (seeded random-init weights, uniform random prompt tokens)",
         "config": {"workload": wl.name, "shape": s.name, "batch": B, "cache_len": lens, "k": k,
-                   "gamma": gamma, "n_causal": 1, "decode_path": args.decode_path},
+                   "gamma": gamma, "n_causal": 1, "decode_path": args.decode_path, "weights": args.weights},
         "block_forward_ms": round(ms_fwd, 4),
         "block_forward_gbs": round(fwd_bytes / (ms_fwd * 1e-3) / 1e9, 1),
         "block_forward_frac_of_peak": round(fwd_bytes / (ms_fwd * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),

@@ -64,10 +64,26 @@ typedef struct {
   int32_t qk_norm;
   float rms_eps, rope_theta;
   int32_t max_batch, max_seq_len, max_block, prefill_chunk;
+  int32_t weight_format;  /* SBD_WEIGHTS_BF16 (0) or SBD_WEIGHTS_FP8_E4M3 (1), see sbd_weights */
 } sbd_model_config;
 
 /*
- * Weights: device bf16, borrowed (they must outlive the context and not change).
+ * Formats of the projection and LM-head matrices (wq, wk, wv, wo, w_gate, w_up, w_down,
+ * lm_head).  The embedding and every norm gain are bf16 in both.
+ *   SBD_WEIGHTS_BF16      bf16 values.
+ *   SBD_WEIGHTS_FP8_E4M3  OCP e4m3 bytes (1 sign, 4 exponent bits of bias 7, 3 mantissa
+ *                         bits; no infinities, 0x7f / 0xff NaN) with a power-of-two scale per
+ *                         matrix: the weight is e4m3(q) * 2^e (the FP8 weights of the
+ *                         paper's timing model, Sec. 4.1).  Forwards of at most 16 rows stream
+ *                         the bytes and widen them to bf16 in registers (exactly); longer
+ *                         forwards (prefill chunks, batched decode) and the fused decode
+ *                         path stream a bf16 copy of the same values, made in sbd_create.
+ */
+enum { SBD_WEIGHTS_BF16 = 0, SBD_WEIGHTS_FP8_E4M3 = 1 };
+
+/*
+ * Weights: device memory, borrowed (they must outlive the context and not change); bf16,
+ * or for the projection and LM-head matrices the format of cfg->weight_format.
  * Matrices are logical [out][in] row-major.  Per-layer fields are host arrays of
  * n_layers device pointers.  q_norm / k_norm may be NULL when qk_norm == 0.
  *   embed [vocab][d_model], lm_head [vocab][d_model], final_norm [d_model]
@@ -80,6 +96,10 @@ typedef struct {
   const void *const *attn_norm, *const *wq, *const *wk, *const *wv, *const *wo;
   const void *const *q_norm, *const *k_norm, *const *mlp_norm;
   const void *const *w_gate, *const *w_up, *const *w_down;
+  /* SBD_WEIGHTS_FP8_E4M3 only (else ignored): host int32 [n_layers * 7 + 1], the scale
+   * exponents e of wq, wk, wv, wo, w_gate, w_up, w_down of layer 0, of layer 1, ..., then
+   * of lm_head; each in [-100, 100]. */
+  const int32_t* fp8_scale_exp;
 } sbd_weights;
 
 /* Bytes of device workspace sbd_create needs for this config (KV cache, activations,

@@ -33,6 +33,9 @@ Readings where the paper is silent (each is listed with its reason in the design
 * equal entropies are ordered by row index; argmax ties go to the smallest token id;
 * gamma may be 0 (used in Sec. 3.2) or +inf.
 
+Weights are bf16 bit patterns, or (FP8 weights, the paper's timing assumption of Sec. 4.1)
+e4m3 bytes with a power-of-two scale per matrix, decoded here from the format's definition.
+
 Precision: everything runs in the dtype given to ``Model`` (float64 by default);
 EB statistics are always float64.  With ``kv_bf16`` the keys and values are held in
 bfloat16, the storage format of the KV cache; activations stay in the working dtype.
@@ -55,6 +58,27 @@ def decode_weight(a, dtype=np.float64) -> np.ndarray:
         np.left_shift(a, 16, out=bits, dtype=np.uint32)
         a = bits.view(np.float32)
     return a.astype(dtype, copy=False)
+
+
+def decode_e4m3(bits, dtype=np.float64) -> np.ndarray:
+    """Values of OCP FP8 E4M3 bytes (the "fn" variant): 1 sign bit, 4 exponent bits of bias
+    7, 3 mantissa bits; exponent field 0 holds the subnormals m/8 * 2^-6; the two patterns
+    with every exponent and mantissa bit set are NaN; there are no infinities."""
+    return _E4M3_VALUES.astype(dtype)[np.asarray(bits, dtype=np.uint8)]
+
+
+def _e4m3_table() -> np.ndarray:
+    """The value of each of the 256 e4m3 codes, from the format's definition."""
+    b = np.arange(256)
+    sign = (b >> 7) & 1
+    e = (b >> 3) & 15
+    m = (b & 7).astype(np.float64)
+    mag = np.where(e == 0, m / 8.0 * 2.0 ** -6, (1.0 + m / 8.0) * np.exp2(e.astype(np.float64) - 7.0))
+    mag = np.where((e == 15) & (b & 7 == 7), np.nan, mag)
+    return np.where(sign == 1, -mag, mag)
+
+
+_E4M3_VALUES = _e4m3_table()
 
 
 def round_to_bf16(a: np.ndarray) -> np.ndarray:
@@ -194,12 +218,21 @@ class Model:
         self._memo = {} if cache_decoded else None
         self.kv_bf16 = kv_bf16
 
+    # FP8 weights (uint8 arrays): the order of the per-matrix scale exponents in
+    # weights["fp8_scale_exp"], per layer; the LM head's comes after every layer's
+    FP8_ORDER = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down")
+
     def W(self, name: str, layer: Optional[int] = None) -> np.ndarray:
         key = (name, layer)
         if self._memo is not None and key in self._memo:
             return self._memo[key]
         src = self.w[name] if layer is None else self.w["layers"][layer][name]
-        a = decode_weight(src, self.dtype)
+        if np.asarray(src).dtype == np.uint8:
+            # e4m3 bytes times the matrix's power-of-two scale (exact)
+            i = self.s.n_layers * 7 if layer is None else layer * 7 + self.FP8_ORDER.index(name)
+            a = decode_e4m3(src, self.dtype) * self.dtype.type(2.0 ** int(self.w["fp8_scale_exp"][i]))
+        else:
+            a = decode_weight(src, self.dtype)
         if self._memo is not None:
             self._memo[key] = a
         return a

@@ -70,12 +70,15 @@ class ModelConfig(ctypes.Structure):
                 ("n_kv_heads", c_int32), ("head_dim", c_int32), ("ffn_dim", c_int32),
                 ("vocab", c_int32), ("mask_id", c_int32), ("qk_norm", c_int32),
                 ("rms_eps", c_float), ("rope_theta", c_float), ("max_batch", c_int32),
-                ("max_seq_len", c_int32), ("max_block", c_int32), ("prefill_chunk", c_int32)]
+                ("max_seq_len", c_int32), ("max_block", c_int32), ("prefill_chunk", c_int32),
+                ("weight_format", c_int32)]
 
 
 class Weights(ctypes.Structure):
     _fields_ = [("embed", c_void_p), ("lm_head", c_void_p), ("final_norm", c_void_p)] + \
-               [(f, POINTER(c_void_p)) for f in LAYER_FIELDS]
+               [(f, POINTER(c_void_p)) for f in LAYER_FIELDS] + [("fp8_scale_exp", POINTER(c_int32))]
+
+WEIGHT_FORMATS = {"bf16": 0, "fp8_e4m3": 1}  # SBD_WEIGHTS_*
 
 
 class SbdError(RuntimeError):
@@ -106,11 +109,11 @@ def load_library(path: str = LIB_PATH):
 
 
 def make_config(shape, max_batch: int, max_seq_len: int, max_block: int,
-                prefill_chunk: int = 0) -> ModelConfig:
+                prefill_chunk: int = 0, weight_format: str = "bf16") -> ModelConfig:
     return ModelConfig(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads,
                        shape.head_dim, shape.ffn_dim, shape.vocab, shape.mask_id,
                        int(bool(shape.qk_norm)), float(shape.rms_eps), float(shape.rope_theta),
-                       max_batch, max_seq_len, max_block, prefill_chunk)
+                       max_batch, max_seq_len, max_block, prefill_chunk, WEIGHT_FORMATS[weight_format])
 
 
 def _check(lib, st: int, where: str, ctx=None):
@@ -149,9 +152,12 @@ class Sbd:
 
     def __init__(self, shape, weights: dict, max_batch: int, max_seq_len: int, max_block: int,
                  prefill_chunk: int = 0, device="cuda"):
+        """weights: bf16 tensors, or with an "fp8_scale_exp" entry (synth.make_weights_fp8) the
+        projection and LM-head matrices as e4m3 bytes (uint8) with those scale exponents."""
         self.lib = load_library()
         self.shape = shape
-        self.cfg = make_config(shape, max_batch, max_seq_len, max_block, prefill_chunk)
+        self.weight_format = "fp8_e4m3" if "fp8_scale_exp" in weights else "bf16"
+        self.cfg = make_config(shape, max_batch, max_seq_len, max_block, prefill_chunk, self.weight_format)
         self.device = torch.device(device)
         self.weights = weights                       # keep the borrowed tensors alive
         nbytes = workspace_bytes(self.cfg)
@@ -166,6 +172,10 @@ class Sbd:
             arr = (c_void_p * nl)(*[weights["layers"][l][f].data_ptr() for l in range(nl)])
             self._arrays[f] = arr
             setattr(w, f, ctypes.cast(arr, POINTER(c_void_p)))
+        if self.weight_format == "fp8_e4m3":
+            exps = [int(e) for e in weights["fp8_scale_exp"]]
+            self._exps = (c_int32 * len(exps))(*exps)
+            w.fp8_scale_exp = ctypes.cast(self._exps, POINTER(c_int32))
         self._w = w
         ctx = c_void_p()
         st = self.lib.sbd_create(ctypes.byref(self.cfg), ctypes.byref(w),

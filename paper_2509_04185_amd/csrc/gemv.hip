@@ -46,7 +46,7 @@ namespace sbd {
 template <int NW>
 __device__ __forceinline__ bool owns_tile(int ct, int wave) { return ct % NW == wave; }
 
-template <int C, int NW, int U, int EPI, int DH>
+template <int C, int NW, int U, int EPI, int DH, class WT>
 __global__ __launch_bounds__(NW * 64) void gemv_kernel(GemvArgs a) {
   static_assert(C >= 1 && C <= 8, "a workgroup takes one to eight tiles");
   static_assert(EPI != EPI_QKV || C == 8, "the QKV epilogue works on whole groups");
@@ -100,16 +100,20 @@ __global__ __launch_bounds__(NW * 64) void gemv_kernel(GemvArgs a) {
   const int arow_m = r < a.M ? r : a.M - 1;
   const uint32_t a_off = (uint32_t)(((int64_t)arow_m * a.lda + g * 8 + s_b * 32) * 2);
   // tile t0 + ct at step s_b; consecutive steps of a tile are kPackStep apart
-  const bf16_t* wt[C];
+  const WT* wbase;
+  if constexpr (sizeof(WT) == 1) wbase = a.Wp8; else wbase = a.Wp;
+  const WT* wt[C];
 #pragma unroll
-  for (int ct = 0; ct < C; ++ct) wt[ct] = a.Wp + packed_frag(t0 + ct, s_b, S) + lane * 8;
+  for (int ct = 0; ct < C; ++ct) wt[ct] = wbase + packed_frag(t0 + ct, s_b, S) + lane * 8;
+  float wsc[C];
+  load_wscale<WT, C>(a.wscale, t0, r, wsc);
 
   f32x4 acc[C];
 #pragma unroll
   for (int ct = 0; ct < C; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
   {
-    i32x4 w0[U][C];
-    gemv_stream<C, U, 0, false>(buf_rsrc(a.A), buf_rsrc(a.A_lo), a_off, wt, ns, w0, acc);
+    typename WFrag<WT>::T w0[U][C];
+    gemv_stream<C, U, 0, false>(buf_rsrc(a.A), buf_rsrc(a.A_lo), a_off, wt, ns, w0, wsc, acc);
   }
 
   // ---- 1/rms of this lane's accumulator rows 4g + i
@@ -272,12 +276,16 @@ __global__ __launch_bounds__(NW * 64) void gemv_kernel(GemvArgs a) {
   }
 }
 
+// An fp8 matrix keeps the bf16 shape's bytes in flight with twice the steps per batch.
 template <int C, int NW, int U, int EPI, int DH = 128>
 static void launch_gemv_cfg(const GemvArgs& a, int KS, const Exec& ex) {
   const int units = (a.n_tiles / C + 7) / 8 * 8;
   GemvArgs b = a;
   b.splits = KS;
-  SBD_KLAUNCH((gemv_kernel<C, NW, U, EPI, DH>), dim3((unsigned)(units * KS)), dim3(NW * 64), ex, b);
+  if (a.Wp8 != nullptr)
+    SBD_KLAUNCH((gemv_kernel<C, NW, 2 * U, EPI, DH, fp8_t>), dim3((unsigned)(units * KS)), dim3(NW * 64), ex, b);
+  else
+    SBD_KLAUNCH((gemv_kernel<C, NW, U, EPI, DH, bf16_t>), dim3((unsigned)(units * KS)), dim3(NW * 64), ex, b);
 }
 
 // Launch shapes from sweeps over the 8B decode shapes (M = 16), timed as chains of launches
@@ -326,6 +334,7 @@ static bool dispatch(const GemvArgs& a, GemvShape sh, const Exec& ex) {
 
 hipError_t launch_gemv(GemmEpi epi, const GemvArgs& a, GemvShape sh, const Exec& ex) {
   if (a.M < 1 || a.M > 16 || a.K < 32 || a.K % 32 || a.n_tiles < 8 || a.n_tiles % 8) return hipErrorInvalidValue;
+  if (a.Wp8 != nullptr && a.wscale == nullptr) return hipErrorInvalidValue;
   if (sh.C == 0) sh = epi == EPI_LOGITS_EB ? GemvShape{8, 1, 2, 1} : gemv_pick(epi, a.n_tiles, a.K);
   if (epi == EPI_LOGITS_EB && (a.eb_part == nullptr || a.eb_arg == nullptr || a.eb_chunks * kEbFChunk != a.n_tiles * 16))
     return hipErrorInvalidValue;
@@ -351,6 +360,58 @@ hipError_t launch_gemv(GemmEpi epi, const GemvArgs& a, GemvShape sh, const Exec&
   }
   if (!ok) return hipErrorInvalidValue;
   return hipGetLastError();
+}
+
+}  // namespace sbd
+
+namespace sbd {
+
+// Packing of e4m3 matrices: one thread per 8-element piece, in the order of the bf16 packing
+// (gemm.hip's pack_kernel; mode 1 interleaves gate and up rows per tile).  WIDEN: write the
+// piece as bf16 values q * 2^e (the scaled conversion, exact) into the bf16 packing, else the
+// bytes themselves into the fp8 packing.
+template <bool WIDEN>
+__global__ __launch_bounds__(256) void pack_fp8_kernel(const fp8_t* src0, const fp8_t* src1, float sc0, float sc1,
+                                                       void* dst, int64_t n_pieces, int K, int mode) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n_pieces) return;
+  const int S = K / 32;
+  const int lane = (int)(i % 64);
+  const int64_t tt = (i / 64) % 8;
+  const int64_t s = (i / 512) % S;
+  const int64_t t = (i / (512 * (int64_t)S)) * 8 + tt;
+  const int rr = lane & 15;
+  const int64_t k0 = 32 * s + 8 * (lane >> 4);
+  const bool second = mode == 1 && rr >= 8;
+  const fp8_t* row = mode == 0 ? src0 + (t * 16 + rr) * (int64_t)K
+                               : (second ? src1 + (t * 8 + rr - 8) * (int64_t)K : src0 + (t * 8 + rr) * (int64_t)K);
+  const i32x2 q = *reinterpret_cast<const i32x2*>(row + k0);
+  if constexpr (WIDEN)
+    *reinterpret_cast<i32x4*>(static_cast<bf16_t*>(dst) + i * 8) = w_operand(q, second ? sc1 : sc0);
+  else
+    *reinterpret_cast<i32x2*>(static_cast<fp8_t*>(dst) + i * 8) = q;
+}
+
+static hipError_t pack_fp8(bool widen, const fp8_t* src0, const fp8_t* src1, float sc0, float sc1, void* dst,
+                           int64_t rows, int K, int mode, hipStream_t s) {
+  if (rows % 128 || K % 32) return hipErrorInvalidValue;
+  const int64_t n_pieces = rows * K / 8;
+  const dim3 grid((unsigned)((n_pieces + 255) / 256));
+  if (widen)
+    hipLaunchKernelGGL(pack_fp8_kernel<true>, grid, dim3(256), 0, s, src0, src1, sc0, sc1, dst, n_pieces, K, mode);
+  else
+    hipLaunchKernelGGL(pack_fp8_kernel<false>, grid, dim3(256), 0, s, src0, src1, sc0, sc1, dst, n_pieces, K, mode);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_fp8(const fp8_t* src0, const fp8_t* src1, fp8_t* dst, int64_t rows, int K, int mode,
+                           hipStream_t s) {
+  return pack_fp8(false, src0, src1, 1.f, 1.f, dst, rows, K, mode, s);
+}
+
+hipError_t launch_pack_fp8_widen(const fp8_t* src0, const fp8_t* src1, int e0, int e1, bf16_t* dst, int64_t rows,
+                                 int K, int mode, hipStream_t s) {
+  return pack_fp8(true, src0, src1, ldexpf(1.f, e0), ldexpf(1.f, e1), dst, rows, K, mode, s);
 }
 
 }  // namespace sbd

@@ -14,14 +14,45 @@
 
 namespace sbd {
 
+// Weight fragments: a lane's 8 weights of a tile's 16 x 32 step, as bf16 (i32x4, 16 bytes)
+// or as OCP e4m3 bytes (i32x2, 8 bytes) widened to bf16 right before the MFMA.  The fp8
+// packing is the bf16 one element for element (kPackStep and packed_frag count elements),
+// one byte per element.  A matrix in fp8 carries a power-of-two scale per output row (the
+// lane's row of the tile): the widening multiplies by it exactly (gfx950's scaled
+// conversion), so the MFMA sees the exact bf16 values q * 2^e.
+template <class WT> struct WFrag;
+template <> struct WFrag<bf16_t> { using T = i32x4; };
+template <> struct WFrag<fp8_t> { using T = i32x2; };
+
+__device__ __forceinline__ i32x4 ld_w(const bf16_t* p) { return ld16_stream(p); }
+__device__ __forceinline__ i32x2 ld_w(const fp8_t* p) { return __builtin_nontemporal_load((const i32x2*)p); }
+
+__device__ __forceinline__ i32x4 w_operand(i32x4 w, float) { return w; }
+__device__ __forceinline__ i32x4 w_operand(i32x2 w, float sc) {
+  i32x4 o;
+  o[0] = __builtin_bit_cast(int, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[0], sc, false));
+  o[1] = __builtin_bit_cast(int, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[0], sc, true));
+  o[2] = __builtin_bit_cast(int, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[1], sc, false));
+  o[3] = __builtin_bit_cast(int, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[1], sc, true));
+  return o;
+}
+
+// The lane's per-row weight scales of tiles t0 .. t0 + C - 1 (row 16 t + r); 1 for bf16.
+template <class WT, int C>
+__device__ __forceinline__ void load_wscale(const float* wscale, int t0, int r, float (&sc)[C]) {
+#pragma unroll
+  for (int ct = 0; ct < C; ++ct) sc[ct] = (sizeof(WT) == 1) ? wscale[(int64_t)(t0 + ct) * 16 + r] : 1.0f;
+}
+
 // Weight fragments of steps b0 .. b0 + U - 1 (clamped to ns - 1) of the C tiles.
-template <int C, int U>
-__device__ __forceinline__ void gemv_issue_w(const bf16_t* const (&wt)[C], int b0, int ns, i32x4 (&wv)[U][C]) {
+template <int C, int U, class WT>
+__device__ __forceinline__ void gemv_issue_w(const WT* const (&wt)[C], int b0, int ns,
+                                             typename WFrag<WT>::T (&wv)[U][C]) {
 #pragma unroll
   for (int uu = 0; uu < U; ++uu) {
     const int st = min(b0 + uu, ns - 1);
 #pragma unroll
-    for (int ct = 0; ct < C; ++ct) wv[uu][ct] = ld16_stream(wt[ct] + (int64_t)st * kPackStep);
+    for (int ct = 0; ct < C; ++ct) wv[uu][ct] = ld_w(wt[ct] + (int64_t)st * kPackStep);
   }
 }
 
@@ -38,9 +69,9 @@ __device__ __forceinline__ void gemv_issue_a(__amdgpu_buffer_rsrc_t ra, __amdgpu
   }
 }
 
-template <int C, int U>
-__device__ __forceinline__ void gemv_mfma(const i32x4 (&wv)[U][C], const i32x4 (&xa)[U], const i32x4 (&xl)[U],
-                                          int b0, int ns, f32x4 (&acc)[C]) {
+template <int C, int U, class WR>
+__device__ __forceinline__ void gemv_mfma(const WR (&wv)[U][C], const i32x4 (&xa)[U], const i32x4 (&xl)[U],
+                                          int b0, int ns, const float (&sc)[C], f32x4 (&acc)[C]) {
 #pragma unroll
   for (int uu = 0; uu < U; ++uu) {
     const bool ok = b0 + uu < ns;
@@ -48,22 +79,24 @@ __device__ __forceinline__ void gemv_mfma(const i32x4 (&wv)[U][C], const i32x4 (
     const i32x4 a_lo = ok ? xl[uu] : i32x4{0, 0, 0, 0};
 #pragma unroll
     for (int ct = 0; ct < C; ++ct) {
-      acc[ct] = mfma16x16x32(a_hi, wv[uu][ct], acc[ct]);
-      acc[ct] = mfma16x16x32(a_lo, wv[uu][ct], acc[ct]);
+      const i32x4 w = w_operand(wv[uu][ct], sc[ct]);
+      acc[ct] = mfma16x16x32(a_hi, w, acc[ct]);
+      acc[ct] = mfma16x16x32(a_lo, w, acc[ct]);
     }
   }
 }
 
 // acc += the wave's steps [0, ns).  wt[ct]: this lane's piece of tile ct's fragment at step
 // 0.  PRE: the caller already issued the weights of batch 0 into w0 (gemv_issue_w), e.g.
-// before waiting for the activations; otherwise w0 is scratch.
-template <int C, int U, int POL, bool PRE>
+// before waiting for the activations; otherwise w0 is scratch.  sc: the lane's weight scales.
+template <int C, int U, int POL, bool PRE, class WT>
 __device__ __forceinline__ void gemv_stream(__amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t ral, uint32_t a_off,
-                                            const bf16_t* const (&wt)[C], int ns, i32x4 (&w0)[U][C],
-                                            f32x4 (&acc)[C]) {
+                                            const WT* const (&wt)[C], int ns, typename WFrag<WT>::T (&w0)[U][C],
+                                            const float (&sc)[C], f32x4 (&acc)[C]) {
   if (ns <= 0) return;
   const int nb = (ns + U - 1) / U;
-  i32x4 w1[U][C], xa0[U], xl0[U], xa1[U], xl1[U];
+  typename WFrag<WT>::T w1[U][C];
+  i32x4 xa0[U], xl0[U], xa1[U], xl1[U];
   gemv_issue_a<U, POL>(ra, ral, a_off, 0, ns, xa0, xl0);
   if constexpr (!PRE) gemv_issue_w<C, U>(wt, 0, ns, w0);
   for (int b = 0; b < nb; b += 2) {
@@ -72,7 +105,7 @@ __device__ __forceinline__ void gemv_stream(__amdgpu_buffer_rsrc_t ra, __amdgpu_
       gemv_issue_w<C, U>(wt, (b + 1) * U, ns, w1);
     }
     __builtin_amdgcn_sched_barrier(0);
-    gemv_mfma<C, U>(w0, xa0, xl0, b * U, ns, acc);
+    gemv_mfma<C, U>(w0, xa0, xl0, b * U, ns, sc, acc);
     __builtin_amdgcn_sched_barrier(0);
     if (b + 1 < nb) {
       if (b + 2 < nb) {
@@ -80,7 +113,7 @@ __device__ __forceinline__ void gemv_stream(__amdgpu_buffer_rsrc_t ra, __amdgpu_
         gemv_issue_w<C, U>(wt, (b + 2) * U, ns, w0);
       }
       __builtin_amdgcn_sched_barrier(0);
-      gemv_mfma<C, U>(w1, xa1, xl1, (b + 1) * U, ns, acc);
+      gemv_mfma<C, U>(w1, xa1, xl1, (b + 1) * U, ns, sc, acc);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
@@ -141,30 +174,32 @@ __device__ __forceinline__ void x64_operand(const i32x4 (&xv)[4], i32x4 gv, bool
   }
 }
 
-template <int C, int U>
-__device__ __forceinline__ void gemv_mfma_x64(const i32x4 (&wv)[U][C], const i32x4 (&xv)[U][4], const i32x4 (&gv)[U],
-                                              int b0, int ns, f32x4 (&acc)[C], float& ss) {
+template <int C, int U, class WR>
+__device__ __forceinline__ void gemv_mfma_x64(const WR (&wv)[U][C], const i32x4 (&xv)[U][4], const i32x4 (&gv)[U],
+                                              int b0, int ns, const float (&sc)[C], f32x4 (&acc)[C], float& ss) {
 #pragma unroll
   for (int uu = 0; uu < U; ++uu) {
     i32x4 a_hi, a_lo;
     x64_operand(xv[uu], gv[uu], b0 + uu < ns, a_hi, a_lo, ss);
 #pragma unroll
     for (int ct = 0; ct < C; ++ct) {
-      acc[ct] = mfma16x16x32(a_hi, wv[uu][ct], acc[ct]);
-      acc[ct] = mfma16x16x32(a_lo, wv[uu][ct], acc[ct]);
+      const i32x4 w = w_operand(wv[uu][ct], sc[ct]);
+      acc[ct] = mfma16x16x32(a_hi, w, acc[ct]);
+      acc[ct] = mfma16x16x32(a_lo, w, acc[ct]);
     }
   }
 }
 
 // gemv_stream with the operand formed from the fixed-point residual: x_off is this lane's
 // byte offset into x at step 0 (8 bytes per element), g_off its byte offset into the gain.
-template <int C, int U>
+template <int C, int U, class WT>
 __device__ __forceinline__ void gemv_stream_x64(__amdgpu_buffer_rsrc_t rx, __amdgpu_buffer_rsrc_t rg, uint32_t x_off,
-                                                uint32_t g_off, const bf16_t* const (&wt)[C], int ns,
-                                                f32x4 (&acc)[C], float& ss) {
+                                                uint32_t g_off, const WT* const (&wt)[C], int ns,
+                                                const float (&sc)[C], f32x4 (&acc)[C], float& ss) {
   if (ns <= 0) return;
   const int nb = (ns + U - 1) / U;
-  i32x4 w0[U][C], w1[U][C], x0[U][4], x1[U][4], g0[U], g1[U];
+  typename WFrag<WT>::T w0[U][C], w1[U][C];
+  i32x4 x0[U][4], x1[U][4], g0[U], g1[U];
   gemv_issue_x64<U>(rx, rg, x_off, g_off, 0, ns, x0, g0);
   gemv_issue_w<C, U>(wt, 0, ns, w0);
   for (int b = 0; b < nb; b += 2) {
@@ -173,7 +208,7 @@ __device__ __forceinline__ void gemv_stream_x64(__amdgpu_buffer_rsrc_t rx, __amd
       gemv_issue_w<C, U>(wt, (b + 1) * U, ns, w1);
     }
     __builtin_amdgcn_sched_barrier(0);
-    gemv_mfma_x64<C, U>(w0, x0, g0, b * U, ns, acc, ss);
+    gemv_mfma_x64<C, U>(w0, x0, g0, b * U, ns, sc, acc, ss);
     __builtin_amdgcn_sched_barrier(0);
     if (b + 1 < nb) {
       if (b + 2 < nb) {
@@ -181,7 +216,7 @@ __device__ __forceinline__ void gemv_stream_x64(__amdgpu_buffer_rsrc_t rx, __amd
         gemv_issue_w<C, U>(wt, (b + 2) * U, ns, w0);
       }
       __builtin_amdgcn_sched_barrier(0);
-      gemv_mfma_x64<C, U>(w1, x1, g1, (b + 1) * U, ns, acc, ss);
+      gemv_mfma_x64<C, U>(w1, x1, g1, (b + 1) * U, ns, sc, acc, ss);
       __builtin_amdgcn_sched_barrier(0);
     }
   }

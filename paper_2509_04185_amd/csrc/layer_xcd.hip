@@ -220,7 +220,11 @@ __device__ __forceinline__ void residual_add(const LayerXArgs& a, int grp, int x
 
 }  // namespace
 
+// WT: the weights' format (bf16_t, or fp8_t widened to bf16 in registers: twice the steps per
+// batch keep the same bytes in flight).
+template <class WT>
 __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
+  constexpr int UW = sizeof(WT) == 1 ? 2 : 1;  // batch scale of the weight streams
   __shared__ __attribute__((aligned(16))) char smem[kLxSmem];
   const int x = blockIdx.x & 7, lw = blockIdx.x >> 3;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -248,15 +252,17 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
     QkvPre<kDH> qpre;
     qkv_epi_prefetch<kDH>(e, a.M, qpre);
     const int arow = r < a.M ? r : a.M - 1;
-    const bf16_t* wt[8];
+    const WT* wt[8];
 #pragma unroll
-    for (int ct = 0; ct < 8; ++ct) wt[ct] = a.wqkv + packed_frag(grp * 8 + ct, s_b, S) + lane * 8;
+    for (int ct = 0; ct < 8; ++ct) wt[ct] = static_cast<const WT*>(a.wqkv) + packed_frag(grp * 8 + ct, s_b, S) + lane * 8;
+    float wsc[8];
+    load_wscale<WT, 8>(a.sc_qkv, grp * 8, r, wsc);
     f32x4 acc[8];
 #pragma unroll
     for (int ct = 0; ct < 8; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
     float ss = 0.f;  // x^2 of this lane's elements of row r: the slice's share of the RMSNorm sums
-    gemv_stream_x64<8, 1>(buf_rsrc(a.x_src), buf_rsrc(a.g_attn), (uint32_t)(((int64_t)arow * a.d + g4 * 8 + s_b * 32) * 8),
-                          (uint32_t)((g4 * 8 + s_b * 32) * 2), wt, ns, acc, ss);
+    gemv_stream_x64<8, UW>(buf_rsrc(a.x_src), buf_rsrc(a.g_attn), (uint32_t)(((int64_t)arow * a.d + g4 * 8 + s_b * 32) * 8),
+                           (uint32_t)((g4 * 8 + s_b * 32) * 2), wt, ns, wsc, acc, ss);
     float* ss_s = reinterpret_cast<float*>(smem + 65536 + 1024);  // [64] wave shares, then [16] rows
     row_ss_reduce(r < a.M ? ss : 0.f, ss_s, ss_s + 64);
     reduce_waves<8>(acc, smem);
@@ -320,10 +326,10 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
   const int o_S = a.n_q * kDH / 32;
   const int o_z0 = x * G * kDH / 32, o_zn = G * kDH / 32;
   const int o_sb = o_z0 + o_zn * wave / 4, o_ns = o_z0 + o_zn * (wave + 1) / 4 - o_sb;
-  const bf16_t* o_wt[8];
+  const WT* o_wt[8];
 #pragma unroll
-  for (int ct = 0; ct < 8; ++ct) o_wt[ct] = a.wo + packed_frag(lw * 8 + ct, o_sb, o_S) + lane * 8;
-  i32x4 o_w01[2][8];
+  for (int ct = 0; ct < 8; ++ct) o_wt[ct] = static_cast<const WT*>(a.wo) + packed_frag(lw * 8 + ct, o_sb, o_S) + lane * 8;
+  typename WFrag<WT>::T o_w01[2][8];
   if (!finisher && o_ns > 0) gemv_issue_w<8, 2>(o_wt, 0, o_ns, o_w01);
 
   // ---- 2. attention of KV head x: task t = (sequence, key range)
@@ -420,12 +426,14 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
     const int ns = o_ns;
     // weights first: they wait for nothing.  Steps 0, 1 in o_w01, the rest in batches of 2.
     if (finisher && ns > 0) gemv_issue_w<8, 2>(o_wt, 0, ns, o_w01);
-    const bf16_t* wt2[8];
+    const WT* wt2[8];
 #pragma unroll
     for (int ct = 0; ct < 8; ++ct) wt2[ct] = o_wt[ct] + 2 * kPackStep;
-    constexpr int U = 2;
-    i32x4 w0[U][8];
+    constexpr int U = 2 * UW;
+    typename WFrag<WT>::T w0[U][8];
     if (ns > 2) gemv_issue_w<8, U>(wt2, 0, ns - 2, w0);
+    float wsc[8];
+    load_wscale<WT, 8>(a.sc_o, grp * 8, r, wsc);
     long long old[4];
     residual_old(a, grp, x, old);
     xcd_wait(a, xcd_ctr(a, x, kCtrMergeDone), kXcdWgs, a.layer * 16 + 3);
@@ -442,17 +450,18 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
     if (ns > 0) {
       i32x4 xa[2], xl[2];
       gemv_issue_a<2, kPolicyL2>(ra, ral, a_off, 0, ns, xa, xl);
-      gemv_mfma<8, 2>(o_w01, xa, xl, 0, ns, acc);
+      gemv_mfma<8, 2>(o_w01, xa, xl, 0, ns, wsc, acc);
     }
-    if (ns > 2) gemv_stream<8, U, kPolicyL2, true>(ra, ral, a_off + 2 * 64, wt2, ns - 2, w0, acc);
+    if (ns > 2) gemv_stream<8, U, kPolicyL2, true>(ra, ral, a_off + 2 * 64, wt2, ns - 2, w0, wsc, acc);
     reduce_waves<8>(acc, smem);
     residual_add(a, grp, x, acc, old);
   }
   if (n_idle == 0) residual_zero(a, blockIdx.x, gridDim.x);
 }
 
-template <int CG>
+template <int CG, class WT>
 __global__ __launch_bounds__(256) void layer_mlp_kernel(LayerXArgs a) {
+  constexpr int UW = sizeof(WT) == 1 ? 2 : 1;  // batch scale of the weight streams
   __shared__ __attribute__((aligned(16))) char smem[kLxSmem];
   const int x = blockIdx.x & 7, lw = blockIdx.x >> 3;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -465,15 +474,17 @@ __global__ __launch_bounds__(256) void layer_mlp_kernel(LayerXArgs a) {
     const int S = a.d / 32;
     const int s_b = S * wave / 4, ns = S * (wave + 1) / 4 - s_b;
     const int arow = r < a.M ? r : a.M - 1;
-    const bf16_t* wt[CG];
+    const WT* wt[CG];
 #pragma unroll
-    for (int ct = 0; ct < CG; ++ct) wt[ct] = a.wgu + packed_frag(t0 + ct, s_b, S) + lane * 8;
+    for (int ct = 0; ct < CG; ++ct) wt[ct] = static_cast<const WT*>(a.wgu) + packed_frag(t0 + ct, s_b, S) + lane * 8;
+    float wsc[CG];
+    load_wscale<WT, CG>(a.sc_gu, t0, r, wsc);
     f32x4 acc[CG];
 #pragma unroll
     for (int ct = 0; ct < CG; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
     float ss = 0.f;  // the whole row passes through the 4 waves: its sum of x^2 for the RMSNorm
-    gemv_stream_x64<CG, 1>(buf_rsrc(a.x_src), buf_rsrc(a.g_mlp), (uint32_t)(((int64_t)arow * a.d + g4 * 8 + s_b * 32) * 8),
-                           (uint32_t)((g4 * 8 + s_b * 32) * 2), wt, ns, acc, ss);
+    gemv_stream_x64<CG, UW>(buf_rsrc(a.x_src), buf_rsrc(a.g_mlp), (uint32_t)(((int64_t)arow * a.d + g4 * 8 + s_b * 32) * 8),
+                            (uint32_t)((g4 * 8 + s_b * 32) * 2), wt, ns, wsc, acc, ss);
     row_ss_reduce(r < a.M ? ss : 0.f, ss_s, ss_s + 64);
     float* rinv_s = ss_s + 64;
     if (threadIdx.x < 16) rinv_s[threadIdx.x] = 1.0f / sqrtf(rinv_s[threadIdx.x] / (float)a.d + a.eps);
@@ -503,12 +514,14 @@ __global__ __launch_bounds__(256) void layer_mlp_kernel(LayerXArgs a) {
     const int grp = lw;
     const int S = a.ffn / 32, zn = a.ffn / 8 / 32, z0 = x * zn;
     const int s_b = z0 + zn * wave / 4, ns = z0 + zn * (wave + 1) / 4 - s_b;
-    const bf16_t* wt[8];
+    const WT* wt[8];
 #pragma unroll
-    for (int ct = 0; ct < 8; ++ct) wt[ct] = a.wdown + packed_frag(grp * 8 + ct, s_b, S) + lane * 8;
-    constexpr int U = 2;
-    i32x4 w0[U][8];
+    for (int ct = 0; ct < 8; ++ct) wt[ct] = static_cast<const WT*>(a.wdown) + packed_frag(grp * 8 + ct, s_b, S) + lane * 8;
+    constexpr int U = 2 * UW;
+    typename WFrag<WT>::T w0[U][8];
     if (ns > 0) gemv_issue_w<8, U>(wt, 0, ns, w0);  // weights first: they wait for nothing
+    float wsc[8];
+    load_wscale<WT, 8>(a.sc_down, grp * 8, r, wsc);
     long long old[4];
     residual_old(a, grp, x, old);
     xcd_wait(a, xcd_ctr(a, x, kCtrGuDone), kXcdWgs, a.layer * 16 + 5);
@@ -521,7 +534,7 @@ __global__ __launch_bounds__(256) void layer_mlp_kernel(LayerXArgs a) {
     for (int ct = 0; ct < 8; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int arow = r < a.M ? r : a.M - 1;
     gemv_stream<8, U, kPolicyL2, true>(buf_rsrc(a.act), buf_rsrc(a.act_lo),
-                                       (uint32_t)(((int64_t)arow * a.ffn + g4 * 8 + s_b * 32) * 2), wt, ns, w0, acc);
+                                       (uint32_t)(((int64_t)arow * a.ffn + g4 * 8 + s_b * 32) * 2), wt, ns, w0, wsc, acc);
     reduce_waves<8>(acc, smem);
     residual_add(a, grp, x, acc, old);
   }
@@ -570,8 +583,11 @@ bool layer_xcd_fits(const sbd_model_config& c, int n_cu, int B, int k) {
   return true;
 }
 
-hipError_t launch_layer_attn(const LayerXArgs& a, const Exec& ex) {
-  SBD_KLAUNCH(layer_attn_kernel, dim3(kXcds * kXcdWgs), dim3(256), ex, a);
+hipError_t launch_layer_attn(const LayerXArgs& a, bool fp8, const Exec& ex) {
+  if (fp8)
+    SBD_KLAUNCH(layer_attn_kernel<fp8_t>, dim3(kXcds * kXcdWgs), dim3(256), ex, a);
+  else
+    SBD_KLAUNCH(layer_attn_kernel<bf16_t>, dim3(kXcds * kXcdWgs), dim3(256), ex, a);
   return hipGetLastError();
 }
 
@@ -581,15 +597,20 @@ hipError_t launch_layer_finalize(const FinalizeArgs& a, const Exec& ex) {
   return hipGetLastError();
 }
 
-hipError_t launch_layer_mlp(const LayerXArgs& a, const Exec& ex) {
+template <class WT>
+static hipError_t launch_layer_mlp_t(const LayerXArgs& a, const Exec& ex) {
   const int cg = a.ffn / (kXcds * kXcdWgs * 8);
   switch (cg) {
-    case 6: SBD_KLAUNCH(layer_mlp_kernel<6>, dim3(kXcds * kXcdWgs), dim3(256), ex, a); break;
-    case 7: SBD_KLAUNCH(layer_mlp_kernel<7>, dim3(kXcds * kXcdWgs), dim3(256), ex, a); break;
-    case 8: SBD_KLAUNCH(layer_mlp_kernel<8>, dim3(kXcds * kXcdWgs), dim3(256), ex, a); break;
+    case 6: SBD_KLAUNCH((layer_mlp_kernel<6, WT>), dim3(kXcds * kXcdWgs), dim3(256), ex, a); break;
+    case 7: SBD_KLAUNCH((layer_mlp_kernel<7, WT>), dim3(kXcds * kXcdWgs), dim3(256), ex, a); break;
+    case 8: SBD_KLAUNCH((layer_mlp_kernel<8, WT>), dim3(kXcds * kXcdWgs), dim3(256), ex, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+hipError_t launch_layer_mlp(const LayerXArgs& a, bool fp8, const Exec& ex) {
+  return fp8 ? launch_layer_mlp_t<fp8_t>(a, ex) : launch_layer_mlp_t<bf16_t>(a, ex);
 }
 
 }  // namespace sbd

@@ -44,6 +44,8 @@ const char* check_config(const sbd_model_config& c) {
   if (c.max_seq_len < 1 || c.max_seq_len > (1 << 24)) return "max_seq_len must lie in [1, 2^24]";
   if (c.max_block < 1 || c.max_block > kMaxBlock) return "max_block must lie in [1, 64]";
   if (c.prefill_chunk < 0 || c.prefill_chunk > 4096) return "prefill_chunk must lie in [0, 4096]";
+  if (c.weight_format != SBD_WEIGHTS_BF16 && c.weight_format != SBD_WEIGHTS_FP8_E4M3)
+    return "weight_format must be SBD_WEIGHTS_BF16 or SBD_WEIGHTS_FP8_E4M3";
   return nullptr;
 }
 
@@ -97,6 +99,15 @@ bool sbd::compute_layout(const sbd_model_config& c, Layout* L) {
   o.wp_layer = o.wp_down + (int64_t)c.d_model * c.ffn_dim;
   o.wp_lm = o.wp_layer * c.n_layers;
   o.wpack = take((o.wp_lm + (int64_t)c.vocab * c.d_model) * 2);
+  if (c.weight_format == SBD_WEIGHTS_FP8_E4M3) {
+    o.wpack8 = take(o.wp_lm + (int64_t)c.vocab * c.d_model);
+    o.ws_o = o.n_qkv;
+    o.ws_gu = o.ws_o + c.d_model;
+    o.ws_down = o.ws_gu + 2 * (int64_t)c.ffn_dim;
+    o.ws_layer = o.ws_down + c.d_model;
+    o.ws_lm = o.ws_layer * c.n_layers;
+    o.wscale = take((o.ws_lm + c.vocab) * sizeof(float));
+  }
   const int64_t widest = std::max<int64_t>(std::max<int64_t>(o.n_qkv, 2 * (int64_t)c.ffn_dim), c.d_model);
   // split-K partials of the per-kernel path, or the parked partial tiles of the fused forward
   o.gemv_part_floats = std::max<int64_t>((int64_t)kGemvMaxSplit * 16 * widest, (int64_t)kFwdMaxWorkgroups * kFwdPartFloats);
@@ -288,6 +299,11 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   const int n_rb = (G * k + 63) / 64;
   const int nblocks = (max_end + 31) / 32;
   const bool small = M <= 16;  // decode-sized forward
+  // fp8 weights: decode-sized GEMMs stream the bytes (the others the widened bf16 copy)
+  const bool f8 = m.weight_format == SBD_WEIGHTS_FP8_E4M3;
+  auto w8 = [&](int64_t off, int64_t soff, GemvArgs& v) {
+    if (f8) { v.Wp8 = c->at<fp8_t>(L.wpack8) + off; v.wscale = c->at<float>(L.wscale) + soff; }
+  };
   // forwards of more than 16 rows keep the GEMMs' activation operands in fragment order
   const int mt = small ? 0 : (M + 15) / 16;
 
@@ -373,15 +389,22 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     lx.spin_limit = c->wait_limit;
     for (int l = 0; l < m.n_layers; ++l) {
       const LayerW& w = c->layers[l];
-      const bf16_t* wp = c->at<bf16_t>(L.wpack) + (int64_t)l * L.wp_layer;
       lx.layer = l;
-      lx.wqkv = wp; lx.wo = wp + L.wp_o; lx.wgu = wp + L.wp_gu; lx.wdown = wp + L.wp_down;
+      if (f8) {
+        const fp8_t* wp8 = c->at<fp8_t>(L.wpack8) + (int64_t)l * L.wp_layer;
+        const float* ws = c->at<float>(L.wscale) + (int64_t)l * L.ws_layer;
+        lx.wqkv = wp8; lx.wo = wp8 + L.wp_o; lx.wgu = wp8 + L.wp_gu; lx.wdown = wp8 + L.wp_down;
+        lx.sc_qkv = ws; lx.sc_o = ws + L.ws_o; lx.sc_gu = ws + L.ws_gu; lx.sc_down = ws + L.ws_down;
+      } else {
+        const bf16_t* wp = c->at<bf16_t>(L.wpack) + (int64_t)l * L.wp_layer;
+        lx.wqkv = wp; lx.wo = wp + L.wp_o; lx.wgu = wp + L.wp_gu; lx.wdown = wp + L.wp_down;
+      }
       lx.q_norm = w.q_norm; lx.k_norm = w.k_norm; lx.g_attn = w.attn_norm; lx.g_mlp = w.mlp_norm;
       // launch i = 2 l + h reads R[i % 3], adds into R[(i + 1) % 3], zeroes R[(i + 2) % 3]
       lx.x_src = xr[(2 * l) % 3]; lx.x_dst = xr[(2 * l + 1) % 3]; lx.x_zero = xr[(2 * l + 2) % 3];
-      SBD_LAUNCH(c, SBD_KERNEL_LAYER_ATTN, launch_layer_attn(lx, ex));
+      SBD_LAUNCH(c, SBD_KERNEL_LAYER_ATTN, launch_layer_attn(lx, f8, ex));
       lx.x_src = xr[(2 * l + 1) % 3]; lx.x_dst = xr[(2 * l + 2) % 3]; lx.x_zero = xr[(2 * l + 3) % 3];
-      SBD_LAUNCH(c, SBD_KERNEL_LAYER_MLP, launch_layer_mlp(lx, ex));
+      SBD_LAUNCH(c, SBD_KERNEL_LAYER_MLP, launch_layer_mlp(lx, f8, ex));
     }
     // the LM head's inputs (and the fp32 residual) from the fixed-point residual
     FinalizeArgs fa{M, d, xr[(2 * m.n_layers) % 3], c->final_norm, x, xn, xn_lo, sumsq};
@@ -401,6 +424,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     if (small) {
       // QKV + q/k norm + RoPE + KV staging in one kernel
       GemvArgs v = gemv_base(xn, xn_lo, d, M, d, wp, (int)(L.n_qkv / 16), vpart, vpart_cap, counters);
+      w8((int64_t)l * L.wp_layer, (int64_t)l * L.ws_layer, v);
       v.sumsq_in = sumsq; v.n_part_in = n_part_cur; v.inv_d = 1.0f / d; v.eps = m.rms_eps;
       v.qkv = qe;
       SBD_LAUNCH(c, SBD_KERNEL_QKV, launch_gemv(EPI_QKV, v, GemvShape{}, ex));
@@ -432,6 +456,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
 
     if (small) {
       GemvArgs v = gemv_base(attn, attn_lo, qd, M, qd, wp + L.wp_o, d / 16, vpart, vpart_cap, counters);
+      w8((int64_t)l * L.wp_layer + L.wp_o, (int64_t)l * L.ws_layer + L.ws_o, v);
       v.x = x; v.ldx = d; v.xn = xn; v.xn_lo = xn_lo; v.g_next = w.mlp_norm;
       v.sumsq = sumsq; v.n_part = n_part_o;
       SBD_LAUNCH(c, SBD_KERNEL_O_PROJ, launch_gemv(EPI_RESID, v, GemvShape{}, ex));
@@ -447,10 +472,12 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     const bf16_t* g_after = (l + 1 < m.n_layers) ? c->layers[l + 1].attn_norm : c->final_norm;
     if (small) {
       GemvArgs vu = gemv_base(xn, xn_lo, d, M, d, wp + L.wp_gu, m.ffn_dim / 8, vpart, vpart_cap, counters);
+      w8((int64_t)l * L.wp_layer + L.wp_gu, (int64_t)l * L.ws_layer + L.ws_gu, vu);
       vu.sumsq_in = sumsq; vu.n_part_in = n_part_o; vu.inv_d = 1.0f / d; vu.eps = m.rms_eps;
       vu.act = act; vu.act_lo = act_lo; vu.ld_act = m.ffn_dim;
       SBD_LAUNCH(c, SBD_KERNEL_GATE_UP, launch_gemv(EPI_SWIGLU, vu, GemvShape{}, ex));
       GemvArgs vd = gemv_base(act, act_lo, m.ffn_dim, M, m.ffn_dim, wp + L.wp_down, d / 16, vpart, vpart_cap, counters);
+      w8((int64_t)l * L.wp_layer + L.wp_down, (int64_t)l * L.ws_layer + L.ws_down, vd);
       vd.x = x; vd.ldx = d; vd.xn = xn; vd.xn_lo = xn_lo; vd.g_next = g_after;
       vd.sumsq = sumsq; vd.n_part = n_part_down;
       n_part_cur = n_part_down;
@@ -480,6 +507,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     if (mt == 0) {  // M <= 16: row-major inputs
       GemvArgs v = gemv_base(xn + (int64_t)r0 * d, xn_lo + (int64_t)r0 * d, d, Ml, d,
                              c->at<bf16_t>(L.wpack) + L.wp_lm, m.vocab / 16, vpart, vpart_cap, counters);
+      w8(L.wp_lm, L.ws_lm, v);
       v.sumsq_in = sumsq + (int64_t)r0 * n_part_cur; v.n_part_in = n_part_cur;
       v.inv_d = 1.0f / d; v.eps = m.rms_eps;
       v.out_f32 = logits; v.ldo = m.vocab;
@@ -556,6 +584,13 @@ sbd_status sbd_create(const sbd_model_config* cfg, const sbd_weights* w, void* w
     return fail(nullptr, SBD_ERR_INVALID_ARG, "a weight pointer is null");
   if (cfg->qk_norm && (!w->q_norm || !w->k_norm))
     return fail(nullptr, SBD_ERR_INVALID_ARG, "qk_norm needs q_norm and k_norm");
+  if (cfg->weight_format == SBD_WEIGHTS_FP8_E4M3) {
+    if (!w->fp8_scale_exp) return fail(nullptr, SBD_ERR_INVALID_ARG, "fp8 weights need fp8_scale_exp");
+    for (int64_t i = 0; i < (int64_t)cfg->n_layers * 7 + 1; ++i)
+      if (w->fp8_scale_exp[i] < -100 || w->fp8_scale_exp[i] > 100)
+        return fail(nullptr, SBD_ERR_INVALID_ARG, "fp8_scale_exp[%lld] = %d out of [-100, 100]", (long long)i,
+                    w->fp8_scale_exp[i]);
+  }
   for (int l = 0; l < cfg->n_layers; ++l) {
     if (!w->attn_norm[l] || !w->wq[l] || !w->wk[l] || !w->wv[l] || !w->wo[l] || !w->mlp_norm[l] ||
         !w->w_gate[l] || !w->w_up[l] || !w->w_down[l] ||
@@ -624,18 +659,48 @@ sbd_status sbd_create(const sbd_model_config* cfg, const sbd_weights* w, void* w
                               c->stream) == hipSuccess;
   const int d = cfg->d_model, F = cfg->ffn_dim;
   const int qd = cfg->n_q_heads * cfg->head_dim, kvd = cfg->n_kv_heads * cfg->head_dim;
+  const bool f8 = cfg->weight_format == SBD_WEIGHTS_FP8_E4M3;
+  // fp8: the bytes in the fp8 packing, the widened values in the bf16 packing (for forwards of
+  // more than 16 rows and the fused path), and per-row scales 2^e for the widening
+  auto pk = [&](const bf16_t* s0, const bf16_t* s1, int e0, int e1, int64_t off, int64_t rows, int K, int mode) {
+    if (!f8) return launch_pack(s0, s1, c->at<bf16_t>(L.wpack) + off, rows, K, mode, c->stream) == hipSuccess;
+    const fp8_t* q0 = reinterpret_cast<const fp8_t*>(s0);
+    const fp8_t* q1 = reinterpret_cast<const fp8_t*>(s1);
+    return launch_pack_fp8(q0, q1, c->at<fp8_t>(L.wpack8) + off, rows, K, mode, c->stream) == hipSuccess &&
+           launch_pack_fp8_widen(q0, q1, e0, e1, c->at<bf16_t>(L.wpack) + off, rows, K, mode, c->stream) ==
+               hipSuccess;
+  };
+  std::vector<float> wscale;
+  auto ex = [&](int l, int j) { return f8 ? w->fp8_scale_exp[(int64_t)l * 7 + j] : 0; };
   for (int l = 0; ok && l < cfg->n_layers; ++l) {
     const LayerW& lw = c->layers[l];
-    bf16_t* wp = c->at<bf16_t>(L.wpack) + (int64_t)l * L.wp_layer;
-    ok = launch_pack(lw.wq, nullptr, wp, qd, d, 0, c->stream) == hipSuccess &&
-         launch_pack(lw.wk, nullptr, wp + (int64_t)qd * d, kvd, d, 0, c->stream) == hipSuccess &&
-         launch_pack(lw.wv, nullptr, wp + (int64_t)(qd + kvd) * d, kvd, d, 0, c->stream) == hipSuccess &&
-         launch_pack(lw.wo, nullptr, wp + L.wp_o, d, qd, 0, c->stream) == hipSuccess &&
-         launch_pack(lw.w_gate, lw.w_up, wp + L.wp_gu, 2 * (int64_t)F, d, 1, c->stream) == hipSuccess &&
-         launch_pack(lw.w_down, nullptr, wp + L.wp_down, d, F, 0, c->stream) == hipSuccess;
+    const int64_t wp = (int64_t)l * L.wp_layer;
+    ok = pk(lw.wq, nullptr, ex(l, 0), 0, wp, qd, d, 0) &&
+         pk(lw.wk, nullptr, ex(l, 1), 0, wp + (int64_t)qd * d, kvd, d, 0) &&
+         pk(lw.wv, nullptr, ex(l, 2), 0, wp + (int64_t)(qd + kvd) * d, kvd, d, 0) &&
+         pk(lw.wo, nullptr, ex(l, 3), 0, wp + L.wp_o, d, qd, 0) &&
+         pk(lw.w_gate, lw.w_up, ex(l, 4), ex(l, 5), wp + L.wp_gu, 2 * (int64_t)F, d, 1) &&
+         pk(lw.w_down, nullptr, ex(l, 6), 0, wp + L.wp_down, d, F, 0);
+    if (f8) {
+      auto put = [&](int64_t rows, int e) { wscale.insert(wscale.end(), (size_t)rows, std::ldexp(1.0f, e)); };
+      put(qd, ex(l, 0));
+      put(kvd, ex(l, 1));
+      put(kvd, ex(l, 2));
+      put(d, ex(l, 3));
+      for (int64_t t = 0; t < 2 * (int64_t)F / 16; ++t) {  // packed gate/up tile: 8 gate rows, then 8 up rows
+        put(8, ex(l, 4));
+        put(8, ex(l, 5));
+      }
+      put(d, ex(l, 6));
+    }
   }
-  ok = ok && launch_pack(c->lm_head, nullptr, c->at<bf16_t>(L.wpack) + L.wp_lm, cfg->vocab, d, 0,
-                         c->stream) == hipSuccess;
+  const int e_lm = f8 ? w->fp8_scale_exp[(int64_t)cfg->n_layers * 7] : 0;
+  ok = ok && pk(c->lm_head, nullptr, e_lm, 0, L.wp_lm, cfg->vocab, d, 0);
+  if (ok && f8) {
+    wscale.insert(wscale.end(), (size_t)cfg->vocab, std::ldexp(1.0f, e_lm));
+    ok = (int64_t)wscale.size() == L.ws_lm + cfg->vocab &&
+         hipMemcpy(c->ws + L.wscale, wscale.data(), wscale.size() * sizeof(float), hipMemcpyHostToDevice) == hipSuccess;
+  }
   // fused decode forward: per-layer gains, error word (sticky) and its pinned host copy
   if (ok) {
     std::vector<FwdGains> gains(cfg->n_layers);

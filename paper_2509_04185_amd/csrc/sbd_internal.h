@@ -11,6 +11,7 @@
 namespace sbd {
 
 typedef uint16_t bf16_t;            // raw IEEE bfloat16 bits
+typedef uint8_t fp8_t;              // raw OCP e4m3 (fn) bits
 
 constexpr int kWave = 64;           // CDNA wavefront width
 constexpr int kMaxSplits = 64;      // split-KV partitions per (sequence, KV head, row block)
@@ -52,6 +53,9 @@ struct Layout {
   int64_t eb_chunks;      // ceil(vocab / kEbChunk)
   size_t kcache, vcache, rope, x, xn, sumsq, qkv, q, attn, act;
   size_t wpack;              // packed weights (see gemm.hip), element offsets below
+  size_t wpack8;             // fp8 weights: the same packing, one byte per element
+  size_t wscale;             // fp8 weights: per-row scales 2^e (floats), offsets below
+  int64_t ws_layer, ws_o, ws_gu, ws_down, ws_lm;
   int64_t wp_layer;          // elements per layer: qkv, then o, then gate/up, then down
   int64_t wp_o, wp_gu, wp_down, wp_lm;
   size_t attn_ml, attn_o, rows, seqs, eb_mask, eb_part, eb_arg, gemv_part, counters;
@@ -168,6 +172,8 @@ struct GemvArgs {
   int64_t lda;
   int M, K;
   const bf16_t* Wp;    // packed weights
+  const fp8_t* Wp8;    // the same in e4m3 (same packing), or null: then Wp is streamed
+  const float* wscale; // with Wp8: per-row power-of-two scales [n_tiles * 16]
   int n_tiles;         // 16-row tiles of the packed matrix (a multiple of 8)
   // EPI_SCALED_STORE, SWIGLU, QKV: the input rows' RMSNorm scale 1/sqrt(mean(x^2) + eps)
   // is formed from the producer's partial sums of squares [M][n_part_in] (none: scale 1)
@@ -370,7 +376,8 @@ struct LayerXArgs {
   int d, n_q, n_kv, ffn, qk_norm;
   float eps, q_scale;
   int n_tasks;                       // attention key splits per sequence
-  const bf16_t *wqkv, *wo, *wgu, *wdown;   // packed weights of the layer
+  const void *wqkv, *wo, *wgu, *wdown;     // packed weights of the layer (bf16_t, or fp8_t)
+  const float *sc_qkv, *sc_o, *sc_gu, *sc_down;  // fp8: per-row weight scales of each
   const bf16_t *q_norm, *k_norm;           // Qwen-3 per-head gains (qk_norm)
   const bf16_t* g_attn;              // attention norm gain of the layer
   const bf16_t* g_mlp;               // MLP norm gain of the layer
@@ -403,8 +410,8 @@ struct FinalizeArgs {
 };
 // True when the per-XCD layer kernels implement this decode-sized forward on this device.
 bool layer_xcd_fits(const sbd_model_config& c, int n_cu, int B, int k);
-hipError_t launch_layer_attn(const LayerXArgs& a, const Exec& ex);
-hipError_t launch_layer_mlp(const LayerXArgs& a, const Exec& ex);
+hipError_t launch_layer_attn(const LayerXArgs& a, bool fp8, const Exec& ex);
+hipError_t launch_layer_mlp(const LayerXArgs& a, bool fp8, const Exec& ex);
 hipError_t launch_layer_finalize(const FinalizeArgs& a, const Exec& ex);
 
 // ---------------------------------------------------------------------------- EB sampler
@@ -444,6 +451,12 @@ constexpr int kNoAllocMaxDevices = 64;
 hipError_t eb_noalloc_scratch(double** part, int32_t** part_arg);
 hipError_t launch_eb_select(const EbArgs& a, bool select_only, const Exec& ex);
 hipError_t launch_eb_merge(const EbArgs& a, const Exec& ex);
+// Packing of e4m3 matrices (mode as launch_pack): into the fp8 packing, or widened to the
+// bf16 packing with the scales 2^e0 (src0) and 2^e1 (src1).
+hipError_t launch_pack_fp8(const fp8_t* src0, const fp8_t* src1, fp8_t* dst, int64_t rows, int K, int mode,
+                           hipStream_t s);
+hipError_t launch_pack_fp8_widen(const fp8_t* src0, const fp8_t* src1, int e0, int e1, bf16_t* dst, int64_t rows,
+                                 int K, int mode, hipStream_t s);
 hipError_t launch_stream_probe(const void* buf, int64_t bytes, uint32_t* sink, int n_cu, hipStream_t s);
 
 }  // namespace sbd

@@ -142,13 +142,46 @@ def make_weights(shape: ModelShape, seed: int, device="cpu", std: float = 0.02,
     return w
 
 
+FP8_KEYS = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down")
+
+
+def make_weights_fp8(shape: ModelShape, seed: int, device="cpu", std: float = 0.02,
+                     gain_std: float = 0.1, layers: Optional[Sequence[int]] = None) -> dict:
+    """make_weights with every projection matrix and the LM head held as OCP e4m3 bytes
+    (torch.uint8) with a power-of-two scale per matrix, the FP8 weights of the paper's
+    timing model (Sec. 4.1): e is the smallest exponent with max|w| / 2^e <= 448 (the
+    largest e4m3 value) and the bytes are torch's float8_e4m3fn conversion of w / 2^e.
+    "fp8_scale_exp" lists e for wq, wk, wv, wo, w_gate, w_up, w_down of each layer, then the
+    LM head's.  The embedding and the norm gains stay bf16."""
+    w = make_weights(shape, seed, device, std, gain_std, layers)
+    exps = []
+
+    def q(t):
+        a = t.float()
+        top = float(a.abs().max())
+        e = math.ceil(math.log2(top / 448.0)) if top > 0 else 0
+        return (a * 2.0 ** -e).to(torch.float8_e4m3fn).view(torch.uint8), e
+
+    for lw in w["layers"]:
+        for key in FP8_KEYS:
+            lw[key], e = q(lw[key])
+            exps.append(e)
+    w["lm_head"], e = q(w["lm_head"])
+    exps.append(e)
+    w["fp8_scale_exp"] = exps
+    return w
+
+
 def to_host_bits(t: torch.Tensor) -> np.ndarray:
-    """Raw bf16 bit patterns of a tensor as a host numpy uint16 array."""
-    return t.detach().to("cpu").contiguous().view(torch.int16).numpy().view(np.uint16)
+    """Raw bit patterns of a tensor as a host numpy array: bf16 as uint16, e4m3 bytes as uint8."""
+    t = t.detach().to("cpu").contiguous()
+    if t.dtype == torch.uint8:
+        return t.numpy()
+    return t.view(torch.int16).numpy().view(np.uint16)
 
 
 def weights_to_host(w: dict) -> dict:
-    out = {k: to_host_bits(v) for k, v in w.items() if k != "layers"}
+    out = {k: (to_host_bits(v) if k != "fp8_scale_exp" else list(v)) for k, v in w.items() if k != "layers"}
     out["layers"] = [{k: to_host_bits(v) for k, v in lw.items()} for lw in w["layers"]]
     return out
 

@@ -70,6 +70,23 @@ def test_unsupported_configs_are_rejected(field, value):
     assert e.value.name == "SBD_ERR_UNSUPPORTED"
 
 
+def test_unknown_weight_format_rejected():
+    cfg = P.make_config(synth.TINY, 1, 64, 4)
+    cfg.weight_format = 2
+    with pytest.raises(P.SbdError, match="weight_format"):
+        P.workspace_bytes(cfg)
+
+
+def test_fp8_workspace_holds_both_packings():
+    """FP8 weights: the e4m3 packing (1 byte per element) and the widened bf16 copy."""
+    s = synth.LLAMA8B
+    b16 = P.workspace_bytes(P.make_config(s, 1, 2112, 16))
+    f8 = P.workspace_bytes(P.make_config(s, 1, 2112, 16, weight_format="fp8_e4m3"))
+    qd, kvd, d, F = s.n_q_heads * s.head_dim, s.n_kv_heads * s.head_dim, s.d_model, s.ffn_dim
+    elems = s.n_layers * ((qd + 2 * kvd) * d + d * qd + 3 * F * d) + s.vocab * d
+    assert elems <= f8 - b16 <= elems + 64 * 2**20
+
+
 def test_bad_eps_and_theta_rejected():
     for field, value in (("rms_eps", 0.0), ("rms_eps", math.nan), ("rope_theta", -1.0)):
         cfg = P.make_config(synth.TINY, 1, 128, 4)

@@ -210,3 +210,44 @@ def test_eight_b_layer_shape_matches_transformers():
         ref = hf(input_ids=torch.from_numpy(tokens.astype(np.int64))[None]).logits[0].numpy()
     model = O.Model(shape, synth.weights_to_host(w), dtype=np.float64)
     assert _rel(model.full_forward(tokens, causal_point=6), ref) <= REL_L2
+
+
+def test_decode_e4m3_matches_torch_float8():
+    """The oracle's e4m3 decoder against torch's float8_e4m3fn, all 256 patterns, and the
+    format's landmarks (1, the largest 448, the smallest subnormal 2^-9, -0)."""
+    bits = np.arange(256, dtype=np.uint8)
+    got = O.decode_e4m3(bits)
+    ref = torch.from_numpy(bits).view(torch.float8_e4m3fn).to(torch.float32).numpy().astype(np.float64)
+    nan = np.isnan(ref)
+    assert nan.sum() == 2 and np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+    assert O.decode_e4m3([0x38, 0x7E, 0x01, 0x80]).tolist() == [1.0, 448.0, 2.0 ** -9, 0.0]
+    assert np.signbit(O.decode_e4m3([0x80]))[0]
+
+
+def test_fp8_weights_model_uses_scaled_values():
+    """An FP8 model's matrices are the decoded bytes times 2^e of their matrix; the causal
+    forward then matches transformers run on those same values."""
+    shape = synth.TINY
+    w8 = synth.make_weights_fp8(shape, 32)
+    host = synth.weights_to_host(w8)
+    model = O.Model(shape, host, dtype=np.float64)
+    exps = w8["fp8_scale_exp"]
+    assert len(exps) == shape.n_layers * 7 + 1 and all(-20 <= e <= 0 for e in exps)
+    wq = model.W("wq", 1)
+    ref = torch.from_numpy(host["layers"][1]["wq"]).view(torch.float8_e4m3fn).double().numpy() * 2.0 ** exps[7]
+    assert np.array_equal(wq, ref)
+    assert np.array_equal(model.W("lm_head"),
+                          torch.from_numpy(host["lm_head"]).view(torch.float8_e4m3fn).double().numpy() * 2.0 ** exps[-1])
+    # the widened values in bf16 (exact: at most 4 significant bits) into the library model
+    wide = {k: v for k, v in w8.items() if k not in ("layers", "fp8_scale_exp")}
+    wide["layers"] = [dict(lw) for lw in w8["layers"]]
+    for li, lw in enumerate(wide["layers"]):
+        for j, key in enumerate(synth.FP8_KEYS):
+            lw[key] = (lw[key].view(torch.float8_e4m3fn).float() * 2.0 ** exps[li * 7 + j]).to(torch.bfloat16)
+    wide["lm_head"] = (w8["lm_head"].view(torch.float8_e4m3fn).float() * 2.0 ** exps[-1]).to(torch.bfloat16)
+    hf = _hf_model(shape, wide)
+    tokens = synth.make_tokens(32, T, shape)
+    with torch.no_grad():
+        out = hf(input_ids=torch.from_numpy(tokens.astype(np.int64))[None]).logits[0].numpy()
+    assert _rel(model.full_forward(tokens, causal_point=T), out) <= REL_L2
