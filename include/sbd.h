@@ -335,6 +335,20 @@ sbd_status sbd_set_wait_limit(sbd_ctx* ctx, int32_t polls);
 sbd_status sbd_decode_path_fits(const sbd_ctx* ctx, int32_t path, int32_t batch, int32_t k, int32_t* fits);
 
 /*
+ * The per-XCD layer kernels and the K-split GEMMs hand partial results between workgroups
+ * through one XCD's L2 and rely on workgroup i of a launch running on XCD i % 8 (256 CUs in
+ * 8 XCDs).  sbd_create checks this with a probe kernel that reads each workgroup's XCC_ID
+ * register (grids of 256, 1000 and 2048 workgroups); where it does not hold, the layer
+ * kernels are not used (SBD_DECODE_LAYERS fails with UNSUPPORTED, AUTO takes one kernel per
+ * step) and no GEMM splits K, so no hand-off between XCDs is needed.
+ *   sbd_xcd_map_ok: *ok = 1 when the probe found the mapping.
+ *   sbd_xcd_map_check: the decision itself on given per-workgroup XCD ids (host only):
+ *   *ok = 1 iff xcc_ids[i] == i % n_xcd for every i < n.
+ */
+sbd_status sbd_xcd_map_ok(const sbd_ctx* ctx, int32_t* ok);
+sbd_status sbd_xcd_map_check(const int32_t* xcc_ids, int32_t n, int32_t n_xcd, int32_t* ok);
+
+/*
  * Per-kernel timing, for measurement tools.  While enabled, every kernel launch the
  * context makes is bracketed by a pair of HIP events on its stream (this adds a little
  * time between kernels).  sbd_profile_read waits for the recorded work, adds up the

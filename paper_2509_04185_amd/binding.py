@@ -58,6 +58,8 @@ SIGNATURES = {
     "sbd_decode_path_fits": [c_void_p, c_int32, c_int32, c_int32, POINTER(c_int32)],
     "sbd_set_wait_limit": [c_void_p, c_int32],
     "sbd_profile_enable": [c_void_p, c_int32],
+    "sbd_xcd_map_ok": [c_void_p, POINTER(c_int32)],
+    "sbd_xcd_map_check": [c_void_p, c_int32, c_int32, POINTER(c_int32)],
     "sbd_stream_probe": [c_void_p, c_void_p, c_size_t, c_void_p],
     "sbd_profile_read": [c_void_p, c_int32, POINTER(c_int32), POINTER(c_double)],
     "sbd_status_string": [c_int32],
@@ -323,6 +325,12 @@ class Sbd:
         _check(self.lib, self.lib.sbd_decode_path_fits(self.ctx, DECODE_PATHS[path], batch, k, ctypes.byref(fits)),
                "sbd_decode_path_fits", self.ctx)
         return bool(fits.value)
+
+    def xcd_map_ok(self) -> bool:
+        """Whether the probe at creation found workgroup i on XCD i % 8 (sbd_xcd_map_ok)."""
+        ok = c_int32(0)
+        _check(self.lib, self.lib.sbd_xcd_map_ok(self.ctx, ctypes.byref(ok)), "sbd_xcd_map_ok", self.ctx)
+        return bool(ok.value)
 
     def profile(self, enable: bool):
         _check(self.lib, self.lib.sbd_profile_enable(self.ctx, int(bool(enable))),

@@ -499,7 +499,7 @@ static void launch_epi(const GemmArgs& a, int mt, int nt, const Exec& ex) {
 
 hipError_t launch_gemm(GemmEpi epi, const GemmArgs& a0, const Exec& ex) {
   if (a0.M < 1 || a0.K < 32 || a0.K % 32 || a0.n_tiles < 8 || a0.n_tiles % 8) return hipErrorInvalidValue;
-  const GemmPlan p = gemm_plan(a0.M, a0.n_tiles, a0.K, a0.part ? a0.part_cap : 0);
+  const GemmPlan p = gemm_plan(a0.M, a0.n_tiles, a0.K, (a0.part && !a0.no_split) ? a0.part_cap : 0);
   if (p.nt == 0) return hipErrorInvalidValue;
   if (p.splits > 1 && (a0.counters == nullptr || (int64_t)p.n_cb * p.m_blocks * kCtrStride > kLayerCtr0))
     return hipErrorInvalidValue;

@@ -336,6 +336,7 @@ hipError_t launch_gemv(GemmEpi epi, const GemvArgs& a, GemvShape sh, const Exec&
   if (a.M < 1 || a.M > 16 || a.K < 32 || a.K % 32 || a.n_tiles < 8 || a.n_tiles % 8) return hipErrorInvalidValue;
   if (a.Wp8 != nullptr && a.wscale == nullptr) return hipErrorInvalidValue;
   if (sh.C == 0) sh = epi == EPI_LOGITS_EB ? GemvShape{8, 1, 2, 1} : gemv_pick(epi, a.n_tiles, a.K);
+  if (a.no_split) sh.KS = 1;
   if (epi == EPI_LOGITS_EB && (a.eb_part == nullptr || a.eb_arg == nullptr || a.eb_chunks * kEbFChunk != a.n_tiles * 16))
     return hipErrorInvalidValue;
   if (sh.KS < 1 || sh.KS > kGemvMaxSplit || a.n_tiles % sh.C) return hipErrorInvalidValue;

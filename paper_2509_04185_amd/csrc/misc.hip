@@ -181,4 +181,18 @@ hipError_t launch_kv_export(const KvCopyArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// The XCD (accelerator complex die) each workgroup of a launch runs on, from the XCC_ID
+// hardware register (bits 3:0): the per-XCD layer kernels and the split-K hand-offs rely on
+// workgroup i running on XCD i % 8 and check it with this probe when a context is created.
+__global__ __launch_bounds__(64) void xcd_probe_kernel(int* out) {
+  const int id = (int)(__builtin_amdgcn_s_getreg((20) | (0 << 6) | ((4 - 1) << 11)) & 15);
+  if (threadIdx.x == 0) out[blockIdx.x] = id;
+}
+
+hipError_t launch_xcd_probe(int* out, int n, hipStream_t s) {
+  if (out == nullptr || n < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(xcd_probe_kernel, dim3(n), dim3(64), 0, s, out);
+  return hipGetLastError();
+}
+
 }  // namespace sbd

@@ -159,6 +159,7 @@ struct sbd_ctx {
   int wait_limit = kLxSpinDefault;  // sbd_set_wait_limit
   int n_cu = 0;                 // workgroups of the fused forward: one per CU, at most kFwdMaxWorkgroups
   int n_cu_dev = 0;             // CUs of the device
+  bool xcd_ok = false;          // workgroup i of a launch runs on XCD i % 8 (probed at creation)
   int32_t* err_host = nullptr;  // pinned copy of the fused forward's sticky error word
 
   template <class T>
@@ -235,19 +236,21 @@ hipEvent_t take_event(sbd_ctx* c) {
     if ((ctx)->prof) (ctx)->recs.push_back(sbd_ctx::Rec{kind, ex.start, ex.stop}); \
   } while (0)
 
+// split_ok: K may be split over workgroups that hand their partials off through one XCD's L2
+// (false when the device does not place workgroup i on XCD i % 8)
 GemmArgs gemm_base(const bf16_t* A, const bf16_t* A_lo, int64_t lda, int M, int K, const bf16_t* Wp,
-                   int n_tiles, float* part, int64_t part_cap, int* counters) {
+                   int n_tiles, float* part, int64_t part_cap, int* counters, bool split_ok) {
   GemmArgs g{};
   g.A = A; g.A_lo = A_lo; g.lda = lda; g.M = M; g.K = K; g.Wp = Wp; g.n_tiles = n_tiles;
-  g.part = part; g.part_cap = part_cap; g.counters = counters;
+  g.part = part; g.part_cap = part_cap; g.counters = counters; g.no_split = split_ok ? 0 : 1;
   return g;
 }
 
 GemvArgs gemv_base(const bf16_t* A, const bf16_t* A_lo, int64_t lda, int M, int K, const bf16_t* Wp,
-                   int n_tiles, float* part, int64_t part_cap, int* counters) {
+                   int n_tiles, float* part, int64_t part_cap, int* counters, bool split_ok) {
   GemvArgs v{};
   v.A = A; v.A_lo = A_lo; v.lda = lda; v.M = M; v.K = K; v.Wp = Wp; v.n_tiles = n_tiles;
-  v.part = part; v.part_cap = part_cap; v.counters = counters;
+  v.part = part; v.part_cap = part_cap; v.counters = counters; v.no_split = split_ok ? 0 : 1;
   return v;
 }
 
@@ -342,10 +345,10 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   // The per-XCD layer kernels: chosen by AUTO where they apply; checked before anything is
   // enqueued when asked for explicitly.
   const bool layers_fit = small && !fused && c->decode_path != SBD_DECODE_KERNELS &&
-                          layer_xcd_fits(m, c->n_cu_dev, B, k);
+                          c->xcd_ok && layer_xcd_fits(m, c->n_cu_dev, B, k);
   if (small && c->decode_path == SBD_DECODE_LAYERS && !layers_fit)
-    return fail(c, SBD_ERR_UNSUPPORTED, "the per-XCD layer kernels do not fit this forward or device (%d CUs)",
-                c->n_cu_dev);
+    return fail(c, SBD_ERR_UNSUPPORTED, "the per-XCD layer kernels do not fit this forward or device (%d CUs%s)",
+                c->n_cu_dev, c->xcd_ok ? "" : "; workgroup i does not run on XCD i % 8 here");
 
   sbd_status st = upload(c, c->ws + L.rows, rows.data(), rows.size() * sizeof(RowParam));
   if (st) return st;
@@ -423,13 +426,13 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     qe.cap = L.cap; qe.n_slots = m.max_batch;
     if (small) {
       // QKV + q/k norm + RoPE + KV staging in one kernel
-      GemvArgs v = gemv_base(xn, xn_lo, d, M, d, wp, (int)(L.n_qkv / 16), vpart, vpart_cap, counters);
+      GemvArgs v = gemv_base(xn, xn_lo, d, M, d, wp, (int)(L.n_qkv / 16), vpart, vpart_cap, counters, c->xcd_ok);
       w8((int64_t)l * L.wp_layer, (int64_t)l * L.ws_layer, v);
       v.sumsq_in = sumsq; v.n_part_in = n_part_cur; v.inv_d = 1.0f / d; v.eps = m.rms_eps;
       v.qkv = qe;
       SBD_LAUNCH(c, SBD_KERNEL_QKV, launch_gemv(EPI_QKV, v, GemvShape{}, ex));
     } else {
-      GemmArgs g = gemm_base(xn, xn_lo, d, M, d, wp, (int)(L.n_qkv / 16), vpart, vpart_cap, counters);
+      GemmArgs g = gemm_base(xn, xn_lo, d, M, d, wp, (int)(L.n_qkv / 16), vpart, vpart_cap, counters, c->xcd_ok);
       g.a_mtiles = mt;
       g.out_f32 = qkv; g.ldo = L.n_qkv;
       g.sumsq_in = sumsq; g.n_part = n_part_cur; g.inv_d = 1.0f / d; g.eps = m.rms_eps;
@@ -455,46 +458,46 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     SBD_LAUNCH(c, SBD_KERNEL_ATTN_MERGE, launch_attention_merge(aa, ex));
 
     if (small) {
-      GemvArgs v = gemv_base(attn, attn_lo, qd, M, qd, wp + L.wp_o, d / 16, vpart, vpart_cap, counters);
+      GemvArgs v = gemv_base(attn, attn_lo, qd, M, qd, wp + L.wp_o, d / 16, vpart, vpart_cap, counters, c->xcd_ok);
       w8((int64_t)l * L.wp_layer + L.wp_o, (int64_t)l * L.ws_layer + L.ws_o, v);
       v.x = x; v.ldx = d; v.xn = xn; v.xn_lo = xn_lo; v.g_next = w.mlp_norm;
       v.sumsq = sumsq; v.n_part = n_part_o;
       SBD_LAUNCH(c, SBD_KERNEL_O_PROJ, launch_gemv(EPI_RESID, v, GemvShape{}, ex));
     } else {
-      GemmArgs go = gemm_base(attn, attn_lo, qd, M, qd, wp + L.wp_o, d / 16, vpart, vpart_cap, counters);
+      GemmArgs go = gemm_base(attn, attn_lo, qd, M, qd, wp + L.wp_o, d / 16, vpart, vpart_cap, counters, c->xcd_ok);
       go.a_mtiles = mt; go.o_mtiles = mt;
       go.x = x; go.ldx = d; go.xn = xn; go.xn_lo = xn_lo; go.g_next = w.mlp_norm; go.sumsq_out = sumsq;
-      go.n_part_out = gemm_plan(M, d / 16, qd, vpart_cap).n_cb;
+      go.n_part_out = gemm_plan(M, d / 16, qd, c->xcd_ok ? vpart_cap : 0).n_cb;
       n_part_cur = go.n_part_out;
       SBD_LAUNCH(c, SBD_KERNEL_O_PROJ, launch_gemm(EPI_RESID, go, ex));
     }
 
     const bf16_t* g_after = (l + 1 < m.n_layers) ? c->layers[l + 1].attn_norm : c->final_norm;
     if (small) {
-      GemvArgs vu = gemv_base(xn, xn_lo, d, M, d, wp + L.wp_gu, m.ffn_dim / 8, vpart, vpart_cap, counters);
+      GemvArgs vu = gemv_base(xn, xn_lo, d, M, d, wp + L.wp_gu, m.ffn_dim / 8, vpart, vpart_cap, counters, c->xcd_ok);
       w8((int64_t)l * L.wp_layer + L.wp_gu, (int64_t)l * L.ws_layer + L.ws_gu, vu);
       vu.sumsq_in = sumsq; vu.n_part_in = n_part_o; vu.inv_d = 1.0f / d; vu.eps = m.rms_eps;
       vu.act = act; vu.act_lo = act_lo; vu.ld_act = m.ffn_dim;
       SBD_LAUNCH(c, SBD_KERNEL_GATE_UP, launch_gemv(EPI_SWIGLU, vu, GemvShape{}, ex));
-      GemvArgs vd = gemv_base(act, act_lo, m.ffn_dim, M, m.ffn_dim, wp + L.wp_down, d / 16, vpart, vpart_cap, counters);
+      GemvArgs vd = gemv_base(act, act_lo, m.ffn_dim, M, m.ffn_dim, wp + L.wp_down, d / 16, vpart, vpart_cap, counters, c->xcd_ok);
       w8((int64_t)l * L.wp_layer + L.wp_down, (int64_t)l * L.ws_layer + L.ws_down, vd);
       vd.x = x; vd.ldx = d; vd.xn = xn; vd.xn_lo = xn_lo; vd.g_next = g_after;
       vd.sumsq = sumsq; vd.n_part = n_part_down;
       n_part_cur = n_part_down;
       SBD_LAUNCH(c, SBD_KERNEL_DOWN, launch_gemv(EPI_RESID, vd, GemvShape{}, ex));
     } else {
-      GemmArgs gu = gemm_base(xn, xn_lo, d, M, d, wp + L.wp_gu, m.ffn_dim / 8, vpart, vpart_cap, counters);
+      GemmArgs gu = gemm_base(xn, xn_lo, d, M, d, wp + L.wp_gu, m.ffn_dim / 8, vpart, vpart_cap, counters, c->xcd_ok);
       gu.a_mtiles = mt; gu.o_mtiles = mt;
       gu.sumsq_in = sumsq; gu.n_part = n_part_cur; gu.inv_d = 1.0f / d; gu.eps = m.rms_eps;
       gu.act = act; gu.act_lo = act_lo; gu.ld_act = m.ffn_dim;
       SBD_LAUNCH(c, SBD_KERNEL_GATE_UP, launch_gemm(EPI_SWIGLU, gu, ex));
 
       GemmArgs gd = gemm_base(act, act_lo, m.ffn_dim, M, m.ffn_dim, wp + L.wp_down, d / 16, vpart, vpart_cap,
-                              counters);
+                              counters, c->xcd_ok);
       gd.a_mtiles = mt; gd.o_mtiles = mt;
       gd.x = x; gd.ldx = d; gd.xn = xn; gd.xn_lo = xn_lo; gd.g_next = g_after;
       gd.sumsq_out = sumsq;
-      gd.n_part_out = gemm_plan(M, d / 16, m.ffn_dim, vpart_cap).n_cb;
+      gd.n_part_out = gemm_plan(M, d / 16, m.ffn_dim, c->xcd_ok ? vpart_cap : 0).n_cb;
       n_part_cur = gd.n_part_out;
       SBD_LAUNCH(c, SBD_KERNEL_DOWN, launch_gemm(EPI_RESID, gd, ex));
     }
@@ -506,7 +509,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     const GemmEpi lm_epi = eb ? EPI_LOGITS_EB : EPI_SCALED_STORE;
     if (mt == 0) {  // M <= 16: row-major inputs
       GemvArgs v = gemv_base(xn + (int64_t)r0 * d, xn_lo + (int64_t)r0 * d, d, Ml, d,
-                             c->at<bf16_t>(L.wpack) + L.wp_lm, m.vocab / 16, vpart, vpart_cap, counters);
+                             c->at<bf16_t>(L.wpack) + L.wp_lm, m.vocab / 16, vpart, vpart_cap, counters, c->xcd_ok);
       w8(L.wp_lm, L.ws_lm, v);
       v.sumsq_in = sumsq + (int64_t)r0 * n_part_cur; v.n_part_in = n_part_cur;
       v.inv_d = 1.0f / d; v.eps = m.rms_eps;
@@ -516,7 +519,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     } else {
       // inputs in fragment order (also for one row of a prefill chunk: rows from a_row0)
       GemmArgs gl = gemm_base(xn, xn_lo, d, Ml, d, c->at<bf16_t>(L.wpack) + L.wp_lm, m.vocab / 16, vpart,
-                              vpart_cap, counters);
+                              vpart_cap, counters, c->xcd_ok);
       gl.a_mtiles = mt; gl.a_row0 = r0;
       gl.out_f32 = logits; gl.ldo = m.vocab;
       gl.sumsq_in = sumsq + (int64_t)r0 * n_part_cur; gl.n_part = n_part_cur;
@@ -718,6 +721,22 @@ sbd_status sbd_create(const sbd_model_config* cfg, const sbd_weights* w, void* w
       c->n_cu = 0;
     c->n_cu_dev = c->n_cu;
     c->n_cu = std::min(c->n_cu, kFwdMaxWorkgroups);
+    // which XCD each workgroup runs on, for grids of the layer kernels' size, of a split
+    // GEMM's and the largest probed; the scratch is the attention partials' region, unused yet
+    c->xcd_ok = c->n_cu_dev == kXcds * kXcdWgs &&
+                (int64_t)kMaxSplits * L.m_max * cfg->n_q_heads * cfg->head_dim >= kXcdProbeMax;
+    int* probe = c->at<int>(L.attn_o);
+    std::vector<int32_t> ids(kXcdProbeMax);
+    for (int n : {kXcds * kXcdWgs, 1000, kXcdProbeMax}) {
+      if (!c->xcd_ok) break;
+      int32_t good = 0;
+      c->xcd_ok = launch_xcd_probe(probe, n, c->stream) == hipSuccess &&
+                  hipMemcpyAsync(ids.data(), probe, (size_t)n * sizeof(int32_t), hipMemcpyDeviceToHost, c->stream) ==
+                      hipSuccess &&
+                  hipStreamSynchronize(c->stream) == hipSuccess &&
+                  sbd_xcd_map_check(ids.data(), n, kXcds, &good) == SBD_OK && good == 1;
+    }
+    (void)hipGetLastError();
   }
   if (!ok) {
     c->err = "initialising the workspace failed";
@@ -1103,9 +1122,26 @@ sbd_status sbd_decode_path_fits(const sbd_ctx* c, int32_t path, int32_t batch, i
       *fits = c->n_cu >= 1 && m.d_model % 128 == 0 && (m.head_dim == 64 || m.head_dim == 128) ? 1 : 0;
       return SBD_OK;
     }
-    case SBD_DECODE_LAYERS: *fits = layer_xcd_fits(c->cfg, c->n_cu_dev, batch, k) ? 1 : 0; return SBD_OK;
+    case SBD_DECODE_LAYERS: *fits = c->xcd_ok && layer_xcd_fits(c->cfg, c->n_cu_dev, batch, k) ? 1 : 0; return SBD_OK;
     default: return fail(nullptr, SBD_ERR_INVALID_ARG, "unknown decode path %d", path);
   }
+}
+
+sbd_status sbd_xcd_map_check(const int32_t* xcc_ids, int32_t n, int32_t n_xcd, int32_t* ok) {
+  if (!xcc_ids || !ok || n < 1 || n_xcd < 1) return fail(nullptr, SBD_ERR_INVALID_ARG, "bad argument");
+  *ok = 1;
+  for (int32_t i = 0; i < n; ++i)
+    if (xcc_ids[i] != i % n_xcd) {
+      *ok = 0;
+      break;
+    }
+  return SBD_OK;
+}
+
+sbd_status sbd_xcd_map_ok(const sbd_ctx* c, int32_t* ok) {
+  if (!c || !ok) return fail(nullptr, SBD_ERR_INVALID_ARG, "null argument");
+  *ok = c->xcd_ok ? 1 : 0;
+  return SBD_OK;
 }
 
 sbd_status sbd_profile_enable(sbd_ctx* c, int32_t enable) {

@@ -152,6 +152,7 @@ struct GemmArgs {
   int* counters;
   // set by launch_gemm from the plan
   int splits, m_blocks;
+  int no_split;        // 1: one K slice per unit (no hand-off between workgroups)
 };
 
 // How launch_gemm cuts a product: mt 16-row tiles per row block (m_blocks row blocks),
@@ -200,6 +201,7 @@ struct GemvArgs {
   int64_t part_cap;      // floats available at part (bounds the split)
   int* counters;         // arrival counters (kCounters words), zero between launches
   int splits;            // K slices per unit (set by the launcher)
+  int no_split;          // 1: one K slice per unit (no hand-off between workgroups)
 };
 // Launch shape of the decode GEMM; a zero field means "pick for the shape".
 struct GemvShape {
@@ -457,6 +459,8 @@ hipError_t launch_pack_fp8(const fp8_t* src0, const fp8_t* src1, fp8_t* dst, int
                            hipStream_t s);
 hipError_t launch_pack_fp8_widen(const fp8_t* src0, const fp8_t* src1, int e0, int e1, bf16_t* dst, int64_t rows,
                                  int K, int mode, hipStream_t s);
+hipError_t launch_xcd_probe(int* out, int n, hipStream_t s);
+constexpr int kXcdProbeMax = 2048;  // largest probed grid
 hipError_t launch_stream_probe(const void* buf, int64_t bytes, uint32_t* sink, int n_cu, hipStream_t s);
 
 }  // namespace sbd

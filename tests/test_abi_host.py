@@ -145,6 +145,26 @@ def test_noalloc_eb_select_validates_before_any_device_call(lib):
     assert b"static scratch" in lib.sbd_last_error(None) or b"mask_id" in lib.sbd_last_error(None)
 
 
+def test_xcd_map_decision():
+    """The check behind the per-XCD kernels' placement assumption: workgroup i on XCD i % n."""
+    f = P.load_library().sbd_xcd_map_check
+    ok = ctypes.c_int32(-1)
+
+    def check(ids, n_xcd=8):
+        arr = (ctypes.c_int32 * len(ids))(*ids)
+        assert f(arr, len(ids), n_xcd, ctypes.byref(ok)) == 0
+        return ok.value
+
+    assert check([i % 8 for i in range(2048)]) == 1
+    assert check([(i + 1) % 8 for i in range(256)]) == 0           # shifted by one XCD
+    assert check([(i // 32) for i in range(256)]) == 0             # blocks of 32 per XCD
+    ids = [i % 8 for i in range(1000)]
+    ids[999] = 0
+    assert check(ids) == 0                                          # one misplaced workgroup
+    assert check([0] * 64, n_xcd=1) == 1
+    assert f(None, 4, 8, ctypes.byref(ok)) == 1
+
+
 def test_workspace_regions():
     cfg = P.make_config(synth.TINY, 1, 128, 4)
     total = P.workspace_bytes(cfg)

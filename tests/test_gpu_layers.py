@@ -241,3 +241,10 @@ def test_generation_loop_two_blocks_of_16(setup):
                      label=f"K layer {li}: ")
         parity.close(vv[li].float().cpu().numpy(), cache.V[li][200:], max_abs=0.07, regress=(0.07, 4e-3),
                      label=f"V layer {li}: ")
+
+
+def test_xcd_placement_probe(setup):
+    """The probe at context creation found workgroup i on XCD i % 8 (the placement the layer
+    kernels and the split GEMMs hand partials off under), so AUTO takes the layer kernels."""
+    assert setup.lib.xcd_map_ok()
+    assert setup.lib.decode_path_fits("layers", 1, 16)
