@@ -29,10 +29,10 @@ METRIC = "SBD block-forward ms + HBM GB/s (8B shape, k=16); EB-select µs"
 PEAK_HBM_GBS = 8000.0
 
 
-def step_bytes(shape, lens, k, wbytes=2):
+def step_bytes(shape, lens, k, wbytes=2, kvbytes=2):
     """Algorithmic HBM bytes of one step: weights once (wbytes per element: 2 for bf16, 1 for
-    e4m3), KV read once, staged K/V written, fp32 logits written, EB reads the masked rows'
-    logits."""
+    e4m3), KV read once and staged K/V written (kvbytes per element, likewise), fp32 logits
+    written, EB reads the masked rows' logits."""
     s = shape
     d, F, V = s.d_model, s.ffn_dim, s.vocab
     qd, kvd = s.n_q_heads * s.head_dim, s.n_kv_heads * s.head_dim
@@ -40,8 +40,8 @@ def step_bytes(shape, lens, k, wbytes=2):
     weights = wbytes * (s.n_layers * per_layer + V * d)
     B = len(lens)
     M = B * k
-    kv_read = sum(lens) * s.n_layers * kvd * 2 * 2
-    kv_write = M * s.n_layers * kvd * 2 * 2
+    kv_read = sum(lens) * s.n_layers * kvd * 2 * kvbytes
+    kv_write = M * s.n_layers * kvd * 2 * kvbytes
     logits = 4 * M * V
     eb = 4 * B * (k - 1) * V
     fwd = weights + kv_read + kv_write + logits
@@ -89,10 +89,10 @@ def blas_threads():
     return len(os.sched_getaffinity(0))
 
 
-def cpu_baseline(wl, w_dev, lens, toks, gamma, min_seconds):
+def cpu_baseline(wl, w_dev, lens, toks, gamma, min_seconds, kv_fp8=False):
     """Time the oracle (fp32, as it stands) on the host: the whole block forward (every layer
     and the LM head) plus the EB step on the same block, repeated until min_seconds have
-    passed; returns the mean seconds per step."""
+    passed; returns the mean seconds per step.  kv_fp8: the cache in e4m3 (scale 1)."""
     import numpy as np
     import synth
     from oracle import sbd_oracle as O
@@ -102,8 +102,9 @@ def cpu_baseline(wl, w_dev, lens, toks, gamma, min_seconds):
     caches = []
     for b, L in enumerate(lens):
         kk, vv = synth.make_kv(s, wl.seed, b, L, device="cpu")
-        caches.append(O.SeqCache.from_arrays(synth.to_host_bits(kk), synth.to_host_bits(vv), np.float32))
-    model = O.Model(s, host, dtype=np.float32, cache_decoded=False)
+        c = O.SeqCache.from_arrays(synth.to_host_bits(kk), synth.to_host_bits(vv), np.float32)
+        caches.append(c.to_e4m3(0) if kv_fp8 else c)
+    model = O.Model(s, host, dtype=np.float32, cache_decoded=False, kv_fp8_exp=0 if kv_fp8 else None)
     is_mask = (toks == s.mask_id).astype(np.uint8)
     reps, total = 0, 0.0
     while total < min_seconds and reps < 8:
@@ -175,8 +176,9 @@ def speedup_table(args):
     batches = (1, 4, 8)
     lens = (2048, 16384)
     print("[bench] speedup table: generating weights", file=sys.stderr, flush=True)
-    w = synth.make_weights(s, 1002, device=dev)
-    lib = Sbd(s, w, max_batch=max(batches), max_seq_len=max(lens) + 2 * k + 64, max_block=2 * k)
+    w = (synth.make_weights_fp8 if args.weights == "fp8" else synth.make_weights)(s, 1002, device=dev)
+    lib = Sbd(s, w, max_batch=max(batches), max_seq_len=max(lens) + 2 * k + 64, max_block=2 * k,
+              kv_format="fp8_e4m3" if args.kv == "fp8" else "bf16")
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
 
     def fwd_ms(B, kk, nc):
@@ -223,7 +225,7 @@ def speedup_table(args):
               file=sys.stderr)
     print(json.dumps({"metric": "SBD block-forward time(1), time(k), time(2k) and speedup(l, k)", "k": k,
                       "shape": s.name, "data": "synthetic (random-init weights, synthetic KV caches)",
-                      "rows": rows}), flush=True)
+                      "weights": args.weights, "kv": args.kv, "rows": rows}), flush=True)
 
 
 def main():
@@ -239,12 +241,17 @@ def main():
                     help="kernels of decode-sized forwards (sbd_set_decode_path)")
     ap.add_argument("--weights", default="bf16", choices=["bf16", "fp8"],
                     help="weight format: bf16, or e4m3 with a power-of-two scale per matrix (Sec. 4.1's FP8 weights)")
+    ap.add_argument("--kv", default="bf16", choices=["bf16", "fp8"],
+                    help="KV-cache format: bf16, or e4m3 with scale 1 (Sec. 4.1's 1-byte KV)")
     ap.add_argument("--speedup-table", action="store_true",
                     help="measure time(1), time(k), time(2k) and the paper's speedup(l, k) instead")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
               "(batch sharding across GPUs is a design note only).", file=sys.stderr)
+        sys.exit(2)
+    if args.kv == "fp8" and args.decode_path == "fused":
+        print("the fused decode path reads a bf16 KV cache only", file=sys.stderr)
         sys.exit(2)
     if args.speedup_table:
         return speedup_table(args)
@@ -265,8 +272,11 @@ def main():
     print(f"[bench] {wl.name}: generating weights", file=sys.stderr, flush=True)
     fp8 = args.weights == "fp8"
     wbytes = 1 if fp8 else 2
+    kv8 = args.kv == "fp8"
+    kvbytes = 1 if kv8 else 2
     w = (synth.make_weights_fp8 if fp8 else synth.make_weights)(s, wl.seed, device=dev)
-    lib = Sbd(s, w, max_batch=B, max_seq_len=max(lens) + k + 64, max_block=k)
+    lib = Sbd(s, w, max_batch=B, max_seq_len=max(lens) + k + 64, max_block=k,
+              kv_format="fp8_e4m3" if kv8 else "bf16")
     lib.set_decode_path(args.decode_path)
     print(f"[bench] prefilling {B} x {lens[0]}..{lens[-1]} tokens", file=sys.stderr, flush=True)
     for b, L in enumerate(lens):
@@ -331,7 +341,7 @@ def main():
     else:
         ms_fused_step = None
 
-    fwd_bytes, eb_bytes = step_bytes(s, lens, k, wbytes)
+    fwd_bytes, eb_bytes = step_bytes(s, lens, k, wbytes, kvbytes)
     value = (fwd_bytes + eb_bytes) / (ms_step * 1e-3) / 1e9
     ceiling = copy_ceiling(torch, dev)
 
@@ -387,7 +397,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         print(f"[bench] oracle: full block forward + EB, at least {args.cpu_seconds:.0f} s", file=sys.stderr, flush=True)
-        est, info = cpu_baseline(wl, w, lens, toks, gamma, args.cpu_seconds)
+        est, info = cpu_baseline(wl, w, lens, toks, gamma, args.cpu_seconds, kv8)
         cores = blas_threads()
         cpu = {"value": round((fwd_bytes + eb_bytes) / est / 1e9, 4), "unit": "GB/s", "cores": cores,
                "kind": "oracle", "ms_per_step": round(est * 1e3, 1), "cpu_model": cpu_model(),
@@ -398,10 +408,12 @@ def main():
         "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "fp8-e4m3 weights, bf16 activations and KV" if fp8 else "bf16",
+        "dtype": (("fp8-e4m3" if fp8 else "bf16") + " weights, bf16 activations, " +
+                  ("fp8-e4m3" if kv8 else "bf16") + " KV") if fp8 or kv8 else "bf16",
         "data": "synthetic (seeded random-init weights, uniform random prompt tokens)",
         "config": {"workload": wl.name, "shape": s.name, "batch": B, "cache_len": lens, "k": k,
-                   "gamma": gamma, "n_causal": 1, "decode_path": args.decode_path, "weights": args.weights},
+                   "gamma": gamma, "n_causal": 1, "decode_path": args.decode_path, "weights": args.weights,
+                   "kv": args.kv},
         "block_forward_ms": round(ms_fwd, 4),
         "block_forward_gbs": round(fwd_bytes / (ms_fwd * 1e-3) / 1e9, 1),
         "block_forward_frac_of_peak": round(fwd_bytes / (ms_fwd * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),

@@ -65,6 +65,8 @@ typedef struct {
   float rms_eps, rope_theta;
   int32_t max_batch, max_seq_len, max_block, prefill_chunk;
   int32_t weight_format;  /* SBD_WEIGHTS_BF16 (0) or SBD_WEIGHTS_FP8_E4M3 (1), see sbd_weights */
+  int32_t kv_format;      /* SBD_KV_BF16 (0) or SBD_KV_FP8_E4M3 (1), see below */
+  int32_t kv_scale_exp;   /* SBD_KV_FP8_E4M3 only (else ignored): scale exponent e in [-100, 100] */
 } sbd_model_config;
 
 /*
@@ -80,6 +82,21 @@ typedef struct {
  *                         path stream a bf16 copy of the same values, made in sbd_create.
  */
 enum { SBD_WEIGHTS_BF16 = 0, SBD_WEIGHTS_FP8_E4M3 = 1 };
+
+/*
+ * Formats of the KV cache (the cache of exact KV caching, Sec. 1 and Alg. 3).
+ *   SBD_KV_BF16      each cached key (after RoPE) and value is the bf16 rounding (nearest,
+ *                    ties to even) of the float the forward computes.
+ *   SBD_KV_FP8_E4M3  one byte per element (the 1-byte KV of the paper's timing model,
+ *                    Sec. 4.1): the e4m3 code of v * 2^-e, e = kv_scale_exp, rounded to the
+ *                    nearest code with ties to even and saturated at +-448 (NaN stays NaN),
+ *                    read back as e4m3 * 2^e.  The rows a forward stages are rounded so
+ *                    before its own attention reads them.  sbd_kv_import rounds its bf16
+ *                    input the same way; sbd_kv_export returns the stored values, which
+ *                    bf16 holds exactly.  The fused decode path reads bf16 caches only
+ *                    (UNSUPPORTED here); the other paths read both formats.
+ */
+enum { SBD_KV_BF16 = 0, SBD_KV_FP8_E4M3 = 1 };
 
 /*
  * Weights: device memory, borrowed (they must outlive the context and not change); bf16,
@@ -273,7 +290,8 @@ sbd_status sbd_eb_select_entropies(sbd_ctx* ctx, int32_t batch, int32_t k,
  * Write n cached rows of a slot from device bf16 K, V [n_layers][n][n_kv_heads][head_dim]
  * (K after RoPE), starting at position pos0 <= cache_len; the slot's cache length
  * becomes pos0 + n and nothing stays staged.  Restores a saved cache, or installs a
- * cache produced elsewhere.  Errors: CAPACITY if pos0 + n > max_seq_len.
+ * cache produced elsewhere.  An SBD_KV_FP8_E4M3 cache stores the rounding of the values
+ * described with that format.  Errors: CAPACITY if pos0 + n > max_seq_len.
  */
 sbd_status sbd_kv_import(sbd_ctx* ctx, int32_t seq, int32_t pos0, int32_t n, const void* k,
                          const void* v);

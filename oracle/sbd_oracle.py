@@ -38,7 +38,8 @@ e4m3 bytes with a power-of-two scale per matrix, decoded here from the format's 
 
 Precision: everything runs in the dtype given to ``Model`` (float64 by default);
 EB statistics are always float64.  With ``kv_bf16`` the keys and values are held in
-bfloat16, the storage format of the KV cache; activations stay in the working dtype.
+bfloat16, the storage format of the KV cache, with ``kv_fp8_exp`` in e4m3 with a
+power-of-two scale (the 1-byte KV of Sec. 4.1); activations stay in the working dtype.
 """
 from __future__ import annotations
 
@@ -91,6 +92,23 @@ def round_to_bf16(a: np.ndarray) -> np.ndarray:
     a = np.asarray(a)
     m, e = np.frexp(a.astype(np.float64))
     return np.ldexp(np.rint(np.ldexp(m, 8)), e - 8).astype(a.dtype)
+
+
+def round_to_e4m3(a: np.ndarray, scale_exp: int = 0) -> np.ndarray:
+    """What a KV cache of e4m3 bytes with the scale 2^e holds for a (the 1-byte KV of the
+    paper's timing model, Sec. 4.1): x = a * 2^-e rounded to the nearest e4m3 value, ties to
+    even, saturated at +-448 (the largest finite code), times 2^e; NaN stays NaN.
+
+    The e4m3 values (decode_e4m3): from 2^-6 up they carry 4 significant bits; below 2^-6
+    they are the multiples of 2^-9.  With x = m * 2^q, 0.5 <= |m| < 1 (frexp), |x| >= 2^-6
+    is q >= -5 and keeps rint(m * 2^4) * 2^(q - 4); below, rint(x * 2^9) * 2^-9 (rint rounds
+    half to even; a carry to 2^q, or from the subnormals to 2^-6, is the next code up).
+    """
+    a = np.asarray(a)
+    x = np.ldexp(a.astype(np.float64), -int(scale_exp))
+    m, q = np.frexp(x)
+    r = np.where(q >= -5, np.ldexp(np.rint(np.ldexp(m, 4)), q - 4), np.ldexp(np.rint(np.ldexp(x, 9)), -9))
+    return np.ldexp(np.clip(r, -448.0, 448.0), int(scale_exp)).astype(a.dtype)
 
 
 def rms_norm(x: np.ndarray, g: np.ndarray, eps: float) -> np.ndarray:
@@ -179,6 +197,13 @@ class SeqCache:
         c.V = [a.copy() for a in self.V]
         return c
 
+    def to_e4m3(self, scale_exp: int) -> "SeqCache":
+        """A copy holding what an e4m3 cache with the scale 2^scale_exp stores (round_to_e4m3)."""
+        c = SeqCache.__new__(SeqCache)
+        c.K = [round_to_e4m3(a, scale_exp) for a in self.K]
+        c.V = [round_to_e4m3(a, scale_exp) for a in self.V]
+        return c
+
     @classmethod
     def from_arrays(cls, K, V, dtype) -> "SeqCache":
         """K, V: [n_layers][L][H_kv][d_h] (float or bf16 bits)."""
@@ -208,15 +233,17 @@ class Model:
     """
 
     def __init__(self, shape, weights: dict, dtype=np.float64, cache_decoded: bool = True,
-                 kv_bf16: bool = False):
+                 kv_bf16: bool = False, kv_fp8_exp: Optional[int] = None):
         """kv_bf16: keys/values are stored in bfloat16 (the KV-cache storage format of the
         GPU path): every K/V row is rounded to bf16 when it is produced, before it is used
-        by attention or appended to the cache."""
+        by attention or appended to the cache.  kv_fp8_exp = e: they are stored as e4m3
+        bytes with the scale 2^e instead (round_to_e4m3), rounded the same way."""
         self.s = shape
         self.w = weights
         self.dtype = np.dtype(dtype)
         self._memo = {} if cache_decoded else None
         self.kv_bf16 = kv_bf16
+        self.kv_fp8_exp = kv_fp8_exp
 
     # FP8 weights (uint8 arrays): the order of the per-matrix scale exponents in
     # weights["fp8_scale_exp"], per layer; the LM head's comes after every layer's
@@ -253,7 +280,9 @@ class Model:
             k = rms_norm(k, self.W("k_norm", li), s.rms_eps)
         cos, sin = rope_cos_sin(pos, s.head_dim, s.rope_theta, self.dtype)
         q, k = apply_rope(q, cos, sin), apply_rope(k, cos, sin)
-        if self.kv_bf16:
+        if self.kv_fp8_exp is not None:
+            k, v = round_to_e4m3(k, self.kv_fp8_exp), round_to_e4m3(v, self.kv_fp8_exp)
+        elif self.kv_bf16:
             k, v = round_to_bf16(k), round_to_bf16(v)
         return q, k, v
 

@@ -73,7 +73,7 @@ class ModelConfig(ctypes.Structure):
                 ("vocab", c_int32), ("mask_id", c_int32), ("qk_norm", c_int32),
                 ("rms_eps", c_float), ("rope_theta", c_float), ("max_batch", c_int32),
                 ("max_seq_len", c_int32), ("max_block", c_int32), ("prefill_chunk", c_int32),
-                ("weight_format", c_int32)]
+                ("weight_format", c_int32), ("kv_format", c_int32), ("kv_scale_exp", c_int32)]
 
 
 class Weights(ctypes.Structure):
@@ -81,6 +81,7 @@ class Weights(ctypes.Structure):
                [(f, POINTER(c_void_p)) for f in LAYER_FIELDS] + [("fp8_scale_exp", POINTER(c_int32))]
 
 WEIGHT_FORMATS = {"bf16": 0, "fp8_e4m3": 1}  # SBD_WEIGHTS_*
+KV_FORMATS = {"bf16": 0, "fp8_e4m3": 1}      # SBD_KV_*
 
 
 class SbdError(RuntimeError):
@@ -111,11 +112,13 @@ def load_library(path: str = LIB_PATH):
 
 
 def make_config(shape, max_batch: int, max_seq_len: int, max_block: int,
-                prefill_chunk: int = 0, weight_format: str = "bf16") -> ModelConfig:
+                prefill_chunk: int = 0, weight_format: str = "bf16", kv_format: str = "bf16",
+                kv_scale_exp: int = 0) -> ModelConfig:
     return ModelConfig(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads,
                        shape.head_dim, shape.ffn_dim, shape.vocab, shape.mask_id,
                        int(bool(shape.qk_norm)), float(shape.rms_eps), float(shape.rope_theta),
-                       max_batch, max_seq_len, max_block, prefill_chunk, WEIGHT_FORMATS[weight_format])
+                       max_batch, max_seq_len, max_block, prefill_chunk, WEIGHT_FORMATS[weight_format],
+                       KV_FORMATS[kv_format], int(kv_scale_exp))
 
 
 def _check(lib, st: int, where: str, ctx=None):
@@ -153,13 +156,16 @@ class Sbd:
                      "attn": torch.bfloat16, "act": torch.bfloat16, "xn": torch.bfloat16}
 
     def __init__(self, shape, weights: dict, max_batch: int, max_seq_len: int, max_block: int,
-                 prefill_chunk: int = 0, device="cuda"):
+                 prefill_chunk: int = 0, device="cuda", kv_format: str = "bf16", kv_scale_exp: int = 0):
         """weights: bf16 tensors, or with an "fp8_scale_exp" entry (synth.make_weights_fp8) the
-        projection and LM-head matrices as e4m3 bytes (uint8) with those scale exponents."""
+        projection and LM-head matrices as e4m3 bytes (uint8) with those scale exponents.
+        kv_format "fp8_e4m3": the KV cache holds e4m3 codes of value * 2^-kv_scale_exp."""
         self.lib = load_library()
         self.shape = shape
         self.weight_format = "fp8_e4m3" if "fp8_scale_exp" in weights else "bf16"
-        self.cfg = make_config(shape, max_batch, max_seq_len, max_block, prefill_chunk, self.weight_format)
+        self.kv_format = kv_format
+        self.cfg = make_config(shape, max_batch, max_seq_len, max_block, prefill_chunk, self.weight_format,
+                               kv_format, kv_scale_exp)
         self.device = torch.device(device)
         self.weights = weights                       # keep the borrowed tensors alive
         nbytes = workspace_bytes(self.cfg)

@@ -18,6 +18,8 @@
 // whole workgroup (see the kernels: attention_body.h for the launches that share a
 // workgroup with other phases, attn_split_kernel below for the standalone split kernel).
 
+#include <type_traits>
+
 #include "attention_body.h"
 
 namespace sbd {
@@ -28,15 +30,16 @@ namespace sbd {
 // rows, so each SIMD has two waves to overlap MFMA, softmax and LDS reads with the stream;
 // a ring of NBUF stages (128 KB) keeps NBUF - 1 stages in flight.  At the end the two key
 // halves of each row set are combined through LDS (log-sum-exp weights) into the split's
-// partial.  LDS reads are ds_read16, ordered by hand (see sbd_device.h).
-template <int DH>
+// partial.  LDS reads are ds_read16 (ds_read8 of an fp8 cache), ordered by hand (see
+// sbd_device.h).
+template <int DH, bool KV8>
 __global__ __launch_bounds__(512) void attn_split_kernel(AttnArgs a) {
+  using KB = KvBlk<DH, KV8>;    // a staged block's layout in LDS
   constexpr int NDT = DH / 16;  // 16-wide dimension tiles
   constexpr int NKS = DH / 32;  // 32-wide reduction steps for the scores
-  constexpr int BLK = 32 * DH * 2;            // bytes of K (or of V) per 32-key block
+  constexpr int BLK = KB::BYTES;              // bytes of K (or of V) per 32-key block
   constexpr int STAGE = 2 * 2 * BLK;          // two blocks, K and V
   constexpr int NBUF = (128 * 1024) / STAGE > 8 ? 8 : (128 * 1024) / STAGE;
-  constexpr int KPR = DH / 8;                 // 16-byte pieces per K row
   constexpr int LPB = BLK / 1024;             // 1 KB wave-loads per part per block
   constexpr int PER_WAVE = STAGE / 1024 / 8;  // wave-loads of one wave per stage
   static_assert(NBUF >= 3 && (NBUF - 2) * PER_WAVE <= 63, "ring shape");
@@ -82,10 +85,11 @@ __global__ __launch_bounds__(512) void attn_split_kernel(AttnArgs a) {
   const int n_st = blk1_wg > blk0 ? (blk1_wg - blk0 + 1) / 2 : 0;
 
   const int64_t hb = attn_head_base(a.layer, sp.slot, g, a.n_slots, a.n_kv, a.cap, DH);
-  const bf16_t* kbase = a.kcache + hb;
-  const bf16_t* vbase = a.vcache + hb;
+  const char* kbase = static_cast<const char*>(a.kcache) + hb * KB::ES;
+  const char* vbase = static_cast<const char*>(a.vcache) + hb * KB::ES;
+  const float kv_sc = a.kv_scale;
   // Wave-load u of wave w in stage st: i = w + 8u -> block i / (2 LPB) of the stage, part
-  // (i / LPB) % 2 (K, V), 1 KB slice i % LPB; pieces XOR-swizzled as in attn_core.
+  // (i / LPB) % 2 (K, V), 1 KB slice i % LPB; pieces XOR-swizzled (KvBlk).
   auto issue = [&](int st) {
     char* buf = smem + (st % NBUF) * STAGE;
 #pragma unroll
@@ -94,15 +98,7 @@ __global__ __launch_bounds__(512) void attn_split_kernel(AttnArgs a) {
       const int bi = idx / (2 * LPB), part = (idx / LPB) % 2, sub = idx % LPB;
       int kb = blk0 + 2 * st + bi;
       if (kb >= blk1_wg) kb = blk1_wg - 1;  // past the end: a valid block, never used
-      const bf16_t* src;
-      if (part == 0) {
-        const int row = sub * (1024 / (DH * 2)) + lane / KPR, pc = lane % KPR;
-        src = kbase + (int64_t)(kb * 32 + row) * DH + ((pc ^ (row % KPR)) * 8);
-      } else {
-        const int row = sub * 16 + lane / 4, pc = lane % 4;
-        src = vbase + (int64_t)kb * DH * 32 + row * 32 + ((pc ^ ((row >> 2) & 3)) * 8);
-      }
-      __builtin_amdgcn_global_load_lds((const void*)src,
+      __builtin_amdgcn_global_load_lds((const void*)KB::src(kbase, vbase, kb, part, sub * 64 + lane),
                                        (__attribute__((address_space(3))) void*)(buf + (bi * 2 + part) * BLK + sub * 1024),
                                        16, 0, 2);  // nt: each cache byte is read once
     }
@@ -119,19 +115,30 @@ __global__ __launch_bounds__(512) void attn_split_kernel(AttnArgs a) {
     if (kb >= blk1) return;  // wave-uniform: nothing of this block is visible to its rows
     const char* kblk = smem + (st % NBUF) * STAGE + (kh * 2) * BLK;
     const char* vblk = kblk + BLK;
+    // fragments: KV8 reads 8 bytes and widens them once the reads are complete
+    typedef typename std::conditional<KV8, i32x2, i32x4>::type Frag;
+    auto rd = [](const char* p) -> Frag {
+      if constexpr (KV8) return ds_read8(lds_addr(p));
+      else return ds_read16(lds_addr(p));
+    };
+    auto widen = [&](Frag v) -> i32x4 {
+      if constexpr (KV8) return e4m3x8_to_bf16(v, kv_sc);
+      else return v;
+    };
+    Frag kr[2][NKS];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int s2 = 0; s2 < NKS; ++s2) kr[t][s2] = rd(kblk + KB::koff(16 * t + r, s2, grp));
+    lds_wait();
     i32x4 kf[2][NKS];
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int s2 = 0; s2 < NKS; ++s2) {
-        const int row = 16 * t + r;
-        kf[t][s2] = ds_read16(lds_addr(kblk + row * DH * 2 + (((4 * s2 + grp) ^ (row % KPR)) * 16)));
+        lds_pin(kr[t][s2]);
+        kf[t][s2] = widen(kr[t][s2]);
       }
-    lds_wait();
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int s2 = 0; s2 < NKS; ++s2) lds_pin(kf[t][s2]);
     f32x4 sc[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
@@ -142,12 +149,9 @@ __global__ __launch_bounds__(512) void attn_split_kernel(AttnArgs a) {
         sc[t] = mfma16x16x32(kf[t][s2], ql[s2], sc[t]);
       }
     }
-    i32x4 vf[NDT];  // requested now: the softmax below hides their latency
+    Frag vr[NDT];  // requested now: the softmax below hides their latency
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt) {
-      const int row = 16 * dt + r;
-      vf[dt] = ds_read16(lds_addr(vblk + row * 64 + ((grp ^ ((row >> 2) & 3)) * 16)));
-    }
+    for (int dt = 0; dt < NDT; ++dt) vr[dt] = rd(vblk + KB::voff(16 * dt + r, grp));
     // sc[t][i]: score of key 32 kb + 16 t + 4 grp + i for query row r
     float mloc = -INFINITY;
 #pragma unroll
@@ -190,11 +194,12 @@ __global__ __launch_bounds__(512) void attn_split_kernel(AttnArgs a) {
     }
     lds_wait();
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt) lds_pin(vf[dt]);
+    for (int dt = 0; dt < NDT; ++dt) lds_pin(vr[dt]);
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) {
-      o[dt] = mfma16x16x32(vf[dt], pf, o[dt]);
-      o[dt] = mfma16x16x32(vf[dt], pl, o[dt]);
+      const i32x4 vf = widen(vr[dt]);
+      o[dt] = mfma16x16x32(vf, pf, o[dt]);
+      o[dt] = mfma16x16x32(vf, pl, o[dt]);
     }
   };
 
@@ -262,10 +267,14 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 
 hipError_t launch_attention_split(const AttnArgs& a, const Exec& ex) {
   dim3 grid(a.n_splits, a.n_kv * a.n_rowblocks, a.B);
-  if (a.d_h == 128)
-    SBD_KLAUNCH(attn_split_kernel<128>, grid, dim3(512), ex, a);
+  if (a.d_h == 128 && a.kv_fp8)
+    SBD_KLAUNCH((attn_split_kernel<128, true>), grid, dim3(512), ex, a);
+  else if (a.d_h == 128)
+    SBD_KLAUNCH((attn_split_kernel<128, false>), grid, dim3(512), ex, a);
+  else if (a.d_h == 64 && a.kv_fp8)
+    SBD_KLAUNCH((attn_split_kernel<64, true>), grid, dim3(512), ex, a);
   else if (a.d_h == 64)
-    SBD_KLAUNCH(attn_split_kernel<64>, grid, dim3(512), ex, a);
+    SBD_KLAUNCH((attn_split_kernel<64, false>), grid, dim3(512), ex, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

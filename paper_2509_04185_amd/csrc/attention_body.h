@@ -13,6 +13,49 @@ __device__ __forceinline__ int64_t attn_head_base(int layer, int slot, int g, in
   return (((int64_t)layer * n_slots + slot) * n_kv + g) * cap * d_h;
 }
 
+// A 32-key block of K (or of V) staged in LDS: 16-byte pieces, XOR-swizzled so that the
+// fragment reads below are free of bank conflicts, and copied straight from the cache into
+// LDS (global_load_lds: wave-load lane l fills LDS piece l of its 1 KB and reads the matching
+// global piece).  The cache holds bf16 or (KV8) e4m3 codes; an fp8 block takes half the LDS
+// and is widened to bf16 (times the cache's scale, exact) at the fragment reads.
+//   K: row `key` (DH elements) holds its piece c at c ^ ksw(key);
+//   V^T: row d (the block's 32 keys in slot order) holds its piece c at c ^ vsw(d).
+template <int DH, bool KV8>
+struct KvBlk {
+  static constexpr int ES = KV8 ? 1 : 2;          // bytes per cached element
+  static constexpr int BYTES = 32 * DH * ES;      // of K, or of V, per block
+  static constexpr int KPR = DH * ES / 16;        // pieces per K row
+  static constexpr int VPR = 32 * ES / 16;        // pieces per V^T row
+  __device__ static int ksw(int key) { return KV8 ? (key / (256 / DH)) % KPR : key % KPR; }
+  __device__ static int vsw(int d) { return KV8 ? (d >> 3) & 1 : (d >> 2) & 3; }
+  // Global source of LDS piece q (< BYTES / 16) of block kb; part 0 K, 1 V.
+  __device__ static const char* src(const char* kbase, const char* vbase, int kb, int part, int q) {
+    if (part == 0) {
+      const int key = q / KPR;
+      return kbase + ((int64_t)(kb * 32 + key) * DH) * ES + ((q % KPR) ^ ksw(key)) * 16;
+    }
+    const int d = q / VPR;
+    return vbase + ((int64_t)kb * DH * 32 + d * 32) * ES + ((q % VPR) ^ vsw(d)) * 16;
+  }
+  // LDS byte offset of this lane's K fragment (A operand: key `key`, dims 32 s + 8 grp .. +8)
+  __device__ static int koff(int key, int s, int grp) {
+    if (KV8) return key * DH + (((2 * s + (grp >> 1)) ^ ksw(key)) * 16) + (grp & 1) * 8;
+    return key * DH * 2 + (((4 * s + grp) ^ ksw(key)) * 16);
+  }
+  // LDS byte offset of this lane's V^T fragment (A operand: dim d, slots 8 grp .. +8)
+  __device__ static int voff(int d, int grp) {
+    if (KV8) return d * 32 + (((grp >> 1) ^ vsw(d)) * 16) + (grp & 1) * 8;
+    return d * 64 + ((grp ^ vsw(d)) * 16);
+  }
+  // The fragment at LDS byte address p as bf16 (sc: the cache's scale)
+  __device__ static i32x4 frag(const char* p, float sc) {
+    if constexpr (KV8)
+      return e4m3x8_to_bf16(*(const i32x2*)p, sc);
+    else
+      return *(const i32x4*)p;
+  }
+};
+
 // What one wave holds after its key range: unnormalised O^T tiles of its 16 query rows
 // (lane: row r = lane % 16, dims 16 dt + 4 (lane / 16) + i), the running max and sum.
 template <int DH>
@@ -27,7 +70,7 @@ struct AttnPart {
 // row block rb, sequence b.  smem: kAttnSmem bytes of LDS.  POL: cache policy of the loads
 // of the queries and of the keys and values (they may have been written earlier in the same
 // launch: kPolicyL2 when by the same XCD, kPolicyDevice when by any).
-template <int DH, int POL>
+template <int DH, int POL, bool KV8 = false>
 __device__ __forceinline__ void attn_core(const AttnArgs& a, int g, int rb, int b, int blk0, int blk_lim,
                                           char* smem, AttnPart<DH>& out) {
   constexpr int NDT = DH / 16;  // 16-wide dimension tiles
@@ -65,8 +108,10 @@ __device__ __forceinline__ void attn_core(const AttnArgs& a, int g, int rb, int 
   }
 
   const int64_t hb = attn_head_base(a.layer, sp.slot, g, a.n_slots, a.n_kv, a.cap, DH);
-  const bf16_t* kbase = a.kcache + hb;
-  const bf16_t* vbase = a.vcache + hb;
+  using KB = KvBlk<DH, KV8>;
+  const char* kbase = static_cast<const char*>(a.kcache) + hb * KB::ES;
+  const char* vbase = static_cast<const char*>(a.vcache) + hb * KB::ES;
+  const float kv_sc = a.kv_scale;
 
   f32x4 o[NDT];
 #pragma unroll
@@ -76,13 +121,9 @@ __device__ __forceinline__ void attn_core(const AttnArgs& a, int g, int rb, int 
   // The workgroup's key blocks are copied from the cache straight into LDS (global_load_lds,
   // no registers) in chunks of CH blocks, alternating between two buffers, so a chunk's
   // loads are all in flight at once and the next chunk streams in while the current one is
-  // used.  Inside a block the 16-byte pieces are XOR-swizzled so that the fragment reads
-  // below are free of bank conflicts: K row `key` holds its piece c at c ^ (key % (DH/8));
-  // V^T row d holds its piece c at c ^ ((d / 4) % 4).  The swizzle is applied on the source
-  // side: wave-load lane l fills LDS piece l of its 1 KB and reads the matching global piece.
-  constexpr int BLK = 32 * DH * 2;          // bytes of K (or of V) per 32-key block
-  constexpr int CH = 65536 / (4 * BLK);     // blocks per chunk (two buffers of K and V: 64 KB)
-  constexpr int KPR = DH / 8;               // 16-byte pieces per K row
+  // used (block layout in LDS: KvBlk).
+  constexpr int BLK = KB::BYTES;            // bytes of K (or of V) per 32-key block
+  constexpr int CH = 65536 / (4 * 32 * DH * 2);  // blocks per chunk (bf16: two buffers of K and V, 64 KB)
   constexpr int LPB = BLK / 1024;           // 1 KB wave-loads per part (K or V) per block
   constexpr int PER_WAVE = CH * 2 * LPB / 4;
   typedef char Chunk[CH][2][BLK];
@@ -107,15 +148,7 @@ __device__ __forceinline__ void attn_core(const AttnArgs& a, int g, int rb, int 
       const int bi = idx / (2 * LPB), part = (idx / LPB) % 2, sub = idx % LPB;
       int kb = blk0 + c * CH + bi;
       if (kb >= blk1_wg) kb = blk1_wg - 1;  // past the end: a valid block, never used
-      const bf16_t* src;
-      if (part == 0) {
-        const int row = sub * (1024 / (DH * 2)) + lane / KPR, pc = lane % KPR;
-        src = kbase + (int64_t)(kb * 32 + row) * DH + ((pc ^ (row % KPR)) * 8);
-      } else {
-        const int row = sub * 16 + lane / 4, pc = lane % 4;
-        src = vbase + (int64_t)kb * DH * 32 + row * 32 + ((pc ^ ((row >> 2) & 3)) * 8);
-      }
-      __builtin_amdgcn_global_load_lds((const void*)src,
+      __builtin_amdgcn_global_load_lds((const void*)KB::src(kbase, vbase, kb, part, sub * 64 + lane),
                                        (__attribute__((address_space(3))) void*)&buf[bi][part][sub * 1024],
                                        16, 0, POL);
     }
@@ -140,8 +173,7 @@ __device__ __forceinline__ void attn_core(const AttnArgs& a, int g, int rb, int 
         const int row = 16 * t + r;
 #pragma unroll
         for (int s2 = 0; s2 < NKS; ++s2) {
-          const int pc = (4 * s2 + grp) ^ (row % KPR);
-          const i32x4 kf = *(const i32x4*)(buf[bi][0] + row * DH * 2 + pc * 16);
+          const i32x4 kf = KB::frag(buf[bi][0] + KB::koff(row, s2, grp), kv_sc);
           st[bi][t] = mfma16x16x32(kf, qf[s2], st[bi][t]);
           st[bi][t] = mfma16x16x32(kf, ql[s2], st[bi][t]);
         }
@@ -197,9 +229,7 @@ __device__ __forceinline__ void attn_core(const AttnArgs& a, int g, int rb, int 
       }
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
-        const int row = 16 * dt + r;
-        const int pc = grp ^ ((row >> 2) & 3);
-        const i32x4 vf = *(const i32x4*)(buf[bi][1] + row * 64 + pc * 16);
+        const i32x4 vf = KB::frag(buf[bi][1] + KB::voff(16 * dt + r, grp), kv_sc);
         o[dt] = mfma16x16x32(vf, pf, o[dt]);
         o[dt] = mfma16x16x32(vf, pl, o[dt]);
       }
@@ -258,13 +288,13 @@ __device__ __forceinline__ void attn_core(const AttnArgs& a, int g, int rb, int 
 // block gy, sequence b.  Leaves the split's unnormalised (max, sum, O) per row for the merge.
 // DEV: the queries, keys and values were written earlier in the same launch (device-scope
 // loads), and the partial results are read by another workgroup of it (device-scope stores).
-template <int DH, bool DEV>
+template <int DH, bool DEV, bool KV8 = false>
 __device__ __forceinline__ void attn_split_body(const AttnArgs& a, int split, int gy, int b, char* smem) {
   constexpr int NDT = DH / 16;
   const int g = gy / a.n_rowblocks, rb = gy % a.n_rowblocks;
   const int blk0 = split * a.blocks_per_split;
   AttnPart<DH> pt;
-  attn_core<DH, DEV ? kPolicyDevice : 0>(a, g, rb, b, blk0, blk0 + a.blocks_per_split, smem, pt);
+  attn_core<DH, DEV ? kPolicyDevice : 0, KV8>(a, g, rb, b, blk0, blk0 + a.blocks_per_split, smem, pt);
   if (!pt.row_ok) return;
   const int lane = threadIdx.x & 63, grp = lane >> 4;
   const int k = a.k, G = a.n_q / a.n_kv;

@@ -28,14 +28,7 @@ __device__ __forceinline__ i32x4 ld_w(const bf16_t* p) { return ld16_stream(p); 
 __device__ __forceinline__ i32x2 ld_w(const fp8_t* p) { return __builtin_nontemporal_load((const i32x2*)p); }
 
 __device__ __forceinline__ i32x4 w_operand(i32x4 w, float) { return w; }
-__device__ __forceinline__ i32x4 w_operand(i32x2 w, float sc) {
-  i32x4 o;
-  o[0] = __builtin_bit_cast(int, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[0], sc, false));
-  o[1] = __builtin_bit_cast(int, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[0], sc, true));
-  o[2] = __builtin_bit_cast(int, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[1], sc, false));
-  o[3] = __builtin_bit_cast(int, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[1], sc, true));
-  return o;
-}
+__device__ __forceinline__ i32x4 w_operand(i32x2 w, float sc) { return e4m3x8_to_bf16(w, sc); }
 
 // The lane's per-row weight scales of tiles t0 .. t0 + C - 1 (row 16 t + r); 1 for bf16.
 template <class WT, int C>

@@ -60,6 +60,20 @@ int main() {
     b = cfg;
     b.weight_format = 7;
     CHECK(sbd_workspace_bytes(&b, &bytes) == SBD_ERR_UNSUPPORTED);
+    b = cfg;
+    b.kv_format = 2;
+    CHECK(sbd_workspace_bytes(&b, &bytes) == SBD_ERR_UNSUPPORTED);
+    b = cfg;
+    b.kv_format = SBD_KV_FP8_E4M3;
+    b.kv_scale_exp = 101;
+    CHECK(sbd_workspace_bytes(&b, &bytes) == SBD_ERR_UNSUPPORTED);
+    b.kv_scale_exp = -100;
+    size_t b8 = 0, b16 = 0;
+    CHECK(sbd_workspace_bytes(&b, &b8) == SBD_OK && sbd_workspace_bytes(&cfg, &b16) == SBD_OK);
+    CHECK(b8 < b16);  // one byte per cached element instead of two
+    b = cfg;
+    b.kv_scale_exp = 1000;  // ignored with a bf16 cache
+    CHECK(sbd_workspace_bytes(&b, &bytes) == SBD_OK);
   }
   CHECK(sbd_workspace_bytes(&cfg, &bytes) == SBD_OK && bytes > 0);
 

@@ -222,7 +222,7 @@ __device__ __forceinline__ void residual_add(const LayerXArgs& a, int grp, int x
 
 // WT: the weights' format (bf16_t, or fp8_t widened to bf16 in registers: twice the steps per
 // batch keep the same bytes in flight).
-template <class WT>
+template <class WT, bool KV8>
 __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
   constexpr int UW = sizeof(WT) == 1 ? 2 : 1;  // batch scale of the weight streams
   __shared__ __attribute__((aligned(16))) char smem[kLxSmem];
@@ -249,6 +249,7 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
     e.n_q = a.n_q; e.n_kv = a.n_kv; e.d_h = kDH; e.qk_norm = a.qk_norm; e.eps = a.eps; e.q_scale = a.q_scale;
     e.rope = a.rope; e.q_norm = a.q_norm; e.k_norm = a.k_norm; e.q = a.q; e.q_lo = a.q_lo;
     e.kcache = a.kcache; e.vcache = a.vcache; e.cap = a.cap; e.n_slots = a.n_slots;
+    e.kv_fp8 = KV8; e.kv_inv = a.kv_inv;
     QkvPre<kDH> qpre;
     qkv_epi_prefetch<kDH>(e, a.M, qpre);
     const int arow = r < a.M ? r : a.M - 1;
@@ -345,18 +346,22 @@ __global__ __launch_bounds__(256) void layer_attn_kernel(LayerXArgs a) {
     {  // key blocks holding only positions cached before this forward: into the L2 now
       const int kb0 = nblk * s / a.n_tasks, kb1 = min(nblk * (s + 1) / a.n_tasks, L / 32);
       if (kb1 > kb0) {
-        const int64_t hb = attn_head_base(a.layer, sp.slot, x, a.n_slots, a.n_kv, a.cap, kDH);
-        touched += l2_touch(a.kcache + hb + (int64_t)kb0 * 32 * kDH, (int64_t)(kb1 - kb0) * 32 * kDH * 2);
-        touched += l2_touch(a.vcache + hb + (int64_t)kb0 * 32 * kDH, (int64_t)(kb1 - kb0) * 32 * kDH * 2);
+        constexpr int es = KV8 ? 1 : 2;  // bytes per cached element
+        const int64_t off = (attn_head_base(a.layer, sp.slot, x, a.n_slots, a.n_kv, a.cap, kDH) +
+                             (int64_t)kb0 * 32 * kDH) * es;
+        const int64_t bytes = (int64_t)(kb1 - kb0) * 32 * kDH * es;
+        touched += l2_touch(static_cast<const char*>(a.kcache) + off, bytes);
+        touched += l2_touch(static_cast<const char*>(a.vcache) + off, bytes);
       }
     }
     xcd_wait(a, xcd_ctr(a, x, kCtrQkvDone), ngrp, a.layer * 16 + 1);
     AttnArgs aa{};
     aa.seqs = a.seqs; aa.B = a.B; aa.k = a.k; aa.layer = a.layer; aa.n_q = a.n_q; aa.n_kv = a.n_kv; aa.d_h = kDH;
     aa.q = a.q; aa.q_lo = a.q_lo; aa.kcache = a.kcache; aa.vcache = a.vcache; aa.cap = a.cap; aa.n_slots = a.n_slots;
+    aa.kv_fp8 = KV8; aa.kv_scale = a.kv_scale;
     aa.n_rowblocks = 1;
     AttnPart<kDH> pt;
-    attn_core<kDH, kPolicyL2>(aa, x, 0, b, nblk * s / a.n_tasks, nblk * (s + 1) / a.n_tasks, smem, pt);
+    attn_core<kDH, kPolicyL2, KV8>(aa, x, 0, b, nblk * s / a.n_tasks, nblk * (s + 1) / a.n_tasks, smem, pt);
     if (pt.row_ok) {
       if (g4 == 0) *(float2*)(att_ml + ((int64_t)lw * kLxRows + pt.rho) * 2) = float2{pt.m, pt.l};
 #pragma unroll
@@ -584,10 +589,15 @@ bool layer_xcd_fits(const sbd_model_config& c, int n_cu, int B, int k) {
 }
 
 hipError_t launch_layer_attn(const LayerXArgs& a, bool fp8, const Exec& ex) {
-  if (fp8)
-    SBD_KLAUNCH(layer_attn_kernel<fp8_t>, dim3(kXcds * kXcdWgs), dim3(256), ex, a);
+  const dim3 grid(kXcds * kXcdWgs), block(256);
+  if (fp8 && a.kv_fp8)
+    SBD_KLAUNCH((layer_attn_kernel<fp8_t, true>), grid, block, ex, a);
+  else if (fp8)
+    SBD_KLAUNCH((layer_attn_kernel<fp8_t, false>), grid, block, ex, a);
+  else if (a.kv_fp8)
+    SBD_KLAUNCH((layer_attn_kernel<bf16_t, true>), grid, block, ex, a);
   else
-    SBD_KLAUNCH(layer_attn_kernel<bf16_t>, dim3(kXcds * kXcdWgs), dim3(256), ex, a);
+    SBD_KLAUNCH((layer_attn_kernel<bf16_t, false>), grid, block, ex, a);
   return hipGetLastError();
 }
 

@@ -109,19 +109,19 @@ __global__ __launch_bounds__(64) void rope_stage_kernel(RopeStageArgs a) {
       a.q_lo[o + lane + half] = lo;
     } else {
       const int g = h - a.n_q;
-      bf16_t* dst = a.kcache + kv_head_base(a.layer, sp.slot, g, a.n_slots, a.n_kv, a.cap, a.d_h) +
-                    (int64_t)p_cache * a.d_h;
-      dst[lane] = f2bf(r0);
-      dst[lane + half] = f2bf(r1);
+      const int64_t dst = kv_head_base(a.layer, sp.slot, g, a.n_slots, a.n_kv, a.cap, a.d_h) +
+                          (int64_t)p_cache * a.d_h;
+      kv_store(a.kcache, dst + lane, r0, a.kv_fp8, a.kv_inv);
+      kv_store(a.kcache, dst + lane + half, r1, a.kv_fp8, a.kv_inv);
     }
   } else {
     if (!act) return;
     const int g = h - a.n_q - a.n_kv;
-    bf16_t* blk = a.vcache + kv_head_base(a.layer, sp.slot, g, a.n_slots, a.n_kv, a.cap, a.d_h) +
-                  (int64_t)(p_cache / 32) * a.d_h * 32;
+    const int64_t blk = kv_head_base(a.layer, sp.slot, g, a.n_slots, a.n_kv, a.cap, a.d_h) +
+                        (int64_t)(p_cache / 32) * a.d_h * 32;
     const int sl = vslot(p_cache & 31);
-    blk[(int64_t)lane * 32 + sl] = f2bf(u0);
-    blk[(int64_t)(lane + half) * 32 + sl] = f2bf(u1);
+    kv_store(a.vcache, blk + (int64_t)lane * 32 + sl, u0, a.kv_fp8, a.kv_inv);
+    kv_store(a.vcache, blk + (int64_t)(lane + half) * 32 + sl, u1, a.kv_fp8, a.kv_inv);
   }
 }
 
@@ -157,16 +157,20 @@ __global__ __launch_bounds__(64) void kv_copy_kernel(KvCopyArgs a) {
   const int p = a.pos0 + t;
   const int64_t hb = kv_head_base(layer, a.slot, g, a.n_slots, a.n_kv, a.cap, a.d_h);
   const int64_t io = (((int64_t)layer * a.n + t) * a.n_kv + g) * a.d_h;
-  bf16_t* kc = a.kcache + hb + (int64_t)p * a.d_h;
-  bf16_t* vb = a.vcache + hb + (int64_t)(p / 32) * a.d_h * 32;
+  const int64_t kc = hb + (int64_t)p * a.d_h;
+  const int64_t vb = hb + (int64_t)(p / 32) * a.d_h * 32;
   const int sl = vslot(p & 31);
   for (int i = threadIdx.x; i < a.d_h; i += 64) {
-    if (IMPORT) {
-      kc[i] = a.k_in[io + i];
-      vb[(int64_t)i * 32 + sl] = a.v_in[io + i];
+    const int64_t ki = kc + i, vi = vb + (int64_t)i * 32 + sl;
+    if (IMPORT) {  // an fp8 cache gets the e4m3 code of the value (kv_store)
+      kv_store(a.kcache, ki, bf2f(a.k_in[io + i]), a.kv_fp8, a.kv_inv);
+      kv_store(a.vcache, vi, bf2f(a.v_in[io + i]), a.kv_fp8, a.kv_inv);
+    } else if (a.kv_fp8) {  // widened: at most 4 significant bits, exact in bf16
+      a.k_out[io + i] = f2bf(e4m3_to_f32(static_cast<const uint8_t*>(a.kcache)[ki], a.kv_scale));
+      a.v_out[io + i] = f2bf(e4m3_to_f32(static_cast<const uint8_t*>(a.vcache)[vi], a.kv_scale));
     } else {
-      a.k_out[io + i] = kc[i];
-      a.v_out[io + i] = vb[(int64_t)i * 32 + sl];
+      a.k_out[io + i] = static_cast<const bf16_t*>(a.kcache)[ki];
+      a.v_out[io + i] = static_cast<const bf16_t*>(a.vcache)[vi];
     }
   }
 }

@@ -91,12 +91,12 @@ __device__ __forceinline__ void qkv_epilogue(const QkvEpi& e, int M, int grp, co
       const int h = grp * heads + hh;
       if (h >= e.n_q + e.n_kv) {  // V: transposed cache block, slot order of misc.hip vslot()
         const int gk = h - e.n_q - e.n_kv;
-        bf16_t* blk = e.vcache + (((int64_t)e.layer * e.n_slots + pre.slot[i]) * e.n_kv + gk) * e.cap * DH +
-                      (int64_t)(p_cache / 32) * DH * 32;
+        const int64_t blk = (((int64_t)e.layer * e.n_slots + pre.slot[i]) * e.n_kv + gk) * e.cap * DH +
+                            (int64_t)(p_cache / 32) * DH * 32;
         const int p = p_cache & 31;
         const int sl = ((p & 15) >> 2) * 8 + (p >> 4) * 4 + (p & 3);
 #pragma unroll
-        for (int t = 0; t < tph; ++t) blk[(16 * t + r) * 32 + sl] = f2bf(u[hh * tph + t]);
+        for (int t = 0; t < tph; ++t) kv_store(e.vcache, blk + (16 * t + r) * 32 + sl, u[hh * tph + t], e.kv_fp8, e.kv_inv);
         continue;
       }
 #pragma unroll
@@ -117,10 +117,10 @@ __device__ __forceinline__ void qkv_epilogue(const QkvEpi& e, int M, int grp, co
           e.q_lo[o + dim + half] = lo;
         } else {
           const int gk = h - e.n_q;
-          bf16_t* dst = e.kcache + (((int64_t)e.layer * e.n_slots + pre.slot[i]) * e.n_kv + gk) * e.cap * DH +
-                        (int64_t)p_cache * DH;
-          dst[dim] = f2bf(r0);
-          dst[dim + half] = f2bf(r1);
+          const int64_t dst = (((int64_t)e.layer * e.n_slots + pre.slot[i]) * e.n_kv + gk) * e.cap * DH +
+                              (int64_t)p_cache * DH;
+          kv_store(e.kcache, dst + dim, r0, e.kv_fp8, e.kv_inv);
+          kv_store(e.kcache, dst + dim + half, r1, e.kv_fp8, e.kv_inv);
         }
       }
     }

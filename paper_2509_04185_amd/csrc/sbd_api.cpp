@@ -25,6 +25,17 @@ size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
 int effective_chunk(const sbd_model_config& c) { return c.prefill_chunk > 0 ? c.prefill_chunk : 256; }
 
+// The KV cache's format as the kernels take it: e4m3 codes of value * inv, read back times
+// scale (scale = 2^kv_scale_exp, exact), or bf16.
+struct KvFmt {
+  int fp8;
+  float scale, inv;
+};
+KvFmt kv_fmt(const sbd_model_config& m) {
+  if (m.kv_format != SBD_KV_FP8_E4M3) return KvFmt{0, 1.f, 1.f};
+  return KvFmt{1, std::ldexp(1.f, m.kv_scale_exp), std::ldexp(1.f, -m.kv_scale_exp)};
+}
+
 const char* check_config(const sbd_model_config& c) {
   if (c.n_layers < 1) return "n_layers must be >= 1";
   if (c.d_model < 256 || c.d_model % 256) return "d_model must be a positive multiple of 256";
@@ -46,6 +57,10 @@ const char* check_config(const sbd_model_config& c) {
   if (c.prefill_chunk < 0 || c.prefill_chunk > 4096) return "prefill_chunk must lie in [0, 4096]";
   if (c.weight_format != SBD_WEIGHTS_BF16 && c.weight_format != SBD_WEIGHTS_FP8_E4M3)
     return "weight_format must be SBD_WEIGHTS_BF16 or SBD_WEIGHTS_FP8_E4M3";
+  if (c.kv_format != SBD_KV_BF16 && c.kv_format != SBD_KV_FP8_E4M3)
+    return "kv_format must be SBD_KV_BF16 or SBD_KV_FP8_E4M3";
+  if (c.kv_format == SBD_KV_FP8_E4M3 && (c.kv_scale_exp < -100 || c.kv_scale_exp > 100))
+    return "kv_scale_exp must lie in [-100, 100]";
   return nullptr;
 }
 
@@ -69,8 +84,9 @@ bool sbd::compute_layout(const sbd_model_config& c, Layout* L) {
     off = align256(off + bytes);
     return at;
   };
-  o.kcache = take(kv_elems * 2);
-  o.vcache = take(kv_elems * 2);
+  const int64_t kv_es = c.kv_format == SBD_KV_FP8_E4M3 ? 1 : 2;  // bytes per cached element
+  o.kcache = take(kv_elems * kv_es);
+  o.vcache = take(kv_elems * kv_es);
   o.rope = take(o.cap * (c.head_dim / 2) * 2 * sizeof(float));
   o.x = take(o.m_max * c.d_model * sizeof(float));
   o.xn = take(2 * o.m_max * c.d_model * 2);             // hi then lo
@@ -309,10 +325,16 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   };
   // forwards of more than 16 rows keep the GEMMs' activation operands in fragment order
   const int mt = small ? 0 : (M + 15) / 16;
+  // the KV cache: bf16, or e4m3 codes of value * 2^-e
+  const KvFmt kvf = kv_fmt(m);
+  void* kcache = c->ws + L.kcache;
+  void* vcache = c->ws + L.vcache;
 
   // The fused decode forward: checked before anything is enqueued.
   const bool fused = small && c->decode_path == SBD_DECODE_FUSED;
   FwdArgs f{};
+  if (fused && kvf.fp8)
+    return fail(c, SBD_ERR_UNSUPPORTED, "the fused decode forward reads a bf16 KV cache only");
   if (fused) {
     f.M = M; f.B = B; f.k = k; f.n_layers = m.n_layers;
     f.d = d; f.n_q = nq; f.n_kv = nkv; f.d_h = dh; f.ffn = m.ffn_dim; f.vocab = m.vocab; f.qk_norm = m.qk_norm;
@@ -385,7 +407,8 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     lx.q_scale = (float)(1.4426950408889634 / std::sqrt((double)dh));
     lx.n_tasks = kXcdWgs / B;
     lx.q = q; lx.q_lo = q_lo; lx.attn = attn; lx.attn_lo = attn_lo; lx.act = act; lx.act_lo = act_lo;
-    lx.kcache = c->at<bf16_t>(L.kcache); lx.vcache = c->at<bf16_t>(L.vcache); lx.cap = L.cap;
+    lx.kcache = kcache; lx.vcache = vcache; lx.cap = L.cap;
+    lx.kv_fp8 = kvf.fp8; lx.kv_scale = kvf.scale; lx.kv_inv = kvf.inv;
     lx.n_slots = m.max_batch; lx.rope = c->at<float>(L.rope); lx.rows = drows; lx.seqs = dseqs;
     lx.xpart = c->at<float>(L.lx_part);
     lx.ctr = c->at<int>(L.counters) + kLayerCtr0; lx.err = c->at<int>(L.fwd_err); lx.err_host = c->err_host;
@@ -422,7 +445,8 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     qe.n_q = nq; qe.n_kv = nkv; qe.d_h = dh; qe.qk_norm = m.qk_norm; qe.eps = m.rms_eps;
     qe.q_scale = (float)(1.4426950408889634 / std::sqrt((double)dh));
     qe.rope = c->at<float>(L.rope); qe.q_norm = w.q_norm; qe.k_norm = w.k_norm;
-    qe.q = q; qe.q_lo = q_lo; qe.kcache = c->at<bf16_t>(L.kcache); qe.vcache = c->at<bf16_t>(L.vcache);
+    qe.q = q; qe.q_lo = q_lo; qe.kcache = kcache; qe.vcache = vcache;
+    qe.kv_fp8 = kvf.fp8; qe.kv_inv = kvf.inv;
     qe.cap = L.cap; qe.n_slots = m.max_batch;
     if (small) {
       // QKV + q/k norm + RoPE + KV staging in one kernel
@@ -442,14 +466,16 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
       ra.n_q = nq; ra.n_kv = nkv; ra.d_h = dh; ra.qk_norm = m.qk_norm; ra.eps = m.rms_eps;
       ra.q_scale = qe.q_scale;
       ra.qkv = qkv; ra.q_norm = w.q_norm; ra.k_norm = w.k_norm; ra.rope = c->at<float>(L.rope);
-      ra.q = q; ra.q_lo = q_lo; ra.kcache = qe.kcache; ra.vcache = qe.vcache;
+      ra.q = q; ra.q_lo = q_lo; ra.kcache = kcache; ra.vcache = vcache;
+      ra.kv_fp8 = kvf.fp8; ra.kv_inv = kvf.inv;
       ra.cap = L.cap; ra.n_slots = m.max_batch;
       SBD_LAUNCH(c, SBD_KERNEL_ROPE, launch_rope_stage(ra, ex));
     }
 
     AttnArgs aa{};
     aa.seqs = dseqs; aa.B = B; aa.k = k; aa.layer = l; aa.n_q = nq; aa.n_kv = nkv; aa.d_h = dh;
-    aa.q = q; aa.q_lo = q_lo; aa.kcache = qe.kcache; aa.vcache = qe.vcache; aa.cap = L.cap; aa.n_slots = m.max_batch;
+    aa.q = q; aa.q_lo = q_lo; aa.kcache = kcache; aa.vcache = vcache; aa.cap = L.cap; aa.n_slots = m.max_batch;
+    aa.kv_fp8 = kvf.fp8; aa.kv_scale = kvf.scale;
     aa.n_rowblocks = n_rb; aa.n_splits = n_splits; aa.blocks_per_split = bps;
     aa.part_ml = c->at<float>(L.attn_ml); aa.part_o = c->at<float>(L.attn_o); aa.out = attn;
     aa.out_lo = attn_lo;
@@ -1073,12 +1099,19 @@ static sbd_status kv_common(sbd_ctx* c, int32_t seq, int32_t pos0, int32_t n, co
   return check_sticky(c);
 }
 
-sbd_status sbd_kv_import(sbd_ctx* c, int32_t seq, int32_t pos0, int32_t n, const void* k, const void* v) {
-  if (sbd_status st = kv_common(c, seq, pos0, n, k, v, true)) return st;
+static KvCopyArgs kv_copy_base(sbd_ctx* c, int32_t seq, int32_t pos0, int32_t n) {
+  const KvFmt kvf = kv_fmt(c->cfg);
   KvCopyArgs a{};
-  a.kcache = c->at<bf16_t>(c->lay.kcache); a.vcache = c->at<bf16_t>(c->lay.vcache); a.cap = c->lay.cap;
+  a.kcache = c->ws + c->lay.kcache; a.vcache = c->ws + c->lay.vcache; a.cap = c->lay.cap;
+  a.kv_fp8 = kvf.fp8; a.kv_scale = kvf.scale; a.kv_inv = kvf.inv;
   a.n_layers = c->cfg.n_layers; a.n_slots = c->cfg.max_batch; a.n_kv = c->cfg.n_kv_heads;
   a.d_h = c->cfg.head_dim; a.slot = seq; a.pos0 = pos0; a.n = n;
+  return a;
+}
+
+sbd_status sbd_kv_import(sbd_ctx* c, int32_t seq, int32_t pos0, int32_t n, const void* k, const void* v) {
+  if (sbd_status st = kv_common(c, seq, pos0, n, k, v, true)) return st;
+  KvCopyArgs a = kv_copy_base(c, seq, pos0, n);
   a.k_in = static_cast<const bf16_t*>(k); a.v_in = static_cast<const bf16_t*>(v);
   SBD_HIP(c, launch_kv_import(a, c->stream));
   c->cache_len[seq] = pos0 + n;
@@ -1088,10 +1121,7 @@ sbd_status sbd_kv_import(sbd_ctx* c, int32_t seq, int32_t pos0, int32_t n, const
 
 sbd_status sbd_kv_export(sbd_ctx* c, int32_t seq, int32_t pos0, int32_t n, void* k, void* v) {
   if (sbd_status st = kv_common(c, seq, pos0, n, k, v, false)) return st;
-  KvCopyArgs a{};
-  a.kcache = c->at<bf16_t>(c->lay.kcache); a.vcache = c->at<bf16_t>(c->lay.vcache); a.cap = c->lay.cap;
-  a.n_layers = c->cfg.n_layers; a.n_slots = c->cfg.max_batch; a.n_kv = c->cfg.n_kv_heads;
-  a.d_h = c->cfg.head_dim; a.slot = seq; a.pos0 = pos0; a.n = n;
+  KvCopyArgs a = kv_copy_base(c, seq, pos0, n);
   a.k_out = static_cast<bf16_t*>(k); a.v_out = static_cast<bf16_t*>(v);
   SBD_HIP(c, launch_kv_export(a, c->stream));
   return SBD_OK;
@@ -1119,7 +1149,8 @@ sbd_status sbd_decode_path_fits(const sbd_ctx* c, int32_t path, int32_t batch, i
     case SBD_DECODE_KERNELS: *fits = 1; return SBD_OK;
     case SBD_DECODE_FUSED: {
       const sbd_model_config& m = c->cfg;
-      *fits = c->n_cu >= 1 && m.d_model % 128 == 0 && (m.head_dim == 64 || m.head_dim == 128) ? 1 : 0;
+      *fits = c->n_cu >= 1 && m.d_model % 128 == 0 && (m.head_dim == 64 || m.head_dim == 128) &&
+              m.kv_format == SBD_KV_BF16 ? 1 : 0;
       return SBD_OK;
     }
     case SBD_DECODE_LAYERS: *fits = c->xcd_ok && layer_xcd_fits(c->cfg, c->n_cu_dev, batch, k) ? 1 : 0; return SBD_OK;

@@ -23,6 +23,52 @@ __device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float(((uint3
 // float -> bf16, round to nearest even (the gfx950 conversion instruction); NaN stays NaN.
 __device__ __forceinline__ bf16_t f2bf(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
 
+// OCP e4m3 ("fn") code of v: round to nearest, ties to even, saturating at +-448 (the
+// largest finite code; infinities saturate too), NaN -> 0x7f.  Below 2^-6 the codes are the
+// subnormals m * 2^-9 (a rounding up to 8 * 2^-9 gives the smallest normal, code 8).
+__device__ __forceinline__ uint32_t f32_to_e4m3(float v) {
+  const uint32_t sign = (__float_as_uint(v) >> 24) & 0x80u;
+  const float a = fabsf(v);
+  if (!(a == a)) return 0x7fu;
+  if (a >= 448.f) return sign | 0x7eu;
+  if (a < 0.015625f) return sign | (uint32_t)rintf(a * 512.f);
+  int e;
+  const float r = frexpf(a, &e);                      // a = r 2^e, r in [0.5, 1)
+  uint32_t m = (uint32_t)rintf((2.f * r - 1.f) * 8.f);  // a = (1 + m/8) 2^(e-1)
+  int ex = e - 1;
+  if (m == 8) {
+    m = 0;
+    ++ex;
+  }
+  return sign | min((uint32_t)((ex + 7) << 3) | m, 0x7eu);
+}
+// Value of an e4m3 code times s (exact for s a power of two in range).
+__device__ __forceinline__ float e4m3_to_f32(uint32_t c, float s) {
+  const uint32_t e = (c >> 3) & 15u, m = c & 7u;
+  float a = e == 0 ? (float)m * 0.001953125f : ldexpf(1.f + (float)m * 0.125f, (int)e - 7);
+  if (e == 15 && m == 7) a = __builtin_nanf("");
+  return ((c & 0x80u) ? -a : a) * s;
+}
+// Eight e4m3 codes (byte i = element i) -> eight bf16 values times s, as an MFMA operand
+// (the gfx950 scaled conversion; exact when s is a power of two and the products are in
+// the normal range of bf16, which holds for every e4m3 value and the scales used here).
+__device__ __forceinline__ i32x4 e4m3x8_to_bf16(i32x2 w, float s) {
+  i32x4 o;
+  o[0] = __builtin_bit_cast(int, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[0], s, false));
+  o[1] = __builtin_bit_cast(int, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[0], s, true));
+  o[2] = __builtin_bit_cast(int, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[1], s, false));
+  o[3] = __builtin_bit_cast(int, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[1], s, true));
+  return o;
+}
+// One value into the KV cache at element idx: bf16, or the e4m3 code of v * inv (inv = 2^-e,
+// the inverse of the cache's scale).
+__device__ __forceinline__ void kv_store(void* base, int64_t idx, float v, int fp8, float inv) {
+  if (fp8)
+    static_cast<uint8_t*>(base)[idx] = (uint8_t)f32_to_e4m3(v * inv);
+  else
+    static_cast<bf16_t*>(base)[idx] = f2bf(v);
+}
+
 // Split v into hi = bf16(v) and lo = bf16(v - hi).
 __device__ __forceinline__ void split_bf16(float v, bf16_t& hi, bf16_t& lo) {
   hi = f2bf(v);
@@ -178,6 +224,14 @@ __device__ __forceinline__ i32x4 ds_read16(uint32_t addr) {
 }
 __device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 __device__ __forceinline__ void lds_pin(i32x4& v) { asm volatile("" : "+v"(v)); }
+template <int OFF = 0>
+__device__ __forceinline__ i32x2 ds_read8(uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
+  i32x2 v;
+  asm volatile("ds_read_b64 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF));
+  return v;
+}
+__device__ __forceinline__ void lds_pin(i32x2& v) { asm volatile("" : "+v"(v)); }
 // LDS byte address of a __shared__ object
 __device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
 

@@ -99,8 +99,10 @@ struct QkvEpi {
   const bf16_t* k_norm;
   bf16_t* q;
   bf16_t* q_lo;
-  bf16_t* kcache;
-  bf16_t* vcache;
+  void* kcache;       // KV cache: bf16, or e4m3 codes (kv_fp8) of value * kv_inv
+  void* vcache;
+  int kv_fp8;
+  float kv_inv;
   int64_t cap;
   int n_slots;
 };
@@ -245,8 +247,10 @@ struct RopeStageArgs {
   const float* rope;  // [cap][d_h/2][2] (cos, sin)
   bf16_t* q;     // [M][n_q][d_h] hi
   bf16_t* q_lo;  // lo
-  bf16_t* kcache;
-  bf16_t* vcache;
+  void* kcache;  // bf16, or e4m3 codes (kv_fp8) of value * kv_inv
+  void* vcache;
+  int kv_fp8;
+  float kv_inv;
   int64_t cap;
   int n_slots;
 };
@@ -255,8 +259,10 @@ hipError_t launch_rope_stage(const RopeStageArgs& a, const Exec& ex);
 hipError_t launch_rope_table(float* rope, int64_t cap, int d_h, double theta, hipStream_t s);
 
 struct KvCopyArgs {
-  bf16_t* kcache;
-  bf16_t* vcache;
+  void* kcache;        // bf16, or e4m3 codes (kv_fp8): imports round, exports widen
+  void* vcache;
+  int kv_fp8;
+  float kv_scale, kv_inv;
   int64_t cap;
   int n_layers, n_slots, n_kv, d_h;
   int slot, pos0, n;
@@ -275,8 +281,10 @@ struct AttnArgs {
   int n_q, n_kv, d_h;
   const bf16_t* q;     // [B*k][n_q][d_h] hi, pre-scaled by log2(e)/sqrt(d_h)
   const bf16_t* q_lo;  // lo
-  const bf16_t* kcache;
-  const bf16_t* vcache;
+  const void* kcache;  // bf16, or e4m3 codes (kv_fp8) with the scale kv_scale
+  const void* vcache;
+  int kv_fp8;
+  float kv_scale;
   int64_t cap;
   int n_slots;
   int n_rowblocks;  // ceil(group * k / 64)
@@ -387,7 +395,9 @@ struct LayerXArgs {
   int64_t* x_dst;                    // the residual after this launch: zero on entry, atomics add into it
   int64_t* x_zero;                   // the third buffer: zeroed for the next launch
   bf16_t *q, *q_lo, *attn, *attn_lo, *act, *act_lo;
-  bf16_t *kcache, *vcache;
+  void *kcache, *vcache;             // bf16, or e4m3 codes (kv_fp8)
+  int kv_fp8;
+  float kv_scale, kv_inv;
   int64_t cap;
   int n_slots;
   const float* rope;

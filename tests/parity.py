@@ -76,3 +76,21 @@ def eb_compare(n_acc, pos, tok, ref_acc, ref_tok, ref_H, is_mask, gamma, label="
         assert (pos[b, n:] == -1).all()
     print(f"    {label}gamma {gamma}: smallest EB decision margin {worst:.3e}", flush=True)
     return worst
+
+
+def kv8_close(got, ref, scale_exp, max_frac=1e-3, label=""):
+    """Keys/values of an e4m3 cache against the oracle's (both on the grid e4m3 * 2^e).
+
+    The two sides round floats that agree to float precision, not bit for bit, so a value
+    near the midpoint of two codes may land on either: at most max_frac of the elements may
+    differ, each by one step of the grid (the larger spacing at a binade edge)."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    s = 2.0 ** scale_exp
+    mag = np.maximum(np.abs(got), np.abs(ref)) / s
+    step = np.where(mag >= 2.0 ** -6, np.exp2(np.floor(np.log2(np.maximum(mag, 2.0 ** -6))) - 3), 2.0 ** -9) * s
+    diff = got != ref
+    n = int(diff.sum())
+    print(f"    {label}{n} of {got.size} values one code apart", flush=True)
+    assert n <= max_frac * got.size, f"{label}{n} of {got.size} e4m3 values differ"
+    assert (np.abs(got - ref)[diff] <= step[diff]).all(), f"{label}values differ by more than one e4m3 step"

@@ -77,6 +77,24 @@ def test_unknown_weight_format_rejected():
         P.workspace_bytes(cfg)
 
 
+def test_kv_format_checks_and_workspace():
+    """An e4m3 KV cache takes one byte per element; unknown formats and out-of-range scale
+    exponents are rejected (the exponent is ignored with a bf16 cache)."""
+    s = synth.LLAMA8B
+    b16 = P.workspace_bytes(P.make_config(s, 2, 4096, 16))
+    b8 = P.workspace_bytes(P.make_config(s, 2, 4096, 16, kv_format="fp8_e4m3", kv_scale_exp=-4))
+    kv_elems = 2 * s.n_layers * 2 * s.n_kv_heads * 4096 * s.head_dim   # K and V
+    assert b16 - b8 == pytest.approx(kv_elems, abs=1024)
+    for fmt, exp in ((2, 0), (1, 101), (1, -101)):
+        cfg = P.make_config(synth.TINY, 1, 64, 4)
+        cfg.kv_format, cfg.kv_scale_exp = fmt, exp
+        with pytest.raises(P.SbdError, match="kv_"):
+            P.workspace_bytes(cfg)
+    cfg = P.make_config(synth.TINY, 1, 64, 4)
+    cfg.kv_scale_exp = 500
+    assert P.workspace_bytes(cfg) > 0
+
+
 def test_fp8_workspace_holds_both_packings():
     """FP8 weights: the e4m3 packing (1 byte per element) and the widened bf16 copy."""
     s = synth.LLAMA8B

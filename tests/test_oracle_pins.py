@@ -142,6 +142,76 @@ def test_kv_bf16_model_stores_bf16_values():
         assert np.array_equal(O.round_to_bf16(c.V[li]), c.V[li])
 
 
+def _e4m3_grid():
+    """The finite e4m3 values and their codes (decode_e4m3 is pinned against torch)."""
+    codes = np.arange(256)
+    vals = O.decode_e4m3(codes)
+    ok = ~np.isnan(vals)
+    return vals[ok], codes[ok]
+
+
+def test_round_to_e4m3_is_nearest_code_ties_to_even():
+    """Brute force over the 254 finite codes: the nearest value; on a tie (every midpoint of
+    neighbouring values is tried) the code with mantissa bit 0 clear; beyond +-448 the
+    largest value (saturation); NaN stays NaN."""
+    vals, codes = _e4m3_grid()
+    rng = np.random.default_rng(11)
+    x = rng.choice([-1.0, 1.0], 6000) * np.exp2(rng.uniform(-12, 9.5, 6000))
+    u = np.unique(vals)
+    x = np.concatenate([x, (u[1:] + u[:-1]) / 2, [448.0, 449.0, 464.0, 500.0, 1e6, -1e6, 0.0]])
+    dist = np.abs(x[:, None] - vals[None, :])
+    want = np.empty_like(x)
+    for i, row in enumerate(dist):
+        idx = np.flatnonzero(row == row.min())
+        if len(idx) > 1:
+            idx = [j for j in idx if codes[j] % 2 == 0]
+        want[i] = vals[idx[0]]
+    got = O.round_to_e4m3(x)
+    assert np.array_equal(got, want)
+    assert O.round_to_e4m3(np.array([np.inf, -np.inf]))[:2].tolist() == [448.0, -448.0]
+    assert np.isnan(O.round_to_e4m3(np.array([np.nan]))[0])
+    # landmarks: 1 + 2^-4 ties to 1 (even), 1 + 3 2^-4 to 1.25; 3 2^-10 ties to 2^-8 (code 2)
+    assert O.round_to_e4m3(np.array([1 + 2**-4, 1 + 3 * 2**-4, 3 * 2**-10, 2**-10])).tolist() == \
+        [1.0, 1.25, 2**-8, 0.0]
+
+
+def test_round_to_e4m3_matches_torch_float8():
+    """Inside the finite range the rounding equals torch's float32 -> float8_e4m3fn cast."""
+    rng = np.random.default_rng(12)
+    a = (rng.normal(size=20000) * np.exp2(rng.uniform(-10, 6, 20000))).astype(np.float32)
+    a = a[np.abs(a) < 440]
+    want = torch.from_numpy(a).to(torch.float8_e4m3fn).float().numpy()
+    assert np.array_equal(O.round_to_e4m3(a), want)
+
+
+def test_round_to_e4m3_scale_is_a_power_of_two():
+    rng = np.random.default_rng(13)
+    a = rng.normal(size=4000) * 3.0
+    for e in (-7, -3, 2):
+        assert np.array_equal(O.round_to_e4m3(a, e), O.round_to_e4m3(a * 2.0 ** -e) * 2.0 ** e)
+
+
+def test_kv_fp8_model_rounds_keys_after_rope():
+    """Layer 0's keys and values depend on the embeddings alone, so with an e4m3 cache they
+    are the e4m3 rounding of the exact model's, keys after RoPE; later layers see the
+    rounded attention and differ.  Every cached value lies on the scaled e4m3 grid."""
+    shape, m = tiny_model()
+    toks = synth.make_tokens(4, 11, shape)
+    c, _ = m.prefill(toks)
+    for e in (0, -2):
+        m8 = O.Model(shape, m.w, dtype=np.float64, kv_fp8_exp=e)
+        c8, _ = m8.prefill(toks)
+        assert np.array_equal(c8.K[0], O.round_to_e4m3(c.K[0], e))
+        assert np.array_equal(c8.V[0], O.round_to_e4m3(c.V[0], e))
+        assert not np.array_equal(c8.K[1], O.round_to_e4m3(c.K[1], e))
+        vals, _ = _e4m3_grid()
+        for a in c8.K + c8.V:
+            assert np.isin(a * 2.0 ** -e, vals).all()
+    # to_e4m3 of a cache is the same rounding
+    c8 = c.to_e4m3(-2)
+    assert np.array_equal(c8.V[1], O.round_to_e4m3(c.V[1], -2))
+
+
 # ------------------------------------------------------------------ SBD network invariants
 
 @pytest.mark.parametrize("qk_norm", [False, True])
