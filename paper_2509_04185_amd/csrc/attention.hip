@@ -25,9 +25,11 @@
 namespace sbd {
 
 // The split kernel of the per-kernel path streams long key ranges, so it is shaped for
-// bytes in flight: 8 waves; the 64 key positions of a ring stage (two 32-key blocks of K
-// and V, copied straight into LDS) are split between two waves holding the same 16 query
-// rows, so each SIMD has two waves to overlap MFMA, softmax and LDS reads with the stream;
+// bytes in flight: 8 waves; the key positions of a ring stage (two 32-key blocks of K and V
+// from a bf16 cache, four from an fp8 cache: the same bytes; copied straight into LDS) are
+// split between two waves holding the same 16 query rows, so each SIMD has two waves to
+// overlap MFMA, softmax and LDS reads with the stream (an fp8 wave takes two blocks per
+// stage under one softmax update: the chain of a stage, not its bytes, sets its time);
 // a ring of NBUF stages (128 KB) keeps NBUF - 1 stages in flight.  At the end the two key
 // halves of each row set are combined through LDS (log-sum-exp weights) into the split's
 // partial.  LDS reads are ds_read16 (ds_read8 of an fp8 cache), ordered by hand (see
@@ -38,7 +40,9 @@ __global__ __launch_bounds__(512) void attn_split_kernel(AttnArgs a) {
   constexpr int NDT = DH / 16;  // 16-wide dimension tiles
   constexpr int NKS = DH / 32;  // 32-wide reduction steps for the scores
   constexpr int BLK = KB::BYTES;              // bytes of K (or of V) per 32-key block
-  constexpr int STAGE = 2 * 2 * BLK;          // two blocks, K and V
+  constexpr int BPW = KV8 ? 2 : 1;            // blocks per wave and stage
+  constexpr int BPS = 2 * BPW;                // blocks per stage (two key halves)
+  constexpr int STAGE = BPS * 2 * BLK;        // K and V of the stage's blocks
   constexpr int NBUF = (128 * 1024) / STAGE > 8 ? 8 : (128 * 1024) / STAGE;
   constexpr int LPB = BLK / 1024;             // 1 KB wave-loads per part per block
   constexpr int PER_WAVE = STAGE / 1024 / 8;  // wave-loads of one wave per stage
@@ -82,7 +86,7 @@ __global__ __launch_bounds__(512) void attn_split_kernel(AttnArgs a) {
   __syncthreads();
   for (int i = 0; i < 8; ++i) kend_wg = max(kend_wg, s_kend[i]);
   const int blk1_wg = min(blk_lim, (kend_wg + 31) / 32);
-  const int n_st = blk1_wg > blk0 ? (blk1_wg - blk0 + 1) / 2 : 0;
+  const int n_st = blk1_wg > blk0 ? (blk1_wg - blk0 + BPS - 1) / BPS : 0;
 
   const int64_t hb = attn_head_base(a.layer, sp.slot, g, a.n_slots, a.n_kv, a.cap, DH);
   const char* kbase = static_cast<const char*>(a.kcache) + hb * KB::ES;
@@ -96,7 +100,7 @@ __global__ __launch_bounds__(512) void attn_split_kernel(AttnArgs a) {
     for (int u = 0; u < PER_WAVE; ++u) {
       const int idx = w + 8 * u;
       const int bi = idx / (2 * LPB), part = (idx / LPB) % 2, sub = idx % LPB;
-      int kb = blk0 + 2 * st + bi;
+      int kb = blk0 + BPS * st + bi;
       if (kb >= blk1_wg) kb = blk1_wg - 1;  // past the end: a valid block, never used
       __builtin_amdgcn_global_load_lds((const void*)KB::src(kbase, vbase, kb, part, sub * 64 + lane),
                                        (__attribute__((address_space(3))) void*)(buf + (bi * 2 + part) * BLK + sub * 1024),
@@ -111,10 +115,9 @@ __global__ __launch_bounds__(512) void attn_split_kernel(AttnArgs a) {
 
   // this wave's block of stage st: scores, online softmax, O^T += V^T P^T
   auto compute = [&](int st) {
-    const int kb = blk0 + 2 * st + kh;
-    if (kb >= blk1) return;  // wave-uniform: nothing of this block is visible to its rows
-    const char* kblk = smem + (st % NBUF) * STAGE + (kh * 2) * BLK;
-    const char* vblk = kblk + BLK;
+    const int kb0 = blk0 + BPS * st + kh * BPW;  // this wave's first block
+    if (kb0 >= blk1) return;  // wave-uniform: nothing of its blocks is visible to its rows
+    const char* blk = smem + (st % NBUF) * STAGE + (kh * BPW * 2) * BLK;  // block j: K at 2 j BLK, V after
     // fragments: KV8 reads 8 bytes and widens them once the reads are complete
     typedef typename std::conditional<KV8, i32x2, i32x4>::type Frag;
     auto rd = [](const char* p) -> Frag {
@@ -125,81 +128,97 @@ __global__ __launch_bounds__(512) void attn_split_kernel(AttnArgs a) {
       if constexpr (KV8) return e4m3x8_to_bf16(v, kv_sc);
       else return v;
     };
-    Frag kr[2][NKS];
+    Frag kr[BPW][2][NKS];
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int jb = 0; jb < BPW; ++jb)
 #pragma unroll
-      for (int s2 = 0; s2 < NKS; ++s2) kr[t][s2] = rd(kblk + KB::koff(16 * t + r, s2, grp));
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int s2 = 0; s2 < NKS; ++s2) kr[jb][t][s2] = rd(blk + jb * 2 * BLK + KB::koff(16 * t + r, s2, grp));
     lds_wait();
-    i32x4 kf[2][NKS];
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int jb = 0; jb < BPW; ++jb)
 #pragma unroll
-      for (int s2 = 0; s2 < NKS; ++s2) {
-        lds_pin(kr[t][s2]);
-        kf[t][s2] = widen(kr[t][s2]);
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int s2 = 0; s2 < NKS; ++s2) lds_pin(kr[jb][t][s2]);
+    f32x4 sc[BPW][2];
+#pragma unroll
+    for (int jb = 0; jb < BPW; ++jb)
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        sc[jb][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s2 = 0; s2 < NKS; ++s2) {
+          const i32x4 kf = widen(kr[jb][t][s2]);
+          sc[jb][t] = mfma16x16x32(kf, qf[s2], sc[jb][t]);
+          sc[jb][t] = mfma16x16x32(kf, ql[s2], sc[jb][t]);
+        }
       }
-    f32x4 sc[2];
+    Frag vr[BPW][NDT];  // requested now: the softmax below hides their latency
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      sc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int jb = 0; jb < BPW; ++jb)
 #pragma unroll
-      for (int s2 = 0; s2 < NKS; ++s2) {
-        sc[t] = mfma16x16x32(kf[t][s2], qf[s2], sc[t]);
-        sc[t] = mfma16x16x32(kf[t][s2], ql[s2], sc[t]);
-      }
-    }
-    Frag vr[NDT];  // requested now: the softmax below hides their latency
-#pragma unroll
-    for (int dt = 0; dt < NDT; ++dt) vr[dt] = rd(vblk + KB::voff(16 * dt + r, grp));
-    // sc[t][i]: score of key 32 kb + 16 t + 4 grp + i for query row r
+      for (int dt = 0; dt < NDT; ++dt) vr[jb][dt] = rd(blk + (jb * 2 + 1) * BLK + KB::voff(16 * dt + r, grp));
+    // sc[jb][t][i]: score of key 32 (kb0 + jb) + 16 t + 4 grp + i for query row r; a block
+    // at or past blk1 (beyond this wave's last key, or in the next split) counts for nothing
     float mloc = -INFINITY;
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int jb = 0; jb < BPW; ++jb)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if (32 * kb + 16 * t + 4 * grp + i >= kend) sc[t][i] = -INFINITY;
-        mloc = fmaxf(mloc, sc[t][i]);
-      }
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (kb0 + jb >= blk1 || 32 * (kb0 + jb) + 16 * t + 4 * grp + i >= kend) sc[jb][t][i] = -INFINITY;
+          mloc = fmaxf(mloc, sc[jb][t][i]);
+        }
     mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
     mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
     const float m_new = fmaxf(m_run, mloc);
     // exponents are <= 0 here: the hardware exp2 suffices (results below 2^-126 flush to 0)
     const float scale = (m_run == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
-    float p[8];
+    float p[BPW][8];
     float lsum = 0.f;
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int jb = 0; jb < BPW; ++jb)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float sv = sc[t][i];
-        const float v = (sv == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(sv - m_new);
-        p[4 * t + i] = v;
-        lsum += v;
-      }
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float sv = sc[jb][t][i];
+          const float v = (sv == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(sv - m_new);
+          p[jb][4 * t + i] = v;
+          lsum += v;
+        }
     lsum += __shfl_xor(lsum, 16);
     lsum += __shfl_xor(lsum, 32);
     l_run = l_run * scale + lsum;
     m_run = m_new;
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) o[dt] *= scale;
-    // P as hi/lo bf16 (B operand): element e holds key 16*(e/4) + 4*grp + e%4.
-    i32x4 pf, pl;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float p0 = p[2 * e], p1 = p[2 * e + 1];
-      const uint32_t hw = pack_bf2(p0, p1);
-      pf[e] = (int)hw;
-      pl[e] = (int)pack_bf2(p0 - __uint_as_float(hw << 16), p1 - __uint_as_float(hw & 0xffff0000u));
-    }
     lds_wait();
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt) lds_pin(vr[dt]);
+    for (int jb = 0; jb < BPW; ++jb)
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt) {
-      const i32x4 vf = widen(vr[dt]);
-      o[dt] = mfma16x16x32(vf, pf, o[dt]);
-      o[dt] = mfma16x16x32(vf, pl, o[dt]);
+      for (int dt = 0; dt < NDT; ++dt) lds_pin(vr[jb][dt]);
+#pragma unroll
+    for (int jb = 0; jb < BPW; ++jb) {
+      if (kb0 + jb >= blk1) continue;  // wave-uniform
+      // P as hi/lo bf16 (B operand): element e holds key 16*(e/4) + 4*grp + e%4.
+      i32x4 pf, pl;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float p0 = p[jb][2 * e], p1 = p[jb][2 * e + 1];
+        const uint32_t hw = pack_bf2(p0, p1);
+        pf[e] = (int)hw;
+        pl[e] = (int)pack_bf2(p0 - __uint_as_float(hw << 16), p1 - __uint_as_float(hw & 0xffff0000u));
+      }
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) {
+        const i32x4 vf = widen(vr[jb][dt]);
+        o[dt] = mfma16x16x32(vf, pf, o[dt]);
+        o[dt] = mfma16x16x32(vf, pl, o[dt]);
+      }
     }
   };
 

@@ -78,12 +78,15 @@ def eb_compare(n_acc, pos, tok, ref_acc, ref_tok, ref_H, is_mask, gamma, label="
     return worst
 
 
-def kv8_close(got, ref, scale_exp, max_frac=1e-3, label=""):
+def kv8_close(got, ref, scale_exp, max_frac=3e-3, label=""):
     """Keys/values of an e4m3 cache against the oracle's (both on the grid e4m3 * 2^e).
 
     The two sides round floats that agree to float precision, not bit for bit, so a value
     near the midpoint of two codes may land on either: at most max_frac of the elements may
-    differ, each by one step of the grid (the larger spacing at a binade edge)."""
+    differ, each by one step of the grid (the larger spacing at a binade edge).  With the
+    inputs agreeing to a relative 5e-5 (hi/lo activations), a flip has a chance of about
+    2 * 5e-5 / 2^-3 = 8e-4 per element; layers whose inputs are bit-identical on both sides
+    (layer 0) show none."""
     got = np.asarray(got, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
     s = 2.0 ** scale_exp
