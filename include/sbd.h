@@ -76,10 +76,10 @@ typedef struct {
  *   SBD_WEIGHTS_FP8_E4M3  OCP e4m3 bytes (1 sign, 4 exponent bits of bias 7, 3 mantissa
  *                         bits; no infinities, 0x7f / 0xff NaN) with a power-of-two scale per
  *                         matrix: the weight is e4m3(q) * 2^e (the FP8 weights of the
- *                         paper's timing model, Sec. 4.1).  Forwards of at most 16 rows stream
- *                         the bytes and widen them to bf16 in registers (exactly); longer
- *                         forwards (prefill chunks, batched decode) and the fused decode
- *                         path stream a bf16 copy of the same values, made in sbd_create.
+ *                         paper's timing model, Sec. 4.1).  Every forward streams the bytes
+ *                         and widens them to bf16 in registers (exactly), except the fused
+ *                         decode path, which streams a bf16 copy of the same values made in
+ *                         sbd_create.
  */
 enum { SBD_WEIGHTS_BF16 = 0, SBD_WEIGHTS_FP8_E4M3 = 1 };
 

@@ -40,13 +40,14 @@
 // scale is constant along a row.
 
 #include <algorithm>
+#include <type_traits>
 #include <utility>
 
 #include "eb_stats.h"
 
 namespace sbd {
 
-template <int MT, int NT>
+template <int MT, int NT, bool W8>
 struct MidCfg {
   // waves across the column block: 2 x 2 waves (each reads half the activation and half the
   // weight fragments of a stage from LDS: 16 KB per 16-tile stage, against 20 KB in a 4 x 1 split)
@@ -54,10 +55,15 @@ struct MidCfg {
   static constexpr int WM = 4 / WC;            // waves across the row block
   static constexpr int CW = NT / WC;           // tiles per wave
   static constexpr int MTW = MT / WM;          // row tiles per wave
-  static constexpr int STAGE = (NT + 2 * MT) * 1024;  // one K step: NT weight + 2 MT A fragments
+  // weight bytes of a K step: 1 KB per tile in bf16, 512 B in e4m3 (one 1 KB wave-load then
+  // carries two tiles' fragments)
+  static constexpr int WB = NT * (W8 ? 512 : 1024);
+  static constexpr int NWL = WB / 1024;               // weight wave-loads per stage
+  static constexpr int STAGE = WB + 2 * MT * 1024;    // one K step: weights + 2 MT A fragments
   static constexpr int NS = (144 * 1024) / STAGE > 8 ? 8 : (144 * 1024) / STAGE;  // ring stages
-  static constexpr int FPW = (NT + 2 * MT) / 4;       // fragments each wave loads per stage
-  static_assert(MTW >= 1 && (NT + 2 * MT) % 4 == 0, "unsupported tile shape");
+  static constexpr int FPW = (NWL + 2 * MT) / 4;      // wave-loads of each wave per stage
+  static constexpr int NWU = NWL / 4;                 // of a wave's FPW loads, the first NWU are weights
+  static_assert(MTW >= 1 && (NWL + 2 * MT) % 4 == 0 && NWL % 4 == 0, "unsupported tile shape");
   static_assert((NS - 1) * FPW <= 63, "vmcnt range");
 };
 
@@ -94,13 +100,17 @@ __device__ __forceinline__ void stage_barrier() {
 }
 
 // STREAM: every weight byte is read by one workgroup (one row block): non-temporal loads.
-template <int MT, int NT, int EPI, bool STREAM>
+// W8: the weights are e4m3 bytes (a.Wp8, per-row scales a.wscale) in the same packing, one
+// byte per element; a fragment is widened to the bf16 MFMA operand (times its row's scale,
+// exact) after its LDS read, so the products are those of the widened bf16 matrix.
+template <int MT, int NT, int EPI, bool STREAM, bool W8>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
-  using Cfg = MidCfg<MT, NT>;
+  using Cfg = MidCfg<MT, NT, W8>;
   constexpr int WC = Cfg::WC, CW = Cfg::CW, MTW = Cfg::MTW, NS = Cfg::NS, FPW = Cfg::FPW;
   constexpr int STAGE = Cfg::STAGE;
-  constexpr int WB = NT * 1024;  // weight bytes of a stage; A fragments follow
-  constexpr int NWU = NT / 4;    // of a wave's FPW loads, the first NWU are weights
+  constexpr int WB = Cfg::WB;    // weight bytes of a stage; A fragments follow
+  constexpr int NWU = Cfg::NWU;
+  typedef typename std::conditional<W8, i32x2, i32x4>::type WFr;  // a weight fragment in registers
   __shared__ __attribute__((aligned(16))) char smem[NS * STAGE];
   __shared__ float rinv_s[MT * 16];
   __shared__ float ssq_s[WC][MT * 16];
@@ -124,18 +134,24 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
   const int nst = s_e - s_b;
   const int t0 = cb * NT;
 
-  // Sources of this wave's loads: load u of a stage fills fragment f = w + 4u of it;
-  // f < NT is weight tile t0 + f, else A fragment f - NT = 2 * (row tile) + (0: hi, 1: lo).
+  // Sources of this wave's loads: load u of a stage fills 1 KB f = w + 4u of it; f < NWL is
+  // weight tile t0 + f (bf16) or the tiles t0 + 2f, t0 + 2f + 1 (e4m3: their fragments are
+  // adjacent in the packing), else A fragment f - NWL = 2 * (row tile) + (0: hi, 1: lo).
   const char* src[FPW];
   int64_t stride[FPW];
 #pragma unroll
   for (int u = 0; u < FPW; ++u) {
     const int f = w + 4 * u;
     if (u < NWU) {
-      src[u] = (const char*)(a.Wp + packed_frag(t0 + f, s_b, S_all) + lane * 8);
-      stride[u] = kPackStep * 2;
+      if constexpr (W8) {
+        src[u] = (const char*)(a.Wp8 + packed_frag(t0 + 2 * f, s_b, S_all) + lane * 16);
+        stride[u] = kPackStep;
+      } else {
+        src[u] = (const char*)(a.Wp + packed_frag(t0 + f, s_b, S_all) + lane * 8);
+        stride[u] = kPackStep * 2;
+      }
     } else {
-      const int ai = f - NT;
+      const int ai = f - Cfg::NWL;
       int row = row0 + (ai >> 1) * 16 + r;
       if (row >= a.M) row = a.M - 1;  // rows past the end: valid data, results discarded
       const bf16_t* base = (ai & 1) ? a.A_lo : a.A;
@@ -174,18 +190,26 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
   // barrier before the reads, lds_wait() after them, and the results pinned behind it.
   // The reads of stage c + 1 are issued before the MFMAs of stage c (two register sets), so
   // the LDS traffic of one step overlaps the matrix work of the previous one.
-  const uint32_t lds_w = (uint32_t)(uintptr_t)smem + (uint32_t)(wc * CW * 1024 + lane * 16);
+  constexpr int WFB = W8 ? 512 : 1024;  // bytes of one weight fragment in LDS
+  const uint32_t lds_w = (uint32_t)(uintptr_t)smem + (uint32_t)(wc * CW * WFB + lane * (WFB / 64));
   const uint32_t lds_a = (uint32_t)(uintptr_t)smem + (uint32_t)(WB + wm * MTW * 2048 + lane * 16);
-  auto read_frags = [&](int st, i32x4 (&wv)[CW], i32x4 (&av)[MTW][2]) {
+  // the lane's weight scales (row r of each of its tiles); 1 for bf16
+  float wsc[CW];
+#pragma unroll
+  for (int cw = 0; cw < CW; ++cw) wsc[cw] = W8 ? a.wscale[(int64_t)(t0 + wc * CW + cw) * 16 + r] : 1.0f;
+  auto read_frags = [&](int st, WFr (&wv)[CW], i32x4 (&av)[MTW][2]) {
     const uint32_t sb = (uint32_t)((st % NS) * STAGE);
     const uint32_t aw = lds_w + sb, aa = lds_a + sb;
-    static_for<CW>([&](auto I) { wv[decltype(I)::value] = ds_read16<decltype(I)::value * 1024>(aw); });
+    static_for<CW>([&](auto I) {
+      if constexpr (W8) wv[decltype(I)::value] = ds_read8<decltype(I)::value * 512>(aw);
+      else wv[decltype(I)::value] = ds_read16<decltype(I)::value * 1024>(aw);
+    });
     static_for<MTW * 2>([&](auto I) {
       constexpr int i = decltype(I)::value;
       av[i / 2][i % 2] = ds_read16<i * 1024>(aa);
     });
   };
-  auto pin_frags = [&](i32x4 (&wv)[CW], i32x4 (&av)[MTW][2]) {
+  auto pin_frags = [&](WFr (&wv)[CW], i32x4 (&av)[MTW][2]) {
 #pragma unroll
     for (int cw = 0; cw < CW; ++cw) lds_pin(wv[cw]);
 #pragma unroll
@@ -193,13 +217,24 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
 #pragma unroll
       for (int h = 0; h < 2; ++h) lds_pin(av[mw][h]);
   };
-  auto mfma_frags = [&](const i32x4 (&wv)[CW], const i32x4 (&av)[MTW][2]) {
+  auto mfma_frags = [&](const WFr (&wv)[CW], const i32x4 (&av)[MTW][2]) {
+    if constexpr (W8) {  // each fragment widened once; every accumulator still takes hi, then lo
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+      for (int cw = 0; cw < CW; ++cw) {
+        const i32x4 wf = e4m3x8_to_bf16(wv[cw], wsc[cw]);
 #pragma unroll
-      for (int mw = 0; mw < MTW; ++mw)
+        for (int h = 0; h < 2; ++h)
 #pragma unroll
-        for (int cw = 0; cw < CW; ++cw) acc[mw][cw] = mfma16x16x32(av[mw][h], wv[cw], acc[mw][cw]);
+          for (int mw = 0; mw < MTW; ++mw) acc[mw][cw] = mfma16x16x32(av[mw][h], wf, acc[mw][cw]);
+      }
+    } else {
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int mw = 0; mw < MTW; ++mw)
+#pragma unroll
+          for (int cw = 0; cw < CW; ++cw) acc[mw][cw] = mfma16x16x32(av[mw][h], wv[cw], acc[mw][cw]);
+    }
   };
 
   // Consumers of a norm: the producer's partial sums of squares of this block's rows,
@@ -224,14 +259,15 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
   // NS stages in flight: stage c's slot is refilled once every wave holds its fragments.
 #pragma unroll 1
   for (int st = 0; st < NS && st < nst; ++st) issue(st);
-  i32x4 wv0[CW], av0[MTW][2], wv1[CW], av1[MTW][2];
+  WFr wv0[CW], wv1[CW];
+  i32x4 av0[MTW][2], av1[MTW][2];
   vm_wait_stages<FPW, NS - 1>(min(NS - 1, nst - 1));  // stage 0 has landed (this wave's part)
   stage_barrier();                                    // ... and every wave's
   read_frags(0, wv0, av0);
   lds_wait();
   pin_frags(wv0, av0);
   // step c: the fragments of stage c are in registers; stage c + 1 is read meanwhile
-  auto step = [&](int c, i32x4 (&wc_)[CW], i32x4 (&ac_)[MTW][2], i32x4 (&wn)[CW], i32x4 (&an)[MTW][2]) {
+  auto step = [&](int c, WFr (&wc_)[CW], i32x4 (&ac_)[MTW][2], WFr (&wn)[CW], i32x4 (&an)[MTW][2]) {
     if (c + 1 < nst) {
       vm_wait_stages<FPW, NS - 2>(min(NS - 2, nst - 2 - c));  // stage c + 1 has landed (this wave's part)
       stage_barrier();  // ... and every wave's; every wave holds stage c's fragments: its slot is free
@@ -478,10 +514,15 @@ template <int MT, int NT, int EPI>
 static void launch_cfg(const GemmArgs& a, const Exec& ex) {
   const int n_cb = a.n_tiles / NT;
   const unsigned grid = (unsigned)(((n_cb + 7) / 8) * 8 * a.splits * a.m_blocks);
-  if (a.m_blocks == 1)
-    SBD_KLAUNCH((gemm_kernel<MT, NT, EPI, true>), dim3(grid), dim3(256), ex, a);
+  const bool w8 = a.Wp8 != nullptr;
+  if (a.m_blocks == 1 && w8)
+    SBD_KLAUNCH((gemm_kernel<MT, NT, EPI, true, true>), dim3(grid), dim3(256), ex, a);
+  else if (a.m_blocks == 1)
+    SBD_KLAUNCH((gemm_kernel<MT, NT, EPI, true, false>), dim3(grid), dim3(256), ex, a);
+  else if (w8)
+    SBD_KLAUNCH((gemm_kernel<MT, NT, EPI, false, true>), dim3(grid), dim3(256), ex, a);
   else
-    SBD_KLAUNCH((gemm_kernel<MT, NT, EPI, false>), dim3(grid), dim3(256), ex, a);
+    SBD_KLAUNCH((gemm_kernel<MT, NT, EPI, false, false>), dim3(grid), dim3(256), ex, a);
 }
 
 template <int EPI>
@@ -499,6 +540,7 @@ static void launch_epi(const GemmArgs& a, int mt, int nt, const Exec& ex) {
 
 hipError_t launch_gemm(GemmEpi epi, const GemmArgs& a0, const Exec& ex) {
   if (a0.M < 1 || a0.K < 32 || a0.K % 32 || a0.n_tiles < 8 || a0.n_tiles % 8) return hipErrorInvalidValue;
+  if (a0.Wp8 != nullptr && a0.wscale == nullptr) return hipErrorInvalidValue;
   const GemmPlan p = gemm_plan(a0.M, a0.n_tiles, a0.K, (a0.part && !a0.no_split) ? a0.part_cap : 0);
   if (p.nt == 0) return hipErrorInvalidValue;
   if (p.splits > 1 && (a0.counters == nullptr || (int64_t)p.n_cb * p.m_blocks * kCtrStride > kLayerCtr0))

@@ -271,7 +271,10 @@ GemvArgs gemv_base(const bf16_t* A, const bf16_t* A_lo, int64_t lda, int M, int 
 }
 
 // Key splits of the attention: enough workgroups for one round of one per CU (a workgroup
-// takes 128 KB of LDS), as long as every split keeps a block.
+// takes 128 KB of LDS), as long as every split keeps a block.  More rounds cost a
+// workgroup's start (queries, first stage of the ring, final combine and partial store)
+// again on every CU: with ragged lengths (batch 32, 512 to 4096 positions) four splits
+// instead of one took the attention from 92 to 105 us.
 int pick_splits(int64_t work_groups_per_split, int nblocks, int n_cu) {
   const int64_t target = std::max(1, n_cu);
   int s = (int)std::max<int64_t>(1, (target + work_groups_per_split - 1) / work_groups_per_split);
@@ -318,10 +321,14 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
   const int n_rb = (G * k + 63) / 64;
   const int nblocks = (max_end + 31) / 32;
   const bool small = M <= 16;  // decode-sized forward
-  // fp8 weights: decode-sized GEMMs stream the bytes (the others the widened bf16 copy)
+  // fp8 weights: the GEMVs, layer kernels and GEMMs stream the bytes (the fused path the
+  // widened bf16 copy)
   const bool f8 = m.weight_format == SBD_WEIGHTS_FP8_E4M3;
   auto w8 = [&](int64_t off, int64_t soff, GemvArgs& v) {
     if (f8) { v.Wp8 = c->at<fp8_t>(L.wpack8) + off; v.wscale = c->at<float>(L.wscale) + soff; }
+  };
+  auto g8 = [&](int64_t off, int64_t soff, GemmArgs& g) {  // the GEMM for more rows streams them too
+    if (f8) { g.Wp8 = c->at<fp8_t>(L.wpack8) + off; g.wscale = c->at<float>(L.wscale) + soff; }
   };
   // forwards of more than 16 rows keep the GEMMs' activation operands in fragment order
   const int mt = small ? 0 : (M + 15) / 16;
@@ -457,6 +464,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
       SBD_LAUNCH(c, SBD_KERNEL_QKV, launch_gemv(EPI_QKV, v, GemvShape{}, ex));
     } else {
       GemmArgs g = gemm_base(xn, xn_lo, d, M, d, wp, (int)(L.n_qkv / 16), vpart, vpart_cap, counters, c->xcd_ok);
+      g8((int64_t)l * L.wp_layer, (int64_t)l * L.ws_layer, g);
       g.a_mtiles = mt;
       g.out_f32 = qkv; g.ldo = L.n_qkv;
       g.sumsq_in = sumsq; g.n_part = n_part_cur; g.inv_d = 1.0f / d; g.eps = m.rms_eps;
@@ -491,6 +499,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
       SBD_LAUNCH(c, SBD_KERNEL_O_PROJ, launch_gemv(EPI_RESID, v, GemvShape{}, ex));
     } else {
       GemmArgs go = gemm_base(attn, attn_lo, qd, M, qd, wp + L.wp_o, d / 16, vpart, vpart_cap, counters, c->xcd_ok);
+      g8((int64_t)l * L.wp_layer + L.wp_o, (int64_t)l * L.ws_layer + L.ws_o, go);
       go.a_mtiles = mt; go.o_mtiles = mt;
       go.x = x; go.ldx = d; go.xn = xn; go.xn_lo = xn_lo; go.g_next = w.mlp_norm; go.sumsq_out = sumsq;
       go.n_part_out = gemm_plan(M, d / 16, qd, c->xcd_ok ? vpart_cap : 0).n_cb;
@@ -513,6 +522,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
       SBD_LAUNCH(c, SBD_KERNEL_DOWN, launch_gemv(EPI_RESID, vd, GemvShape{}, ex));
     } else {
       GemmArgs gu = gemm_base(xn, xn_lo, d, M, d, wp + L.wp_gu, m.ffn_dim / 8, vpart, vpart_cap, counters, c->xcd_ok);
+      g8((int64_t)l * L.wp_layer + L.wp_gu, (int64_t)l * L.ws_layer + L.ws_gu, gu);
       gu.a_mtiles = mt; gu.o_mtiles = mt;
       gu.sumsq_in = sumsq; gu.n_part = n_part_cur; gu.inv_d = 1.0f / d; gu.eps = m.rms_eps;
       gu.act = act; gu.act_lo = act_lo; gu.ld_act = m.ffn_dim;
@@ -520,6 +530,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
 
       GemmArgs gd = gemm_base(act, act_lo, m.ffn_dim, M, m.ffn_dim, wp + L.wp_down, d / 16, vpart, vpart_cap,
                               counters, c->xcd_ok);
+      g8((int64_t)l * L.wp_layer + L.wp_down, (int64_t)l * L.ws_layer + L.ws_down, gd);
       gd.a_mtiles = mt; gd.o_mtiles = mt;
       gd.x = x; gd.ldx = d; gd.xn = xn; gd.xn_lo = xn_lo; gd.g_next = g_after;
       gd.sumsq_out = sumsq;
@@ -546,6 +557,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
       // inputs in fragment order (also for one row of a prefill chunk: rows from a_row0)
       GemmArgs gl = gemm_base(xn, xn_lo, d, Ml, d, c->at<bf16_t>(L.wpack) + L.wp_lm, m.vocab / 16, vpart,
                               vpart_cap, counters, c->xcd_ok);
+      g8(L.wp_lm, L.ws_lm, gl);
       gl.a_mtiles = mt; gl.a_row0 = r0;
       gl.out_f32 = logits; gl.ldo = m.vocab;
       gl.sumsq_in = sumsq + (int64_t)r0 * n_part_cur; gl.n_part = n_part_cur;

@@ -121,6 +121,8 @@ struct GemmArgs {
   int a_row0;          // first row of A used (fragment order only)
   int o_mtiles;        // xn (EPI_RESID) and act (EPI_SWIGLU) written in fragment order (0: row-major)
   const bf16_t* Wp;    // packed weights
+  const fp8_t* Wp8;    // or (non-null) e4m3 weights in the same packing, with per-row scales
+  const float* wscale; //   wscale[16 t + r] of packed tile t, row r
   int n_tiles;         // 16-row tiles of the packed matrix (a multiple of 8)
   // EPI_SCALED_STORE: out[m][n] = rinv[m] * y (rinv = 1 when sumsq_in == nullptr)
   float* out_f32;

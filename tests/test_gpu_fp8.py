@@ -1,9 +1,9 @@
 """FP8 (e4m3) weights, the paper's timing assumption (Sec. 4.1: FP8 weights), on the GPU.
 
 Every projection matrix and the LM head are OCP e4m3 bytes with a power-of-two scale per
-matrix (synth.make_weights_fp8).  Decode-sized forwards stream the bytes and widen them to
-bf16 in registers; forwards of more than 16 rows and the fused path stream a bf16 copy of
-the same values.  The widening is exact, so:
+matrix (synth.make_weights_fp8).  The per-XCD layer kernels, the one-kernel-per-step GEMVs
+and the GEMM for more than 16 rows stream the bytes and widen them to bf16 in registers; the
+fused path streams a bf16 copy of the same values.  The widening is exact, so:
 * an FP8 context gives the same logits, bit for bit, as a bf16 context holding the widened
   values on the one-kernel-per-step and fused paths and the GEMM for more rows (the MFMAs
   see the same operands in the same order); on the per-XCD layer kernels to float rounding
@@ -12,7 +12,7 @@ the same values.  The widening is exact, so:
   the bf16 path apply unchanged (the weights are the model; their rounding is not error).
 Cases: the tiny decoder on every path, two layers of the Llama-3.1-8B shape on the per-XCD
 layer kernels, the benched configuration (32 layers, k = 16, 2048 cached positions) and the
-batch-4 32768-position configuration (64 rows: the bf16 copy).
+batch-4 32768-position configuration (64 rows: the GEMM for more rows on the e4m3 bytes).
 """
 import dataclasses
 
@@ -76,7 +76,7 @@ def test_fp8_tiny_every_path():
         caches.append(cache)
         parity.close(l8.cpu().numpy(), ref_last, regress=REGRESS, label=f"prefill {b}: ")
         assert torch.equal(l8, lb), "FP8 prefill differs from the widened bf16 model"
-    for B, k in ((1, 4), (2, 8), (4, 8)):           # 32 rows: the GEMM path on the bf16 copy
+    for B, k in ((1, 4), (2, 8), (4, 8)):           # 32 rows: the GEMM path
         toks, is_mask = synth.block_rows(9010 + B, shape, B, k, n_causal=1)
         paths = paths_of(lib8, B, k)
         g8 = forward_all(lib8, paths, list(range(B)), toks, is_mask, [1] * B)
@@ -136,7 +136,7 @@ def test_fp8_8b_layer_kernels():
 @pytest.mark.parametrize("name,sample", [("llama8b_b1_l2048_k16", [0]), ("llama8b_b4_l32768_k16", [0, 3])])
 def test_fp8_fullsize(name, sample):
     """The benched configuration (per-XCD layer kernels on e4m3) and the batch-4 long-context
-    one (64 rows: the bf16 copy), on synthetic caches, against the oracle."""
+    one (64 rows: the GEMM for more rows), on synthetic caches, against the oracle."""
     from paper_2509_04185_amd import Sbd
     wl = synth.WORKLOADS[name]
     s = wl.shape
