@@ -25,40 +25,43 @@
 namespace sbd {
 
 // The split kernel of the per-kernel path streams long key ranges, so it is shaped for
-// bytes in flight: 8 waves; the key positions of a ring stage (two 32-key blocks of K and V
-// from a bf16 cache, four from an fp8 cache: the same bytes; copied straight into LDS) are
-// split between two waves holding the same 16 query rows, so each SIMD has two waves to
-// overlap MFMA, softmax and LDS reads with the stream (an fp8 wave takes two blocks per
-// stage under one softmax update: the chain of a stage, not its bytes, sets its time);
-// a ring of NBUF stages (128 KB) keeps NBUF - 1 stages in flight.  At the end the two key
-// halves of each row set are combined through LDS (log-sum-exp weights) into the split's
-// partial.  LDS reads are ds_read16 (ds_read8 of an fp8 cache), ordered by hand (see
-// sbd_device.h).
-template <int DH, bool KV8>
+// bytes in flight: 8 waves, NRS row sets of 16 query rows times KP = 8 / NRS key parts (4 x 2,
+// or 2 x 4 when a row block has at most 32 rows, so that no wave idles); the key positions
+// of a ring stage (KP blocks of 32 keys of K and V from a bf16 cache, 2 KP from an fp8 cache;
+// copied straight into LDS) are split between the KP waves holding the same 16 query rows,
+// so each SIMD has two waves to overlap MFMA, softmax and LDS reads with the stream (an fp8
+// wave takes two blocks per stage under one softmax update: the chain of a stage, not its
+// bytes, sets its time); a ring of NBUF stages (128 KB) keeps NBUF - 1 stages in flight.  At
+// the end the KP key parts of each row set are combined through LDS (log-sum-exp weights,
+// in part order) into the split's partial.  LDS reads are ds_read16 (ds_read8 of an fp8
+// cache), ordered by hand (see sbd_device.h).
+template <int DH, bool KV8, int NRS>
 __global__ __launch_bounds__(512) void attn_split_kernel(AttnArgs a) {
   using KB = KvBlk<DH, KV8>;    // a staged block's layout in LDS
   constexpr int NDT = DH / 16;  // 16-wide dimension tiles
   constexpr int NKS = DH / 32;  // 32-wide reduction steps for the scores
+  constexpr int KP = 8 / NRS;                 // key parts
   constexpr int BLK = KB::BYTES;              // bytes of K (or of V) per 32-key block
   constexpr int BPW = KV8 ? 2 : 1;            // blocks per wave and stage
-  constexpr int BPS = 2 * BPW;                // blocks per stage (two key halves)
+  constexpr int BPS = KP * BPW;               // blocks per stage
   constexpr int STAGE = BPS * 2 * BLK;        // K and V of the stage's blocks
   constexpr int NBUF = (128 * 1024) / STAGE > 8 ? 8 : (128 * 1024) / STAGE;
   constexpr int LPB = BLK / 1024;             // 1 KB wave-loads per part per block
   constexpr int PER_WAVE = STAGE / 1024 / 8;  // wave-loads of one wave per stage
-  static_assert(NBUF >= 3 && (NBUF - 2) * PER_WAVE <= 63, "ring shape");
+  static_assert(NBUF >= 2 && (NBUF - 2) * PER_WAVE <= 63, "ring shape");
+  static_assert(NRS * KP == 8 && (KP - 1) * NRS * 64 * (NDT * 16 + 16) <= NBUF * STAGE, "wave shape");
   __shared__ __attribute__((aligned(16))) char smem[NBUF * STAGE];
   __shared__ int s_kend[8];
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int rs = w & 3, kh = w >> 2;  // row set (16 rows), key half of each stage
+  const int rs = w % NRS, kh = w / NRS;  // row set (16 rows), key part of each stage
   const int r = lane & 15, grp = lane >> 4;
   const int split = blockIdx.x, g = blockIdx.y / a.n_rowblocks, rb = blockIdx.y % a.n_rowblocks, b = blockIdx.z;
   const SeqParam sp = a.seqs[b];
   const int L = sp.cache_len, nc = sp.n_causal, k = a.k;
   const int G = a.n_q / a.n_kv;
   const int R = G * k;
-  const int rho = rb * 64 + rs * 16 + r;
+  const int rho = rb * 16 * NRS + rs * 16 + r;
   const bool row_ok = rho < R;
   const int hh = row_ok ? rho / k : 0;
   const int j = row_ok ? rho % k : 0;
@@ -242,26 +245,49 @@ __global__ __launch_bounds__(512) void attn_split_kernel(AttnArgs a) {
     if (c + NBUF - 1 < n_st) issue(c + NBUF - 1);
     compute(c);
   }
-  __syncthreads();  // the ring is free: it holds the second key half's states next
+  __syncthreads();  // the ring is free: it holds the other key parts' states next
 
-  // combine the two key halves of each row set: waves 4..7 park (m, l, O), waves 0..3 add
+  // combine the key parts of each row set: parts 1 .. KP - 1 park (m, l, O), part 0 adds
   constexpr int SLOT = NDT * 16 + 16;  // bytes per lane (16-byte aligned pieces)
-  char* park = smem + (rs * 64 + lane) * SLOT;
-  if (kh == 1) {
+  auto park_of = [&](int part) { return smem + (((part - 1) * NRS + rs) * 64 + lane) * SLOT; };
+  if (kh > 0) {
+    char* park = park_of(kh);
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) *(f32x4*)(park + dt * 16) = o[dt];
     *(float*)(park + NDT * 16) = m_run;
     *(float*)(park + NDT * 16 + 4) = l_run;
   }
   __syncthreads();
-  if (kh == 1 || !row_ok) return;
-  const float m1 = *(const float*)(park + NDT * 16), l1 = *(const float*)(park + NDT * 16 + 4);
-  const float mm = fmaxf(m_run, m1);
-  const float s0 = (m_run == -INFINITY) ? 0.f : exp2f(m_run - mm);
-  const float s1 = (m1 == -INFINITY) ? 0.f : exp2f(m1 - mm);
+  if (kh > 0 || !row_ok) return;
+  float mm = m_run;
 #pragma unroll
-  for (int dt = 0; dt < NDT; ++dt) o[dt] = o[dt] * s0 + *(const f32x4*)(park + dt * 16) * s1;
-  const float ll = l_run * s0 + l1 * s1;
+  for (int part = 1; part < KP; ++part) mm = fmaxf(mm, *(const float*)(park_of(part) + NDT * 16));
+  const float s0 = (m_run == -INFINITY) ? 0.f : exp2f(m_run - mm);
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt) o[dt] *= s0;
+  float ll = l_run * s0;
+#pragma unroll
+  for (int part = 1; part < KP; ++part) {
+    const char* park = park_of(part);
+    const float mp = *(const float*)(park + NDT * 16), lp = *(const float*)(park + NDT * 16 + 4);
+    const float sp_ = (mp == -INFINITY) ? 0.f : exp2f(mp - mm);
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) o[dt] += *(const f32x4*)(park + dt * 16) * sp_;
+    ll += lp * sp_;
+  }
+  if (a.n_splits == 1) {  // the whole key range: normalise and store the output (no merge launch)
+    const float inv = 1.0f / ll;
+    const int64_t orow = (int64_t)b * k + j;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) {
+      i32x2 hi, lo;
+      split_bf16x4(o[dt] * inv, hi, lo);
+      const int64_t dst = aoff(orow, (int64_t)hq * DH + 16 * dt + 4 * grp, (int64_t)a.n_q * DH, a.out_mtiles);
+      *(i32x2*)(a.out + dst) = hi;
+      *(i32x2*)(a.out_lo + dst) = lo;
+    }
+    return;
+  }
 
   // the split's unnormalised (max, sum, O) per row, as attn_split_body leaves them
   const int64_t item = (int64_t)(b * k + j) * a.n_q + hq;
@@ -284,16 +310,25 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   attn_merge_body<DH, false>(a, item);
 }
 
+template <int DH, bool KV8>
+static void launch_split_rs(const AttnArgs& a, dim3 grid, const Exec& ex) {
+  // a row block of at most 32 rows (one block: n_rowblocks == 1) takes two row sets
+  if ((a.n_q / a.n_kv) * a.k <= 32 && a.n_rowblocks == 1)
+    SBD_KLAUNCH((attn_split_kernel<DH, KV8, 2>), grid, dim3(512), ex, a);
+  else
+    SBD_KLAUNCH((attn_split_kernel<DH, KV8, 4>), grid, dim3(512), ex, a);
+}
+
 hipError_t launch_attention_split(const AttnArgs& a, const Exec& ex) {
   dim3 grid(a.n_splits, a.n_kv * a.n_rowblocks, a.B);
   if (a.d_h == 128 && a.kv_fp8)
-    SBD_KLAUNCH((attn_split_kernel<128, true>), grid, dim3(512), ex, a);
+    launch_split_rs<128, true>(a, grid, ex);
   else if (a.d_h == 128)
-    SBD_KLAUNCH((attn_split_kernel<128, false>), grid, dim3(512), ex, a);
+    launch_split_rs<128, false>(a, grid, ex);
   else if (a.d_h == 64 && a.kv_fp8)
-    SBD_KLAUNCH((attn_split_kernel<64, true>), grid, dim3(512), ex, a);
+    launch_split_rs<64, true>(a, grid, ex);
   else if (a.d_h == 64)
-    SBD_KLAUNCH((attn_split_kernel<64, false>), grid, dim3(512), ex, a);
+    launch_split_rs<64, false>(a, grid, ex);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

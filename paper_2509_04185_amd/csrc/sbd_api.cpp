@@ -489,7 +489,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     aa.out_lo = attn_lo;
     aa.out_mtiles = mt;
     SBD_LAUNCH(c, SBD_KERNEL_ATTENTION, launch_attention_split(aa, ex));
-    SBD_LAUNCH(c, SBD_KERNEL_ATTN_MERGE, launch_attention_merge(aa, ex));
+    if (n_splits > 1) SBD_LAUNCH(c, SBD_KERNEL_ATTN_MERGE, launch_attention_merge(aa, ex));
 
     if (small) {
       GemvArgs v = gemv_base(attn, attn_lo, qd, M, qd, wp + L.wp_o, d / 16, vpart, vpart_cap, counters, c->xcd_ok);
