@@ -90,14 +90,16 @@ def test_fp8_tiny_every_path():
     libb.close()
 
 
-def test_fp8_8b_layer_kernels():
-    """Two layers of the Llama-3.1-8B shape, 16 rows, synthetic 700-position cache: the
-    per-XCD layer kernels streaming e4m3 against the same kernels on the widened values and
-    against the oracle; also n_causal = 0 and the block step's statistics."""
+@pytest.mark.parametrize("family", ["llama", "qwen"])
+def test_fp8_8b_layer_kernels(family):
+    """Two layers of the Llama-3.1-8B or Qwen-3-8B shape, 16 rows, synthetic 700-position
+    cache: the per-XCD layer kernels streaming e4m3 against the same kernels on the widened
+    values and against the oracle; also n_causal = 0 and the block step's statistics."""
     from paper_2509_04185_amd import Sbd
-    shape = dataclasses.replace(synth.LLAMA8B, name="llama8b_2layers", n_layers=2)
+    base = synth.LLAMA8B if family == "llama" else synth.QWEN8B
+    shape = dataclasses.replace(base, name=f"{family}8b_2layers", n_layers=2)
     torch.cuda.empty_cache()
-    print("[gpu] 2-layer 8B shape with FP8 weights", flush=True)
+    print(f"[gpu] 2-layer {family} 8B shape with FP8 weights", flush=True)
     w8 = synth.make_weights_fp8(shape, 9100, device="cuda")
     lib8 = Sbd(shape, w8, max_batch=1, max_seq_len=1024, max_block=16)
     libb = Sbd(shape, widened(w8), max_batch=1, max_seq_len=1024, max_block=16)

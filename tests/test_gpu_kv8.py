@@ -127,16 +127,19 @@ def test_kv8_tiny_prefill_blocks_commit(shape, e):
     lib.close()
 
 
+@pytest.mark.parametrize("family", ["llama", "qwen"])
 @pytest.mark.parametrize("weights", ["bf16", "fp8"])
-def test_kv8_8b_layer_shape(weights):
-    """Two layers of the Llama-3.1-8B shape (head_dim 128), synthetic 700-position cache in
-    e4m3, 16 rows on the per-XCD layer kernels and on the per-kernel path, 4 x 8 rows on the
-    GEMM path; also the block step's selection."""
+def test_kv8_8b_layer_shape(weights, family):
+    """Two layers of the Llama-3.1-8B or Qwen-3-8B shape (head_dim 128; Qwen: per-head q/k
+    RMSNorm, ffn 12288), synthetic 700-position cache in e4m3, 16 rows on the per-XCD layer
+    kernels and on the per-kernel path, 4 x 8 rows on the GEMM path; also the block step's
+    selection."""
     from paper_2509_04185_amd import Sbd
-    shape = dataclasses.replace(synth.LLAMA8B, name="llama8b_2layers", n_layers=2)
+    base = synth.LLAMA8B if family == "llama" else synth.QWEN8B
+    shape = dataclasses.replace(base, name=f"{family}8b_2layers", n_layers=2)
     e = 0
     torch.cuda.empty_cache()
-    print(f"[gpu] 2-layer 8B shape, {weights} weights, e4m3 KV cache", flush=True)
+    print(f"[gpu] 2-layer {family} 8B shape, {weights} weights, e4m3 KV cache", flush=True)
     if weights == "fp8":
         w = synth.make_weights_fp8(shape, 9400, device="cuda")
     else:
