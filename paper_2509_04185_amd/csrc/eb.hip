@@ -147,7 +147,6 @@ __global__ __launch_bounds__(64 * kEbSelWaves) void eb_select_kernel(EbArgs a) {
   __shared__ int sbad[64];     // 1: the row's statistics are NaN (undefined softmax)
   __shared__ int stok[64];
   __shared__ int order[64];
-  __shared__ int s_count;
   const int b = blockIdx.x;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int k = a.k;
@@ -234,10 +233,11 @@ __global__ __launch_bounds__(64 * kEbSelWaves) void eb_select_kernel(EbArgs a) {
     }
   }
   __syncthreads();
-  // Wave 0 ranks and selects; the other waves only join the barriers below.
-  const bool w0 = w == 0;
+  // Wave 0 ranks and selects; every value it needs from another lane is broadcast with
+  // readlane (a uniform loop over the rows or ranks), not read back from LDS one by one.
+  if (w != 0) return;
   const int j = lane;
-  const bool in = w0 && j < k;
+  const bool in = j < k;
   const bool masked = in && smask[j] != 0;
   const double H = in ? sh[j] : 0.0;
   const double C = in ? sconf[j] : 0.0;
@@ -246,41 +246,45 @@ __global__ __launch_bounds__(64 * kEbSelWaves) void eb_select_kernel(EbArgs a) {
   // rank by (NaN statistics, key, row) ascending: a permutation of the masked rows whose
   // first n places hold the rows with usable statistics; only those can be accepted
   int rank = 0, n = 0;
-  for (int i = 0; i < k; ++i) {
-    if (!smask[i]) continue;
-    n += sbad[i] ? 0 : 1;
-    if (sbad[i] < bad || (sbad[i] == bad && (skey[i] < key || (skey[i] == key && i < j)))) ++rank;
+  for (int i = 0; i < k; ++i) {  // uniform
+    if (!__builtin_amdgcn_readlane((int)masked, i)) continue;
+    const int bi = __builtin_amdgcn_readlane(bad, i);
+    const double ki = readlane_d(key, i);
+    n += bi ? 0 : 1;
+    if (bi < bad || (bi == bad && (ki < key || (ki == key && i < j)))) ++rank;
   }
   if (masked) order[rank] = j;
-  __syncthreads();
-  if (w0 && j == 0) {
-    int s = 0;
-    if (a.rule == SBD_SELECT_EB_ENTROPY) {  // eq. (eb_sampler): c_{r-1} <= gamma
-      double c = 0.0;
-      for (int r = 0; r < n; ++r) {
-        if (c <= a.gamma) s = r + 1;
-        c += sh[order[r]];
-      }
-    } else if (a.rule == SBD_SELECT_EB_CONFIDENCE) {  // App. B: sum - max of the prefix <= gamma
-      double c = 0.0, top = -INFINITY;
-      s = n > 0 ? 1 : 0;
-      for (int r = 0; r < n; ++r) {
-        c += sh[order[r]];
-        top = fmax(top, sh[order[r]]);
-        if (c - top <= a.gamma) s = r + 1;
-      }
-    } else {  // Factor: (r + 1)(1 - c_r) < f
-      s = n > 0 ? 1 : 0;
-      for (int r = 0; r < n; ++r)
-        if ((double)(r + 2) * (1.0 - sconf[order[r]]) < a.gamma) s = r + 1;
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the wave's order[] stores are done
+  // lane r holds the statistics of the row ranked r; the prefix sums run over the ranks in
+  // order, one float64 addition after another, as the selection rule is written
+  const int ro = lane < n ? order[lane] : 0;
+  const double hr = lane < n ? sh[ro] : 0.0;
+  const double cr = lane < n ? sconf[ro] : 0.0;
+  int s = 0;
+  if (a.rule == SBD_SELECT_EB_ENTROPY) {  // eq. (eb_sampler): c_{r-1} <= gamma
+    double c = 0.0;
+    for (int r = 0; r < n; ++r) {
+      if (c <= a.gamma) s = r + 1;
+      c += readlane_d(hr, r);
     }
-    s_count = s;
-    a.n_accepted[b] = s;
+  } else if (a.rule == SBD_SELECT_EB_CONFIDENCE) {  // App. B: sum - max of the prefix <= gamma
+    double c = 0.0, top = -INFINITY;
+    s = n > 0 ? 1 : 0;
+    for (int r = 0; r < n; ++r) {
+      const double h = readlane_d(hr, r);
+      c += h;
+      top = fmax(top, h);
+      if (c - top <= a.gamma) s = r + 1;
+    }
+  } else {  // Factor: (r + 1)(1 - c_r) < f
+    s = n > 0 ? 1 : 0;
+    for (int r = 0; r < n; ++r)
+      if ((double)(r + 2) * (1.0 - readlane_d(cr, r)) < a.gamma) s = r + 1;
   }
-  __syncthreads();
-  const int s = s_count;
+  if (lane == 0) a.n_accepted[b] = s;
   const bool acc = masked && rank < s;
-  // output slot = number of accepted rows before j
+  // output slot = number of accepted rows before j; accepted slots (< s) and the slots
+  // cleared below (>= s) are disjoint
   const unsigned long long before = __ballot(acc) & ((1ull << j) - 1ull);
   const int idx = __popcll(before);
   const int64_t row = (int64_t)b * k + j;
@@ -292,7 +296,6 @@ __global__ __launch_bounds__(64 * kEbSelWaves) void eb_select_kernel(EbArgs a) {
     if (a.entropy_out) a.entropy_out[row] = masked ? H : __builtin_nan("");
     if (a.conf_out) a.conf_out[row] = masked ? C : __builtin_nan("");
   }
-  __syncthreads();
   if (acc) {
     a.accepted_pos[(int64_t)b * k + idx] = j;
     if (a.accepted_tok) a.accepted_tok[(int64_t)b * k + idx] = stok[j];

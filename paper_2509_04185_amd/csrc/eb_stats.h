@@ -15,6 +15,15 @@ __device__ __forceinline__ double shfl_xor_d(double v, int m) {
   return *reinterpret_cast<double*>(&o);
 }
 
+// v of lane i (i uniform across the wave), in every lane
+__device__ __forceinline__ double readlane_d(double v, int i) {
+  const int2 iv = *reinterpret_cast<int2*>(&v);
+  int2 o;
+  o.x = __builtin_amdgcn_readlane(iv.x, i);
+  o.y = __builtin_amdgcn_readlane(iv.y, i);
+  return *reinterpret_cast<double*>(&o);
+}
+
 // One 64-column chunk of one row held by LPC adjacent lanes (xor distances below LPC), each
 // with VPL consecutive columns col0 .. col0 + VPL - 1 staged in LDS at p (fp32 products,
 // times `scale` = the row's norm scale gives the logit exactly as stored).  The mask column
