@@ -375,7 +375,8 @@ __device__ __forceinline__ void attn_merge_body(const AttnArgs& a, int64_t item)
     }
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
-      const float wu = __shfl(wgt, s0 + u);
+      if (s0 + u >= ns) break;  // wave-uniform
+      const float wu = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, wgt), s0 + u));
 #pragma unroll
       for (int e = 0; e < PER; ++e) acc[e] += wu * v[u][e];
     }
