@@ -149,7 +149,7 @@ int main() {
   CHECK(sbd_cache_len(ctx, 0, &len) == SBD_OK && len == 40);
   CHECK(sbd_prefill(ctx, 1, prompt.data(), 10, nullptr) == SBD_OK);
 
-  // ---- block forward: every forced error of the survey's list
+  // ---- block forward: each argument check of sbd_block_forward, forced one at a time
   const int k = 4;
   static float logits_buf[2 * 8 * 1024];
   float* logits = logits_buf;
