@@ -366,6 +366,33 @@ def test_ragged_batch_matches_single_sequences(tiny):
     close(both, ref[[3, 1, 0, 2]])
 
 
+@pytest.mark.parametrize("nc", [0, 1])
+def test_block_forward_on_an_empty_cache(tiny_qk, nc):
+    """Nothing cached (a sequence without a prompt): the App. A mask with L = 0, so row 0
+    attends to itself alone when causal (nc = 1) and every row to the whole block when
+    nc = 0.  A decode-sized forward on each decode path, then one of 32 rows (4 sequences x
+    8 rows, two of them with empty caches, two after prefills) on the kernels for more rows."""
+    t = tiny_qk
+    s = t.shape
+    fresh(t)
+    toks, is_mask = synth.block_rows(90 + nc, s, 1, 6, n_causal=1)
+    assert t.lib.cache_len(0) == 0
+    got = t.lib.block_forward([0], toks, is_mask=is_mask, n_causal=[nc]).cpu().numpy()
+    ref = t.model.block_forward([t.model.new_cache()], toks, [nc]).logits
+    close(got, ref)
+
+    fresh(t)
+    prompts = {1: synth.make_tokens(95, 20, s), 3: synth.make_tokens(96, 45, s)}
+    for b, p in prompts.items():
+        t.lib.prefill(b, p, want_logits=False)
+    toks4, is_mask4 = synth.block_rows(97 + nc, s, 4, 8, n_causal=1)
+    ncs = [nc, 1, 1 - nc, 1]
+    got4 = t.lib.block_forward([0, 1, 2, 3], toks4, is_mask=is_mask4, n_causal=ncs).cpu().numpy()
+    caches = [t.model.prefill(prompts[b])[0] if b in prompts else t.model.new_cache() for b in range(4)]
+    ref4 = t.model.block_forward(caches, toks4, ncs).logits
+    close(got4, ref4)
+
+
 def test_qk_norm_model_block_forward(tiny_qk):
     t = tiny_qk
     fresh(t)
