@@ -7,6 +7,7 @@ the same bf16 weights and caches.  Cases:
 * n_causal = 0: every iteration of Alg. 3 after a block's first feeds the block alone,
   each row seeing every other (App. A mask with the causal point at the cache end);
 * a batch whose sequences carry different n_causal and cache lengths;
+* an empty cache (no prompt), n_causal 1 and 0;
 * permuted positions: moving the prediction rows together with their pos_ids permutes
   their logits (the block is bidirectional, Fig. 3);
 * n_causal = 2 after a real prefill: the cached block equals a full recompute without a
@@ -112,6 +113,19 @@ def test_mixed_n_causal_batch_on_layer_kernels(setup):
     ref = setup.model.block_forward(caches, toks, [0, 3]).logits
     for path, g in got.items():
         parity.close(g, ref, regress=REGRESS, label=f"{path}: ")
+
+
+def test_empty_cache_on_layer_kernels(setup):
+    """Nothing cached (a sequence without a prompt): 31 of each XCD's 32 attention tasks get
+    an empty key range and the merge takes the one that holds the block; n_causal 1 and 0."""
+    for nc in (1, 0):
+        setup.lib.reset(0)
+        toks, is_mask = revealed_block(41 + nc, 16, nc, 0.2)
+        got = run_paths(setup, [0], toks[None], is_mask[None], [nc])
+        assert "layers" in got
+        ref = setup.model.block_forward([setup.model.new_cache()], toks[None], [nc]).logits
+        for path, g in got.items():
+            parity.close(g, ref, regress=REGRESS, label=f"{path}, n_causal {nc}: ")
 
 
 def test_permuted_positions_on_layer_kernels(setup):
