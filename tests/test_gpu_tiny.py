@@ -393,6 +393,31 @@ def test_block_forward_on_an_empty_cache(tiny_qk, nc):
     close(got4, ref4)
 
 
+def test_largest_block_at_full_capacity():
+    """k = 64 (the largest block) on a cache filled to max_seq_len by the block (cache_len +
+    k = max_seq_len = 200: 128 query rows per KV head, two row blocks of the split attention)
+    beside a short sequence, against the oracle; one position more is refused."""
+    from paper_2509_04185_amd import SbdError
+    s = synth.TINY
+    t = Tiny(s, 5005, max_batch=2, max_seq_len=200, max_block=64)
+    k = 64
+    prompts = [synth.make_tokens(70, 200 - k, s), synth.make_tokens(71, 9, s)]
+    for b, p in enumerate(prompts):
+        t.lib.prefill(b, p, want_logits=False)
+    toks, is_mask = synth.block_rows(72, s, 2, k, n_causal=3)
+    nc = [3, 1]
+    got = t.lib.block_forward([0, 1], toks, is_mask=is_mask, n_causal=nc).cpu().numpy()
+    caches = [t.model.prefill(p)[0] for p in prompts]
+    ref = t.model.block_forward(caches, toks, nc).logits
+    close(got, ref)
+    t.lib.commit([0, 1], [3, 1])
+    assert t.lib.cache_len(0) == 200 - k + 3
+    with pytest.raises(SbdError) as e:
+        t.lib.block_forward([0], toks[:1], is_mask=is_mask[:1], n_causal=[1])
+    assert e.value.name == "SBD_ERR_CAPACITY", str(e.value)
+    t.lib.close()
+
+
 def test_qk_norm_model_block_forward(tiny_qk):
     t = tiny_qk
     fresh(t)
