@@ -172,6 +172,33 @@ def test_select_rules_ladder_bit_exact(wide, B, k, V, mask_id):
     assert torch.equal(n1, n2) and torch.equal(p1, p2) and torch.equal(t1, t2)
 
 
+@pytest.mark.parametrize("name,rule", [("eb_entropy", O.RULE_EB_ENTROPY),
+                                       ("eb_confidence", O.RULE_EB_CONFIDENCE),
+                                       ("factor", O.RULE_FACTOR)])
+def test_select_sequences_with_no_or_one_masked_row(wide, name, rule):
+    """Degenerate masked sets: a sequence with no masked row accepts nothing (n = 0, every
+    slot -1) at any threshold; one with a single masked row accepts it at every threshold,
+    0 included (the rule keeps at least one row); a full sequence beside them as usual."""
+    B, k, V, mask_id = 3, 16, 4096, 4095
+    logits = synth.entropy_ladder_logits(78, B, k, V)
+    is_mask = np.zeros((B, k), np.uint8)
+    is_mask[1, 9] = 1
+    is_mask[2, 1:] = 1
+    m = is_mask.astype(bool)
+    for thr in (0.0, 1.0, math.inf):
+        acc, rtok, rH, rC = O.select(logits.numpy(), is_mask, rule, thr, mask_id)
+        assert acc[0] == [] and acc[1] == [9]
+        n_acc, pos, tok, H, C = wide.lib.select(logits.cuda(), is_mask, name, thr, mask_id)
+        for b in range(B):
+            n = int(n_acc[b])
+            assert pos[b, :n].tolist() == acc[b], (name, thr, b)
+            assert tok[b, :n].tolist() == rtok[b], (name, thr, b)
+            assert (pos[b, n:] == -1).all()
+        assert int(n_acc[0]) == 0 and int(n_acc[1]) == 1
+        np.testing.assert_allclose(H.cpu().numpy()[m], rH[m], rtol=1e-12, atol=1e-13)
+        assert np.isnan(H.cpu().numpy()[~m]).all()
+
+
 @pytest.mark.parametrize("name,rule,thr", [("eb_entropy", O.RULE_EB_ENTROPY, 0.5),
                                            ("eb_entropy", O.RULE_EB_ENTROPY, math.inf),
                                            ("eb_confidence", O.RULE_EB_CONFIDENCE, 1.0),
