@@ -8,6 +8,7 @@ the same bf16 weights and caches.  Cases:
   each row seeing every other (App. A mask with the causal point at the cache end);
 * a batch whose sequences carry different n_causal and cache lengths;
 * an empty cache (no prompt), n_causal 1 and 0;
+* blocks of 1, 2 and 5 rows (k = 1: the next-token forward of the speedup model);
 * permuted positions: moving the prediction rows together with their pos_ids permutes
   their logits (the block is bidirectional, Fig. 3);
 * n_causal = 2 after a real prefill: the cached block equals a full recompute without a
@@ -126,6 +127,19 @@ def test_empty_cache_on_layer_kernels(setup):
         ref = setup.model.block_forward([setup.model.new_cache()], toks[None], [nc]).logits
         for path, g in got.items():
             parity.close(g, ref, regress=REGRESS, label=f"{path}, n_causal {nc}: ")
+
+
+@pytest.mark.parametrize("k", [1, 2, 5])
+def test_small_blocks_on_layer_kernels(setup, k):
+    """The small blocks the speedup model times (k = 1 is the next-token forward, Sec. 4.2):
+    one causal row, then k - 1 masks, on a 1000-position cache."""
+    cache = setup.install(0, 1000, stream=4)
+    toks, is_mask = revealed_block(50 + k, k, 1, 0.0)
+    got = run_paths(setup, [0], toks[None], is_mask[None], [1])
+    assert "layers" in got
+    ref = setup.model.block_forward([cache], toks[None], [1]).logits
+    for path, g in got.items():
+        parity.close(g, ref, regress=REGRESS, label=f"{path}, k {k}: ")
 
 
 def test_permuted_positions_on_layer_kernels(setup):
