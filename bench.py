@@ -377,7 +377,10 @@ def main():
             label = "layer_mlp_kernel (gate/up + SwiGLU + down + residual, per-XCD)"
         else:
             kind, bpl = "gate_up", gate_up_bytes(s, B * k)
-            label = "gemv_kernel<8,4,1,EPI_SWIGLU> (gate/up projection + SwiGLU)"
+            if B * k <= 16:
+                label = "gemv_kernel<…, EPI_SWIGLU> (gate/up projection + SwiGLU, decode-sized GEMM)"
+            else:
+                label = f"gemm_kernel<…, EPI_SWIGLU> (gate/up projection + SwiGLU, M = {B * k})"
         c, t = prof[kind]
         avg_s = t / c * 1e-3
         achieved = bpl / avg_s / 1e9
