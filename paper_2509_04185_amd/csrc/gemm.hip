@@ -23,8 +23,10 @@
 //     quarters (or halves x row halves); a wave reads its weight fragments and the A
 //     fragments (hi and lo) of its rows from LDS and runs two MFMAs per pair.
 //   - When there are too few column blocks to fill the chip, K is split over workgroups
-//     of one XCD: each parks its partial tiles in that XCD's L2, and the last to arrive
-//     adds the slices in slice order (deterministic) and runs the epilogue.
+//     of one XCD, all resident at once (plans of one round): each parks its partial tiles
+//     in that XCD's L2 and waits for the others, then adds the slices of a share of the row
+//     tiles in slice order (deterministic) and runs their epilogue, so the finishing work
+//     of a unit is spread over its slices.
 // Epilogues (acc in the MFMA D layout: lane l holds column l % 16 of a tile, rows
 // 4*(l/16) + i):
 //   EPI_SCALED_STORE  out = rinv[m] * y           (QKV projection, LM head)
@@ -97,6 +99,46 @@ __device__ __forceinline__ void stage_barrier() {
   __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
+}
+
+// Value of an XCD-local counter, read with an atomic (a load could be served by the CU's own
+// L1); the zero comes from an instruction the compiler cannot see through, so the atomic
+// stays one.
+__device__ __forceinline__ int ctr_peek(int* ctr) {
+  int zero;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(zero));
+  return __hip_atomic_fetch_add(ctr, zero, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// The K slices of a unit (all on one XCD, all resident) wait until every one has parked its
+// partials: word 0 of the unit's counter line counts arrivals, word 1 departures, and the
+// last to depart resets both for the next launch.  The wait is bounded: one that gives up
+// raises the sticky error and the workgroup goes on (its results are then wrong, and the
+// next API call reports it).
+__device__ __forceinline__ void slices_arrived(const GemmArgs& a, int* ctr, int ks, int what) {
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's stores have reached the L2
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    int it = 0;
+    while (ctr_peek(ctr) < ks) {
+      __builtin_amdgcn_s_sleep(1);
+      if (++it > a.spin_limit) {
+        atomicOr(a.err, 1);
+        atomicExch(a.err + 1, what);
+        if (a.err_host != nullptr) {
+          __hip_atomic_store(a.err_host + 1, what, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+          __hip_atomic_store(a.err_host, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        }
+        break;
+      }
+    }
+    if (__hip_atomic_fetch_add(ctr + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) == ks - 1) {
+      __hip_atomic_store(ctr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      __hip_atomic_store(ctr + 1, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+  }
+  __syncthreads();
 }
 
 // STREAM: every weight byte is read by one workgroup (one row block): non-temporal loads.
@@ -288,41 +330,21 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
     if (c + 1 < nst) step(c + 1, wv1, av1, wv0, av0);
   }
 
-  // ---- K split over workgroups: park the slice, the last to arrive adds all in order
+  // ---- K split over workgroups (a plan of one round: every slice of a unit is resident):
+  // each slice parks its partial tiles and waits for the others; the epilogue then adds the
+  // slices of the row tiles kc, kc + KS, ... of the block in slice order and finishes them
+  // (every output is the same sum of the same slices, whichever slice finishes it).  The
+  // accumulators are not written again after the K loop: the sums go straight to LDS.
+  auto own = [&](int rt) { return rt % KS == kc; };
+  const int64_t slot = ((int64_t)uid * 4 + w) * (MTW * CW);       // in 1 KB (64 x f32x4) pieces
+  const int64_t zstride = (int64_t)n_cb * MB * 4 * MTW * CW;       // pieces per slice
   if (KS > 1) {
-    const int n_units = n_cb * MB;
-    const int64_t slot = ((int64_t)uid * 4 + w) * (MTW * CW);  // in 1 KB (64 x f32x4) pieces
-    const int64_t zstride = (int64_t)n_units * 4 * MTW * CW;     // pieces per slice
 #pragma unroll
     for (int mw = 0; mw < MTW; ++mw)
 #pragma unroll
       for (int cw = 0; cw < CW; ++cw)
         *(f32x4*)(a.part + ((kc * zstride + slot + mw * CW + cw) * 64 + lane) * 4) = acc[mw][cw];
-    if (!last_arrival_xcd(a.counters + (int64_t)uid * kCtrStride, KS)) return;
-    // ZB slices at a time, every piece of a slice in flight together; added in slice order
-    constexpr int ZB = MTW * CW >= 32 ? 1 : (MTW * CW >= 16 ? 2 : 4);
-    const __amdgpu_buffer_rsrc_t rp = buf_rsrc(a.part);
-#pragma unroll
-    for (int mw = 0; mw < MTW; ++mw)
-#pragma unroll
-      for (int cw = 0; cw < CW; ++cw) acc[mw][cw] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int z0 = 0; z0 < KS; z0 += ZB) {
-      i32x4 v[ZB][MTW][CW];
-#pragma unroll
-      for (int zz = 0; zz < ZB; ++zz)
-#pragma unroll
-        for (int mw = 0; mw < MTW; ++mw)
-#pragma unroll
-          for (int cw = 0; cw < CW; ++cw)
-            v[zz][mw][cw] = z0 + zz < KS ? ld16_l2(rp, (uint32_t)((((z0 + zz) * zstride + slot + mw * CW + cw) * 64 + lane) * 16))
-                                         : i32x4{0, 0, 0, 0};
-#pragma unroll
-      for (int zz = 0; zz < ZB; ++zz)
-#pragma unroll
-        for (int mw = 0; mw < MTW; ++mw)
-#pragma unroll
-          for (int cw = 0; cw < CW; ++cw) acc[mw][cw] += __builtin_bit_cast(f32x4, v[zz][mw][cw]);
-    }
+    slices_arrived(a, a.counters + (int64_t)uid * kCtrStride, KS, 65536 + EPI);
   }
 
   // ---- 1/rms of the block's rows (partials beyond the prefetched ones read here)
@@ -369,91 +391,120 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
   };
   if constexpr (EPI == EPI_RESID) {
     gw = *(const i32x2*)(a.g_next + n_l);
-    load_x(0, xcur);
+    if (own(wm * MTW)) load_x(0, xcur);
   }
 #pragma unroll
   for (int mw = 0; mw < MTW; ++mw) {
     const int rl0 = (wm * MTW + mw) * 16;  // first local row of this row tile
     if constexpr (EPI == EPI_RESID) {
-      if (mw + 1 < MTW) load_x(mw + 1, xnxt);
+      if (mw + 1 < MTW && own(wm * MTW + mw + 1)) load_x(mw + 1, xnxt);
     }
+    if (own(wm * MTW + mw)) {
+      if (KS > 1) {
+        // the slices' sums of this wave's tiles of the row tile: ZR slices at a time, all
+        // their pieces in flight
+        constexpr int ZR = 4;
+        const __amdgpu_buffer_rsrc_t rp = buf_rsrc(a.part);
+        f32x4 sum[CW];
 #pragma unroll
-    for (int cw = 0; cw < CW; ++cw)
+        for (int cw = 0; cw < CW; ++cw) sum[cw] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int z0 = 0; z0 < KS; z0 += ZR) {
+          i32x4 v[ZR][CW];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) stg[(4 * g + i) * LDR + cw * 16 + r] = acc[mw][cw][i];
-    if constexpr (EPI == EPI_SWIGLU) {
-      // task: (row, tile tt, half h) -> act columns 8 (tile) + 4 h .. + 3
-      constexpr int NT2 = 16 * CW * 2;
+          for (int zz = 0; zz < ZR; ++zz)
 #pragma unroll
-      for (int j = 0; j < (NT2 + 63) / 64; ++j) {
-        const int idx = j * 64 + lane;
-        const int row = idx / (CW * 2), tt = (idx % (CW * 2)) >> 1, h = idx & 1;
-        const int m = row0 + rl0 + row;
-        if (idx < NT2 && m < a.M) {
-          const f32x4 gt = *(const f32x4*)(stg + row * LDR + tt * 16 + h * 4);
-          const f32x4 up = *(const f32x4*)(stg + row * LDR + tt * 16 + 8 + h * 4);
-          const float rv = rinv_s[rl0 + row];
-          f32x4 y;
+            for (int cw = 0; cw < CW; ++cw)
+              v[zz][cw] = z0 + zz < KS ? ld16_l2(rp, (uint32_t)((((z0 + zz) * zstride + slot + mw * CW + cw) * 64 + lane) * 16))
+                                       : i32x4{0, 0, 0, 0};
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float gv = gt[e] * rv;
-            y[e] = gv / (1.0f + expf(-gv)) * (up[e] * rv);
-          }
-          i32x2 hi, lo;
-          split_bf16x4(y, hi, lo);
-          const int64_t o = aoff(m, (int64_t)(t0 + wc * CW + tt) * 8 + h * 4, a.ld_act, a.o_mtiles);
-          *(i32x2*)(a.act + o) = hi;
-          *(i32x2*)(a.act_lo + o) = lo;
+          for (int zz = 0; zz < ZR; ++zz)
+#pragma unroll
+            for (int cw = 0; cw < CW; ++cw) sum[cw] += __builtin_bit_cast(f32x4, v[zz][cw]);
         }
-      }
-    } else {
 #pragma unroll
-      for (int j = 0; j < 16 * CPR / 64; ++j) {
-        const int idx = j * 64 + lane;
-        const int row = idx / CPR, pc = idx % CPR;
-        const int m = row0 + rl0 + row;
-        const int n = n_w0 + pc * 4;
-        const f32x4 y = *(const f32x4*)(stg + row * LDR + pc * 4);
-        if constexpr (EPI == EPI_SCALED_STORE) {
-          if (m < a.M) *(f32x4*)(a.out_f32 + (int64_t)m * a.ldo + n) = y * rinv_s[rl0 + row];
-        } else if constexpr (EPI == EPI_LOGITS_EB) {
-          if (m < a.M && a.out_f32 != nullptr) *(f32x4*)(a.out_f32 + (int64_t)m * a.ldo + n) = y * rinv_s[rl0 + row];
-        } else {  // EPI_RESID
-          float s2 = 0.f;
-          if (m < a.M) {
-            const f32x4 xv = xcur[j] + y;
-            *(f32x4*)(a.x + (int64_t)m * a.ldx + n) = xv;
-            f32x4 xg;
-            xg[0] = xv[0] * __uint_as_float((uint32_t)gw[0] << 16);
-            xg[1] = xv[1] * __uint_as_float((uint32_t)gw[0] & 0xffff0000u);
-            xg[2] = xv[2] * __uint_as_float((uint32_t)gw[1] << 16);
-            xg[3] = xv[3] * __uint_as_float((uint32_t)gw[1] & 0xffff0000u);
+        for (int cw = 0; cw < CW; ++cw)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) stg[(4 * g + i) * LDR + cw * 16 + r] = sum[cw][i];
+      } else {
+#pragma unroll
+        for (int cw = 0; cw < CW; ++cw)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) stg[(4 * g + i) * LDR + cw * 16 + r] = acc[mw][cw][i];
+      }
+      if constexpr (EPI == EPI_SWIGLU) {
+        // task: (row, tile tt, half h) -> act columns 8 (tile) + 4 h .. + 3
+        constexpr int NT2 = 16 * CW * 2;
+#pragma unroll
+        for (int j = 0; j < (NT2 + 63) / 64; ++j) {
+          const int idx = j * 64 + lane;
+          const int row = idx / (CW * 2), tt = (idx % (CW * 2)) >> 1, h = idx & 1;
+          const int m = row0 + rl0 + row;
+          if (idx < NT2 && m < a.M) {
+            const f32x4 gt = *(const f32x4*)(stg + row * LDR + tt * 16 + h * 4);
+            const f32x4 up = *(const f32x4*)(stg + row * LDR + tt * 16 + 8 + h * 4);
+            const float rv = rinv_s[rl0 + row];
+            f32x4 y;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float gv = gt[e] * rv;
+              y[e] = gv / (1.0f + expf(-gv)) * (up[e] * rv);
+            }
             i32x2 hi, lo;
-            split_bf16x4(xg, hi, lo);
-            const int64_t on = aoff(m, n, a.ldx, a.o_mtiles);
-            *(i32x2*)(a.xn + on) = hi;
-            *(i32x2*)(a.xn_lo + on) = lo;
-            s2 = (xv[0] * xv[0] + xv[1] * xv[1]) + (xv[2] * xv[2] + xv[3] * xv[3]);
+            split_bf16x4(y, hi, lo);
+            const int64_t o = aoff(m, (int64_t)(t0 + wc * CW + tt) * 8 + h * 4, a.ld_act, a.o_mtiles);
+            *(i32x2*)(a.act + o) = hi;
+            *(i32x2*)(a.act_lo + o) = lo;
           }
+        }
+      } else {
 #pragma unroll
-          for (int o = 1; o < CPR; o <<= 1) s2 += __shfl_xor(s2, o);  // the row's CPR lanes
-          if (pc == 0) ssq_s[wc][rl0 + row] = s2;
+        for (int j = 0; j < 16 * CPR / 64; ++j) {
+          const int idx = j * 64 + lane;
+          const int row = idx / CPR, pc = idx % CPR;
+          const int m = row0 + rl0 + row;
+          const int n = n_w0 + pc * 4;
+          const f32x4 y = *(const f32x4*)(stg + row * LDR + pc * 4);
+          if constexpr (EPI == EPI_SCALED_STORE) {
+            if (m < a.M) *(f32x4*)(a.out_f32 + (int64_t)m * a.ldo + n) = y * rinv_s[rl0 + row];
+          } else if constexpr (EPI == EPI_LOGITS_EB) {
+            if (m < a.M && a.out_f32 != nullptr) *(f32x4*)(a.out_f32 + (int64_t)m * a.ldo + n) = y * rinv_s[rl0 + row];
+          } else {  // EPI_RESID
+            float s2 = 0.f;
+            if (m < a.M) {
+              const f32x4 xv = xcur[j] + y;
+              *(f32x4*)(a.x + (int64_t)m * a.ldx + n) = xv;
+              f32x4 xg;
+              xg[0] = xv[0] * __uint_as_float((uint32_t)gw[0] << 16);
+              xg[1] = xv[1] * __uint_as_float((uint32_t)gw[0] & 0xffff0000u);
+              xg[2] = xv[2] * __uint_as_float((uint32_t)gw[1] << 16);
+              xg[3] = xv[3] * __uint_as_float((uint32_t)gw[1] & 0xffff0000u);
+              i32x2 hi, lo;
+              split_bf16x4(xg, hi, lo);
+              const int64_t on = aoff(m, n, a.ldx, a.o_mtiles);
+              *(i32x2*)(a.xn + on) = hi;
+              *(i32x2*)(a.xn_lo + on) = lo;
+              s2 = (xv[0] * xv[0] + xv[1] * xv[1]) + (xv[2] * xv[2] + xv[3] * xv[3]);
+            }
+#pragma unroll
+            for (int o = 1; o < CPR; o <<= 1) s2 += __shfl_xor(s2, o);  // the row's CPR lanes
+            if (pc == 0) ssq_s[wc][rl0 + row] = s2;
+          }
         }
       }
-    }
-    if constexpr (EPI == EPI_LOGITS_EB) {
-      // the staged row tile again: lane L reduces VPL = 4 CW consecutive columns of row L / 4,
-      // 16 / CW lanes per 64-column chunk
-      constexpr int VPL = 4 * CW, LPC = 16 / CW;
-      static_assert(VPL * LPC == kEbFChunk, "a chunk is 64 columns");
-      const int row = lane >> 2, seg = lane & 3;
-      const int m = row0 + rl0 + row;
-      const int col0 = n_w0 + seg * VPL;
-      float mx;
-      int arg;
-      double z, sz;
-      eb_seg_stats<VPL, LPC>(stg + row * LDR + seg * VPL, rinv_s[rl0 + row], col0, a.eb_mask_id, mx, arg, z, sz);
-      if (seg % LPC == 0 && m < a.M) eb_chunk_store(a.eb_part, a.eb_arg, a.eb_chunks, m, col0 / kEbFChunk, mx, arg, z, sz);
+      if constexpr (EPI == EPI_LOGITS_EB) {
+        // the staged row tile again: lane L reduces VPL = 4 CW consecutive columns of row L / 4,
+        // 16 / CW lanes per 64-column chunk
+        constexpr int VPL = 4 * CW, LPC = 16 / CW;
+        static_assert(VPL * LPC == kEbFChunk, "a chunk is 64 columns");
+        const int row = lane >> 2, seg = lane & 3;
+        const int m = row0 + rl0 + row;
+        const int col0 = n_w0 + seg * VPL;
+        float mx;
+        int arg;
+        double z, sz;
+        eb_seg_stats<VPL, LPC>(stg + row * LDR + seg * VPL, rinv_s[rl0 + row], col0, a.eb_mask_id, mx, arg, z, sz);
+        if (seg % LPC == 0 && m < a.M) eb_chunk_store(a.eb_part, a.eb_arg, a.eb_chunks, m, col0 / kEbFChunk, mx, arg, z, sz);
+      }
     }
     if constexpr (EPI == EPI_RESID) {
 #pragma unroll
@@ -467,7 +518,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
       float s = ssq_s[0][threadIdx.x];
 #pragma unroll
       for (int q = 1; q < WC; ++q) s += ssq_s[q][threadIdx.x];
-      if (m < a.M) a.sumsq_out[(int64_t)m * a.n_part_out + cb] = s;
+      if (m < a.M && own((int)threadIdx.x / 16)) a.sumsq_out[(int64_t)m * a.n_part_out + cb] = s;
     }
   }
 }
@@ -487,8 +538,10 @@ GemmPlan gemm_plan(int M, int n_tiles, int K, int64_t part_cap) {
       if (ks > 1 && S_all / ks < 4) break;
       if (ks > 1 && (int64_t)ks * n_cb * nt * 16 * mb * mt * 16 > part_cap) break;
       if (ks > 1 && (int64_t)n_cb * mb * kCtrStride > kLayerCtr0) break;  // one counter line per unit
-      // one workgroup per CU, 32 CUs per XCD; units of a column block share its XCD
+      // one workgroup per CU, 32 CUs per XCD; units of a column block share its XCD.  The
+      // slices of a unit wait for each other, so a split plan runs in one round.
       const int per_xcd = ((n_cb + 7) / 8) * mb * ks;
+      if (ks > 1 && per_xcd > kXcdWgs) break;
       const int rounds = (per_xcd + 31) / 32;
       const double steps = (double)S_all / ks;
       const double w_time = steps * nt * 1024.0 / (8e12 / 256);                   // weights at a CU's share of HBM
@@ -555,6 +608,10 @@ hipError_t launch_gemm(GemmEpi epi, const GemmArgs& a0, const Exec& ex) {
   GemmArgs a = a0;
   a.splits = p.splits;
   a.m_blocks = p.m_blocks;
+  // the slices of a unit wait for each other: only in a plan of one round (gemm_plan), on a
+  // device that keeps every workgroup of an XCD resident at once
+  if (p.splits > 1 && (!a0.wait_ok || a0.err == nullptr || ((p.n_cb + 7) / 8) * p.m_blocks * p.splits > kXcdWgs))
+    return hipErrorInvalidValue;
   switch (epi) {
     case EPI_SCALED_STORE: launch_epi<EPI_SCALED_STORE>(a, p.mt, p.nt, ex); break;
     case EPI_RESID: launch_epi<EPI_RESID>(a, p.mt, p.nt, ex); break;

@@ -205,10 +205,11 @@ sbd_status fail(sbd_ctx* c, sbd_status st, const char* fmt, ...) {
 sbd_status check_sticky(sbd_ctx* c) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(c, SBD_ERR_HIP, "earlier HIP error: %s", hipGetErrorString(e));
-  // written by copies queued after each fused forward, or by a layer kernel whose wait gave
-  // up; it never goes back to zero
+  // written by copies queued after each fused forward, or by a layer kernel or GEMM whose
+  // wait gave up; it never goes back to zero
   if (c->err_host != nullptr && __atomic_load_n(c->err_host, __ATOMIC_ACQUIRE) != 0)
-    return fail(c, SBD_ERR_HIP, "a decode forward gave up waiting for its inputs (task code %d)",
+    return fail(c, SBD_ERR_HIP, "a forward gave up waiting for its inputs (task code %d: layer * 16 + phase "
+                "of a per-XCD layer kernel, or 65536 + epilogue of a GEMM's K slices)",
                 __atomic_load_n(c->err_host + 1, __ATOMIC_ACQUIRE));
   return SBD_OK;
 }
@@ -252,13 +253,18 @@ hipEvent_t take_event(sbd_ctx* c) {
     if ((ctx)->prof) (ctx)->recs.push_back(sbd_ctx::Rec{kind, ex.start, ex.stop}); \
   } while (0)
 
-// split_ok: K may be split over workgroups that hand their partials off through one XCD's L2
-// (false when the device does not place workgroup i on XCD i % 8)
+// K may be split over workgroups that hand their partials off through one XCD's L2, and
+// the slices of a unit may wait for each other, only when the device places workgroup i on
+// XCD i % 8 (probed at creation)
 GemmArgs gemm_base(const bf16_t* A, const bf16_t* A_lo, int64_t lda, int M, int K, const bf16_t* Wp,
-                   int n_tiles, float* part, int64_t part_cap, int* counters, bool split_ok) {
+                   int n_tiles, float* part, int64_t part_cap, int* counters, const sbd_ctx* c) {
   GemmArgs g{};
   g.A = A; g.A_lo = A_lo; g.lda = lda; g.M = M; g.K = K; g.Wp = Wp; g.n_tiles = n_tiles;
-  g.part = part; g.part_cap = part_cap; g.counters = counters; g.no_split = split_ok ? 0 : 1;
+  g.part = part; g.part_cap = part_cap; g.counters = counters; g.no_split = c->xcd_ok ? 0 : 1;
+  g.wait_ok = c->xcd_ok ? 1 : 0;
+  g.spin_limit = c->wait_limit;
+  g.err = c->at<int>(c->lay.fwd_err);
+  g.err_host = c->err_host;
   return g;
 }
 
@@ -463,7 +469,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
       v.qkv = qe;
       SBD_LAUNCH(c, SBD_KERNEL_QKV, launch_gemv(EPI_QKV, v, GemvShape{}, ex));
     } else {
-      GemmArgs g = gemm_base(xn, xn_lo, d, M, d, wp, (int)(L.n_qkv / 16), vpart, vpart_cap, counters, c->xcd_ok);
+      GemmArgs g = gemm_base(xn, xn_lo, d, M, d, wp, (int)(L.n_qkv / 16), vpart, vpart_cap, counters, c);
       g8((int64_t)l * L.wp_layer, (int64_t)l * L.ws_layer, g);
       g.a_mtiles = mt;
       g.out_f32 = qkv; g.ldo = L.n_qkv;
@@ -498,7 +504,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
       v.sumsq = sumsq; v.n_part = n_part_o;
       SBD_LAUNCH(c, SBD_KERNEL_O_PROJ, launch_gemv(EPI_RESID, v, GemvShape{}, ex));
     } else {
-      GemmArgs go = gemm_base(attn, attn_lo, qd, M, qd, wp + L.wp_o, d / 16, vpart, vpart_cap, counters, c->xcd_ok);
+      GemmArgs go = gemm_base(attn, attn_lo, qd, M, qd, wp + L.wp_o, d / 16, vpart, vpart_cap, counters, c);
       g8((int64_t)l * L.wp_layer + L.wp_o, (int64_t)l * L.ws_layer + L.ws_o, go);
       go.a_mtiles = mt; go.o_mtiles = mt;
       go.x = x; go.ldx = d; go.xn = xn; go.xn_lo = xn_lo; go.g_next = w.mlp_norm; go.sumsq_out = sumsq;
@@ -521,7 +527,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
       n_part_cur = n_part_down;
       SBD_LAUNCH(c, SBD_KERNEL_DOWN, launch_gemv(EPI_RESID, vd, GemvShape{}, ex));
     } else {
-      GemmArgs gu = gemm_base(xn, xn_lo, d, M, d, wp + L.wp_gu, m.ffn_dim / 8, vpart, vpart_cap, counters, c->xcd_ok);
+      GemmArgs gu = gemm_base(xn, xn_lo, d, M, d, wp + L.wp_gu, m.ffn_dim / 8, vpart, vpart_cap, counters, c);
       g8((int64_t)l * L.wp_layer + L.wp_gu, (int64_t)l * L.ws_layer + L.ws_gu, gu);
       gu.a_mtiles = mt; gu.o_mtiles = mt;
       gu.sumsq_in = sumsq; gu.n_part = n_part_cur; gu.inv_d = 1.0f / d; gu.eps = m.rms_eps;
@@ -529,7 +535,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
       SBD_LAUNCH(c, SBD_KERNEL_GATE_UP, launch_gemm(EPI_SWIGLU, gu, ex));
 
       GemmArgs gd = gemm_base(act, act_lo, m.ffn_dim, M, m.ffn_dim, wp + L.wp_down, d / 16, vpart, vpart_cap,
-                              counters, c->xcd_ok);
+                              counters, c);
       g8((int64_t)l * L.wp_layer + L.wp_down, (int64_t)l * L.ws_layer + L.ws_down, gd);
       gd.a_mtiles = mt; gd.o_mtiles = mt;
       gd.x = x; gd.ldx = d; gd.xn = xn; gd.xn_lo = xn_lo; gd.g_next = g_after;
@@ -556,7 +562,7 @@ sbd_status run_forward(sbd_ctx* c, int B, int k, const std::vector<RowParam>& ro
     } else {
       // inputs in fragment order (also for one row of a prefill chunk: rows from a_row0)
       GemmArgs gl = gemm_base(xn, xn_lo, d, Ml, d, c->at<bf16_t>(L.wpack) + L.wp_lm, m.vocab / 16, vpart,
-                              vpart_cap, counters, c->xcd_ok);
+                              vpart_cap, counters, c);
       g8(L.wp_lm, L.ws_lm, gl);
       gl.a_mtiles = mt; gl.a_row0 = r0;
       gl.out_f32 = logits; gl.ldo = m.vocab;

@@ -154,6 +154,15 @@ struct GemmArgs {
   float* part;
   int64_t part_cap;
   int* counters;
+  // wait_ok: the device places workgroup i on XCD i % 8 and has 32 CUs per XCD, so in a plan
+  // of one round every workgroup is resident at once and the K slices of a unit may wait for
+  // each other (K is split only then): each slice then sums the slices of its own row tiles
+  // and finishes them.  A wait that gives up after spin_limit polls raises the sticky error
+  // err (device word, and its pinned host copy err_host).
+  int wait_ok;
+  int spin_limit;
+  int* err;
+  int* err_host;
   // set by launch_gemm from the plan
   int splits, m_blocks;
   int no_split;        // 1: one K slice per unit (no hand-off between workgroups)

@@ -374,6 +374,42 @@ def test_kv_import_roundtrip_and_parity(tiny):
     close(got.cpu().numpy(), ref)
 
 
+def test_split_gemm_wait_gives_up_then_recovers():
+    """The K slices of a split GEMM wait for each other with a bounded wait.  A forward of 64
+    rows on the tiny model runs its down projection (K = 768) as 4 K slices; with a limit of
+    zero polls the slices that arrive first give up, the launch still ends, and the next call
+    reports the sticky error (task code 65536 + the residual epilogue, 1); a fresh context then
+    computes the same logits as before, to the bit."""
+    from paper_2509_04185_amd import SbdError
+    s = synth.TINY
+    B, k = 4, 16
+
+    def make():
+        t = Tiny(s, 5105, max_batch=B, max_seq_len=128, max_block=k)
+        for b in range(B):
+            t.lib.prefill(b, synth.make_tokens(80 + b, 20 + 7 * b, s), want_logits=False)
+        return t
+
+    toks, is_mask = synth.block_rows(81, s, B, k, n_causal=1)
+    seqs = list(range(B))
+    t = make()
+    print("[gpu] split GEMM: forced wait failure, 4 x 16 rows", flush=True)
+    ref = t.lib.block_forward(seqs, toks, is_mask=is_mask).clone()
+    torch.cuda.synchronize()
+    t.lib.set_wait_limit(0)
+    t.lib.block_forward(seqs, toks, is_mask=is_mask)  # its waits give up; the launch still ends
+    torch.cuda.synchronize()
+    with pytest.raises(SbdError) as e:
+        t.lib.block_forward(seqs, toks, is_mask=is_mask)
+    assert "gave up waiting" in str(e.value) and "task code 65537" in str(e.value), str(e.value)
+    t.lib.close()
+    t2 = make()
+    got = t2.lib.block_forward(seqs, toks, is_mask=is_mask)
+    torch.cuda.synchronize()
+    assert torch.equal(got, ref)
+    t2.lib.close()
+
+
 def test_ragged_batch_matches_single_sequences(tiny):
     fresh(tiny)
     s = tiny.shape
