@@ -548,8 +548,10 @@ GemmPlan gemm_plan(int M, int n_tiles, int K, int64_t part_cap) {
       const double m_time = steps * nt * mt * 2.0 * 16.0 / 4.0 / 2.4e9;           // MFMA issue, 4 SIMDs
       const double part_bytes = ks > 1 ? 2.0 * ks * n_tiles * 16.0 * mb * mt * 16 * 4 : 0.0;
       const double a_bytes = (double)n_cb * mb * mt * 16 * K * 4;
-      // the last arriver reads the slices in batches of ZB (fewer when a wave holds more
-      // accumulators), one dependent round trip each
+      // the split's own cost (parked partials, the slices' wait, their sums): a price per slice
+      // batch fitted to the single-finisher reduction this kernel used before; on the measured
+      // shapes it still picks the faster plans (a model of the shared sums alone moved gate/up
+      // to unsplit plans that ran 0.5 % slower per forward)
       const int nacc = (mt / 2) * (nt / 2);  // accumulator tiles per wave (2 x 2 waves)
       const int zb = nacc >= 32 ? 1 : (nacc >= 16 ? 2 : 4);
       const double reduce = ks > 1 ? 1e-6 + 0.6e-6 * ((ks + zb - 1) / zb) : 0.0;
