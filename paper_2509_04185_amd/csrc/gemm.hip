@@ -14,7 +14,7 @@
 // gemv.hip.  At these M every projection still reads far more weight bytes than it does
 // MFMA work per byte (M flop per weight byte, against a ridge of ~300), so the design
 // streams every weight byte from HBM once:
-//   - A workgroup owns a column block of NT tiles (128 or 256 columns) and a row block of
+//   - A workgroup owns a column block of NT tiles (128, 256, or for gate/up 192 columns) and a row block of
 //     MT tiles (up to 128 rows; larger M is cut into row blocks that run on the same XCD
 //     and meet the same weights in its L2), and a range of K steps.
 //   - Weights and activations reach LDS by direct loads (global_load_lds, no registers)
@@ -525,14 +525,16 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
 
 // ---- host side: plan and launch
 
-GemmPlan gemm_plan(int M, int n_tiles, int K, int64_t part_cap) {
+GemmPlan gemm_plan(int M, int n_tiles, int K, int64_t part_cap, bool nt12) {
   GemmPlan best{};
   const int mt = M <= 32 ? 2 : (M <= 64 ? 4 : 8);
   const int mb = (M + mt * 16 - 1) / (mt * 16);
   const int S_all = K / 32;
   double best_cost = 1e300;
-  for (int nt : {16, 8}) {
-    if (n_tiles % nt) continue;
+  // 12-tile blocks (gate/up only): Qwen 8B's 1536 gate/up tiles then fill all 32 CUs of an
+  // XCD in one round (16 blocks x 2 K slices) where 16-tile blocks leave 8 idle
+  for (int nt : {16, 12, 8}) {
+    if (n_tiles % nt || (nt == 12 && !nt12)) continue;
     const int n_cb = n_tiles / nt;
     for (int ks = 1; ks <= 8; ++ks) {
       if (ks > 1 && S_all / ks < 4) break;
@@ -570,18 +572,33 @@ static void launch_cfg(const GemmArgs& a, const Exec& ex) {
   const int n_cb = a.n_tiles / NT;
   const unsigned grid = (unsigned)(((n_cb + 7) / 8) * 8 * a.splits * a.m_blocks);
   const bool w8 = a.Wp8 != nullptr;
-  if (a.m_blocks == 1 && w8)
-    SBD_KLAUNCH((gemm_kernel<MT, NT, EPI, true, true>), dim3(grid), dim3(256), ex, a);
-  else if (a.m_blocks == 1)
-    SBD_KLAUNCH((gemm_kernel<MT, NT, EPI, true, false>), dim3(grid), dim3(256), ex, a);
-  else if (w8)
-    SBD_KLAUNCH((gemm_kernel<MT, NT, EPI, false, true>), dim3(grid), dim3(256), ex, a);
-  else
-    SBD_KLAUNCH((gemm_kernel<MT, NT, EPI, false, false>), dim3(grid), dim3(256), ex, a);
+  if constexpr (NT == 12) {  // bf16 weights only (gemm_plan)
+    if (a.m_blocks == 1)
+      SBD_KLAUNCH((gemm_kernel<MT, NT, EPI, true, false>), dim3(grid), dim3(256), ex, a);
+    else
+      SBD_KLAUNCH((gemm_kernel<MT, NT, EPI, false, false>), dim3(grid), dim3(256), ex, a);
+  } else {
+    if (a.m_blocks == 1 && w8)
+      SBD_KLAUNCH((gemm_kernel<MT, NT, EPI, true, true>), dim3(grid), dim3(256), ex, a);
+    else if (a.m_blocks == 1)
+      SBD_KLAUNCH((gemm_kernel<MT, NT, EPI, true, false>), dim3(grid), dim3(256), ex, a);
+    else if (w8)
+      SBD_KLAUNCH((gemm_kernel<MT, NT, EPI, false, true>), dim3(grid), dim3(256), ex, a);
+    else
+      SBD_KLAUNCH((gemm_kernel<MT, NT, EPI, false, false>), dim3(grid), dim3(256), ex, a);
+  }
 }
 
 template <int EPI>
 static void launch_epi(const GemmArgs& a, int mt, int nt, const Exec& ex) {
+  if constexpr (EPI == EPI_SWIGLU) {
+    if (nt == 12) {
+      if (mt == 2) launch_cfg<2, 12, EPI>(a, ex);
+      else if (mt == 4) launch_cfg<4, 12, EPI>(a, ex);
+      else launch_cfg<8, 12, EPI>(a, ex);
+      return;
+    }
+  }
   if (nt == 16) {
     if (mt == 2) launch_cfg<2, 16, EPI>(a, ex);
     else if (mt == 4) launch_cfg<4, 16, EPI>(a, ex);
@@ -596,7 +613,8 @@ static void launch_epi(const GemmArgs& a, int mt, int nt, const Exec& ex) {
 hipError_t launch_gemm(GemmEpi epi, const GemmArgs& a0, const Exec& ex) {
   if (a0.M < 1 || a0.K < 32 || a0.K % 32 || a0.n_tiles < 8 || a0.n_tiles % 8) return hipErrorInvalidValue;
   if (a0.Wp8 != nullptr && a0.wscale == nullptr) return hipErrorInvalidValue;
-  const GemmPlan p = gemm_plan(a0.M, a0.n_tiles, a0.K, (a0.part && !a0.no_split) ? a0.part_cap : 0);
+  const bool nt12 = epi == EPI_SWIGLU && a0.Wp8 == nullptr;
+  const GemmPlan p = gemm_plan(a0.M, a0.n_tiles, a0.K, (a0.part && !a0.no_split) ? a0.part_cap : 0, nt12);
   if (p.nt == 0) return hipErrorInvalidValue;
   if (p.splits > 1 && (a0.counters == nullptr || (int64_t)p.n_cb * p.m_blocks * kCtrStride > kLayerCtr0))
     return hipErrorInvalidValue;

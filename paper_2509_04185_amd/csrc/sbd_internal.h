@@ -173,7 +173,9 @@ struct GemmArgs {
 struct GemmPlan {
   int mt, nt, splits, m_blocks, n_cb;
 };
-GemmPlan gemm_plan(int M, int n_tiles, int K, int64_t part_cap);
+// nt12: 12-tile column blocks may be used (EPI_SWIGLU with bf16 weights: an epilogue
+// without row reductions across the block's columns)
+GemmPlan gemm_plan(int M, int n_tiles, int K, int64_t part_cap, bool nt12 = false);
 
 hipError_t launch_gemm(GemmEpi epi, const GemmArgs& a, const Exec& ex);
 
