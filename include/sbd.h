@@ -337,12 +337,15 @@ typedef enum {
 } sbd_decode_path;
 sbd_status sbd_set_decode_path(sbd_ctx* ctx, int32_t path);
 /*
- * Testing aid: the number of polls after which a dependency wait inside a decode launch of
- * the per-XCD layer kernels gives up (a negative value restores the default of about two
- * million, which no correct launch comes near).  A wait that gives up raises the sticky
- * error that every later call on the context reports as SBD_ERR_HIP; the launch still runs
- * to its end (on wrong data), it never hangs.  With a small limit a test can take that
- * path on purpose.  INVALID_ARG for a null context.
+ * Testing aid: the number of polls after which a dependency wait inside a launch gives up:
+ * those of the per-XCD layer kernels (decode-sized forwards), and the wait of a split GEMM's
+ * K slices for each other (forwards and prefill chunks of more than 16 rows).  A negative
+ * value restores the default of about two million, which no correct launch comes near.  A
+ * wait that gives up raises the sticky error that every later call on the context reports
+ * as SBD_ERR_HIP, with a task code (layer * 16 + phase for a layer kernel, 65536 + the
+ * epilogue for GEMM slices); the launch still runs to its end (on wrong data), it never
+ * hangs.  With a small limit a test can take that path on purpose.  INVALID_ARG for a null
+ * context.
  */
 sbd_status sbd_set_wait_limit(sbd_ctx* ctx, int32_t polls);
 /*

@@ -322,7 +322,7 @@ class Sbd:
         _check(self.lib, self.lib.sbd_set_decode_path(self.ctx, code), "sbd_set_decode_path", self.ctx)
 
     def set_wait_limit(self, polls: int):
-        """Polls before a wait inside a layer-kernel launch gives up; negative: the default."""
+        """Polls before a wait inside a layer-kernel or split-GEMM launch gives up; negative: the default."""
         _check(self.lib, self.lib.sbd_set_wait_limit(self.ctx, polls), "sbd_set_wait_limit", self.ctx)
 
     def decode_path_fits(self, path: str, batch: int, k: int) -> bool:
