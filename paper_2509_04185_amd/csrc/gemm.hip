@@ -166,7 +166,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
   const int KS = a.splits, MB = a.m_blocks, P = KS * MB;
   const int jx = (int)(blockIdx.x >> 3);
   const int cb = (jx / P) * 8 + (int)(blockIdx.x & 7);
-  const int n_cb = a.n_tiles / NT;
+  // a last column block may be half full (n_tiles % NT == 8, LM head with bf16 weights and
+  // two waves across the block: the second wave's tiles are past the end)
+  const int n_cb = (a.n_tiles + NT - 1) / NT;
   if (cb >= n_cb) return;
   const int mb = (jx % P) / KS, kc = (jx % P) % KS;
   const int uid = cb * MB + mb;
@@ -189,7 +191,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
         src[u] = (const char*)(a.Wp8 + packed_frag(t0 + 2 * f, s_b, S_all) + lane * 16);
         stride[u] = kPackStep;
       } else {
-        src[u] = (const char*)(a.Wp + packed_frag(t0 + f, s_b, S_all) + lane * 8);
+        // a half-full block's tiles past the end read the last tile (results discarded)
+        constexpr bool kHalf = EPI == EPI_SCALED_STORE || EPI == EPI_LOGITS_EB;
+        src[u] = (const char*)(a.Wp + packed_frag(kHalf ? min(t0 + f, a.n_tiles - 1) : t0 + f, s_b, S_all) + lane * 8);
         stride[u] = kPackStep * 2;
       }
     } else {
@@ -375,6 +379,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
   constexpr int CPR = CW * 4;       // float4 pieces per staged row
   float* stg = reinterpret_cast<float*>(smem) + w * 16 * LDR;
   const int n_w0 = (t0 + wc * CW) * 16;  // first output column of this wave
+  // false only for the empty half of a half-full block (an LM head's last block)
+  const bool cols_in = (EPI != EPI_SCALED_STORE && EPI != EPI_LOGITS_EB) || n_w0 < a.n_tiles * 16;
   // EPI_RESID: a lane's residual pieces of row tile mw + 1 are requested before the stores
   // of row tile mw (which the compiler may not move them past); the gain is the same for
   // every row of the lane.
@@ -399,7 +405,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
     if constexpr (EPI == EPI_RESID) {
       if (mw + 1 < MTW && own(wm * MTW + mw + 1)) load_x(mw + 1, xnxt);
     }
-    if (own(wm * MTW + mw)) {
+    if (own(wm * MTW + mw) && cols_in) {
       if (KS > 1) {
         // the slices' sums of this wave's tiles of the row tile: ZR slices at a time, all
         // their pieces in flight
@@ -525,7 +531,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
 
 // ---- host side: plan and launch
 
-GemmPlan gemm_plan(int M, int n_tiles, int K, int64_t part_cap, bool nt12) {
+GemmPlan gemm_plan(int M, int n_tiles, int K, int64_t part_cap, bool nt12, bool half_block) {
   GemmPlan best{};
   const int mt = M <= 32 ? 2 : (M <= 64 ? 4 : 8);
   const int mb = (M + mt * 16 - 1) / (mt * 16);
@@ -534,10 +540,13 @@ GemmPlan gemm_plan(int M, int n_tiles, int K, int64_t part_cap, bool nt12) {
   // 12-tile blocks (gate/up only): Qwen 8B's 1536 gate/up tiles then fill all 32 CUs of an
   // XCD in one round (16 blocks x 2 K slices) where 16-tile blocks leave 8 idle
   for (int nt : {16, 12, 8}) {
-    if (n_tiles % nt || (nt == 12 && !nt12)) continue;
-    const int n_cb = n_tiles / nt;
+    // half_block: 16-tile blocks also when n_tiles % 16 == 8, the last one half full (one K
+    // slice: its empty half would otherwise park and sum nothing)
+    const bool half = half_block && nt == 16 && n_tiles % 16 == 8;
+    if ((n_tiles % nt && !half) || (nt == 12 && !nt12)) continue;
+    const int n_cb = (n_tiles + nt - 1) / nt;
     for (int ks = 1; ks <= 8; ++ks) {
-      if (ks > 1 && S_all / ks < 4) break;
+      if (ks > 1 && (S_all / ks < 4 || half)) break;
       if (ks > 1 && (int64_t)ks * n_cb * nt * 16 * mb * mt * 16 > part_cap) break;
       if (ks > 1 && (int64_t)n_cb * mb * kCtrStride > kLayerCtr0) break;  // one counter line per unit
       // one workgroup per CU, 32 CUs per XCD; units of a column block share its XCD.  The
@@ -569,7 +578,7 @@ GemmPlan gemm_plan(int M, int n_tiles, int K, int64_t part_cap, bool nt12) {
 
 template <int MT, int NT, int EPI>
 static void launch_cfg(const GemmArgs& a, const Exec& ex) {
-  const int n_cb = a.n_tiles / NT;
+  const int n_cb = (a.n_tiles + NT - 1) / NT;
   const unsigned grid = (unsigned)(((n_cb + 7) / 8) * 8 * a.splits * a.m_blocks);
   const bool w8 = a.Wp8 != nullptr;
   if constexpr (NT == 12) {  // bf16 weights only (gemm_plan)
@@ -614,7 +623,8 @@ hipError_t launch_gemm(GemmEpi epi, const GemmArgs& a0, const Exec& ex) {
   if (a0.M < 1 || a0.K < 32 || a0.K % 32 || a0.n_tiles < 8 || a0.n_tiles % 8) return hipErrorInvalidValue;
   if (a0.Wp8 != nullptr && a0.wscale == nullptr) return hipErrorInvalidValue;
   const bool nt12 = epi == EPI_SWIGLU && a0.Wp8 == nullptr;
-  const GemmPlan p = gemm_plan(a0.M, a0.n_tiles, a0.K, (a0.part && !a0.no_split) ? a0.part_cap : 0, nt12);
+  const bool half_block = (epi == EPI_SCALED_STORE || epi == EPI_LOGITS_EB) && a0.Wp8 == nullptr;
+  const GemmPlan p = gemm_plan(a0.M, a0.n_tiles, a0.K, (a0.part && !a0.no_split) ? a0.part_cap : 0, nt12, half_block);
   if (p.nt == 0) return hipErrorInvalidValue;
   if (p.splits > 1 && (a0.counters == nullptr || (int64_t)p.n_cb * p.m_blocks * kCtrStride > kLayerCtr0))
     return hipErrorInvalidValue;

@@ -64,7 +64,7 @@ hipError_t hipDeviceGetAttribute(int* value, hipDeviceAttribute_t, int) {
 
 namespace sbd {
 
-GemmPlan gemm_plan(int, int n_tiles, int, int64_t, bool) { return GemmPlan{2, 8, 1, 1, n_tiles / 8}; }
+GemmPlan gemm_plan(int, int n_tiles, int, int64_t, bool, bool) { return GemmPlan{2, 8, 1, 1, n_tiles / 8}; }
 hipError_t launch_gemm(GemmEpi, const GemmArgs&, const Exec&) { return hipSuccess; }
 GemvShape gemv_pick(GemmEpi, int, int) { return GemvShape{8, 1, 2, 1}; }
 hipError_t launch_gemv(GemmEpi, const GemvArgs&, GemvShape, const Exec&) { return hipSuccess; }

@@ -174,8 +174,10 @@ struct GemmPlan {
   int mt, nt, splits, m_blocks, n_cb;
 };
 // nt12: 12-tile column blocks may be used (EPI_SWIGLU with bf16 weights: an epilogue
-// without row reductions across the block's columns)
-GemmPlan gemm_plan(int M, int n_tiles, int K, int64_t part_cap, bool nt12 = false);
+// without row reductions across the block's columns).  half_block: 16-tile blocks may be
+// used when n_tiles % 16 == 8, the last one half full (EPI_SCALED_STORE / EPI_LOGITS_EB with
+// bf16 weights; n_cb then counts it).
+GemmPlan gemm_plan(int M, int n_tiles, int K, int64_t part_cap, bool nt12 = false, bool half_block = false);
 
 hipError_t launch_gemm(GemmEpi epi, const GemmArgs& a, const Exec& ex);
 
