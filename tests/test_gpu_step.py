@@ -11,7 +11,8 @@ The stored logits equal sbd_block_forward's up to the summation order of the LM 
 launch shape (the step always takes whole 128-column groups in one wave).  Paths: the
 decode GEMM (at most 16 rows), the GEMM for more rows, and at the 8B layer shape the
 per-XCD layer kernels; the tiny decoder's LM head is scaled by 16 (exact in bf16) so that
-the entropies spread and every rule accepts varying numbers of rows.
+the entropies spread and every rule accepts varying numbers of rows.  At the Qwen-3-8B
+vocabulary (9496 tiles) the LM head of more than 64 rows ends in a half-full 16-tile block.
 """
 import dataclasses
 import math
@@ -153,4 +154,23 @@ def test_block_step_8b_layer_shape():
     lib.set_decode_path("auto")
     toks, is_mask = synth.block_rows(8502, shape, 4, 8, n_causal=1)
     check_step(lib, shape, [0, 1, 2, 3], toks, is_mask, [1] * 4, "8B 4x8")
+    lib.close()
+
+
+def test_block_step_qwen_vocab_half_block():
+    """Two layers of the Qwen-3-8B shape, 8 x 16 rows on the GEMM path: its 9496 vocabulary
+    tiles (8 mod 16) run as 16-tile blocks, the last one half full, both in the LM head that
+    stores logits and in the one that hands the EB statistics to the selection (the last 128
+    columns come from that block)."""
+    from paper_2509_04185_amd import Sbd
+    shape = dataclasses.replace(synth.QWEN8B, name="qwen8b_2layers", n_layers=2)
+    torch.cuda.empty_cache()
+    print("[gpu] 2-layer Qwen 8B shape for the block step (half-full last LM-head block)", flush=True)
+    w = synth.make_weights(shape, 8600, device="cuda")
+    lib = Sbd(shape, w, max_batch=8, max_seq_len=512, max_block=16)
+    for b in range(8):
+        kk, vv = synth.make_kv(shape, 8600, b, 100 + 37 * b, device="cuda")
+        lib.kv_import(b, 0, kk, vv)
+    toks, is_mask = synth.block_rows(8601, shape, 8, 16, n_causal=1)
+    check_step(lib, shape, list(range(8)), toks, is_mask, [1] * 8, "Qwen 8x16")
     lib.close()
