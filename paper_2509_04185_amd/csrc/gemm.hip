@@ -339,7 +339,12 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
   // slices of the row tiles kc, kc + KS, ... of the block in slice order and finishes them
   // (every output is the same sum of the same slices, whichever slice finishes it).  The
   // accumulators are not written again after the K loop: the sums go straight to LDS.
-  auto own = [&](int rt) { return rt % KS == kc; };
+  // e4m3 weights and two row tiles (M <= 32) keep the single finisher: the last slice to
+  // arrive sums every slice into the accumulators and finishes the whole block (there the
+  // shared sums made the compiler move accumulators between register files inside the K
+  // loop, which cost more than the shared finishing saves)
+  constexpr bool kSingle = W8 && MT == 2;
+  auto own = [&](int rt) { return kSingle || rt % KS == kc; };
   const int64_t slot = ((int64_t)uid * 4 + w) * (MTW * CW);       // in 1 KB (64 x f32x4) pieces
   const int64_t zstride = (int64_t)n_cb * MB * 4 * MTW * CW;       // pieces per slice
   if (KS > 1) {
@@ -348,7 +353,35 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
 #pragma unroll
       for (int cw = 0; cw < CW; ++cw)
         *(f32x4*)(a.part + ((kc * zstride + slot + mw * CW + cw) * 64 + lane) * 4) = acc[mw][cw];
-    slices_arrived(a, a.counters + (int64_t)uid * kCtrStride, KS, 65536 + EPI);
+    if constexpr (kSingle) {
+      if (!last_arrival_xcd(a.counters + (int64_t)uid * kCtrStride, KS)) return;
+      // ZB slices at a time, every piece of a slice in flight together; added in slice order
+      constexpr int ZB = MTW * CW >= 32 ? 1 : (MTW * CW >= 16 ? 2 : 4);
+      const __amdgpu_buffer_rsrc_t rp = buf_rsrc(a.part);
+#pragma unroll
+      for (int mw = 0; mw < MTW; ++mw)
+#pragma unroll
+        for (int cw = 0; cw < CW; ++cw) acc[mw][cw] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int z0 = 0; z0 < KS; z0 += ZB) {
+        i32x4 v[ZB][MTW][CW];
+#pragma unroll
+        for (int zz = 0; zz < ZB; ++zz)
+#pragma unroll
+          for (int mw = 0; mw < MTW; ++mw)
+#pragma unroll
+            for (int cw = 0; cw < CW; ++cw)
+              v[zz][mw][cw] = z0 + zz < KS ? ld16_l2(rp, (uint32_t)((((z0 + zz) * zstride + slot + mw * CW + cw) * 64 + lane) * 16))
+                                           : i32x4{0, 0, 0, 0};
+#pragma unroll
+        for (int zz = 0; zz < ZB; ++zz)
+#pragma unroll
+          for (int mw = 0; mw < MTW; ++mw)
+#pragma unroll
+            for (int cw = 0; cw < CW; ++cw) acc[mw][cw] += __builtin_bit_cast(f32x4, v[zz][mw][cw]);
+      }
+    } else {
+      slices_arrived(a, a.counters + (int64_t)uid * kCtrStride, KS, 65536 + EPI);
+    }
   }
 
   // ---- 1/rms of the block's rows (partials beyond the prefetched ones read here)
@@ -406,7 +439,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
       if (mw + 1 < MTW && own(wm * MTW + mw + 1)) load_x(mw + 1, xnxt);
     }
     if (own(wm * MTW + mw) && cols_in) {
-      if (KS > 1) {
+      if (!kSingle && KS > 1) {
         // the slices' sums of this wave's tiles of the row tile: ZR slices at a time, all
         // their pieces in flight
         constexpr int ZR = 4;
