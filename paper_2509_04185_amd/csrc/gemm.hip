@@ -26,7 +26,8 @@
 //     of one XCD, all resident at once (plans of one round): each parks its partial tiles
 //     in that XCD's L2 and waits for the others, then adds the slices of a share of the row
 //     tiles in slice order (deterministic) and runs their epilogue, so the finishing work
-//     of a unit is spread over its slices.
+//     of a unit is spread over its slices (e4m3 weights at M <= 32: the last slice to
+//     arrive adds all slices and finishes the block, without waiting).
 // Epilogues (acc in the MFMA D layout: lane l holds column l % 16 of a tile, rows
 // 4*(l/16) + i):
 //   EPI_SCALED_STORE  out = rinv[m] * y           (QKV projection, LM head)
